@@ -1,0 +1,613 @@
+"""Pins of the CPU oracle against facts fixed outside the oracle itself:
+inverses derived from the mathematics, closed forms, brute force on tiny
+inputs, the paper's worked examples and its stated guarantees.
+
+Citations name the paper's sections (DualMap, arXiv 2602.06502).
+"""
+import math
+import os
+import random
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+M64 = (1 << 64) - 1
+GOLDEN_DIR = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def setup_module(_):
+    oracle.build(force=False)
+
+
+# ---------------------------------------------------------------------------
+# mix64 / SplitMix64 (reading of the unnamed hash functions, Sec. 3.2)
+# ---------------------------------------------------------------------------
+
+def _unxorshift(y, s):
+    x = y
+    for _ in range(64 // s + 1):
+        x = y ^ (x >> s)
+    return x & M64
+
+
+def mix64_inverse(z):
+    """Inverse of the SplitMix64 finaliser, derived step by step: invert the
+    final xorshift-31, multiply by the modular inverse of the second
+    constant, invert xorshift-27, multiply by the inverse of the first
+    constant, invert xorshift-30."""
+    z = _unxorshift(z, 31)
+    z = (z * pow(0x94D049BB133111EB, -1, 1 << 64)) & M64
+    z = _unxorshift(z, 27)
+    z = (z * pow(0xBF58476D1CE4E5B9, -1, 1 << 64)) & M64
+    return _unxorshift(z, 30)
+
+
+def test_mix64_roundtrips_through_independent_inverse():
+    rng = random.Random(7)
+    xs = [0, 1, 2, M64, 1 << 63] + [rng.getrandbits(64) for _ in range(2000)]
+    for x in xs:
+        assert mix64_inverse(oracle.mix64(x)) == x
+
+
+def test_mix64_avalanche():
+    # flipping any single input bit flips about half the output bits
+    rng = random.Random(11)
+    flips = np.zeros(64)
+    n = 300
+    for _ in range(n):
+        x = rng.getrandbits(64)
+        hx = oracle.mix64(x)
+        for b in range(64):
+            flips[b] += bin(hx ^ oracle.mix64(x ^ (1 << b))).count("1")
+    mean = flips / n
+    assert np.all(np.abs(mean - 32) < 3.0), mean
+
+
+def test_golden_increment_is_two_pow_64_over_phi():
+    # floor(2^64 / phi) = floor(2^63 (sqrt5 - 1)) from an integer square root
+    golden = math.isqrt(5 << 126) - (1 << 63)
+    assert golden == 0x9E3779B97F4A7C15
+
+
+@pytest.mark.parametrize("seed,B", [(1, 16), (2, 16), (1, 32), (5, 2)])
+def test_hash_parameters_follow_the_splitmix_stream(seed, B):
+    """Key words, multiplier and chain start are consecutive outputs of a
+    SplitMix64 stream at `seed`: their pre-images under mix64 step by the
+    golden increment."""
+    golden = math.isqrt(5 << 126) - (1 << 63)
+    kk, mult, h_init = oracle.params(seed, B)
+    assert mult & 1 == 1
+    pre_h = mix64_inverse(h_init)
+    assert pre_h == (seed + (B + 2) * golden) & M64
+    pre_m = {mix64_inverse(mult), mix64_inverse(mult ^ 1)}
+    assert (seed + (B + 1) * golden) & M64 in pre_m
+    for j in range(B):
+        assert int(kk[j]) == oracle.mix64((seed + (j + 1) * golden) & M64) & 0xFFFFFFFF
+
+
+# ---------------------------------------------------------------------------
+# NH block digest and the chain (Sec. A.3.2: one hash per KV block)
+# ---------------------------------------------------------------------------
+
+def test_nh_with_zero_keys_is_pairwise_dot_product():
+    rng = np.random.default_rng(3)
+    for B in (2, 4, 16, 32):
+        t = rng.integers(-2**31, 2**31, size=B, dtype=np.int64).astype(np.int32)
+        want = sum((int(t[2 * j]) & 0xFFFFFFFF) * (int(t[2 * j + 1]) & 0xFFFFFFFF)
+                   for j in range(B // 2)) & M64
+        assert oracle.nh(t, np.zeros(B, np.uint32)) == want
+
+
+def test_nh_keys_enter_as_token_translation_mod_2_32():
+    rng = np.random.default_rng(4)
+    B = 16
+    for _ in range(50):
+        t = rng.integers(0, 2**31, size=B).astype(np.int32)
+        k = rng.integers(0, 2**32, size=B, dtype=np.uint64).astype(np.uint32)
+        shifted = ((t.astype(np.uint64) + k.astype(np.uint64)) & 0xFFFFFFFF).astype(np.uint32).view(np.int32)
+        assert oracle.nh(t, k) == oracle.nh(shifted, np.zeros(B, np.uint32))
+
+
+def _cfg(B=16, K=4, seeds=(1, 2), V=8, S=8):
+    return dict(block=B, key_blocks=K, seeds=seeds, vnodes=V, max_slots=S)
+
+
+@pytest.mark.parametrize("B,seed_idx", [(16, 0), (16, 1), (32, 0), (4, 1)])
+def test_chain_matches_closed_form(B, seed_idx):
+    """H[b] = H[-1] P^(b+1) + sum_k NH(k) P^(b-k) (mod 2^64), recovered from
+    each block key through the independent inverse of mix64."""
+    o = oracle.Oracle(_cfg(B=B, seeds=(1, 2)))
+    seed = (1, 2)[seed_idx]
+    kk, P, H0 = oracle.params(seed, B)
+    rng = np.random.default_rng(B)
+    t = rng.integers(0, 32000, size=B * 9 + B // 2).astype(np.int32)
+    keys = o.chain(seed_idx, t)
+    assert len(keys) == 9  # partial trailing tokens are not hashed
+    nhs = [oracle.nh(t[b * B:(b + 1) * B], kk) for b in range(9)]
+    for b in range(9):
+        H = (H0 * pow(P, b + 1, 1 << 64) + sum(nhs[k] * pow(P, b - k, 1 << 64) for k in range(b + 1))) & M64
+        assert mix64_inverse(int(keys[b])) ^ seed == H
+
+
+def test_block_keys_equal_iff_token_prefixes_equal():
+    """Tiny collision check: across prompts sharing prefixes of various
+    lengths, block key b agrees exactly when blocks 0..b agree token for
+    token."""
+    B = 4
+    o = oracle.Oracle(_cfg(B=B))
+    rng = np.random.default_rng(9)
+    base = rng.integers(0, 5, size=40).astype(np.int32)
+    prompts = []
+    for cut in range(0, 40, 3):
+        p = base.copy()
+        p[cut:] = rng.integers(0, 5, size=40 - cut)
+        prompts.append(p)
+    chains = [o.chain(0, p) for p in prompts]
+    for a in range(len(prompts)):
+        for c in range(len(prompts)):
+            for b in range(10):
+                same = np.array_equal(prompts[a][:(b + 1) * B], prompts[c][:(b + 1) * B])
+                assert (chains[a][b] == chains[c][b]) == same
+
+
+def test_ring_key_is_key_of_last_hashed_block():
+    B, K = 16, 4
+    o = oracle.Oracle(_cfg(B=B, K=K))
+    rng = np.random.default_rng(5)
+    for length in (0, 1, 15, 16, 17, 47, 48, 64, 65, 200):
+        t = rng.integers(0, 1000, size=length).astype(np.int32)
+        for s in (0, 1):
+            x = o.ring_key(s, t)
+            ch = o.chain(s, t)
+            kr = min(K, length // B)
+            if kr:
+                assert x == int(ch[kr - 1])
+            else:  # empty-prefix key: mix64(H[-1] xor seed)
+                _, _, H0 = oracle.params((1, 2)[s], B)
+                assert mix64_inverse(x) ^ (1, 2)[s] == H0
+
+
+# ---------------------------------------------------------------------------
+# Rings (Sec. 3.4; Sec. A.1.3)
+# ---------------------------------------------------------------------------
+
+def test_vnode_positions_are_the_bijective_mix_of_id_and_vnode():
+    o = oracle.Oracle(_cfg(S=40, V=16))
+    seen = set()
+    for s in (0, 1):
+        seed = (1, 2)[s]
+        for i in range(40):
+            for v in range(16):
+                p = o.vpos(s, i, v)
+                assert mix64_inverse(p) == ((i << 32) | v) ^ oracle.mix64(seed)
+                seen.add((s, p))
+    assert len(seen) == 2 * 40 * 16
+
+
+def _brute_owner(entries, x):
+    """Linear scan: smallest position >= x, else the smallest overall."""
+    ge = [(p, i) for p, i in entries if p >= x]
+    return min(ge)[1] if ge else min(entries)[1]
+
+
+def test_ring_build_and_owner_against_linear_scan():
+    ids = [0, 3, 4, 7, 9]
+    o = oracle.Oracle(_cfg(S=12, V=6))
+    assert o.build_rings(ids) == oracle.OK
+    rng = random.Random(1)
+    for s in (0, 1):
+        pos, own = o.ring(s)
+        entries = sorted((o.vpos(s, i, v), i) for i in ids for v in range(6))
+        assert [p for p, _ in entries] == [int(p) for p in pos]
+        assert [i for _, i in entries] == [int(i) for i in own]
+        probes = [0, M64, int(pos[0]), int(pos[-1]), int(pos[-1]) + 1, int(pos[3]) - 1]
+        probes += [rng.getrandbits(64) for _ in range(500)]
+        for x in probes:
+            x &= M64
+            assert o.owner(s, x) == _brute_owner(entries, x)
+
+
+def _read_ring_example():
+    rows = []
+    with open(os.path.join(GOLDEN_DIR, "ring_example.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                rows.append(line.split())
+    return rows
+
+
+def test_ring_worked_example_A_to_E():
+    """Sec. A.1.3: (A,B]->B, (B,C]->C, (C,D]->D; adding E between B and C
+    moves only (B,E] to E."""
+    place = dict(A=1000, B=2000, E=2500, C=3000, D=4000)
+    ident = dict(A=0, B=1, C=2, D=3, E=4)
+    rows = _read_ring_example()
+    for phase, names in (("before", "ABCD"), ("after", "ABECD")):
+        pos = np.array([place[n] for n in names], np.uint64)
+        ids = np.array([ident[n] for n in names], np.uint32)
+        for ph, lo, hi, own in rows:
+            if ph != phase:
+                continue
+            for x in (place[lo] + 1, (place[lo] + place[hi]) // 2, place[hi]):
+                assert oracle.owner_sorted(pos, ids, x) == ident[own]
+    # only keys in (B, E] change owner
+    before = (np.array([1000, 2000, 3000, 4000], np.uint64), np.array([0, 1, 2, 3], np.uint32))
+    after = (np.array([1000, 2000, 2500, 3000, 4000], np.uint64), np.array([0, 1, 4, 2, 3], np.uint32))
+    for x in range(0, 5000, 7):
+        moved = oracle.owner_sorted(*before, x) != oracle.owner_sorted(*after, x)
+        assert moved == (2000 < x <= 2500)
+
+
+def test_second_candidate_adjustment_dense_ids():
+    """Sec. 3.2: if both hashes pick one instance, id2 = (id1 + 1) mod n."""
+    n = 6
+    o = oracle.Oracle(_cfg(S=n, V=4))
+    o.build_rings(range(n))
+    rng = random.Random(3)
+    hits = 0
+    for _ in range(4000):
+        x1, x2 = rng.getrandbits(64), rng.getrandbits(64)
+        c1, c2, fix = o.candidates(x1, x2)
+        if o.owner(0, x1) == o.owner(1, x2):
+            hits += 1
+            assert fix and c2 == (c1 + 1) % n
+        else:
+            assert not fix and c2 == o.owner(1, x2)
+        assert c1 != c2
+    assert hits > 100
+
+
+def test_second_candidate_adjustment_sparse_ids_and_single_instance():
+    o = oracle.Oracle(_cfg(S=10, V=4))
+    o.build_rings([0, 3, 5])
+    nxt = {0: 3, 3: 5, 5: 0}
+    rng = random.Random(4)
+    for _ in range(3000):
+        x1, x2 = rng.getrandbits(64), rng.getrandbits(64)
+        c1, c2, fix = o.candidates(x1, x2)
+        if fix:
+            assert c2 == nxt[c1]
+        assert c1 != c2
+    o1 = oracle.Oracle(_cfg(S=4, V=4))
+    o1.build_rings([2])
+    c1, c2, fix = o1.candidates(5, 6)
+    assert (c1, c2, fix) == (2, 2, True)
+
+
+# ---------------------------------------------------------------------------
+# Match, TTFT, selection (Sec. 3.2; Sec. A.1.1; Sec. A.3.2)
+# ---------------------------------------------------------------------------
+
+def _lcp(a, b):
+    n = min(len(a), len(b))
+    k = 0
+    while k < n and a[k] == b[k]:
+        k += 1
+    return k
+
+
+def test_match_equals_floor_lcp_over_block():
+    B = 8
+    o = oracle.Oracle(_cfg(B=B, K=2, S=3, V=4))
+    o.build_rings([0, 1, 2])
+    rng = np.random.default_rng(12)
+    A = rng.integers(0, 4, size=120).astype(np.int32)
+    for inst in range(3):
+        o.index_insert(inst, o.chain(0, A))
+    prompts = []
+    for cut in list(range(0, 120, 5)) + [120]:
+        for extra in (0, 3, 17):
+            p = np.concatenate([A[:cut], rng.integers(4, 8, size=extra).astype(np.int32)])
+            prompts.append(p)
+    off = np.zeros(len(prompts) + 1, np.int64)
+    off[1:] = np.cumsum([len(p) for p in prompts])
+    out = o.route(np.concatenate(prompts), off, np.zeros(3, np.int64))
+    n = len(prompts)
+    for r, p in enumerate(prompts):
+        want = min(_lcp(A, p), len(p)) // B
+        assert out["match"][r] == want and out["match"][n + r] == want
+
+
+def test_ttft_hand_values():
+    o = oracle.Oracle(_cfg())
+    assert o.ttft(0, 0) == 2000
+    assert o.ttft(100, 10) == 2000 + 300 + 2
+    assert o.ttft(7, 3) == 2000 + 21 + 0
+    assert o.ttft(0, -1) == 2000 - 1  # floor division
+    assert o.ttft(0, 4_000_000) == 1_002_000
+
+
+@pytest.mark.parametrize("case", [
+    # (m1, m2, L1, L2, len, expected chosen (1|2), flags without fixup bit)
+    (3, 3, 10, 20, 100, 1, 4),      # equal hits -> less loaded
+    (3, 3, 20, 20, 100, 1, 4),      # equal hits, equal load -> c1
+    (3, 3, 21, 20, 100, 2, 4),
+    (5, 1, 10**6, 0, 100, 1, 0),    # affinity kept while TTFT <= SLO
+    (5, 1, 2_000_000, 0, 100, 2, 1),    # affinity TTFT over SLO -> less loaded
+    (5, 1, 2_000_000, 2_000_000, 100, 1, 2),  # over, other not less loaded: keep; both over
+    (1, 5, 0, 2_000_000, 100, 1, 1),    # symmetric: c2 affine, over -> c1
+    (1, 5, 2_000_001, 2_000_000, 100, 2, 2),  # both over, c1 not less loaded: c2 kept
+])
+def test_selection_truth_table(case):
+    m1, m2, L1, L2, length, want, want_flags = case
+    o = oracle.Oracle(dict(_cfg(B=16), slo_us=400_000))
+    loads = np.array([L1, L2], np.int64)
+    ch, t, f = o.select(0, 1, m1, m2, length, loads)
+    assert ch == want - 1
+    assert f == want_flags
+    unc = length - 16 * (m1 if ch == 0 else m2)
+    assert t == 2000 + 3 * unc + loads[ch] // 4
+    # the SLO threshold is inclusive: TTFT == SLO keeps affinity
+    L_eq = 4 * (400_000 - 2000 - 3 * (length - 16 * 5))
+    ch, t, f = o.select(0, 1, 5, 1, length, np.array([L_eq, 0], np.int64))
+    assert t == 400_000 and ch == 0
+
+
+def _read_narrative():
+    rows = []
+    with open(os.path.join(GOLDEN_DIR, "slo_narrative.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                r, inst, why = line.split()
+                rows.append((int(r), int(inst), why))
+    return rows
+
+
+def test_slo_narrative_scenario():
+    """Fig. 'SLO-aware request routing': instance 1 (id 0 here) caches all
+    prefixes, instance 2 (id 1) none; requests 1-4 stay, 5 switches, 6-7
+    (equal hits) go to the less-loaded instance."""
+    B, slo = 16, 10_000
+    o = oracle.Oracle(dict(block=B, key_blocks=4, seeds=(1, 2), vnodes=8, max_slots=2, slo_us=slo))
+    o.build_rings([0, 1])
+    rng = np.random.default_rng(21)
+    tpl = rng.integers(0, 1000, size=160).astype(np.int32)       # 10 blocks, cached on id 0
+    shared = rng.integers(0, 1000, size=160).astype(np.int32)    # cached on both
+    o.index_insert(0, o.chain(0, tpl))
+    o.index_insert(0, o.chain(0, shared))
+    o.index_insert(1, o.chain(0, shared))
+    reqs = []
+    for r in range(7):
+        base = tpl if r < 5 else shared
+        reqs.append(np.concatenate([base, rng.integers(2000, 3000, size=32).astype(np.int32)]))
+    off = np.zeros(8, np.int64)
+    off[1:] = np.cumsum([len(p) for p in reqs])
+    # id 0 starts just below the SLO knee: TTFT = 2000 + 3*32 + L/4 <= 10000
+    L0 = np.array([31_616 - 3 * 32, 0], np.int64)
+    out = o.route(np.concatenate(reqs), off, L0)
+    for (r, inst, why) in _read_narrative():
+        assert out["chosen"][r - 1] == inst - 1, (r, why)
+        if why == "slo_switch":
+            assert out["flags"][r - 1] & 1
+        if why.startswith("equal"):
+            assert out["flags"][r - 1] & 4
+
+
+def test_cache_affinity_guarantee():
+    """Sec. 2.3: m requests sharing a prefix get hit rate >= max(0, 1 - 2/m)
+    (routing one at a time, each routed chain then cached on its instance)."""
+    B = 16
+    for seed in range(5):
+        o = oracle.Oracle(dict(block=B, key_blocks=4, seeds=(1, 2), vnodes=16, max_slots=8, slo_us=20_000))
+        o.build_rings(range(8))
+        rng = np.random.default_rng(100 + seed)
+        prefix = rng.integers(0, 5000, size=8 * B).astype(np.int32)
+        loads = rng.integers(0, 80_000, size=8).astype(np.int64)
+        m = 25
+        hits = 0
+        for _ in range(m):
+            p = np.concatenate([prefix, rng.integers(5000, 9000, size=40).astype(np.int32)])
+            out = o.route(p, np.array([0, len(p)], np.int64), loads, block_keys=True)
+            ch = int(out["chosen"][0])
+            got = out["match"][0] if ch == out["cand"][0] else out["match"][1]
+            hits += int(got >= 8)
+            o.index_insert(ch, out["block_keys"])
+            loads = out["loads"]
+        assert hits / m >= max(0.0, 1 - 2 / m)
+
+
+def test_two_choices_spread_less_than_one_choice():
+    """Sec. 2.3 (power of two choices): with equal cache hits everywhere the
+    rule joins the less-loaded candidate; the max-minus-mean load gap is far
+    below placing every request on its first candidate."""
+    gaps1, gaps2 = [], []
+    for seed in range(10):
+        wl = workloads.small_random(seed, 16, 64, 16, 4000)
+        o = oracle.Oracle(dict(wl.route.as_dict(), max_slots=16))
+        o.build_rings(range(16))
+        rng = np.random.default_rng(seed)
+        tok = rng.integers(0, 1 << 30, size=4000 * 64).astype(np.int32)
+        off = np.arange(0, 4000 * 64 + 1, 64, dtype=np.int64)
+        out = o.route(tok, off, np.zeros(16, np.int64))
+        two = np.bincount(out["chosen"], minlength=16)
+        one = np.bincount(out["cand"][:4000], minlength=16)
+        gaps2.append(two.max() - two.mean())
+        gaps1.append(one.max() - one.mean())
+    assert np.mean(gaps2) * 4 < np.mean(gaps1)
+    # max load stays within m/n + log log n / log 2 + O(1) (Eq. potc_2_choices)
+    assert np.max(gaps2) <= math.log(math.log(16)) / math.log(2) + 4
+
+
+# ---------------------------------------------------------------------------
+# Rebalance (Sec. 3.3; Sec. A.1.2)
+# ---------------------------------------------------------------------------
+
+def brute_rebalance(cfg, qoff, rec, here, alt, other, W0):
+    """Literal pass recomputing every queue TTFT from scratch at each step."""
+    base, per, div, slo = cfg["ttft_base_us"], cfg["ttft_per_token_us"], cfg["queue_div"], cfg["slo_us"]
+    S = len(W0)
+
+    def T(unc, load):
+        return base + per * unc + load // div
+
+    queues = {i: list(range(qoff[i], qoff[i + 1])) for i in range(S)}
+
+    def qts(i, q):
+        ahead, out = W0[i], []
+        for r in q:
+            out.append(T(int(here[r]), ahead))
+            ahead += int(here[r])
+        return out
+
+    L = [W0[i] + sum(int(here[r]) for r in queues[i]) for i in range(S)]
+    over = [bool(queues[i]) and max(qts(i, queues[i])) > slo for i in range(S)]
+    L0 = list(L)
+    migs = []
+    for i in sorted([i for i in range(S) if over[i]], key=lambda i: (-L0[i], i)):
+        ts = qts(i, queues[i])
+        cands = []
+        for p, r in enumerate(queues[i]):
+            j = int(alt[r])
+            b = ts[p] - T(int(other[r]), L0[j])
+            if b > 0 and not over[j]:
+                cands.append((-b, p, r))
+        cands.sort()
+        cur = list(queues[i])
+        for negb, p, r in cands:
+            now = qts(i, cur)
+            if not now or max(now) <= slo:
+                break
+            j = int(alt[r])
+            tj = T(int(other[r]), L[j])
+            if tj < slo:
+                cur.remove(r)
+                L[i] -= int(here[r])
+                L[j] += int(other[r])
+                migs.append((int(rec[r]), i, j, -negb, tj))
+    return migs, L
+
+
+def _random_queues(seed, S=5, maxq=12):
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(0, maxq + 1, size=S)
+    qoff = np.zeros(S + 1, np.int64)
+    qoff[1:] = np.cumsum(lens)
+    Q = int(qoff[-1])
+    owner = np.repeat(np.arange(S), lens)
+    alt = (owner + rng.integers(1, S, size=Q)) % S
+    here = rng.integers(0, 30, size=Q).astype(np.uint32)
+    other = rng.integers(0, 30, size=Q).astype(np.uint32)
+    rec = np.arange(Q, dtype=np.uint64) + 100
+    W0 = rng.integers(0, 120, size=S).astype(np.int64)
+    return qoff, rec, here, alt.astype(np.uint32), other, W0
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_rebalance_matches_brute_force(seed):
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=5,
+               ttft_base_us=2, ttft_per_token_us=1, queue_div=4, slo_us=40 + seed % 20)
+    o = oracle.Oracle(cfg)
+    qoff, rec, here, alt, other, W0 = _random_queues(seed)
+    got = o.rebalance(qoff, rec, here, alt, other, W0)
+    want, L = brute_rebalance(cfg, qoff, rec, here, alt, other, W0)
+    assert got["status"] == oracle.OK
+    assert got["count"] == len(want)
+    g = list(zip(got["rec"].tolist(), got["src"].tolist(), got["dst"].tolist(),
+                 got["benefit"].tolist(), got["ttft_to"].tolist()))
+    assert g == want
+    assert got["loads"].tolist() == L
+
+
+def test_rebalance_invariants_and_cap():
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=5,
+               ttft_base_us=2, ttft_per_token_us=1, queue_div=4, slo_us=45)
+    o = oracle.Oracle(cfg)
+    total_moves = 0
+    for seed in range(100, 140):
+        qoff, rec, here, alt, other, W0 = _random_queues(seed)
+        got = o.rebalance(qoff, rec, here, alt, other, W0)
+        total_moves += got["count"]
+        recidx = {int(r): k for k, r in enumerate(rec)}
+        L_start = np.array([W0[i] + here[qoff[i]:qoff[i + 1]].astype(np.int64).sum() for i in range(5)])
+        delta = 0
+        for r, i, j, b, tj in zip(got["rec"], got["src"], got["dst"], got["benefit"], got["ttft_to"]):
+            k = recidx[int(r)]
+            assert b > 0 and tj < cfg["slo_us"] and int(alt[k]) == j and qoff[i] <= k < qoff[i + 1]
+            delta += int(other[k]) - int(here[k])
+        assert got["loads"].sum() == L_start.sum() + delta
+        if got["count"] > 1:
+            capped = o.rebalance(qoff, rec, here, alt, other, W0, cap=1)
+            assert capped["status"] == oracle.EFULL and capped["count"] == got["count"]
+    assert total_moves > 20
+
+
+# ---------------------------------------------------------------------------
+# Scaling (Sec. 3.4; Sec. A.1.3)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(4))
+def test_scale_moves_only_affected_keys(seed):
+    N, V, S = 16, 64, 24
+    o = oracle.Oracle(_cfg(S=S, V=V))
+    o.build_rings(range(N))
+    rng = np.random.default_rng(seed)
+    keys = rng.integers(0, 2**64, size=2 * 20000, dtype=np.uint64)
+    rm = np.sort(rng.choice(N, size=2, replace=False)).astype(np.uint32)
+    add = np.array([16, 17, 18], np.uint32)
+    out = o.scale(add, rm, keys)
+    assert out["status"] == oracle.OK
+    assert out["violations"] == 0
+    n = 20000
+    live = sorted(set(range(N)) - set(rm.tolist()) | set(add.tolist()))
+    for s in (0, 1):
+        entries = sorted((o.vpos(s, i, v), i) for i in live for v in range(V))
+        for k in range(0, n, 97):
+            assert out["new"][s * n + k] == _brute_owner(entries, int(keys[s * n + k]))
+        frac = out["moved"][s] / n
+        expect = 2 / N + 3 / (N + 1) - (2 / N) * (3 / (N + 1))
+        assert abs(frac - expect) < 0.06, (frac, expect)
+    assert o.n_live() == N + 1
+
+
+def test_scale_rejects_bad_sets_and_keeps_state():
+    o = oracle.Oracle(_cfg(S=8, V=4))
+    o.build_rings([0, 1, 2])
+    keys = np.arange(10, dtype=np.uint64)
+    assert o.scale([1], [], keys)["status"] == oracle.EINVAL      # add existing
+    assert o.scale([], [5], keys)["status"] == oracle.EINVAL      # remove unknown
+    assert o.scale([9], [], keys)["status"] == oracle.EINVAL      # out of range
+    assert o.scale([], [0, 1, 2], keys)["status"] == oracle.EINVAL  # empty result
+    assert o.n_live() == 3
+
+
+# ---------------------------------------------------------------------------
+# Index set semantics and the sort primitive
+# ---------------------------------------------------------------------------
+
+def test_index_set_semantics_and_reserved_keys():
+    o = oracle.Oracle(_cfg(S=2))
+    keys = np.array([5, 5, 0, 1, 1 << 63, 7], np.uint64)
+    o.index_insert(0, keys)
+    # 0 and 1 map to 2^63 and 2^63+1; 2^63 itself collides with canon(0)
+    assert o.index_size(0) == 4
+    for k in (5, 0, 1, 7, 1 << 63):
+        assert o.index_contains(0, k)
+    assert not o.index_contains(1, 5)
+    o.index_erase(0, np.array([5, 99], np.uint64))
+    assert not o.index_contains(0, 5) and o.index_size(0) == 3
+    o.index_clear(0)
+    assert o.index_size(0) == 0
+
+
+def test_radix_sort_matches_numpy():
+    rng = np.random.default_rng(0)
+    for n in (0, 1, 2, 100, 100_000):
+        a = rng.integers(0, 2**64, size=n, dtype=np.uint64)
+        assert np.array_equal(oracle.sort_u64(a), np.sort(a))
+
+
+def test_metadata_footprint_fixture():
+    """Sec. A.3.2: 16 B per block (8 B hash + 8 B id).  The device table
+    spends 8 B per slot at load factor <= 1/2, i.e. at least 16 B per cached
+    block -- the same footprint."""
+    vals = {}
+    with open(os.path.join(GOLDEN_DIR, "metadata_footprint.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                k, v = line.split()
+                vals[k] = int(v)
+    assert vals["bytes_per_block"] == 8 + 8
+    assert 8 / 0.5 == vals["bytes_per_block"]

@@ -1,0 +1,243 @@
+"""Seeded synthetic inputs for the DualMap routing path.
+
+This module holds none of the method's arithmetic: it draws token streams,
+prompt lengths, template choices, loads, coin flips, random key streams and
+queue records with the shapes and distributions of the workloads the routing
+path is measured on, and nothing else.  Both the HIP path (tests, benchmark)
+and the CPU oracle take their inputs from here; every state that needs the
+method's arithmetic (cached block sets built from routed prompts, candidate
+pairs, loads after routing) is built by each side with its own code.
+
+The paper measures on two Mooncake traces (Conversation and Tool&Agent,
+Table 1 and Sec. A.2.1); those traces are not available, so the generators
+below stand in for them: template-plus-suffix prompts with Zipf-distributed
+template popularity reproduce the shared-prefix structure, multi-turn
+sessions reproduce the conversation structure.
+
+Random streams: numpy's PCG64 seeded by SeedSequence([workload_seed, stream]),
+one stream per component, so each component is reproducible on its own.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, Optional, Tuple
+
+import numpy as np
+
+# Stream ids: one independent random stream per generated component.
+_S_TEMPLATE_LEN, _S_TEMPLATE_TOK, _S_REQ_LEN, _S_REQ_TPL, _S_REQ_TOK = 1, 2, 3, 4, 5
+_S_LOADS, _S_COINS, _S_FILLER, _S_PRIOR, _S_SCALE, _S_QUEUE = 6, 7, 8, 9, 10, 11
+
+
+def _rng(seed: int, stream: int, sub: int = 0) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, stream, sub])))
+
+
+@dataclasses.dataclass(frozen=True)
+class RouteConfig:
+    """Routing parameters of one workload (passed to both implementations)."""
+
+    name: str
+    n_inst: int               # live instances at start (ids 0..n_inst-1)
+    vnodes: int               # virtual nodes per instance on each ring
+    block: int                # tokens per KV block
+    key_blocks: int           # ring key covers the first key_blocks full blocks
+    seeds: Tuple[int, int]    # seeds of the two hash functions
+    max_slots: int            # instance-id space
+    index_log2_slots: int     # per-instance device table: 2**k slots
+    ttft_base_us: int = 2000
+    ttft_per_token_us: int = 3
+    queue_div: int = 4
+    slo_us: int = 400_000
+
+    def as_dict(self) -> Dict:
+        return dataclasses.asdict(self)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    route: RouteConfig
+    seed: int
+    n_req: int
+    vocab: int
+    # prompt lengths
+    len_kind: str             # "uniform" | "lognormal"
+    len_a: float              # uniform: low;  lognormal: median
+    len_b: float              # uniform: high; lognormal: sigma
+    len_cap: int
+    # shared-prefix templates
+    n_templates: int
+    tlen_lo: int
+    tlen_hi: int
+    zipf_s: float
+    load_hi: int = 50_000     # initial per-instance load ~ U[0, load_hi]
+    n_prior: int = 0          # prior requests whose chains pre-fill the index
+    filler_per_inst: int = 0  # random keys topping each instance index up to this size
+    suffix_lo: int = 0        # template prompts: random tail ~ U[suffix_lo, suffix_hi]
+    suffix_hi: int = 0        #   (0, 0 = prompt length drawn from len_kind instead)
+
+
+def tiny(slo_us: int = 400_000) -> Workload:
+    """8 instances x 64 vnodes, 1,024 requests of U[256,768] tokens over 64
+    Zipf(1.0) templates of U[128,512] tokens, vocab 32,000, block 16; the index
+    is pre-filled by routing 256 prior requests."""
+    rc = RouteConfig("tiny", 8, 64, 16, 4, (1, 2), 8, 14, slo_us=slo_us)
+    return Workload("tiny" if slo_us == 400_000 else "tiny-tight", rc, 101, 1024, 32_000,
+                    "uniform", 256, 768, 768, 64, 128, 512, 1.0, n_prior=256)
+
+
+def large(n_req: int = 1_048_576) -> Workload:
+    """128 instances x 512 vnodes, 1,048,576 requests with lognormal lengths
+    (median 1,024, sigma 1.0, cap 16,384), 4,096 Zipf(1.1) templates of
+    U[128,2048] tokens, vocab 152,000, block 16; each instance index holds
+    1,048,576 keys in 2**21 slots."""
+    rc = RouteConfig("large", 128, 512, 16, 4, (1, 2), 256, 21)
+    return Workload("large" if n_req == 1_048_576 else f"large-{n_req}", rc, 104, n_req, 152_000,
+                    "lognormal", 1024.0, 1.0, 16_384, 4096, 128, 2048, 1.1,
+                    filler_per_inst=1_048_576)
+
+
+def small_random(seed: int, n_inst: int, vnodes: int, block: int, n_req: int,
+                 key_blocks: Optional[int] = None, slo_us: int = 400_000) -> Workload:
+    """Small randomized configuration for property and parity sweeps; lengths
+    include 0, shorter than a block and exact multiples of the block."""
+    kb = key_blocks if key_blocks is not None else max(1, 64 // block)
+    rc = RouteConfig(f"rand{seed}", n_inst, vnodes, block, kb, (1 + seed, 2 + seed),
+                     max(n_inst, 1) + 3, 12, slo_us=slo_us)
+    return Workload(f"rand{seed}", rc, 1000 + seed, n_req, 50,
+                    "uniform", 0, 6 * block, 6 * block, 6, 1, 4 * block, 1.0, n_prior=n_req // 2)
+
+
+# --------------------------------------------------------------------------
+# Building blocks
+# --------------------------------------------------------------------------
+
+def zipf_ranks(rng: np.random.Generator, n_items: int, s: float, size: int) -> np.ndarray:
+    """Item indices 0..n_items-1 with P(k) proportional to (k+1)^-s, via the CDF
+    and a 53-bit uniform."""
+    w = np.arange(1, n_items + 1, dtype=np.float64) ** (-s)
+    cdf = np.cumsum(w)
+    cdf /= cdf[-1]
+    u = rng.random(size)
+    idx = np.searchsorted(cdf, u, side="right")
+    return np.minimum(idx, n_items - 1).astype(np.int64)
+
+
+def uniform_tokens(rng: np.random.Generator, vocab: int, size: int) -> np.ndarray:
+    return rng.integers(0, vocab, size=size, dtype=np.int32)
+
+
+def templates(wl: Workload) -> Tuple[np.ndarray, np.ndarray]:
+    """Template token CSR: (tokens int32, offsets int64)."""
+    lens = _rng(wl.seed, _S_TEMPLATE_LEN).integers(wl.tlen_lo, wl.tlen_hi + 1, size=wl.n_templates)
+    off = np.zeros(wl.n_templates + 1, dtype=np.int64)
+    np.cumsum(lens, out=off[1:])
+    tok = uniform_tokens(_rng(wl.seed, _S_TEMPLATE_TOK), wl.vocab, int(off[-1]))
+    return tok, off
+
+
+def _lengths(wl: Workload, rng: np.random.Generator, n: int) -> np.ndarray:
+    if wl.len_kind == "uniform":
+        return rng.integers(int(wl.len_a), int(wl.len_b) + 1, size=n).astype(np.int64)
+    z = rng.standard_normal(n)
+    lens = np.rint(np.exp(math.log(wl.len_a) + wl.len_b * z))
+    return np.minimum(lens, wl.len_cap).astype(np.int64)
+
+
+def prompts(wl: Workload, n: int, sub: int = 0, chunk: int = 1 << 16) -> Tuple[np.ndarray, np.ndarray]:
+    """n prompts: each is the first min(len, T_len) tokens of a Zipf-chosen
+    template followed by uniform random tokens up to len.  Returns the token
+    CSR (int32 tokens, int64 offsets).  `sub` selects an independent batch
+    (0 = measured batch, 1 = prior requests)."""
+    ttok, toff = templates(wl)
+    tlen = np.diff(toff)
+    lens = _lengths(wl, _rng(wl.seed, _S_REQ_LEN, sub), n)
+    tpl = zipf_ranks(_rng(wl.seed, _S_REQ_TPL, sub), wl.n_templates, wl.zipf_s, n)
+    off = np.zeros(n + 1, dtype=np.int64)
+    np.cumsum(lens, out=off[1:])
+    total = int(off[-1])
+    tok = np.empty(total, dtype=np.int32)
+    rng_tok = _rng(wl.seed, _S_REQ_TOK, sub)
+    # random tokens everywhere, in fixed-size pieces so memory stays bounded
+    piece = 1 << 26
+    for s in range(0, total, piece):
+        e = min(total, s + piece)
+        tok[s:e] = uniform_tokens(rng_tok, wl.vocab, e - s)
+    # overwrite each prompt's shared part with its template's prefix
+    shared = np.minimum(lens, tlen[tpl])
+    for r0 in range(0, n, chunk):
+        r1 = min(n, r0 + chunk)
+        sh = shared[r0:r1]
+        cnt = int(sh.sum())
+        if cnt == 0:
+            continue
+        rep = np.repeat(np.arange(r0, r1), sh)
+        within = np.arange(cnt, dtype=np.int64) - np.repeat(np.cumsum(sh) - sh, sh)
+        tok[off[rep] + within] = ttok[toff[tpl[rep]] + within]
+    return tok, off
+
+
+def initial_loads(wl: Workload, n_slots: int) -> np.ndarray:
+    """Per-slot pending work U[0, load_hi] (int64)."""
+    return _rng(wl.seed, _S_LOADS).integers(0, wl.load_hi + 1, size=n_slots).astype(np.int64)
+
+
+def coin_flips(wl: Workload, n: int) -> np.ndarray:
+    """n fair coins (uint8 0/1)."""
+    return _rng(wl.seed, _S_COINS).integers(0, 2, size=n).astype(np.uint8)
+
+
+def filler_keys(wl: Workload, inst: int, count: int) -> np.ndarray:
+    """The first `count` values of instance inst's random 64-bit key stream."""
+    if count <= 0:
+        return np.zeros(0, dtype=np.uint64)
+    return _rng(wl.seed, _S_FILLER, inst).integers(0, 2**64, size=count, dtype=np.uint64)
+
+
+def scale_sets(wl: Workload, n_add: int, n_rm: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Elastic step: add ids n_inst..n_inst+n_add-1, remove n_rm seed-chosen
+    ids from 0..n_inst-1."""
+    add = np.arange(wl.route.n_inst, wl.route.n_inst + n_add, dtype=np.uint32)
+    rm = np.sort(_rng(wl.seed, _S_SCALE).choice(wl.route.n_inst, size=n_rm, replace=False))
+    return add, rm.astype(np.uint32)
+
+
+@dataclasses.dataclass
+class Queues:
+    """Per-instance pending-request queues in CSR form (head first)."""
+
+    qoff: np.ndarray       # int64 [n_slots + 1]
+    rec_id: np.ndarray     # uint64 [Q]
+    unc_here: np.ndarray   # uint32 [Q]
+    alt: np.ndarray        # uint32 [Q]
+    unc_alt: np.ndarray    # uint32 [Q]
+    base_work: np.ndarray  # int64 [n_slots]
+
+
+def synthetic_queues(seed: int, n_slots: int, n_live: int, sources: np.ndarray, per_source: int,
+                     unc_hi: int, cold_hi: int, base_src: int = 0) -> Queues:
+    """Queues on the given source instances (ids < n_live), each holding
+    per_source records whose alternative is a uniformly drawn other live
+    instance; uncached tokens ~ U[0, unc_hi] on the alternative and the
+    smaller of two such draws on the queue's own instance (it holds more of
+    the prefix).  Sources start with base work base_src; the other instances
+    get base work U[0, cold_hi] and empty queues."""
+    rng = _rng(seed, _S_QUEUE)
+    lens = np.zeros(n_slots, dtype=np.int64)
+    lens[sources] = per_source
+    qoff = np.zeros(n_slots + 1, dtype=np.int64)
+    np.cumsum(lens, out=qoff[1:])
+    Q = int(qoff[-1])
+    owner = np.repeat(np.arange(n_slots), lens)
+    alt = rng.integers(0, n_live - 1, size=Q)
+    alt = np.where(alt >= owner, alt + 1, alt).astype(np.uint32)
+    a = rng.integers(0, unc_hi + 1, size=Q)
+    b = rng.integers(0, unc_hi + 1, size=Q)
+    here = np.minimum(a, b).astype(np.uint32)
+    other = rng.integers(0, unc_hi + 1, size=Q).astype(np.uint32)
+    rec = rng.permutation(np.arange(Q, dtype=np.uint64) * 7 + 3).astype(np.uint64)
+    base = rng.integers(0, cold_hi + 1, size=n_slots).astype(np.int64)
+    base[sources] = base_src
+    return Queues(qoff, rec, here, alt, other, base)

@@ -1,0 +1,186 @@
+#!/usr/bin/env python3
+"""Benchmark of batched dual-mapping routing on one MI355X.
+
+One step = one dm_route_batch over the large workload: 1,048,576 requests
+(lognormal lengths, median 1,024 tokens, cap 16,384; 4,096 Zipf(1.1)
+shared-prefix templates; vocab 152,000) against 128 instances x 512 virtual
+nodes per ring, block 16, each instance index holding 1,048,576 keys in
+2^21 slots.  Inputs are resident in HBM before timing; the loads are reset
+to the snapshot before every step (a 2 KB device copy inside the step).
+
+Prints one JSON line: requests routed/s, prompt tokens hashed/s, the HBM
+roofline of the hash+match kernel (algorithmic bytes / its average
+duration measured with HIP events on the engine's stream), and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def route_source_hash():
+    h = hashlib.sha256()
+    for f in ("dm_route.hip", "dm_internal.h"):
+        with open(os.path.join(ROOT, "paper_2602_06502_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(name):
+    """HBM bytes per launch from rocprofv3 FETCH_SIZE/WRITE_SIZE counters, if
+    recorded for the current kernel source."""
+    p = os.path.join(ROOT, "profiles", name)
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        d = json.load(f)
+    if d.get("source_hash") != route_source_hash():
+        return None
+    return d.get("bytes_per_launch")
+
+
+def algorithmic_bytes(off_np, B, match, cand, n):
+    """Bytes the hash+match kernel must move: full-block tokens, offsets,
+    per-request outputs (2 ring keys, 2 candidates, 2 match lengths, flags)
+    and one 8-byte slot per index probe the first-miss rule needs
+    (match_c blocks plus the missing one, per distinct candidate)."""
+    import numpy as np
+    lens = np.diff(off_np)
+    nfull = np.maximum(lens, 0) // B
+    tok = 4 * int((nfull * B).sum())
+    m1, m2 = match[:n].astype(np.int64), match[n:].astype(np.int64)
+    distinct = cand[:n] != cand[n:]
+    probes = (m1 + (m1 < nfull)).sum() + ((m2 + (m2 < nfull)) * distinct).sum()
+    return tok + 8 * (n + 1) + 33 * n + 8 * int(probes), int((nfull * B).sum())
+
+
+def cpu_baseline(wl, sample):
+    """The oracle as it stands, single-threaded, on the first `sample`
+    requests of the same workload (same index, same initial loads)."""
+    import numpy as np
+
+    import oracle
+    import oracle.harness as oh
+    import workloads
+    oracle.build(force=False)
+    log("cpu baseline: building oracle state")
+    st = oh.setup(wl, with_batch=False)
+    tok, off = workloads.prompts(wl, sample, sub=0)
+    t0 = time.perf_counter()
+    st["oracle"].route(tok, off, st["loads0"])
+    dt = time.perf_counter() - t0
+    ntok = int(((np.diff(off) // wl.route.block) * wl.route.block).sum())
+    return {"value": sample / dt, "unit": "requests/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {sample:,} of the {wl.n_req:,} requests (same index and loads), "
+                      f"{dt:.1f} s single-threaded on the host",
+            "tokens_hashed_per_s": ntok / dt}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--n-req", type=int, default=1_048_576)
+    ap.add_argument("--cpu-sample", type=int, default=100_000)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the routing path is built and measured on a "
+              "single MI355X (see the sharding note in DESIGN.md); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2602_06502_amd.harness as gh
+    import workloads
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = workloads.large(args.n_req)
+    log("setup", wl.name, "n_req", wl.n_req)
+    t0 = time.perf_counter()
+    st = gh.setup(wl, device="cuda:0")
+    eng, tokens, offsets = st["eng"], st["tokens"], st["offsets"]
+    n = wl.n_req
+    log(f"setup done in {time.perf_counter() - t0:.1f} s; tokens {tokens.numel():,}")
+    L0 = gh.to_dev(st["loads0"], eng.device)
+    loads = L0.clone()
+    out = eng.alloc_route_out(n)
+    eng.set_timing(True)
+    for _ in range(args.warmup):
+        loads.copy_(L0)
+        eng.route_into(tokens, offsets, loads, out)
+    eng.sync()
+    torch.cuda.synchronize()
+    hash_ms, sel_ms = [], []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        loads.copy_(L0)
+        eng.route_into(tokens, offsets, loads, out)
+        h, s, _ = eng.stage_ms()
+        hash_ms.append(h)
+        sel_ms.append(s)
+    eng.sync()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_step = 1000.0 * dt / args.steps
+    match = out["match"].cpu().numpy()
+    cand = out["cand"].cpu().numpy()
+    alg, ntok = algorithmic_bytes(st["offsets_np"], wl.route.block, match, cand, n)
+    hash_avg = float(np.mean(hash_ms))
+    achieved = alg / (hash_avg * 1e-3) / 1e9
+    traffic = load_traffic("traffic_hash_match_large.json")
+    flags = out["flags"].cpu().numpy()
+    res = {
+        "metric": "requests routed/sec and prompt tokens hashed/sec at 1 GPU; % of HBM peak",
+        "value": n / (ms_step * 1e-3),
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {"workload": f"large: {n:,} requests, lognormal lengths (median 1,024, "
+                               "sigma 1.0, cap 16,384), 4,096 Zipf(1.1) templates, "
+                               "128 instances x 512 vnodes, block 16, K 4, 2^21-slot "
+                               "indexes of 1,048,576 keys",
+                   "n_req": n, "tokens": int(tokens.numel()), "full_block_tokens": ntok,
+                   "instances": wl.route.n_inst, "vnodes": wl.route.vnodes,
+                   "block": wl.route.block},
+        "tokens_hashed_per_s": ntok / (ms_step * 1e-3),
+        "tokens_hashed_per_s_hash_kernel": ntok / (hash_avg * 1e-3),
+        "stage_ms": {"hash_match": hash_avg, "select": float(np.mean(sel_ms))},
+        "roofline": {"bound": "hbm", "kernel": "hash_match_kernel<16>", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "algorithmic_bytes": alg},
+        "routing_stats": {"slo_switch_frac": float((flags & 1).mean()),
+                          "both_over_frac": float(((flags >> 1) & 1).mean()),
+                          "hit_blocks_frac": float(
+                              np.where(out["chosen"].cpu().numpy() == cand[:n], match[:n],
+                                       match[n:]).sum() / max(1, ntok // wl.route.block))},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_sample, n))
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,218 @@
+/*
+ * dualmap.h -- C ABI of the DualMap routing engine for AMD Instinct MI355X
+ * (gfx950).
+ *
+ * DualMap (arXiv 2602.06502) maps every request to two candidate instances
+ * with two independent hash functions over its prompt prefix, placed on two
+ * consistent-hash rings, and picks one with an SLO-aware rule that keeps the
+ * cache-affine candidate unless its expected TTFT breaks the SLO (Sec. 3.2);
+ * overloaded instances hand queued requests to the other member of their
+ * pair (Sec. 3.3); instances join and leave with only local remapping
+ * (Sec. 3.4).  This library runs that path as HIP kernels on one GPU.
+ *
+ * Conventions shared by every entry point
+ *   - Array arguments are caller-owned DEVICE memory unless marked "host".
+ *     The library never frees them; they must stay valid until the work is
+ *     complete (dm_sync returns).
+ *   - Calls are ordered on the stream given to dm_create.  Argument errors
+ *     are detected on the host, return DM_EINVAL at once and change no state.
+ *     Errors found by kernels (malformed offsets, a full index table, more
+ *     migrations than the output holds) set a device status word that the
+ *     next dm_sync returns (and clears).
+ *   - Integers: token ids are read as u32; block keys, ring positions and
+ *     ring keys are u64; loads and times are int64 (microseconds for times).
+ *   - No entry point throws or aborts; dm_last_error gives a message for the
+ *     last failing call on a context.
+ *   - A context is not thread safe: one host thread at a time.
+ */
+#ifndef DUALMAP_H
+#define DUALMAP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct dm_ctx dm_ctx;
+
+typedef enum {
+    DM_OK = 0,
+    DM_EINVAL = 1,  /* bad argument (host check) or malformed input (device) */
+    DM_ENOMEM = 2,  /* device or host allocation failed                      */
+    DM_EFULL = 3,   /* index table past its load limit / migrations > cap    */
+    DM_ESTATE = 4,  /* call out of order (e.g. routing before rings exist)   */
+    DM_EDEVICE = 5  /* HIP runtime error                                     */
+} dm_status;
+
+/* Engine configuration.  The hash functions f1, f2 of Sec. 3.2 are left
+ * unnamed by the paper; this engine uses, per function s, NH block digests
+ * keyed from a SplitMix64 stream seeded by seed[s], chained across blocks by
+ * an affine step with an odd multiplier, and finalised by the SplitMix64 mix
+ * xor seed[s].  Block b's key covers tokens [0, (b+1)*block_size). */
+typedef struct {
+    uint32_t block_size;        /* B: tokens per KV block; power of two, 4..64      */
+    uint32_t key_blocks;        /* K: ring keys hash the first K full blocks, 1..64  */
+    uint64_t seed[2];           /* seeds of f1 (ring 1) and f2 (ring 2)              */
+    uint32_t vnodes;            /* V >= 1 virtual nodes per instance on each ring    */
+    uint32_t max_slots;         /* instance ids are < max_slots; 1..4096             */
+    uint32_t index_log2_slots;  /* per-instance table holds 2^k keys, 4 <= k <= 30;  */
+                                /*   inserts fail (DM_EFULL) past 2^(k-1) keys       */
+    uint32_t reserved;          /* must be 0                                         */
+    int64_t ttft_base_us;       /* TTFT(us) = base + per_token * uncached tokens     */
+    int64_t ttft_per_token_us;  /*          + floor(load / queue_div)   (Sec. 3.2)   */
+    int64_t queue_div;          /* power of two >= 1                                 */
+    int64_t slo_us;             /* TTFT SLO; "exceeds" means >, "meets" means <=     */
+} dm_config;
+
+/* Create a context on the current HIP device, ordered on hip_stream (a
+ * hipStream_t; NULL = the default stream).  Allocates the per-instance index
+ * tables (max_slots * 2^index_log2_slots * 8 bytes) up front.  *out is set
+ * only on DM_OK. */
+dm_status dm_create(const dm_config* cfg, void* hip_stream, dm_ctx** out);
+
+/* Free a context and everything it owns (waits for its stream first). */
+void dm_destroy(dm_ctx* ctx);
+
+/* Set the live instance set to ids[0..n) (host array, distinct, each
+ * < max_slots, n >= 1) and build both consistent-hash rings (Sec. 3.4): each
+ * live instance gets V virtual nodes per ring at positions mixed from
+ * (id, v) and the ring's seed; a ring key belongs to the first virtual node
+ * at or after it, wrapping past the top (the (A,B] -> B rule of Sec. A.1.3).
+ * Index tables keep their contents. */
+dm_status dm_build_rings(dm_ctx* ctx, const uint32_t* ids, uint32_t n);
+
+/* Copy ring s (0 or 1) to host memory: *len entries sorted by position.
+ * pos/id may be NULL to query the length only; otherwise they hold cap
+ * entries.  Synchronises the stream. */
+dm_status dm_ring_export(dm_ctx* ctx, int s, uint64_t* pos_host, uint32_t* id_host,
+                         uint64_t cap, uint64_t* len);
+
+/* Add n block keys (device array) to instance id's cached-block index (the
+ * per-instance KV metadata of Sec. A.3.2) with set semantics.  Keys 0 and 1
+ * are stored as 2^63 and 2^63 + 1 (0 and 1 mark empty and erased slots).
+ * A table holds at most 2^(index_log2_slots - 1) keys; keys past that are
+ * dropped and dm_sync reports DM_EFULL. */
+dm_status dm_index_insert(dm_ctx* ctx, uint32_t id, const uint64_t* keys, uint64_t n);
+
+/* Remove n keys (device array) from instance id's index; absent keys are
+ * ignored.  Erased slots stay occupied until dm_index_clear. */
+dm_status dm_index_erase(dm_ctx* ctx, uint32_t id, const uint64_t* keys, uint64_t n);
+
+/* Empty instance id's index. */
+dm_status dm_index_clear(dm_ctx* ctx, uint32_t id);
+
+/* Number of keys held by instance id's index (host out).  Synchronises. */
+dm_status dm_index_size(dm_ctx* ctx, uint32_t id, uint64_t* n_host);
+
+/* Outputs of dm_route_batch (device arrays; all required except
+ * block_keys). */
+typedef struct {
+    uint64_t* key;        /* [2n] ring keys: f1 at [r], f2 at [n + r]               */
+    uint32_t* cand;       /* [2n] candidates c1 at [r], c2 at [n + r]               */
+    uint32_t* match;      /* [2n] cached leading blocks on c1 / c2                  */
+    uint32_t* chosen;     /* [n]  selected instance                                 */
+    int64_t* ttft_us;     /* [n]  estimated TTFT on the selected instance           */
+    uint8_t* flags;       /* [n]  bit0 left the cache-affine candidate for the SLO, */
+                          /*      bit1 both candidates' TTFT exceed the SLO (the    */
+                          /*      rebalance trigger of Sec. A.1.2), bit2 equal      */
+                          /*      match, bit3 second candidate adjusted             */
+    uint64_t* block_keys; /* NULL, or [sum of full blocks] every full block's f1    */
+                          /*      key, request-major (the keys a KV save inserts)   */
+} dm_route_out;
+
+/* Route a batch of n requests (Sec. 3.2, Sec. A.1.1).  Request r's prompt is
+ * tokens[offsets[r] .. offsets[r+1]) (int32 token ids; offsets int64, n + 1
+ * entries, non-decreasing, offsets[0] >= 0).  For every request:
+ *   1. chained f1/f2 block keys; ring keys x_s = key of the first
+ *      min(K, full blocks) blocks (no full block: the empty-prefix key);
+ *   2. c1 = owner of x1 on ring 1, c2 = owner of x2 on ring 2; if they
+ *      coincide c2 becomes the next live id after c1 in cyclic id order
+ *      (Sec. 3.2, id2 = (id1 + 1) mod n for dense ids);
+ *   3. match_c = number of leading full blocks whose f1 keys are all in
+ *      candidate c's index (index snapshot: not updated within the batch);
+ *   4. TTFT_c = base + per_token * (len - B * match_c) + floor(L[c] / div);
+ *   5. selection in request order with loads L = loads[] updated after each
+ *      request (L[chosen] += its uncached tokens): equal match -> the
+ *      less-loaded candidate (ties c1); otherwise the candidate with more
+ *      cached blocks unless its TTFT exceeds the SLO, then the other one if
+ *      strictly less loaded.
+ * loads: device int64 [max_slots], read and updated in place.  Requires
+ * rings (DM_ESTATE otherwise).  n = 0 is a no-op. */
+dm_status dm_route_batch(dm_ctx* ctx, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                         int64_t* loads, const dm_route_out* out);
+
+/* Pending-request queues, CSR over instance slots (device arrays).  Queue i
+ * is records [qoff[i], qoff[i+1]) head first; record q costs unc_here[q]
+ * uncached tokens on i and unc_alt[q] on its alternative candidate alt[q]
+ * (the other member of its dual-mapping pair); base_work[i] is pending work
+ * ahead of queue i. */
+typedef struct {
+    const int64_t* qoff;       /* [max_slots + 1], qoff[0] = 0, non-decreasing */
+    const uint64_t* rec_id;    /* [Q] caller's record ids                      */
+    const uint32_t* unc_here;  /* [Q]                                          */
+    const uint32_t* alt;       /* [Q] each < max_slots                         */
+    const uint32_t* unc_alt;   /* [Q]                                          */
+    const int64_t* base_work;  /* [max_slots]                                  */
+} dm_queues;
+
+/* Migration list of dm_rebalance (device arrays of cap entries). */
+typedef struct {
+    uint64_t* rec_id;
+    uint32_t* from;
+    uint32_t* to;
+    int64_t* benefit_us;  /* TTFT on the source minus TTFT on the target, at pass start */
+    int64_t* ttft_to_us;  /* TTFT on the target with its load when the record moved    */
+    uint64_t* count;      /* [1] number of migrations (may exceed cap: DM_EFULL)       */
+} dm_migrations;
+
+/* One non-recursive, single-round hotspot rebalancing pass (Sec. 3.3,
+ * Eq. of the migration benefit; Sec. A.1.2).  The TTFT of the record at
+ * queue position p of instance i waits behind base_work[i] and the records
+ * ahead of it.  Instance i is overloaded when some queued TTFT exceeds the
+ * SLO (judged at pass start).  Overloaded sources are taken heaviest load
+ * first (ties: lower id); within a source, records with benefit B > 0 whose
+ * alternative is not overloaded go in order of descending B (ties: nearer
+ * the head first).  Before each record the source stops if every queued
+ * TTFT meets the SLO; the record moves iff its TTFT on the target with the
+ * target's current load is below the SLO.  Migrations are listed in the
+ * order they happen.  loads_out[i] (device int64 [max_slots]) receives the
+ * final load: base work + queued uncached tokens + received records. */
+dm_status dm_rebalance(dm_ctx* ctx, const dm_queues* q, int64_t* loads_out,
+                       const dm_migrations* out, uint64_t cap);
+
+/* Change membership (Sec. 3.4; Sec. A.1.3): add ids add[0..n_add), remove
+ * rm[0..n_rm) (host arrays), rebuild both rings, and check the remap of n
+ * ring keys per ring (keys: device u64 [2n], ring 1 keys then ring 2 keys,
+ * e.g. dm_route_out.key).  old_owner/new_owner (device u32 [2n]) get each
+ * key's owner before and after; moved (device u64 [2]) counts changed owners
+ * per ring; violations (device u64 [1]) counts changes that neither leave a
+ * removed instance nor land on an added one (zero for consistent hashing).
+ * Removed and added instances' indexes are emptied.  DM_EINVAL (and no
+ * change) if an added id is live or out of range, a removed id is not live,
+ * either list repeats an id, or the new set would be empty. */
+dm_status dm_scale(dm_ctx* ctx, const uint32_t* add, uint32_t n_add, const uint32_t* rm,
+                   uint32_t n_rm, const uint64_t* keys, uint64_t n, uint32_t* old_owner,
+                   uint32_t* new_owner, uint64_t* moved, uint64_t* violations);
+
+/* Instrumentation.  With on != 0, dm_route_batch records HIP events on the
+ * context's stream around its stages; dm_route_stage_ms then waits for the
+ * last batch and writes up to n stage times in milliseconds to ms_host:
+ * [0] hashing, ring lookup and prefix match (one kernel), [1] in-order
+ * selection, [2] block-key offsets (0 when block keys were not requested). */
+dm_status dm_set_timing(dm_ctx* ctx, int on);
+dm_status dm_route_stage_ms(dm_ctx* ctx, float* ms_host, int n);
+
+/* Wait for all work on the context's stream; return and clear the first
+ * device-side error since the last dm_sync. */
+dm_status dm_sync(dm_ctx* ctx);
+
+/* Message of the last failing call on ctx ("" if none); valid until the next
+ * call on ctx. */
+const char* dm_last_error(const dm_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DUALMAP_H */

@@ -1,0 +1,504 @@
+// C ABI of the DualMap engine: argument checks, context state and the
+// host-side orchestration of the kernels.  Every computation on the routing
+// path runs in the kernels of the other files; this file only validates,
+// allocates and launches.
+#include <algorithm>
+#include <cstring>
+#include <string>
+
+#include "dm_internal.h"
+
+using namespace dm;
+
+namespace dm {
+
+dm_status fail(dm_ctx* c, dm_status s, const std::string& msg)
+{
+    if (c)
+        c->err = msg;
+    return s;
+}
+
+dm_status hip_fail(dm_ctx* c, hipError_t e, const char* what)
+{
+    if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation)
+        return fail(c, DM_ENOMEM, std::string(what) + ": out of device memory");
+    return fail(c, DM_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e)
+{
+    Scratch& s = c->scratch[slot];
+    *e = hipSuccess;
+    if (bytes == 0)
+        bytes = 256;
+    if (s.bytes >= bytes)
+        return s.p;
+    // Work already queued may still use the old buffer.
+    *e = hipStreamSynchronize(c->stream);
+    if (*e != hipSuccess)
+        return nullptr;
+    size_t nb = std::max(bytes, s.bytes * 2);
+    nb = (nb + 4095) & ~size_t(4095);
+    if (s.p)
+        hipFree(s.p);
+    s.p = nullptr;
+    s.bytes = 0;
+    *e = hipMalloc(&s.p, nb);
+    if (*e != hipSuccess) {
+        s.p = nullptr;
+        return nullptr;
+    }
+    s.bytes = nb;
+    return s.p;
+}
+
+}  // namespace dm
+
+namespace {
+
+// Makes ctx's device current for the duration of a call.
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = true;
+    explicit DeviceGuard(int dev)
+    {
+        if (hipGetDevice(&prev) != hipSuccess)
+            prev = -1;
+        if (prev != dev)
+            ok = hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard()
+    {
+        int now = -1;
+        if (prev >= 0 && hipGetDevice(&now) == hipSuccess && now != prev)
+            hipSetDevice(prev);
+    }
+};
+
+bool is_pow2(uint64_t x) { return x && !(x & (x - 1)); }
+
+uint32_t log2u(uint64_t x)
+{
+    uint32_t k = 0;
+    while ((1ull << k) < x)
+        k++;
+    return k;
+}
+
+uint64_t sm_next(uint64_t& st)
+{
+    st += 0x9E3779B97F4A7C15ull;
+    return mix64(st);
+}
+
+// Per-function hash parameters: B key words, odd multiplier P, chain start,
+// then the modular inverse of P and the lane power tables.
+void make_params(HashParams& hp, const dm_config& cfg)
+{
+    std::memset(&hp, 0, sizeof(hp));
+    for (int s = 0; s < 2; s++) {
+        uint64_t st = cfg.seed[s];
+        hp.seed[s] = cfg.seed[s];
+        for (uint32_t j = 0; j < cfg.block_size; j++)
+            hp.kk[s][j] = (uint32_t)sm_next(st);
+        const uint64_t P = sm_next(st) | 1ull;
+        hp.P[s] = P;
+        hp.H0[s] = sm_next(st);
+        uint64_t x = P;  // Newton iteration for P^-1 mod 2^64 (3 -> 96 bits)
+        for (int it = 0; it < 5; it++)
+            x *= 2 - P * x;
+        hp.Q[s] = x;
+        uint64_t pp = 1, qq = 1;
+        for (int l = 0; l < kWave; l++) {
+            pp *= P;
+            qq *= x;
+            hp.ppow[s][l] = pp;
+            hp.qpow[s][l] = qq;
+        }
+    }
+}
+
+template <typename T>
+bool aligned(const T* p)
+{
+    return (reinterpret_cast<uintptr_t>(p) % alignof(T)) == 0;
+}
+
+hipError_t upload_live(dm_ctx* c)
+{
+    const uint32_t S = c->cfg.max_slots;
+    std::vector<uint32_t> ids, nxt(S, 0);
+    for (uint32_t i = 0; i < S; i++)
+        if (c->live[i])
+            ids.push_back(i);
+    for (size_t k = 0; k < ids.size(); k++)
+        nxt[ids[k]] = ids[(k + 1) % ids.size()];
+    ids.resize(S, 0);
+    hipError_t e = hipMemcpyAsync(c->d_live_ids, ids.data(), S * sizeof(uint32_t),
+                                  hipMemcpyHostToDevice, c->stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(c->d_next_live, nxt.data(), S * sizeof(uint32_t),
+                           hipMemcpyHostToDevice, c->stream);
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(c->stream);  // host vectors go out of scope
+    return e;
+}
+
+void free_ring(dm::Ring& r)
+{
+    hipFree(r.pos);
+    hipFree(r.id);
+    hipFree(r.dir);
+    r = dm::Ring{};
+}
+
+}  // namespace
+
+extern "C" {
+
+dm_status dm_create(const dm_config* cfg, void* hip_stream, dm_ctx** out)
+{
+    if (!cfg || !out)
+        return DM_EINVAL;
+    const dm_config& k = *cfg;
+    if (!is_pow2(k.block_size) || k.block_size < 4 || k.block_size > 64 || k.key_blocks < 1 ||
+        k.key_blocks > 64 || k.vnodes < 1 || k.vnodes > (1u << 20) || k.max_slots < 1 ||
+        k.max_slots > kMaxSlots || k.index_log2_slots < 4 || k.index_log2_slots > 30 ||
+        k.reserved != 0 || k.queue_div < 1 || !is_pow2((uint64_t)k.queue_div))
+        return DM_EINVAL;
+    dm_ctx* c = new (std::nothrow) dm_ctx();
+    if (!c)
+        return DM_ENOMEM;
+    c->cfg = k;
+    c->stream = static_cast<hipStream_t>(hip_stream);
+    c->shift_div = log2u((uint64_t)k.queue_div);
+    c->live.assign(k.max_slots, 0);
+    make_params(c->hp, k);
+    hipError_t e = hipGetDevice(&c->device);
+    const size_t S = k.max_slots;
+    const size_t table_slots = S << k.index_log2_slots;
+    if (e == hipSuccess) e = hipMalloc(&c->d_hp, sizeof(HashParams));
+    if (e == hipSuccess) e = hipMalloc(&c->d_next_live, S * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMalloc(&c->d_live_ids, S * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMalloc(&c->d_flag_add, S);
+    if (e == hipSuccess) e = hipMalloc(&c->d_flag_rm, S);
+    if (e == hipSuccess) e = hipMalloc(&c->d_tables, table_slots * sizeof(uint64_t));
+    if (e == hipSuccess) e = hipMalloc(&c->d_counts, 2 * S * sizeof(uint64_t));
+    if (e == hipSuccess) e = hipMalloc(&c->d_status, sizeof(uint32_t));
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(c->d_hp, &c->hp, sizeof(HashParams), hipMemcpyHostToDevice, c->stream);
+    if (e == hipSuccess)
+        e = hipMemsetAsync(c->d_tables, 0, table_slots * sizeof(uint64_t), c->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(c->d_counts, 0, 2 * S * sizeof(uint64_t), c->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(c->d_status, 0, sizeof(uint32_t), c->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(c->d_next_live, 0, S * sizeof(uint32_t), c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) {
+        dm_status s = (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) ? DM_ENOMEM
+                                                                                   : DM_EDEVICE;
+        dm_destroy(c);
+        return s;
+    }
+    *out = c;
+    return DM_OK;
+}
+
+void dm_destroy(dm_ctx* c)
+{
+    if (!c)
+        return;
+    DeviceGuard g(c->device);
+    hipStreamSynchronize(c->stream);
+    for (auto& b : c->ring)
+        for (auto& r : b)
+            free_ring(r);
+    for (auto& s : c->scratch)
+        hipFree(s.p);
+    for (auto& ev : c->ev)
+        if (ev)
+            hipEventDestroy(ev);
+    hipFree(c->d_hp);
+    hipFree(c->d_next_live);
+    hipFree(c->d_live_ids);
+    hipFree(c->d_flag_add);
+    hipFree(c->d_flag_rm);
+    hipFree(c->d_tables);
+    hipFree(c->d_counts);
+    hipFree(c->d_status);
+    delete c;
+}
+
+dm_status dm_build_rings(dm_ctx* c, const uint32_t* ids, uint32_t n)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (!ids || n == 0)
+        return fail(c, DM_EINVAL, "dm_build_rings: need at least one instance id");
+    std::vector<uint8_t> seen(c->cfg.max_slots, 0);
+    for (uint32_t i = 0; i < n; i++) {
+        if (ids[i] >= c->cfg.max_slots)
+            return fail(c, DM_EINVAL, "dm_build_rings: id out of range");
+        if (seen[ids[i]])
+            return fail(c, DM_EINVAL, "dm_build_rings: duplicate id");
+        seen[ids[i]] = 1;
+    }
+    DeviceGuard g(c->device);
+    c->live = seen;
+    c->n_live = n;
+    hipError_t e = upload_live(c);
+    for (int s = 0; s < 2 && e == hipSuccess; s++)
+        e = ring_build(c, c->ring[c->cur][s], s, c->d_live_ids, n);
+    if (e != hipSuccess) {
+        c->n_live = 0;
+        return hip_fail(c, e, "dm_build_rings");
+    }
+    return DM_OK;
+}
+
+dm_status dm_ring_export(dm_ctx* c, int s, uint64_t* pos, uint32_t* id, uint64_t cap,
+                         uint64_t* len)
+{
+    if (!c || s < 0 || s > 1 || !len)
+        return fail(c, DM_EINVAL, "dm_ring_export: bad arguments");
+    const Ring& r = c->ring[c->cur][s];
+    *len = c->n_live ? r.len : 0;
+    if (!pos && !id)
+        return DM_OK;
+    if (cap < *len)
+        return fail(c, DM_EINVAL, "dm_ring_export: output too small");
+    DeviceGuard g(c->device);
+    hipError_t e = hipStreamSynchronize(c->stream);
+    if (e == hipSuccess && pos && *len)
+        e = hipMemcpy(pos, r.pos, *len * sizeof(uint64_t), hipMemcpyDeviceToHost);
+    if (e == hipSuccess && id && *len)
+        e = hipMemcpy(id, r.id, *len * sizeof(uint32_t), hipMemcpyDeviceToHost);
+    return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_ring_export");
+}
+
+dm_status dm_index_insert(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (id >= c->cfg.max_slots || (n && (!keys || !aligned(keys))))
+        return fail(c, DM_EINVAL, "dm_index_insert: bad id or key pointer");
+    if (n == 0)
+        return DM_OK;
+    DeviceGuard g(c->device);
+    hipError_t e = index_insert(c, id, keys, n);
+    return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_index_insert");
+}
+
+dm_status dm_index_erase(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (id >= c->cfg.max_slots || (n && (!keys || !aligned(keys))))
+        return fail(c, DM_EINVAL, "dm_index_erase: bad id or key pointer");
+    if (n == 0)
+        return DM_OK;
+    DeviceGuard g(c->device);
+    hipError_t e = index_erase(c, id, keys, n);
+    return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_index_erase");
+}
+
+dm_status dm_index_clear(dm_ctx* c, uint32_t id)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (id >= c->cfg.max_slots)
+        return fail(c, DM_EINVAL, "dm_index_clear: bad id");
+    DeviceGuard g(c->device);
+    hipError_t e = index_clear(c, id);
+    return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_index_clear");
+}
+
+dm_status dm_index_size(dm_ctx* c, uint32_t id, uint64_t* n_host)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (id >= c->cfg.max_slots || !n_host)
+        return fail(c, DM_EINVAL, "dm_index_size: bad arguments");
+    DeviceGuard g(c->device);
+    hipError_t e = hipStreamSynchronize(c->stream);
+    if (e == hipSuccess)
+        e = hipMemcpy(n_host, c->d_counts + id, sizeof(uint64_t), hipMemcpyDeviceToHost);
+    return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_index_size");
+}
+
+dm_status dm_route_batch(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                         int64_t* loads, const dm_route_out* out)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (c->n_live == 0)
+        return fail(c, DM_ESTATE, "dm_route_batch: rings not built");
+    if (n == 0)
+        return DM_OK;
+    if (!tokens || !offsets || !loads || !out || !out->key || !out->cand || !out->match ||
+        !out->chosen || !out->ttft_us || !out->flags)
+        return fail(c, DM_EINVAL, "dm_route_batch: null argument");
+    if (!aligned(tokens) || !aligned(offsets) || !aligned(loads) || !aligned(out->key) ||
+        !aligned(out->cand) || !aligned(out->match) || !aligned(out->chosen) ||
+        !aligned(out->ttft_us) || (out->block_keys && !aligned(out->block_keys)))
+        return fail(c, DM_EINVAL, "dm_route_batch: misaligned pointer");
+    if (n > (1ull << 40))
+        return fail(c, DM_EINVAL, "dm_route_batch: batch too large");
+    DeviceGuard g(c->device);
+    hipError_t e = route(c, tokens, offsets, n, loads, out);
+    return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_route_batch");
+}
+
+dm_status dm_rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out,
+                       const dm_migrations* out, uint64_t cap)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (!q || !q->qoff || !q->base_work || !loads_out || !out || !out->count)
+        return fail(c, DM_EINVAL, "dm_rebalance: null argument");
+    if (cap && (!out->rec_id || !out->from || !out->to || !out->benefit_us || !out->ttft_to_us))
+        return fail(c, DM_EINVAL, "dm_rebalance: null migration array");
+    if (!aligned(q->qoff) || !aligned(q->base_work) || !aligned(loads_out) ||
+        !aligned(out->count))
+        return fail(c, DM_EINVAL, "dm_rebalance: misaligned pointer");
+    DeviceGuard g(c->device);
+    // The record count sizes the work arrays: read qoff[max_slots].
+    int64_t Qs = 0, q0 = 0;
+    hipError_t e = hipStreamSynchronize(c->stream);
+    if (e == hipSuccess)
+        e = hipMemcpy(&Qs, q->qoff + c->cfg.max_slots, sizeof(int64_t), hipMemcpyDeviceToHost);
+    if (e == hipSuccess)
+        e = hipMemcpy(&q0, q->qoff, sizeof(int64_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess)
+        return hip_fail(c, e, "dm_rebalance");
+    if (q0 != 0 || Qs < 0 || Qs >= (1ll << 32))
+        return fail(c, DM_EINVAL, "dm_rebalance: qoff[0] must be 0 and the record count < 2^32");
+    if (Qs && (!q->rec_id || !q->unc_here || !q->alt || !q->unc_alt))
+        return fail(c, DM_EINVAL, "dm_rebalance: null record array");
+    e = rebalance(c, q, loads_out, out, cap, (uint64_t)Qs);
+    return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_rebalance");
+}
+
+dm_status dm_scale(dm_ctx* c, const uint32_t* add, uint32_t n_add, const uint32_t* rm,
+                   uint32_t n_rm, const uint64_t* keys, uint64_t n, uint32_t* old_owner,
+                   uint32_t* new_owner, uint64_t* moved, uint64_t* violations)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (c->n_live == 0)
+        return fail(c, DM_ESTATE, "dm_scale: rings not built");
+    if ((n_add && !add) || (n_rm && !rm) || !moved || !violations ||
+        (n && (!keys || !old_owner || !new_owner)))
+        return fail(c, DM_EINVAL, "dm_scale: null argument");
+    if (!aligned(moved) || !aligned(violations) || (n && (!aligned(keys) || !aligned(old_owner) ||
+                                                          !aligned(new_owner))))
+        return fail(c, DM_EINVAL, "dm_scale: misaligned pointer");
+    const uint32_t S = c->cfg.max_slots;
+    std::vector<uint8_t> fa(S, 0), fr(S, 0);
+    for (uint32_t k = 0; k < n_add; k++) {
+        if (add[k] >= S || c->live[add[k]] || fa[add[k]])
+            return fail(c, DM_EINVAL, "dm_scale: added id is live, repeated or out of range");
+        fa[add[k]] = 1;
+    }
+    for (uint32_t k = 0; k < n_rm; k++) {
+        if (rm[k] >= S || !c->live[rm[k]] || fr[rm[k]])
+            return fail(c, DM_EINVAL, "dm_scale: removed id is not live or repeated");
+        fr[rm[k]] = 1;
+    }
+    if (c->n_live - n_rm + n_add == 0)
+        return fail(c, DM_EINVAL, "dm_scale: no instance would remain");
+    DeviceGuard g(c->device);
+    std::vector<uint8_t> live = c->live;
+    for (uint32_t i = 0; i < S; i++)
+        live[i] = (live[i] && !fr[i]) || fa[i];
+    const std::vector<uint8_t> old_live = c->live;
+    const uint32_t old_n = c->n_live;
+    c->live = live;
+    c->n_live = old_n - n_rm + n_add;
+    hipError_t e = upload_live(c);
+    if (e == hipSuccess)
+        e = hipMemcpy(c->d_flag_add, fa.data(), S, hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(c->d_flag_rm, fr.data(), S, hipMemcpyHostToDevice);
+    const int nb = 1 - c->cur;
+    for (int s = 0; s < 2 && e == hipSuccess; s++)
+        e = ring_build(c, c->ring[nb][s], s, c->d_live_ids, c->n_live);
+    if (e == hipSuccess)
+        e = ring_remap(c, c->ring[c->cur], c->ring[nb], keys, n, old_owner, new_owner, moved,
+                       violations);
+    for (uint32_t i = 0; i < S && e == hipSuccess; i++)
+        if (fa[i] || fr[i])
+            e = index_clear(c, i);
+    if (e != hipSuccess) {
+        c->live = old_live;
+        c->n_live = old_n;
+        upload_live(c);
+        return hip_fail(c, e, "dm_scale");
+    }
+    c->cur = nb;
+    return DM_OK;
+}
+
+dm_status dm_set_timing(dm_ctx* c, int on)
+{
+    if (!c)
+        return DM_EINVAL;
+    DeviceGuard g(c->device);
+    if (on && !c->ev[0]) {
+        for (auto& ev : c->ev) {
+            hipError_t e = hipEventCreate(&ev);
+            if (e != hipSuccess)
+                return hip_fail(c, e, "dm_set_timing");
+        }
+    }
+    c->timing = on != 0;
+    return DM_OK;
+}
+
+dm_status dm_route_stage_ms(dm_ctx* c, float* ms, int n)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (!ms || n < 1)
+        return fail(c, DM_EINVAL, "dm_route_stage_ms: bad output");
+    if (!c->timing || !c->ev[0])
+        return fail(c, DM_ESTATE, "dm_route_stage_ms: timing is off");
+    DeviceGuard g(c->device);
+    hipError_t e = hipEventSynchronize(c->ev[3]);
+    float t[3] = {0, 0, 0};
+    if (e == hipSuccess) e = hipEventElapsedTime(&t[0], c->ev[1], c->ev[2]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t[1], c->ev[2], c->ev[3]);
+    if (e == hipSuccess && c->timed_bk) e = hipEventElapsedTime(&t[2], c->ev[0], c->ev[1]);
+    if (e != hipSuccess)
+        return hip_fail(c, e, "dm_route_stage_ms");
+    for (int k = 0; k < n && k < 3; k++)
+        ms[k] = t[k];
+    return DM_OK;
+}
+
+dm_status dm_sync(dm_ctx* c)
+{
+    if (!c)
+        return DM_EINVAL;
+    DeviceGuard g(c->device);
+    hipError_t e = hipStreamSynchronize(c->stream);
+    uint32_t st = 0;
+    if (e == hipSuccess)
+        e = hipMemcpy(&st, c->d_status, sizeof(uint32_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess)
+        return hip_fail(c, e, "dm_sync");
+    if (st) {
+        uint32_t zero = 0;
+        e = hipMemcpy(c->d_status, &zero, sizeof(uint32_t), hipMemcpyHostToDevice);
+        if (e != hipSuccess)
+            return hip_fail(c, e, "dm_sync");
+        if (st & kErrInval)
+            return fail(c, DM_EINVAL, "device: malformed input (offsets or queue records)");
+        return fail(c, DM_EFULL, "device: index table full or migration list over capacity");
+    }
+    return DM_OK;
+}
+
+const char* dm_last_error(const dm_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+}  // extern "C"

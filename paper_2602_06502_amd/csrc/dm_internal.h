@@ -1,0 +1,234 @@
+// Internal declarations of the DualMap HIP engine (gfx950).  Not part of the
+// public ABI: include/dualmap.h is.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "dualmap.h"
+
+namespace dm {
+
+constexpr int kWave = 64;
+constexpr uint32_t kMaxSlots = 4096;
+constexpr uint64_t kEmpty = 0;      // index slot never used
+constexpr uint64_t kTomb = 1;       // index slot erased
+constexpr uint32_t kBucket = 8;     // slots per probe bucket (one 64-byte line)
+
+// Device status word bits (reported by dm_sync).
+constexpr uint32_t kErrInval = 1u;
+constexpr uint32_t kErrFull = 2u;
+
+// Hash parameters of both functions, computed on the host at dm_create.
+// For function s: key words kk[s][0..B), odd multiplier P, its inverse
+// Q = P^-1 mod 2^64, chain start H0, and per-lane powers P^(l+1), Q^(l+1)
+// for l = 0..63 used by the wave-parallel chain.
+struct HashParams {
+    uint64_t seed[2];
+    uint64_t P[2];
+    uint64_t Q[2];
+    uint64_t H0[2];
+    uint64_t ppow[2][kWave];
+    uint64_t qpow[2][kWave];
+    uint32_t kk[2][64];
+};
+
+// One consistent-hash ring: positions ascending, owner ids, and a radix
+// directory dir[k] = first index whose position >= k << (64 - dbits).
+struct Ring {
+    uint64_t* pos = nullptr;
+    uint32_t* id = nullptr;
+    uint32_t* dir = nullptr;
+    uint64_t cap = 0;      // entries allocated
+    uint32_t dcap = 0;     // directory entries allocated
+    uint64_t len = 0;
+    uint32_t dbits = 1;
+};
+
+struct RingView {
+    const uint64_t* pos;
+    const uint32_t* id;
+    const uint32_t* dir;
+    uint64_t len;
+    uint32_t dbits;
+};
+
+// Growable device scratch.
+struct Scratch {
+    void* p = nullptr;
+    size_t bytes = 0;
+};
+
+}  // namespace dm
+
+struct dm_ctx {
+    dm_config cfg;
+    hipStream_t stream = nullptr;
+    int device = 0;
+    std::string err;
+
+    // live set (host) and cyclic next-live table (device)
+    std::vector<uint8_t> live;
+    uint32_t n_live = 0;
+    uint32_t* d_next_live = nullptr;  // [max_slots]
+    uint32_t* d_live_ids = nullptr;   // [max_slots] ascending live ids
+    uint8_t* d_flag_add = nullptr;    // [max_slots] scale: added this call
+    uint8_t* d_flag_rm = nullptr;     // [max_slots] scale: removed this call
+
+    dm::HashParams hp{};
+    dm::HashParams* d_hp = nullptr;
+
+    dm::Ring ring[2][2];   // [buffer][s]
+    int cur = 0;           // active ring buffer
+
+    uint64_t* d_tables = nullptr;  // [max_slots << log2slots]
+    uint64_t* d_counts = nullptr;  // [2 * max_slots] live keys, then occupied slots
+    uint32_t* d_status = nullptr;  // device status word
+
+    dm::Scratch scratch[8];
+    uint32_t shift_div = 0;        // log2(queue_div)
+
+    // stage timing of dm_route_batch (events recorded only when enabled)
+    bool timing = false;
+    bool timed_bk = false;         // last timed batch emitted block keys
+    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+};
+
+namespace dm {
+
+// ---------------------------------------------------------------------------
+// Host helpers (dm_api.hip)
+// ---------------------------------------------------------------------------
+dm_status fail(dm_ctx* c, dm_status s, const std::string& msg);
+dm_status hip_fail(dm_ctx* c, hipError_t e, const char* what);
+void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e);
+
+inline RingView view(const Ring& r) { return RingView{r.pos, r.id, r.dir, r.len, r.dbits}; }
+
+// ---------------------------------------------------------------------------
+// Launchers (one per kernel family), all asynchronous on c->stream.
+// ---------------------------------------------------------------------------
+
+// dm_scan.hip: exclusive prefix sums.
+hipError_t exclusive_scan_u64(dm_ctx* c, const uint64_t* in, uint64_t n, uint64_t* out,
+                              uint64_t* total_out);
+hipError_t block_starts(dm_ctx* c, const int64_t* offsets, uint64_t n, uint64_t* starts);
+
+// dm_sort.hip: stable LSD radix sort of (u64 key, u32 value) pairs on the
+// low `bits` bits of the key (bits multiple of 8).  Sorted data ends in
+// keys/vals; ktmp/vtmp are same-sized work arrays.
+hipError_t radix_sort_kv(dm_ctx* c, uint64_t* keys, uint32_t* vals, uint64_t* ktmp,
+                         uint32_t* vtmp, uint64_t n, int bits);
+
+// dm_ring.hip
+hipError_t ring_build(dm_ctx* c, Ring& r, int s, const uint32_t* d_live_ids, uint32_t n_live);
+hipError_t ring_remap(dm_ctx* c, const Ring old_r[2], const Ring new_r[2], const uint64_t* keys,
+                      uint64_t n, uint32_t* old_owner, uint32_t* new_owner, uint64_t* moved,
+                      uint64_t* violations);
+
+// dm_index.hip
+hipError_t index_insert(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n);
+hipError_t index_erase(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n);
+hipError_t index_clear(dm_ctx* c, uint32_t id);
+
+// dm_route.hip
+hipError_t route(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                 int64_t* loads, const dm_route_out* out);
+
+// dm_rebalance.hip
+hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm_migrations* out,
+                     uint64_t cap, uint64_t Q);
+
+}  // namespace dm
+
+// ---------------------------------------------------------------------------
+// Device helpers shared by the kernels.
+// ---------------------------------------------------------------------------
+namespace dm {
+
+// SplitMix64 finaliser (Steele, Lea and Flood 2014).
+__host__ __device__ __forceinline__ uint64_t mix64(uint64_t z)
+{
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// Index key: 0 and 1 are reserved for empty and erased slots.
+__host__ __device__ __forceinline__ uint64_t canon_key(uint64_t k)
+{
+    return k >= 2 ? k : k + (1ull << 63);
+}
+
+// Home bucket of a key in a table of 2^log2slots slots (8-slot buckets).
+__device__ __forceinline__ uint64_t home_bucket(uint64_t ck, uint32_t log2slots)
+{
+    return ck >> (64 - (log2slots - 3));
+}
+
+// Integer TTFT estimate: base + per_token * uncached + floor(load / 2^shift).
+__device__ __forceinline__ int64_t ttft_us(int64_t base, int64_t per, uint32_t shift, int64_t unc,
+                                           int64_t load)
+{
+    return base + per * unc + (load >> shift);
+}
+
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src)
+{
+    uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+    lo = __shfl(lo, src);
+    hi = __shfl(hi, src);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane)
+{
+    uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, lane);
+    uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), lane);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Inclusive prefix sum of a u64 over the 64 lanes of a wave.
+__device__ __forceinline__ uint64_t wave_incl_sum_u64(uint64_t v, int lane)
+{
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        uint64_t o = shfl_u64(v, lane >= d ? lane - d : lane);
+        if (lane >= d)
+            v += o;
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
+{
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+        uint32_t lo = __shfl_xor((uint32_t)v, d), hi = __shfl_xor((uint32_t)(v >> 32), d);
+        v += ((uint64_t)hi << 32) | lo;
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+
+// Owner of ring key x: the first ring entry at a position >= x, wrapping to
+// entry 0 past the top.  The directory bounds the search to x's bucket.
+__device__ __forceinline__ uint32_t ring_owner(const RingView& r, uint64_t x)
+{
+    const uint64_t b = x >> (64 - r.dbits);
+    uint64_t i = r.dir[b];
+    const uint64_t e = r.dir[b + 1];
+    while (i < e && r.pos[i] < x)
+        i++;
+    if (i >= r.len)
+        i = 0;
+    return r.id[i];
+}
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+}  // namespace dm

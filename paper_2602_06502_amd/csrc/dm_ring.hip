@@ -1,0 +1,151 @@
+// Consistent-hash rings (Sec. 3.4; Sec. A.1.3): virtual-node placement,
+// sorting, the bucket directory used by lookups, and the remap check of a
+// membership change.
+#include "dm_internal.h"
+
+namespace dm {
+namespace {
+
+constexpr int kRingSlot = 5;  // sort work arrays
+
+// Virtual node v of live instance k on ring s sits at
+// mix64(((id << 32) | v) xor mix64(seed_s)).
+__global__ void vnode_kernel(const uint32_t* __restrict__ live_ids, uint32_t vnodes, uint64_t len,
+                             uint64_t salt, uint64_t* __restrict__ pos, uint32_t* __restrict__ id)
+{
+    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < len;
+         i += (uint64_t)gridDim.x * blockDim.x) {
+        const uint32_t inst = live_ids[i / vnodes];
+        const uint32_t v = (uint32_t)(i % vnodes);
+        pos[i] = mix64((((uint64_t)inst << 32) | v) ^ salt);
+        id[i] = inst;
+    }
+}
+
+// dir[k] = first index whose position >= k << (64 - dbits), k = 0..2^dbits.
+// Entry i (i = 0..len, i = len meaning "past the end") fills the buckets
+// after its predecessor's bucket up to its own.
+__global__ void directory_kernel(const uint64_t* __restrict__ pos, uint64_t len, uint32_t dbits,
+                                 uint32_t* __restrict__ dir)
+{
+    const uint64_t nb = 1ull << dbits;
+    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i <= len;
+         i += (uint64_t)gridDim.x * blockDim.x) {
+        const uint64_t lo = i == 0 ? 0 : (pos[i - 1] >> (64 - dbits)) + 1;
+        const uint64_t hi = i == len ? nb : (pos[i] >> (64 - dbits));
+        for (uint64_t b = lo; b <= hi; b++)
+            dir[b] = (uint32_t)i;
+    }
+}
+
+__global__ void zero_u64_kernel(uint64_t* p, uint32_t n)
+{
+    if (threadIdx.x < n)
+        p[threadIdx.x] = 0;
+}
+
+__global__ void remap_kernel(RingView o1, RingView o2, RingView n1, RingView n2,
+                             const uint64_t* __restrict__ keys, uint64_t n,
+                             const uint8_t* __restrict__ is_add, const uint8_t* __restrict__ is_rm,
+                             uint32_t* __restrict__ old_owner, uint32_t* __restrict__ new_owner,
+                             uint64_t* __restrict__ moved, uint64_t* __restrict__ violations)
+{
+    const uint64_t total = 2 * n;
+    for (uint64_t base = blockIdx.x * (uint64_t)blockDim.x; base < total;
+         base += (uint64_t)gridDim.x * blockDim.x) {
+        const uint64_t k = base + threadIdx.x;
+        const bool ok = k < total;
+        const bool second = ok && k >= n;
+        bool mv = false, bad = false;
+        if (ok) {
+            const uint64_t x = keys[k];
+            const uint32_t a = ring_owner(second ? o2 : o1, x);
+            const uint32_t b = ring_owner(second ? n2 : n1, x);
+            old_owner[k] = a;
+            new_owner[k] = b;
+            mv = a != b;
+            bad = mv && !is_rm[a] && !is_add[b];
+        }
+        const uint64_t m1 = ballot(mv && !second), m2 = ballot(mv && second), mb = ballot(bad);
+        if ((threadIdx.x & 63) == 0) {
+            if (m1) atomicAdd((unsigned long long*)&moved[0], (unsigned long long)__popcll(m1));
+            if (m2) atomicAdd((unsigned long long*)&moved[1], (unsigned long long)__popcll(m2));
+            if (mb) atomicAdd((unsigned long long*)violations, (unsigned long long)__popcll(mb));
+        }
+    }
+}
+
+uint32_t grid_for(uint64_t n, int threads, uint32_t cap = 65536)
+{
+    uint64_t g = (n + threads - 1) / threads;
+    if (g < 1) g = 1;
+    return (uint32_t)(g > cap ? cap : g);
+}
+
+}  // namespace
+
+hipError_t ring_build(dm_ctx* c, Ring& r, int s, const uint32_t* d_live_ids, uint32_t n_live)
+{
+    const uint64_t len = (uint64_t)n_live * c->cfg.vnodes;
+    uint32_t dbits = 1;
+    while ((1ull << dbits) < len && dbits < 24)
+        dbits++;
+    hipError_t e = hipSuccess;
+    if (r.cap < len) {
+        e = hipStreamSynchronize(c->stream);
+        hipFree(r.pos);
+        hipFree(r.id);
+        r.pos = nullptr;
+        r.id = nullptr;
+        r.cap = 0;
+        if (e == hipSuccess) e = hipMalloc(&r.pos, len * sizeof(uint64_t));
+        if (e == hipSuccess) e = hipMalloc(&r.id, len * sizeof(uint32_t));
+        if (e != hipSuccess)
+            return e;
+        r.cap = len;
+    }
+    const uint32_t dneed = (1u << dbits) + 1;
+    if (r.dcap < dneed) {
+        e = hipStreamSynchronize(c->stream);
+        hipFree(r.dir);
+        r.dir = nullptr;
+        r.dcap = 0;
+        if (e == hipSuccess) e = hipMalloc(&r.dir, dneed * sizeof(uint32_t));
+        if (e != hipSuccess)
+            return e;
+        r.dcap = dneed;
+    }
+    uint8_t* tmp = static_cast<uint8_t*>(
+        scratch_get(c, kRingSlot, len * (sizeof(uint64_t) + sizeof(uint32_t)) + 64, &e));
+    if (!tmp)
+        return e;
+    uint64_t* ktmp = reinterpret_cast<uint64_t*>(tmp);
+    uint32_t* vtmp = reinterpret_cast<uint32_t*>(tmp + len * sizeof(uint64_t));
+    const uint64_t salt = mix64(c->cfg.seed[s]);
+    vnode_kernel<<<grid_for(len, 256), 256, 0, c->stream>>>(d_live_ids, c->cfg.vnodes, len, salt,
+                                                            r.pos, r.id);
+    e = hipGetLastError();
+    if (e == hipSuccess)
+        e = radix_sort_kv(c, r.pos, r.id, ktmp, vtmp, len, 64);
+    if (e != hipSuccess)
+        return e;
+    directory_kernel<<<grid_for(len + 1, 256), 256, 0, c->stream>>>(r.pos, len, dbits, r.dir);
+    r.len = len;
+    r.dbits = dbits;
+    return hipGetLastError();
+}
+
+hipError_t ring_remap(dm_ctx* c, const Ring old_r[2], const Ring new_r[2], const uint64_t* keys,
+                      uint64_t n, uint32_t* old_owner, uint32_t* new_owner, uint64_t* moved,
+                      uint64_t* violations)
+{
+    zero_u64_kernel<<<1, 64, 0, c->stream>>>(moved, 2);
+    zero_u64_kernel<<<1, 64, 0, c->stream>>>(violations, 1);
+    if (n)
+        remap_kernel<<<grid_for(2 * n, 256, 8192), 256, 0, c->stream>>>(
+            view(old_r[0]), view(old_r[1]), view(new_r[0]), view(new_r[1]), keys, n,
+            c->d_flag_add, c->d_flag_rm, old_owner, new_owner, moved, violations);
+    return hipGetLastError();
+}
+
+}  // namespace dm

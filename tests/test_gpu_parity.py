@@ -1,0 +1,431 @@
+"""HIP engine vs CPU oracle, element by element, through the C ABI.
+
+Every case builds its starting state on each side with that side's own code
+(paper_2602_06502_amd.harness for the engine, oracle.harness for the
+oracle) from the same seeded inputs, then compares all outputs bit for bit:
+ring arrays, ring keys, candidates, match lengths, chosen instances, TTFTs,
+flags, updated loads, block keys, migration lists and remap results.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import oracle.harness as oh
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2602_06502_amd as pk
+    pk.load_library()  # fails loudly if the library is missing
+    oracle.build(force=False)
+    yield
+
+
+def _h():
+    import paper_2602_06502_amd.harness as gh
+    return gh
+
+
+def cpu(t):
+    return t.cpu().numpy()
+
+
+def compare_route(g, o, n, with_bk=False):
+    for k in ("key", "cand", "match", "chosen", "ttft", "flags"):
+        a, b = cpu(g[k]), o[k]
+        if not np.array_equal(a, b):
+            bad = np.nonzero(a != b)[0]
+            raise AssertionError(f"{k}: {len(bad)} mismatches, first at {bad[:5]}: "
+                                 f"gpu {a[bad[:5]]} oracle {b[bad[:5]]}")
+    if with_bk:
+        assert np.array_equal(cpu(g["block_keys"])[:len(o["block_keys"])], o["block_keys"])
+
+
+def run_pair(wl, block_keys=True, n_live=None):
+    gh = _h()
+    _say("setup", wl.name, wl.route)
+    eng = gh.engine_for(wl, n_live=n_live)
+    o = oh.oracle_for(wl, n_live=n_live)
+    if wl.filler_per_inst:
+        gh.prefill_templates(eng, wl)
+        oh.prefill_templates(o, wl)
+    else:
+        gh.prefill_from_prior(eng, wl)
+        oh.prefill_from_prior(o, wl)
+    tok, off = workloads.prompts(wl, wl.n_req, sub=0)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    _say("route", wl.name, "n", wl.n_req, "tokens", len(tok))
+    Ld = gh.to_dev(L0, eng.device)
+    g = eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld, block_keys=block_keys)
+    eng.sync()
+    r = o.route(tok, off, L0, block_keys=block_keys)
+    compare_route(g, r, wl.n_req, with_bk=block_keys)
+    assert np.array_equal(cpu(Ld), r["loads"])
+    return eng, o, g, r, tok, off
+
+
+def test_rings_match_oracle():
+    for wl in (workloads.tiny(), workloads.small_random(3, 5, 7, 16, 10)):
+        gh = _h()
+        eng = gh.engine_for(wl)
+        o = oh.oracle_for(wl)
+        for s in (0, 1):
+            gp, gi = eng.ring(s)
+            op, oi = o.ring(s)
+            assert np.array_equal(gp, op) and np.array_equal(gi, oi)
+
+
+def test_tiny_parity():
+    eng, o, g, r, tok, off = run_pair(workloads.tiny())
+    # Tiny never reaches the SLO knee (every TTFT << 400 ms)
+    assert (r["flags"] & 1).sum() == 0
+    assert (r["match"] > 0).mean() > 0.2
+
+
+def test_tiny_tight_parity():
+    eng, o, g, r, tok, off = run_pair(workloads.tiny(slo_us=20_000))
+    f = r["flags"]
+    assert (f & 1).sum() > 0 and (f & 2).sum() > 0  # both SLO branches taken
+
+
+@pytest.mark.parametrize("seed,n_inst,vnodes,block", [
+    (0, 1, 4, 16), (1, 2, 1, 4), (2, 3, 16, 8), (3, 9, 5, 32), (4, 7, 16, 64), (5, 4, 2, 16),
+    (6, 5, 9, 4), (7, 8, 16, 16),
+])
+def test_random_small_parity(seed, n_inst, vnodes, block):
+    wl = workloads.small_random(seed, n_inst, vnodes, block, 300 + 37 * seed,
+                                slo_us=3_000 if seed % 2 else 400_000)
+    run_pair(wl)
+
+
+def test_sparse_live_ids_parity():
+    # ids 0..n-1 not all live: fixup must take the next live id
+    wl = workloads.small_random(11, 6, 3, 16, 400)
+    gh = _h()
+    eng = gh.DualMap(wl.route.as_dict(), device="cuda:0")
+    o = oracle.Oracle(wl.route.as_dict())
+    ids = [0, 2, 5, 8]
+    eng.build_rings(ids)
+    o.build_rings(ids)
+    tok, off = workloads.prompts(wl, wl.n_req)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    Ld = gh.to_dev(L0, eng.device)
+    g = eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld)
+    eng.sync()
+    r = o.route(tok, off, L0)
+    compare_route(g, r, wl.n_req)
+    assert (r["flags"] & 8).sum() > 0
+    assert set(np.unique(r["cand"]).tolist()) <= set(ids)
+
+
+def test_long_prompts_cross_chunks():
+    """Prompts spanning many 64-block chunks, with cached prefixes ending
+    inside, at and across chunk boundaries (ragged tails included)."""
+    gh = _h()
+    B = 16
+    cfg = dict(block=B, key_blocks=4, seeds=(7, 9), vnodes=8, max_slots=4, index_log2_slots=14)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    o = oracle.Oracle(cfg)
+    eng.build_rings([0, 1, 2, 3])
+    o.build_rings([0, 1, 2, 3])
+    rng = np.random.default_rng(5)
+    base = rng.integers(0, 1000, size=B * 300).astype(np.int32)
+    # cache the first 200 blocks of `base` on every instance
+    keys = o.chain(0, base[:200 * B])
+    for c in range(4):
+        eng.index_insert(c, gh.to_dev(keys, eng.device))
+        o.index_insert(c, keys)
+    prompts = []
+    for cut in (0, 1, 63, 64, 65, 127, 128, 129, 199, 200, 250):
+        for extra in (0, 5, B * 70 + 3):
+            p = np.concatenate([base[:cut * B], rng.integers(2000, 3000, size=extra).astype(np.int32)])
+            prompts.append(p)
+    off = np.zeros(len(prompts) + 1, np.int64)
+    off[1:] = np.cumsum([len(p) for p in prompts])
+    tok = np.concatenate(prompts)
+    L0 = rng.integers(0, 1000, size=4).astype(np.int64)
+    Ld = gh.to_dev(L0, eng.device)
+    g = eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld, block_keys=True)
+    eng.sync()
+    r = o.route(tok, off, L0, block_keys=True)
+    compare_route(g, r, len(prompts), with_bk=True)
+    assert np.array_equal(cpu(Ld), r["loads"])
+
+
+def test_edge_cases_and_errors():
+    gh = _h()
+    import paper_2602_06502_amd as pk
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=4, index_log2_slots=10)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    dev = eng.device
+    L = torch.zeros(4, dtype=torch.int64, device=dev)
+    # routing before rings exist
+    with pytest.raises(pk.DMError) as ei:
+        eng.route(torch.zeros(4, dtype=torch.int32, device=dev),
+                  torch.tensor([0, 4], dtype=torch.int64, device=dev), L)
+    assert ei.value.status == pk.DM_ESTATE
+    with pytest.raises(pk.DMError):
+        eng.build_rings([])
+    with pytest.raises(pk.DMError):
+        eng.build_rings([1, 1])
+    with pytest.raises(pk.DMError):
+        eng.build_rings([9])
+    eng.build_rings([0, 1, 2, 3])
+    o = oracle.Oracle(cfg)
+    o.build_rings([0, 1, 2, 3])
+    # n = 0 is a no-op
+    out = eng.route(torch.zeros(1, dtype=torch.int32, device=dev),
+                    torch.zeros(1, dtype=torch.int64, device=dev), L)
+    eng.sync()
+    # empty and sub-block prompts
+    off = np.array([0, 0, 5, 5, 21, 37], np.int64)
+    tok = np.arange(37, dtype=np.int32)
+    g = eng.route(gh.to_dev(tok, dev), gh.to_dev(off, dev), L)
+    eng.sync()
+    r = o.route(tok, off, np.zeros(4, np.int64))
+    compare_route(g, r, 5)
+    # malformed offsets are reported by dm_sync (the batch is not read past them)
+    bad = torch.tensor([0, 8, 4], dtype=torch.int64, device=dev)
+    eng.route(torch.zeros(8, dtype=torch.int32, device=dev), bad, L)
+    with pytest.raises(pk.DMError) as ei:
+        eng.sync()
+    assert ei.value.status == pk.DM_EINVAL
+    eng.sync()  # cleared
+    # misaligned pointer rejected on the host
+    lib = pk.load_library()
+    import ctypes as C
+    buf = torch.zeros(64, dtype=torch.int64, device=dev)
+    ro = pk.dm_route_out(buf.data_ptr() + 4, buf.data_ptr(), buf.data_ptr(), buf.data_ptr(),
+                         buf.data_ptr(), buf.data_ptr(), None)
+    st = lib.dm_route_batch(eng._h, buf.data_ptr(), buf.data_ptr(), 2, L.data_ptr(), C.byref(ro))
+    assert st == pk.DM_EINVAL
+    st = lib.dm_route_batch(eng._h, None, buf.data_ptr(), 2, L.data_ptr(), C.byref(ro))
+    assert st == pk.DM_EINVAL
+
+
+def test_index_ops_and_capacity():
+    gh = _h()
+    import paper_2602_06502_amd as pk
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=3, index_log2_slots=8)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    dev = eng.device
+    rng = np.random.default_rng(1)
+    keys = rng.integers(0, 2**64, size=100, dtype=np.uint64)
+    keys[:3] = [0, 1, 1 << 63]
+    dup = np.concatenate([keys, keys[:50]])
+    eng.index_insert(0, gh.to_dev(dup, dev))
+    eng.sync()
+    assert eng.index_size(0) == len(np.unique([oracle.canon(int(k)) for k in keys]))
+    eng.index_erase(0, gh.to_dev(keys[10:20], dev))
+    eng.sync()
+    left = {oracle.canon(int(k)) for k in keys} - {oracle.canon(int(k)) for k in keys[10:20]}
+    assert eng.index_size(0) == len(left)
+    eng.index_clear(0)
+    eng.sync()
+    assert eng.index_size(0) == 0
+    # capacity: 2^8 slots hold at most 128 keys
+    many = rng.integers(2, 2**64, size=200, dtype=np.uint64)
+    eng.index_insert(1, gh.to_dev(many[:128], dev))
+    eng.sync()
+    assert eng.index_size(1) == 128
+    eng.index_insert(1, gh.to_dev(many[128:], dev))
+    with pytest.raises(pk.DMError) as ei:
+        eng.sync()
+    assert ei.value.status == pk.DM_EFULL
+    assert eng.index_size(1) == 128
+
+
+def test_index_erase_then_match_parity():
+    """Erased blocks break a cached prefix at the erased block."""
+    gh = _h()
+    wl = workloads.tiny()
+    eng = gh.engine_for(wl)
+    o = oh.oracle_for(wl)
+    gh.prefill_from_prior(eng, wl)
+    oh.prefill_from_prior(o, wl)
+    ttok, toff = workloads.templates(wl)
+    some = o.chain(0, ttok[toff[0]:toff[1]])[3:6]
+    for c in range(8):
+        eng.index_erase(c, gh.to_dev(some, eng.device))
+        o.index_erase(c, some)
+    tok, off = workloads.prompts(wl, wl.n_req)
+    L0 = workloads.initial_loads(wl, 8)
+    Ld = gh.to_dev(L0, eng.device)
+    g = eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld)
+    eng.sync()
+    r = o.route(tok, off, L0)
+    compare_route(g, r, wl.n_req)
+    for c in range(8):
+        assert eng.index_size(c) == o.index_size(c)
+
+
+# ---------------------------------------------------------------------------
+# Rebalance
+# ---------------------------------------------------------------------------
+
+def compare_rebalance(eng, o, q, cap=None):
+    gh = _h()
+    dev = eng.device
+    g = eng.rebalance(gh.to_dev(q.qoff, dev), gh.to_dev(q.rec_id, dev), gh.to_dev(q.unc_here, dev),
+                      gh.to_dev(q.alt, dev), gh.to_dev(q.unc_alt, dev), gh.to_dev(q.base_work, dev),
+                      cap=cap)
+    status = 0
+    try:
+        eng.sync()
+    except Exception as e:  # DM_EFULL when cap is exceeded
+        status = e.status
+    r = o.rebalance(q.qoff, q.rec_id, q.unc_here, q.alt, q.unc_alt, q.base_work, cap=cap)
+    assert status == r["status"]
+    n = int(cpu(g["count"])[0])
+    assert n == r["count"]
+    m = min(n, len(r["rec"]))
+    for k in ("rec", "src", "dst", "benefit", "ttft_to"):
+        assert np.array_equal(cpu(g[k])[:m], r[k][:m]), k
+    assert np.array_equal(cpu(g["loads"]), r["loads"])
+    return r
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_rebalance_synthetic_parity(seed):
+    gh = _h()
+    S, n_live = 16, 12
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=S, index_log2_slots=8,
+               slo_us=60_000 + 20_000 * seed)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    o = oracle.Oracle(cfg)
+    rng = np.random.default_rng(seed)
+    src = np.sort(rng.choice(n_live, size=1 + seed % 4, replace=False))
+    q = workloads.synthetic_queues(seed, S, n_live, src, 300 + 500 * seed, 400, 150_000, 0)
+    _say("rebalance synthetic", seed, "records", len(q.rec_id))
+    r = compare_rebalance(eng, o, q)
+    assert r["count"] > 0
+
+
+def test_rebalance_cap_and_empty():
+    gh = _h()
+    S = 8
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=S, index_log2_slots=8,
+               slo_us=50_000)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    o = oracle.Oracle(cfg)
+    q = workloads.synthetic_queues(3, S, S, np.array([1, 5]), 400, 300, 100_000, 0)
+    r = compare_rebalance(eng, o, q)
+    assert r["count"] > 2
+    compare_rebalance(eng, o, q, cap=2)
+    # no records at all
+    empty = workloads.Queues(np.zeros(S + 1, np.int64), np.zeros(0, np.uint64),
+                             np.zeros(0, np.uint32), np.zeros(0, np.uint32), np.zeros(0, np.uint32),
+                             np.arange(S, dtype=np.int64))
+    r = compare_rebalance(eng, o, empty)
+    assert r["count"] == 0
+
+
+def _queues_from_route(chosen, cand, match, off, B, S, base_work):
+    """Queues built from a routed batch: each request queued on its chosen
+    instance in arrival order; alternative = the other candidate."""
+    n = len(chosen)
+    c1, c2 = cand[:n], cand[n:]
+    lens = np.diff(off)
+    unc1, unc2 = lens - B * match[:n].astype(np.int64), lens - B * match[n:].astype(np.int64)
+    here_is1 = chosen == c1
+    alt = np.where(here_is1, c2, c1).astype(np.uint32)
+    uh = np.where(here_is1, unc1, unc2).astype(np.uint32)
+    ua = np.where(here_is1, unc2, unc1).astype(np.uint32)
+    order = np.argsort(chosen, kind="stable")
+    qoff = np.zeros(S + 1, np.int64)
+    qoff[1:] = np.cumsum(np.bincount(chosen, minlength=S))
+    return workloads.Queues(qoff, order.astype(np.uint64) + 1000, uh[order], alt[order], ua[order],
+                            base_work.astype(np.int64))
+
+
+def test_tiny_rebalance_parity():
+    """Tiny-rebalance: queues formed by a Tiny-tight batch (each side from
+    its own routing), then one migration pass."""
+    wl = workloads.tiny(slo_us=20_000)
+    eng, o, g, r, tok, off = run_pair(wl, block_keys=False)
+    L0 = workloads.initial_loads(wl, 8)
+    qg = _queues_from_route(cpu(g["chosen"]), cpu(g["cand"]), cpu(g["match"]), off, 16, 8, L0)
+    qo = _queues_from_route(r["chosen"], r["cand"], r["match"], off, 16, 8, L0)
+    gh = _h()
+    dev = eng.device
+    gg = eng.rebalance(gh.to_dev(qg.qoff, dev), gh.to_dev(qg.rec_id, dev),
+                       gh.to_dev(qg.unc_here, dev), gh.to_dev(qg.alt, dev),
+                       gh.to_dev(qg.unc_alt, dev), gh.to_dev(qg.base_work, dev))
+    eng.sync()
+    rr = o.rebalance(qo.qoff, qo.rec_id, qo.unc_here, qo.alt, qo.unc_alt, qo.base_work)
+    n = int(cpu(gg["count"])[0])
+    assert n == rr["count"] and n > 0
+    for k in ("rec", "src", "dst", "benefit", "ttft_to"):
+        assert np.array_equal(cpu(gg[k])[:n], rr[k]), k
+    assert np.array_equal(cpu(gg["loads"]), rr["loads"])
+
+
+# ---------------------------------------------------------------------------
+# Scaling
+# ---------------------------------------------------------------------------
+
+def test_scale_parity_then_reroute():
+    wl = workloads.tiny()
+    eng, o, g, r, tok, off = run_pair(wl, block_keys=False)
+    gh = _h()
+    keys = r["key"]
+    add, rm = [9, 10], [2, 6]
+    cfg = dict(wl.route.as_dict(), max_slots=12)
+    # fresh engines with room for the added ids
+    eng = gh.DualMap(cfg, device="cuda:0")
+    o = oracle.Oracle(cfg)
+    eng.build_rings(range(8))
+    o.build_rings(range(8))
+    gs = eng.scale(add, rm, gh.to_dev(keys, eng.device))
+    eng.sync()
+    rs = o.scale(add, rm, keys)
+    assert rs["status"] == 0 and rs["violations"] == 0
+    for k in ("old", "new", "moved"):
+        assert np.array_equal(cpu(gs[k]), rs[k]), k
+    assert int(cpu(gs["violations"])[0]) == 0
+    for s in (0, 1):
+        gp, gi = eng.ring(s)
+        op, oi = o.ring(s)
+        assert np.array_equal(gp, op) and np.array_equal(gi, oi)
+    # bad scale requests change nothing
+    import paper_2602_06502_amd as pk
+    for a_, r_ in (([1], []), ([], [2]), ([20], []), ([11, 11], [])):
+        with pytest.raises(pk.DMError):
+            eng.scale(a_, r_, gh.to_dev(keys, eng.device))
+    L0 = workloads.initial_loads(wl, 12)
+    Ld = gh.to_dev(L0, eng.device)
+    g2 = eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld)
+    eng.sync()
+    r2 = o.route(tok, off, L0)
+    compare_route(g2, r2, wl.n_req)
+    assert not set(np.unique(r2["cand"]).tolist()) & set(rm)
+
+
+def test_determinism_repeat():
+    wl = workloads.small_random(21, 6, 8, 16, 500, slo_us=5_000)
+    gh = _h()
+    eng = gh.engine_for(wl)
+    gh.prefill_from_prior(eng, wl)
+    tok, off = workloads.prompts(wl, wl.n_req)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    outs = []
+    for _ in range(2):
+        Ld = gh.to_dev(L0, eng.device)
+        outs.append({k: cpu(v) for k, v in eng.route(gh.to_dev(tok, eng.device),
+                                                     gh.to_dev(off, eng.device), Ld).items()})
+    for k in outs[0]:
+        assert np.array_equal(outs[0][k], outs[1][k])

@@ -19,11 +19,45 @@ one stream per component, so each component is reproducible on its own.
 """
 from __future__ import annotations
 
+import ctypes as C
 import dataclasses
 import math
+import os
+import subprocess
 from typing import Dict, Optional, Tuple
 
 import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_FG_SRC = os.path.join(_HERE, "_fastgen.c")
+_FG_LIB = os.path.join(_HERE, "libfastgen.so")
+_fg = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the token-fill helper (gcc, OpenMP)."""
+    if force or not os.path.exists(_FG_LIB) or os.path.getmtime(_FG_LIB) < os.path.getmtime(_FG_SRC):
+        tmp = _FG_LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O3", "-fopenmp", "-shared", "-fPIC", "-o", tmp, _FG_SRC])
+        os.replace(tmp, _FG_LIB)
+    return _FG_LIB
+
+
+def _fastgen():
+    global _fg
+    if _fg is None:
+        build(force=False)
+        L = C.CDLL(_FG_LIB)
+        L.fg_uniform_tokens.argtypes = [C.c_void_p, C.c_int64, C.c_uint32, C.c_uint64]
+        L.fg_uniform_tokens.restype = None
+        L.fg_copy_prefixes.argtypes = [C.c_void_p] * 6 + [C.c_int64]
+        L.fg_copy_prefixes.restype = None
+        _fg = L
+    return _fg
+
+
+def _vp(a: np.ndarray):
+    return a.ctypes.data_as(C.c_void_p)
 
 # Stream ids: one independent random stream per generated component.
 _S_TEMPLATE_LEN, _S_TEMPLATE_TOK, _S_REQ_LEN, _S_REQ_TPL, _S_REQ_TOK = 1, 2, 3, 4, 5
@@ -126,7 +160,12 @@ def zipf_ranks(rng: np.random.Generator, n_items: int, s: float, size: int) -> n
 
 
 def uniform_tokens(rng: np.random.Generator, vocab: int, size: int) -> np.ndarray:
-    return rng.integers(0, vocab, size=size, dtype=np.int32)
+    """size tokens uniform in [0, vocab), from chunked PCG32 streams seeded by
+    one draw of rng."""
+    out = np.empty(size, dtype=np.int32)
+    if size:
+        _fastgen().fg_uniform_tokens(_vp(out), size, vocab, int(rng.integers(0, 2**63)))
+    return out
 
 
 def templates(wl: Workload) -> Tuple[np.ndarray, np.ndarray]:
@@ -158,24 +197,13 @@ def prompts(wl: Workload, n: int, sub: int = 0, chunk: int = 1 << 16) -> Tuple[n
     off = np.zeros(n + 1, dtype=np.int64)
     np.cumsum(lens, out=off[1:])
     total = int(off[-1])
-    tok = np.empty(total, dtype=np.int32)
-    rng_tok = _rng(wl.seed, _S_REQ_TOK, sub)
-    # random tokens everywhere, in fixed-size pieces so memory stays bounded
-    piece = 1 << 26
-    for s in range(0, total, piece):
-        e = min(total, s + piece)
-        tok[s:e] = uniform_tokens(rng_tok, wl.vocab, e - s)
-    # overwrite each prompt's shared part with its template's prefix
-    shared = np.minimum(lens, tlen[tpl])
-    for r0 in range(0, n, chunk):
-        r1 = min(n, r0 + chunk)
-        sh = shared[r0:r1]
-        cnt = int(sh.sum())
-        if cnt == 0:
-            continue
-        rep = np.repeat(np.arange(r0, r1), sh)
-        within = np.arange(cnt, dtype=np.int64) - np.repeat(np.cumsum(sh) - sh, sh)
-        tok[off[rep] + within] = ttok[toff[tpl[rep]] + within]
+    # random tokens everywhere, then each prompt's shared part overwritten
+    # with its template's prefix
+    tok = uniform_tokens(_rng(wl.seed, _S_REQ_TOK, sub), wl.vocab, total)
+    shared = np.ascontiguousarray(np.minimum(lens, tlen[tpl]), dtype=np.int64)
+    _fastgen().fg_copy_prefixes(_vp(tok), _vp(off), _vp(np.ascontiguousarray(tpl)), _vp(shared),
+                                _vp(ttok), _vp(toff), n)
+    del chunk
     return tok, off
 
 

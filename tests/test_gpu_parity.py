@@ -229,7 +229,7 @@ def test_index_ops_and_capacity():
     dup = np.concatenate([keys, keys[:50]])
     eng.index_insert(0, gh.to_dev(dup, dev))
     eng.sync()
-    assert eng.index_size(0) == len(np.unique([oracle.canon(int(k)) for k in keys]))
+    assert eng.index_size(0) == len({oracle.canon(int(k)) for k in keys})
     eng.index_erase(0, gh.to_dev(keys[10:20], dev))
     eng.sync()
     left = {oracle.canon(int(k)) for k in keys} - {oracle.canon(int(k)) for k in keys[10:20]}
@@ -309,7 +309,9 @@ def test_rebalance_synthetic_parity(seed):
     o = oracle.Oracle(cfg)
     rng = np.random.default_rng(seed)
     src = np.sort(rng.choice(n_live, size=1 + seed % 4, replace=False))
-    q = workloads.synthetic_queues(seed, S, n_live, src, 300 + 500 * seed, 400, 150_000, 0)
+    # sources start 10 ms under the SLO so the tail of each queue is over it
+    q = workloads.synthetic_queues(seed, S, n_live, src, 300 + 500 * seed, 400, 150_000,
+                                   4 * (cfg["slo_us"] - 10_000))
     _say("rebalance synthetic", seed, "records", len(q.rec_id))
     r = compare_rebalance(eng, o, q)
     assert r["count"] > 0
@@ -322,7 +324,7 @@ def test_rebalance_cap_and_empty():
                slo_us=50_000)
     eng = gh.DualMap(cfg, device="cuda:0")
     o = oracle.Oracle(cfg)
-    q = workloads.synthetic_queues(3, S, S, np.array([1, 5]), 400, 300, 100_000, 0)
+    q = workloads.synthetic_queues(3, S, S, np.array([1, 5]), 400, 300, 100_000, 4 * 40_000)
     r = compare_rebalance(eng, o, q)
     assert r["count"] > 2
     compare_rebalance(eng, o, q, cap=2)
@@ -357,9 +359,17 @@ def test_tiny_rebalance_parity():
     its own routing), then one migration pass."""
     wl = workloads.tiny(slo_us=20_000)
     eng, o, g, r, tok, off = run_pair(wl, block_keys=False)
-    L0 = workloads.initial_loads(wl, 8)
-    qg = _queues_from_route(cpu(g["chosen"]), cpu(g["cand"]), cpu(g["match"]), off, 16, 8, L0)
-    qo = _queues_from_route(r["chosen"], r["cand"], r["match"], off, 16, 8, L0)
+
+    def base_work(chosen):
+        # the two instances holding the most queued tokens start 8 ms under the SLO
+        work = np.bincount(chosen, weights=np.diff(off), minlength=8)
+        bw = np.zeros(8, np.int64)
+        bw[np.argsort(-work, kind="stable")[:2]] = 4 * (20_000 - 8_000)
+        return bw
+
+    gch = cpu(g["chosen"])
+    qg = _queues_from_route(gch, cpu(g["cand"]), cpu(g["match"]), off, 16, 8, base_work(gch))
+    qo = _queues_from_route(r["chosen"], r["cand"], r["match"], off, 16, 8, base_work(r["chosen"]))
     gh = _h()
     dev = eng.device
     gg = eng.rebalance(gh.to_dev(qg.qoff, dev), gh.to_dev(qg.rec_id, dev),

@@ -198,8 +198,8 @@ dm_status dm_scale(dm_ctx* ctx, const uint32_t* add, uint32_t n_add, const uint3
 /* Instrumentation.  With on != 0, dm_route_batch records HIP events on the
  * context's stream around its stages; dm_route_stage_ms then waits for the
  * last batch and writes up to n stage times in milliseconds to ms_host:
- * [0] hashing, ring lookup and prefix match (one kernel), [1] in-order
- * selection, [2] block-key offsets (0 when block keys were not requested). */
+ * [0] chained block hashing (one kernel), [1] ring lookup and longest
+ * cached prefix, [2] in-order selection, [3] per-request block offsets. */
 dm_status dm_set_timing(dm_ctx* ctx, int on);
 dm_status dm_route_stage_ms(dm_ctx* ctx, float* ms_host, int n);
 

@@ -175,9 +175,9 @@ class DualMap:
         self._check(self.lib.dm_set_timing(self._h, 1 if on else 0), "dm_set_timing")
 
     def stage_ms(self):
-        """(hash+match ms, selection ms, block-offset ms) of the last batch."""
-        ms = (C.c_float * 3)()
-        self._check(self.lib.dm_route_stage_ms(self._h, ms, 3), "dm_route_stage_ms")
+        """(hash, lookup+match, selection, block offsets) ms of the last batch."""
+        ms = (C.c_float * 4)()
+        self._check(self.lib.dm_route_stage_ms(self._h, ms, 4), "dm_route_stage_ms")
         return tuple(float(x) for x in ms)
 
     def sync(self) -> None:

@@ -41,7 +41,7 @@ void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e)
     size_t nb = std::max(bytes, s.bytes * 2);
     nb = (nb + 4095) & ~size_t(4095);
     if (s.p)
-        hipFree(s.p);
+        (void)hipFree(s.p);
     s.p = nullptr;
     s.bytes = 0;
     *e = hipMalloc(&s.p, nb);
@@ -128,12 +128,14 @@ bool aligned(const T* p)
 hipError_t upload_live(dm_ctx* c)
 {
     const uint32_t S = c->cfg.max_slots;
-    std::vector<uint32_t> ids, nxt(S, 0);
+    std::vector<uint32_t> ids, nxt(S, 0), dense(S, 0);
     for (uint32_t i = 0; i < S; i++)
         if (c->live[i])
             ids.push_back(i);
-    for (size_t k = 0; k < ids.size(); k++)
+    for (size_t k = 0; k < ids.size(); k++) {
         nxt[ids[k]] = ids[(k + 1) % ids.size()];
+        dense[ids[k]] = (uint32_t)k;
+    }
     ids.resize(S, 0);
     hipError_t e = hipMemcpyAsync(c->d_live_ids, ids.data(), S * sizeof(uint32_t),
                                   hipMemcpyHostToDevice, c->stream);
@@ -141,15 +143,18 @@ hipError_t upload_live(dm_ctx* c)
         e = hipMemcpyAsync(c->d_next_live, nxt.data(), S * sizeof(uint32_t),
                            hipMemcpyHostToDevice, c->stream);
     if (e == hipSuccess)
+        e = hipMemcpyAsync(c->d_dense, dense.data(), S * sizeof(uint32_t), hipMemcpyHostToDevice,
+                           c->stream);
+    if (e == hipSuccess)
         e = hipStreamSynchronize(c->stream);  // host vectors go out of scope
     return e;
 }
 
 void free_ring(dm::Ring& r)
 {
-    hipFree(r.pos);
-    hipFree(r.id);
-    hipFree(r.dir);
+    (void)hipFree(r.pos);
+    (void)hipFree(r.id);
+    (void)hipFree(r.dir);
     r = dm::Ring{};
 }
 
@@ -181,6 +186,7 @@ dm_status dm_create(const dm_config* cfg, void* hip_stream, dm_ctx** out)
     if (e == hipSuccess) e = hipMalloc(&c->d_hp, sizeof(HashParams));
     if (e == hipSuccess) e = hipMalloc(&c->d_next_live, S * sizeof(uint32_t));
     if (e == hipSuccess) e = hipMalloc(&c->d_live_ids, S * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMalloc(&c->d_dense, S * sizeof(uint32_t));
     if (e == hipSuccess) e = hipMalloc(&c->d_flag_add, S);
     if (e == hipSuccess) e = hipMalloc(&c->d_flag_rm, S);
     if (e == hipSuccess) e = hipMalloc(&c->d_tables, table_slots * sizeof(uint64_t));
@@ -209,23 +215,24 @@ void dm_destroy(dm_ctx* c)
     if (!c)
         return;
     DeviceGuard g(c->device);
-    hipStreamSynchronize(c->stream);
+    (void)hipStreamSynchronize(c->stream);
     for (auto& b : c->ring)
         for (auto& r : b)
             free_ring(r);
     for (auto& s : c->scratch)
-        hipFree(s.p);
+        (void)hipFree(s.p);
     for (auto& ev : c->ev)
         if (ev)
-            hipEventDestroy(ev);
-    hipFree(c->d_hp);
-    hipFree(c->d_next_live);
-    hipFree(c->d_live_ids);
-    hipFree(c->d_flag_add);
-    hipFree(c->d_flag_rm);
-    hipFree(c->d_tables);
-    hipFree(c->d_counts);
-    hipFree(c->d_status);
+            (void)hipEventDestroy(ev);
+    (void)hipFree(c->d_hp);
+    (void)hipFree(c->d_next_live);
+    (void)hipFree(c->d_live_ids);
+    (void)hipFree(c->d_dense);
+    (void)hipFree(c->d_flag_add);
+    (void)hipFree(c->d_flag_rm);
+    (void)hipFree(c->d_tables);
+    (void)hipFree(c->d_counts);
+    (void)hipFree(c->d_status);
     delete c;
 }
 
@@ -432,7 +439,7 @@ dm_status dm_scale(dm_ctx* c, const uint32_t* add, uint32_t n_add, const uint32_
     if (e != hipSuccess) {
         c->live = old_live;
         c->n_live = old_n;
-        upload_live(c);
+        (void)upload_live(c);
         return hip_fail(c, e, "dm_scale");
     }
     c->cur = nb;
@@ -464,14 +471,15 @@ dm_status dm_route_stage_ms(dm_ctx* c, float* ms, int n)
     if (!c->timing || !c->ev[0])
         return fail(c, DM_ESTATE, "dm_route_stage_ms: timing is off");
     DeviceGuard g(c->device);
-    hipError_t e = hipEventSynchronize(c->ev[3]);
-    float t[3] = {0, 0, 0};
+    hipError_t e = hipEventSynchronize(c->ev[4]);
+    float t[4] = {0, 0, 0, 0};
     if (e == hipSuccess) e = hipEventElapsedTime(&t[0], c->ev[1], c->ev[2]);
     if (e == hipSuccess) e = hipEventElapsedTime(&t[1], c->ev[2], c->ev[3]);
-    if (e == hipSuccess && c->timed_bk) e = hipEventElapsedTime(&t[2], c->ev[0], c->ev[1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t[2], c->ev[3], c->ev[4]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t[3], c->ev[0], c->ev[1]);
     if (e != hipSuccess)
         return hip_fail(c, e, "dm_route_stage_ms");
-    for (int k = 0; k < n && k < 3; k++)
+    for (int k = 0; k < n && k < 4; k++)
         ms[k] = t[k];
     return DM_OK;
 }

@@ -75,6 +75,7 @@ struct dm_ctx {
     uint32_t n_live = 0;
     uint32_t* d_next_live = nullptr;  // [max_slots]
     uint32_t* d_live_ids = nullptr;   // [max_slots] ascending live ids
+    uint32_t* d_dense = nullptr;      // [max_slots] live id -> its index in d_live_ids
     uint8_t* d_flag_add = nullptr;    // [max_slots] scale: added this call
     uint8_t* d_flag_rm = nullptr;     // [max_slots] scale: removed this call
 
@@ -93,8 +94,7 @@ struct dm_ctx {
 
     // stage timing of dm_route_batch (events recorded only when enabled)
     bool timing = false;
-    bool timed_bk = false;         // last timed batch emitted block keys
-    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    hipEvent_t ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
 };
 
 namespace dm {

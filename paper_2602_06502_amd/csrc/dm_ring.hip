@@ -93,8 +93,8 @@ hipError_t ring_build(dm_ctx* c, Ring& r, int s, const uint32_t* d_live_ids, uin
     hipError_t e = hipSuccess;
     if (r.cap < len) {
         e = hipStreamSynchronize(c->stream);
-        hipFree(r.pos);
-        hipFree(r.id);
+        (void)hipFree(r.pos);
+        (void)hipFree(r.id);
         r.pos = nullptr;
         r.id = nullptr;
         r.cap = 0;
@@ -107,7 +107,7 @@ hipError_t ring_build(dm_ctx* c, Ring& r, int s, const uint32_t* d_live_ids, uin
     const uint32_t dneed = (1u << dbits) + 1;
     if (r.dcap < dneed) {
         e = hipStreamSynchronize(c->stream);
-        hipFree(r.dir);
+        (void)hipFree(r.dir);
         r.dir = nullptr;
         r.dcap = 0;
         if (e == hipSuccess) e = hipMalloc(&r.dir, dneed * sizeof(uint32_t));

@@ -1,0 +1,193 @@
+"""Full-size GPU checks on the large (1,048,576-request) and elastic workloads.
+
+- Sampled parity: 2,048 random requests of the large batch are routed by the
+  oracle over its own copy of the index (ring keys, candidates, match lengths
+  and the adjustment flag compared exactly).
+- Selection replay property: from the engine's per-request candidates and
+  match lengths, the loads every request saw are recomputed by per-instance
+  prefix sums of the chosen uncached tokens; every decision, TTFT, flag and
+  the final loads must follow the rule of Sec. 3.2 exactly.  Since each
+  decision is then the rule applied to the loads left by all earlier
+  decisions, the whole sequence equals the request-order result.
+- Elastic scaling: dm_scale (add 16, remove 8 of 128 instances) against the
+  oracle on 2 x 1,048,576 seeded random ring keys (rings, owners, moved
+  counts, zero violations), and the zero-violation and moved-fraction
+  properties on the batch's own ring keys.
+- Rebalance at full size: 8 sources x 32,768 queued records against the
+  oracle, element by element.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import oracle.harness as oh
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def large():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2602_06502_amd.harness as gh
+    oracle.build(force=False)
+    wl = workloads.large()
+    _say("setup large on GPU")
+    g = gh.setup(wl, device="cuda:0")
+    eng = g["eng"]
+    loads = gh.to_dev(g["loads0"], eng.device)
+    _say("route large", wl.n_req)
+    out = eng.route(g["tokens"], g["offsets"], loads)
+    eng.sync()
+    res = {k: v.cpu().numpy() for k, v in out.items()}
+    res["loads"] = loads.cpu().numpy()
+    return dict(wl=wl, gh=gh, eng=eng, g=g, out=res)
+
+
+def replay_check(wl, offsets, L0, out):
+    """Verify every decision against the rule given the loads implied by the
+    earlier decisions (see module docstring)."""
+    rc = wl.route
+    n = len(offsets) - 1
+    c1, c2 = out["cand"][:n].astype(np.int64), out["cand"][n:].astype(np.int64)
+    m1, m2 = out["match"][:n].astype(np.int64), out["match"][n:].astype(np.int64)
+    ln = np.diff(offsets).astype(np.int64)
+    u1, u2 = ln - rc.block * m1, ln - rc.block * m2
+    ch = out["chosen"].astype(np.int64)
+    assert np.all((ch == c1) | (ch == c2))
+    pick1 = ch == c1
+    uch = np.where(pick1, u1, u2)
+    S = rc.max_slots
+    L1 = np.zeros(n, np.int64)
+    L2 = np.zeros(n, np.int64)
+    order = np.argsort(ch, kind="stable")
+    cnt = np.bincount(ch, minlength=S)
+    starts = np.concatenate([[0], np.cumsum(cnt)])
+    idx = np.arange(n)
+    for x in np.unique(np.concatenate([c1, c2])):
+        rs = order[starts[x]:starts[x + 1]]            # requests that chose x, in order
+        pref = np.concatenate([[0], np.cumsum(uch[rs])])
+        for Lout, cx in ((L1, c1), (L2, c2)):
+            q = idx[cx == x]
+            Lout[q] = L0[x] + pref[np.searchsorted(rs, q, side="left")]
+    T1 = rc.ttft_base_us + rc.ttft_per_token_us * u1 + L1 // rc.queue_div
+    T2 = rc.ttft_base_us + rc.ttft_per_token_us * u2 + L2 // rc.queue_div
+    slo = rc.slo_us
+    eq, aff1 = m1 == m2, m1 > m2
+    rule1 = np.where(eq, L1 <= L2,
+                     np.where(aff1, (T1 <= slo) | ~(L2 < L1), ~((T2 <= slo) | ~(L1 < L2))))
+    bad = np.nonzero(rule1 != pick1)[0]
+    assert len(bad) == 0, f"{len(bad)} decisions off the rule, first {bad[:5]}"
+    assert np.array_equal(out["ttft"], np.where(pick1, T1, T2))
+    f = out["flags"].astype(np.int64)
+    assert np.array_equal((f >> 1) & 1, ((T1 > slo) & (T2 > slo)).astype(np.int64))
+    assert np.array_equal((f >> 2) & 1, eq.astype(np.int64))
+    assert np.array_equal(f & 1, (~eq & (pick1 != aff1)).astype(np.int64))
+    final = L0.copy()
+    np.add.at(final, ch, uch)
+    assert np.array_equal(final, out["loads"])
+
+
+def test_large_sampled_parity_and_replay(large):
+    wl, g, out = large["wl"], large["g"], large["out"]
+    n = wl.n_req
+    # every decision follows the rule given the earlier ones
+    _say("replay property over", n)
+    replay_check(wl, g["offsets_np"], g["loads0"], out)
+    # oracle on a sample of requests, same index built by the oracle itself
+    _say("oracle setup (large index)")
+    o = oh.setup(wl, with_batch=False)["oracle"]
+    rng = np.random.default_rng(7)
+    sample = np.sort(rng.choice(n, size=2048, replace=False))
+    tok, off = g["tokens_np"], g["offsets_np"]
+    parts = [tok[off[r]:off[r + 1]] for r in sample]
+    soff = np.zeros(len(sample) + 1, np.int64)
+    soff[1:] = np.cumsum([len(p) for p in parts])
+    r = o.route(np.concatenate(parts), soff, np.zeros(wl.route.max_slots, np.int64))
+    k = len(sample)
+    for name in ("key", "cand", "match"):
+        got = np.concatenate([out[name][:n][sample], out[name][n:][sample]])
+        assert np.array_equal(got, r[name]), name
+    assert np.array_equal(out["flags"][sample] & 8, r["flags"] & 8)
+    # the workload exercises both SLO branches and both match cases
+    f = out["flags"]
+    assert (f & 1).any() and (f & 2).any() and (f & 4).any() and (~f & 4).any()
+    assert k == 2048
+
+
+def test_elastic_scale_full(large):
+    wl, gh, eng, out = large["wl"], large["gh"], large["eng"], large["out"]
+    n = wl.n_req
+    add, rm = workloads.scale_sets(wl, 16, 8)
+    # parity on seeded random ring keys (same distribution as mixed ring keys)
+    keys = np.random.default_rng(5).integers(0, 2**64, size=2 * n, dtype=np.uint64)
+    o = oh.oracle_for(wl)
+    _say("scale on GPU: add", len(add), "remove", rm.tolist())
+    gs = eng.scale(add.tolist(), rm.tolist(), gh.to_dev(keys, eng.device))
+    eng.sync()
+    rs = o.scale(add, rm, keys)
+    assert rs["status"] == 0 and rs["violations"] == 0
+    for name in ("old", "new", "moved"):
+        assert np.array_equal(gs[name].cpu().numpy(), rs[name]), name
+    assert int(gs["violations"].cpu().numpy()[0]) == 0
+    for s in (0, 1):
+        gp, gi = eng.ring(s)
+        op, oi = o.ring(s)
+        assert np.array_equal(gp, op) and np.array_equal(gi, oi)
+    expect = len(rm) / 128 + len(add) / 136 - (len(rm) / 128) * (len(add) / 136)
+    for s in (0, 1):
+        assert abs(rs["moved"][s] / n - expect) < 0.03
+    # properties on the batch's own ring keys: scale back, then forward again
+    back = eng.scale(rm.tolist(), add.tolist(), gh.to_dev(out["key"], eng.device))
+    eng.sync()
+    fwd = eng.scale(add.tolist(), rm.tolist(), gh.to_dev(out["key"], eng.device))
+    eng.sync()
+    assert int(back["violations"].cpu()[0]) == 0 and int(fwd["violations"].cpu()[0]) == 0
+    old, new = fwd["old"].cpu().numpy(), fwd["new"].cpu().numpy()
+    # on the restored rings every ring key maps back to the batch's candidates
+    assert np.array_equal(old[:n], out["cand"][:n])
+    unadjusted = (out["flags"] & 8) == 0
+    assert np.array_equal(old[n:][unadjusted], out["cand"][n:][unadjusted])
+    # requests sharing a prefix share ring keys: the moved share is a
+    # property of distinct keys
+    for s in (0, 1):
+        k = out["key"][s * n:(s + 1) * n]
+        _, first = np.unique(k, return_index=True)
+        mv = old[s * n:(s + 1) * n][first] != new[s * n:(s + 1) * n][first]
+        assert len(first) > 2000 and abs(mv.mean() - expect) < 0.05, (len(first), mv.mean())
+
+
+def test_rebalance_full_size():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2602_06502_amd.harness as gh
+    wl = workloads.large()
+    S, n_live = wl.route.max_slots, 136
+    eng = gh.DualMap(wl.route.as_dict(), device="cuda:0")
+    o = oracle.Oracle(wl.route.as_dict())
+    sources = np.sort(np.random.default_rng(3).choice(n_live, size=8, replace=False))
+    q = workloads.synthetic_queues(105, S, n_live, sources, 32_768, 2_000, 50_000,
+                                   4 * (wl.route.slo_us - 50_000))
+    _say("rebalance full size: records", len(q.rec_id))
+    dev = eng.device
+    g = eng.rebalance(gh.to_dev(q.qoff, dev), gh.to_dev(q.rec_id, dev), gh.to_dev(q.unc_here, dev),
+                      gh.to_dev(q.alt, dev), gh.to_dev(q.unc_alt, dev), gh.to_dev(q.base_work, dev))
+    eng.sync()
+    r = o.rebalance(q.qoff, q.rec_id, q.unc_here, q.alt, q.unc_alt, q.base_work)
+    cnt = int(g["count"].cpu().numpy()[0])
+    assert r["status"] == 0 and cnt == r["count"]
+    assert cnt > 0.1 * len(q.rec_id)  # at least 10% of queued records migrate
+    for name in ("rec", "src", "dst", "benefit", "ttft_to"):
+        assert np.array_equal(g[name].cpu().numpy()[:cnt], r[name]), name
+    assert np.array_equal(g["loads"].cpu().numpy(), r["loads"])

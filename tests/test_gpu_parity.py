@@ -112,6 +112,42 @@ def test_random_small_parity(seed, n_inst, vnodes, block):
     run_pair(wl)
 
 
+def _pair_with_loads(wl, L0):
+    gh = _h()
+    eng = gh.engine_for(wl)
+    o = oh.oracle_for(wl)
+    gh.prefill_from_prior(eng, wl)
+    oh.prefill_from_prior(o, wl)
+    tok, off = workloads.prompts(wl, wl.n_req, sub=0)
+    Ld = gh.to_dev(L0, eng.device)
+    g = eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld, block_keys=True)
+    eng.sync()
+    r = o.route(tok, off, L0, block_keys=True)
+    compare_route(g, r, wl.n_req, with_bk=True)
+    assert np.array_equal(cpu(Ld), r["loads"])
+    return r
+
+
+@pytest.mark.parametrize("n_inst", [8, 150, 200])
+def test_selection_wide_loads_parity(n_inst):
+    """Loads spread beyond 2^30 force the exact 64-bit serial selection."""
+    wl = workloads.small_random(31, n_inst, 3, 16, 700, slo_us=6_000_000_000)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    L0[::3] += 1 << 40
+    L0[1] = (1 << 62) - (1 << 50)
+    _say("wide loads", n_inst)
+    r = _pair_with_loads(wl, L0)
+    assert (r["flags"] & 1).sum() + (r["flags"] & 4).sum() > 0
+
+
+def test_selection_many_instances_parity():
+    """More live instances than the register banks hold (LDS selection)."""
+    wl = workloads.small_random(32, 300, 2, 16, 900, slo_us=30_000)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    _say("300 instances")
+    _pair_with_loads(wl, L0)
+
+
 def test_sparse_live_ids_parity():
     # ids 0..n-1 not all live: fixup must take the next live id
     wl = workloads.small_random(11, 6, 3, 16, 400)

@@ -102,6 +102,9 @@ def main():
     ap.add_argument("--n-req", type=int, default=1_048_576)
     ap.add_argument("--cpu-sample", type=int, default=100_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="after timing, copy 1 GiB device to device once (a plain copy kernel "
+                         "of known size, to scale hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the routing path is built and measured on a "
@@ -188,6 +191,13 @@ def main():
                               np.where(out["chosen"].cpu().numpy() == cand[:n], match[:n],
                                        match[n:]).sum() / max(1, ntok // wl.route.block))},
     }
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.int32, device=eng.device)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        res["calibration_copy_bytes"] = {"read": src.numel() * 4, "write": dst.numel() * 4}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_sample, n))
     print(json.dumps(res), flush=True)

@@ -206,10 +206,12 @@ struct ProbeArgs {
 };
 
 // Longest cached prefix of every (request, candidate) task, first miss exact.
-// Wave w owns the tasks of requests [first[w], first[w+1]); an idle lane takes
-// the wave's next task (a wave-local counter advanced with a ballot), so
-// short and long tasks pack the lanes.  Each probe reads one 64-byte bucket
-// while the next block key is already being fetched.
+// Wave w owns the tasks of requests [first[w], first[w+1]); every lane keeps
+// a current task and a prefetched next one taken from the wave's task
+// counter (advanced with a ballot), so a finished lane switches to work
+// whose block range, table and first key are already loaded while the
+// wave keeps probing.  Each probe reads one 64-byte bucket while the next
+// block key is already being fetched.
 __global__ __launch_bounds__(kRouteThreads) void probe_kernel(ProbeArgs a)
 {
     const int lane = lane_id();
@@ -219,33 +221,53 @@ __global__ __launch_bounds__(kRouteThreads) void probe_kernel(ProbeArgs a)
     const uint64_t T = re > rb ? 2 * (re - rb) : 0;
     const uint64_t nbk = 1ull << (a.log2slots - 3);
     uint64_t next = 0;  // wave-uniform: next unassigned task of this wave
+    // current task
     bool have = false;
     uint64_t kb = 0, ke = 0, k0 = 0, key = 0, nkey = 0, bkt = 0, steps = 0, out = 0;
     const uint64_t* tab = a.tables;
+    // prefetched task: stage 0 none, 1 range/table loaded, 2 first key loaded
+    int pst = 0;
+    uint64_t pk0 = 0, pke = 0, pout = 0, pkey = 0;
+    const uint64_t* ptab = a.tables;
     for (;;) {
-        const uint64_t idle = ballot(!have);
-        if (idle && next < T) {
-            const uint64_t t = next + __popcll(idle & lt_mask);
-            next += __popcll(idle);
-            if (!have && t < T) {
-                const uint64_t r = rb + (t >> 1);
-                out = (t & 1) * a.n + r;
-                k0 = a.bstart[r];
-                ke = a.bstart[r + 1];
-                if (ke == k0) {
-                    a.match[out] = 0;  // no full block
-                } else {
-                    kb = k0;
-                    tab = a.tables + ((uint64_t)a.cand[out] << a.log2slots);
-                    key = canon_key(a.hkeys[kb]);
-                    bkt = home_bucket(key, a.log2slots);
-                    steps = 0;
-                    have = true;
-                }
+        // advance the prefetched task one stage (its loads land during the probe below)
+        if (pst == 1) {
+            if (pke == pk0) {
+                a.match[pout] = 0;  // no full block: done without probing
+                pst = 0;
+            } else {
+                pkey = a.hkeys[pk0];
+                pst = 2;
             }
         }
+        const uint64_t need = ballot(pst == 0);
+        if (need && next < T) {
+            const uint64_t t = next + __popcll(need & lt_mask);
+            next += __popcll(need);
+            if (pst == 0 && t < T) {
+                const uint64_t r = rb + (t >> 1);
+                pout = (t & 1) * a.n + r;
+                pk0 = a.bstart[r];
+                pke = a.bstart[r + 1];
+                ptab = a.tables + ((uint64_t)a.cand[pout] << a.log2slots);
+                pst = 1;
+            }
+        }
+        // an idle lane takes its prefetched task
+        if (!have && pst == 2) {
+            k0 = pk0;
+            kb = pk0;
+            ke = pke;
+            out = pout;
+            tab = ptab;
+            key = canon_key(pkey);
+            bkt = home_bucket(key, a.log2slots);
+            steps = 0;
+            have = true;
+            pst = 0;
+        }
         if (!__any(have)) {
-            if (next >= T)
+            if (next >= T && !__any(pst != 0))
                 break;
             continue;
         }

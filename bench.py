@@ -32,7 +32,7 @@ def log(*a):
 
 def route_source_hash():
     h = hashlib.sha256()
-    for f in ("dm_route.hip", "dm_internal.h"):
+    for f in ("dm_hash.hip", "dm_internal.h"):
         with open(os.path.join(ROOT, "paper_2602_06502_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -102,12 +102,6 @@ TableRef table_of(dm_ctx* c, uint32_t id)
                     c->d_counts + c->cfg.max_slots + id, k, 1ull << (k - 1)};
 }
 
-uint32_t grid_for(uint64_t n, int threads, uint32_t cap = 65536)
-{
-    uint64_t g = (n + threads - 1) / threads;
-    if (g < 1) g = 1;
-    return (uint32_t)(g > cap ? cap : g);
-}
 
 }  // namespace
 

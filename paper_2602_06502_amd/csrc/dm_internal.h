@@ -108,6 +108,14 @@ void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e);
 
 inline RingView view(const Ring& r) { return RingView{r.pos, r.id, r.dir, r.len, r.dbits}; }
 
+// Grid of a grid-stride loop over n items, at least one block, at most cap.
+inline uint32_t grid_for(uint64_t n, int threads, uint32_t cap = 65536)
+{
+    uint64_t g = (n + threads - 1) / threads;
+    if (g < 1) g = 1;
+    return (uint32_t)(g > cap ? cap : g);
+}
+
 // ---------------------------------------------------------------------------
 // Launchers (one per kernel family), all asynchronous on c->stream.
 // ---------------------------------------------------------------------------
@@ -134,7 +142,22 @@ hipError_t index_insert(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n
 hipError_t index_erase(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n);
 hipError_t index_clear(dm_ctx* c, uint32_t id);
 
-// dm_route.hip
+// dm_hash.hip: block keys of every full block (hkeys at bstart[r]) and the
+// two ring keys of every request (key_out[r], key_out[n + r]).
+hipError_t hash_blocks(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                       const uint64_t* bstart, uint64_t* hkeys, uint64_t* key_out);
+
+// dm_probe.hip: candidates on the current rings (cand, fix-up flag bit 3)
+// and the longest cached prefix on each (match).
+hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64_t* hkeys,
+                        const uint64_t* bstart, uint32_t* cand, uint32_t* match, uint8_t* flags);
+
+// dm_select.hip: SLO-aware choice in request order; chosen, ttft_us and
+// flags bits 0-2 written, loads updated.
+hipError_t select_batch(dm_ctx* c, const int64_t* offsets, uint64_t n, const dm_route_out* out,
+                        int64_t* loads);
+
+// dm_route.hip: the whole batch, stage by stage.
 hipError_t route(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
                  int64_t* loads, const dm_route_out* out);
 

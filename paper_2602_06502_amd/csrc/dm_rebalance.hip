@@ -406,12 +406,6 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
     }
 }
 
-uint32_t grid_for(uint64_t n, int threads, uint32_t cap = 65536)
-{
-    uint64_t g = (n + threads - 1) / threads;
-    if (g < 1) g = 1;
-    return (uint32_t)(g > cap ? cap : g);
-}
 
 template <typename T>
 T* carve(uint8_t*& p, uint64_t n)

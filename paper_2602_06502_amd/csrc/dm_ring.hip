@@ -75,12 +75,6 @@ __global__ void remap_kernel(RingView o1, RingView o2, RingView n1, RingView n2,
     }
 }
 
-uint32_t grid_for(uint64_t n, int threads, uint32_t cap = 65536)
-{
-    uint64_t g = (n + threads - 1) / threads;
-    if (g < 1) g = 1;
-    return (uint32_t)(g > cap ? cap : g);
-}
 
 }  // namespace
 

@@ -1,0 +1,515 @@
+// SLO-aware candidate selection in request order (Sec. 3.2).
+//
+// Every request takes its cache-affine candidate unless that candidate's
+// TTFT misses the SLO and the other one is less loaded (equal matches: the
+// less loaded, first candidate on ties); the chosen instance's load grows by
+// the request's uncached tokens before the next request is decided.  The
+// batch result is therefore defined by processing the requests one by one.
+//
+// Fast path (every live load within 2^30 of the batch's smallest one, at
+// most 256 live instances; checked on the device):
+//   sel_prep_kernel   one thread per request packs a 16-byte record: the
+//                     affine candidate a and the other o (dense indices),
+//                     their uncached tokens, and th such that the rule reads
+//                     "take a iff L_a <= max(th, L_o)" on 32-bit loads
+//                     relative to that base;
+//   sel_level_kernel  one wave per 64-request window: the depth of every
+//                     request in the window's dependency graph (an edge
+//                     from each earlier request sharing a candidate);
+//   select_fast_kernel one wave walks the windows in order and, inside a
+//                     window, the depths in order: requests of one depth
+//                     share no instance, so they run together on loads kept
+//                     in LDS, and each sees exactly the loads that the
+//                     request-order walk would show it;
+//   sel_out_kernel    chosen instance, TTFT and flags of every request from
+//                     its recorded pre-update loads, in parallel.
+// Slow path: the same rule, one request at a time, on 64-bit loads in
+// registers (at most 256 slots) or in LDS.
+#include <algorithm>
+
+#include "dm_internal.h"
+
+namespace dm {
+namespace {
+
+constexpr int kSelSlot = 3;  // selection work arrays
+
+// Shared by both selection kernels: the SLO-aware rule given the two
+// candidates' pre-update loads.  kind bit0 = equal match, bit1 = c1 is the
+// cache-affine candidate; th = the affine candidate's load below which its
+// TTFT meets the SLO.
+__device__ __forceinline__ bool pick_first(uint32_t kind, int64_t L1, int64_t L2, int64_t th)
+{
+    if (kind & 1)
+        return L1 <= L2;
+    if (kind & 2)
+        return L1 < th || !(L2 < L1);
+    return !(L2 < th || !(L1 < L2));
+}
+
+// Per-lane request record for the serial loop and the output epilogue.
+struct SelRec {
+    uint32_t c1, c2, kind;
+    int64_t u1, u2, th;
+};
+
+__device__ __forceinline__ SelRec load_rec(const int64_t* offsets, uint64_t n, uint64_t r, bool ok,
+                                           uint32_t bshift, const uint32_t* cand,
+                                           const uint32_t* match, int64_t base, int64_t per,
+                                           uint32_t qshift, int64_t slo)
+{
+    SelRec s;
+    s.c1 = ok ? cand[r] : 0;
+    s.c2 = ok ? cand[n + r] : 0;
+    const uint32_t m1 = ok ? match[r] : 0, m2 = ok ? match[n + r] : 0;
+    const int64_t len = ok ? offsets[r + 1] - offsets[r] : 0;
+    s.u1 = len - ((int64_t)m1 << bshift);
+    s.u2 = len - ((int64_t)m2 << bshift);
+    const bool eq = m1 == m2, aff1 = m1 > m2;
+    // T_a <= slo  <=>  floor(L_a / 2^q) <= slo - base - per*u_a  <=>  L_a < th
+    s.th = (slo - base - per * (aff1 ? s.u1 : s.u2) + 1) * ((int64_t)1 << qshift);
+    s.kind = (eq ? 1u : 0u) | (aff1 ? 2u : 0u);
+    return s;
+}
+
+__device__ __forceinline__ void store_out(const SelRec& s, uint64_t r, int64_t L1, int64_t L2,
+                                          uint8_t* flags, uint32_t* chosen, int64_t* ttft,
+                                          int64_t base, int64_t per, uint32_t qshift, int64_t slo)
+{
+    const bool pick1 = pick_first(s.kind, L1, L2, s.th);
+    const int64_t t1 = base + per * s.u1 + (L1 >> qshift);
+    const int64_t t2 = base + per * s.u2 + (L2 >> qshift);
+    uint32_t f = flags[r];
+    if (t1 > slo && t2 > slo)
+        f |= 2;
+    if (s.kind & 1)
+        f |= 4;
+    else if (pick1 != ((s.kind & 2) != 0))
+        f |= 1;
+    chosen[r] = pick1 ? s.c1 : s.c2;
+    ttft[r] = pick1 ? t1 : t2;
+    flags[r] = (uint8_t)f;
+}
+
+// Serial SLO-aware selection, loads in R register banks of one wave.
+template <int R>
+__global__ __launch_bounds__(kWave) void select_kernel(
+    const int64_t* __restrict__ offsets, uint64_t n, uint32_t bshift,
+    const uint32_t* __restrict__ cand, const uint32_t* __restrict__ match,
+    uint8_t* __restrict__ flags, uint32_t* __restrict__ chosen, int64_t* __restrict__ ttft,
+    int64_t* __restrict__ loads, uint32_t S, int64_t base, int64_t per, uint32_t qshift, int64_t slo,
+    const uint32_t* __restrict__ plan)
+{
+    if (!plan[0])
+        return;
+    const int lane = lane_id();
+    uint32_t Llo[R], Lhi[R];
+#pragma unroll
+    for (int k = 0; k < R; k++) {
+        const uint32_t i = 64 * k + lane;
+        const int64_t v = i < S ? loads[i] : 0;
+        Llo[k] = (uint32_t)v;
+        Lhi[k] = (uint32_t)((uint64_t)v >> 32);
+    }
+    auto get = [&](uint32_t c) -> int64_t {
+        const uint32_t bank = c >> 6, l = c & 63;
+        uint32_t lo = __builtin_amdgcn_readlane(Llo[0], l), hi = __builtin_amdgcn_readlane(Lhi[0], l);
+#pragma unroll
+        for (int k = 1; k < R; k++) {
+            const uint32_t lo_k = __builtin_amdgcn_readlane(Llo[k], l);
+            const uint32_t hi_k = __builtin_amdgcn_readlane(Lhi[k], l);
+            lo = bank == (uint32_t)k ? lo_k : lo;
+            hi = bank == (uint32_t)k ? hi_k : hi;
+        }
+        return (int64_t)(((uint64_t)hi << 32) | lo);
+    };
+    for (uint64_t r0 = 0; r0 < n; r0 += kWave) {
+        const uint64_t r = r0 + lane;
+        const bool ok = r < n;
+        const SelRec s = load_rec(offsets, n, r, ok, bshift, cand, match, base, per, qshift, slo);
+        int64_t myL1 = 0, myL2 = 0;
+        const int cnt = (int)(n - r0 < (uint64_t)kWave ? n - r0 : kWave);
+        for (int j = 0; j < cnt; j++) {
+            const uint32_t C1 = __builtin_amdgcn_readlane(s.c1, j);
+            const uint32_t C2 = __builtin_amdgcn_readlane(s.c2, j);
+            const uint32_t K = __builtin_amdgcn_readlane(s.kind, j);
+            const int64_t TH = (int64_t)readlane_u64((uint64_t)s.th, j);
+            const int64_t U1 = (int64_t)readlane_u64((uint64_t)s.u1, j);
+            const int64_t U2 = (int64_t)readlane_u64((uint64_t)s.u2, j);
+            const int64_t L1 = get(C1), L2 = get(C2);
+            const bool pick1 = pick_first(K, L1, L2, TH);
+            const uint32_t ch = pick1 ? C1 : C2;
+            const int64_t nv = (pick1 ? L1 : L2) + (pick1 ? U1 : U2);
+            const uint32_t bank = ch >> 6, l = ch & 63;
+            const bool mine = lane == (int)l;
+#pragma unroll
+            for (int k = 0; k < R; k++)
+                if (bank == (uint32_t)k) {
+                    Llo[k] = mine ? (uint32_t)nv : Llo[k];
+                    Lhi[k] = mine ? (uint32_t)((uint64_t)nv >> 32) : Lhi[k];
+                }
+            if (lane == j) {
+                myL1 = L1;
+                myL2 = L2;
+            }
+        }
+        if (ok)
+            store_out(s, r, myL1, myL2, flags, chosen, ttft, base, per, qshift, slo);
+    }
+#pragma unroll
+    for (int k = 0; k < R; k++) {
+        const uint32_t i = 64 * k + lane;
+        if (i < S)
+            loads[i] = (int64_t)(((uint64_t)Lhi[k] << 32) | Llo[k]);
+    }
+}
+
+// Same rule with loads in LDS, for slot spaces beyond the register banks.
+__global__ __launch_bounds__(kWave) void select_lds_kernel(
+    const int64_t* __restrict__ offsets, uint64_t n, uint32_t bshift,
+    const uint32_t* __restrict__ cand, const uint32_t* __restrict__ match,
+    uint8_t* __restrict__ flags, uint32_t* __restrict__ chosen, int64_t* __restrict__ ttft,
+    int64_t* __restrict__ loads, uint32_t S, int64_t base, int64_t per, uint32_t qshift, int64_t slo,
+    const uint32_t* __restrict__ plan)
+{
+    if (!plan[0])
+        return;
+    __shared__ int64_t L[kMaxSlots];
+    const int lane = lane_id();
+    for (uint32_t i = lane; i < S; i += kWave)
+        L[i] = loads[i];
+    __syncthreads();
+    for (uint64_t r0 = 0; r0 < n; r0 += kWave) {
+        const uint64_t r = r0 + lane;
+        const bool ok = r < n;
+        const SelRec s = load_rec(offsets, n, r, ok, bshift, cand, match, base, per, qshift, slo);
+        int64_t myL1 = 0, myL2 = 0;
+        const int cnt = (int)(n - r0 < (uint64_t)kWave ? n - r0 : kWave);
+        for (int j = 0; j < cnt; j++) {
+            const uint32_t C1 = __builtin_amdgcn_readlane(s.c1, j);
+            const uint32_t C2 = __builtin_amdgcn_readlane(s.c2, j);
+            const uint32_t K = __builtin_amdgcn_readlane(s.kind, j);
+            const int64_t TH = (int64_t)readlane_u64((uint64_t)s.th, j);
+            const int64_t U1 = (int64_t)readlane_u64((uint64_t)s.u1, j);
+            const int64_t U2 = (int64_t)readlane_u64((uint64_t)s.u2, j);
+            const int64_t L1 = L[C1], L2 = L[C2];
+            const bool pick1 = pick_first(K, L1, L2, TH);
+            const uint32_t ch = pick1 ? C1 : C2;
+            const int64_t nv = (pick1 ? L1 : L2) + (pick1 ? U1 : U2);
+            __syncthreads();
+            if (lane == 0)
+                L[ch] = nv;
+            __syncthreads();
+            if (lane == j) {
+                myL1 = L1;
+                myL2 = L2;
+            }
+        }
+        if (ok)
+            store_out(s, r, myL1, myL2, flags, chosen, ttft, base, per, qshift, slo);
+    }
+    __syncthreads();
+    for (uint32_t i = lane; i < S; i += kWave)
+        loads[i] = L[i];
+}
+
+// ---------------------------------------------------------------------------
+// Fast path.
+// ---------------------------------------------------------------------------
+
+// w: a | o << 8 | (depth - 1) << 16 | (window depth - 1) << 22 | (a is c2) << 28
+struct SelPack {
+    uint32_t w;
+    uint32_t ua;  // uncached tokens on a
+    uint32_t uo;  // uncached tokens on o
+    int32_t th;   // take a iff L_a <= max(th, L_o), relative loads
+};
+
+// plan[0] = 1 for the 64-bit path; plan[1] = 1 for the 32-bit path.
+// base[0] = smallest live load; grow[d] bounds how much live instance d's
+// load can grow in this batch (the larger uncached count of every request
+// that has it as a candidate).
+__global__ __launch_bounds__(256) void sel_base_kernel(const int64_t* __restrict__ loads,
+                                                       const uint32_t* __restrict__ live_ids,
+                                                       uint32_t n_live, int64_t* __restrict__ base,
+                                                       unsigned long long* __restrict__ grow)
+{
+    __shared__ int64_t smin[256];
+    int64_t mn = INT64_MAX;
+    for (uint32_t k = threadIdx.x; k < n_live; k += blockDim.x) {
+        const int64_t v = loads[live_ids[k]];
+        mn = v < mn ? v : mn;
+        grow[k] = 0;
+    }
+    smin[threadIdx.x] = mn;
+    __syncthreads();
+    for (int d = 128; d > 0; d >>= 1) {
+        if (threadIdx.x < d)
+            smin[threadIdx.x] = std::min(smin[threadIdx.x], smin[threadIdx.x + d]);
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        base[0] = smin[0];
+        grow[kMaxSlots] = 0;  // set if some record does not fit 32 bits
+    }
+}
+
+constexpr uint32_t kFastMaxLive = 256;
+
+__global__ __launch_bounds__(256) void sel_prep_kernel(
+    const int64_t* __restrict__ offsets, uint64_t n, uint32_t bshift,
+    const uint32_t* __restrict__ cand, const uint32_t* __restrict__ match,
+    const uint32_t* __restrict__ dense, uint32_t n_live, const int64_t* __restrict__ base,
+    int64_t tbase, int64_t per, uint32_t qshift, int64_t slo, SelPack* __restrict__ rec,
+    unsigned long long* __restrict__ grow)
+{
+    __shared__ unsigned long long sg[kFastMaxLive];
+    const bool track = n_live <= kFastMaxLive;
+    if (track)
+        for (uint32_t k = threadIdx.x; k < n_live; k += blockDim.x)
+            sg[k] = 0;
+    __syncthreads();
+    const int64_t b0 = base[0];
+    unsigned long long bad = 0;
+    for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
+         r += (uint64_t)gridDim.x * blockDim.x) {
+        const uint32_t m1 = match[r], m2 = match[n + r];
+        const int64_t len = offsets[r + 1] - offsets[r];
+        const int64_t u1 = len - ((int64_t)m1 << bshift), u2 = len - ((int64_t)m2 << bshift);
+        const bool eq = m1 == m2, aff2 = m2 > m1;
+        const uint32_t d1 = dense[cand[r]], d2 = dense[cand[n + r]];
+        // T_a <= slo  <=>  floor(L_a / 2^q) <= slo - base - per*u_a  <=>  L_a < th_abs;
+        // relative loads lie in [0, 2^31 - 1), so the bound is clamped to that range.
+        // Equal matches: take c1 iff L1 <= L2, i.e. th = -2^31.
+        int32_t th = INT32_MIN;
+        if (!eq) {
+            const int64_t th_abs = (slo - tbase - per * (aff2 ? u2 : u1) + 1) * ((int64_t)1 << qshift);
+            int64_t t = th_abs - 1 - b0;
+            th = (int32_t)(t < -1 ? -1 : (t > INT32_MAX ? INT32_MAX : t));
+        }
+        SelPack p;
+        p.w = aff2 ? ((d2 & 0xFF) | (d1 & 0xFF) << 8 | 1u << 28) : ((d1 & 0xFF) | (d2 & 0xFF) << 8);
+        p.ua = (uint32_t)(aff2 ? u2 : u1);
+        p.uo = (uint32_t)(aff2 ? u1 : u2);
+        p.th = th;
+        rec[r] = p;
+        const bool ok = u1 >= 0 && u2 >= 0 && u1 <= INT32_MAX && u2 <= INT32_MAX;
+        bad |= ok ? 0ull : 1ull;
+        if (track && ok) {
+            const unsigned long long g = (unsigned long long)(u1 > u2 ? u1 : u2);
+            atomicAdd(&sg[d1], g);
+            if (d2 != d1)
+                atomicAdd(&sg[d2], g);
+        }
+    }
+    __syncthreads();
+    if (track)
+        for (uint32_t k = threadIdx.x; k < n_live; k += blockDim.x)
+            if (sg[k])
+                atomicAdd(&grow[k], sg[k]);
+    if (bad)
+        atomicOr(&grow[kMaxSlots], 1ull);
+}
+
+// Fast path iff at most 256 instances are live and every live load stays
+// below base + 2^31 - 1 whatever the decisions.
+__global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict__ loads,
+                                                       const uint32_t* __restrict__ live_ids,
+                                                       uint32_t n_live,
+                                                       const int64_t* __restrict__ base,
+                                                       const unsigned long long* __restrict__ grow,
+                                                       uint32_t* __restrict__ plan)
+{
+    __shared__ int ok_all;
+    if (threadIdx.x == 0)
+        ok_all = n_live <= kFastMaxLive && grow[kMaxSlots] == 0;
+    __syncthreads();
+    for (uint32_t k = threadIdx.x; k < n_live && k < kFastMaxLive; k += blockDim.x) {
+        const unsigned long long span = (unsigned long long)(loads[live_ids[k]] - base[0]);
+        if (span >= (1ull << 30) || grow[k] >= (1ull << 30))
+            atomicAnd(&ok_all, 0);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        plan[0] = ok_all ? 0 : 1;
+        plan[1] = ok_all ? 1 : 0;
+    }
+}
+
+// Depth of every request inside its 64-request window: 1 + the larger depth
+// of the latest earlier request of the window on either candidate (0 when
+// none).  Along every instance's requests the depth strictly grows, so the
+// requests of one depth touch pairwise distinct instances.
+constexpr int kLevelWaves = 4;
+
+__global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(
+    SelPack* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ plan)
+{
+    if (!plan[1])
+        return;
+    __shared__ unsigned long long M[kLevelWaves][kFastMaxLive];
+    const int lane = lane_id(), wv = threadIdx.x >> 6;
+    unsigned long long* m = M[wv];
+    for (uint32_t k = lane; k < kFastMaxLive; k += kWave)
+        m[k] = 0;
+    const uint64_t r = ((uint64_t)blockIdx.x * kLevelWaves + wv) * kWave + lane;
+    const bool valid = r < n;
+    const uint32_t w = valid ? rec[r].w : 0;
+    const uint32_t a = w & 0xFF, o = (w >> 8) & 0xFF;
+    const unsigned long long bit = 1ull << lane, lt = bit - 1;
+    __syncthreads();
+    if (valid) {
+        atomicOr(&m[a], bit);
+        atomicOr(&m[o], bit);
+    }
+    __syncthreads();
+    const unsigned long long P1 = valid ? m[a] & lt : 0, P2 = valid ? m[o] & lt : 0;
+    const int p1 = P1 ? 63 - __clzll(P1) : lane, p2 = P2 ? 63 - __clzll(P2) : lane;
+    // Jacobi relaxation from depth 1: values only grow and reach the depths
+    // after at most max-depth rounds; a round without change is the fixed point.
+    int lv = valid ? 1 : 0;
+    for (;;) {
+        const int l1 = __shfl(lv, p1), l2 = __shfl(lv, p2);
+        const int nl = valid ? 1 + std::max(P1 ? l1 : 0, P2 ? l2 : 0) : 0;
+        const bool changed = nl != lv;
+        lv = nl;
+        if (!__any(changed))
+            break;
+    }
+    int mx = lv;
+    for (int d = 1; d < kWave; d <<= 1)
+        mx = std::max(mx, __shfl_xor(mx, d));
+    if (valid)
+        rec[r].w = (w & 0x1000FFFFu) | (uint32_t)(lv - 1) << 16 | (uint32_t)(mx - 1) << 22;
+}
+
+// Walks the windows in order; see the file comment.  rec holds one padding
+// window past the last so that the prefetch stays in bounds; lpre receives
+// the pre-update loads (L_c1, L_c2) of every request (padded to whole
+// windows).
+__global__ __launch_bounds__(kWave) void select_fast_kernel(
+    const SelPack* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ live_ids,
+    uint32_t n_live, int64_t* __restrict__ loads, const uint32_t* __restrict__ plan,
+    const int64_t* __restrict__ base, int2* __restrict__ lpre)
+{
+    if (!plan[1])
+        return;
+    __shared__ int32_t L[kFastMaxLive];
+    const int lane = lane_id();
+    const int64_t b0 = base[0];
+    for (uint32_t d = lane; d < kFastMaxLive; d += kWave)
+        L[d] = d < n_live ? (int32_t)(loads[live_ids[d]] - b0) : 0;
+    __syncthreads();
+    const uint64_t nw = (n + kWave - 1) / kWave;
+    SelPack cur = rec[lane];
+    for (uint64_t w = 0; w < nw; w++) {
+        const SelPack nxt = rec[(w + 1) * kWave + lane];
+        const bool valid = w * kWave + lane < n;
+        const uint32_t a = cur.w & 0xFF, o = (cur.w >> 8) & 0xFF;
+        const uint32_t mylv = valid ? (cur.w >> 16) & 63 : 64;
+        const uint32_t depth = __builtin_amdgcn_readfirstlane((cur.w >> 22) & 63) + 1;
+        int32_t La = 0, Lo = 0;
+        for (uint32_t l = 0; l < depth; l++) {
+            if (mylv == l) {
+                La = L[a];
+                Lo = L[o];
+                const bool take_a = La <= std::max(cur.th, Lo);
+                L[take_a ? a : o] = take_a ? La + (int32_t)cur.ua : Lo + (int32_t)cur.uo;
+            }
+        }
+        const bool flip = (cur.w >> 28) & 1;
+        lpre[w * kWave + lane] = flip ? make_int2(Lo, La) : make_int2(La, Lo);
+        cur = nxt;
+    }
+    __syncthreads();
+    for (uint32_t d = lane; d < n_live && d < kFastMaxLive; d += kWave)
+        loads[live_ids[d]] = b0 + L[d];
+}
+
+__global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, uint32_t bshift,
+                               const uint32_t* __restrict__ cand, const uint32_t* __restrict__ match,
+                               const int2* __restrict__ lpre, const int64_t* __restrict__ base,
+                               const uint32_t* __restrict__ plan, uint8_t* __restrict__ flags,
+                               uint32_t* __restrict__ chosen, int64_t* __restrict__ ttft,
+                               int64_t tbase, int64_t per, uint32_t qshift, int64_t slo)
+{
+    if (!plan[1])
+        return;
+    const int64_t b0 = base[0];
+    for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
+         r += (uint64_t)gridDim.x * blockDim.x) {
+        SelRec s = load_rec(offsets, n, r, true, bshift, cand, match, tbase, per, qshift, slo);
+        const int2 lp = lpre[r];
+        store_out(s, r, b0 + lp.x, b0 + lp.y, flags, chosen, ttft, tbase, per, qshift, slo);
+    }
+}
+
+template <int R>
+void launch_select(dm_ctx* c, const int64_t* offsets, uint64_t n, uint32_t bshift,
+                   const dm_route_out* out, int64_t* loads, const uint32_t* plan)
+{
+    const dm_config& k = c->cfg;
+    select_kernel<R><<<1, kWave, 0, c->stream>>>(offsets, n, bshift, out->cand, out->match,
+                                                 out->flags, out->chosen, out->ttft_us, loads,
+                                                 k.max_slots, k.ttft_base_us, k.ttft_per_token_us,
+                                                 c->shift_div, k.slo_us, plan);
+}
+
+}  // namespace
+
+hipError_t select_batch(dm_ctx* c, const int64_t* offsets, uint64_t n, const dm_route_out* out,
+                        int64_t* loads)
+{
+    hipError_t e = hipSuccess;
+    hipStream_t st = c->stream;
+    uint32_t bshift = 0;
+    while ((1u << bshift) < c->cfg.block_size)
+        bshift++;
+    const uint32_t S = c->cfg.max_slots;
+    const dm_config& k = c->cfg;
+    // work arrays: records (one padding window), pre-update loads, base/plan words
+    const uint64_t nw = (n + kWave - 1) / kWave;
+    const uint64_t nrec = (nw + 1) * kWave;
+    const size_t rec_bytes = nrec * sizeof(SelPack), lpre_bytes = nw * kWave * sizeof(int2);
+    const size_t tail_bytes = 256 + (kMaxSlots + 1) * sizeof(unsigned long long);
+    uint8_t* sw = static_cast<uint8_t*>(
+        scratch_get(c, kSelSlot, rec_bytes + lpre_bytes + tail_bytes + 256, &e));
+    if (!sw)
+        return e;
+    SelPack* rec = reinterpret_cast<SelPack*>(sw);
+    int2* lpre = reinterpret_cast<int2*>(sw + rec_bytes);
+    uint8_t* tail = sw + ((rec_bytes + lpre_bytes + 255) & ~size_t(255));
+    int64_t* base = reinterpret_cast<int64_t*>(tail);
+    uint32_t* plan = reinterpret_cast<uint32_t*>(tail + 128);
+    unsigned long long* grow = reinterpret_cast<unsigned long long*>(tail + 256);
+    const uint32_t NL = c->n_live;
+    sel_base_kernel<<<1, 256, 0, st>>>(loads, c->d_live_ids, NL, base, grow);
+    sel_prep_kernel<<<grid_for(n, 256, 4096), 256, 0, st>>>(
+        offsets, n, bshift, out->cand, out->match, c->d_dense, NL, base, k.ttft_base_us,
+        k.ttft_per_token_us, c->shift_div, k.slo_us, rec, grow);
+    sel_plan_kernel<<<1, 256, 0, st>>>(loads, c->d_live_ids, NL, base, grow, plan);
+    const uint64_t lgrid = (nw + kLevelWaves - 1) / kLevelWaves;
+    if (lgrid > 0x7FFFFFFFull)
+        return hipErrorInvalidValue;
+    sel_level_kernel<<<(uint32_t)lgrid, kLevelWaves * kWave, 0, st>>>(rec, n, plan);
+    select_fast_kernel<<<1, kWave, 0, st>>>(rec, n, c->d_live_ids, NL, loads, plan, base, lpre);
+    sel_out_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(
+        offsets, n, bshift, out->cand, out->match, lpre, base, plan, out->flags, out->chosen,
+        out->ttft_us, k.ttft_base_us, k.ttft_per_token_us, c->shift_div, k.slo_us);
+    if (S <= 64)
+        launch_select<1>(c, offsets, n, bshift, out, loads, plan);
+    else if (S <= 128)
+        launch_select<2>(c, offsets, n, bshift, out, loads, plan);
+    else if (S <= 192)
+        launch_select<3>(c, offsets, n, bshift, out, loads, plan);
+    else if (S <= 256)
+        launch_select<4>(c, offsets, n, bshift, out, loads, plan);
+    else
+        select_lds_kernel<<<1, kWave, 0, st>>>(offsets, n, bshift, out->cand, out->match,
+                                               out->flags, out->chosen, out->ttft_us, loads, S,
+                                               k.ttft_base_us, k.ttft_per_token_us, c->shift_div,
+                                               k.slo_us, plan);
+    return hipGetLastError();
+}
+
+}  // namespace dm

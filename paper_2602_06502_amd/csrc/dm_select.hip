@@ -394,10 +394,10 @@ __global__ __launch_bounds__(kWave) void select_fast_kernel(
 {
     if (!plan[1])
         return;
-    __shared__ int32_t L[kFastMaxLive];
+    __shared__ int32_t L[kFastMaxLive + kWave];  // loads, then one spare slot per lane
     const int lane = lane_id();
     const int64_t b0 = base[0];
-    for (uint32_t d = lane; d < kFastMaxLive; d += kWave)
+    for (uint32_t d = lane; d < kFastMaxLive + kWave; d += kWave)
         L[d] = d < n_live ? (int32_t)(loads[live_ids[d]] - b0) : 0;
     __syncthreads();
     const uint64_t nw = (n + kWave - 1) / kWave;
@@ -408,14 +408,18 @@ __global__ __launch_bounds__(kWave) void select_fast_kernel(
         const uint32_t a = cur.w & 0xFF, o = (cur.w >> 8) & 0xFF;
         const uint32_t mylv = valid ? (cur.w >> 16) & 63 : 64;
         const uint32_t depth = __builtin_amdgcn_readfirstlane((cur.w >> 22) & 63) + 1;
+        // Every lane reads and writes at every depth, without branches; a lane
+        // not at the current depth writes its own spare slot.
         int32_t La = 0, Lo = 0;
+        const int32_t ua = (int32_t)cur.ua, uo = (int32_t)cur.uo, th = cur.th;
         for (uint32_t l = 0; l < depth; l++) {
-            if (mylv == l) {
-                La = L[a];
-                Lo = L[o];
-                const bool take_a = La <= std::max(cur.th, Lo);
-                L[take_a ? a : o] = take_a ? La + (int32_t)cur.ua : Lo + (int32_t)cur.uo;
-            }
+            const int32_t xa = L[a], xo = L[o];
+            const bool act = mylv == l;
+            const bool take_a = xa <= std::max(th, xo);
+            const uint32_t dst = act ? (take_a ? a : o) : kFastMaxLive + lane;
+            L[dst] = take_a ? xa + ua : xo + uo;
+            La = act ? xa : La;
+            Lo = act ? xo : Lo;
         }
         const bool flip = (cur.w >> 28) & 1;
         lpre[w * kWave + lane] = flip ? make_int2(Lo, La) : make_int2(La, Lo);

@@ -382,19 +382,30 @@ int or_index_erase(or_state *st, uint32_t id, const uint64_t *keys, uint64_t n)
 {
     if (!st || id >= st->cfg.max_slots || (!keys && n))
         return OR_EINVAL;
+    uint64_t *a = st->set[id];
+    uint64_t len = st->set_len[id];
+    if (n == 0 || len == 0)
+        return OR_OK;
+    /* mark every present key, then keep the unmarked ones in order */
+    uint8_t *gone = (uint8_t *)calloc(len, 1);
+    if (!gone)
+        return OR_ENOMEM;
     for (uint64_t i = 0; i < n; i++) {
         uint64_t k = canon(keys[i]);
-        uint64_t *a = st->set[id];
-        uint64_t len = st->set_len[id], lo = 0, hi = len;
+        uint64_t lo = 0, hi = len;
         while (lo < hi) {
             uint64_t mid = lo + (hi - lo) / 2;
             if (a[mid] < k) lo = mid + 1; else hi = mid;
         }
-        if (lo < len && a[lo] == k) {
-            memmove(a + lo, a + lo + 1, (len - lo - 1) * sizeof(uint64_t));
-            st->set_len[id] = len - 1;
-        }
+        if (lo < len && a[lo] == k)
+            gone[lo] = 1;
     }
+    uint64_t w = 0;
+    for (uint64_t i = 0; i < len; i++)
+        if (!gone[i])
+            a[w++] = a[i];
+    free(gone);
+    st->set_len[id] = w;
     return OR_OK;
 }
 

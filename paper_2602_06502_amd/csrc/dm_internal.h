@@ -13,6 +13,7 @@
 namespace dm {
 
 constexpr int kWave = 64;
+constexpr int kScratchSlots = 9;  // context work buffers, one per use (each file names its slots)
 constexpr uint32_t kMaxSlots = 4096;
 constexpr uint64_t kEmpty = 0;      // index slot never used
 constexpr uint64_t kTomb = 1;       // index slot erased
@@ -89,7 +90,7 @@ struct dm_ctx {
     uint64_t* d_counts = nullptr;  // [2 * max_slots] live keys, then occupied slots
     uint32_t* d_status = nullptr;  // device status word
 
-    dm::Scratch scratch[8];
+    dm::Scratch scratch[dm::kScratchSlots];
     uint32_t shift_div = 0;        // log2(queue_div)
 
     // stage timing of dm_route_batch (events recorded only when enabled)

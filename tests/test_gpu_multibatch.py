@@ -1,0 +1,145 @@
+"""Multi-batch parity on the chat and agent workloads.
+
+Each side -- the engine through the C ABI, and the CPU oracle -- routes every
+batch and then evolves its own serving state from its own outputs
+(tests/sim.py): routed chains saved into the serving instance's LRU-bounded
+index (evictions through dm_index_erase), queued work drained between
+batches, and on the agent workload queues rebalanced after every batch.
+Every routed batch (ring keys, candidates, matches, choices, TTFT, flags,
+block keys, loads) and every rebalancing pass (migration list, loads) must
+agree element by element.
+
+Chat: 16 instances, 2,048-session warm-up (16,384 requests), then 16
+batches of 4,096 requests from 8,192 sessions.  Agent: 32 instances, 16,384
+warm-up requests, then 16 batches of 16,384 requests over 32 system prompts;
+before each pass, four seed-chosen instances stall to 5x the mean queued
+work (a load the router did not see, as with a decode-bound instance).
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+sys.path.insert(0, __file__.rsplit("/", 1)[0])
+import sim  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+AGENT_MU = 320_000  # mean queued work per instance: 5x crosses the SLO (5 mu / 4 > 400 ms)
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+class OracleSide:
+    def __init__(self, rc):
+        self.o = oracle.Oracle(rc.as_dict())
+        assert self.o.build_rings(range(rc.n_inst)) == 0
+
+    def route(self, tok, off, loads):
+        return self.o.route(tok, off, loads, block_keys=True)
+
+    def insert(self, c, keys):
+        self.o.index_insert(c, keys)
+
+    def erase(self, c, keys):
+        self.o.index_erase(c, keys)
+
+    def rebalance(self, q):
+        r = self.o.rebalance(*q)
+        assert r["status"] == 0
+        return r
+
+
+class EngineSide:
+    def __init__(self, rc):
+        import paper_2602_06502_amd.harness as gh
+        self.gh = gh
+        self.eng = gh.DualMap(rc.as_dict(), device="cuda:0")
+        self.eng.build_rings(list(range(rc.n_inst)))
+
+    def _d(self, a):
+        return self.gh.to_dev(a, self.eng.device)
+
+    def route(self, tok, off, loads):
+        L = self._d(np.asarray(loads, np.int64))
+        out = self.eng.route(self._d(tok), self._d(off), L, block_keys=True)
+        self.eng.sync()
+        res = {k: v.cpu().numpy() for k, v in out.items()}
+        res["loads"] = L.cpu().numpy()
+        return res
+
+    def insert(self, c, keys):
+        self.eng.index_insert(c, self._d(keys))
+
+    def erase(self, c, keys):
+        self.eng.index_erase(c, self._d(keys))
+
+    def rebalance(self, q):
+        g = self.eng.rebalance(*[self._d(a) for a in q])
+        self.eng.sync()
+        n = int(g["count"].cpu().numpy()[0])
+        res = {k: g[k].cpu().numpy()[:n] for k in ("rec", "src", "dst", "benefit", "ttft_to")}
+        res["count"] = n
+        res["loads"] = g["loads"].cpu().numpy()
+        return res
+
+
+ROUTE_KEYS = ("key", "cand", "match", "chosen", "ttft", "flags", "block_keys", "loads")
+MIGRATION_KEYS = ("rec", "src", "dst", "benefit", "ttft_to", "loads")
+
+
+def _compare(stage, b, g, o):
+    keys = ROUTE_KEYS if stage in ("warm", "route") else MIGRATION_KEYS
+    for k in keys:
+        assert np.array_equal(g[k], o[k]), f"{stage} batch {b}: {k} differs"
+    if stage == "rebalance":
+        assert g["count"] == o["count"], f"batch {b}: migration count"
+
+
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def test_chat_multibatch_parity():
+    _gpu()
+    cfg = workloads.chat()
+    rc = cfg.route
+    gs, os_ = EngineSide(rc), OracleSide(rc)
+    flags = []
+    for (st, b, g), (st2, b2, o) in zip(sim.run_chat(gs, cfg, 16), sim.run_chat(os_, cfg, 16)):
+        assert (st, b) == (st2, b2)
+        _say("chat", st, b, "requests", len(o["chosen"]))
+        _compare(st, b, g, o)
+        if st == "route":
+            flags.append(o["flags"])
+    f = np.concatenate(flags)
+    assert len(f) == cfg.n_req
+    # the cache-affinity branch dominates; both equal and unequal matches occur
+    assert (f & 4).any() and (~f & 4).any()
+
+
+def test_agent_multibatch_parity():
+    _gpu()
+    cfg = workloads.agent()
+    rc = cfg.route
+    gs, os_ = EngineSide(rc), OracleSide(rc)
+    migrated = queued = 0
+    for (st, b, g), (st2, b2, o) in zip(sim.run_agent(gs, cfg, AGENT_MU, 16),
+                                        sim.run_agent(os_, cfg, AGENT_MU, 16)):
+        assert (st, b) == (st2, b2)
+        _say("agent", st, b, "migrations" if st == "rebalance" else "requests",
+             o["count"] if st == "rebalance" else len(o["chosen"]))
+        _compare(st, b, g, o)
+        if st == "rebalance":
+            migrated += o["count"]
+            queued += o["queued"]
+    assert migrated > 0
+    _say("agent migrated", migrated, "of", queued, "queued records over 16 passes")

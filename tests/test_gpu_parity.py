@@ -285,6 +285,39 @@ def test_index_ops_and_capacity():
     assert eng.index_size(1) == 128
 
 
+def test_index_churn_rebuilds_erased_slots():
+    """Erased slots never take new keys, so churn would fill a table with
+    them; an insert that would pass the load limit while erased slots exist
+    rebuilds the table first.  2^8 slots hold at most 128 keys."""
+    gh = _h()
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=2, index_log2_slots=8)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    d = lambda a: gh.to_dev(a, eng.device)
+    rng = np.random.default_rng(11)
+    keys = rng.integers(2, 2**64, size=180, dtype=np.uint64)
+    assert len(set(keys.tolist())) == 180
+    eng.index_insert(0, d(keys[:100]))
+    eng.index_erase(0, d(keys[:60]))
+    eng.index_insert(0, d(keys[100:]))  # 100 occupied + 80 > 128: rebuilt, 40 + 80 live
+    eng.sync()
+    assert eng.index_size(0) == 120
+    eng.index_erase(0, d(keys[:60]))  # absent keys: nothing changes
+    eng.sync()
+    assert eng.index_size(0) == 120
+    eng.index_erase(0, d(keys[60:]))  # all 120 present
+    eng.sync()
+    assert eng.index_size(0) == 0
+    # many rounds of churn, each inserting 100 fresh keys and erasing them
+    for r in range(20):
+        k = rng.integers(2, 2**64, size=100, dtype=np.uint64)
+        eng.index_insert(1, d(k))
+        eng.sync()
+        assert eng.index_size(1) == 100, r
+        eng.index_erase(1, d(k))
+        eng.sync()
+        assert eng.index_size(1) == 0, r
+
+
 def test_index_erase_then_match_parity():
     """Erased blocks break a cached prefix at the erased block."""
     gh = _h()

@@ -269,3 +269,198 @@ def synthetic_queues(seed: int, n_slots: int, n_live: int, sources: np.ndarray, 
     base = rng.integers(0, cold_hi + 1, size=n_slots).astype(np.int64)
     base[sources] = base_src
     return Queues(qoff, rec, here, alt, other, base)
+
+
+# --------------------------------------------------------------------------
+# Multi-batch workloads: conversation sessions and agent system prompts.
+# They stand in for the Mooncake Conversation and Tool&Agent traces
+# (Table 1, Sec. A.2.1): the first reproduces multi-turn prefix reuse, the
+# second a few very hot, long shared system prompts.
+# --------------------------------------------------------------------------
+
+_S_SESSION_BUDGET, _S_SESSION_TURNS, _S_SESSION_TOK, _S_ARRIVAL = 12, 13, 14, 15
+_S_GAPS, _S_AGENT_TPL, _S_AGENT_TAIL, _S_AGENT_TOK, _S_AGENT_HOT = 16, 17, 18, 19, 20
+
+
+@dataclasses.dataclass(frozen=True)
+class Chat:
+    """Multi-turn chat: sessions of 1..max_turns user turns; a turn's prompt is
+    the first history_cap tokens of the session's earlier turns followed by
+    the new turn; sessions arrive by Zipf popularity among those with turns
+    left.  A disjoint population of warm_sessions sessions supplies the
+    warm-up requests that fill the LRU-bounded indexes."""
+
+    route: RouteConfig
+    seed: int = 102
+    vocab: int = 128_000
+    n_sessions: int = 8192
+    warm_sessions: int = 2048
+    max_turns: int = 16
+    turn_lo: int = 64
+    turn_hi: int = 512
+    history_cap: int = 8192
+    zipf_s: float = 0.9
+    n_req: int = 65_536
+    n_warm: int = 16_384
+    batch: int = 4096
+    lru_blocks: int = 200_000
+    load_hi: int = 50_000
+    drain_per_us: int = 4
+    utilisation: float = 0.9
+
+
+def chat(n_req: int = 65_536, n_warm: int = 16_384) -> Chat:
+    """16 instances x 128 vnodes, block 16, K 4, vocab 128,000; 8,192 sessions
+    (2,048 more for warm-up), turns U[64,512] tokens, history cap 8,192,
+    Zipf 0.9; batches of 4,096; LRU of 200,000 blocks per instance in 2^19-slot
+    tables."""
+    rc = RouteConfig("chat", 16, 128, 16, 4, (1, 2), 16, 19)
+    return Chat(rc, n_req=n_req, n_warm=n_warm)
+
+
+class ChatStream:
+    """Arrivals of one session population (0 = measured, 1 = warm-up) and the
+    prompts they carry."""
+
+    def __init__(self, cfg: Chat, population: int):
+        self.cfg = cfg
+        S = cfg.n_sessions if population == 0 else cfg.warm_sessions
+        n = cfg.n_req if population == 0 else cfg.n_warm
+        self.pop = population
+        self.budget = _rng(cfg.seed, _S_SESSION_BUDGET, population).integers(
+            1, cfg.max_turns + 1, size=S)
+        self.turn_len = _rng(cfg.seed, _S_SESSION_TURNS, population).integers(
+            cfg.turn_lo, cfg.turn_hi + 1, size=(S, cfg.max_turns)).astype(np.int64)
+        self.session, self.turn = self._arrivals(S, min(n, int(self.budget.sum())))
+        self.n = len(self.session)
+        self._tok: Dict[int, np.ndarray] = {}
+
+    def _arrivals(self, S: int, n: int) -> Tuple[np.ndarray, np.ndarray]:
+        """Zipf draws over sessions; a draw of a session with no turns left is
+        drawn again (rejection), which samples Zipf restricted to the sessions
+        with turns left."""
+        rng = _rng(self.cfg.seed, _S_ARRIVAL, self.pop)
+        used = np.zeros(S, dtype=np.int64)
+        parts = []
+        got = 0
+        while got < n:
+            d = zipf_ranks(rng, S, self.cfg.zipf_s, 1 << 20)
+            order = np.argsort(d, kind="stable")
+            ds = d[order]
+            starts = np.r_[0, np.flatnonzero(np.diff(ds)) + 1]
+            occ_sorted = np.arange(len(ds)) - np.repeat(starts, np.diff(np.r_[starts, len(ds)]))
+            occ = np.empty_like(occ_sorted)
+            occ[order] = occ_sorted
+            acc = d[(used[d] + occ) < self.budget[d]][: n - got]
+            np.add.at(used, acc, 1)
+            parts.append(acc)
+            got += len(acc)
+        ses = np.concatenate(parts) if parts else np.zeros(0, dtype=np.int64)
+        # turn index of each arrival = earlier arrivals of its session
+        order = np.argsort(ses, kind="stable")
+        ss = ses[order]
+        starts = np.r_[0, np.flatnonzero(np.diff(ss)) + 1] if len(ss) else np.zeros(0, np.int64)
+        occ_sorted = np.arange(len(ss)) - np.repeat(starts, np.diff(np.r_[starts, len(ss)]))
+        turn = np.empty_like(occ_sorted)
+        turn[order] = occ_sorted
+        return ses.astype(np.int64), turn.astype(np.int64)
+
+    def _session_tokens(self, s: int) -> np.ndarray:
+        t = self._tok.get(s)
+        if t is None:
+            total = int(self.turn_len[s, : self.budget[s]].sum())
+            t = uniform_tokens(_rng(self.cfg.seed, _S_SESSION_TOK, self.pop * (1 << 20) + s),
+                               self.cfg.vocab, total)
+            self._tok[s] = t
+        return t
+
+    def batch(self, lo: int, hi: int) -> Tuple[np.ndarray, np.ndarray]:
+        """Prompts of arrivals lo..hi-1 as a token CSR."""
+        parts = []
+        for i in range(lo, min(hi, self.n)):
+            s, t = int(self.session[i]), int(self.turn[i])
+            tok = self._session_tokens(s)
+            cum = np.concatenate([[0], np.cumsum(self.turn_len[s, : t + 1])])
+            hist = tok[: min(int(cum[t]), self.cfg.history_cap)]
+            parts.append(np.concatenate([hist, tok[cum[t]: cum[t + 1]]]))
+        off = np.zeros(len(parts) + 1, dtype=np.int64)
+        np.cumsum([len(p) for p in parts], out=off[1:])
+        tok = np.concatenate(parts).astype(np.int32) if parts else np.zeros(0, np.int32)
+        return tok, off
+
+
+@dataclasses.dataclass(frozen=True)
+class Agent:
+    """Agent/tool workload: a few long system prompts with Zipf popularity and
+    a random tail per request; queued work skewed onto hot_inst instances."""
+
+    route: RouteConfig
+    seed: int = 103
+    vocab: int = 128_000
+    n_templates: int = 32
+    tlen_lo: int = 2048
+    tlen_hi: int = 8192
+    zipf_s: float = 1.3
+    tail_lo: int = 128
+    tail_hi: int = 1024
+    n_req: int = 262_144
+    n_warm: int = 16_384
+    batch: int = 16_384
+    lru_blocks: int = 200_000
+    hot_inst: int = 4
+    hot_factor: int = 5
+    drain_per_us: int = 4
+    utilisation: float = 0.9
+
+
+def agent(n_req: int = 262_144, n_warm: int = 16_384, batch: int = 16_384) -> Agent:
+    """32 instances x 256 vnodes, block 32, K 2, vocab 128,000; 32 system
+    prompts of U[2,048, 8,192] tokens, Zipf 1.3, tails U[128, 1,024]; batches
+    of 16,384; LRU of 200,000 blocks per instance in 2^19-slot tables."""
+    rc = RouteConfig("agent", 32, 256, 32, 2, (1, 2), 32, 19)
+    return Agent(rc, n_req=n_req, n_warm=n_warm, batch=batch)
+
+
+def agent_templates(cfg: Agent) -> Tuple[np.ndarray, np.ndarray]:
+    lens = _rng(cfg.seed, _S_TEMPLATE_LEN).integers(cfg.tlen_lo, cfg.tlen_hi + 1,
+                                                    size=cfg.n_templates)
+    off = np.zeros(cfg.n_templates + 1, dtype=np.int64)
+    np.cumsum(lens, out=off[1:])
+    return uniform_tokens(_rng(cfg.seed, _S_TEMPLATE_TOK), cfg.vocab, int(off[-1])), off
+
+
+def agent_batch(cfg: Agent, index: int, n: int, warm: bool = False) -> Tuple[np.ndarray, np.ndarray]:
+    """n prompts of batch `index` (warm-up batches draw from other streams):
+    a Zipf-chosen system prompt followed by a uniform random tail."""
+    sub = index + (1 << 16 if warm else 0)
+    ttok, toff = agent_templates(cfg)
+    tpl = zipf_ranks(_rng(cfg.seed, _S_AGENT_TPL, sub), cfg.n_templates, cfg.zipf_s, n)
+    tail = _rng(cfg.seed, _S_AGENT_TAIL, sub).integers(cfg.tail_lo, cfg.tail_hi + 1, size=n)
+    tlen = np.diff(toff)[tpl]
+    lens = tlen + tail
+    off = np.zeros(n + 1, dtype=np.int64)
+    np.cumsum(lens, out=off[1:])
+    tok = uniform_tokens(_rng(cfg.seed, _S_AGENT_TOK, sub), cfg.vocab, int(off[-1]))
+    _fastgen().fg_copy_prefixes(_vp(tok), _vp(off), _vp(np.ascontiguousarray(tpl)),
+                                _vp(np.ascontiguousarray(tlen, dtype=np.int64)), _vp(ttok),
+                                _vp(toff), n)
+    return tok, off
+
+
+def agent_hot_instances(cfg: Agent, batch: int = 0) -> np.ndarray:
+    """The seed-chosen instances whose queued work jumps to hot_factor times
+    the mean before batch `batch`'s rebalancing pass."""
+    return np.sort(_rng(cfg.seed, _S_AGENT_HOT, batch).choice(cfg.route.n_inst, size=cfg.hot_inst,
+                                                              replace=False)).astype(np.int64)
+
+
+def arrival_gaps(seed: int, n_batches: int, batch: int, mean_gap_us: float) -> np.ndarray:
+    """Duration of each batch's arrivals (microseconds): the sum of `batch`
+    exponential gaps of mean mean_gap_us (Poisson arrivals)."""
+    rng = _rng(seed, _S_GAPS)
+    return rng.gamma(batch, mean_gap_us, size=n_batches)
+
+
+def batch_initial_loads(seed: int, n_slots: int, hi: int) -> np.ndarray:
+    """Per-slot queued work U[0, hi] for the multi-batch workloads."""
+    return _rng(seed, _S_LOADS).integers(0, hi + 1, size=n_slots).astype(np.int64)

@@ -195,16 +195,42 @@ dm_status dm_scale(dm_ctx* ctx, const uint32_t* add, uint32_t n_add, const uint3
                    uint32_t n_rm, const uint64_t* keys, uint64_t n, uint32_t* old_owner,
                    uint32_t* new_owner, uint64_t* moved, uint64_t* violations);
 
-/* Instrumentation.  With on != 0, dm_route_batch records HIP events on the
- * context's stream around its stages; dm_route_stage_ms then waits for the
- * last batch and writes up to n stage times in milliseconds to ms_host:
- * [0] chained block hashing (one kernel), [1] ring lookup and longest
- * cached prefix, [2] in-order selection, [3] per-request block offsets. */
+/* Instrumentation.  With on != 0, dm_route_batch records HIP events around
+ * its stages; dm_route_stage_ms waits for the last batch and writes up to n
+ * stage times in milliseconds to ms_host, averaged over the batches routed
+ * since timing was (re)enabled (the last 64 at most): [0] chained block
+ * hashing (one kernel), [1] ring lookup and longest cached prefix, [2]
+ * in-order selection (with pipelining: from the end of the batch's probe
+ * stage to the end of its selection, so it includes waiting for the
+ * previous batch's selection), [3] per-request block offsets.
+ * dm_route_stage_ms returns DM_ESTATE if timing is off or no batch was
+ * timed. */
 dm_status dm_set_timing(dm_ctx* ctx, int on);
 dm_status dm_route_stage_ms(dm_ctx* ctx, float* ms_host, int n);
 
-/* Wait for all work on the context's stream; return and clear the first
- * device-side error since the last dm_sync. */
+/* Pipelined routing of consecutive batches.  The selection stage is a chain
+ * in request order over shared loads (Sec. 3.2) and runs on one compute
+ * unit, while hashing and probing use the whole GPU.  With on != 0,
+ * dm_route_batch runs its selection on a second stream owned by the
+ * context.  That selection starts once the batch's probe stage and the
+ * previous batch's selection are done, so batches are still decided in
+ * order.  The call does not make the context's stream wait for it, so the
+ * next batch's hashing and probing overlap it.
+ *
+ * Until that selection has run, the batch's tokens, offsets, output arrays
+ * and the loads must stay valid and unmodified, and the next batch needs
+ * distinct output arrays.  The same loads array may be passed to every
+ * batch.
+ *
+ * dm_sync waits for both streams.  Every other call except dm_route_batch,
+ * dm_set_timing and dm_route_stage_ms first orders the context's stream
+ * after the last selection.  Turning pipelining off does the same.  Returns
+ * DM_EDEVICE if the stream or its events cannot be created. */
+dm_status dm_set_pipelining(dm_ctx* ctx, int on);
+
+/* Wait for all work on the context's stream (and, with pipelining, on its
+ * selection stream); return and clear the first device-side error since the
+ * last dm_sync. */
 dm_status dm_sync(dm_ctx* ctx);
 
 /* Message of the last failing call on ctx ("" if none); valid until the next

@@ -25,8 +25,8 @@ _NAMES = {0: "DM_OK", 1: "DM_EINVAL", 2: "DM_ENOMEM", 3: "DM_EFULL", 4: "DM_ESTA
 
 EXPORTS = ("dm_create", "dm_destroy", "dm_build_rings", "dm_ring_export", "dm_index_insert",
            "dm_index_erase", "dm_index_clear", "dm_index_size", "dm_route_batch",
-           "dm_rebalance", "dm_scale", "dm_set_timing", "dm_route_stage_ms", "dm_sync",
-           "dm_last_error")
+           "dm_rebalance", "dm_scale", "dm_set_timing", "dm_route_stage_ms",
+           "dm_set_pipelining", "dm_sync", "dm_last_error")
 
 
 class DMError(RuntimeError):
@@ -85,6 +85,7 @@ def load_library(path: str = LIB_PATH):
         "dm_scale": (i32, [P, P, u32, P, u32, P, u64, P, P, P, P]),
         "dm_set_timing": (i32, [P, i32]),
         "dm_route_stage_ms": (i32, [P, P, i32]),
+        "dm_set_pipelining": (i32, [P, i32]),
         "dm_sync": (i32, [P]),
         "dm_last_error": (C.c_char_p, [P]),
     }
@@ -174,8 +175,15 @@ class DualMap:
     def set_timing(self, on: bool) -> None:
         self._check(self.lib.dm_set_timing(self._h, 1 if on else 0), "dm_set_timing")
 
+    def set_pipelining(self, on: bool) -> None:
+        """Overlap each batch's selection with the next batch's hashing and
+        probing (see dm_set_pipelining): consecutive batches need distinct
+        output buffers, and results are final after sync()."""
+        self._check(self.lib.dm_set_pipelining(self._h, 1 if on else 0), "dm_set_pipelining")
+
     def stage_ms(self):
-        """(hash, lookup+match, selection, block offsets) ms of the last batch."""
+        """(hash, lookup+match, selection, block offsets) ms, averaged over the
+        batches routed since timing was turned on (the last 64 at most)."""
         ms = (C.c_float * 4)()
         self._check(self.lib.dm_route_stage_ms(self._h, ms, 4), "dm_route_stage_ms")
         return tuple(float(x) for x in ms)

@@ -34,8 +34,10 @@ void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e)
         bytes = 256;
     if (s.bytes >= bytes)
         return s.p;
-    // Work already queued may still use the old buffer.
+    // Work already queued (on either stream) may still use the old buffer.
     *e = hipStreamSynchronize(c->stream);
+    if (*e == hipSuccess && c->sel_stream)
+        *e = hipStreamSynchronize(c->sel_stream);
     if (*e != hipSuccess)
         return nullptr;
     size_t nb = std::max(bytes, s.bytes * 2);
@@ -51,6 +53,13 @@ void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e)
     }
     s.bytes = nb;
     return s.p;
+}
+
+hipError_t join_selection(dm_ctx* c)
+{
+    if (!c->pipelined || !c->sel_done)
+        return hipSuccess;
+    return hipStreamWaitEvent(c->stream, c->sel_done, 0);
 }
 
 }  // namespace dm
@@ -216,14 +225,22 @@ void dm_destroy(dm_ctx* c)
         return;
     DeviceGuard g(c->device);
     (void)hipStreamSynchronize(c->stream);
+    if (c->sel_stream)
+        (void)hipStreamSynchronize(c->sel_stream);
     for (auto& b : c->ring)
         for (auto& r : b)
             free_ring(r);
     for (auto& s : c->scratch)
         (void)hipFree(s.p);
-    for (auto& ev : c->ev)
+    for (auto& ev : c->tev)
         if (ev)
             (void)hipEventDestroy(ev);
+    if (c->probe_done)
+        (void)hipEventDestroy(c->probe_done);
+    if (c->sel_done)
+        (void)hipEventDestroy(c->sel_done);
+    if (c->sel_stream)
+        (void)hipStreamDestroy(c->sel_stream);
     (void)hipFree(c->d_hp);
     (void)hipFree(c->d_next_live);
     (void)hipFree(c->d_live_ids);
@@ -251,6 +268,8 @@ dm_status dm_build_rings(dm_ctx* c, const uint32_t* ids, uint32_t n)
         seen[ids[i]] = 1;
     }
     DeviceGuard g(c->device);
+    if (hipError_t je = join_selection(c); je != hipSuccess)
+        return hip_fail(c, je, "dm_build_rings");
     c->live = seen;
     c->n_live = n;
     hipError_t e = upload_live(c);
@@ -275,6 +294,8 @@ dm_status dm_ring_export(dm_ctx* c, int s, uint64_t* pos, uint32_t* id, uint64_t
     if (cap < *len)
         return fail(c, DM_EINVAL, "dm_ring_export: output too small");
     DeviceGuard g(c->device);
+    if (hipError_t je = join_selection(c); je != hipSuccess)
+        return hip_fail(c, je, "dm_ring_export");
     hipError_t e = hipStreamSynchronize(c->stream);
     if (e == hipSuccess && pos && *len)
         e = hipMemcpy(pos, r.pos, *len * sizeof(uint64_t), hipMemcpyDeviceToHost);
@@ -292,6 +313,8 @@ dm_status dm_index_insert(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t
     if (n == 0)
         return DM_OK;
     DeviceGuard g(c->device);
+    if (hipError_t je = join_selection(c); je != hipSuccess)
+        return hip_fail(c, je, "dm_index_insert");
     hipError_t e = index_insert(c, id, keys, n);
     return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_index_insert");
 }
@@ -305,6 +328,8 @@ dm_status dm_index_erase(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t 
     if (n == 0)
         return DM_OK;
     DeviceGuard g(c->device);
+    if (hipError_t je = join_selection(c); je != hipSuccess)
+        return hip_fail(c, je, "dm_index_erase");
     hipError_t e = index_erase(c, id, keys, n);
     return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_index_erase");
 }
@@ -316,6 +341,8 @@ dm_status dm_index_clear(dm_ctx* c, uint32_t id)
     if (id >= c->cfg.max_slots)
         return fail(c, DM_EINVAL, "dm_index_clear: bad id");
     DeviceGuard g(c->device);
+    if (hipError_t je = join_selection(c); je != hipSuccess)
+        return hip_fail(c, je, "dm_index_clear");
     hipError_t e = index_clear(c, id);
     return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_index_clear");
 }
@@ -327,6 +354,8 @@ dm_status dm_index_size(dm_ctx* c, uint32_t id, uint64_t* n_host)
     if (id >= c->cfg.max_slots || !n_host)
         return fail(c, DM_EINVAL, "dm_index_size: bad arguments");
     DeviceGuard g(c->device);
+    if (hipError_t je = join_selection(c); je != hipSuccess)
+        return hip_fail(c, je, "dm_index_size");
     hipError_t e = hipStreamSynchronize(c->stream);
     if (e == hipSuccess)
         e = hipMemcpy(n_host, c->d_counts + id, sizeof(uint64_t), hipMemcpyDeviceToHost);
@@ -369,6 +398,8 @@ dm_status dm_rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out,
         !aligned(out->count))
         return fail(c, DM_EINVAL, "dm_rebalance: misaligned pointer");
     DeviceGuard g(c->device);
+    if (hipError_t je = join_selection(c); je != hipSuccess)
+        return hip_fail(c, je, "dm_rebalance");
     // The record count sizes the work arrays: read qoff[max_slots].
     int64_t Qs = 0, q0 = 0;
     hipError_t e = hipStreamSynchronize(c->stream);
@@ -415,6 +446,8 @@ dm_status dm_scale(dm_ctx* c, const uint32_t* add, uint32_t n_add, const uint32_
     if (c->n_live - n_rm + n_add == 0)
         return fail(c, DM_EINVAL, "dm_scale: no instance would remain");
     DeviceGuard g(c->device);
+    if (hipError_t je = join_selection(c); je != hipSuccess)
+        return hip_fail(c, je, "dm_scale");
     std::vector<uint8_t> live = c->live;
     for (uint32_t i = 0; i < S; i++)
         live[i] = (live[i] && !fr[i]) || fa[i];
@@ -451,14 +484,16 @@ dm_status dm_set_timing(dm_ctx* c, int on)
     if (!c)
         return DM_EINVAL;
     DeviceGuard g(c->device);
-    if (on && !c->ev[0]) {
-        for (auto& ev : c->ev) {
+    if (on && c->tev.empty()) {
+        c->tev.assign(dm_ctx::kTimingRing * 5, nullptr);
+        for (auto& ev : c->tev) {
             hipError_t e = hipEventCreate(&ev);
             if (e != hipSuccess)
                 return hip_fail(c, e, "dm_set_timing");
         }
     }
     c->timing = on != 0;
+    c->tcount = 0;
     return DM_OK;
 }
 
@@ -468,19 +503,52 @@ dm_status dm_route_stage_ms(dm_ctx* c, float* ms, int n)
         return DM_EINVAL;
     if (!ms || n < 1)
         return fail(c, DM_EINVAL, "dm_route_stage_ms: bad output");
-    if (!c->timing || !c->ev[0])
-        return fail(c, DM_ESTATE, "dm_route_stage_ms: timing is off");
+    if (!c->timing || c->tev.empty() || c->tcount == 0)
+        return fail(c, DM_ESTATE, "dm_route_stage_ms: timing is off or no batch was timed");
     DeviceGuard g(c->device);
-    hipError_t e = hipEventSynchronize(c->ev[4]);
-    float t[4] = {0, 0, 0, 0};
-    if (e == hipSuccess) e = hipEventElapsedTime(&t[0], c->ev[1], c->ev[2]);
-    if (e == hipSuccess) e = hipEventElapsedTime(&t[1], c->ev[2], c->ev[3]);
-    if (e == hipSuccess) e = hipEventElapsedTime(&t[2], c->ev[3], c->ev[4]);
-    if (e == hipSuccess) e = hipEventElapsedTime(&t[3], c->ev[0], c->ev[1]);
+    const uint64_t R = dm_ctx::kTimingRing;
+    const uint64_t nrec = c->tcount < R ? c->tcount : R;
+    // the last batch's selection ends after every earlier recorded event
+    hipError_t e = hipEventSynchronize(c->tev[((c->tcount - 1) % R) * 5 + 4]);
+    double t[4] = {0, 0, 0, 0};
+    for (uint64_t b = c->tcount - nrec; b < c->tcount && e == hipSuccess; b++) {
+        hipEvent_t* ev = &c->tev[(b % R) * 5];
+        float x[4] = {0, 0, 0, 0};
+        if (e == hipSuccess) e = hipEventElapsedTime(&x[0], ev[1], ev[2]);
+        if (e == hipSuccess) e = hipEventElapsedTime(&x[1], ev[2], ev[3]);
+        if (e == hipSuccess) e = hipEventElapsedTime(&x[2], ev[3], ev[4]);
+        if (e == hipSuccess) e = hipEventElapsedTime(&x[3], ev[0], ev[1]);
+        for (int k = 0; k < 4; k++)
+            t[k] += x[k];
+    }
     if (e != hipSuccess)
         return hip_fail(c, e, "dm_route_stage_ms");
     for (int k = 0; k < n && k < 4; k++)
-        ms[k] = t[k];
+        ms[k] = (float)(t[k] / (double)nrec);
+    return DM_OK;
+}
+
+dm_status dm_set_pipelining(dm_ctx* c, int on)
+{
+    if (!c)
+        return DM_EINVAL;
+    DeviceGuard g(c->device);
+    hipError_t e = hipSuccess;
+    if (on && !c->sel_stream) {
+        e = hipStreamCreateWithFlags(&c->sel_stream, hipStreamNonBlocking);
+        if (e == hipSuccess)
+            e = hipEventCreateWithFlags(&c->probe_done, hipEventDisableTiming);
+        if (e == hipSuccess)
+            e = hipEventCreateWithFlags(&c->sel_done, hipEventDisableTiming);
+        if (e != hipSuccess)
+            return hip_fail(c, e, "dm_set_pipelining");
+    }
+    if (!on && c->pipelined) {
+        // later work on the context's stream must follow the last selection
+        if ((e = join_selection(c)) != hipSuccess)
+            return hip_fail(c, e, "dm_set_pipelining");
+    }
+    c->pipelined = on != 0;
     return DM_OK;
 }
 
@@ -489,6 +557,8 @@ dm_status dm_sync(dm_ctx* c)
     if (!c)
         return DM_EINVAL;
     DeviceGuard g(c->device);
+    if (hipError_t je = join_selection(c); je != hipSuccess)
+        return hip_fail(c, je, "dm_sync");
     hipError_t e = hipStreamSynchronize(c->stream);
     uint32_t st = 0;
     if (e == hipSuccess)

@@ -93,9 +93,19 @@ struct dm_ctx {
     dm::Scratch scratch[dm::kScratchSlots];
     uint32_t shift_div = 0;        // log2(queue_div)
 
-    // stage timing of dm_route_batch (events recorded only when enabled)
+    // stage timing of dm_route_batch: one set of 5 events per batch, in a
+    // ring (recorded only when enabled)
+    static constexpr int kTimingRing = 64;
     bool timing = false;
-    hipEvent_t ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+    std::vector<hipEvent_t> tev;  // [kTimingRing * 5]
+    uint64_t tcount = 0;          // batches recorded since timing was enabled
+
+    // pipelined routing: selection runs on its own stream, after the probe
+    // stage of its batch and the selection of the previous batch
+    bool pipelined = false;
+    hipStream_t sel_stream = nullptr;
+    hipEvent_t probe_done = nullptr;  // main stream: probe stage of the last batch
+    hipEvent_t sel_done = nullptr;    // selection stream: the last selection
 };
 
 namespace dm {
@@ -153,10 +163,14 @@ hipError_t hash_blocks(dm_ctx* c, const int32_t* tokens, const int64_t* offsets,
 hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64_t* hkeys,
                         const uint64_t* bstart, uint32_t* cand, uint32_t* match, uint8_t* flags);
 
-// dm_select.hip: SLO-aware choice in request order; chosen, ttft_us and
-// flags bits 0-2 written, loads updated.
-hipError_t select_batch(dm_ctx* c, const int64_t* offsets, uint64_t n, const dm_route_out* out,
-                        int64_t* loads);
+// dm_select.hip: SLO-aware choice in request order on stream st; chosen,
+// ttft_us and flags bits 0-2 written, loads updated.
+hipError_t select_batch(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint64_t n,
+                        const dm_route_out* out, int64_t* loads);
+
+// dm_api.hip: with pipelining on, make the context's stream wait for the
+// last selection (every call except dm_route_batch starts with this).
+hipError_t join_selection(dm_ctx* c);
 
 // dm_route.hip: the whole batch, stage by stage.
 hipError_t route(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,

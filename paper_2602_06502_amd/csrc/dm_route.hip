@@ -8,7 +8,10 @@
 //   select_batch   SLO-aware choice in request order, loads updated
 //                  (dm_select.hip).
 // With timing on, events between the stages give the per-stage times that
-// dm_route_stage_ms reports.
+// dm_route_stage_ms reports.  With pipelining on, the selection stage runs
+// on the context's selection stream: it waits for this batch's probe stage
+// (an event) and, being on one stream, for the previous batch's selection,
+// so the next batch's hashing and probing overlap it.
 #include "dm_internal.h"
 
 namespace dm {
@@ -23,7 +26,13 @@ hipError_t route(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint6
 {
     hipError_t e = hipSuccess;
     hipStream_t st = c->stream;
-    if (c->timing && (e = hipEventRecord(c->ev[0], st)) != hipSuccess)
+    hipStream_t ss = c->pipelined ? c->sel_stream : st;
+    hipEvent_t* ev = nullptr;
+    if (c->timing) {
+        ev = &c->tev[(c->tcount % dm_ctx::kTimingRing) * 5];
+        c->tcount++;
+    }
+    if (ev && (e = hipEventRecord(ev[0], st)) != hipSuccess)
         return e;
     uint64_t* bstart = static_cast<uint64_t*>(scratch_get(c, 0, (n + 1) * sizeof(uint64_t), &e));
     if (!bstart)
@@ -42,21 +51,28 @@ hipError_t route(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint6
         if (!hkeys)
             return e;
     }
-    if (c->timing && (e = hipEventRecord(c->ev[1], st)) != hipSuccess)
+    if (ev && (e = hipEventRecord(ev[1], st)) != hipSuccess)
         return e;
     if ((e = hash_blocks(c, tokens, offsets, n, bstart, hkeys, out->key)) != hipSuccess)
         return e;
-    if (c->timing && (e = hipEventRecord(c->ev[2], st)) != hipSuccess)
+    if (ev && (e = hipEventRecord(ev[2], st)) != hipSuccess)
         return e;
     if ((e = lookup_probe(c, n, out->key, hkeys, bstart, out->cand, out->match, out->flags)) !=
         hipSuccess)
         return e;
-    if (c->timing && (e = hipEventRecord(c->ev[3], st)) != hipSuccess)
+    if (ev && (e = hipEventRecord(ev[3], st)) != hipSuccess)
         return e;
-    if ((e = select_batch(c, offsets, n, out, loads)) != hipSuccess)
+    if (c->pipelined) {
+        if ((e = hipEventRecord(c->probe_done, st)) != hipSuccess ||
+            (e = hipStreamWaitEvent(ss, c->probe_done, 0)) != hipSuccess)
+            return e;
+    }
+    if ((e = select_batch(c, ss, offsets, n, out, loads)) != hipSuccess)
         return e;
-    if (c->timing)
-        e = hipEventRecord(c->ev[4], st);
+    if (c->pipelined && (e = hipEventRecord(c->sel_done, ss)) != hipSuccess)
+        return e;
+    if (ev)
+        e = hipEventRecord(ev[4], ss);
     return e;
 }
 

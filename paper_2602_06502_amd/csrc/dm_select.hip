@@ -225,7 +225,8 @@ struct SelPack {
     int32_t th;   // take a iff L_a <= max(th, L_o), relative loads
 };
 
-// plan[0] = 1 for the 64-bit path; plan[1] = 1 for the 32-bit path.
+// plan[0] = 1 for the serial path; plan[1] = 1 for the windowed path, whose
+// loads are 64-bit when plan[2] = 1.
 // base[0] = smallest live load; grow[d] bounds how much live instance d's
 // load can grow in this batch (the larger uncached count of every request
 // that has it as a candidate).
@@ -311,8 +312,11 @@ __global__ __launch_bounds__(256) void sel_prep_kernel(
         atomicOr(&grow[kMaxSlots], 1ull);
 }
 
-// Fast path iff at most 256 instances are live and every live load stays
-// below base + 2^31 - 1 whatever the decisions.
+// Windowed path iff at most 256 instances are live and every record's
+// uncached counts fit 32 bits (plan[1]); its loads are relative to the
+// smallest live load, in 32 bits when every live load stays below base +
+// 2^31 - 1 whatever the decisions, else in 64 bits (plan[2]) as long as
+// they stay below base + 2^62.  Otherwise the serial path (plan[0]).
 __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict__ loads,
                                                        const uint32_t* __restrict__ live_ids,
                                                        uint32_t n_live,
@@ -320,19 +324,26 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
                                                        const unsigned long long* __restrict__ grow,
                                                        uint32_t* __restrict__ plan)
 {
-    __shared__ int ok_all;
-    if (threadIdx.x == 0)
+    __shared__ int ok_all, narrow;
+    if (threadIdx.x == 0) {
         ok_all = n_live <= kFastMaxLive && grow[kMaxSlots] == 0;
+        narrow = 1;
+    }
     __syncthreads();
     for (uint32_t k = threadIdx.x; k < n_live && k < kFastMaxLive; k += blockDim.x) {
-        const unsigned long long span = (unsigned long long)(loads[live_ids[k]] - base[0]);
+        // loads - base cannot wrap in unsigned arithmetic: base is the minimum
+        const unsigned long long span = (unsigned long long)loads[live_ids[k]] -
+                                        (unsigned long long)base[0];
         if (span >= (1ull << 30) || grow[k] >= (1ull << 30))
+            atomicAnd(&narrow, 0);
+        if (span >= (1ull << 62) || grow[k] >= (1ull << 62))
             atomicAnd(&ok_all, 0);
     }
     __syncthreads();
     if (threadIdx.x == 0) {
         plan[0] = ok_all ? 0 : 1;
         plan[1] = ok_all ? 1 : 0;
+        plan[2] = ok_all && !narrow ? 1 : 0;
     }
 }
 
@@ -383,22 +394,31 @@ __global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(
         rec[r].w = (w & 0x1000FFFFu) | (uint32_t)(lv - 1) << 16 | (uint32_t)(mx - 1) << 22;
 }
 
-// Walks the windows in order; see the file comment.  rec holds one padding
-// window past the last so that the prefetch stays in bounds; lpre receives
-// the pre-update loads (L_c1, L_c2) of every request (padded to whole
-// windows).
+// Walks the windows in order; see the file comment.  T is the load type:
+// int32_t or int64_t relative loads (plan[2] selects int64_t).  rec holds one
+// padding window past the last so that the prefetch stays in bounds; lpre
+// receives the pre-update loads (L_c1, L_c2) of every request, relative to
+// the base (padded to whole windows).
+template <typename T>
 __global__ __launch_bounds__(kWave) void select_fast_kernel(
     const SelPack* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ live_ids,
     uint32_t n_live, int64_t* __restrict__ loads, const uint32_t* __restrict__ plan,
-    const int64_t* __restrict__ base, int2* __restrict__ lpre)
+    const int64_t* __restrict__ base, longlong2* __restrict__ lpre, int64_t tbase, int64_t per,
+    uint32_t qshift, int64_t slo)
 {
-    if (!plan[1])
+    constexpr bool wide = sizeof(T) == 8;
+    // Claim the whole register file of this wave's SIMD (256 + 256
+    // registers), so that no wave of another kernel shares its issue slots:
+    // this single wave is the serial critical path of a batch, and with
+    // pipelining the next batch's kernels run beside it.
+    asm volatile("" ::: "v255", "a255");
+    if (!plan[1] || (plan[2] != 0) != wide)
         return;
-    __shared__ int32_t L[kFastMaxLive + kWave];  // loads, then one spare slot per lane
+    __shared__ T L[kFastMaxLive + kWave];  // loads, then one spare slot per lane
     const int lane = lane_id();
     const int64_t b0 = base[0];
     for (uint32_t d = lane; d < kFastMaxLive + kWave; d += kWave)
-        L[d] = d < n_live ? (int32_t)(loads[live_ids[d]] - b0) : 0;
+        L[d] = d < n_live ? (T)(loads[live_ids[d]] - b0) : (T)0;
     __syncthreads();
     const uint64_t nw = (n + kWave - 1) / kWave;
     SelPack cur = rec[lane];
@@ -408,12 +428,21 @@ __global__ __launch_bounds__(kWave) void select_fast_kernel(
         const uint32_t a = cur.w & 0xFF, o = (cur.w >> 8) & 0xFF;
         const uint32_t mylv = valid ? (cur.w >> 16) & 63 : 64;
         const uint32_t depth = __builtin_amdgcn_readfirstlane((cur.w >> 22) & 63) + 1;
+        const T ua = (T)cur.ua, uo = (T)cur.uo;
+        T th;
+        if (wide) {
+            // exact bound: L_a < (slo - tbase - per u_a + 1) 2^q (th = -2^31 marks equal matches)
+            th = cur.th == INT32_MIN
+                     ? (T)INT64_MIN
+                     : (T)((slo - tbase - per * (int64_t)cur.ua + 1) * ((int64_t)1 << qshift) - 1 - b0);
+        } else {
+            th = (T)cur.th;
+        }
         // Every lane reads and writes at every depth, without branches; a lane
         // not at the current depth writes its own spare slot.
-        int32_t La = 0, Lo = 0;
-        const int32_t ua = (int32_t)cur.ua, uo = (int32_t)cur.uo, th = cur.th;
+        T La = 0, Lo = 0;
         for (uint32_t l = 0; l < depth; l++) {
-            const int32_t xa = L[a], xo = L[o];
+            const T xa = L[a], xo = L[o];
             const bool act = mylv == l;
             const bool take_a = xa <= std::max(th, xo);
             const uint32_t dst = act ? (take_a ? a : o) : kFastMaxLive + lane;
@@ -422,17 +451,17 @@ __global__ __launch_bounds__(kWave) void select_fast_kernel(
             Lo = act ? xo : Lo;
         }
         const bool flip = (cur.w >> 28) & 1;
-        lpre[w * kWave + lane] = flip ? make_int2(Lo, La) : make_int2(La, Lo);
+        lpre[w * kWave + lane] = flip ? make_longlong2(Lo, La) : make_longlong2(La, Lo);
         cur = nxt;
     }
     __syncthreads();
     for (uint32_t d = lane; d < n_live && d < kFastMaxLive; d += kWave)
-        loads[live_ids[d]] = b0 + L[d];
+        loads[live_ids[d]] = b0 + (int64_t)L[d];
 }
 
 __global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, uint32_t bshift,
                                const uint32_t* __restrict__ cand, const uint32_t* __restrict__ match,
-                               const int2* __restrict__ lpre, const int64_t* __restrict__ base,
+                               const longlong2* __restrict__ lpre, const int64_t* __restrict__ base,
                                const uint32_t* __restrict__ plan, uint8_t* __restrict__ flags,
                                uint32_t* __restrict__ chosen, int64_t* __restrict__ ttft,
                                int64_t tbase, int64_t per, uint32_t qshift, int64_t slo)
@@ -443,17 +472,17 @@ __global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, 
     for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
          r += (uint64_t)gridDim.x * blockDim.x) {
         SelRec s = load_rec(offsets, n, r, true, bshift, cand, match, tbase, per, qshift, slo);
-        const int2 lp = lpre[r];
+        const longlong2 lp = lpre[r];
         store_out(s, r, b0 + lp.x, b0 + lp.y, flags, chosen, ttft, tbase, per, qshift, slo);
     }
 }
 
 template <int R>
-void launch_select(dm_ctx* c, const int64_t* offsets, uint64_t n, uint32_t bshift,
+void launch_select(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint64_t n, uint32_t bshift,
                    const dm_route_out* out, int64_t* loads, const uint32_t* plan)
 {
     const dm_config& k = c->cfg;
-    select_kernel<R><<<1, kWave, 0, c->stream>>>(offsets, n, bshift, out->cand, out->match,
+    select_kernel<R><<<1, kWave, 0, st>>>(offsets, n, bshift, out->cand, out->match,
                                                  out->flags, out->chosen, out->ttft_us, loads,
                                                  k.max_slots, k.ttft_base_us, k.ttft_per_token_us,
                                                  c->shift_div, k.slo_us, plan);
@@ -461,11 +490,10 @@ void launch_select(dm_ctx* c, const int64_t* offsets, uint64_t n, uint32_t bshif
 
 }  // namespace
 
-hipError_t select_batch(dm_ctx* c, const int64_t* offsets, uint64_t n, const dm_route_out* out,
-                        int64_t* loads)
+hipError_t select_batch(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint64_t n,
+                        const dm_route_out* out, int64_t* loads)
 {
     hipError_t e = hipSuccess;
-    hipStream_t st = c->stream;
     uint32_t bshift = 0;
     while ((1u << bshift) < c->cfg.block_size)
         bshift++;
@@ -474,14 +502,14 @@ hipError_t select_batch(dm_ctx* c, const int64_t* offsets, uint64_t n, const dm_
     // work arrays: records (one padding window), pre-update loads, base/plan words
     const uint64_t nw = (n + kWave - 1) / kWave;
     const uint64_t nrec = (nw + 1) * kWave;
-    const size_t rec_bytes = nrec * sizeof(SelPack), lpre_bytes = nw * kWave * sizeof(int2);
+    const size_t rec_bytes = nrec * sizeof(SelPack), lpre_bytes = nw * kWave * sizeof(longlong2);
     const size_t tail_bytes = 256 + (kMaxSlots + 1) * sizeof(unsigned long long);
     uint8_t* sw = static_cast<uint8_t*>(
         scratch_get(c, kSelSlot, rec_bytes + lpre_bytes + tail_bytes + 256, &e));
     if (!sw)
         return e;
     SelPack* rec = reinterpret_cast<SelPack*>(sw);
-    int2* lpre = reinterpret_cast<int2*>(sw + rec_bytes);
+    longlong2* lpre = reinterpret_cast<longlong2*>(sw + rec_bytes);
     uint8_t* tail = sw + ((rec_bytes + lpre_bytes + 255) & ~size_t(255));
     int64_t* base = reinterpret_cast<int64_t*>(tail);
     uint32_t* plan = reinterpret_cast<uint32_t*>(tail + 128);
@@ -496,18 +524,23 @@ hipError_t select_batch(dm_ctx* c, const int64_t* offsets, uint64_t n, const dm_
     if (lgrid > 0x7FFFFFFFull)
         return hipErrorInvalidValue;
     sel_level_kernel<<<(uint32_t)lgrid, kLevelWaves * kWave, 0, st>>>(rec, n, plan);
-    select_fast_kernel<<<1, kWave, 0, st>>>(rec, n, c->d_live_ids, NL, loads, plan, base, lpre);
+    select_fast_kernel<int32_t><<<1, kWave, 0, st>>>(rec, n, c->d_live_ids, NL, loads, plan, base,
+                                                     lpre, k.ttft_base_us, k.ttft_per_token_us,
+                                                     c->shift_div, k.slo_us);
+    select_fast_kernel<int64_t><<<1, kWave, 0, st>>>(rec, n, c->d_live_ids, NL, loads, plan, base,
+                                                     lpre, k.ttft_base_us, k.ttft_per_token_us,
+                                                     c->shift_div, k.slo_us);
     sel_out_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(
         offsets, n, bshift, out->cand, out->match, lpre, base, plan, out->flags, out->chosen,
         out->ttft_us, k.ttft_base_us, k.ttft_per_token_us, c->shift_div, k.slo_us);
     if (S <= 64)
-        launch_select<1>(c, offsets, n, bshift, out, loads, plan);
+        launch_select<1>(c, st, offsets, n, bshift, out, loads, plan);
     else if (S <= 128)
-        launch_select<2>(c, offsets, n, bshift, out, loads, plan);
+        launch_select<2>(c, st, offsets, n, bshift, out, loads, plan);
     else if (S <= 192)
-        launch_select<3>(c, offsets, n, bshift, out, loads, plan);
+        launch_select<3>(c, st, offsets, n, bshift, out, loads, plan);
     else if (S <= 256)
-        launch_select<4>(c, offsets, n, bshift, out, loads, plan);
+        launch_select<4>(c, st, offsets, n, bshift, out, loads, plan);
     else
         select_lds_kernel<<<1, kWave, 0, st>>>(offsets, n, bshift, out->cand, out->match,
                                                out->flags, out->chosen, out->ttft_us, loads, S,

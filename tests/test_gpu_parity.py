@@ -128,14 +128,15 @@ def _pair_with_loads(wl, L0):
     return r
 
 
-@pytest.mark.parametrize("n_inst", [8, 150, 200])
-def test_selection_wide_loads_parity(n_inst):
-    """Loads spread beyond 2^30 force the exact 64-bit serial selection."""
+@pytest.mark.parametrize("n_inst,top", [(8, 0), (150, 0), (200, 0), (8, 1), (150, 1)])
+def test_selection_wide_loads_parity(n_inst, top):
+    """Loads spread beyond 2^30 take the windowed selection on 64-bit loads;
+    a spread beyond 2^62 (top=1) takes the serial 64-bit selection."""
     wl = workloads.small_random(31, n_inst, 3, 16, 700, slo_us=6_000_000_000)
     L0 = workloads.initial_loads(wl, wl.route.max_slots)
     L0[::3] += 1 << 40
-    L0[1] = (1 << 62) - (1 << 50)
-    _say("wide loads", n_inst)
+    L0[1] = (1 << 62) - (1 << 50) if not top else (1 << 62) + (1 << 50)
+    _say("wide loads", n_inst, top)
     r = _pair_with_loads(wl, L0)
     assert (r["flags"] & 1).sum() + (r["flags"] & 4).sum() > 0
 
@@ -508,3 +509,56 @@ def test_determinism_repeat():
                                                      gh.to_dev(off, eng.device), Ld).items()})
     for k in outs[0]:
         assert np.array_equal(outs[0][k], outs[1][k])
+
+
+# ---------------------------------------------------------------------------
+# Pipelined batches
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("slo_us", [400_000, 20_000])
+def test_pipelined_batches_parity(slo_us):
+    """Three consecutive batches routed with pipelining (each batch's
+    selection overlapping the next batch's hashing and probing), one loads
+    array carried through; the oracle routes the same batches one after the
+    other.  Then an index change after the batches must be ordered after
+    their selections."""
+    wl = workloads.tiny(slo_us=slo_us)
+    gh = _h()
+    eng = gh.engine_for(wl)
+    o = oh.oracle_for(wl)
+    gh.prefill_from_prior(eng, wl)
+    oh.prefill_from_prior(o, wl)
+    tok, off = workloads.prompts(wl, wl.n_req)
+    cuts = [0, 300, 301, 1024]  # ragged batches, one of a single request
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    dev = eng.device
+    Ld = gh.to_dev(L0, dev)
+    eng.set_pipelining(True)
+    eng.set_timing(True)
+    outs, refs = [], []
+    Lo = L0
+    for lo, hi in zip(cuts[:-1], cuts[1:]):
+        t = tok[off[lo]:off[hi]]
+        f = off[lo:hi + 1] - off[lo]
+        outs.append(eng.route(gh.to_dev(t, dev), gh.to_dev(f, dev), Ld, block_keys=True))
+        r = o.route(t, f, Lo, block_keys=True)
+        refs.append(r)
+        Lo = r["loads"]
+    eng.sync()
+    ms = eng.stage_ms()
+    assert all(x >= 0 for x in ms)
+    for g, r, (lo, hi) in zip(outs, refs, zip(cuts[:-1], cuts[1:])):
+        compare_route(g, r, hi - lo, with_bk=True)
+    assert np.array_equal(cpu(Ld), Lo)
+    # a later call is ordered after the last selection
+    eng.index_clear(0)
+    assert eng.index_size(0) == 0
+    eng.set_pipelining(False)
+    t = tok[off[0]:off[300]]
+    f = off[0:301] - off[0]
+    g = eng.route(gh.to_dev(t, dev), gh.to_dev(f, dev), Ld)
+    eng.sync()
+    o.index_clear(0)
+    r = o.route(t, f, Lo)
+    compare_route(g, r, 300)
+    assert np.array_equal(cpu(Ld), r["loads"])

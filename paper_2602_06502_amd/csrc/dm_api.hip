@@ -34,10 +34,12 @@ void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e)
         bytes = 256;
     if (s.bytes >= bytes)
         return s.p;
-    // Work already queued (on either stream) may still use the old buffer.
+    // Work already queued (on any of the context's streams) may still use
+    // the old buffer.
     *e = hipStreamSynchronize(c->stream);
-    if (*e == hipSuccess && c->sel_stream)
-        *e = hipStreamSynchronize(c->sel_stream);
+    for (hipStream_t s : {c->work_stream, c->sel_stream, c->out_stream})
+        if (*e == hipSuccess && s)
+            *e = hipStreamSynchronize(s);
     if (*e != hipSuccess)
         return nullptr;
     size_t nb = std::max(bytes, s.bytes * 2);
@@ -57,9 +59,9 @@ void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e)
 
 hipError_t join_selection(dm_ctx* c)
 {
-    if (!c->pipelined || !c->sel_done)
+    if (!c->pipelined || c->batches == 0)
         return hipSuccess;
-    return hipStreamWaitEvent(c->stream, c->sel_done, 0);
+    return hipStreamWaitEvent(c->stream, c->out_done[(c->batches - 1) & 1], 0);
 }
 
 }  // namespace dm
@@ -225,8 +227,9 @@ void dm_destroy(dm_ctx* c)
         return;
     DeviceGuard g(c->device);
     (void)hipStreamSynchronize(c->stream);
-    if (c->sel_stream)
-        (void)hipStreamSynchronize(c->sel_stream);
+    for (hipStream_t s : {c->work_stream, c->sel_stream, c->out_stream})
+        if (s)
+            (void)hipStreamSynchronize(s);
     for (auto& b : c->ring)
         for (auto& r : b)
             free_ring(r);
@@ -235,12 +238,12 @@ void dm_destroy(dm_ctx* c)
     for (auto& ev : c->tev)
         if (ev)
             (void)hipEventDestroy(ev);
-    if (c->probe_done)
-        (void)hipEventDestroy(c->probe_done);
-    if (c->sel_done)
-        (void)hipEventDestroy(c->sel_done);
-    if (c->sel_stream)
-        (void)hipStreamDestroy(c->sel_stream);
+    for (hipEvent_t ev : {c->in_ready, c->prep_done, c->sel_done, c->out_done[0], c->out_done[1]})
+        if (ev)
+            (void)hipEventDestroy(ev);
+    for (hipStream_t s : {c->work_stream, c->sel_stream, c->out_stream})
+        if (s)
+            (void)hipStreamDestroy(s);
     (void)hipFree(c->d_hp);
     (void)hipFree(c->d_next_live);
     (void)hipFree(c->d_live_ids);
@@ -528,27 +531,53 @@ dm_status dm_route_stage_ms(dm_ctx* c, float* ms, int n)
     return DM_OK;
 }
 
+// Streams of pipelined routing: the serial selection gets one compute unit
+// of its own and the work and output streams all the others, so that the
+// next batches' kernels never share the selection's unit.  Without CU
+// masks (a runtime that refuses them), plain streams are used.
+static hipError_t make_streams(dm_ctx* c)
+{
+    int cus = 0;
+    hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, c->device);
+    if (e != hipSuccess)
+        return e;
+    std::vector<uint32_t> one((cus + 31) / 32, 0u), rest((cus + 31) / 32, 0u);
+    for (int i = 0; i < cus; i++)
+        (i == 0 ? one : rest)[i / 32] |= 1u << (i % 32);
+    const bool masked = cus >= 2 &&
+        hipExtStreamCreateWithCUMask(&c->sel_stream, (uint32_t)one.size(), one.data()) == hipSuccess &&
+        hipExtStreamCreateWithCUMask(&c->work_stream, (uint32_t)rest.size(), rest.data()) == hipSuccess &&
+        hipExtStreamCreateWithCUMask(&c->out_stream, (uint32_t)rest.size(), rest.data()) == hipSuccess;
+    if (!masked) {
+        for (hipStream_t* s : {&c->work_stream, &c->sel_stream, &c->out_stream}) {
+            if (*s)
+                (void)hipStreamDestroy(*s);
+            *s = nullptr;
+        }
+        (void)hipGetLastError();
+        for (hipStream_t* s : {&c->work_stream, &c->sel_stream, &c->out_stream})
+            if (e == hipSuccess)
+                e = hipStreamCreateWithFlags(s, hipStreamNonBlocking);
+    }
+    for (hipEvent_t* ev : {&c->in_ready, &c->prep_done, &c->sel_done, &c->out_done[0], &c->out_done[1]})
+        if (e == hipSuccess)
+            e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+    return e;
+}
+
 dm_status dm_set_pipelining(dm_ctx* c, int on)
 {
     if (!c)
         return DM_EINVAL;
     DeviceGuard g(c->device);
     hipError_t e = hipSuccess;
-    if (on && !c->sel_stream) {
-        e = hipStreamCreateWithFlags(&c->sel_stream, hipStreamNonBlocking);
-        if (e == hipSuccess)
-            e = hipEventCreateWithFlags(&c->probe_done, hipEventDisableTiming);
-        if (e == hipSuccess)
-            e = hipEventCreateWithFlags(&c->sel_done, hipEventDisableTiming);
-        if (e != hipSuccess)
-            return hip_fail(c, e, "dm_set_pipelining");
-    }
-    if (!on && c->pipelined) {
-        // later work on the context's stream must follow the last selection
-        if ((e = join_selection(c)) != hipSuccess)
-            return hip_fail(c, e, "dm_set_pipelining");
-    }
+    if (on && !c->sel_stream && (e = make_streams(c)) != hipSuccess)
+        return hip_fail(c, e, "dm_set_pipelining");
+    // later work on the context's stream follows the last pipelined batch
+    if ((e = join_selection(c)) != hipSuccess)
+        return hip_fail(c, e, "dm_set_pipelining");
     c->pipelined = on != 0;
+    c->batches = 0;
     return DM_OK;
 }
 

@@ -100,12 +100,19 @@ struct dm_ctx {
     std::vector<hipEvent_t> tev;  // [kTimingRing * 5]
     uint64_t tcount = 0;          // batches recorded since timing was enabled
 
-    // pipelined routing: selection runs on its own stream, after the probe
-    // stage of its batch and the selection of the previous batch
+    // Pipelined routing.  Per batch: hashing, probing and record packing on
+    // work_stream (every compute unit but one), the serial selection on
+    // sel_stream (that one unit), the output epilogue on out_stream.  A
+    // batch's selection follows its packing and the previous selection; a
+    // batch's work first waits for the batch two back to finish, so at most
+    // two batches' outputs and work arrays (by batch parity) are in use.
     bool pipelined = false;
-    hipStream_t sel_stream = nullptr;
-    hipEvent_t probe_done = nullptr;  // main stream: probe stage of the last batch
-    hipEvent_t sel_done = nullptr;    // selection stream: the last selection
+    hipStream_t work_stream = nullptr, sel_stream = nullptr, out_stream = nullptr;
+    hipEvent_t in_ready = nullptr;                 // caller's stream: inputs of the batch
+    hipEvent_t prep_done = nullptr;                // work stream: records packed
+    hipEvent_t sel_done = nullptr;                 // selection stream: selection done
+    hipEvent_t out_done[2] = {nullptr, nullptr};   // output stream, by batch parity
+    uint64_t batches = 0;                          // pipelined batches routed
 };
 
 namespace dm {
@@ -163,8 +170,17 @@ hipError_t hash_blocks(dm_ctx* c, const int32_t* tokens, const int64_t* offsets,
 hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64_t* hkeys,
                         const uint64_t* bstart, uint32_t* cand, uint32_t* match, uint8_t* flags);
 
-// dm_select.hip: SLO-aware choice in request order on stream st; chosen,
-// ttft_us and flags bits 0-2 written, loads updated.
+// dm_select.hip: SLO-aware choice in request order; chosen, ttft_us and
+// flags bits 0-2 written, loads updated.  select_prepare packs the batch's
+// records (no loads needed); select_run takes the loads' base and plan, walks
+// the batch on ss and writes the outputs on os (after an event when os is
+// another stream).  par picks one of two work-array sets.  select_batch is
+// both on one stream.
+hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint64_t n,
+                          const dm_route_out* out, int par);
+hipError_t select_run(dm_ctx* c, hipStream_t ss, hipStream_t os, hipEvent_t sel_done,
+                      const int64_t* offsets, uint64_t n, const dm_route_out* out,
+                      int64_t* loads, int par);
 hipError_t select_batch(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint64_t n,
                         const dm_route_out* out, int64_t* loads);
 

@@ -8,10 +8,12 @@
 //   select_batch   SLO-aware choice in request order, loads updated
 //                  (dm_select.hip).
 // With timing on, events between the stages give the per-stage times that
-// dm_route_stage_ms reports.  With pipelining on, the selection stage runs
-// on the context's selection stream: it waits for this batch's probe stage
-// (an event) and, being on one stream, for the previous batch's selection,
-// so the next batch's hashing and probing overlap it.
+// dm_route_stage_ms reports.  With pipelining on, the batch's work runs on
+// the context's work stream (after the caller's stream and after the batch
+// two back), its serial selection on the selection stream (after the
+// batch's record packing and the previous selection), and the output
+// epilogue on the output stream; the next batch's hashing and probing thus
+// overlap this batch's selection.
 #include "dm_internal.h"
 
 namespace dm {
@@ -21,12 +23,35 @@ constexpr int kKeySlot = 4;  // block keys when the caller keeps none
 
 }  // namespace
 
+namespace {
+
+// Routes launches of the helper stages to another stream for one call.
+struct StreamSwap {
+    dm_ctx* c;
+    hipStream_t saved;
+    StreamSwap(dm_ctx* ctx, hipStream_t s) : c(ctx), saved(ctx->stream) { c->stream = s; }
+    ~StreamSwap() { c->stream = saved; }
+};
+
+}  // namespace
+
 hipError_t route(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
                  int64_t* loads, const dm_route_out* out)
 {
     hipError_t e = hipSuccess;
+    const bool pipe = c->pipelined;
+    const int par = pipe ? (int)(c->batches & 1) : 0;
+    if (pipe) {
+        if ((e = hipEventRecord(c->in_ready, c->stream)) != hipSuccess ||
+            (e = hipStreamWaitEvent(c->work_stream, c->in_ready, 0)) != hipSuccess)
+            return e;
+        // outputs and work arrays two batches back may be this batch's
+        if (c->batches >= 2 &&
+            (e = hipStreamWaitEvent(c->work_stream, c->out_done[par], 0)) != hipSuccess)
+            return e;
+    }
+    StreamSwap swap(c, pipe ? c->work_stream : c->stream);
     hipStream_t st = c->stream;
-    hipStream_t ss = c->pipelined ? c->sel_stream : st;
     hipEvent_t* ev = nullptr;
     if (c->timing) {
         ev = &c->tev[(c->tcount % dm_ctx::kTimingRing) * 5];
@@ -60,20 +85,25 @@ hipError_t route(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint6
     if ((e = lookup_probe(c, n, out->key, hkeys, bstart, out->cand, out->match, out->flags)) !=
         hipSuccess)
         return e;
+    if ((e = select_prepare(c, st, offsets, n, out, par)) != hipSuccess)
+        return e;
     if (ev && (e = hipEventRecord(ev[3], st)) != hipSuccess)
         return e;
-    if (c->pipelined) {
-        if ((e = hipEventRecord(c->probe_done, st)) != hipSuccess ||
-            (e = hipStreamWaitEvent(ss, c->probe_done, 0)) != hipSuccess)
+    if (!pipe) {
+        if ((e = select_run(c, st, st, nullptr, offsets, n, out, loads, 0)) != hipSuccess)
             return e;
+        return ev ? hipEventRecord(ev[4], st) : hipSuccess;
     }
-    if ((e = select_batch(c, ss, offsets, n, out, loads)) != hipSuccess)
+    if ((e = hipEventRecord(c->prep_done, st)) != hipSuccess ||
+        (e = hipStreamWaitEvent(c->sel_stream, c->prep_done, 0)) != hipSuccess)
         return e;
-    if (c->pipelined && (e = hipEventRecord(c->sel_done, ss)) != hipSuccess)
+    if ((e = select_run(c, c->sel_stream, c->out_stream, c->sel_done, offsets, n, out, loads,
+                        par)) != hipSuccess)
         return e;
-    if (ev)
-        e = hipEventRecord(ev[4], ss);
-    return e;
+    if ((e = hipEventRecord(c->out_done[par], c->out_stream)) != hipSuccess)
+        return e;
+    c->batches++;
+    return ev ? hipEventRecord(ev[4], c->out_stream) : hipSuccess;
 }
 
 }  // namespace dm

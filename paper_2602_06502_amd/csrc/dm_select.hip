@@ -240,7 +240,6 @@ __global__ __launch_bounds__(256) void sel_base_kernel(const int64_t* __restrict
     for (uint32_t k = threadIdx.x; k < n_live; k += blockDim.x) {
         const int64_t v = loads[live_ids[k]];
         mn = v < mn ? v : mn;
-        grow[k] = 0;
     }
     smin[threadIdx.x] = mn;
     __syncthreads();
@@ -249,20 +248,27 @@ __global__ __launch_bounds__(256) void sel_base_kernel(const int64_t* __restrict
             smin[threadIdx.x] = std::min(smin[threadIdx.x], smin[threadIdx.x + d]);
         __syncthreads();
     }
-    if (threadIdx.x == 0) {
+    if (threadIdx.x == 0)
         base[0] = smin[0];
-        grow[kMaxSlots] = 0;  // set if some record does not fit 32 bits
-    }
 }
 
 constexpr uint32_t kFastMaxLive = 256;
+constexpr int kPrefetch = 4;  // record windows in flight ahead of the walk
+
+// grow[0..n_live) and the bad-record word grow[kMaxSlots] start at zero.
+__global__ void sel_zero_kernel(unsigned long long* __restrict__ grow, uint32_t n_live)
+{
+    for (uint32_t k = threadIdx.x; k < n_live && k < kMaxSlots; k += blockDim.x)
+        grow[k] = 0;
+    if (threadIdx.x == 0)
+        grow[kMaxSlots] = 0;
+}
 
 __global__ __launch_bounds__(256) void sel_prep_kernel(
     const int64_t* __restrict__ offsets, uint64_t n, uint32_t bshift,
     const uint32_t* __restrict__ cand, const uint32_t* __restrict__ match,
-    const uint32_t* __restrict__ dense, uint32_t n_live, const int64_t* __restrict__ base,
-    int64_t tbase, int64_t per, uint32_t qshift, int64_t slo, SelPack* __restrict__ rec,
-    unsigned long long* __restrict__ grow)
+    const uint32_t* __restrict__ dense, uint32_t n_live, int64_t tbase, int64_t per,
+    uint32_t qshift, int64_t slo, SelPack* __restrict__ rec, unsigned long long* __restrict__ grow)
 {
     __shared__ unsigned long long sg[kFastMaxLive];
     const bool track = n_live <= kFastMaxLive;
@@ -270,7 +276,6 @@ __global__ __launch_bounds__(256) void sel_prep_kernel(
         for (uint32_t k = threadIdx.x; k < n_live; k += blockDim.x)
             sg[k] = 0;
     __syncthreads();
-    const int64_t b0 = base[0];
     unsigned long long bad = 0;
     for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
          r += (uint64_t)gridDim.x * blockDim.x) {
@@ -279,13 +284,14 @@ __global__ __launch_bounds__(256) void sel_prep_kernel(
         const int64_t u1 = len - ((int64_t)m1 << bshift), u2 = len - ((int64_t)m2 << bshift);
         const bool eq = m1 == m2, aff2 = m2 > m1;
         const uint32_t d1 = dense[cand[r]], d2 = dense[cand[n + r]];
-        // T_a <= slo  <=>  floor(L_a / 2^q) <= slo - base - per*u_a  <=>  L_a < th_abs;
-        // relative loads lie in [0, 2^31 - 1), so the bound is clamped to that range.
-        // Equal matches: take c1 iff L1 <= L2, i.e. th = -2^31.
+        // T_a <= slo  <=>  floor(L_a / 2^q) <= slo - tbase - per*u_a  <=>
+        // L_a < (slo - tbase - per*u_a + 1) 2^q, i.e. "take a iff L_a <=
+        // max(th, L_o)" with th one less.  The 32-bit walk uses absolute loads
+        // in [0, 2^31 - 1), so th is clamped to that range; equal matches:
+        // take c1 iff L1 <= L2, th = -2^31.
         int32_t th = INT32_MIN;
         if (!eq) {
-            const int64_t th_abs = (slo - tbase - per * (aff2 ? u2 : u1) + 1) * ((int64_t)1 << qshift);
-            int64_t t = th_abs - 1 - b0;
+            const int64_t t = (slo - tbase - per * (aff2 ? u2 : u1) + 1) * ((int64_t)1 << qshift) - 1;
             th = (int32_t)(t < -1 ? -1 : (t > INT32_MAX ? INT32_MAX : t));
         }
         SelPack p;
@@ -313,10 +319,11 @@ __global__ __launch_bounds__(256) void sel_prep_kernel(
 }
 
 // Windowed path iff at most 256 instances are live and every record's
-// uncached counts fit 32 bits (plan[1]); its loads are relative to the
-// smallest live load, in 32 bits when every live load stays below base +
-// 2^31 - 1 whatever the decisions, else in 64 bits (plan[2]) as long as
-// they stay below base + 2^62.  Otherwise the serial path (plan[0]).
+// uncached counts fit 32 bits (plan[1]).  Its loads are absolute 32-bit
+// values when every live load lies in [0, 2^30) and grows by less than 2^30
+// whatever the decisions; otherwise (plan[2]) 64-bit values relative to the
+// smallest live load, as long as they stay below it + 2^62.  Otherwise the
+// serial path (plan[0]).
 __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict__ loads,
                                                        const uint32_t* __restrict__ live_ids,
                                                        uint32_t n_live,
@@ -332,9 +339,9 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
     __syncthreads();
     for (uint32_t k = threadIdx.x; k < n_live && k < kFastMaxLive; k += blockDim.x) {
         // loads - base cannot wrap in unsigned arithmetic: base is the minimum
-        const unsigned long long span = (unsigned long long)loads[live_ids[k]] -
-                                        (unsigned long long)base[0];
-        if (span >= (1ull << 30) || grow[k] >= (1ull << 30))
+        const int64_t v = loads[live_ids[k]];
+        const unsigned long long span = (unsigned long long)v - (unsigned long long)base[0];
+        if (v < 0 || v >= (1ll << 30) || grow[k] >= (1ull << 30))
             atomicAnd(&narrow, 0);
         if (span >= (1ull << 62) || grow[k] >= (1ull << 62))
             atomicAnd(&ok_all, 0);
@@ -353,11 +360,9 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
 // requests of one depth touch pairwise distinct instances.
 constexpr int kLevelWaves = 4;
 
-__global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(
-    SelPack* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ plan)
+__global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(SelPack* __restrict__ rec,
+                                                                        uint64_t n)
 {
-    if (!plan[1])
-        return;
     __shared__ unsigned long long M[kLevelWaves][kFastMaxLive];
     const int lane = lane_id(), wv = threadIdx.x >> 6;
     unsigned long long* m = M[wv];
@@ -395,35 +400,25 @@ __global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(
 }
 
 // Walks the windows in order; see the file comment.  T is the load type:
-// int32_t or int64_t relative loads (plan[2] selects int64_t).  rec holds one
-// padding window past the last so that the prefetch stays in bounds; lpre
-// receives the pre-update loads (L_c1, L_c2) of every request, relative to
-// the base (padded to whole windows).
+// int32_t or int64_t relative loads.  rec holds 2 * kPrefetch padding
+// windows past the last and lpre kPrefetch, so that the unrolled walk and
+// its prefetch stay in bounds; lpre receives the pre-update loads (L_c1,
+// L_c2) of every request, relative to the base.
 template <typename T>
-__global__ __launch_bounds__(kWave) void select_fast_kernel(
-    const SelPack* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ live_ids,
-    uint32_t n_live, int64_t* __restrict__ loads, const uint32_t* __restrict__ plan,
-    const int64_t* __restrict__ base, longlong2* __restrict__ lpre, int64_t tbase, int64_t per,
-    uint32_t qshift, int64_t slo)
+__device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, uint64_t n,
+                                             const uint32_t* __restrict__ live_ids,
+                                             uint32_t n_live, int64_t* __restrict__ loads,
+                                             int64_t b0, longlong2* __restrict__ lpre,
+                                             int64_t tbase, int64_t per, uint32_t qshift,
+                                             int64_t slo, T* L)
 {
     constexpr bool wide = sizeof(T) == 8;
-    // Claim the whole register file of this wave's SIMD (256 + 256
-    // registers), so that no wave of another kernel shares its issue slots:
-    // this single wave is the serial critical path of a batch, and with
-    // pipelining the next batch's kernels run beside it.
-    asm volatile("" ::: "v255", "a255");
-    if (!plan[1] || (plan[2] != 0) != wide)
-        return;
-    __shared__ T L[kFastMaxLive + kWave];  // loads, then one spare slot per lane
     const int lane = lane_id();
-    const int64_t b0 = base[0];
     for (uint32_t d = lane; d < kFastMaxLive + kWave; d += kWave)
         L[d] = d < n_live ? (T)(loads[live_ids[d]] - b0) : (T)0;
     __syncthreads();
     const uint64_t nw = (n + kWave - 1) / kWave;
-    SelPack cur = rec[lane];
-    for (uint64_t w = 0; w < nw; w++) {
-        const SelPack nxt = rec[(w + 1) * kWave + lane];
+    auto window = [&](const SelPack& cur, uint64_t w) {
         const bool valid = w * kWave + lane < n;
         const uint32_t a = cur.w & 0xFF, o = (cur.w >> 8) & 0xFF;
         const uint32_t mylv = valid ? (cur.w >> 16) & 63 : 64;
@@ -431,7 +426,8 @@ __global__ __launch_bounds__(kWave) void select_fast_kernel(
         const T ua = (T)cur.ua, uo = (T)cur.uo;
         T th;
         if (wide) {
-            // exact bound: L_a < (slo - tbase - per u_a + 1) 2^q (th = -2^31 marks equal matches)
+            // the packed bound is clamped to 32 bits: recompute it exactly,
+            // relative to the base (equal matches: -inf)
             th = cur.th == INT32_MIN
                      ? (T)INT64_MIN
                      : (T)((slo - tbase - per * (int64_t)cur.ua + 1) * ((int64_t)1 << qshift) - 1 - b0);
@@ -452,11 +448,49 @@ __global__ __launch_bounds__(kWave) void select_fast_kernel(
         }
         const bool flip = (cur.w >> 28) & 1;
         lpre[w * kWave + lane] = flip ? make_longlong2(Lo, La) : make_longlong2(La, Lo);
-        cur = nxt;
+    };
+    // Records arrive kPrefetch windows ahead.  The loop is unrolled by
+    // kPrefetch so that each slot is used where it was loaded (no register
+    // moves, which would wait for every load in flight); windows past the
+    // last (all lanes invalid, padded records and outputs) change nothing.
+    SelPack q0 = rec[0 * kWave + lane], q1 = rec[1 * kWave + lane];
+    SelPack q2 = rec[2 * kWave + lane], q3 = rec[3 * kWave + lane];
+    for (uint64_t w = 0; w < nw; w += kPrefetch) {
+        window(q0, w);
+        q0 = rec[(w + 4) * kWave + lane];
+        window(q1, w + 1);
+        q1 = rec[(w + 5) * kWave + lane];
+        window(q2, w + 2);
+        q2 = rec[(w + 6) * kWave + lane];
+        window(q3, w + 3);
+        q3 = rec[(w + 7) * kWave + lane];
     }
     __syncthreads();
     for (uint32_t d = lane; d < n_live && d < kFastMaxLive; d += kWave)
         loads[live_ids[d]] = b0 + (int64_t)L[d];
+}
+
+// One wave: 32-bit relative loads unless plan[2] asks for 64-bit ones.
+__global__ __launch_bounds__(kWave) void select_fast_kernel(
+    const SelPack* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ live_ids,
+    uint32_t n_live, int64_t* __restrict__ loads, const uint32_t* __restrict__ plan,
+    const int64_t* __restrict__ base, longlong2* __restrict__ lpre, int64_t tbase, int64_t per,
+    uint32_t qshift, int64_t slo)
+{
+    // Claim the whole register file of this wave's SIMD (256 + 256
+    // registers), so that no wave of another kernel shares its issue slots:
+    // this single wave is the serial critical path of a batch, and with
+    // pipelining the next batch's kernels run beside it.
+    asm volatile("" ::: "v255", "a255");
+    if (!plan[1])
+        return;
+    __shared__ int64_t L[kFastMaxLive + kWave];  // loads, then one spare slot per lane
+    const int64_t b0 = plan[2] ? base[0] : 0;  // 32-bit walks use absolute loads
+    if (plan[2])
+        walk_windows<int64_t>(rec, n, live_ids, n_live, loads, b0, lpre, tbase, per, qshift, slo, L);
+    else
+        walk_windows<int32_t>(rec, n, live_ids, n_live, loads, b0, lpre, tbase, per, qshift, slo,
+                              reinterpret_cast<int32_t*>(L));
 }
 
 __global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, uint32_t bshift,
@@ -468,7 +502,7 @@ __global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, 
 {
     if (!plan[1])
         return;
-    const int64_t b0 = base[0];
+    const int64_t b0 = plan[2] ? base[0] : 0;
     for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
          r += (uint64_t)gridDim.x * blockDim.x) {
         SelRec s = load_rec(offsets, n, r, true, bshift, cand, match, tbase, per, qshift, slo);
@@ -488,65 +522,119 @@ void launch_select(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint64_t n
                                                  c->shift_div, k.slo_us, plan);
 }
 
+
 }  // namespace
+
+// Work arrays of one batch in flight: records (kPrefetch padding windows),
+// pre-update loads, base/plan words and growth bounds.  Two such sets live
+// in the selection slot, one per batch parity.
+struct SelBuf {
+    SelPack* rec;
+    longlong2* lpre;
+    int64_t* base;
+    uint32_t* plan;
+    unsigned long long* grow;
+};
+
+static hipError_t sel_buffers(dm_ctx* c, uint64_t n, int par, SelBuf* b)
+{
+    hipError_t e = hipSuccess;
+    const uint64_t nw = (n + kWave - 1) / kWave;
+    const uint64_t nrec = (nw + 2 * kPrefetch) * kWave;
+    const size_t rec_bytes = (nrec * sizeof(SelPack) + 255) & ~size_t(255);
+    const size_t lpre_bytes = ((nw + kPrefetch) * kWave * sizeof(longlong2) + 255) & ~size_t(255);
+    const size_t tail_bytes = 256 + (kMaxSlots + 1) * sizeof(unsigned long long);
+    const size_t one = (rec_bytes + lpre_bytes + tail_bytes + 255) & ~size_t(255);
+    uint8_t* sw = static_cast<uint8_t*>(scratch_get(c, kSelSlot, 2 * one, &e));
+    if (!sw)
+        return e;
+    sw += par * one;
+    b->rec = reinterpret_cast<SelPack*>(sw);
+    b->lpre = reinterpret_cast<longlong2*>(sw + rec_bytes);
+    uint8_t* tail = sw + rec_bytes + lpre_bytes;
+    b->base = reinterpret_cast<int64_t*>(tail);
+    b->plan = reinterpret_cast<uint32_t*>(tail + 128);
+    b->grow = reinterpret_cast<unsigned long long*>(tail + 256);
+    return hipSuccess;
+}
+
+static uint32_t block_shift(const dm_ctx* c)
+{
+    uint32_t bshift = 0;
+    while ((1u << bshift) < c->cfg.block_size)
+        bshift++;
+    return bshift;
+}
+
+hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint64_t n,
+                          const dm_route_out* out, int par)
+{
+    SelBuf b;
+    hipError_t e = sel_buffers(c, n, par, &b);
+    if (e != hipSuccess)
+        return e;
+    const uint64_t nw = (n + kWave - 1) / kWave;
+    const uint64_t lgrid = (nw + kLevelWaves - 1) / kLevelWaves;
+    if (lgrid > 0x7FFFFFFFull)
+        return hipErrorInvalidValue;
+    const uint32_t NL = c->n_live;
+    sel_zero_kernel<<<1, 256, 0, st>>>(b.grow, NL);
+    const dm_config& k = c->cfg;
+    sel_prep_kernel<<<grid_for(n, 256, 4096), 256, 0, st>>>(
+        offsets, n, block_shift(c), out->cand, out->match, c->d_dense, NL, k.ttft_base_us,
+        k.ttft_per_token_us, c->shift_div, k.slo_us, b.rec, b.grow);
+    sel_level_kernel<<<(uint32_t)lgrid, kLevelWaves * kWave, 0, st>>>(b.rec, n);
+    return hipGetLastError();
+}
+
+hipError_t select_run(dm_ctx* c, hipStream_t ss, hipStream_t os, hipEvent_t sel_done,
+                      const int64_t* offsets, uint64_t n, const dm_route_out* out,
+                      int64_t* loads, int par)
+{
+    SelBuf b;
+    hipError_t e = sel_buffers(c, n, par, &b);
+    if (e != hipSuccess)
+        return e;
+    const dm_config& k = c->cfg;
+    const uint32_t S = k.max_slots, NL = c->n_live, bshift = block_shift(c);
+    sel_base_kernel<<<1, 256, 0, ss>>>(loads, c->d_live_ids, NL, b.base, b.grow);
+    sel_plan_kernel<<<1, 256, 0, ss>>>(loads, c->d_live_ids, NL, b.base, b.grow, b.plan);
+    select_fast_kernel<<<1, kWave, 0, ss>>>(b.rec, n, c->d_live_ids, NL, loads, b.plan, b.base,
+                                            b.lpre, k.ttft_base_us, k.ttft_per_token_us,
+                                            c->shift_div, k.slo_us);
+    if (S <= 64)
+        launch_select<1>(c, ss, offsets, n, bshift, out, loads, b.plan);
+    else if (S <= 128)
+        launch_select<2>(c, ss, offsets, n, bshift, out, loads, b.plan);
+    else if (S <= 192)
+        launch_select<3>(c, ss, offsets, n, bshift, out, loads, b.plan);
+    else if (S <= 256)
+        launch_select<4>(c, ss, offsets, n, bshift, out, loads, b.plan);
+    else
+        select_lds_kernel<<<1, kWave, 0, ss>>>(offsets, n, bshift, out->cand, out->match,
+                                               out->flags, out->chosen, out->ttft_us, loads, S,
+                                               k.ttft_base_us, k.ttft_per_token_us, c->shift_div,
+                                               k.slo_us, b.plan);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    if (os != ss) {
+        if ((e = hipEventRecord(sel_done, ss)) != hipSuccess ||
+            (e = hipStreamWaitEvent(os, sel_done, 0)) != hipSuccess)
+            return e;
+    }
+    sel_out_kernel<<<grid_for(n, 256, 8192), 256, 0, os>>>(
+        offsets, n, bshift, out->cand, out->match, b.lpre, b.base, b.plan, out->flags, out->chosen,
+        out->ttft_us, k.ttft_base_us, k.ttft_per_token_us, c->shift_div, k.slo_us);
+    return hipGetLastError();
+}
 
 hipError_t select_batch(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint64_t n,
                         const dm_route_out* out, int64_t* loads)
 {
-    hipError_t e = hipSuccess;
-    uint32_t bshift = 0;
-    while ((1u << bshift) < c->cfg.block_size)
-        bshift++;
-    const uint32_t S = c->cfg.max_slots;
-    const dm_config& k = c->cfg;
-    // work arrays: records (one padding window), pre-update loads, base/plan words
-    const uint64_t nw = (n + kWave - 1) / kWave;
-    const uint64_t nrec = (nw + 1) * kWave;
-    const size_t rec_bytes = nrec * sizeof(SelPack), lpre_bytes = nw * kWave * sizeof(longlong2);
-    const size_t tail_bytes = 256 + (kMaxSlots + 1) * sizeof(unsigned long long);
-    uint8_t* sw = static_cast<uint8_t*>(
-        scratch_get(c, kSelSlot, rec_bytes + lpre_bytes + tail_bytes + 256, &e));
-    if (!sw)
-        return e;
-    SelPack* rec = reinterpret_cast<SelPack*>(sw);
-    longlong2* lpre = reinterpret_cast<longlong2*>(sw + rec_bytes);
-    uint8_t* tail = sw + ((rec_bytes + lpre_bytes + 255) & ~size_t(255));
-    int64_t* base = reinterpret_cast<int64_t*>(tail);
-    uint32_t* plan = reinterpret_cast<uint32_t*>(tail + 128);
-    unsigned long long* grow = reinterpret_cast<unsigned long long*>(tail + 256);
-    const uint32_t NL = c->n_live;
-    sel_base_kernel<<<1, 256, 0, st>>>(loads, c->d_live_ids, NL, base, grow);
-    sel_prep_kernel<<<grid_for(n, 256, 4096), 256, 0, st>>>(
-        offsets, n, bshift, out->cand, out->match, c->d_dense, NL, base, k.ttft_base_us,
-        k.ttft_per_token_us, c->shift_div, k.slo_us, rec, grow);
-    sel_plan_kernel<<<1, 256, 0, st>>>(loads, c->d_live_ids, NL, base, grow, plan);
-    const uint64_t lgrid = (nw + kLevelWaves - 1) / kLevelWaves;
-    if (lgrid > 0x7FFFFFFFull)
-        return hipErrorInvalidValue;
-    sel_level_kernel<<<(uint32_t)lgrid, kLevelWaves * kWave, 0, st>>>(rec, n, plan);
-    select_fast_kernel<int32_t><<<1, kWave, 0, st>>>(rec, n, c->d_live_ids, NL, loads, plan, base,
-                                                     lpre, k.ttft_base_us, k.ttft_per_token_us,
-                                                     c->shift_div, k.slo_us);
-    select_fast_kernel<int64_t><<<1, kWave, 0, st>>>(rec, n, c->d_live_ids, NL, loads, plan, base,
-                                                     lpre, k.ttft_base_us, k.ttft_per_token_us,
-                                                     c->shift_div, k.slo_us);
-    sel_out_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(
-        offsets, n, bshift, out->cand, out->match, lpre, base, plan, out->flags, out->chosen,
-        out->ttft_us, k.ttft_base_us, k.ttft_per_token_us, c->shift_div, k.slo_us);
-    if (S <= 64)
-        launch_select<1>(c, st, offsets, n, bshift, out, loads, plan);
-    else if (S <= 128)
-        launch_select<2>(c, st, offsets, n, bshift, out, loads, plan);
-    else if (S <= 192)
-        launch_select<3>(c, st, offsets, n, bshift, out, loads, plan);
-    else if (S <= 256)
-        launch_select<4>(c, st, offsets, n, bshift, out, loads, plan);
-    else
-        select_lds_kernel<<<1, kWave, 0, st>>>(offsets, n, bshift, out->cand, out->match,
-                                               out->flags, out->chosen, out->ttft_us, loads, S,
-                                               k.ttft_base_us, k.ttft_per_token_us, c->shift_div,
-                                               k.slo_us, plan);
-    return hipGetLastError();
+    hipError_t e = select_prepare(c, st, offsets, n, out, 0);
+    if (e == hipSuccess)
+        e = select_run(c, st, st, nullptr, offsets, n, out, loads, 0);
+    return e;
 }
 
 }  // namespace dm

@@ -404,6 +404,49 @@ __global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(SelPack*
 // windows past the last and lpre kPrefetch, so that the unrolled walk and
 // its prefetch stay in bounds; lpre receives the pre-update loads (L_c1,
 // L_c2) of every request, relative to the base.
+// Byte address of a shared-memory element within the workgroup's LDS.
+template <typename T>
+__device__ __forceinline__ uint32_t lds_addr(T* p)
+{
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) T*)p;
+}
+
+// One depth of the 32-bit walk for the lanes whose depth is K + (l - rel),
+// i.e. whose rel equals the inline constant K.  Reads (XA, XO) of this depth
+// into one register set; captures the previous depth's reads (XAP, XOP,
+// lane mask MP) into (La, Lo); M receives this depth's lane mask.  A lane on
+// the depth writes its chosen instance, the others their spare slot; the
+// reads of a depth precede its write in the LDS queue, and the write of one
+// depth precedes the reads of the next.  Uses (a4, o4, sp4, rel, th, ua, uo,
+// La, Lo) from the enclosing scope.
+#define DM_DEPTH_STEP(K, XA, XO, M, XAP, XOP, MP)                                             \
+    do {                                                                                     \
+        int32_t t1, t2, da, dz;                                                              \
+        asm volatile("ds_read_b32 %[xo], %[o4]\n\t"                                          \
+                     "ds_read_b32 %[xa], %[a4]\n\t"                                          \
+                     "v_cmp_eq_u32_e64 %[m], %[k], %[rel]\n\t"                               \
+                     "v_cndmask_b32_e64 %[La], %[La], %[xap], %[mp]\n\t"                     \
+                     "v_cndmask_b32_e64 %[Lo], %[Lo], %[xop], %[mp]\n\t"                     \
+                     "v_cndmask_b32_e64 %[da], %[sp], %[a4], %[m]\n\t"                       \
+                     "v_cndmask_b32_e64 %[dz], %[sp], %[o4], %[m]\n\t"                       \
+                     "s_waitcnt lgkmcnt(1)\n\t"                                              \
+                     "v_max_i32_e32 %[t1], %[th], %[xo]\n\t"                                 \
+                     "v_add_u32_e32 %[t2], %[xo], %[uo]\n\t"                                 \
+                     "s_waitcnt lgkmcnt(0)\n\t"                                              \
+                     "v_cmp_le_i32_e32 vcc, %[xa], %[t1]\n\t"                                \
+                     "v_add_u32_e32 %[t1], %[xa], %[ua]\n\t"                                 \
+                     "v_cndmask_b32_e32 %[t2], %[t2], %[t1], vcc\n\t"                        \
+                     "v_cndmask_b32_e32 %[t1], %[dz], %[da], vcc\n\t"                        \
+                     "ds_write_b32 %[t1], %[t2]"                                             \
+                     : [xa] "=&v"(XA), [xo] "=&v"(XO), [m] "=&s"(M), [La] "+v"(La),          \
+                       [Lo] "+v"(Lo), [t1] "=&v"(t1), [t2] "=&v"(t2), [da] "=&v"(da),        \
+                       [dz] "=&v"(dz)                                                        \
+                     : [a4] "v"(a4), [o4] "v"(o4), [sp] "v"(sp4), [k] "n"(K), [rel] "v"(rel), \
+                       [xap] "v"(XAP), [xop] "v"(XOP), [mp] "s"(MP), [th] "v"(th),           \
+                       [ua] "v"(ua), [uo] "v"(uo)                                            \
+                     : "vcc", "memory");                                                     \
+    } while (0)
+
 template <typename T>
 __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, uint64_t n,
                                              const uint32_t* __restrict__ live_ids,
@@ -434,21 +477,75 @@ __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, ui
         } else {
             th = (T)cur.th;
         }
-        // Every lane reads and writes at every depth, without branches; a lane
-        // not at the current depth writes its own spare slot.
         T La = 0, Lo = 0;
-        for (uint32_t l = 0; l < depth; l++) {
-            const T xa = L[a], xo = L[o];
-            const bool act = mylv == l;
-            const bool take_a = xa <= std::max(th, xo);
-            const uint32_t dst = act ? (take_a ? a : o) : kFastMaxLive + lane;
-            L[dst] = take_a ? xa + ua : xo + uo;
-            La = act ? xa : La;
-            Lo = act ? xo : Lo;
+        if constexpr (wide) {
+            // Every lane reads and writes at every depth, without branches; a
+            // lane not on the current depth writes its own spare slot.
+            for (uint32_t l = 0; l < depth; l++) {
+                const T xa = L[a], xo = L[o];
+                const bool act = mylv == l;
+                const bool take_a = xa <= std::max(th, xo);
+                const uint32_t dst = act ? (take_a ? a : o) : kFastMaxLive + lane;
+                L[dst] = take_a ? xa + ua : xo + uo;
+                La = act ? xa : La;
+                Lo = act ? xo : Lo;
+            }
+        } else {
+            // The same walk in hand-scheduled depth steps (DM_DEPTH_STEP): the
+            // ALU work of a step that does not wait for its reads runs in the
+            // shadow of the LDS round trip, so the serial chain per depth is
+            // the round trip plus six ALU steps.  Steps come in groups of 8,
+            // 4, 2 and 1 with the depth compared against an inline constant,
+            // and two register sets alternate between consecutive depths.
+            const uint32_t a4 = lds_addr(&L[a]), o4 = lds_addr(&L[o]);
+            const uint32_t sp4 = lds_addr(&L[kFastMaxLive + lane]);
+            int32_t xa0 = 0, xo0 = 0, xa1 = 0, xo1 = 0;
+            uint64_t m0 = 0, m1 = 0;
+            // the steps count LDS completions only: no scalar load is in flight
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            uint32_t l = 0;
+            for (; l + 8 <= depth; l += 8) {
+                const uint32_t rel = mylv - l;
+                DM_DEPTH_STEP(0, xa0, xo0, m0, xa1, xo1, m1);
+                DM_DEPTH_STEP(1, xa1, xo1, m1, xa0, xo0, m0);
+                DM_DEPTH_STEP(2, xa0, xo0, m0, xa1, xo1, m1);
+                DM_DEPTH_STEP(3, xa1, xo1, m1, xa0, xo0, m0);
+                DM_DEPTH_STEP(4, xa0, xo0, m0, xa1, xo1, m1);
+                DM_DEPTH_STEP(5, xa1, xo1, m1, xa0, xo0, m0);
+                DM_DEPTH_STEP(6, xa0, xo0, m0, xa1, xo1, m1);
+                DM_DEPTH_STEP(7, xa1, xo1, m1, xa0, xo0, m0);
+            }
+            if (l + 4 <= depth) {
+                const uint32_t rel = mylv - l;
+                DM_DEPTH_STEP(0, xa0, xo0, m0, xa1, xo1, m1);
+                DM_DEPTH_STEP(1, xa1, xo1, m1, xa0, xo0, m0);
+                DM_DEPTH_STEP(2, xa0, xo0, m0, xa1, xo1, m1);
+                DM_DEPTH_STEP(3, xa1, xo1, m1, xa0, xo0, m0);
+                l += 4;
+            }
+            if (l + 2 <= depth) {
+                const uint32_t rel = mylv - l;
+                DM_DEPTH_STEP(0, xa0, xo0, m0, xa1, xo1, m1);
+                DM_DEPTH_STEP(1, xa1, xo1, m1, xa0, xo0, m0);
+                l += 2;
+            }
+            if (l < depth) {
+                const uint32_t rel = mylv - l;
+                DM_DEPTH_STEP(0, xa0, xo0, m0, xa1, xo1, m1);
+                xa1 = xa0;
+                xo1 = xo0;
+                m1 = m0;
+            }
+            // the last depth's reads are captured here
+            if ((m1 >> lane) & 1) {
+                La = xa1;
+                Lo = xo1;
+            }
         }
         const bool flip = (cur.w >> 28) & 1;
         lpre[w * kWave + lane] = flip ? make_longlong2(Lo, La) : make_longlong2(La, Lo);
     };
+    static_assert(kPrefetch == 4, "the walk below holds four record windows");
     // Records arrive kPrefetch windows ahead.  The loop is unrolled by
     // kPrefetch so that each slot is used where it was loaded (no register
     // moves, which would wait for every load in flight); windows past the
@@ -469,6 +566,8 @@ __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, ui
     for (uint32_t d = lane; d < n_live && d < kFastMaxLive; d += kWave)
         loads[live_ids[d]] = b0 + (int64_t)L[d];
 }
+
+#undef DM_DEPTH_STEP
 
 // One wave: 32-bit relative loads unless plan[2] asks for 64-bit ones.
 __global__ __launch_bounds__(kWave) void select_fast_kernel(

@@ -115,8 +115,8 @@ def cpu_baseline(wl, sample):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--n-req", type=int, default=1_048_576)
     ap.add_argument("--cpu-sample", type=int, default=100_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -215,11 +215,12 @@ def main():
                      "note": "averaged over the timed steps; with pipelining, select runs "
                              "from the batch's probe end to its selection end"},
         "pipelined": True,
-        "select_bound": {"kernel": "select_fast_kernel<int>", "bound": "latency",
+        "select_bound": {"kernel": "select_fast_kernel", "bound": "latency",
                          "depth_steps": depth_steps,
                          "ns_per_step": ref_stage[2] * 1e6 / depth_steps,
                          "note": "one wave walks 64-request windows in dependency depth order; "
-                                 "each step is an LDS round trip plus ~16 instructions; "
+                                 "each step is an LDS round trip plus six dependent ALU "
+                                 "instructions (15 issued); "
                                  "time from the unpipelined stage"},
         "unpipelined": {"ms_per_step": ms_ref, "requests_per_s": n / (ms_ref * 1e-3),
                         "steps": n_ref,

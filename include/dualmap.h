@@ -209,28 +209,37 @@ dm_status dm_set_timing(dm_ctx* ctx, int on);
 dm_status dm_route_stage_ms(dm_ctx* ctx, float* ms_host, int n);
 
 /* Pipelined routing of consecutive batches.  The selection stage is a chain
- * in request order over shared loads (Sec. 3.2) and runs on one compute
- * unit, while hashing and probing use the whole GPU.  With on != 0,
- * dm_route_batch runs its selection on a second stream owned by the
- * context.  That selection starts once the batch's probe stage and the
- * previous batch's selection are done, so batches are still decided in
- * order.  The call does not make the context's stream wait for it, so the
- * next batch's hashing and probing overlap it.
+ * in request order over shared loads (Sec. 3.2) and runs as one wave, while
+ * hashing and probing use the whole GPU.  With on != 0, dm_route_batch runs
+ * on three streams owned by the context: hashing, probing and record
+ * packing on a work stream restricted to all compute units but one, the
+ * selection walk on a stream restricted to that one unit, and the
+ * per-request epilogue (chosen, TTFT, flags) on a third stream (where the
+ * runtime refuses compute-unit masks, the streams are unrestricted).  A
+ * batch's work starts after the work queued on the context's stream before
+ * the call; its selection starts once its records are packed and the
+ * previous batch's selection is done, so batches are still decided in
+ * order.  The context's stream is not made to wait, so the next batch's
+ * hashing and probing overlap this batch's selection.  At most two batches
+ * are in flight: a batch's work also waits for the epilogue of the batch
+ * two before it.
  *
- * Until that selection has run, the batch's tokens, offsets, output arrays
- * and the loads must stay valid and unmodified, and the next batch needs
- * distinct output arrays.  The same loads array may be passed to every
+ * Until the batch's selection and epilogue have run (dm_sync, or any call
+ * that orders the context's stream after them, below), the batch's tokens,
+ * offsets, output arrays and the loads must stay valid and unmodified.
+ * Consecutive batches need distinct output arrays; a batch may reuse those
+ * of the batch two before it.  The same loads array may be passed to every
  * batch.
  *
- * dm_sync waits for both streams.  Every other call except dm_route_batch,
+ * dm_sync waits for all streams.  Every other call except dm_route_batch,
  * dm_set_timing and dm_route_stage_ms first orders the context's stream
- * after the last selection.  Turning pipelining off does the same.  Returns
- * DM_EDEVICE if the stream or its events cannot be created. */
+ * after the last epilogue.  Turning pipelining off does the same.  Returns
+ * DM_EDEVICE if the streams or their events cannot be created. */
 dm_status dm_set_pipelining(dm_ctx* ctx, int on);
 
 /* Wait for all work on the context's stream (and, with pipelining, on its
- * selection stream); return and clear the first device-side error since the
- * last dm_sync. */
+ * work, selection and epilogue streams); return and clear the first
+ * device-side error since the last dm_sync. */
 dm_status dm_sync(dm_ctx* ctx);
 
 /* Message of the last failing call on ctx ("" if none); valid until the next

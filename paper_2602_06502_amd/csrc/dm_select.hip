@@ -253,7 +253,7 @@ __global__ __launch_bounds__(256) void sel_base_kernel(const int64_t* __restrict
 }
 
 constexpr uint32_t kFastMaxLive = 256;
-constexpr int kPrefetch = 4;  // record windows in flight ahead of the walk
+constexpr int kPrefetch = 8;  // record windows in flight ahead of the walk
 
 // grow[0..n_live) and the bad-record word grow[kMaxSlots] start at zero.
 __global__ void sel_zero_kernel(unsigned long long* __restrict__ grow, uint32_t n_live)
@@ -545,22 +545,32 @@ __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, ui
         const bool flip = (cur.w >> 28) & 1;
         lpre[w * kWave + lane] = flip ? make_longlong2(Lo, La) : make_longlong2(La, Lo);
     };
-    static_assert(kPrefetch == 4, "the walk below holds four record windows");
+    static_assert(kPrefetch == 8, "the walk below holds eight record windows");
     // Records arrive kPrefetch windows ahead.  The loop is unrolled by
     // kPrefetch so that each slot is used where it was loaded (no register
     // moves, which would wait for every load in flight); windows past the
     // last (all lanes invalid, padded records and outputs) change nothing.
     SelPack q0 = rec[0 * kWave + lane], q1 = rec[1 * kWave + lane];
     SelPack q2 = rec[2 * kWave + lane], q3 = rec[3 * kWave + lane];
+    SelPack q4 = rec[4 * kWave + lane], q5 = rec[5 * kWave + lane];
+    SelPack q6 = rec[6 * kWave + lane], q7 = rec[7 * kWave + lane];
     for (uint64_t w = 0; w < nw; w += kPrefetch) {
         window(q0, w);
-        q0 = rec[(w + 4) * kWave + lane];
+        q0 = rec[(w + 8) * kWave + lane];
         window(q1, w + 1);
-        q1 = rec[(w + 5) * kWave + lane];
+        q1 = rec[(w + 9) * kWave + lane];
         window(q2, w + 2);
-        q2 = rec[(w + 6) * kWave + lane];
+        q2 = rec[(w + 10) * kWave + lane];
         window(q3, w + 3);
-        q3 = rec[(w + 7) * kWave + lane];
+        q3 = rec[(w + 11) * kWave + lane];
+        window(q4, w + 4);
+        q4 = rec[(w + 12) * kWave + lane];
+        window(q5, w + 5);
+        q5 = rec[(w + 13) * kWave + lane];
+        window(q6, w + 6);
+        q6 = rec[(w + 14) * kWave + lane];
+        window(q7, w + 7);
+        q7 = rec[(w + 15) * kWave + lane];
     }
     __syncthreads();
     for (uint32_t d = lane; d < n_live && d < kFastMaxLive; d += kWave)

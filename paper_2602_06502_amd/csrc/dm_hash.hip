@@ -1,12 +1,13 @@
 // Chained block keys and ring keys of every request (Sec. 3.2; Sec. A.1.1).
 //
-// One wave per request walks the prompt 64 blocks at a time, lane l owning
-// block l of the chunk:
+// Each wave takes requests in turn (one, unless the batch has more than 4 Mi
+// requests) and walks each prompt 64 blocks at a time, lane l owning block l
+// of the chunk:
 //   - NH digest of its block from B/4 16-byte loads;
 //   - the affine chain H[b] = H[b-1] P + NH(b) for all 64 lanes at once:
 //     with Q = P^-1 mod 2^64, H[c+l] = P^(l+1) (G + sum_{k<=l} NH(c+k)
 //     Q^(k+1)), G carrying H of the previous chunk -- a wave prefix sum of
-//     u64 instead of a serial chain;
+//     u64 (register-level DPP moves) instead of a serial chain;
 //   - block key mix64(H xor seed), stored for every full block;
 //   - in the first chunk the f2 chain over the first K blocks (one wave
 //     sum) gives the second ring key.
@@ -16,6 +17,7 @@ namespace dm {
 namespace {
 
 constexpr int kHashThreads = 256;
+constexpr uint32_t kHashBlocks = 1u << 20;  // one wave per request up to 4 Mi requests
 
 typedef int v4i __attribute__((ext_vector_type(4), aligned(4)));
 
@@ -77,20 +79,40 @@ __global__ __launch_bounds__(kHashThreads) void hash_kernel(HashArgs a)
         k1[j] = hp->kk[0][j];
         k2[j] = hp->kk[1][j];
     }
+    // The next request's offsets and block start are fetched while this one
+    // is hashed, so no wave waits on them between requests.
+    int64_t o0 = 0, o1 = 0;
+    uint64_t bs = 0;
+    if (gw < a.n) {
+        o0 = a.offsets[gw];
+        o1 = a.offsets[gw + 1];
+        bs = a.bstart[gw];
+    }
     for (uint64_t r = gw; r < a.n; r += nw) {
-        const int64_t o0 = a.offsets[r], len = a.offsets[r + 1] - o0;
+        const uint64_t rn = r + nw;
+        int64_t no0 = 0, no1 = 0;
+        uint64_t nbs = 0;
+        if (rn < a.n) {
+            no0 = a.offsets[rn];
+            no1 = a.offsets[rn + 1];
+            nbs = a.bstart[rn];
+        }
+        const int64_t len = o1 - o0;
         if (o0 < 0 || len < 0) {
             if (lane == 0) {
                 atomicOr(a.status, kErrInval);
                 a.key_out[r] = 0;
                 a.key_out[a.n + r] = 0;
             }
+            o0 = no0;
+            o1 = no1;
+            bs = nbs;
             continue;
         }
         const uint64_t nfull = (uint64_t)len / B;
         const uint32_t kr = (uint32_t)(nfull < a.key_blocks ? nfull : a.key_blocks);
         const int32_t* tp = a.tokens + o0;
-        uint64_t* hk = a.hkeys + a.bstart[r];
+        uint64_t* hk = a.hkeys + bs;
         uint64_t x1 = mix64(H01 ^ seed1), x2 = mix64(H02 ^ seed2);  // empty-prefix keys
         uint64_t G = H01;
         for (uint64_t cb = 0; cb < nfull; cb += kWave) {
@@ -119,6 +141,9 @@ __global__ __launch_bounds__(kHashThreads) void hash_kernel(HashArgs a)
             a.key_out[r] = x1;
             a.key_out[a.n + r] = x2;
         }
+        o0 = no0;
+        o1 = no1;
+        bs = nbs;
     }
 }
 
@@ -135,7 +160,7 @@ hipError_t hash_blocks(dm_ctx* c, const int32_t* tokens, const int64_t* offsets,
 {
     HashArgs ha{tokens, offsets, n, c->d_hp, c->cfg.key_blocks, bstart, hkeys, key_out,
                 c->d_status};
-    const uint32_t grid = grid_for(n, kHashThreads / kWave, 1u << 20);
+    const uint32_t grid = grid_for(n, kHashThreads / kWave, kHashBlocks);
     switch (c->cfg.block_size) {
         case 4: launch_hash<4>(ha, grid, c->stream); break;
         case 8: launch_hash<8>(ha, grid, c->stream); break;

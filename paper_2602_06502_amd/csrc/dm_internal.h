@@ -245,26 +245,37 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane)
     return ((uint64_t)hi << 32) | lo;
 }
 
-// Inclusive prefix sum of a u64 over the 64 lanes of a wave.
-__device__ __forceinline__ uint64_t wave_incl_sum_u64(uint64_t v, int lane)
+// v moved across lanes by a DPP control (both 32-bit halves); lanes whose
+// source is out of range or whose row is masked off read 0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v)
 {
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        uint64_t o = shfl_u64(v, lane >= d ? lane - d : lane);
-        if (lane >= d)
-            v += o;
-    }
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, ROW_MASK,
+                                                              0xF, true);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL,
+                                                              ROW_MASK, 0xF, true);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Inclusive prefix sum (mod 2^64) of a u64 over the 64 lanes of a wave; every
+// lane must be active.  Register-level data movement only: shifts by 1, 2,
+// 4, 8 inside each 16-lane row, then the last lane of row 0 (row 2) into
+// row 1 (row 3), then the last lane of row 1 into rows 2 and 3.
+__device__ __forceinline__ uint64_t wave_incl_sum_u64(uint64_t v, int /*lane*/)
+{
+    v += dpp_u64<0x111, 0xF>(v);  // row_shr:1
+    v += dpp_u64<0x112, 0xF>(v);  // row_shr:2
+    v += dpp_u64<0x114, 0xF>(v);  // row_shr:4
+    v += dpp_u64<0x118, 0xF>(v);  // row_shr:8
+    v += dpp_u64<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+    v += dpp_u64<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
     return v;
 }
 
+// Sum over the 64 lanes of a wave, in every lane; every lane must be active.
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
 {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) {
-        uint32_t lo = __shfl_xor((uint32_t)v, d), hi = __shfl_xor((uint32_t)(v >> 32), d);
-        v += ((uint64_t)hi << 32) | lo;
-    }
-    return v;
+    return readlane_u64(wave_incl_sum_u64(v, 0), kWave - 1);
 }
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }

@@ -138,7 +138,9 @@ typedef struct {
  *      cached blocks unless its TTFT exceeds the SLO, then the other one if
  *      strictly less loaded.
  * loads: device int64 [max_slots], read and updated in place.  Requires
- * rings (DM_ESTATE otherwise).  n = 0 is a no-op. */
+ * rings (DM_ESTATE otherwise).  n = 0 is a no-op; n must be below 2^32
+ * (DM_EINVAL).  Match lengths are 32-bit: a request with 2^32 or more full
+ * blocks sets the device status word (DM_EINVAL from dm_sync). */
 dm_status dm_route_batch(dm_ctx* ctx, const int32_t* tokens, const int64_t* offsets, uint64_t n,
                          int64_t* loads, const dm_route_out* out);
 
@@ -200,9 +202,10 @@ dm_status dm_scale(dm_ctx* ctx, const uint32_t* add, uint32_t n_add, const uint3
  * stage times in milliseconds to ms_host, averaged over the batches routed
  * since timing was (re)enabled (the last 64 at most): [0] chained block
  * hashing (one kernel), [1] ring lookup and longest cached prefix, [2]
- * in-order selection (with pipelining: from the end of the batch's probe
- * stage to the end of its selection, so it includes waiting for the
- * previous batch's selection), [3] per-request block offsets.
+ * record packing and in-order selection (with pipelining: from the end of
+ * the batch's probe stage to the end of its selection, so it includes
+ * waiting for the previous batch's selection), [3] per-request block
+ * offsets.
  * dm_route_stage_ms returns DM_ESTATE if timing is off or no batch was
  * timed. */
 dm_status dm_set_timing(dm_ctx* ctx, int on);

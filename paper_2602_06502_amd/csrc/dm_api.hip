@@ -192,6 +192,8 @@ dm_status dm_create(const dm_config* cfg, void* hip_stream, dm_ctx** out)
     c->live.assign(k.max_slots, 0);
     make_params(c->hp, k);
     hipError_t e = hipGetDevice(&c->device);
+    if (e == hipSuccess)
+        e = hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, c->device);
     const size_t S = k.max_slots;
     const size_t table_slots = S << k.index_log2_slots;
     if (e == hipSuccess) e = hipMalloc(&c->d_hp, sizeof(HashParams));
@@ -381,8 +383,8 @@ dm_status dm_route_batch(dm_ctx* c, const int32_t* tokens, const int64_t* offset
         !aligned(out->cand) || !aligned(out->match) || !aligned(out->chosen) ||
         !aligned(out->ttft_us) || (out->block_keys && !aligned(out->block_keys)))
         return fail(c, DM_EINVAL, "dm_route_batch: misaligned pointer");
-    if (n > (1ull << 40))
-        return fail(c, DM_EINVAL, "dm_route_batch: batch too large");
+    if (n > 0xFFFFFFFFull)
+        return fail(c, DM_EINVAL, "dm_route_batch: batch too large (n < 2^32)");
     DeviceGuard g(c->device);
     hipError_t e = route(c, tokens, offsets, n, loads, out);
     return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_route_batch");

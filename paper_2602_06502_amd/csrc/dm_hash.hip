@@ -54,7 +54,8 @@ __device__ __forceinline__ void nh_block2(const int32_t* p, const uint32_t* k1, 
 struct HashArgs {
     const int32_t* tokens;
     const int64_t* offsets;
-    uint64_t n;
+    uint64_t n;             // batch size (key_out holds 2n keys)
+    uint64_t r0, r1;        // requests of this launch
     const HashParams* hp;
     uint32_t key_blocks;
     const uint64_t* bstart;  // [n+1]
@@ -83,16 +84,16 @@ __global__ __launch_bounds__(kHashThreads) void hash_kernel(HashArgs a)
     // is hashed, so no wave waits on them between requests.
     int64_t o0 = 0, o1 = 0;
     uint64_t bs = 0;
-    if (gw < a.n) {
-        o0 = a.offsets[gw];
-        o1 = a.offsets[gw + 1];
-        bs = a.bstart[gw];
+    if (a.r0 + gw < a.r1) {
+        o0 = a.offsets[a.r0 + gw];
+        o1 = a.offsets[a.r0 + gw + 1];
+        bs = a.bstart[a.r0 + gw];
     }
-    for (uint64_t r = gw; r < a.n; r += nw) {
+    for (uint64_t r = a.r0 + gw; r < a.r1; r += nw) {
         const uint64_t rn = r + nw;
         int64_t no0 = 0, no1 = 0;
         uint64_t nbs = 0;
-        if (rn < a.n) {
+        if (rn < a.r1) {
             no0 = a.offsets[rn];
             no1 = a.offsets[rn + 1];
             nbs = a.bstart[rn];
@@ -156,11 +157,12 @@ void launch_hash(const HashArgs& a, uint32_t grid, hipStream_t s)
 }  // namespace
 
 hipError_t hash_blocks(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                       const uint64_t* bstart, uint64_t* hkeys, uint64_t* key_out)
+                       const uint64_t* bstart, uint64_t* hkeys, uint64_t* key_out, uint64_t r0,
+                       uint64_t r1)
 {
-    HashArgs ha{tokens, offsets, n, c->d_hp, c->cfg.key_blocks, bstart, hkeys, key_out,
+    HashArgs ha{tokens, offsets, n, r0, r1, c->d_hp, c->cfg.key_blocks, bstart, hkeys, key_out,
                 c->d_status};
-    const uint32_t grid = grid_for(n, kHashThreads / kWave, kHashBlocks);
+    const uint32_t grid = grid_for(r1 > r0 ? r1 - r0 : 0, kHashThreads / kWave, kHashBlocks);
     switch (c->cfg.block_size) {
         case 4: launch_hash<4>(ha, grid, c->stream); break;
         case 8: launch_hash<8>(ha, grid, c->stream); break;

@@ -69,6 +69,8 @@ struct dm_ctx {
     dm_config cfg;
     hipStream_t stream = nullptr;
     int device = 0;
+    int n_cu = 0;           // compute units of the device
+    uint32_t probe_grid = 0;  // resident workgroups of the probe kernel (set on first use)
     std::string err;
 
     // live set (host) and cyclic next-live table (device)
@@ -161,14 +163,18 @@ hipError_t index_erase(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n)
 hipError_t index_clear(dm_ctx* c, uint32_t id);
 
 // dm_hash.hip: block keys of every full block (hkeys at bstart[r]) and the
-// two ring keys of every request (key_out[r], key_out[n + r]).
+// two ring keys of every request (key_out[r], key_out[n + r]) for the
+// requests r in [r0, r1) of a batch of n.
 hipError_t hash_blocks(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                       const uint64_t* bstart, uint64_t* hkeys, uint64_t* key_out);
+                       const uint64_t* bstart, uint64_t* hkeys, uint64_t* key_out, uint64_t r0,
+                       uint64_t r1);
 
 // dm_probe.hip: candidates on the current rings (cand, fix-up flag bit 3)
-// and the longest cached prefix on each (match).
+// and the longest cached prefix on each (match), for the requests r in
+// [r0, r1) of a batch of n.
 hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64_t* hkeys,
-                        const uint64_t* bstart, uint32_t* cand, uint32_t* match, uint8_t* flags);
+                        const uint64_t* bstart, uint32_t* cand, uint32_t* match, uint8_t* flags,
+                        uint64_t r0, uint64_t r1);
 
 // dm_select.hip: SLO-aware choice in request order; chosen, ttft_us and
 // flags bits 0-2 written, loads updated.  select_prepare packs the batch's

@@ -6,11 +6,11 @@
 //   exact.  Requests are first ordered by the top 16 bits of their first
 //   ring key, which puts requests that share a prompt prefix (hence the
 //   same candidates and the same leading block keys) side by side.  A wave
-//   takes 32 consecutive requests, lanes 0-31 probing their first
-//   candidate and lanes 32-63 their second, all walking their key
-//   sequences in step: lanes that share a prefix load the same 64-byte
-//   bucket in the same instruction, so one line fetch serves them all.  No
-//   probe past a lane's first miss is issued.
+//   takes 64 consecutive requests on one of the two candidates, all lanes
+//   walking their key sequences in step: lanes that share a prefix load the
+//   same 64-byte bucket in the same instruction, so one line fetch serves
+//   them all, and they tend to stop at the same block.  No probe past a
+//   lane's first miss is issued.
 #include <algorithm>
 
 #include "dm_internal.h"
@@ -20,17 +20,16 @@ namespace {
 
 constexpr int kProbeThreads = 256;
 constexpr int kProbeSlot = 1;             // sort keys, request order and sort work arrays
-constexpr uint32_t kProbeBlocks = 2048;   // persistent: 8,192 waves, 256 CUs x 4 SIMDs x 8
-constexpr int kGroupReq = kWave / 2;      // requests per wave step (two candidates each)
 constexpr int kOrderBits = 16;            // top bits of the first ring key used for ordering
 
 typedef unsigned long long v2u64 __attribute__((ext_vector_type(2), aligned(16)));
 
-__global__ void lookup_kernel(uint64_t n, const uint64_t* __restrict__ key, RingView r1, RingView r2,
-                              const uint32_t* __restrict__ next_live, uint32_t n_live,
-                              uint32_t* __restrict__ cand, uint8_t* __restrict__ flags)
+__global__ void lookup_kernel(uint64_t n, uint64_t q0, uint64_t q1, const uint64_t* __restrict__ key,
+                              RingView r1, RingView r2, const uint32_t* __restrict__ next_live,
+                              uint32_t n_live, uint32_t* __restrict__ cand,
+                              uint8_t* __restrict__ flags)
 {
-    for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
+    for (uint64_t r = q0 + blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < q1;
          r += (uint64_t)gridDim.x * blockDim.x) {
         const uint32_t c1 = ring_owner(r1, key[r]);
         uint32_t c2 = ring_owner(r2, key[n + r]);
@@ -45,84 +44,186 @@ __global__ void lookup_kernel(uint64_t n, const uint64_t* __restrict__ key, Ring
     }
 }
 
-// keys[i] = top kOrderBits bits of request i's first ring key; vals[i] = i.
-__global__ void order_init_kernel(const uint64_t* __restrict__ key, uint64_t n,
+// keys[i] = top kOrderBits bits of request r0 + i's first ring key;
+// vals[i] = r0 + i.
+__global__ void order_init_kernel(const uint64_t* __restrict__ key, uint64_t r0, uint64_t m,
                                   uint64_t* __restrict__ keys, uint32_t* __restrict__ vals)
 {
-    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < n;
+    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < m;
          i += (uint64_t)gridDim.x * blockDim.x) {
-        keys[i] = key[i] >> (64 - kOrderBits);
-        vals[i] = (uint32_t)i;
+        keys[i] = key[r0 + i] >> (64 - kOrderBits);
+        vals[i] = (uint32_t)(r0 + i);
     }
 }
 
 struct ProbeArgs {
     const uint64_t* hkeys;
     const uint64_t* bstart;
-    uint64_t n;
+    uint64_t n;      // batch size (cand and match hold 2n entries)
+    uint64_t count;  // requests in order[]
     const uint32_t* cand;
     const uint64_t* tables;
     uint32_t log2slots;
     uint32_t* match;
-    const uint32_t* order;  // [n] requests ordered by first ring key prefix
+    const uint32_t* order;  // [count] requests ordered by first ring key prefix
+    uint32_t* status;
 };
 
+// Probe outcome of one key against one bucket: the key is there, the bucket
+// has an empty slot (so the key is absent: the probe sequence of an insert
+// would have stopped here), or neither (go on to the next bucket).  Inserts
+// take a bucket's slots in order and slots never return to empty, so a
+// bucket's empty slots are a suffix of it: it has one iff its last slot is.
+enum : int { kHit = 0, kMiss = 1, kNext = 2 };
+
+__device__ __forceinline__ int bucket_probe(const uint64_t* tab, uint32_t bkt, uint64_t key)
+{
+    const v2u64* line = reinterpret_cast<const v2u64*>(tab + (uint64_t)bkt * kBucket);
+    const v2u64 s0 = line[0], s1 = line[1], s2 = line[2], s3 = line[3];
+    const bool hit = s0.x == key || s0.y == key || s1.x == key || s1.y == key || s2.x == key ||
+                     s2.y == key || s3.x == key || s3.y == key;
+    return hit ? kHit : (s3.y == kEmpty ? kMiss : kNext);
+}
+
+// Home bucket of a canonical key in 8-slot buckets of a 2^ls-slot table
+// (ls <= 30): its top ls - 3 bits.
+__device__ __forceinline__ uint32_t home32(uint64_t ck, uint32_t ls)
+{
+    return (uint32_t)(ck >> 32) >> (35 - ls);
+}
+
+// Block keys of a lane's probe sequence are read kWin at a time into a
+// window in LDS; a step needs the keys of its two blocks and of the two
+// after them, so a window serves three steps and only one step in three
+// waits for HBM (keys are touched once, by the probe that needs them, long
+// after the hash kernel wrote them).
+constexpr int kWin = 8;
+
+typedef unsigned long long v2u64a8 __attribute__((ext_vector_type(2), aligned(8)));
+
+// Loads hk[q, q + kWin) (zeros from index lim on) into w[0..kWin).
+__device__ __forceinline__ void window_load(const uint64_t* hk, uint64_t q, uint64_t lim,
+                                            uint64_t (&w)[kWin])
+{
+    if (q + kWin <= lim) {
+        const v2u64a8* p = reinterpret_cast<const v2u64a8*>(hk + q);
+#pragma unroll
+        for (int k = 0; k < kWin / 2; k++) {
+            const v2u64a8 v = p[k];
+            w[2 * k] = v.x;
+            w[2 * k + 1] = v.y;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < kWin; k++)
+            w[k] = q + k < lim ? hk[q + k] : 0;
+    }
+}
+
 // Longest cached prefix of every (request, candidate), first miss exact.
-// Wave w takes request groups w, w + W, ... of the ordered list; within a
-// group every lane probes one 64-byte bucket per step while the next block
-// key of its sequence is already being fetched, and the group is done when
-// every lane has met its first miss or its last full block.
+// Group g covers the requests at positions [64 (g >> 1), 64 (g >> 1) + 64)
+// of the ordered list, on their first candidate (g even) or second (g odd);
+// wave w takes groups w, w + W, ....  Within a group every lane probes two
+// consecutive blocks per step (slot 0: the first unresolved block kb,
+// slot 1: kb + 1), the keys of the next two coming from its window; a step
+// resolves up to two blocks.  The group is done when every lane has met its
+// first miss or its last full block.  Block positions are relative to the
+// request's first block (a request has fewer than 2^32 full blocks, as its
+// 32-bit match length requires; more set the status word).
 __global__ __launch_bounds__(kProbeThreads) void probe_kernel(ProbeArgs a)
 {
+    __shared__ uint64_t win_all[kProbeThreads / kWave][kWin][kWave];
     const int lane = lane_id();
+    uint64_t (*win)[kWave] = win_all[threadIdx.x >> 6];
     const uint64_t gw = ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const uint64_t nw = ((uint64_t)gridDim.x * blockDim.x) >> 6;
-    const uint64_t ng = (a.n + kGroupReq - 1) / kGroupReq;
-    const uint64_t nbk = 1ull << (a.log2slots - 3);
-    const uint64_t side = lane >= kGroupReq ? a.n : 0;  // second candidate's half of cand/match
+    const uint64_t ng = 2 * ((a.count + kWave - 1) / kWave);
+    const uint32_t nbk = 1u << (a.log2slots - 3);
+    const uint32_t ls = a.log2slots;
+    const uint64_t total = a.bstart[a.n];  // block keys in hkeys
     for (uint64_t g = gw; g < ng; g += nw) {
-        const uint64_t i = g * kGroupReq + (lane & (kGroupReq - 1));
-        const bool valid = i < a.n;
-        uint64_t kb = 0, ke = 0, out = 0;
+        const uint64_t i = (g >> 1) * kWave + lane;
+        const bool valid = i < a.count;
+        uint64_t k0 = 0, out = 0;
+        uint32_t len = 0;
         const uint64_t* tab = a.tables;
         if (valid) {
             const uint32_t r = a.order[i];
-            out = side + r;
-            kb = a.bstart[r];
-            ke = a.bstart[(uint64_t)r + 1];
-            tab = a.tables + ((uint64_t)a.cand[out] << a.log2slots);
+            out = (g & 1) * a.n + r;
+            k0 = a.bstart[r];
+            const uint64_t ke = a.bstart[(uint64_t)r + 1];
+            if (ke - k0 > 0xFFFFFFFFull) {
+                atomicOr(a.status, kErrInval);
+                k0 = ke;
+            }
+            len = (uint32_t)(ke - k0);
+            tab = a.tables + ((uint64_t)a.cand[out] << ls);
         }
-        const uint64_t k0 = kb;
-        bool active = valid && kb < ke;
+        const uint64_t* hk = a.hkeys + k0;
+        const uint64_t lim = total - k0;  // keys readable from hk
+        bool active = valid && len > 0;
         if (valid && !active)
             a.match[out] = 0;  // no full block
-        uint64_t key = active ? canon_key(a.hkeys[kb]) : 0;
-        uint64_t bkt = home_bucket(key, a.log2slots), steps = 0;
+        // slot 0: block kb; slot 1: block kb + 1 (when kb + 1 < len); the
+        // window holds blocks [w0, w0 + kWin)
+        uint32_t kb = 0, w0 = 0, st0 = 0, st1 = 0;
+        uint64_t key0 = 0, key1 = 0;
+        if (active) {
+            uint64_t w[kWin];
+            window_load(hk, 0, lim, w);
+#pragma unroll
+            for (int k = 0; k < kWin; k++)
+                win[k][lane] = w[k];
+            key0 = canon_key(w[0]);
+            key1 = canon_key(w[1]);
+        }
+        uint32_t b0 = home32(key0, ls), b1 = home32(key1, ls);
         while (__any(active)) {
             if (active) {
-                const v2u64* line = reinterpret_cast<const v2u64*>(tab + bkt * kBucket);
-                const v2u64 s0 = line[0], s1 = line[1], s2 = line[2], s3 = line[3];
-                const uint64_t nkey = kb + 1 < ke ? a.hkeys[kb + 1] : 0;
-                const bool hit = s0.x == key || s0.y == key || s1.x == key || s1.y == key ||
-                                 s2.x == key || s2.y == key || s3.x == key || s3.y == key;
-                const bool empty = s0.x == kEmpty || s0.y == kEmpty || s1.x == kEmpty ||
-                                   s1.y == kEmpty || s2.x == kEmpty || s2.y == kEmpty ||
-                                   s3.x == kEmpty || s3.y == kEmpty;
-                if (hit) {
-                    kb++;
-                    if (kb == ke) {
-                        a.match[out] = (uint32_t)(kb - k0);
-                        active = false;
-                    } else {
-                        key = canon_key(nkey);
-                        bkt = home_bucket(key, a.log2slots);
-                        steps = 0;
-                    }
-                } else if (empty || ++steps >= nbk) {
-                    a.match[out] = (uint32_t)(kb - k0);  // first miss (or scanned the whole table)
+                const bool two = kb + 1 < len;
+                const int r0 = bucket_probe(tab, b0, key0);
+                const int r1 = two ? bucket_probe(tab, b1, key1) : kMiss;
+                const uint64_t p2 = kb + 2 < len ? win[kb + 2 - w0][lane] : 0;
+                const uint64_t p3 = kb + 3 < len ? win[kb + 3 - w0][lane] : 0;
+                const bool h0 = r0 == kHit, h1 = two && r1 == kHit;
+                const uint32_t adv = h0 ? (h1 ? 2u : 1u) : 0u;
+                // next step of slot 0's sequence (slot 0 unresolved), or of
+                // slot 1's sequence moving to slot 0 (block kb present)
+                const uint32_t nst = h0 ? st1 + 1 : st0 + 1;
+                const bool fin = !h0 ? (r0 == kMiss || nst >= nbk)
+                                     : (!two || r1 == kMiss || (h1 ? kb + 2 == len : nst >= nbk));
+                if (fin) {
+                    a.match[out] = kb + adv;
                     active = false;
                 } else {
-                    bkt = (bkt + 1) & (nbk - 1);
+                    if (!h0) {  // slot 0 goes on to its next bucket, slot 1 is probed again
+                        b0 = (b0 + 1) & (nbk - 1);
+                        st0 = nst;
+                    } else if (h1) {  // both present: the next two blocks
+                        key0 = canon_key(p2);
+                        key1 = canon_key(p3);
+                        b0 = home32(key0, ls);
+                        b1 = home32(key1, ls);
+                        st0 = 0;
+                        st1 = 0;
+                    } else {  // block kb present, kb + 1 goes on in slot 0
+                        key0 = key1;
+                        b0 = (b1 + 1) & (nbk - 1);
+                        st0 = nst;
+                        key1 = canon_key(p2);
+                        b1 = home32(key1, ls);
+                        st1 = 0;
+                    }
+                    kb += adv;
+                    // the next step reads blocks kb + 2 and kb + 3 from the window
+                    if (kb + 4 > w0 + kWin) {
+                        uint64_t w[kWin];
+                        window_load(hk, kb, lim, w);
+                        w0 = kb;
+#pragma unroll
+                        for (int k = 0; k < kWin; k++)
+                            win[k][lane] = w[k];
+                    }
                 }
             }
         }
@@ -132,18 +233,22 @@ __global__ __launch_bounds__(kProbeThreads) void probe_kernel(ProbeArgs a)
 }  // namespace
 
 hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64_t* hkeys,
-                        const uint64_t* bstart, uint32_t* cand, uint32_t* match, uint8_t* flags)
+                        const uint64_t* bstart, uint32_t* cand, uint32_t* match, uint8_t* flags,
+                        uint64_t r0, uint64_t r1)
 {
     hipError_t e = hipSuccess;
     hipStream_t st = c->stream;
-    lookup_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(
-        n, key, view(c->ring[c->cur][0]), view(c->ring[c->cur][1]), c->d_next_live, c->n_live,
-        cand, flags);
-    if (n > 0xFFFFFFFFull)
+    if (r1 <= r0)
+        return hipSuccess;
+    const uint64_t m = r1 - r0;
+    lookup_kernel<<<grid_for(m, 256, 8192), 256, 0, st>>>(
+        n, r0, r1, key, view(c->ring[c->cur][0]), view(c->ring[c->cur][1]), c->d_next_live,
+        c->n_live, cand, flags);
+    if (r1 > 0xFFFFFFFFull)
         return hipErrorInvalidValue;
     // requests ordered by the top bits of their first ring key (stable radix sort)
-    const size_t kbytes = ((n * sizeof(uint64_t)) + 255) & ~size_t(255);
-    const size_t vbytes = ((n * sizeof(uint32_t)) + 255) & ~size_t(255);
+    const size_t kbytes = ((m * sizeof(uint64_t)) + 255) & ~size_t(255);
+    const size_t vbytes = ((m * sizeof(uint32_t)) + 255) & ~size_t(255);
     uint8_t* w = static_cast<uint8_t*>(scratch_get(c, kProbeSlot, 2 * (kbytes + vbytes) + 256, &e));
     if (!w)
         return e;
@@ -151,11 +256,20 @@ hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64
     uint64_t* ktmp = reinterpret_cast<uint64_t*>(w + kbytes);
     uint32_t* order = reinterpret_cast<uint32_t*>(w + 2 * kbytes);
     uint32_t* vtmp = reinterpret_cast<uint32_t*>(w + 2 * kbytes + vbytes);
-    order_init_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(key, n, keys, order);
-    if ((e = radix_sort_kv(c, keys, order, ktmp, vtmp, n, kOrderBits)) != hipSuccess)
+    order_init_kernel<<<grid_for(m, 256, 8192), 256, 0, st>>>(key, r0, m, keys, order);
+    if ((e = radix_sort_kv(c, keys, order, ktmp, vtmp, m, kOrderBits)) != hipSuccess)
         return e;
-    ProbeArgs pa{hkeys, bstart, n, cand, c->d_tables, c->cfg.index_log2_slots, match, order};
-    probe_kernel<<<kProbeBlocks, kProbeThreads, 0, st>>>(pa);
+    if (!c->probe_grid) {
+        // persistent: as many workgroups as stay resident at once
+        int per_cu = 0;
+        if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, probe_kernel, kProbeThreads,
+                                                              0)) != hipSuccess)
+            return e;
+        c->probe_grid = (uint32_t)std::max(1, per_cu * std::max(1, c->n_cu));
+    }
+    ProbeArgs pa{hkeys,   bstart, n,     m, cand, c->d_tables, c->cfg.index_log2_slots,
+                 match,   order,  c->d_status};
+    probe_kernel<<<c->probe_grid, kProbeThreads, 0, st>>>(pa);
     return hipGetLastError();
 }
 

@@ -78,16 +78,16 @@ hipError_t route(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint6
     }
     if (ev && (e = hipEventRecord(ev[1], st)) != hipSuccess)
         return e;
-    if ((e = hash_blocks(c, tokens, offsets, n, bstart, hkeys, out->key)) != hipSuccess)
+    if ((e = hash_blocks(c, tokens, offsets, n, bstart, hkeys, out->key, 0, n)) != hipSuccess)
         return e;
     if (ev && (e = hipEventRecord(ev[2], st)) != hipSuccess)
         return e;
-    if ((e = lookup_probe(c, n, out->key, hkeys, bstart, out->cand, out->match, out->flags)) !=
+    if ((e = lookup_probe(c, n, out->key, hkeys, bstart, out->cand, out->match, out->flags, 0, n)) !=
         hipSuccess)
         return e;
-    if ((e = select_prepare(c, st, offsets, n, out, par)) != hipSuccess)
-        return e;
     if (ev && (e = hipEventRecord(ev[3], st)) != hipSuccess)
+        return e;
+    if ((e = select_prepare(c, st, offsets, n, out, par)) != hipSuccess)
         return e;
     if (!pipe) {
         if ((e = select_run(c, st, st, nullptr, offsets, n, out, loads, 0)) != hipSuccess)

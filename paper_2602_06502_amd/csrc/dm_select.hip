@@ -689,7 +689,9 @@ hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uin
     const uint32_t NL = c->n_live;
     sel_zero_kernel<<<1, 256, 0, st>>>(b.grow, NL);
     const dm_config& k = c->cfg;
-    sel_prep_kernel<<<grid_for(n, 256, 4096), 256, 0, st>>>(
+    // few workgroups: each adds its per-instance growth sums to the global
+    // ones with one atomic per instance, and those atomics meet on a few lines
+    sel_prep_kernel<<<grid_for(n, 256, 512), 256, 0, st>>>(
         offsets, n, block_shift(c), out->cand, out->match, c->d_dense, NL, k.ttft_base_us,
         k.ttft_per_token_us, c->shift_div, k.slo_us, b.rec, b.grow);
     sel_level_kernel<<<(uint32_t)lgrid, kLevelWaves * kWave, 0, st>>>(b.rec, n);

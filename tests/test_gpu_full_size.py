@@ -3,6 +3,10 @@
 - Sampled parity: 2,048 random requests of the large batch are routed by the
   oracle over its own copy of the index (ring keys, candidates, match lengths
   and the adjustment flag compared exactly).
+- Full parity on a 131,072-request prefix of the large batch (big enough to
+  be hashed and probed in overlapping request chunks), with and without
+  pipelining: every output and the final loads against the oracle, element
+  by element, block keys included.
 - Selection replay property: from the engine's per-request candidates and
   match lengths, the loads every request saw are recomputed by per-instance
   prefix sums of the chosen uncached tokens; every decision, TTFT, flag and
@@ -99,15 +103,44 @@ def replay_check(wl, offsets, L0, out):
     assert np.array_equal(final, out["loads"])
 
 
-def test_large_sampled_parity_and_replay(large):
+@pytest.fixture(scope="module")
+def large_oracle(large):
+    _say("oracle setup (large index)")
+    return oh.setup(large["wl"], with_batch=False)["oracle"]
+
+
+@pytest.mark.parametrize("pipelined", [False, True])
+def test_large_prefix_full_parity(large, large_oracle, pipelined):
+    wl, g, eng, gh = large["wl"], large["g"], large["eng"], large["gh"]
+    m = 131_072
+    off = g["offsets_np"][:m + 1]
+    tok = g["tokens_np"][:off[-1]]
+    _say("route prefix", m, "pipelined" if pipelined else "single stream")
+    L0 = g["loads0"]
+    loads = gh.to_dev(L0, eng.device)
+    nb = int((np.diff(off) // wl.route.block).sum())
+    outs = eng.alloc_route_out(m, nb)
+    eng.set_pipelining(pipelined)
+    try:
+        eng.route_into(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), loads, outs)
+        eng.sync()
+    finally:
+        eng.set_pipelining(False)
+    ref = large_oracle.route(tok, off, L0.copy(), block_keys=True)
+    for k in ("key", "cand", "match", "chosen", "ttft", "flags", "block_keys"):
+        got = outs[k].cpu().numpy()[:len(ref[k])]
+        assert np.array_equal(got, ref[k]), k
+    assert np.array_equal(loads.cpu().numpy(), ref["loads"])
+
+
+def test_large_sampled_parity_and_replay(large, large_oracle):
     wl, g, out = large["wl"], large["g"], large["out"]
     n = wl.n_req
     # every decision follows the rule given the earlier ones
     _say("replay property over", n)
     replay_check(wl, g["offsets_np"], g["loads0"], out)
     # oracle on a sample of requests, same index built by the oracle itself
-    _say("oracle setup (large index)")
-    o = oh.setup(wl, with_batch=False)["oracle"]
+    o = large_oracle
     rng = np.random.default_rng(7)
     sample = np.sort(rng.choice(n, size=2048, replace=False))
     tok, off = g["tokens_np"], g["offsets_np"]

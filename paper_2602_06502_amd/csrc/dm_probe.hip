@@ -67,6 +67,7 @@ struct ProbeArgs {
     uint32_t* match;
     const uint32_t* order;  // [count] requests ordered by first ring key prefix
     uint32_t* status;
+    unsigned long long* next;  // per-XCD group counters, kCounterStride apart, zeroed
 };
 
 // Probe outcome of one key against one bucket: the key is there, the bucket
@@ -120,10 +121,25 @@ __device__ __forceinline__ void window_load(const uint64_t* hk, uint64_t q, uint
     }
 }
 
+// Groups are claimed one at a time: the waves of XCD x (workgroups x, x + 8,
+// ...) take claims h = x, x + 8, x + 16, ... in turn through a counter of
+// their own, on a line of its own, so group lengths (unknown until probed)
+// even out inside each XCD.  Claim h is request block ((h >> 4) << 3) | (h & 7)
+// on candidate (h >> 3) & 1: an XCD probes both candidates of its blocks,
+// one after the other (their block keys are shared through its L2), and the
+// XCDs get statistically equal shares.
+constexpr uint32_t kXcds = 8;
+constexpr uint32_t kCounterStride = 32;  // 256 bytes
+
+__global__ void probe_zero_kernel(unsigned long long* next)
+{
+    if (threadIdx.x < kXcds)
+        next[threadIdx.x * kCounterStride] = 0;
+}
+
 // Longest cached prefix of every (request, candidate), first miss exact.
-// Group g covers the requests at positions [64 (g >> 1), 64 (g >> 1) + 64)
-// of the ordered list, on their first candidate (g even) or second (g odd);
-// wave w takes groups w, w + W, ....  Within a group every lane probes two
+// A group covers the 64 requests of one block of the ordered list on one of
+// their candidates.  Within a group every lane probes two
 // consecutive blocks per step (slot 0: the first unresolved block kb,
 // slot 1: kb + 1), the keys of the next two coming from its window; a step
 // resolves up to two blocks.  The group is done when every lane has met its
@@ -135,21 +151,30 @@ __global__ __launch_bounds__(kProbeThreads) void probe_kernel(ProbeArgs a)
     __shared__ uint64_t win_all[kProbeThreads / kWave][kWin][kWave];
     const int lane = lane_id();
     uint64_t (*win)[kWave] = win_all[threadIdx.x >> 6];
-    const uint64_t gw = ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-    const uint64_t nw = ((uint64_t)gridDim.x * blockDim.x) >> 6;
-    const uint64_t ng = 2 * ((a.count + kWave - 1) / kWave);
+    const uint64_t nblk = (a.count + kWave - 1) / kWave;
+    const uint64_t nclaims = 16 * ((nblk + kXcds - 1) / kXcds);
+    const uint32_t xcd = blockIdx.x % kXcds;
+    unsigned long long* counter = a.next + xcd * kCounterStride;
     const uint32_t nbk = 1u << (a.log2slots - 3);
     const uint32_t ls = a.log2slots;
     const uint64_t total = a.bstart[a.n];  // block keys in hkeys
-    for (uint64_t g = gw; g < ng; g += nw) {
-        const uint64_t i = (g >> 1) * kWave + lane;
+    // the claim of the next group is issued before the current one is probed
+    uint64_t claim = 0;
+    if (lane == 0)
+        claim = atomicAdd(counter, 1ull);
+    uint64_t h = xcd + kXcds * readlane_u64(claim, 0);
+    while (h < nclaims) {
+        if (lane == 0)
+            claim = atomicAdd(counter, 1ull);
+        const uint64_t blk = ((h >> 4) << 3) | (h & 7), side = (h >> 3) & 1;
+        const uint64_t i = blk * kWave + lane;
         const bool valid = i < a.count;
         uint64_t k0 = 0, out = 0;
         uint32_t len = 0;
         const uint64_t* tab = a.tables;
         if (valid) {
             const uint32_t r = a.order[i];
-            out = (g & 1) * a.n + r;
+            out = side * a.n + r;
             k0 = a.bstart[r];
             const uint64_t ke = a.bstart[(uint64_t)r + 1];
             if (ke - k0 > 0xFFFFFFFFull) {
@@ -179,54 +204,53 @@ __global__ __launch_bounds__(kProbeThreads) void probe_kernel(ProbeArgs a)
         }
         uint32_t b0 = home32(key0, ls), b1 = home32(key1, ls);
         while (__any(active)) {
+            const bool two = kb + 1 < len;
+            int r0 = kMiss, r1 = kMiss;
             if (active) {
-                const bool two = kb + 1 < len;
-                const int r0 = bucket_probe(tab, b0, key0);
-                const int r1 = two ? bucket_probe(tab, b1, key1) : kMiss;
-                const uint64_t p2 = kb + 2 < len ? win[kb + 2 - w0][lane] : 0;
-                const uint64_t p3 = kb + 3 < len ? win[kb + 3 - w0][lane] : 0;
-                const bool h0 = r0 == kHit, h1 = two && r1 == kHit;
-                const uint32_t adv = h0 ? (h1 ? 2u : 1u) : 0u;
-                // next step of slot 0's sequence (slot 0 unresolved), or of
-                // slot 1's sequence moving to slot 0 (block kb present)
-                const uint32_t nst = h0 ? st1 + 1 : st0 + 1;
-                const bool fin = !h0 ? (r0 == kMiss || nst >= nbk)
-                                     : (!two || r1 == kMiss || (h1 ? kb + 2 == len : nst >= nbk));
-                if (fin) {
-                    a.match[out] = kb + adv;
-                    active = false;
-                } else {
-                    if (!h0) {  // slot 0 goes on to its next bucket, slot 1 is probed again
-                        b0 = (b0 + 1) & (nbk - 1);
-                        st0 = nst;
-                    } else if (h1) {  // both present: the next two blocks
-                        key0 = canon_key(p2);
-                        key1 = canon_key(p3);
-                        b0 = home32(key0, ls);
-                        b1 = home32(key1, ls);
-                        st0 = 0;
-                        st1 = 0;
-                    } else {  // block kb present, kb + 1 goes on in slot 0
-                        key0 = key1;
-                        b0 = (b1 + 1) & (nbk - 1);
-                        st0 = nst;
-                        key1 = canon_key(p2);
-                        b1 = home32(key1, ls);
-                        st1 = 0;
-                    }
-                    kb += adv;
-                    // the next step reads blocks kb + 2 and kb + 3 from the window
-                    if (kb + 4 > w0 + kWin) {
-                        uint64_t w[kWin];
-                        window_load(hk, kb, lim, w);
-                        w0 = kb;
+                r0 = bucket_probe(tab, b0, key0);
+                r1 = bucket_probe(tab, b1, key1);  // slot 1 past the last block: a valid, unused bucket
+            }
+            // the window covers blocks kb + 2 and kb + 3 (kb + 4 <= w0 + kWin)
+            const uint64_t c2 = canon_key(win[kb + 2 - w0][lane]);
+            const uint64_t c3 = canon_key(win[kb + 3 - w0][lane]);
+            const bool h0 = r0 == kHit, h1 = two && r1 == kHit;
+            const uint32_t adv = h0 ? (h1 ? 2u : 1u) : 0u;
+            // next step of slot 0's sequence (slot 0 unresolved), or of slot
+            // 1's sequence moving to slot 0 (block kb present)
+            const uint32_t nst = h0 ? st1 + 1 : st0 + 1;
+            const bool fin = active && (!h0 ? (r0 == kMiss || nst >= nbk)
+                                            : (!two || r1 == kMiss || (h1 ? kb + 2 == len : nst >= nbk)));
+            if (fin)
+                a.match[out] = kb + adv;
+            const bool go = active && !fin;
+            // slot 0 unresolved: it goes on to its next bucket and slot 1 is
+            // probed again; both present: the next two blocks; block kb
+            // present only: slot 1's sequence continues in slot 0
+            const uint64_t nk0 = !h0 ? key0 : (h1 ? c2 : key1);
+            const uint64_t nk1 = !h0 ? key1 : (h1 ? c3 : c2);
+            const uint32_t nb0 = !h0 ? ((b0 + 1) & (nbk - 1))
+                                     : (h1 ? home32(c2, ls) : ((b1 + 1) & (nbk - 1)));
+            const uint32_t nb1 = !h0 ? b1 : home32(h1 ? c3 : c2, ls);
+            key0 = go ? nk0 : key0;
+            key1 = go ? nk1 : key1;
+            b0 = go ? nb0 : b0;
+            b1 = go ? nb1 : b1;
+            st0 = go ? (h1 ? 0u : nst) : st0;
+            st1 = go && h0 ? 0u : st1;
+            kb = go ? kb + adv : kb;
+            active = go;
+            // the next step reads blocks kb + 2 and kb + 3 from the window
+            const bool refill = go && kb + 4 > w0 + kWin;
+            if (__any(refill) && refill) {
+                uint64_t w[kWin];
+                window_load(hk, kb, lim, w);
+                w0 = kb;
 #pragma unroll
-                        for (int k = 0; k < kWin; k++)
-                            win[k][lane] = w[k];
-                    }
-                }
+                for (int k = 0; k < kWin; k++)
+                    win[k][lane] = w[k];
             }
         }
+        h = xcd + kXcds * readlane_u64(claim, 0);
     }
 }
 
@@ -249,13 +273,17 @@ hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64
     // requests ordered by the top bits of their first ring key (stable radix sort)
     const size_t kbytes = ((m * sizeof(uint64_t)) + 255) & ~size_t(255);
     const size_t vbytes = ((m * sizeof(uint32_t)) + 255) & ~size_t(255);
-    uint8_t* w = static_cast<uint8_t*>(scratch_get(c, kProbeSlot, 2 * (kbytes + vbytes) + 256, &e));
+    const size_t cbytes = kXcds * kCounterStride * sizeof(unsigned long long);
+    uint8_t* w = static_cast<uint8_t*>(
+        scratch_get(c, kProbeSlot, 2 * (kbytes + vbytes) + cbytes + 256, &e));
     if (!w)
         return e;
     uint64_t* keys = reinterpret_cast<uint64_t*>(w);
     uint64_t* ktmp = reinterpret_cast<uint64_t*>(w + kbytes);
     uint32_t* order = reinterpret_cast<uint32_t*>(w + 2 * kbytes);
     uint32_t* vtmp = reinterpret_cast<uint32_t*>(w + 2 * kbytes + vbytes);
+    unsigned long long* next =
+        reinterpret_cast<unsigned long long*>(w + ((2 * (kbytes + vbytes) + 255) & ~size_t(255)));
     order_init_kernel<<<grid_for(m, 256, 8192), 256, 0, st>>>(key, r0, m, keys, order);
     if ((e = radix_sort_kv(c, keys, order, ktmp, vtmp, m, kOrderBits)) != hipSuccess)
         return e;
@@ -265,10 +293,13 @@ hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64
         if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, probe_kernel, kProbeThreads,
                                                               0)) != hipSuccess)
             return e;
-        c->probe_grid = (uint32_t)std::max(1, per_cu * std::max(1, c->n_cu));
+        // every XCD residue class of workgroup indices needs workgroups
+        const uint32_t g = (uint32_t)std::max(1, per_cu * std::max(1, c->n_cu));
+        c->probe_grid = (g + kXcds - 1) / kXcds * kXcds;
     }
-    ProbeArgs pa{hkeys,   bstart, n,     m, cand, c->d_tables, c->cfg.index_log2_slots,
-                 match,   order,  c->d_status};
+    ProbeArgs pa{hkeys, bstart, n,           m,    cand, c->d_tables, c->cfg.index_log2_slots,
+                 match, order,  c->d_status, next};
+    probe_zero_kernel<<<1, 64, 0, st>>>(next);
     probe_kernel<<<c->probe_grid, kProbeThreads, 0, st>>>(pa);
     return hipGetLastError();
 }

@@ -218,12 +218,22 @@ __global__ __launch_bounds__(kWave) void select_lds_kernel(
 // ---------------------------------------------------------------------------
 
 // w: a | o << 8 | (depth - 1) << 16 | (window depth - 1) << 22 | (a is c2) << 28
+//    | (head of a two-request run) << 29
+// A request whose latest earlier request in its window on both of its
+// instances is one request with the same cache-affine instance forms a run
+// with it (runs of two): both take the same depth, the second replays the
+// first's decision from (pua, puo, pth) before its own, and only the second
+// writes the pair's loads.  (pua, puo) = (0, 0) replays nothing.
 struct SelPack {
     uint32_t w;
     uint32_t ua;  // uncached tokens on a
     uint32_t uo;  // uncached tokens on o
     int32_t th;   // take a iff L_a <= max(th, L_o), relative loads
+    uint32_t pua, puo;  // the run's first request: its uncached tokens on a and o
+    int32_t pth;        // and its threshold
+    uint32_t pad;
 };
+constexpr uint32_t kHeadBit = 1u << 29;
 
 // plan[0] = 1 for the serial path; plan[1] = 1 for the windowed path, whose
 // loads are 64-bit when plan[2] = 1.
@@ -298,6 +308,10 @@ __global__ __launch_bounds__(256) void sel_prep_kernel(
         p.w = aff2 ? ((d2 & 0xFF) | (d1 & 0xFF) << 8 | 1u << 28) : ((d1 & 0xFF) | (d2 & 0xFF) << 8);
         p.ua = (uint32_t)(aff2 ? u2 : u1);
         p.uo = (uint32_t)(aff2 ? u1 : u2);
+        p.pua = 0;
+        p.puo = 0;
+        p.pth = 0;
+        p.pad = 0;
         p.th = th;
         rec[r] = p;
         const bool ok = u1 >= 0 && u2 >= 0 && u1 <= INT32_MAX && u2 <= INT32_MAX;
@@ -356,21 +370,28 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
 
 // Depth of every request inside its 64-request window: 1 + the larger depth
 // of the latest earlier request of the window on either candidate (0 when
-// none).  Along every instance's requests the depth strictly grows, so the
-// requests of one depth touch pairwise distinct instances.
+// none), except that the second request of a two-request run takes the
+// depth of the first.  Along every instance's requests the depth strictly
+// grows outside runs, so the requests (runs) of one depth touch pairwise
+// distinct instances.
 constexpr int kLevelWaves = 4;
 
 __global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(SelPack* __restrict__ rec,
                                                                         uint64_t n)
 {
     __shared__ unsigned long long M[kLevelWaves][kFastMaxLive];
+    __shared__ uint32_t H[kLevelWaves][kWave];
     const int lane = lane_id(), wv = threadIdx.x >> 6;
     unsigned long long* m = M[wv];
     for (uint32_t k = lane; k < kFastMaxLive; k += kWave)
         m[k] = 0;
+    H[wv][lane] = 0;
     const uint64_t r = ((uint64_t)blockIdx.x * kLevelWaves + wv) * kWave + lane;
     const bool valid = r < n;
-    const uint32_t w = valid ? rec[r].w : 0;
+    SelPack me{};
+    if (valid)
+        me = rec[r];
+    const uint32_t w = me.w;
     const uint32_t a = w & 0xFF, o = (w >> 8) & 0xFF;
     const unsigned long long bit = 1ull << lane, lt = bit - 1;
     __syncthreads();
@@ -381,12 +402,27 @@ __global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(SelPack*
     __syncthreads();
     const unsigned long long P1 = valid ? m[a] & lt : 0, P2 = valid ? m[o] & lt : 0;
     const int p1 = P1 ? 63 - __clzll(P1) : lane, p2 = P2 ? 63 - __clzll(P2) : lane;
+    // run candidate: the latest earlier request on both instances is one
+    // request, on the same pair with the same cache-affine instance
+    const uint32_t pw = (uint32_t)__shfl((int)w, p1);
+    const bool cand = valid && P1 != 0 && p1 == p2 && a != o && (pw & 0xFFFFu) == (w & 0xFFFFu);
+    // runs of two: a candidate joins its predecessor unless that one has
+    // joined its own (the fixed point grows from each chain's head)
+    bool mg = cand;
+    for (;;) {
+        const bool pm = __shfl((int)mg, p1) != 0;
+        const bool nm = cand && !pm;
+        const bool changed = nm != mg;
+        mg = nm;
+        if (!__any(changed))
+            break;
+    }
     // Jacobi relaxation from depth 1: values only grow and reach the depths
     // after at most max-depth rounds; a round without change is the fixed point.
     int lv = valid ? 1 : 0;
     for (;;) {
         const int l1 = __shfl(lv, p1), l2 = __shfl(lv, p2);
-        const int nl = valid ? 1 + std::max(P1 ? l1 : 0, P2 ? l2 : 0) : 0;
+        const int nl = !valid ? 0 : (mg ? l1 : 1 + std::max(P1 ? l1 : 0, P2 ? l2 : 0));
         const bool changed = nl != lv;
         lv = nl;
         if (!__any(changed))
@@ -395,8 +431,21 @@ __global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(SelPack*
     int mx = lv;
     for (int d = 1; d < kWave; d <<= 1)
         mx = std::max(mx, __shfl_xor(mx, d));
-    if (valid)
-        rec[r].w = (w & 0x1000FFFFu) | (uint32_t)(lv - 1) << 16 | (uint32_t)(mx - 1) << 22;
+    const uint32_t pua = (uint32_t)__shfl((int)me.ua, p1), puo = (uint32_t)__shfl((int)me.uo, p1);
+    const int32_t pth = __shfl(me.th, p1);
+    if (mg)
+        H[wv][p1] = 1;
+    __syncthreads();
+    const bool head = H[wv][lane] != 0;
+    if (valid) {
+        SelPack q = me;
+        q.w = (w & 0x1000FFFFu) | (uint32_t)(lv - 1) << 16 | (uint32_t)(mx - 1) << 22 |
+              (head ? kHeadBit : 0u);
+        q.pua = mg ? pua : 0;
+        q.puo = mg ? puo : 0;
+        q.pth = mg ? pth : 0;
+        rec[r] = q;
+    }
 }
 
 // Walks the windows in order; see the file comment.  T is the load type:
@@ -413,12 +462,16 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
 
 // One depth of the 32-bit walk for the lanes whose depth is K + (l - rel),
 // i.e. whose rel equals the inline constant K.  Reads (XA, XO) of this depth
-// into one register set; captures the previous depth's reads (XAP, XOP,
-// lane mask MP) into (La, Lo); M receives this depth's lane mask.  A lane on
-// the depth writes its chosen instance, the others their spare slot; the
-// reads of a depth precede its write in the LDS queue, and the write of one
-// depth precedes the reads of the next.  Uses (a4, o4, sp4, rel, th, ua, uo,
-// La, Lo) from the enclosing scope.
+// into one register set, replays the run predecessor's decision (no change
+// when it has none) and leaves the result (X1, Y1) there: the loads this
+// request saw; captures the previous depth's (XAP, XOP, lane mask MP) into
+// (La, Lo); M receives this depth's lane mask.  Then the lane's own
+// decision, and both loads of the pair written back (the second instance
+// first, so that a pair of one instance keeps the first's value) -- to the
+// lane's write slots (wa, wo) when on the depth, else to its spare slot.
+// The reads of a depth precede its writes in the LDS queue, and the writes
+// of one depth precede the reads of the next.  Uses (a4, o4, wa, wo, sp4,
+// rel, th, ua, uo, pth, pua, puo, La, Lo) from the enclosing scope.
 #define DM_DEPTH_STEP(K, XA, XO, M, XAP, XOP, MP)                                             \
     do {                                                                                     \
         int32_t t1, t2, da, dz;                                                              \
@@ -427,23 +480,31 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
                      "v_cmp_eq_u32_e64 %[m], %[k], %[rel]\n\t"                               \
                      "v_cndmask_b32_e64 %[La], %[La], %[xap], %[mp]\n\t"                     \
                      "v_cndmask_b32_e64 %[Lo], %[Lo], %[xop], %[mp]\n\t"                     \
-                     "v_cndmask_b32_e64 %[da], %[sp], %[a4], %[m]\n\t"                       \
-                     "v_cndmask_b32_e64 %[dz], %[sp], %[o4], %[m]\n\t"                       \
+                     "v_cndmask_b32_e64 %[da], %[sp], %[wa], %[m]\n\t"                       \
+                     "v_cndmask_b32_e64 %[dz], %[sp], %[wo], %[m]\n\t"                       \
                      "s_waitcnt lgkmcnt(1)\n\t"                                              \
-                     "v_max_i32_e32 %[t1], %[th], %[xo]\n\t"                                 \
-                     "v_add_u32_e32 %[t2], %[xo], %[uo]\n\t"                                 \
+                     "v_max_i32_e32 %[t1], %[pth], %[xo]\n\t"                                \
                      "s_waitcnt lgkmcnt(0)\n\t"                                              \
                      "v_cmp_le_i32_e32 vcc, %[xa], %[t1]\n\t"                                \
+                     "v_cndmask_b32_e64 %[t1], %[puo], 0, vcc\n\t"                           \
+                     "v_cndmask_b32_e64 %[t2], 0, %[pua], vcc\n\t"                           \
+                     "v_add_u32_e32 %[xo], %[xo], %[t1]\n\t"                                 \
+                     "v_add_u32_e32 %[xa], %[xa], %[t2]\n\t"                                 \
+                     "v_max_i32_e32 %[t1], %[th], %[xo]\n\t"                                 \
+                     "v_add_u32_e32 %[t2], %[xo], %[uo]\n\t"                                 \
+                     "v_cmp_le_i32_e32 vcc, %[xa], %[t1]\n\t"                                \
                      "v_add_u32_e32 %[t1], %[xa], %[ua]\n\t"                                 \
-                     "v_cndmask_b32_e32 %[t2], %[t2], %[t1], vcc\n\t"                        \
-                     "v_cndmask_b32_e32 %[t1], %[dz], %[da], vcc\n\t"                        \
-                     "ds_write_b32 %[t1], %[t2]"                                             \
+                     "v_cndmask_b32_e32 %[t2], %[t2], %[xo], vcc\n\t"                        \
+                     "v_cndmask_b32_e32 %[t1], %[xa], %[t1], vcc\n\t"                        \
+                     "ds_write_b32 %[dz], %[t2]\n\t"                                         \
+                     "ds_write_b32 %[da], %[t1]"                                             \
                      : [xa] "=&v"(XA), [xo] "=&v"(XO), [m] "=&s"(M), [La] "+v"(La),          \
                        [Lo] "+v"(Lo), [t1] "=&v"(t1), [t2] "=&v"(t2), [da] "=&v"(da),        \
                        [dz] "=&v"(dz)                                                        \
-                     : [a4] "v"(a4), [o4] "v"(o4), [sp] "v"(sp4), [k] "n"(K), [rel] "v"(rel), \
-                       [xap] "v"(XAP), [xop] "v"(XOP), [mp] "s"(MP), [th] "v"(th),           \
-                       [ua] "v"(ua), [uo] "v"(uo)                                            \
+                     : [a4] "v"(a4), [o4] "v"(o4), [wa] "v"(wa), [wo] "v"(wo), [sp] "v"(sp4), \
+                       [k] "n"(K), [rel] "v"(rel), [xap] "v"(XAP), [xop] "v"(XOP),           \
+                       [mp] "s"(MP), [th] "v"(th), [ua] "v"(ua), [uo] "v"(uo),               \
+                       [pth] "v"(pth), [pua] "v"(pua), [puo] "v"(puo)                        \
                      : "vcc", "memory");                                                     \
     } while (0)
 
@@ -467,28 +528,40 @@ __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, ui
         const uint32_t mylv = valid ? (cur.w >> 16) & 63 : 64;
         const uint32_t depth = __builtin_amdgcn_readfirstlane((cur.w >> 22) & 63) + 1;
         const T ua = (T)cur.ua, uo = (T)cur.uo;
-        T th;
+        const T pua = (T)cur.pua, puo = (T)cur.puo;
+        const bool head = (cur.w & kHeadBit) != 0;
+        T th, pth;
         if (wide) {
-            // the packed bound is clamped to 32 bits: recompute it exactly,
-            // relative to the base (equal matches: -inf)
-            th = cur.th == INT32_MIN
-                     ? (T)INT64_MIN
-                     : (T)((slo - tbase - per * (int64_t)cur.ua + 1) * ((int64_t)1 << qshift) - 1 - b0);
+            // the packed bounds are clamped to 32 bits: recompute them
+            // exactly, relative to the base (equal matches: -inf)
+            auto exact = [&](int32_t packed, uint32_t u) -> T {
+                return packed == INT32_MIN
+                           ? (T)INT64_MIN
+                           : (T)((slo - tbase - per * (int64_t)u + 1) * ((int64_t)1 << qshift) - 1 - b0);
+            };
+            th = exact(cur.th, cur.ua);
+            pth = exact(cur.pth, cur.pua);
         } else {
             th = (T)cur.th;
+            pth = (T)cur.pth;
         }
         T La = 0, Lo = 0;
         if constexpr (wide) {
             // Every lane reads and writes at every depth, without branches; a
-            // lane not on the current depth writes its own spare slot.
+            // lane not on the current depth, and the first of a run, write
+            // their own spare slot.
+            const uint32_t sp = kFastMaxLive + lane;
+            const uint32_t wa = head ? sp : a, wo = head ? sp : o;
             for (uint32_t l = 0; l < depth; l++) {
-                const T xa = L[a], xo = L[o];
                 const bool act = mylv == l;
-                const bool take_a = xa <= std::max(th, xo);
-                const uint32_t dst = act ? (take_a ? a : o) : kFastMaxLive + lane;
-                L[dst] = take_a ? xa + ua : xo + uo;
-                La = act ? xa : La;
-                Lo = act ? xo : Lo;
+                const T xa = L[a], xo = L[o];
+                const bool pa = xa <= std::max(pth, xo);
+                const T x1 = xa + (pa ? pua : (T)0), y1 = xo + (pa ? (T)0 : puo);
+                const bool take_a = x1 <= std::max(th, y1);
+                L[act ? wo : sp] = take_a ? y1 : y1 + uo;
+                L[act ? wa : sp] = take_a ? x1 + ua : x1;
+                La = act ? x1 : La;
+                Lo = act ? y1 : Lo;
             }
         } else {
             // The same walk in hand-scheduled depth steps (DM_DEPTH_STEP): the
@@ -499,6 +572,7 @@ __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, ui
             // and two register sets alternate between consecutive depths.
             const uint32_t a4 = lds_addr(&L[a]), o4 = lds_addr(&L[o]);
             const uint32_t sp4 = lds_addr(&L[kFastMaxLive + lane]);
+            const uint32_t wa = head ? sp4 : a4, wo = head ? sp4 : o4;
             int32_t xa0 = 0, xo0 = 0, xa1 = 0, xo1 = 0;
             uint64_t m0 = 0, m1 = 0;
             // the steps count LDS completions only: no scalar load is in flight

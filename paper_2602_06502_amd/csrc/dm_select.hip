@@ -460,53 +460,93 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
     return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) T*)p;
 }
 
-// One depth of the 32-bit walk for the lanes whose depth is K + (l - rel),
-// i.e. whose rel equals the inline constant K.  Reads (XA, XO) of this depth
-// into one register set, replays the run predecessor's decision (no change
-// when it has none) and leaves the result (X1, Y1) there: the loads this
-// request saw; captures the previous depth's (XAP, XOP, lane mask MP) into
-// (La, Lo); M receives this depth's lane mask.  Then the lane's own
-// decision, and both loads of the pair written back (the second instance
-// first, so that a pair of one instance keeps the first's value) -- to the
-// lane's write slots (wa, wo) when on the depth, else to its spare slot.
-// The reads of a depth precede its writes in the LDS queue, and the writes
-// of one depth precede the reads of the next.  Uses (a4, o4, wa, wo, sp4,
-// rel, th, ua, uo, pth, pua, puo, La, Lo) from the enclosing scope.
-#define DM_DEPTH_STEP(K, XA, XO, M, XAP, XOP, MP)                                             \
-    do {                                                                                     \
-        int32_t t1, t2, da, dz;                                                              \
-        asm volatile("ds_read_b32 %[xo], %[o4]\n\t"                                          \
-                     "ds_read_b32 %[xa], %[a4]\n\t"                                          \
-                     "v_cmp_eq_u32_e64 %[m], %[k], %[rel]\n\t"                               \
-                     "v_cndmask_b32_e64 %[La], %[La], %[xap], %[mp]\n\t"                     \
-                     "v_cndmask_b32_e64 %[Lo], %[Lo], %[xop], %[mp]\n\t"                     \
-                     "v_cndmask_b32_e64 %[da], %[sp], %[wa], %[m]\n\t"                       \
-                     "v_cndmask_b32_e64 %[dz], %[sp], %[wo], %[m]\n\t"                       \
-                     "s_waitcnt lgkmcnt(1)\n\t"                                              \
-                     "v_max_i32_e32 %[t1], %[pth], %[xo]\n\t"                                \
-                     "s_waitcnt lgkmcnt(0)\n\t"                                              \
-                     "v_cmp_le_i32_e32 vcc, %[xa], %[t1]\n\t"                                \
-                     "v_cndmask_b32_e64 %[t1], %[puo], 0, vcc\n\t"                           \
-                     "v_cndmask_b32_e64 %[t2], 0, %[pua], vcc\n\t"                           \
-                     "v_add_u32_e32 %[xo], %[xo], %[t1]\n\t"                                 \
-                     "v_add_u32_e32 %[xa], %[xa], %[t2]\n\t"                                 \
-                     "v_max_i32_e32 %[t1], %[th], %[xo]\n\t"                                 \
-                     "v_add_u32_e32 %[t2], %[xo], %[uo]\n\t"                                 \
-                     "v_cmp_le_i32_e32 vcc, %[xa], %[t1]\n\t"                                \
-                     "v_add_u32_e32 %[t1], %[xa], %[ua]\n\t"                                 \
-                     "v_cndmask_b32_e32 %[t2], %[t2], %[xo], vcc\n\t"                        \
-                     "v_cndmask_b32_e32 %[t1], %[xa], %[t1], vcc\n\t"                        \
-                     "ds_write_b32 %[dz], %[t2]\n\t"                                         \
-                     "ds_write_b32 %[da], %[t1]"                                             \
-                     : [xa] "=&v"(XA), [xo] "=&v"(XO), [m] "=&s"(M), [La] "+v"(La),          \
-                       [Lo] "+v"(Lo), [t1] "=&v"(t1), [t2] "=&v"(t2), [da] "=&v"(da),        \
-                       [dz] "=&v"(dz)                                                        \
-                     : [a4] "v"(a4), [o4] "v"(o4), [wa] "v"(wa), [wo] "v"(wo), [sp] "v"(sp4), \
-                       [k] "n"(K), [rel] "v"(rel), [xap] "v"(XAP), [xop] "v"(XOP),           \
-                       [mp] "s"(MP), [th] "v"(th), [ua] "v"(ua), [uo] "v"(uo),               \
-                       [pth] "v"(pth), [pua] "v"(pua), [puo] "v"(puo)                        \
-                     : "vcc", "memory");                                                     \
-    } while (0)
+// One depth step of the 32-bit walk, as asm text for DM_WALK_BLOCK: the
+// lanes whose rel equals the inline constant K are on this depth.  Reads
+// (XA, XO) of this depth into one register set, replays the run
+// predecessor's decision (no change when it has none) and leaves the result
+// (X1, Y1) there: the loads this request saw; captures the previous step's
+// (XAP, XOP, lane mask MP) into (La, Lo); M receives this step's lane mask.
+// Then the lane's own decision, and both loads of the pair written back (the
+// second instance first, so that a pair of one instance keeps the first's
+// value) -- to the lane's write slots (wa, wo) when on the depth, else to its
+// spare slot.  The reads of a depth precede its writes in the LDS queue, and
+// the writes of one depth precede the reads of the next, so the waits count
+// this step's reads only.  Every step has the same instructions with
+// fixed-size encodings (operands are registers and inline constants), which
+// the computed entry relies on; the assembler checks the sizes.
+#define DM_STEP_TEXT(K, XA, XO, M, XAP, XOP, MP)                                               \
+    ".Ldmw%=_" #K ":\n\t"                                                                      \
+    "ds_read_b32 %[" XO "], %[o4]\n\t"                                                         \
+    "ds_read_b32 %[" XA "], %[a4]\n\t"                                                         \
+    "v_cmp_eq_u32_e64 %[" M "], " #K ", %[rel]\n\t"                                           \
+    "v_cndmask_b32_e64 %[La], %[La], %[" XAP "], %[" MP "]\n\t"                                \
+    "v_cndmask_b32_e64 %[Lo], %[Lo], %[" XOP "], %[" MP "]\n\t"                                \
+    "v_cndmask_b32_e64 %[da], %[sp], %[wa], %[" M "]\n\t"                                      \
+    "v_cndmask_b32_e64 %[dz], %[sp], %[wo], %[" M "]\n\t"                                      \
+    "s_waitcnt lgkmcnt(1)\n\t"                                                                 \
+    "v_max_i32_e32 %[t1], %[pth], %[" XO "]\n\t"                                               \
+    "s_waitcnt lgkmcnt(0)\n\t"                                                                 \
+    "v_cmp_le_i32_e32 vcc, %[" XA "], %[t1]\n\t"                                               \
+    "v_cndmask_b32_e64 %[t1], %[puo], 0, vcc\n\t"                                              \
+    "v_cndmask_b32_e64 %[t2], 0, %[pua], vcc\n\t"                                              \
+    "v_add_u32_e32 %[" XO "], %[" XO "], %[t1]\n\t"                                            \
+    "v_add_u32_e32 %[" XA "], %[" XA "], %[t2]\n\t"                                            \
+    "v_max_i32_e32 %[t1], %[th], %[" XO "]\n\t"                                                \
+    "v_add_u32_e32 %[t2], %[" XO "], %[uo]\n\t"                                                \
+    "v_cmp_le_i32_e32 vcc, %[" XA "], %[t1]\n\t"                                               \
+    "v_add_u32_e32 %[t1], %[" XA "], %[ua]\n\t"                                                \
+    "v_cndmask_b32_e32 %[t2], %[t2], %[" XO "], vcc\n\t"                                       \
+    "v_cndmask_b32_e32 %[t1], %[" XA "], %[t1], vcc\n\t"                                       \
+    "ds_write_b32 %[dz], %[t2]\n\t"                                                            \
+    "ds_write_b32 %[da], %[t1]\n\t"
+
+#define DM_STEP_PAIR(K0, K1)                                                                   \
+    DM_STEP_TEXT(K0, "xa0", "xo0", "m0", "xa1", "xo1", "m1")                                   \
+    DM_STEP_TEXT(K1, "xa1", "xo1", "m1", "xa0", "xo0", "m0")
+
+#define DM_SIZE_CHECK(K0, K1)                                                                  \
+    ".if (.Ldmw%=_" #K1 " - .Ldmw%=_" #K0 ") != (.Ldmw%=_1 - .Ldmw%=_0)\n\t"                   \
+    ".error \"walk steps differ in size\"\n\t"                                                 \
+    ".endif\n\t"
+
+// All depths of one window of the 32-bit walk in one block of 16 steps
+// (K = 0..15), entered at step e by a computed jump (the PC-relative
+// sequence of a long branch) and repeated nb times; lane l is on step K of
+// pass j when rel - 16 j = K, with rel = its depth + e.  Both lane masks start
+// empty, so the first step captures nothing; after the last pass, the last
+// depth's reads sit in (xa1, xo1, m1).  e < 16 by construction, and the
+// assembler checks that the 16 steps have one size.
+#define DM_WALK_BLOCK()                                                                        \
+    asm volatile("s_mov_b64 %[m0], 0\n\t"                                                      \
+                 "s_mov_b64 %[m1], 0\n\t"                                                      \
+                 "s_getpc_b64 s[96:97]\n"                                                      \
+                 ".Ldmw%=_pc:\n\t"                                                             \
+                 "s_mul_i32 s98, %[e], (.Ldmw%=_1 - .Ldmw%=_0)\n\t"                            \
+                 "s_add_u32 s98, s98, (.Ldmw%=_0 - .Ldmw%=_pc)\n\t"                            \
+                 "s_add_u32 s96, s96, s98\n\t"                                                 \
+                 "s_addc_u32 s97, s97, 0\n\t"                                                  \
+                 "s_setpc_b64 s[96:97]\n"                                                      \
+                 DM_STEP_PAIR(0, 1) DM_STEP_PAIR(2, 3) DM_STEP_PAIR(4, 5) DM_STEP_PAIR(6, 7)  \
+                 DM_STEP_PAIR(8, 9) DM_STEP_PAIR(10, 11) DM_STEP_PAIR(12, 13)                 \
+                 DM_STEP_PAIR(14, 15)                                                          \
+                 ".Ldmw%=_16:\n\t"                                                             \
+                 "v_add_u32_e32 %[rel], -16, %[rel]\n\t"                                       \
+                 "s_sub_u32 %[nb], %[nb], 1\n\t"                                               \
+                 "s_cmp_lg_u32 %[nb], 0\n\t"                                                   \
+                 "s_cbranch_scc1 .Ldmw%=_0\n\t"                                                \
+                 DM_SIZE_CHECK(1, 2) DM_SIZE_CHECK(2, 3) DM_SIZE_CHECK(3, 4)                   \
+                 DM_SIZE_CHECK(4, 5) DM_SIZE_CHECK(5, 6) DM_SIZE_CHECK(6, 7)                   \
+                 DM_SIZE_CHECK(7, 8) DM_SIZE_CHECK(8, 9) DM_SIZE_CHECK(9, 10)                  \
+                 DM_SIZE_CHECK(10, 11) DM_SIZE_CHECK(11, 12) DM_SIZE_CHECK(12, 13)             \
+                 DM_SIZE_CHECK(13, 14) DM_SIZE_CHECK(14, 15) DM_SIZE_CHECK(15, 16)             \
+                 : [xa0] "=&v"(xa0), [xo0] "=&v"(xo0), [xa1] "=&v"(xa1), [xo1] "=&v"(xo1),    \
+                   [m0] "=&s"(m0), [m1] "=&s"(m1), [La] "+v"(La), [Lo] "+v"(Lo),              \
+                   [t1] "=&v"(t1), [t2] "=&v"(t2), [da] "=&v"(da), [dz] "=&v"(dz),            \
+                   [rel] "+v"(rel), [nb] "+s"(nb)                                             \
+                 : [a4] "v"(a4), [o4] "v"(o4), [wa] "v"(wa), [wo] "v"(wo), [sp] "v"(sp4),     \
+                   [th] "v"(th), [ua] "v"(ua), [uo] "v"(uo), [pth] "v"(pth), [pua] "v"(pua),  \
+                   [puo] "v"(puo), [e] "s"(e)                                                  \
+                 : "s96", "s97", "s98", "vcc", "scc", "memory")
 
 template <typename T>
 __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, uint64_t n,
@@ -564,52 +604,22 @@ __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, ui
                 Lo = act ? y1 : Lo;
             }
         } else {
-            // The same walk in hand-scheduled depth steps (DM_DEPTH_STEP): the
+            // The same walk in hand-scheduled depth steps (DM_WALK_BLOCK): the
             // ALU work of a step that does not wait for its reads runs in the
-            // shadow of the LDS round trip, so the serial chain per depth is
-            // the round trip plus six ALU steps.  Steps come in groups of 8,
-            // 4, 2 and 1 with the depth compared against an inline constant,
-            // and two register sets alternate between consecutive depths.
+            // shadow of the LDS round trip, and the window's depths run as one
+            // straight block entered at the step that leaves exactly `depth`
+            // steps (a pass of 16 more per further 16 depths).
             const uint32_t a4 = lds_addr(&L[a]), o4 = lds_addr(&L[o]);
             const uint32_t sp4 = lds_addr(&L[kFastMaxLive + lane]);
             const uint32_t wa = head ? sp4 : a4, wo = head ? sp4 : o4;
-            int32_t xa0 = 0, xo0 = 0, xa1 = 0, xo1 = 0;
-            uint64_t m0 = 0, m1 = 0;
+            const uint32_t e = (0u - depth) & 15u;
+            uint32_t nb = (depth + 15u) >> 4, rel = mylv + e;
+            int32_t xa0, xo0, xa1, xo1, t1, t2, da, dz;
+            uint64_t m0, m1;
             // the steps count LDS completions only: no scalar load is in flight
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-            uint32_t l = 0;
-            for (; l + 8 <= depth; l += 8) {
-                const uint32_t rel = mylv - l;
-                DM_DEPTH_STEP(0, xa0, xo0, m0, xa1, xo1, m1);
-                DM_DEPTH_STEP(1, xa1, xo1, m1, xa0, xo0, m0);
-                DM_DEPTH_STEP(2, xa0, xo0, m0, xa1, xo1, m1);
-                DM_DEPTH_STEP(3, xa1, xo1, m1, xa0, xo0, m0);
-                DM_DEPTH_STEP(4, xa0, xo0, m0, xa1, xo1, m1);
-                DM_DEPTH_STEP(5, xa1, xo1, m1, xa0, xo0, m0);
-                DM_DEPTH_STEP(6, xa0, xo0, m0, xa1, xo1, m1);
-                DM_DEPTH_STEP(7, xa1, xo1, m1, xa0, xo0, m0);
-            }
-            if (l + 4 <= depth) {
-                const uint32_t rel = mylv - l;
-                DM_DEPTH_STEP(0, xa0, xo0, m0, xa1, xo1, m1);
-                DM_DEPTH_STEP(1, xa1, xo1, m1, xa0, xo0, m0);
-                DM_DEPTH_STEP(2, xa0, xo0, m0, xa1, xo1, m1);
-                DM_DEPTH_STEP(3, xa1, xo1, m1, xa0, xo0, m0);
-                l += 4;
-            }
-            if (l + 2 <= depth) {
-                const uint32_t rel = mylv - l;
-                DM_DEPTH_STEP(0, xa0, xo0, m0, xa1, xo1, m1);
-                DM_DEPTH_STEP(1, xa1, xo1, m1, xa0, xo0, m0);
-                l += 2;
-            }
-            if (l < depth) {
-                const uint32_t rel = mylv - l;
-                DM_DEPTH_STEP(0, xa0, xo0, m0, xa1, xo1, m1);
-                xa1 = xa0;
-                xo1 = xo0;
-                m1 = m0;
-            }
+            DM_WALK_BLOCK();
+            (void)xa0; (void)xo0; (void)m0; (void)t1; (void)t2; (void)da; (void)dz;
             // the last depth's reads are captured here
             if ((m1 >> lane) & 1) {
                 La = xa1;
@@ -651,7 +661,10 @@ __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, ui
         loads[live_ids[d]] = b0 + (int64_t)L[d];
 }
 
-#undef DM_DEPTH_STEP
+#undef DM_WALK_BLOCK
+#undef DM_SIZE_CHECK
+#undef DM_STEP_PAIR
+#undef DM_STEP_TEXT
 
 // One wave: 32-bit relative loads unless plan[2] asks for 64-bit ones.
 __global__ __launch_bounds__(kWave) void select_fast_kernel(

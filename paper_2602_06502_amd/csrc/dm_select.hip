@@ -224,16 +224,30 @@ __global__ __launch_bounds__(kWave) void select_lds_kernel(
 // with it (runs of two): both take the same depth, the second replays the
 // first's decision from (pua, puo, pth) before its own, and only the second
 // writes the pair's loads.  (pua, puo) = (0, 0) replays nothing.
+// Per-request record of the packing kernel.
 struct SelPack {
-    uint32_t w;
+    uint32_t w;   // a | o << 8 (dense indices) | 1 << 28 when a is c2
     uint32_t ua;  // uncached tokens on a
     uint32_t uo;  // uncached tokens on o
     int32_t th;   // take a iff L_a <= max(th, L_o), relative loads
+};
+
+// Per-request record of the walk, in the form its depth steps consume: the
+// LDS byte offsets (within the load array, 4-byte slots) of L_a and L_o,
+// where the request writes them (its spare slot when it is the first of a
+// run), rel = its depth (0-based) + the window's entry step e, and the
+// window's control word e | (passes - 1) << 4.  Lanes past the batch and
+// the padding windows are inert: every offset is the lane's spare slot and
+// rel matches no step.
+struct WalkRec {
+    uint32_t a4, o4, wa, wo;
+    uint32_t rel, ctl;
+    uint32_t ua, uo;
+    int32_t th;
     uint32_t pua, puo;  // the run's first request: its uncached tokens on a and o
     int32_t pth;        // and its threshold
-    uint32_t pad;
 };
-constexpr uint32_t kHeadBit = 1u << 29;
+constexpr uint32_t kInertRel = 0xFFFFFFFFu;
 
 // plan[0] = 1 for the serial path; plan[1] = 1 for the windowed path, whose
 // loads are 64-bit when plan[2] = 1.
@@ -308,10 +322,6 @@ __global__ __launch_bounds__(256) void sel_prep_kernel(
         p.w = aff2 ? ((d2 & 0xFF) | (d1 & 0xFF) << 8 | 1u << 28) : ((d1 & 0xFF) | (d2 & 0xFF) << 8);
         p.ua = (uint32_t)(aff2 ? u2 : u1);
         p.uo = (uint32_t)(aff2 ? u1 : u2);
-        p.pua = 0;
-        p.puo = 0;
-        p.pth = 0;
-        p.pad = 0;
         p.th = th;
         rec[r] = p;
         const bool ok = u1 >= 0 && u2 >= 0 && u1 <= INT32_MAX && u2 <= INT32_MAX;
@@ -373,24 +383,26 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
 // none), except that the second request of a two-request run takes the
 // depth of the first.  Along every instance's requests the depth strictly
 // grows outside runs, so the requests (runs) of one depth touch pairwise
-// distinct instances.
+// distinct instances.  Writes the walk record of every lane of nwin windows
+// (the batch's, then inert padding windows).
 constexpr int kLevelWaves = 4;
 
-__global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(SelPack* __restrict__ rec,
-                                                                        uint64_t n)
+__global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(
+    const SelPack* __restrict__ prep, uint64_t n, WalkRec* __restrict__ rec, uint64_t nwin)
 {
     __shared__ unsigned long long M[kLevelWaves][kFastMaxLive];
     __shared__ uint32_t H[kLevelWaves][kWave];
     const int lane = lane_id(), wv = threadIdx.x >> 6;
+    const uint64_t win = (uint64_t)blockIdx.x * kLevelWaves + wv;
     unsigned long long* m = M[wv];
     for (uint32_t k = lane; k < kFastMaxLive; k += kWave)
         m[k] = 0;
     H[wv][lane] = 0;
-    const uint64_t r = ((uint64_t)blockIdx.x * kLevelWaves + wv) * kWave + lane;
+    const uint64_t r = win * kWave + lane;
     const bool valid = r < n;
     SelPack me{};
     if (valid)
-        me = rec[r];
+        me = prep[r];
     const uint32_t w = me.w;
     const uint32_t a = w & 0xFF, o = (w >> 8) & 0xFF;
     const unsigned long long bit = 1ull << lane, lt = bit - 1;
@@ -437,22 +449,42 @@ __global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(SelPack*
         H[wv][p1] = 1;
     __syncthreads();
     const bool head = H[wv][lane] != 0;
+    if (win >= nwin)
+        return;
+    // the window's depth (at least one step, also for a window of inert
+    // lanes), its entry step e and its number of 16-step passes
+    const uint32_t depth = mx > 0 ? (uint32_t)mx : 1u;
+    const uint32_t e = (0u - depth) & 15u, passes = (depth + 15u) >> 4;
+    const uint32_t sp = 4u * (kFastMaxLive + lane);
+    WalkRec q;
+    q.ctl = e | (passes - 1) << 4;
     if (valid) {
-        SelPack q = me;
-        q.w = (w & 0x1000FFFFu) | (uint32_t)(lv - 1) << 16 | (uint32_t)(mx - 1) << 22 |
-              (head ? kHeadBit : 0u);
+        q.a4 = 4u * a;
+        q.o4 = 4u * o;
+        q.wa = head ? sp : q.a4;
+        q.wo = head ? sp : q.o4;
+        q.rel = (uint32_t)(lv - 1) + e;
+        q.ua = me.ua;
+        q.uo = me.uo;
+        q.th = me.th;
         q.pua = mg ? pua : 0;
         q.puo = mg ? puo : 0;
         q.pth = mg ? pth : 0;
-        rec[r] = q;
+    } else {
+        q.a4 = q.o4 = q.wa = q.wo = sp;
+        q.rel = kInertRel;
+        q.ua = q.uo = q.pua = q.puo = 0;
+        q.th = q.pth = 0;
     }
+    rec[r] = q;
 }
 
 // Walks the windows in order; see the file comment.  T is the load type:
-// int32_t or int64_t relative loads.  rec holds 2 * kPrefetch padding
+// int32_t or int64_t relative loads.  rec holds 2 * kPrefetch inert padding
 // windows past the last and lpre kPrefetch, so that the unrolled walk and
-// its prefetch stay in bounds; lpre receives the pre-update loads (L_c1,
-// L_c2) of every request, relative to the base.
+// its prefetch stay in bounds; lpre receives the pre-update loads (L_a, L_o)
+// of every request relative to the base, as int32 pairs for the 32-bit walk
+// and int64 pairs for the 64-bit one.
 // Byte address of a shared-memory element within the workgroup's LDS.
 template <typename T>
 __device__ __forceinline__ uint32_t lds_addr(T* p)
@@ -511,29 +543,35 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
 
 // All depths of one window of the 32-bit walk in one block of 16 steps
 // (K = 0..15), entered at step e by a computed jump (the PC-relative
-// sequence of a long branch) and repeated nb times; lane l is on step K of
-// pass j when rel - 16 j = K, with rel = its depth + e.  Both lane masks start
-// empty, so the first step captures nothing; after the last pass, the last
-// depth's reads sit in (xa1, xo1, m1).  e < 16 by construction, and the
-// assembler checks that the 16 steps have one size.
+// sequence of a long branch) and run np1 + 1 times, where the window's
+// control word (the same in every lane) is e | np1 << 4; lane l is on step K
+// of pass j when rel - 16 j = K.  The control word is read inside the block,
+// so that the compiler waits only for this window's record.  The first step
+// captures whatever its register set held, which is harmless: every lane of
+// the batch is captured again after its own depth, and inert lanes' results
+// are never read.  After the last pass the last depth's reads are captured
+// into (La, Lo).  e < 16 and np1 < 4 by the masks, and the assembler checks
+// that the 16 steps have one size.
 #define DM_WALK_BLOCK()                                                                        \
-    asm volatile("s_mov_b64 %[m0], 0\n\t"                                                      \
-                 "s_mov_b64 %[m1], 0\n\t"                                                      \
+    asm volatile("v_readfirstlane_b32 s99, %[ctl]\n\t"                                         \
                  "s_getpc_b64 s[96:97]\n"                                                      \
                  ".Ldmw%=_pc:\n\t"                                                             \
-                 "s_mul_i32 s98, %[e], (.Ldmw%=_1 - .Ldmw%=_0)\n\t"                            \
+                 "s_and_b32 s98, s99, 15\n\t"                                                  \
+                 "s_mul_i32 s98, s98, (.Ldmw%=_1 - .Ldmw%=_0)\n\t"                             \
                  "s_add_u32 s98, s98, (.Ldmw%=_0 - .Ldmw%=_pc)\n\t"                            \
                  "s_add_u32 s96, s96, s98\n\t"                                                 \
                  "s_addc_u32 s97, s97, 0\n\t"                                                  \
+                 "s_bfe_u32 s99, s99, 0x20004\n\t"                                             \
                  "s_setpc_b64 s[96:97]\n"                                                      \
                  DM_STEP_PAIR(0, 1) DM_STEP_PAIR(2, 3) DM_STEP_PAIR(4, 5) DM_STEP_PAIR(6, 7)  \
                  DM_STEP_PAIR(8, 9) DM_STEP_PAIR(10, 11) DM_STEP_PAIR(12, 13)                 \
                  DM_STEP_PAIR(14, 15)                                                          \
                  ".Ldmw%=_16:\n\t"                                                             \
                  "v_add_u32_e32 %[rel], -16, %[rel]\n\t"                                       \
-                 "s_sub_u32 %[nb], %[nb], 1\n\t"                                               \
-                 "s_cmp_lg_u32 %[nb], 0\n\t"                                                   \
-                 "s_cbranch_scc1 .Ldmw%=_0\n\t"                                                \
+                 "s_sub_u32 s99, s99, 1\n\t"                                                   \
+                 "s_cbranch_scc0 .Ldmw%=_0\n\t"                                                \
+                 "v_cndmask_b32_e64 %[La], %[La], %[xa1], %[m1]\n\t"                           \
+                 "v_cndmask_b32_e64 %[Lo], %[Lo], %[xo1], %[m1]\n\t"                           \
                  DM_SIZE_CHECK(1, 2) DM_SIZE_CHECK(2, 3) DM_SIZE_CHECK(3, 4)                   \
                  DM_SIZE_CHECK(4, 5) DM_SIZE_CHECK(5, 6) DM_SIZE_CHECK(6, 7)                   \
                  DM_SIZE_CHECK(7, 8) DM_SIZE_CHECK(8, 9) DM_SIZE_CHECK(9, 10)                  \
@@ -542,14 +580,14 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
                  : [xa0] "=&v"(xa0), [xo0] "=&v"(xo0), [xa1] "=&v"(xa1), [xo1] "=&v"(xo1),    \
                    [m0] "=&s"(m0), [m1] "=&s"(m1), [La] "+v"(La), [Lo] "+v"(Lo),              \
                    [t1] "=&v"(t1), [t2] "=&v"(t2), [da] "=&v"(da), [dz] "=&v"(dz),            \
-                   [rel] "+v"(rel), [nb] "+s"(nb)                                             \
+                   [rel] "+v"(rel)                                                            \
                  : [a4] "v"(a4), [o4] "v"(o4), [wa] "v"(wa), [wo] "v"(wo), [sp] "v"(sp4),     \
                    [th] "v"(th), [ua] "v"(ua), [uo] "v"(uo), [pth] "v"(pth), [pua] "v"(pua),  \
-                   [puo] "v"(puo), [e] "s"(e)                                                  \
-                 : "s96", "s97", "s98", "vcc", "scc", "memory")
+                   [puo] "v"(puo), [ctl] "v"(ctl)                                              \
+                 : "s96", "s97", "s98", "s99", "vcc", "scc", "memory")
 
 template <typename T>
-__device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, uint64_t n,
+__device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec, uint64_t n,
                                              const uint32_t* __restrict__ live_ids,
                                              uint32_t n_live, int64_t* __restrict__ loads,
                                              int64_t b0, longlong2* __restrict__ lpre,
@@ -562,16 +600,15 @@ __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, ui
         L[d] = d < n_live ? (T)(loads[live_ids[d]] - b0) : (T)0;
     __syncthreads();
     const uint64_t nw = (n + kWave - 1) / kWave;
-    auto window = [&](const SelPack& cur, uint64_t w) {
-        const bool valid = w * kWave + lane < n;
-        const uint32_t a = cur.w & 0xFF, o = (cur.w >> 8) & 0xFF;
-        const uint32_t mylv = valid ? (cur.w >> 16) & 63 : 64;
-        const uint32_t depth = __builtin_amdgcn_readfirstlane((cur.w >> 22) & 63) + 1;
+    // the records hold offsets within L in 4-byte slots; the LDS address of
+    // L itself is a link-time constant (zero when it is the only array)
+    const uint32_t lbase = lds_addr(reinterpret_cast<int32_t*>(L));
+    const uint32_t sp4 = lbase + 4u * (kFastMaxLive + lane);
+    int32_t La32 = 0, Lo32 = 0;
+    auto window = [&](WalkRec& cur, uint64_t w) {
         const T ua = (T)cur.ua, uo = (T)cur.uo;
         const T pua = (T)cur.pua, puo = (T)cur.puo;
-        const bool head = (cur.w & kHeadBit) != 0;
-        T th, pth;
-        if (wide) {
+        if constexpr (wide) {
             // the packed bounds are clamped to 32 bits: recompute them
             // exactly, relative to the base (equal matches: -inf)
             auto exact = [&](int32_t packed, uint32_t u) -> T {
@@ -579,19 +616,15 @@ __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, ui
                            ? (T)INT64_MIN
                            : (T)((slo - tbase - per * (int64_t)u + 1) * ((int64_t)1 << qshift) - 1 - b0);
             };
-            th = exact(cur.th, cur.ua);
-            pth = exact(cur.pth, cur.pua);
-        } else {
-            th = (T)cur.th;
-            pth = (T)cur.pth;
-        }
-        T La = 0, Lo = 0;
-        if constexpr (wide) {
+            const T th = exact(cur.th, cur.ua), pth = exact(cur.pth, cur.pua);
             // Every lane reads and writes at every depth, without branches; a
             // lane not on the current depth, and the first of a run, write
             // their own spare slot.
-            const uint32_t sp = kFastMaxLive + lane;
-            const uint32_t wa = head ? sp : a, wo = head ? sp : o;
+            const uint32_t ctl = __builtin_amdgcn_readfirstlane(cur.ctl), e = ctl & 15u;
+            const uint32_t depth = 16u * (((ctl >> 4) & 3u) + 1u) - e;
+            const uint32_t a = cur.a4 >> 2, o = cur.o4 >> 2, wa = cur.wa >> 2, wo = cur.wo >> 2;
+            const uint32_t sp = kFastMaxLive + lane, mylv = cur.rel - e;
+            T La = 0, Lo = 0;
             for (uint32_t l = 0; l < depth; l++) {
                 const bool act = mylv == l;
                 const T xa = L[a], xo = L[o];
@@ -603,41 +636,44 @@ __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, ui
                 La = act ? x1 : La;
                 Lo = act ? y1 : Lo;
             }
+            lpre[w * kWave + lane] = make_longlong2(La, Lo);
         } else {
             // The same walk in hand-scheduled depth steps (DM_WALK_BLOCK): the
             // ALU work of a step that does not wait for its reads runs in the
             // shadow of the LDS round trip, and the window's depths run as one
-            // straight block entered at the step that leaves exactly `depth`
-            // steps (a pass of 16 more per further 16 depths).
-            const uint32_t a4 = lds_addr(&L[a]), o4 = lds_addr(&L[o]);
-            const uint32_t sp4 = lds_addr(&L[kFastMaxLive + lane]);
-            const uint32_t wa = head ? sp4 : a4, wo = head ? sp4 : o4;
-            const uint32_t e = (0u - depth) & 15u;
-            uint32_t nb = (depth + 15u) >> 4, rel = mylv + e;
+            // straight block entered at the step that leaves exactly its
+            // depth's steps (a pass of 16 more per further 16 depths).
+            const uint32_t a4 = lbase + cur.a4, o4 = lbase + cur.o4;
+            const uint32_t wa = lbase + cur.wa, wo = lbase + cur.wo;
+            const int32_t th = cur.th, pth = cur.pth;
+            const uint32_t ctl = cur.ctl;
+            uint32_t rel = cur.rel;
             int32_t xa0, xo0, xa1, xo1, t1, t2, da, dz;
             uint64_t m0, m1;
-            // the steps count LDS completions only: no scalar load is in flight
-            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            int32_t La = La32, Lo = Lo32;
             DM_WALK_BLOCK();
-            (void)xa0; (void)xo0; (void)m0; (void)t1; (void)t2; (void)da; (void)dz;
-            // the last depth's reads are captured here
-            if ((m1 >> lane) & 1) {
-                La = xa1;
-                Lo = xo1;
-            }
+            (void)xa0; (void)xo0; (void)xa1; (void)xo1; (void)m0; (void)m1;
+            (void)t1; (void)t2; (void)da; (void)dz;
+            La32 = La;
+            Lo32 = Lo;
+            reinterpret_cast<int2*>(lpre)[w * kWave + lane] = make_int2(La, Lo);
         }
-        const bool flip = (cur.w >> 28) & 1;
-        lpre[w * kWave + lane] = flip ? make_longlong2(Lo, La) : make_longlong2(La, Lo);
     };
     static_assert(kPrefetch == 8, "the walk below holds eight record windows");
     // Records arrive kPrefetch windows ahead.  The loop is unrolled by
     // kPrefetch so that each slot is used where it was loaded (no register
     // moves, which would wait for every load in flight); windows past the
-    // last (all lanes invalid, padded records and outputs) change nothing.
-    SelPack q0 = rec[0 * kWave + lane], q1 = rec[1 * kWave + lane];
-    SelPack q2 = rec[2 * kWave + lane], q3 = rec[3 * kWave + lane];
-    SelPack q4 = rec[4 * kWave + lane], q5 = rec[5 * kWave + lane];
-    SelPack q6 = rec[6 * kWave + lane], q7 = rec[7 * kWave + lane];
+    // last (inert padded records and outputs) change nothing.
+    WalkRec q0 = rec[0 * kWave + lane], q1 = rec[1 * kWave + lane];
+    WalkRec q2 = rec[2 * kWave + lane], q3 = rec[3 * kWave + lane];
+    WalkRec q4 = rec[4 * kWave + lane], q5 = rec[5 * kWave + lane];
+    WalkRec q6 = rec[6 * kWave + lane], q7 = rec[7 * kWave + lane];
+    // Let the first records land before the loop: the wait the compiler
+    // places at the loop head must hold on entry as well as on the
+    // back-edge, and with these loads in flight on entry it would wait for
+    // every record in flight on each iteration.  (s_waitcnt vmcnt(0),
+    // expcnt and lgkmcnt unconstrained, in the gfx9 encoding.)
+    __builtin_amdgcn_s_waitcnt(0x0F70);
     for (uint64_t w = 0; w < nw; w += kPrefetch) {
         window(q0, w);
         q0 = rec[(w + 8) * kWave + lane];
@@ -668,7 +704,7 @@ __device__ __forceinline__ void walk_windows(const SelPack* __restrict__ rec, ui
 
 // One wave: 32-bit relative loads unless plan[2] asks for 64-bit ones.
 __global__ __launch_bounds__(kWave) void select_fast_kernel(
-    const SelPack* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ live_ids,
+    const WalkRec* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ live_ids,
     uint32_t n_live, int64_t* __restrict__ loads, const uint32_t* __restrict__ plan,
     const int64_t* __restrict__ base, longlong2* __restrict__ lpre, int64_t tbase, int64_t per,
     uint32_t qshift, int64_t slo)
@@ -698,12 +734,25 @@ __global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, 
 {
     if (!plan[1])
         return;
-    const int64_t b0 = plan[2] ? base[0] : 0;
+    const bool wide = plan[2] != 0;
+    const int64_t b0 = wide ? base[0] : 0;
     for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
          r += (uint64_t)gridDim.x * blockDim.x) {
         SelRec s = load_rec(offsets, n, r, true, bshift, cand, match, tbase, per, qshift, slo);
-        const longlong2 lp = lpre[r];
-        store_out(s, r, b0 + lp.x, b0 + lp.y, flags, chosen, ttft, tbase, per, qshift, slo);
+        int64_t La, Lo;
+        if (wide) {
+            const longlong2 lp = lpre[r];
+            La = lp.x;
+            Lo = lp.y;
+        } else {
+            const int2 lp = reinterpret_cast<const int2*>(lpre)[r];
+            La = lp.x;
+            Lo = lp.y;
+        }
+        // the walk records (L_a, L_o); a is c2 when c2 has the longer match
+        const bool a_is_c2 = s.kind == 0;
+        store_out(s, r, b0 + (a_is_c2 ? Lo : La), b0 + (a_is_c2 ? La : Lo), flags, chosen, ttft,
+                  tbase, per, qshift, slo);
     }
 }
 
@@ -721,33 +770,38 @@ void launch_select(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint64_t n
 
 }  // namespace
 
-// Work arrays of one batch in flight: records (kPrefetch padding windows),
-// pre-update loads, base/plan words and growth bounds.  Two such sets live
-// in the selection slot, one per batch parity.
+// Work arrays of one batch in flight: packing records, walk records
+// (2 * kPrefetch inert padding windows), pre-update loads (kPrefetch padding
+// windows), base/plan words and growth bounds.  Two such sets live in the
+// selection slot, one per batch parity.
 struct SelBuf {
-    SelPack* rec;
+    SelPack* prep;
+    WalkRec* rec;
     longlong2* lpre;
     int64_t* base;
     uint32_t* plan;
     unsigned long long* grow;
+    uint64_t nwin;  // windows of walk records
 };
 
 static hipError_t sel_buffers(dm_ctx* c, uint64_t n, int par, SelBuf* b)
 {
     hipError_t e = hipSuccess;
     const uint64_t nw = (n + kWave - 1) / kWave;
-    const uint64_t nrec = (nw + 2 * kPrefetch) * kWave;
-    const size_t rec_bytes = (nrec * sizeof(SelPack) + 255) & ~size_t(255);
+    b->nwin = nw + 2 * kPrefetch;
+    const size_t prep_bytes = (n * sizeof(SelPack) + 255) & ~size_t(255);
+    const size_t rec_bytes = (b->nwin * kWave * sizeof(WalkRec) + 255) & ~size_t(255);
     const size_t lpre_bytes = ((nw + kPrefetch) * kWave * sizeof(longlong2) + 255) & ~size_t(255);
     const size_t tail_bytes = 256 + (kMaxSlots + 1) * sizeof(unsigned long long);
-    const size_t one = (rec_bytes + lpre_bytes + tail_bytes + 255) & ~size_t(255);
+    const size_t one = (prep_bytes + rec_bytes + lpre_bytes + tail_bytes + 255) & ~size_t(255);
     uint8_t* sw = static_cast<uint8_t*>(scratch_get(c, kSelSlot, 2 * one, &e));
     if (!sw)
         return e;
     sw += par * one;
-    b->rec = reinterpret_cast<SelPack*>(sw);
-    b->lpre = reinterpret_cast<longlong2*>(sw + rec_bytes);
-    uint8_t* tail = sw + rec_bytes + lpre_bytes;
+    b->prep = reinterpret_cast<SelPack*>(sw);
+    b->rec = reinterpret_cast<WalkRec*>(sw + prep_bytes);
+    b->lpre = reinterpret_cast<longlong2*>(sw + prep_bytes + rec_bytes);
+    uint8_t* tail = sw + prep_bytes + rec_bytes + lpre_bytes;
     b->base = reinterpret_cast<int64_t*>(tail);
     b->plan = reinterpret_cast<uint32_t*>(tail + 128);
     b->grow = reinterpret_cast<unsigned long long*>(tail + 256);
@@ -769,8 +823,7 @@ hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uin
     hipError_t e = sel_buffers(c, n, par, &b);
     if (e != hipSuccess)
         return e;
-    const uint64_t nw = (n + kWave - 1) / kWave;
-    const uint64_t lgrid = (nw + kLevelWaves - 1) / kLevelWaves;
+    const uint64_t lgrid = (b.nwin + kLevelWaves - 1) / kLevelWaves;
     if (lgrid > 0x7FFFFFFFull)
         return hipErrorInvalidValue;
     const uint32_t NL = c->n_live;
@@ -780,8 +833,8 @@ hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uin
     // ones with one atomic per instance, and those atomics meet on a few lines
     sel_prep_kernel<<<grid_for(n, 256, 512), 256, 0, st>>>(
         offsets, n, block_shift(c), out->cand, out->match, c->d_dense, NL, k.ttft_base_us,
-        k.ttft_per_token_us, c->shift_div, k.slo_us, b.rec, b.grow);
-    sel_level_kernel<<<(uint32_t)lgrid, kLevelWaves * kWave, 0, st>>>(b.rec, n);
+        k.ttft_per_token_us, c->shift_div, k.slo_us, b.prep, b.grow);
+    sel_level_kernel<<<(uint32_t)lgrid, kLevelWaves * kWave, 0, st>>>(b.prep, n, b.rec, b.nwin);
     return hipGetLastError();
 }
 

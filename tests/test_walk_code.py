@@ -44,15 +44,20 @@ def test_walk_entries_land_on_step_starts(tmp_path):
         if text != "s_getpc_b64 s[96:97]":
             continue
         blocks += 1
+        # the window's control word e | (passes - 1) << 4 is read just before
+        assert re.fullmatch(r"v_readfirstlane_b32 s99, v\d+", ins[i - 1][1]), ins[i - 1]
         pc = ins[i + 1][0]  # s_getpc_b64 yields the address of the next instruction
-        mul = re.fullmatch(r"s_mul_i32 s98, s\d+, " + lit, ins[i + 1][1])
-        add = re.fullmatch(r"s_add_u32 s98, s98, " + lit, ins[i + 2][1])
-        assert mul and add, (ins[i + 1], ins[i + 2])
-        assert ins[i + 3][1] == "s_add_u32 s96, s96, s98"
-        assert ins[i + 4][1] == "s_addc_u32 s97, s97, 0"
-        assert ins[i + 5][1] == "s_setpc_b64 s[96:97]"
+        assert ins[i + 1][1] == "s_and_b32 s98, s99, 15", ins[i + 1]  # e < 16
+        mul = re.fullmatch(r"s_mul_i32 s98, s98, " + lit, ins[i + 2][1])
+        add = re.fullmatch(r"s_add_u32 s98, s98, " + lit, ins[i + 3][1])
+        assert mul and add, (ins[i + 2], ins[i + 3])
+        assert ins[i + 4][1] == "s_add_u32 s96, s96, s98"
+        assert ins[i + 5][1] == "s_addc_u32 s97, s97, 0"
+        # passes - 1 = bits 4..5 of the control word: at most four passes
+        assert ins[i + 6][1] == "s_bfe_u32 s99, s99, 0x20004", ins[i + 6]
+        assert ins[i + 7][1] == "s_setpc_b64 s[96:97]"
         step, off = int(mul.group(1), 0), int(add.group(1), 0)
-        assert pc + off == ins[i + 6][0], "entry 0 is not the instruction after the jump"
+        assert pc + off == ins[i + 8][0], "entry 0 is not the instruction after the jump"
         for e in range(16):
             tgt = pc + e * step + off
             assert tgt in at, f"entry {e} lands inside an instruction"
@@ -63,8 +68,9 @@ def test_walk_entries_land_on_step_starts(tmp_path):
             assert m and int(m.group(1)) == e, (e, ins[j + 2])
         j = at[pc + 16 * step + off]
         assert re.fullmatch(r"v_add_u32_e32 (v\d+), -16, \1", ins[j][1]), ins[j]
-        br_addr, br = ins[j + 3]
-        assert br.startswith("s_cbranch_scc1"), br
+        assert ins[j + 1][1] == "s_sub_u32 s99, s99, 1", ins[j + 1]
+        br_addr, br = ins[j + 2]
+        assert br.startswith("s_cbranch_scc0"), br
         simm = int(br.split()[-1], 0)
         simm = simm - 65536 if simm >= 32768 else simm
         assert br_addr + 4 + 4 * simm == pc + off, "back-edge does not return to step 0"

@@ -378,105 +378,240 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
     }
 }
 
-// Depth of every request inside its 64-request window: 1 + the larger depth
-// of the latest earlier request of the window on either candidate (0 when
-// none), except that the second request of a two-request run takes the
-// depth of the first.  Along every instance's requests the depth strictly
-// grows outside runs, so the requests (runs) of one depth touch pairwise
-// distinct instances.  Writes the walk record of every lane of nwin windows
-// (the batch's, then inert padding windows).
-constexpr int kLevelWaves = 4;
+// Walk windows from dependency levels.  Requests are grouped in blocks of
+// kLevelBlock (request order).  Inside a block, a request's level is 1 + the
+// larger level of the latest earlier request of the block on either
+// candidate (0 when none), except that a run's second request -- whose
+// latest earlier request on both instances is one request of the same pair
+// and cache-affine instance, itself not a second -- takes its head's level.
+// Along every instance's requests the level strictly grows outside runs, so
+// the requests (runs) of one level touch pairwise distinct instances, and
+// any order of the levels' requests that keeps levels in order and the
+// blocks in order gives every request exactly the loads of the one-by-one
+// walk.  Windows of at most 64 lanes take whole consecutive levels; a level
+// that does not fit starts a new window, and a level of more than 64
+// requests is split between windows with runs kept whole.  Any two
+// consecutive windows of a block hold at least 64 requests, so a block has
+// at most 2 * ceil(kLevelBlock / 64) + 1 windows.
+constexpr uint32_t kLevelBlock = 1024;
+constexpr uint32_t kWinCap = 36;  // windows per block; the bound above is 33
 
-__global__ __launch_bounds__(kLevelWaves * kWave) void sel_level_kernel(
-    const SelPack* __restrict__ prep, uint64_t n, WalkRec* __restrict__ rec, uint64_t nwin)
+// One wave per block: lane 0 runs the block's requests in order (levels and
+// runs), then its levels in order (windows).  Writes, per request, info =
+// depth in its window | head << 6 | second << 7 | head index << 8; per
+// block, its window count, each window's depth and the block-local request
+// index in every window lane (0xFFFF for none).
+__global__ __launch_bounds__(kWave) void sel_level_kernel(
+    const SelPack* __restrict__ prep, uint64_t n, uint32_t* __restrict__ info,
+    uint16_t* __restrict__ slotmap, uint8_t* __restrict__ wdepth, uint32_t* __restrict__ wcount,
+    uint32_t* __restrict__ status)
 {
-    __shared__ unsigned long long M[kLevelWaves][kFastMaxLive];
-    __shared__ uint32_t H[kLevelWaves][kWave];
-    const int lane = lane_id(), wv = threadIdx.x >> 6;
-    const uint64_t win = (uint64_t)blockIdx.x * kLevelWaves + wv;
-    unsigned long long* m = M[wv];
-    for (uint32_t k = lane; k < kFastMaxLive; k += kWave)
-        m[k] = 0;
-    H[wv][lane] = 0;
-    const uint64_t r = win * kWave + lane;
-    const bool valid = r < n;
-    SelPack me{};
-    if (valid)
-        me = prep[r];
-    const uint32_t w = me.w;
-    const uint32_t a = w & 0xFF, o = (w >> 8) & 0xFF;
-    const unsigned long long bit = 1ull << lane, lt = bit - 1;
+    __shared__ uint16_t W[kLevelBlock];       // a | o << 8
+    __shared__ uint16_t lv[kLevelBlock];      // level
+    __shared__ uint16_t nxt[kLevelBlock];     // next run head of the same level, + 1
+    __shared__ uint16_t mate[kLevelBlock];    // head: its second; second: its head
+    __shared__ uint8_t fl[kLevelBlock];       // bit0 second of a run, bit1 head of a run
+    __shared__ uint16_t last[kFastMaxLive];   // latest request on each instance, + 1
+    __shared__ uint16_t lhead[kLevelBlock + 1], ltail[kLevelBlock + 1], cnt[kLevelBlock + 1];
+    __shared__ uint32_t inf[kLevelBlock];
+    __shared__ uint16_t smap[kWinCap * kWave];
+    __shared__ uint8_t wdep[kWinCap];
+    __shared__ uint32_t nwin;
+    const int lane = lane_id();
+    const uint64_t r0 = (uint64_t)blockIdx.x * kLevelBlock;
+    const uint32_t nb = (uint32_t)std::min<uint64_t>(kLevelBlock, n - r0);
+    for (uint32_t i = lane; i < kLevelBlock; i += kWave) {
+        W[i] = i < nb ? (uint16_t)(prep[r0 + i].w & 0xFFFFu) : 0;
+        fl[i] = 0;
+        inf[i] = 0;
+    }
+    for (uint32_t i = lane; i <= kLevelBlock; i += kWave)
+        lhead[i] = ltail[i] = cnt[i] = 0;
+    for (uint32_t i = lane; i < kFastMaxLive; i += kWave)
+        last[i] = 0;
+    for (uint32_t i = lane; i < kWinCap * kWave; i += kWave)
+        smap[i] = 0xFFFF;
     __syncthreads();
-    if (valid) {
-        atomicOr(&m[a], bit);
-        atomicOr(&m[o], bit);
+    if (lane == 0) {
+        uint32_t Lmax = 0;
+        for (uint32_t i = 0; i < nb; i++) {
+            const uint32_t w = W[i], a = w & 0xFF, o = w >> 8;
+            const int pa = (int)last[a] - 1, po = (int)last[o] - 1;
+            const bool run = pa >= 0 && pa == po && a != o && !(fl[pa] & 1) && W[pa] == w;
+            uint32_t L;
+            if (run) {
+                L = lv[pa];
+                fl[i] = 1;
+                fl[pa] |= 2;
+                mate[pa] = (uint16_t)i;
+                mate[i] = (uint16_t)pa;
+            } else {
+                L = 1 + std::max(pa >= 0 ? (uint32_t)lv[pa] : 0u, po >= 0 ? (uint32_t)lv[po] : 0u);
+                nxt[i] = 0;
+                if (lhead[L] == 0)
+                    lhead[L] = (uint16_t)(i + 1);
+                else
+                    nxt[ltail[L] - 1] = (uint16_t)(i + 1);
+                ltail[L] = (uint16_t)(i + 1);
+            }
+            lv[i] = (uint16_t)L;
+            cnt[L]++;
+            last[a] = last[o] = (uint16_t)(i + 1);
+            Lmax = L > Lmax ? L : Lmax;
+        }
+        uint32_t win = 0, lanes = 0, dep = 0;
+        bool ok = true;
+        for (uint32_t L = 1; L <= Lmax && ok; L++) {
+            if (lanes > 0 && lanes + cnt[L] > kWave) {  // the level does not fit: next window
+                wdep[win++] = (uint8_t)dep;
+                lanes = dep = 0;
+            }
+            dep++;
+            for (uint32_t u1 = lhead[L]; u1 != 0; u1 = nxt[u1 - 1]) {
+                const uint32_t u = u1 - 1, sz = (fl[u] & 2) ? 2 : 1;
+                if (lanes + sz > kWave) {  // a level of more than 64 requests: split
+                    wdep[win++] = (uint8_t)dep;
+                    lanes = 0;
+                    dep = 1;
+                }
+                if (win >= kWinCap) {
+                    ok = false;
+                    break;
+                }
+                const uint32_t d = dep - 1;
+                smap[win * kWave + lanes] = (uint16_t)u;
+                inf[u] = d | (sz == 2 ? 1u << 6 : 0u);
+                if (sz == 2) {
+                    const uint32_t v = mate[u];
+                    smap[win * kWave + lanes + 1] = (uint16_t)v;
+                    inf[v] = d | 1u << 7 | u << 8;
+                }
+                lanes += sz;
+            }
+        }
+        if (ok && lanes > 0) {
+            if (win >= kWinCap)
+                ok = false;
+            else
+                wdep[win++] = (uint8_t)dep;
+        }
+        if (!ok) {  // cannot happen (see above); no window of this block is walked
+            atomicOr(status, kErrInval);
+            win = 0;
+        }
+        nwin = win;
     }
     __syncthreads();
-    const unsigned long long P1 = valid ? m[a] & lt : 0, P2 = valid ? m[o] & lt : 0;
-    const int p1 = P1 ? 63 - __clzll(P1) : lane, p2 = P2 ? 63 - __clzll(P2) : lane;
-    // run candidate: the latest earlier request on both instances is one
-    // request, on the same pair with the same cache-affine instance
-    const uint32_t pw = (uint32_t)__shfl((int)w, p1);
-    const bool cand = valid && P1 != 0 && p1 == p2 && a != o && (pw & 0xFFFFu) == (w & 0xFFFFu);
-    // runs of two: a candidate joins its predecessor unless that one has
-    // joined its own (the fixed point grows from each chain's head)
-    bool mg = cand;
-    for (;;) {
-        const bool pm = __shfl((int)mg, p1) != 0;
-        const bool nm = cand && !pm;
-        const bool changed = nm != mg;
-        mg = nm;
-        if (!__any(changed))
-            break;
-    }
-    // Jacobi relaxation from depth 1: values only grow and reach the depths
-    // after at most max-depth rounds; a round without change is the fixed point.
-    int lv = valid ? 1 : 0;
-    for (;;) {
-        const int l1 = __shfl(lv, p1), l2 = __shfl(lv, p2);
-        const int nl = !valid ? 0 : (mg ? l1 : 1 + std::max(P1 ? l1 : 0, P2 ? l2 : 0));
-        const bool changed = nl != lv;
-        lv = nl;
-        if (!__any(changed))
-            break;
-    }
-    int mx = lv;
-    for (int d = 1; d < kWave; d <<= 1)
-        mx = std::max(mx, __shfl_xor(mx, d));
-    const uint32_t pua = (uint32_t)__shfl((int)me.ua, p1), puo = (uint32_t)__shfl((int)me.uo, p1);
-    const int32_t pth = __shfl(me.th, p1);
-    if (mg)
-        H[wv][p1] = 1;
+    for (uint32_t i = lane; i < nb; i += kWave)
+        info[r0 + i] = inf[i];
+    for (uint32_t i = lane; i < kWinCap * kWave; i += kWave)
+        slotmap[(uint64_t)blockIdx.x * kWinCap * kWave + i] = smap[i];
+    if (lane < (int)kWinCap)
+        wdepth[(uint64_t)blockIdx.x * kWinCap + lane] = lane < (int)nwin ? wdep[lane] : 0;
+    if (lane == 0)
+        wcount[blockIdx.x] = nwin;
+}
+
+// Exclusive scan of the blocks' window counts (one workgroup); total[0] =
+// all windows.
+__global__ __launch_bounds__(1024) void sel_scan_kernel(const uint32_t* __restrict__ wcount,
+                                                        uint64_t nblk, uint32_t* __restrict__ woff,
+                                                        uint32_t* __restrict__ total)
+{
+    __shared__ uint32_t part[1024 / kWave];
+    __shared__ uint32_t carry;
+    const uint32_t t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    if (t == 0)
+        carry = 0;
     __syncthreads();
-    const bool head = H[wv][lane] != 0;
-    if (win >= nwin)
-        return;
-    // the window's depth (at least one step, also for a window of inert
-    // lanes), its entry step e and its number of 16-step passes
-    const uint32_t depth = mx > 0 ? (uint32_t)mx : 1u;
-    const uint32_t e = (0u - depth) & 15u, passes = (depth + 15u) >> 4;
+    for (uint64_t c0 = 0; c0 < nblk; c0 += 1024) {
+        const uint64_t b = c0 + t;
+        const uint32_t v = b < nblk ? wcount[b] : 0;
+        uint32_t x = v;  // inclusive scan within the wave
+        for (int d = 1; d < kWave; d <<= 1) {
+            const uint32_t y = (uint32_t)__shfl_up((int)x, d);
+            if ((int)lane >= d)
+                x += y;
+        }
+        if (lane == 63)
+            part[wv] = x;
+        __syncthreads();
+        uint32_t before = carry;
+        for (uint32_t k = 0; k < wv; k++)
+            before += part[k];
+        if (b < nblk)
+            woff[b] = before + x - v;
+        __syncthreads();
+        if (t == 1023)
+            carry = before + x;
+        __syncthreads();
+    }
+    if (t == 0)
+        total[0] = carry;
+}
+
+// One wave per (block, window) of capacity, then 2 * kPrefetch padding
+// windows: the walk records of every lane (inert past the window's
+// requests) and each request's slot.
+__global__ __launch_bounds__(4 * kWave) void sel_fill_kernel(
+    const SelPack* __restrict__ prep, uint64_t n, const uint32_t* __restrict__ info,
+    const uint16_t* __restrict__ slotmap, const uint8_t* __restrict__ wdepth,
+    const uint32_t* __restrict__ wcount, const uint32_t* __restrict__ woff,
+    const uint32_t* __restrict__ total, uint64_t nblk, WalkRec* __restrict__ rec,
+    uint32_t* __restrict__ slot_of)
+{
+    const int lane = lane_id();
+    const uint64_t gw = ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const uint32_t sp = 4u * (kFastMaxLive + lane);
+    uint64_t win;
+    uint32_t k = 0xFFFF, depth = 1;
+    uint64_t blk = 0;
+    if (gw < nblk * kWinCap) {
+        blk = gw / kWinCap;
+        const uint32_t lw = (uint32_t)(gw % kWinCap);
+        if (lw >= wcount[blk])
+            return;
+        win = (uint64_t)woff[blk] + lw;
+        k = slotmap[gw * kWave + lane];
+        depth = wdepth[gw];
+    } else if (gw < nblk * kWinCap + 2 * kPrefetch) {
+        win = (uint64_t)total[0] + (gw - nblk * kWinCap);
+    } else {
+        return;
+    }
+    const uint32_t e = (0u - depth) & 15u, passes = (depth + 15u) >> 4;
     WalkRec q;
     q.ctl = e | (passes - 1) << 4;
-    if (valid) {
-        q.a4 = 4u * a;
-        q.o4 = 4u * o;
+    const uint64_t r = blk * kLevelBlock + k;
+    if (k != 0xFFFF && r < n) {
+        const SelPack me = prep[r];
+        const uint32_t f = info[r];
+        const bool head = (f >> 6) & 1, second = (f >> 7) & 1;
+        q.a4 = 4u * (me.w & 0xFF);
+        q.o4 = 4u * ((me.w >> 8) & 0xFF);
         q.wa = head ? sp : q.a4;
         q.wo = head ? sp : q.o4;
-        q.rel = (uint32_t)(lv - 1) + e;
+        q.rel = (f & 63) + e;
         q.ua = me.ua;
         q.uo = me.uo;
         q.th = me.th;
-        q.pua = mg ? pua : 0;
-        q.puo = mg ? puo : 0;
-        q.pth = mg ? pth : 0;
+        if (second) {
+            const SelPack hd = prep[blk * kLevelBlock + (f >> 8)];
+            q.pua = hd.ua;
+            q.puo = hd.uo;
+            q.pth = hd.th;
+        } else {
+            q.pua = q.puo = 0;
+            q.pth = 0;
+        }
+        slot_of[r] = (uint32_t)(win * kWave + lane);
     } else {
         q.a4 = q.o4 = q.wa = q.wo = sp;
         q.rel = kInertRel;
         q.ua = q.uo = q.pua = q.puo = 0;
         q.th = q.pth = 0;
     }
-    rec[r] = q;
+    rec[win * kWave + lane] = q;
 }
 
 // Walks the windows in order; see the file comment.  T is the load type:
@@ -587,7 +722,8 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
                  : "s96", "s97", "s98", "s99", "vcc", "scc", "memory")
 
 template <typename T>
-__device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec, uint64_t n,
+__device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
+                                             const uint32_t* __restrict__ nwin,
                                              const uint32_t* __restrict__ live_ids,
                                              uint32_t n_live, int64_t* __restrict__ loads,
                                              int64_t b0, longlong2* __restrict__ lpre,
@@ -599,7 +735,7 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec, ui
     for (uint32_t d = lane; d < kFastMaxLive + kWave; d += kWave)
         L[d] = d < n_live ? (T)(loads[live_ids[d]] - b0) : (T)0;
     __syncthreads();
-    const uint64_t nw = (n + kWave - 1) / kWave;
+    const uint64_t nw = __builtin_amdgcn_readfirstlane(nwin[0]);
     // the records hold offsets within L in 4-byte slots; the LDS address of
     // L itself is a link-time constant (zero when it is the only array)
     const uint32_t lbase = lds_addr(reinterpret_cast<int32_t*>(L));
@@ -704,8 +840,9 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec, ui
 
 // One wave: 32-bit relative loads unless plan[2] asks for 64-bit ones.
 __global__ __launch_bounds__(kWave) void select_fast_kernel(
-    const WalkRec* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ live_ids,
-    uint32_t n_live, int64_t* __restrict__ loads, const uint32_t* __restrict__ plan,
+    const WalkRec* __restrict__ rec, const uint32_t* __restrict__ nwin,
+    const uint32_t* __restrict__ live_ids, uint32_t n_live, int64_t* __restrict__ loads,
+    const uint32_t* __restrict__ plan,
     const int64_t* __restrict__ base, longlong2* __restrict__ lpre, int64_t tbase, int64_t per,
     uint32_t qshift, int64_t slo)
 {
@@ -719,15 +856,18 @@ __global__ __launch_bounds__(kWave) void select_fast_kernel(
     __shared__ int64_t L[kFastMaxLive + kWave];  // loads, then one spare slot per lane
     const int64_t b0 = plan[2] ? base[0] : 0;  // 32-bit walks use absolute loads
     if (plan[2])
-        walk_windows<int64_t>(rec, n, live_ids, n_live, loads, b0, lpre, tbase, per, qshift, slo, L);
+        walk_windows<int64_t>(rec, nwin, live_ids, n_live, loads, b0, lpre, tbase, per, qshift, slo,
+                              L);
     else
-        walk_windows<int32_t>(rec, n, live_ids, n_live, loads, b0, lpre, tbase, per, qshift, slo,
+        walk_windows<int32_t>(rec, nwin, live_ids, n_live, loads, b0, lpre, tbase, per, qshift, slo,
                               reinterpret_cast<int32_t*>(L));
 }
 
 __global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, uint32_t bshift,
                                const uint32_t* __restrict__ cand, const uint32_t* __restrict__ match,
-                               const longlong2* __restrict__ lpre, const int64_t* __restrict__ base,
+                               const longlong2* __restrict__ lpre,
+                               const uint32_t* __restrict__ slot_of, uint64_t nslots,
+                               const int64_t* __restrict__ base,
                                const uint32_t* __restrict__ plan, uint8_t* __restrict__ flags,
                                uint32_t* __restrict__ chosen, int64_t* __restrict__ ttft,
                                int64_t tbase, int64_t per, uint32_t qshift, int64_t slo)
@@ -739,13 +879,16 @@ __global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, 
     for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
          r += (uint64_t)gridDim.x * blockDim.x) {
         SelRec s = load_rec(offsets, n, r, true, bshift, cand, match, tbase, per, qshift, slo);
+        const uint32_t q = slot_of[r];
+        if (q >= nslots)  // only when the packing failed, which the status reports
+            continue;
         int64_t La, Lo;
         if (wide) {
-            const longlong2 lp = lpre[r];
+            const longlong2 lp = lpre[q];
             La = lp.x;
             Lo = lp.y;
         } else {
-            const int2 lp = reinterpret_cast<const int2*>(lpre)[r];
+            const int2 lp = reinterpret_cast<const int2*>(lpre)[q];
             La = lp.x;
             Lo = lp.y;
         }
@@ -770,41 +913,75 @@ void launch_select(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint64_t n
 
 }  // namespace
 
-// Work arrays of one batch in flight: packing records, walk records
-// (2 * kPrefetch inert padding windows), pre-update loads (kPrefetch padding
-// windows), base/plan words and growth bounds.  Two such sets live in the
-// selection slot, one per batch parity.
+// Work arrays of one batch in flight: packing records, the level kernel's
+// outputs, walk records (room for every block's window capacity, then
+// 2 * kPrefetch inert padding windows), pre-update loads (kPrefetch padding
+// windows), each request's slot, base/plan words and growth bounds.  Two
+// such sets live in the selection slot, one per batch parity.
 struct SelBuf {
     SelPack* prep;
     WalkRec* rec;
     longlong2* lpre;
+    uint32_t* info;
+    uint32_t* slot_of;
+    uint16_t* slotmap;
+    uint8_t* wdepth;
+    uint32_t* wcount;
+    uint32_t* woff;
+    uint32_t* total;
     int64_t* base;
     uint32_t* plan;
     unsigned long long* grow;
-    uint64_t nwin;  // windows of walk records
+    uint64_t nblk;   // request blocks
+    uint64_t nslots; // walk slots that can hold a request
 };
+
+static size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 
 static hipError_t sel_buffers(dm_ctx* c, uint64_t n, int par, SelBuf* b)
 {
     hipError_t e = hipSuccess;
-    const uint64_t nw = (n + kWave - 1) / kWave;
-    b->nwin = nw + 2 * kPrefetch;
-    const size_t prep_bytes = (n * sizeof(SelPack) + 255) & ~size_t(255);
-    const size_t rec_bytes = (b->nwin * kWave * sizeof(WalkRec) + 255) & ~size_t(255);
-    const size_t lpre_bytes = ((nw + kPrefetch) * kWave * sizeof(longlong2) + 255) & ~size_t(255);
-    const size_t tail_bytes = 256 + (kMaxSlots + 1) * sizeof(unsigned long long);
-    const size_t one = (prep_bytes + rec_bytes + lpre_bytes + tail_bytes + 255) & ~size_t(255);
+    b->nblk = (n + kLevelBlock - 1) / kLevelBlock;
+    const uint64_t wcap = b->nblk * kWinCap;
+    b->nslots = wcap * kWave;
+    const size_t sizes[] = {
+        up256(n * sizeof(SelPack)),                                  // prep
+        up256((wcap + 2 * kPrefetch) * kWave * sizeof(WalkRec)),     // rec
+        up256((wcap + kPrefetch) * kWave * sizeof(longlong2)),       // lpre
+        up256(n * sizeof(uint32_t)),                                 // info
+        up256(n * sizeof(uint32_t)),                                 // slot_of
+        up256(wcap * kWave * sizeof(uint16_t)),                      // slotmap
+        up256(wcap),                                                 // wdepth
+        up256(b->nblk * sizeof(uint32_t)),                           // wcount
+        up256(b->nblk * sizeof(uint32_t)),                           // woff
+        256 + 256 + (kMaxSlots + 1) * sizeof(unsigned long long),   // total, base/plan, grow
+    };
+    size_t one = 0;
+    for (size_t z : sizes)
+        one += z;
     uint8_t* sw = static_cast<uint8_t*>(scratch_get(c, kSelSlot, 2 * one, &e));
     if (!sw)
         return e;
     sw += par * one;
-    b->prep = reinterpret_cast<SelPack*>(sw);
-    b->rec = reinterpret_cast<WalkRec*>(sw + prep_bytes);
-    b->lpre = reinterpret_cast<longlong2*>(sw + prep_bytes + rec_bytes);
-    uint8_t* tail = sw + prep_bytes + rec_bytes + lpre_bytes;
-    b->base = reinterpret_cast<int64_t*>(tail);
-    b->plan = reinterpret_cast<uint32_t*>(tail + 128);
-    b->grow = reinterpret_cast<unsigned long long*>(tail + 256);
+    uint8_t* at[10];
+    for (int i = 0; i < 10; i++) {
+        at[i] = sw;
+        sw += sizes[i];
+    }
+    b->prep = reinterpret_cast<SelPack*>(at[0]);
+    b->rec = reinterpret_cast<WalkRec*>(at[1]);
+    b->lpre = reinterpret_cast<longlong2*>(at[2]);
+    b->info = reinterpret_cast<uint32_t*>(at[3]);
+    b->slot_of = reinterpret_cast<uint32_t*>(at[4]);
+    b->slotmap = reinterpret_cast<uint16_t*>(at[5]);
+    b->wdepth = at[6];
+    b->wcount = reinterpret_cast<uint32_t*>(at[7]);
+    b->woff = reinterpret_cast<uint32_t*>(at[8]);
+    uint8_t* tail = at[9];
+    b->total = reinterpret_cast<uint32_t*>(tail);
+    b->base = reinterpret_cast<int64_t*>(tail + 256);
+    b->plan = reinterpret_cast<uint32_t*>(tail + 256 + 128);
+    b->grow = reinterpret_cast<unsigned long long*>(tail + 512);
     return hipSuccess;
 }
 
@@ -823,8 +1000,7 @@ hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uin
     hipError_t e = sel_buffers(c, n, par, &b);
     if (e != hipSuccess)
         return e;
-    const uint64_t lgrid = (b.nwin + kLevelWaves - 1) / kLevelWaves;
-    if (lgrid > 0x7FFFFFFFull)
+    if (b.nblk > 0x7FFFFFFFull || b.nblk * kWinCap + 2 * kPrefetch > (0x7FFFFFFFull / 4))
         return hipErrorInvalidValue;
     const uint32_t NL = c->n_live;
     sel_zero_kernel<<<1, 256, 0, st>>>(b.grow, NL);
@@ -834,7 +1010,14 @@ hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uin
     sel_prep_kernel<<<grid_for(n, 256, 512), 256, 0, st>>>(
         offsets, n, block_shift(c), out->cand, out->match, c->d_dense, NL, k.ttft_base_us,
         k.ttft_per_token_us, c->shift_div, k.slo_us, b.prep, b.grow);
-    sel_level_kernel<<<(uint32_t)lgrid, kLevelWaves * kWave, 0, st>>>(b.prep, n, b.rec, b.nwin);
+    if (b.nblk > 0)
+        sel_level_kernel<<<(uint32_t)b.nblk, kWave, 0, st>>>(b.prep, n, b.info, b.slotmap, b.wdepth,
+                                                             b.wcount, c->d_status);
+    sel_scan_kernel<<<1, 1024, 0, st>>>(b.wcount, b.nblk, b.woff, b.total);
+    const uint64_t fill_waves = b.nblk * kWinCap + 2 * kPrefetch;
+    sel_fill_kernel<<<(uint32_t)((fill_waves + 3) / 4), 4 * kWave, 0, st>>>(
+        b.prep, n, b.info, b.slotmap, b.wdepth, b.wcount, b.woff, b.total, b.nblk, b.rec,
+        b.slot_of);
     return hipGetLastError();
 }
 
@@ -850,8 +1033,8 @@ hipError_t select_run(dm_ctx* c, hipStream_t ss, hipStream_t os, hipEvent_t sel_
     const uint32_t S = k.max_slots, NL = c->n_live, bshift = block_shift(c);
     sel_base_kernel<<<1, 256, 0, ss>>>(loads, c->d_live_ids, NL, b.base, b.grow);
     sel_plan_kernel<<<1, 256, 0, ss>>>(loads, c->d_live_ids, NL, b.base, b.grow, b.plan);
-    select_fast_kernel<<<1, kWave, 0, ss>>>(b.rec, n, c->d_live_ids, NL, loads, b.plan, b.base,
-                                            b.lpre, k.ttft_base_us, k.ttft_per_token_us,
+    select_fast_kernel<<<1, kWave, 0, ss>>>(b.rec, b.total, c->d_live_ids, NL, loads, b.plan,
+                                            b.base, b.lpre, k.ttft_base_us, k.ttft_per_token_us,
                                             c->shift_div, k.slo_us);
     if (S <= 64)
         launch_select<1>(c, ss, offsets, n, bshift, out, loads, b.plan);
@@ -874,8 +1057,9 @@ hipError_t select_run(dm_ctx* c, hipStream_t ss, hipStream_t os, hipEvent_t sel_
             return e;
     }
     sel_out_kernel<<<grid_for(n, 256, 8192), 256, 0, os>>>(
-        offsets, n, bshift, out->cand, out->match, b.lpre, b.base, b.plan, out->flags, out->chosen,
-        out->ttft_us, k.ttft_base_us, k.ttft_per_token_us, c->shift_div, k.slo_us);
+        offsets, n, bshift, out->cand, out->match, b.lpre, b.slot_of, b.nslots, b.base, b.plan,
+        out->flags, out->chosen, out->ttft_us, k.ttft_base_us, k.ttft_per_token_us, c->shift_div,
+        k.slo_us);
     return hipGetLastError();
 }
 

@@ -72,42 +72,55 @@ def algorithmic_bytes(off_np, B, match, cand, n):
     return hash_bytes, stage_bytes, ntok, probes
 
 
-def window_depth_steps(cand, match, n, window=64):
-    """Depth steps of the windowed selection walk: per window of 64 requests,
-    the depth of its dependency graph, summed.  A request whose latest
-    earlier request in the window on both of its instances is one request of
-    the same pair with the same cache-affine candidate (the one with more
-    cached blocks, c1 on equal matches) shares that request's depth when the
-    latter is not itself such a second request (runs of two)."""
+def walk_steps(cand, match, n, block=1024, lanes=64, runs=True):
+    """Depth steps and windows of the selection walk.  Requests are taken in
+    blocks of `block` (request order); inside a block a request's level is
+    1 + the larger level of the latest earlier request of the block on
+    either candidate, except that a request whose latest earlier request on
+    both instances is one request of the same pair with the same
+    cache-affine candidate (the one with more cached blocks, c1 on equal
+    matches), itself not such a second request, shares its level (runs of
+    two).  Whole consecutive levels are packed into windows of at most
+    `lanes` requests; a larger level is split with runs kept whole.  Steps =
+    the sum of the windows' level counts."""
     c1, c2 = cand[:n].tolist(), cand[n:].tolist()
     m1, m2 = match[:n].tolist(), match[n:].tolist()
-    total = 0
-    plain = 0
-    for w0 in range(0, n, window):
-        depth, last, merged = {}, {}, {}
-        mx = mx_plain = 0
-        dplain = {}
-        for i in range(w0, min(n, w0 + window)):
-            a, b = (c2[i], c1[i]) if m2[i] > m1[i] else (c1[i], c2[i])
-            pa, pb = last.get(a), last.get(b)
+    steps = windows = 0
+    for b0 in range(0, n, block):
+        last, lv, second, units = {}, {}, {}, {}
+        for i in range(b0, min(n, b0 + block)):
+            a, o = (c2[i], c1[i]) if m2[i] > m1[i] else (c1[i], c2[i])
+            pa, po = last.get(a), last.get(o)
             run = False
-            if pa is not None and pa == pb and a != b and not merged[pa]:
+            if runs and pa is not None and pa == po and a != o and not second[pa]:
                 pab = (c2[pa], c1[pa]) if m2[pa] > m1[pa] else (c1[pa], c2[pa])
-                run = pab == (a, b)
-            merged[i] = run
-            d = depth[pa] if run else 1 + max(depth.get(pa, 0) if pa is not None else 0,
-                                              depth.get(pb, 0) if pb is not None else 0)
-            depth[i] = d
-            last[a] = i
-            last[b] = i
-            mx = d if d > mx else mx
-            dp = max(dplain.get(a, 0), dplain.get(b, 0)) + 1
-            dplain[a] = dp
-            dplain[b] = dp
-            mx_plain = dp if dp > mx_plain else mx_plain
-        total += mx
-        plain += mx_plain
-    return total, plain
+                run = pab == (a, o)
+            second[i] = run
+            if run:
+                lv[i] = lv[pa]
+                units[lv[i]][-1] = 2  # the head's unit grows to two requests
+            else:
+                lv[i] = 1 + max(lv[pa] if pa is not None else 0, lv[po] if po is not None else 0)
+                units.setdefault(lv[i], []).append(1)
+            last[a] = last[o] = i
+        used = dep = 0
+        for L in range(1, max(units) + 1):
+            sizes = units[L]
+            if used and used + sum(sizes) > lanes:
+                steps += dep
+                windows += 1
+                used = dep = 0
+            dep += 1
+            for sz in sizes:
+                if used + sz > lanes:
+                    steps += dep
+                    windows += 1
+                    used, dep = 0, 1
+                used += sz
+        if used:
+            steps += dep
+            windows += 1
+    return steps, windows
 
 
 def cpu_baseline(wl, sample):
@@ -207,7 +220,8 @@ def main():
     stage_gbs = sbytes / ((hash_avg + match_avg) * 1e-3) / 1e9
     traffic = load_traffic("traffic_hash_kernel_large.json")
     flags = out["flags"].cpu().numpy()
-    depth_steps, depth_steps_no_runs = window_depth_steps(cand, match, n)
+    depth_steps, walk_windows = walk_steps(cand, match, n)
+    depth_steps_no_runs, _ = walk_steps(cand, match, n, runs=False)
     res = {
         "metric": "requests routed/sec and prompt tokens hashed/sec at 1 GPU; % of HBM peak",
         "value": n / (ms_step * 1e-3),
@@ -236,13 +250,14 @@ def main():
                              "from the batch's probe end to its selection end"},
         "pipelined": True,
         "select_bound": {"kernel": "select_fast_kernel", "bound": "latency",
-                         "depth_steps": depth_steps,
+                         "depth_steps": depth_steps, "windows": walk_windows,
                          "depth_steps_without_runs": depth_steps_no_runs,
                          "ns_per_step": ref_stage[2] * 1e6 / depth_steps,
-                         "note": "one wave walks 64-request windows in dependency depth order, "
-                                 "runs of two same-pair requests sharing a step; each step is "
-                                 "an LDS round trip plus the run replay and the decision; "
-                                 "time from the unpipelined stage (record packing included)"},
+                         "note": "one wave walks windows of up to 64 requests packed from the "
+                                 "dependency levels of 1024-request blocks, runs of two "
+                                 "same-pair requests sharing a level; each step is an LDS "
+                                 "round trip plus the run replay and the decision; time from "
+                                 "the unpipelined stage (record packing and levels included)"},
         "unpipelined": {"ms_per_step": ms_ref, "requests_per_s": n / (ms_ref * 1e-3),
                         "steps": n_ref,
                         "stage_ms": {"hash": ref_stage[0], "lookup_match": ref_stage[1],

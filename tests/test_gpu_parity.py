@@ -141,6 +141,72 @@ def test_selection_wide_loads_parity(n_inst, top):
     assert (r["flags"] & 1).sum() + (r["flags"] & 4).sum() > 0
 
 
+def _disjoint_pair_prompts(o, rng, n_pool):
+    """Random prompts whose candidate pairs are pairwise disjoint (greedy
+    over a pool), found with the oracle's ring keys and candidates."""
+    used, out = set(), []
+    for _ in range(n_pool):
+        p = rng.integers(0, 1 << 20, size=int(rng.integers(8, 160)), dtype=np.int32)
+        c1, c2, _ = o.candidates(o.ring_key(0, p), o.ring_key(1, p))
+        if c1 == c2 or c1 in used or c2 in used:
+            continue
+        used |= {c1, c2}
+        out.append(p)
+    return out
+
+
+@pytest.mark.parametrize("wide", [False, True])
+def test_levels_above_64_requests_parity(wide):
+    """Levels of more than 64 requests: prompts with pairwise disjoint
+    candidate pairs over 200 instances, each sent twice in a row (runs of
+    two), fill a dependency level with well over 64 requests, in three
+    rounds (three such levels).  The walk splits each level between windows
+    and must keep every run whole.  Random prompts follow, across the next
+    request block.  wide: loads spread beyond 2^30 (64-bit walk)."""
+    gh = _h()
+    wl = workloads.small_random(33, 200, 3, 16, 64, slo_us=5_000)
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    rng = np.random.default_rng(33)
+    uniq = _disjoint_pair_prompts(o, rng, 4000)
+    assert len(uniq) >= 40, len(uniq)
+    seq = []
+    for _ in range(3):
+        for p in uniq:
+            seq += [p, p]
+    assert 2 * len(uniq) > 64
+    # each side caches the prompts' chains where a prior routing of them
+    # (zero loads) sends them, so that matches differ between candidates
+    uoff = np.zeros(len(uniq) + 1, np.int64)
+    uoff[1:] = np.cumsum([len(p) for p in uniq])
+    utok = np.concatenate(uniq).astype(np.int32)
+    zero = np.zeros(wl.route.max_slots, np.int64)
+    pr = o.route(utok, uoff, zero, block_keys=True)
+    oh.insert_blocks(o, pr["block_keys"], np.repeat(pr["chosen"], np.diff(uoff) // wl.route.block))
+    uoff_d = gh.to_dev(uoff, eng.device)
+    pg = eng.route(gh.to_dev(utok, eng.device), uoff_d, gh.to_dev(zero, eng.device),
+                   block_keys=True)
+    gh.insert_blocks(eng, pg["block_keys"],
+                     torch.repeat_interleave(pg["chosen"].to(torch.int64), gh.full_blocks(eng, uoff_d)))
+    eng.sync()
+    for _ in range(1100 - len(seq)):
+        seq.append(rng.integers(0, 1 << 20, size=int(rng.integers(0, 120)), dtype=np.int32))
+    off = np.zeros(len(seq) + 1, np.int64)
+    off[1:] = np.cumsum([len(p) for p in seq])
+    tok = np.concatenate(seq).astype(np.int32)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    if wide:
+        L0[::3] += 1 << 40
+    _say("levels above 64", len(uniq), "pairs", len(seq), "requests", "wide" if wide else "")
+    Ld = gh.to_dev(L0, eng.device)
+    g = eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld)
+    eng.sync()
+    r = o.route(tok, off, L0)
+    compare_route(g, r, len(seq))
+    assert np.array_equal(cpu(Ld), r["loads"])
+    # the affine-candidate rule ran, with SLO switches among its decisions
+    assert ((r["flags"] >> 2) & 1).sum() < len(seq) and (r["flags"] & 1).sum() > 0
+
+
 def test_selection_many_instances_parity():
     """More live instances than the register banks hold (LDS selection)."""
     wl = workloads.small_random(32, 300, 2, 16, 900, slo_us=30_000)

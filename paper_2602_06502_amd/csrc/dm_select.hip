@@ -628,48 +628,51 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
 }
 
 // One depth step of the 32-bit walk, as asm text for DM_WALK_BLOCK: the
-// lanes whose rel equals the inline constant K are on this depth.  Reads
-// (XA, XO) of this depth into one register set, replays the run
-// predecessor's decision (no change when it has none) and leaves the result
-// (X1, Y1) there: the loads this request saw; captures the previous step's
-// (XAP, XOP, lane mask MP) into (La, Lo); M receives this step's lane mask.
-// Then the lane's own decision, and both loads of the pair written back (the
-// second instance first, so that a pair of one instance keeps the first's
-// value) -- to the lane's write slots (wa, wo) when on the depth, else to its
-// spare slot.  The reads of a depth precede its writes in the LDS queue, and
-// the writes of one depth precede the reads of the next, so the waits count
-// this step's reads only.  Every step has the same instructions with
-// fixed-size encodings (operands are registers and inline constants), which
-// the computed entry relies on; the assembler checks the sizes.
-#define DM_STEP_TEXT(K, XA, XO, M, XAP, XOP, MP)                                               \
+// lanes whose rel equals the inline constant K are on this depth.  The loads
+// of a step live in one register pair X = (L_a, L_o): v[240:241] or
+// v[242:243], alternating between steps, so that a decision adds both of its
+// increments with one 64-bit add.  No carry crosses the halves for a lane on
+// its depth: on this path every live load and its growth stay below 2^31.
+// (A lane off its depth may carry; its values only reach its spare slot.)
+// Reads X (L_o first), replays the run predecessor's decision (no change
+// when it has none) into X: the loads this request saw; captures the
+// previous step's pair XP (lane mask MP) into (La, Lo); M receives this
+// step's lane mask.  Then the lane's own decision into v[246:247], and both
+// loads of the pair written back (the second instance first, so that a pair
+// of one instance keeps the first's value) -- to the lane's write slots
+// (wa, wo) when on the depth, else to its spare slot.  The reads of a depth
+// precede its writes in the LDS queue, and the writes of one depth precede
+// the reads of the next, so the waits count this step's reads only.  Every
+// step has the same instructions with fixed-size encodings (operands are
+// registers and inline constants), which the computed entry relies on; the
+// assembler checks the sizes.
+#define DM_STEP_TEXT(K, XA, XO, X, M, XAP, XOP, MP)                                            \
     ".Ldmw%=_" #K ":\n\t"                                                                      \
-    "ds_read_b32 %[" XO "], %[o4]\n\t"                                                         \
-    "ds_read_b32 %[" XA "], %[a4]\n\t"                                                         \
+    "ds_read_b32 " XO ", %[o4]\n\t"                                                            \
+    "ds_read_b32 " XA ", %[a4]\n\t"                                                            \
     "v_cmp_eq_u32_e64 %[" M "], " #K ", %[rel]\n\t"                                           \
-    "v_cndmask_b32_e64 %[La], %[La], %[" XAP "], %[" MP "]\n\t"                                \
-    "v_cndmask_b32_e64 %[Lo], %[Lo], %[" XOP "], %[" MP "]\n\t"                                \
+    "v_cndmask_b32_e64 %[La], %[La], " XAP ", %[" MP "]\n\t"                                   \
+    "v_cndmask_b32_e64 %[Lo], %[Lo], " XOP ", %[" MP "]\n\t"                                   \
     "v_cndmask_b32_e64 %[da], %[sp], %[wa], %[" M "]\n\t"                                      \
     "v_cndmask_b32_e64 %[dz], %[sp], %[wo], %[" M "]\n\t"                                      \
     "s_waitcnt lgkmcnt(1)\n\t"                                                                 \
-    "v_max_i32_e32 %[t1], %[pth], %[" XO "]\n\t"                                               \
+    "v_max_i32_e32 v244, %[pth], " XO "\n\t"                                                   \
     "s_waitcnt lgkmcnt(0)\n\t"                                                                 \
-    "v_cmp_le_i32_e32 vcc, %[" XA "], %[t1]\n\t"                                               \
-    "v_cndmask_b32_e64 %[t1], %[puo], 0, vcc\n\t"                                              \
-    "v_cndmask_b32_e64 %[t2], 0, %[pua], vcc\n\t"                                              \
-    "v_add_u32_e32 %[" XO "], %[" XO "], %[t1]\n\t"                                            \
-    "v_add_u32_e32 %[" XA "], %[" XA "], %[t2]\n\t"                                            \
-    "v_max_i32_e32 %[t1], %[th], %[" XO "]\n\t"                                                \
-    "v_add_u32_e32 %[t2], %[" XO "], %[uo]\n\t"                                                \
-    "v_cmp_le_i32_e32 vcc, %[" XA "], %[t1]\n\t"                                               \
-    "v_add_u32_e32 %[t1], %[" XA "], %[ua]\n\t"                                                \
-    "v_cndmask_b32_e32 %[t2], %[t2], %[" XO "], vcc\n\t"                                       \
-    "v_cndmask_b32_e32 %[t1], %[" XA "], %[t1], vcc\n\t"                                       \
-    "ds_write_b32 %[dz], %[t2]\n\t"                                                            \
-    "ds_write_b32 %[da], %[t1]\n\t"
+    "v_cmp_le_i32_e32 vcc, " XA ", v244\n\t"                                                   \
+    "v_cndmask_b32_e64 v244, 0, %[pua], vcc\n\t"                                               \
+    "v_cndmask_b32_e64 v245, %[puo], 0, vcc\n\t"                                               \
+    "v_lshl_add_u64 " X ", " X ", 0, v[244:245]\n\t"                                           \
+    "v_max_i32_e32 v246, %[th], " XO "\n\t"                                                    \
+    "v_cmp_le_i32_e32 vcc, " XA ", v246\n\t"                                                   \
+    "v_cndmask_b32_e64 v244, 0, %[ua], vcc\n\t"                                                \
+    "v_cndmask_b32_e64 v245, %[uo], 0, vcc\n\t"                                                \
+    "v_lshl_add_u64 v[246:247], " X ", 0, v[244:245]\n\t"                                      \
+    "ds_write_b32 %[dz], v247\n\t"                                                             \
+    "ds_write_b32 %[da], v246\n\t"
 
 #define DM_STEP_PAIR(K0, K1)                                                                   \
-    DM_STEP_TEXT(K0, "xa0", "xo0", "m0", "xa1", "xo1", "m1")                                   \
-    DM_STEP_TEXT(K1, "xa1", "xo1", "m1", "xa0", "xo0", "m0")
+    DM_STEP_TEXT(K0, "v240", "v241", "v[240:241]", "m0", "v242", "v243", "m1")                 \
+    DM_STEP_TEXT(K1, "v242", "v243", "v[242:243]", "m1", "v240", "v241", "m0")
 
 #define DM_SIZE_CHECK(K0, K1)                                                                  \
     ".if (.Ldmw%=_" #K1 " - .Ldmw%=_" #K0 ") != (.Ldmw%=_1 - .Ldmw%=_0)\n\t"                   \
@@ -705,21 +708,20 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
                  "v_add_u32_e32 %[rel], -16, %[rel]\n\t"                                       \
                  "s_sub_u32 s99, s99, 1\n\t"                                                   \
                  "s_cbranch_scc0 .Ldmw%=_0\n\t"                                                \
-                 "v_cndmask_b32_e64 %[La], %[La], %[xa1], %[m1]\n\t"                           \
-                 "v_cndmask_b32_e64 %[Lo], %[Lo], %[xo1], %[m1]\n\t"                           \
+                 "v_cndmask_b32_e64 %[La], %[La], v242, %[m1]\n\t"                               \
+                 "v_cndmask_b32_e64 %[Lo], %[Lo], v243, %[m1]\n\t"                               \
                  DM_SIZE_CHECK(1, 2) DM_SIZE_CHECK(2, 3) DM_SIZE_CHECK(3, 4)                   \
                  DM_SIZE_CHECK(4, 5) DM_SIZE_CHECK(5, 6) DM_SIZE_CHECK(6, 7)                   \
                  DM_SIZE_CHECK(7, 8) DM_SIZE_CHECK(8, 9) DM_SIZE_CHECK(9, 10)                  \
                  DM_SIZE_CHECK(10, 11) DM_SIZE_CHECK(11, 12) DM_SIZE_CHECK(12, 13)             \
                  DM_SIZE_CHECK(13, 14) DM_SIZE_CHECK(14, 15) DM_SIZE_CHECK(15, 16)             \
-                 : [xa0] "=&v"(xa0), [xo0] "=&v"(xo0), [xa1] "=&v"(xa1), [xo1] "=&v"(xo1),    \
-                   [m0] "=&s"(m0), [m1] "=&s"(m1), [La] "+v"(La), [Lo] "+v"(Lo),              \
-                   [t1] "=&v"(t1), [t2] "=&v"(t2), [da] "=&v"(da), [dz] "=&v"(dz),            \
-                   [rel] "+v"(rel)                                                            \
+                 : [m0] "=&s"(m0), [m1] "=&s"(m1), [La] "+v"(La), [Lo] "+v"(Lo),              \
+                   [da] "=&v"(da), [dz] "=&v"(dz), [rel] "+v"(rel)                            \
                  : [a4] "v"(a4), [o4] "v"(o4), [wa] "v"(wa), [wo] "v"(wo), [sp] "v"(sp4),     \
                    [th] "v"(th), [ua] "v"(ua), [uo] "v"(uo), [pth] "v"(pth), [pua] "v"(pua),  \
                    [puo] "v"(puo), [ctl] "v"(ctl)                                              \
-                 : "s96", "s97", "s98", "s99", "vcc", "scc", "memory")
+                 : "s96", "s97", "s98", "s99", "v240", "v241", "v242", "v243", "v244", "v245",  \
+                   "v246", "v247", "vcc", "scc", "memory")
 
 template <typename T>
 __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
@@ -784,12 +786,11 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
             const int32_t th = cur.th, pth = cur.pth;
             const uint32_t ctl = cur.ctl;
             uint32_t rel = cur.rel;
-            int32_t xa0, xo0, xa1, xo1, t1, t2, da, dz;
+            int32_t da, dz;
             uint64_t m0, m1;
             int32_t La = La32, Lo = Lo32;
             DM_WALK_BLOCK();
-            (void)xa0; (void)xo0; (void)xa1; (void)xo1; (void)m0; (void)m1;
-            (void)t1; (void)t2; (void)da; (void)dz;
+            (void)m0; (void)m1; (void)da; (void)dz;
             La32 = La;
             Lo32 = Lo;
             reinterpret_cast<int2*>(lpre)[w * kWave + lane] = make_int2(La, Lo);

@@ -72,40 +72,41 @@ def algorithmic_bytes(off_np, B, match, cand, n):
     return hash_bytes, stage_bytes, ntok, probes
 
 
-def walk_steps(cand, match, n, block=1024, lanes=64, runs=True):
+def walk_steps(cand, match, n, block=1024, lanes=64, run_max=3):
     """Depth steps and windows of the selection walk.  Requests are taken in
     blocks of `block` (request order); inside a block a request's level is
     1 + the larger level of the latest earlier request of the block on
     either candidate, except that a request whose latest earlier request on
     both instances is one request of the same pair with the same
     cache-affine candidate (the one with more cached blocks, c1 on equal
-    matches), itself not such a second request, shares its level (runs of
-    two).  Whole consecutive levels are packed into windows of at most
-    `lanes` requests; a larger level is split with runs kept whole.  Steps =
-    the sum of the windows' level counts."""
+    matches) joins that request's run, at its level, while the run holds
+    fewer than `run_max` requests.  Whole consecutive levels are packed into
+    windows of at most `lanes` requests; a larger level is split with runs
+    kept whole.  Steps = the sum of the windows' level counts."""
     c1, c2 = cand[:n].tolist(), cand[n:].tolist()
     m1, m2 = match[:n].tolist(), match[n:].tolist()
     steps = windows = 0
     for b0 in range(0, n, block):
-        last, lv, second, units = {}, {}, {}, {}
+        last, lv, head, unit, units = {}, {}, {}, {}, {}
         for i in range(b0, min(n, b0 + block)):
             a, o = (c2[i], c1[i]) if m2[i] > m1[i] else (c1[i], c2[i])
             pa, po = last.get(a), last.get(o)
             run = False
-            if runs and pa is not None and pa == po and a != o and not second[pa]:
+            if pa is not None and pa == po and a != o and unit[head[pa]][0] < run_max:
                 pab = (c2[pa], c1[pa]) if m2[pa] > m1[pa] else (c1[pa], c2[pa])
                 run = pab == (a, o)
-            second[i] = run
             if run:
-                lv[i] = lv[pa]
-                units[lv[i]][-1] = 2  # the head's unit grows to two requests
+                head[i], lv[i] = head[pa], lv[pa]
+                unit[head[i]][0] += 1
             else:
                 lv[i] = 1 + max(lv[pa] if pa is not None else 0, lv[po] if po is not None else 0)
-                units.setdefault(lv[i], []).append(1)
+                head[i] = i
+                unit[i] = [1]
+                units.setdefault(lv[i], []).append(unit[i])
             last[a] = last[o] = i
         used = dep = 0
         for L in range(1, max(units) + 1):
-            sizes = units[L]
+            sizes = [u[0] for u in units[L]]
             if used and used + sum(sizes) > lanes:
                 steps += dep
                 windows += 1
@@ -221,7 +222,7 @@ def main():
     traffic = load_traffic("traffic_hash_kernel_large.json")
     flags = out["flags"].cpu().numpy()
     depth_steps, walk_windows = walk_steps(cand, match, n)
-    depth_steps_no_runs, _ = walk_steps(cand, match, n, runs=False)
+    depth_steps_no_runs, _ = walk_steps(cand, match, n, run_max=1)
     res = {
         "metric": "requests routed/sec and prompt tokens hashed/sec at 1 GPU; % of HBM peak",
         "value": n / (ms_step * 1e-3),
@@ -254,7 +255,7 @@ def main():
                          "depth_steps_without_runs": depth_steps_no_runs,
                          "ns_per_step": ref_stage[2] * 1e6 / depth_steps,
                          "note": "one wave walks windows of up to 64 requests packed from the "
-                                 "dependency levels of 1024-request blocks, runs of two "
+                                 "dependency levels of 1024-request blocks, runs of up to three "
                                  "same-pair requests sharing a level; each step is an LDS "
                                  "round trip plus the run replay and the decision; time from "
                                  "the unpipelined stage (record packing and levels included)"},

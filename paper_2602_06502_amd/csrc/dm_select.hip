@@ -13,11 +13,14 @@
 //                     their uncached tokens, and th such that the rule reads
 //                     "take a iff L_a <= max(th, L_o)" on 32-bit loads
 //                     relative to that base;
-//   sel_level_kernel  one wave per 64-request window: the depth of every
-//                     request in the window's dependency graph (an edge
-//                     from each earlier request sharing a candidate);
+//   sel_level_kernel  one wave per block of 1024 requests: the dependency
+//                     level of every request inside its block (runs of up
+//                     to three same-pair requests sharing a level), and the
+//                     packing of whole levels into windows of 64 lanes;
+//   sel_scan_kernel,  the windows' places, the walk records of every
+//   sel_fill_kernel   window lane and each request's slot;
 //   select_fast_kernel one wave walks the windows in order and, inside a
-//                     window, the depths in order: requests of one depth
+//                     window, the levels in order: requests of one level
 //                     share no instance, so they run together on loads kept
 //                     in LDS, and each sees exactly the loads that the
 //                     request-order walk would show it;
@@ -217,13 +220,15 @@ __global__ __launch_bounds__(kWave) void select_lds_kernel(
 // Fast path.
 // ---------------------------------------------------------------------------
 
-// w: a | o << 8 | (depth - 1) << 16 | (window depth - 1) << 22 | (a is c2) << 28
-//    | (head of a two-request run) << 29
-// A request whose latest earlier request in its window on both of its
-// instances is one request with the same cache-affine instance forms a run
-// with it (runs of two): both take the same depth, the second replays the
-// first's decision from (pua, puo, pth) before its own, and only the second
-// writes the pair's loads.  (pua, puo) = (0, 0) replays nothing.
+// A request whose latest earlier request of its block on both of its
+// instances is one request with the same pair and cache-affine instance
+// joins that request's run while the run holds fewer than kRunMax requests:
+// all take the same level, each replays the decisions of the run's earlier
+// members (uncached tokens and thresholds copied into its record) before
+// its own, and only the run's last member writes the pair's loads.
+// Replaying zero increments changes nothing.
+constexpr uint32_t kRunMax = 3;
+
 // Per-request record of the packing kernel.
 struct SelPack {
     uint32_t w;   // a | o << 8 (dense indices) | 1 << 28 when a is c2
@@ -234,8 +239,9 @@ struct SelPack {
 
 // Per-request record of the walk, in the form its depth steps consume: the
 // LDS byte offsets (within the load array, 4-byte slots) of L_a and L_o,
-// where the request writes them (its spare slot when it is the first of a
-// run), rel = its depth (0-based) + the window's entry step e, and the
+// where the request writes them (its spare slot unless it is the last
+// member of its run), rel = its depth (0-based) + the window's entry step e,
+// and the
 // window's control word e | (passes - 1) << 4.  Lanes past the batch and
 // the padding windows are inert: every offset is the lane's spare slot and
 // rel matches no step.
@@ -244,8 +250,11 @@ struct WalkRec {
     uint32_t rel, ctl;
     uint32_t ua, uo;
     int32_t th;
-    uint32_t pua, puo;  // the run's first request: its uncached tokens on a and o
-    int32_t pth;        // and its threshold
+    uint32_t pua, puo;    // the run's first member: its uncached tokens on a and o
+    int32_t pth;          // and its threshold (zeros for a run's first member)
+    uint32_t pua2, puo2;  // the run's second member, for its third (else zeros)
+    int32_t pth2;
+    uint32_t pad;
 };
 constexpr uint32_t kInertRel = 0xFFFFFFFFu;
 
@@ -381,9 +390,8 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
 // Walk windows from dependency levels.  Requests are grouped in blocks of
 // kLevelBlock (request order).  Inside a block, a request's level is 1 + the
 // larger level of the latest earlier request of the block on either
-// candidate (0 when none), except that a run's second request -- whose
-// latest earlier request on both instances is one request of the same pair
-// and cache-affine instance, itself not a second -- takes its head's level.
+// candidate (0 when none), except that a request that joins a run (see
+// kRunMax) takes the run's level.
 // Along every instance's requests the level strictly grows outside runs, so
 // the requests (runs) of one level touch pairwise distinct instances, and
 // any order of the levels' requests that keeps levels in order and the
@@ -391,16 +399,17 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
 // walk.  Windows of at most 64 lanes take whole consecutive levels; a level
 // that does not fit starts a new window, and a level of more than 64
 // requests is split between windows with runs kept whole.  Any two
-// consecutive windows of a block hold at least 64 requests, so a block has
-// at most 2 * ceil(kLevelBlock / 64) + 1 windows.
+// consecutive windows of a block hold more than 64 - kRunMax requests, so a
+// block has at most 2 * ceil(kLevelBlock / 62) + 1 windows.
 constexpr uint32_t kLevelBlock = 1024;
-constexpr uint32_t kWinCap = 36;  // windows per block; the bound above is 33
+constexpr uint32_t kWinCap = 36;  // windows per block; the bound above is 35
 
 // One wave per block: lane 0 runs the block's requests in order (levels and
 // runs), then its levels in order (windows).  Writes, per request, info =
-// depth in its window | head << 6 | second << 7 | head index << 8; per
-// block, its window count, each window's depth and the block-local request
-// index in every window lane (0xFFFF for none).
+// depth in its window | position in its run << 6 | (not the run's last) << 8
+// | run's first member << 9 | run's second member << 19 (block-local
+// indices); per block, its window count, each window's depth and the
+// block-local request index in every window lane (0xFFFF for none).
 __global__ __launch_bounds__(kWave) void sel_level_kernel(
     const SelPack* __restrict__ prep, uint64_t n, uint32_t* __restrict__ info,
     uint16_t* __restrict__ slotmap, uint8_t* __restrict__ wdepth, uint32_t* __restrict__ wcount,
@@ -409,8 +418,9 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
     __shared__ uint16_t W[kLevelBlock];       // a | o << 8
     __shared__ uint16_t lv[kLevelBlock];      // level
     __shared__ uint16_t nxt[kLevelBlock];     // next run head of the same level, + 1
-    __shared__ uint16_t mate[kLevelBlock];    // head: its second; second: its head
-    __shared__ uint8_t fl[kLevelBlock];       // bit0 second of a run, bit1 head of a run
+    __shared__ uint16_t head[kLevelBlock];    // first member of the request's run
+    __shared__ uint16_t mem1[kLevelBlock], mem2[kLevelBlock];  // a head's 2nd and 3rd
+    __shared__ uint8_t rsz[kLevelBlock];      // a head's run size
     __shared__ uint16_t last[kFastMaxLive];   // latest request on each instance, + 1
     __shared__ uint16_t lhead[kLevelBlock + 1], ltail[kLevelBlock + 1], cnt[kLevelBlock + 1];
     __shared__ uint32_t inf[kLevelBlock];
@@ -422,7 +432,7 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
     const uint32_t nb = (uint32_t)std::min<uint64_t>(kLevelBlock, n - r0);
     for (uint32_t i = lane; i < kLevelBlock; i += kWave) {
         W[i] = i < nb ? (uint16_t)(prep[r0 + i].w & 0xFFFFu) : 0;
-        fl[i] = 0;
+        rsz[i] = 0;
         inf[i] = 0;
     }
     for (uint32_t i = lane; i <= kLevelBlock; i += kWave)
@@ -437,15 +447,21 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
         for (uint32_t i = 0; i < nb; i++) {
             const uint32_t w = W[i], a = w & 0xFF, o = w >> 8;
             const int pa = (int)last[a] - 1, po = (int)last[o] - 1;
-            const bool run = pa >= 0 && pa == po && a != o && !(fl[pa] & 1) && W[pa] == w;
+            // pa, the latest request on both instances, is its run's last member
+            const uint32_t h = pa >= 0 ? head[pa] : 0;
+            const bool run = pa >= 0 && pa == po && a != o && W[pa] == w && rsz[h] < kRunMax;
             uint32_t L;
             if (run) {
                 L = lv[pa];
-                fl[i] = 1;
-                fl[pa] |= 2;
-                mate[pa] = (uint16_t)i;
-                mate[i] = (uint16_t)pa;
+                head[i] = (uint16_t)h;
+                if (rsz[h] == 1)
+                    mem1[h] = (uint16_t)i;
+                else
+                    mem2[h] = (uint16_t)i;
+                rsz[h]++;
             } else {
+                head[i] = (uint16_t)i;
+                rsz[i] = 1;
                 L = 1 + std::max(pa >= 0 ? (uint32_t)lv[pa] : 0u, po >= 0 ? (uint32_t)lv[po] : 0u);
                 nxt[i] = 0;
                 if (lhead[L] == 0)
@@ -468,7 +484,7 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
             }
             dep++;
             for (uint32_t u1 = lhead[L]; u1 != 0; u1 = nxt[u1 - 1]) {
-                const uint32_t u = u1 - 1, sz = (fl[u] & 2) ? 2 : 1;
+                const uint32_t u = u1 - 1, sz = rsz[u];
                 if (lanes + sz > kWave) {  // a level of more than 64 requests: split
                     wdep[win++] = (uint8_t)dep;
                     lanes = 0;
@@ -478,13 +494,17 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
                     ok = false;
                     break;
                 }
-                const uint32_t d = dep - 1;
+                const uint32_t d = dep - 1, m1 = sz > 1 ? mem1[u] : 0, m2 = sz > 2 ? mem2[u] : 0;
+                const uint32_t common = d | u << 9 | m1 << 19;
                 smap[win * kWave + lanes] = (uint16_t)u;
-                inf[u] = d | (sz == 2 ? 1u << 6 : 0u);
-                if (sz == 2) {
-                    const uint32_t v = mate[u];
-                    smap[win * kWave + lanes + 1] = (uint16_t)v;
-                    inf[v] = d | 1u << 7 | u << 8;
+                inf[u] = common | (sz > 1 ? 1u << 8 : 0u);
+                if (sz > 1) {
+                    smap[win * kWave + lanes + 1] = (uint16_t)m1;
+                    inf[m1] = common | 1u << 6 | (sz > 2 ? 1u << 8 : 0u);
+                }
+                if (sz > 2) {
+                    smap[win * kWave + lanes + 2] = (uint16_t)m2;
+                    inf[m2] = common | 2u << 6;
                 }
                 lanes += sz;
             }
@@ -585,31 +605,37 @@ __global__ __launch_bounds__(4 * kWave) void sel_fill_kernel(
     const uint64_t r = blk * kLevelBlock + k;
     if (k != 0xFFFF && r < n) {
         const SelPack me = prep[r];
-        const uint32_t f = info[r];
-        const bool head = (f >> 6) & 1, second = (f >> 7) & 1;
+        const uint32_t f = info[r], pos = (f >> 6) & 3;
+        const bool not_last = (f >> 8) & 1;
         q.a4 = 4u * (me.w & 0xFF);
         q.o4 = 4u * ((me.w >> 8) & 0xFF);
-        q.wa = head ? sp : q.a4;
-        q.wo = head ? sp : q.o4;
+        q.wa = not_last ? sp : q.a4;
+        q.wo = not_last ? sp : q.o4;
         q.rel = (f & 63) + e;
         q.ua = me.ua;
         q.uo = me.uo;
         q.th = me.th;
-        if (second) {
-            const SelPack hd = prep[blk * kLevelBlock + (f >> 8)];
-            q.pua = hd.ua;
-            q.puo = hd.uo;
-            q.pth = hd.th;
-        } else {
-            q.pua = q.puo = 0;
-            q.pth = 0;
+        q.pua = q.puo = q.pua2 = q.puo2 = 0;
+        q.pth = q.pth2 = 0;
+        q.pad = 0;
+        if (pos >= 1) {
+            const SelPack m0 = prep[blk * kLevelBlock + ((f >> 9) & 1023)];
+            q.pua = m0.ua;
+            q.puo = m0.uo;
+            q.pth = m0.th;
+        }
+        if (pos >= 2) {
+            const SelPack m1 = prep[blk * kLevelBlock + ((f >> 19) & 1023)];
+            q.pua2 = m1.ua;
+            q.puo2 = m1.uo;
+            q.pth2 = m1.th;
         }
         slot_of[r] = (uint32_t)(win * kWave + lane);
     } else {
         q.a4 = q.o4 = q.wa = q.wo = sp;
         q.rel = kInertRel;
-        q.ua = q.uo = q.pua = q.puo = 0;
-        q.th = q.pth = 0;
+        q.ua = q.uo = q.pua = q.puo = q.pua2 = q.puo2 = q.pad = 0;
+        q.th = q.pth = q.pth2 = 0;
     }
     rec[win * kWave + lane] = q;
 }
@@ -634,8 +660,9 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
 // increments with one 64-bit add.  No carry crosses the halves for a lane on
 // its depth: on this path every live load and its growth stay below 2^31.
 // (A lane off its depth may carry; its values only reach its spare slot.)
-// Reads X (L_o first), replays the run predecessor's decision (no change
-// when it has none) into X: the loads this request saw; captures the
+// Reads X (L_o first), replays the decisions of the run's earlier members
+// (no change for zero increments) into X: the loads this request saw;
+// captures the
 // previous step's pair XP (lane mask MP) into (La, Lo); M receives this
 // step's lane mask.  Then the lane's own decision into v[246:247], and both
 // loads of the pair written back (the second instance first, so that a pair
@@ -661,6 +688,11 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
     "v_cmp_le_i32_e32 vcc, " XA ", v244\n\t"                                                   \
     "v_cndmask_b32_e64 v244, 0, %[pua], vcc\n\t"                                               \
     "v_cndmask_b32_e64 v245, %[puo], 0, vcc\n\t"                                               \
+    "v_lshl_add_u64 " X ", " X ", 0, v[244:245]\n\t"                                           \
+    "v_max_i32_e32 v244, %[pth2], " XO "\n\t"                                                  \
+    "v_cmp_le_i32_e32 vcc, " XA ", v244\n\t"                                                   \
+    "v_cndmask_b32_e64 v244, 0, %[pua2], vcc\n\t"                                              \
+    "v_cndmask_b32_e64 v245, %[puo2], 0, vcc\n\t"                                              \
     "v_lshl_add_u64 " X ", " X ", 0, v[244:245]\n\t"                                           \
     "v_max_i32_e32 v246, %[th], " XO "\n\t"                                                    \
     "v_cmp_le_i32_e32 vcc, " XA ", v246\n\t"                                                   \
@@ -719,7 +751,8 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
                    [da] "=&v"(da), [dz] "=&v"(dz), [rel] "+v"(rel)                            \
                  : [a4] "v"(a4), [o4] "v"(o4), [wa] "v"(wa), [wo] "v"(wo), [sp] "v"(sp4),     \
                    [th] "v"(th), [ua] "v"(ua), [uo] "v"(uo), [pth] "v"(pth), [pua] "v"(pua),  \
-                   [puo] "v"(puo), [ctl] "v"(ctl)                                              \
+                   [puo] "v"(puo), [pth2] "v"(pth2), [pua2] "v"(pua2), [puo2] "v"(puo2),      \
+                   [ctl] "v"(ctl)                                                              \
                  : "s96", "s97", "s98", "s99", "v240", "v241", "v242", "v243", "v244", "v245",  \
                    "v246", "v247", "vcc", "scc", "memory")
 
@@ -745,7 +778,7 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
     int32_t La32 = 0, Lo32 = 0;
     auto window = [&](WalkRec& cur, uint64_t w) {
         const T ua = (T)cur.ua, uo = (T)cur.uo;
-        const T pua = (T)cur.pua, puo = (T)cur.puo;
+        const T pua = (T)cur.pua, puo = (T)cur.puo, pua2 = (T)cur.pua2, puo2 = (T)cur.puo2;
         if constexpr (wide) {
             // the packed bounds are clamped to 32 bits: recompute them
             // exactly, relative to the base (equal matches: -inf)
@@ -755,9 +788,10 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
                            : (T)((slo - tbase - per * (int64_t)u + 1) * ((int64_t)1 << qshift) - 1 - b0);
             };
             const T th = exact(cur.th, cur.ua), pth = exact(cur.pth, cur.pua);
+            const T pth2 = exact(cur.pth2, cur.pua2);
             // Every lane reads and writes at every depth, without branches; a
-            // lane not on the current depth, and the first of a run, write
-            // their own spare slot.
+            // lane not on the current depth, and a run member other than the
+            // last, write their own spare slot.
             const uint32_t ctl = __builtin_amdgcn_readfirstlane(cur.ctl), e = ctl & 15u;
             const uint32_t depth = 16u * (((ctl >> 4) & 3u) + 1u) - e;
             const uint32_t a = cur.a4 >> 2, o = cur.o4 >> 2, wa = cur.wa >> 2, wo = cur.wo >> 2;
@@ -766,8 +800,10 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
             for (uint32_t l = 0; l < depth; l++) {
                 const bool act = mylv == l;
                 const T xa = L[a], xo = L[o];
-                const bool pa = xa <= std::max(pth, xo);
-                const T x1 = xa + (pa ? pua : (T)0), y1 = xo + (pa ? (T)0 : puo);
+                const bool p1 = xa <= std::max(pth, xo);
+                const T x0 = xa + (p1 ? pua : (T)0), y0 = xo + (p1 ? (T)0 : puo);
+                const bool p2 = x0 <= std::max(pth2, y0);
+                const T x1 = x0 + (p2 ? pua2 : (T)0), y1 = y0 + (p2 ? (T)0 : puo2);
                 const bool take_a = x1 <= std::max(th, y1);
                 L[act ? wo : sp] = take_a ? y1 : y1 + uo;
                 L[act ? wa : sp] = take_a ? x1 + ua : x1;
@@ -783,7 +819,7 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
             // depth's steps (a pass of 16 more per further 16 depths).
             const uint32_t a4 = lbase + cur.a4, o4 = lbase + cur.o4;
             const uint32_t wa = lbase + cur.wa, wo = lbase + cur.wo;
-            const int32_t th = cur.th, pth = cur.pth;
+            const int32_t th = cur.th, pth = cur.pth, pth2 = cur.pth2;
             const uint32_t ctl = cur.ctl;
             uint32_t rel = cur.rel;
             int32_t da, dz;

@@ -158,11 +158,12 @@ def _disjoint_pair_prompts(o, rng, n_pool):
 @pytest.mark.parametrize("wide", [False, True])
 def test_levels_above_64_requests_parity(wide):
     """Levels of more than 64 requests: prompts with pairwise disjoint
-    candidate pairs over 200 instances, each sent twice in a row (runs of
-    two), fill a dependency level with well over 64 requests, in three
-    rounds (three such levels).  The walk splits each level between windows
-    and must keep every run whole.  Random prompts follow, across the next
-    request block.  wide: loads spread beyond 2^30 (64-bit walk)."""
+    candidate pairs over 200 instances, each sent twice in a row in three
+    rounds, so that consecutive same-pair requests form runs (of three, then
+    of three again) and a dependency level holds far more than 64 requests.
+    The walk splits each such level between windows and must keep every run
+    whole.  Random prompts follow, across the next request block.  wide:
+    loads spread beyond 2^30 (64-bit walk)."""
     gh = _h()
     wl = workloads.small_random(33, 200, 3, 16, 64, slo_us=5_000)
     eng, o = gh.engine_for(wl), oh.oracle_for(wl)

@@ -404,109 +404,231 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
 constexpr uint32_t kLevelBlock = 1024;
 constexpr uint32_t kWinCap = 36;  // windows per block; the bound above is 35
 
-// One wave per block: lane 0 runs the block's requests in order (levels and
-// runs), then its levels in order (windows).  Writes, per request, info =
-// depth in its window | position in its run << 6 | (not the run's last) << 8
-// | run's first member << 9 | run's second member << 19 (block-local
-// indices); per block, its window count, each window's depth and the
-// block-local request index in every window lane (0xFFFF for none).
+// One wave per block.  Writes, per request, info = depth in its window |
+// position in its run << 6 | (not the run's last) << 8 | run's first member
+// << 9 | run's second member << 19 (block-local indices); per block, its
+// window count, each window's depth and the block-local request index in
+// every window lane (0xFFFF for none).  The result is that of taking the
+// requests one by one; the wave takes them 64 at a time, in order:
+//   - the latest earlier request on each instance: within the chunk from
+//     per-instance lane masks, before it from the latest request of the
+//     earlier chunks on that instance;
+//   - a request whose latest earlier request on both instances is one
+//     request of the same pair and orientation is a run candidate; its
+//     position in the run is (the predecessor's position + 1) mod kRunMax,
+//     0 for any other request (settled along the chunk's candidate chains
+//     with wave-wide votes);
+//   - levels: the least fixed point of the level rule over the chunk
+//     (earlier chunks' levels are final; relaxation from 1, wave-wide votes);
+//   - then, chunk by chunk again with the runs' sizes final, each run takes
+//     its lanes within its level after the runs that start earlier
+//     (ballots per level);
+//   - lane 0 walks the levels in order to place them into windows, run by run
+//     for a level of more than 64 requests.
+// Every LDS access is by this one wave, so no barrier is needed.
 __global__ __launch_bounds__(kWave) void sel_level_kernel(
     const SelPack* __restrict__ prep, uint64_t n, uint32_t* __restrict__ info,
     uint16_t* __restrict__ slotmap, uint8_t* __restrict__ wdepth, uint32_t* __restrict__ wcount,
     uint32_t* __restrict__ status)
 {
-    __shared__ uint16_t W[kLevelBlock];       // a | o << 8
-    __shared__ uint16_t lv[kLevelBlock];      // level
-    __shared__ uint16_t nxt[kLevelBlock];     // next run head of the same level, + 1
-    __shared__ uint16_t head[kLevelBlock];    // first member of the request's run
-    __shared__ uint16_t mem1[kLevelBlock], mem2[kLevelBlock];  // a head's 2nd and 3rd
-    __shared__ uint8_t rsz[kLevelBlock];      // a head's run size
-    __shared__ uint16_t last[kFastMaxLive];   // latest request on each instance, + 1
-    __shared__ uint16_t lhead[kLevelBlock + 1], ltail[kLevelBlock + 1], cnt[kLevelBlock + 1];
-    __shared__ uint32_t inf[kLevelBlock];
+    __shared__ unsigned long long cm[kFastMaxLive];  // lanes of the chunk on each instance
+    __shared__ uint16_t last[kFastMaxLive];         // latest request of earlier chunks, + 1
+    __shared__ uint16_t W[kLevelBlock];              // a | o << 8
+    __shared__ int16_t P[kLevelBlock];               // latest earlier request on a
+    __shared__ uint8_t psn[kLevelBlock];             // position in the run
+    __shared__ uint16_t hd[kLevelBlock];             // the run's first member
+    __shared__ uint16_t lv[kLevelBlock];
+    __shared__ uint8_t has1[kLevelBlock], has2[kLevelBlock];  // a run has a 2nd / 3rd member
+    __shared__ __align__(16) uint16_t key[kLevelBlock];  // a run's first member: level << 2 | size
+    __shared__ uint16_t hrank[kLevelBlock];    // lanes of earlier runs of the same level
+    __shared__ uint32_t cnt[kLevelBlock + 1];  // requests per level (so far)
+    __shared__ uint16_t lstart[kLevelBlock + 1];
+    __shared__ uint8_t lwin[kLevelBlock + 1], lbase[kLevelBlock + 1], ldep[kLevelBlock + 1];
+    __shared__ uint8_t lsplit[kLevelBlock + 1];
+    __shared__ uint16_t sorted[kLevelBlock];   // requests by level, runs in order
+    __shared__ uint8_t rwin[kLevelBlock], rlane[kLevelBlock], rdep[kLevelBlock];
     __shared__ uint16_t smap[kWinCap * kWave];
     __shared__ uint8_t wdep[kWinCap];
-    __shared__ uint32_t nwin;
-    const int lane = lane_id();
+    const uint32_t lane = (uint32_t)lane_id();
     const uint64_t r0 = (uint64_t)blockIdx.x * kLevelBlock;
     const uint32_t nb = (uint32_t)std::min<uint64_t>(kLevelBlock, n - r0);
-    for (uint32_t i = lane; i < kLevelBlock; i += kWave) {
-        W[i] = i < nb ? (uint16_t)(prep[r0 + i].w & 0xFFFFu) : 0;
-        rsz[i] = 0;
-        inf[i] = 0;
-    }
-    for (uint32_t i = lane; i <= kLevelBlock; i += kWave)
-        lhead[i] = ltail[i] = cnt[i] = 0;
-    for (uint32_t i = lane; i < kFastMaxLive; i += kWave)
-        last[i] = 0;
-    for (uint32_t i = lane; i < kWinCap * kWave; i += kWave)
-        smap[i] = 0xFFFF;
-    __syncthreads();
-    if (lane == 0) {
-        uint32_t Lmax = 0;
-        for (uint32_t i = 0; i < nb; i++) {
-            const uint32_t w = W[i], a = w & 0xFF, o = w >> 8;
-            const int pa = (int)last[a] - 1, po = (int)last[o] - 1;
-            // pa, the latest request on both instances, is its run's last member
-            const uint32_t h = pa >= 0 ? head[pa] : 0;
-            const bool run = pa >= 0 && pa == po && a != o && W[pa] == w && rsz[h] < kRunMax;
-            uint32_t L;
-            if (run) {
-                L = lv[pa];
-                head[i] = (uint16_t)h;
-                if (rsz[h] == 1)
-                    mem1[h] = (uint16_t)i;
-                else
-                    mem2[h] = (uint16_t)i;
-                rsz[h]++;
-            } else {
-                head[i] = (uint16_t)i;
-                rsz[i] = 1;
-                L = 1 + std::max(pa >= 0 ? (uint32_t)lv[pa] : 0u, po >= 0 ? (uint32_t)lv[po] : 0u);
-                nxt[i] = 0;
-                if (lhead[L] == 0)
-                    lhead[L] = (uint16_t)(i + 1);
-                else
-                    nxt[ltail[L] - 1] = (uint16_t)(i + 1);
-                ltail[L] = (uint16_t)(i + 1);
-            }
-            lv[i] = (uint16_t)L;
-            cnt[L]++;
-            last[a] = last[o] = (uint16_t)(i + 1);
-            Lmax = L > Lmax ? L : Lmax;
+    const unsigned long long below = (1ull << lane) - 1, above = ~below << 1;
+    for (uint32_t k = lane; k < kFastMaxLive; k += kWave)
+        last[k] = 0;
+    for (uint32_t k = lane; k <= kLevelBlock; k += kWave)
+        cnt[k] = 0;
+    for (uint32_t k = lane; k < kWinCap * kWave; k += kWave)
+        smap[k] = 0xFFFF;
+    {
+        // all pair codes first: sixteen loads in flight per lane, one wait
+        uint32_t wv[kLevelBlock / kWave];
+#pragma unroll
+        for (uint32_t k = 0; k < kLevelBlock / kWave; k++) {
+            const uint32_t t = k * kWave + lane;
+            wv[k] = t < nb ? prep[r0 + t].w : 0u;
         }
+#pragma unroll
+        for (uint32_t k = 0; k < kLevelBlock / kWave; k++)
+            W[k * kWave + lane] = (uint16_t)(wv[k] & 0xFFFFu);
+    }
+    uint32_t lmax = 0;
+    for (uint32_t c0 = 0; c0 < kLevelBlock; c0 += kWave) {
+        const uint32_t t = c0 + lane;
+        const bool valid = t < nb;
+        const uint32_t w = W[t], a = w & 0xFF, o = w >> 8;
+        has1[t] = has2[t] = 0;
+        for (uint32_t k = lane; k < kFastMaxLive; k += kWave)
+            cm[k] = 0;
+        if (valid) {
+            atomicOr(&cm[a], 1ull << lane);
+            if (o != a)
+                atomicOr(&cm[o], 1ull << lane);
+        }
+        const unsigned long long ma = valid ? cm[a] : 0, mo = valid ? cm[o] : 0;
+        auto latest = [&](unsigned long long m, uint32_t x) -> int {
+            m &= below;
+            return m ? (int)(c0 + 63 - __clzll(m)) : (int)last[x] - 1;
+        };
+        const int pa = valid ? latest(ma, a) : -1, po = valid ? latest(mo, o) : -1;
+        P[t] = (int16_t)pa;
+        // the last lane of the chunk on an instance records it for later chunks
+        if (valid && !(ma & above))
+            last[a] = (uint16_t)(t + 1);
+        if (valid && o != a && !(mo & above))
+            last[o] = (uint16_t)(t + 1);
+        const bool cand = valid && pa >= 0 && pa == po && a != o && W[pa] == w;
+        // positions: 0 off the candidate chains; a predecessor in an earlier
+        // chunk is settled; one in this chunk settles in turn
+        const bool inchunk = cand && (uint32_t)pa >= c0;
+        uint32_t pos = cand && !inchunk ? (psn[pa] + 1u) % kRunMax : 0u;
+        bool done = !inchunk;
+        for (;;) {
+            const int src = inchunk ? pa - (int)c0 : (int)lane;
+            const uint32_t ppos = (uint32_t)__shfl((int)pos, src);
+            const bool pdone = __shfl((int)done, src) != 0;
+            const bool now = !done && pdone;
+            if (now) {
+                pos = (ppos + 1u) % kRunMax;
+                done = true;
+            }
+            if (!__any(now))
+                break;
+        }
+        psn[t] = (uint8_t)pos;
+        uint32_t h = t;
+        for (uint32_t k = 0; k < pos; k++)
+            h = (uint32_t)P[h];
+        hd[t] = (uint16_t)h;
+        if (valid && pos == 1)
+            has1[h] = 1;
+        if (valid && pos == 2)
+            has2[h] = 1;
+        // levels of the chunk: the least fixed point, from 1 up
+        uint32_t L = valid ? 1u : 0u;
+        lv[t] = (uint16_t)L;
+        for (;;) {
+            uint32_t nl = 0;
+            if (valid)
+                nl = pos > 0 ? lv[pa]
+                             : 1u + std::max(pa >= 0 ? (uint32_t)lv[pa] : 0u,
+                                             po >= 0 ? (uint32_t)lv[po] : 0u);
+            const bool ch = nl != L;
+            if (ch) {
+                L = nl;
+                lv[t] = (uint16_t)L;
+            }
+            if (!__any(ch))
+                break;
+        }
+        lmax = std::max(lmax, L);
+    }
+    for (int d = 1; d < kWave; d <<= 1)
+        lmax = std::max(lmax, (uint32_t)__shfl_xor((int)lmax, d));
+    // lanes of the runs within their levels, chunk by chunk: each run's first
+    // member sums the sizes of the chunk's earlier runs of its level (every
+    // lane reads the chunk's 64 keys), after the count of the earlier chunks;
+    // the last one of its level in the chunk advances that count
+    for (uint32_t c0 = 0; c0 < kLevelBlock; c0 += kWave) {
+        const uint32_t t = c0 + lane;
+        const uint32_t L = lv[t], rs = 1u + has1[t] + has2[t];
+        const bool head = t < nb && psn[t] == 0;
+        const uint32_t k = head ? (L << 2 | rs) : 0u;
+        key[t] = (uint16_t)k;
+        const uint32_t base = head ? cnt[L] : 0u;
+        uint32_t acc = 0;
+        bool later = false;
+        const uint4* kq = reinterpret_cast<const uint4*>(&key[c0]);
+#pragma unroll
+        for (int q = 0; q < kWave / 8; q++) {
+            const uint4 v = kq[q];
+            const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int e = 0; e < 8; e++) {
+                const uint32_t j = (uint32_t)(q * 8 + e), kj = (d[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+                const bool same = kj != 0 && (kj >> 2) == L;
+                acc += (same && j < lane) ? (kj & 3u) : 0u;
+                later = later || (same && j > lane);
+            }
+        }
+        if (head) {
+            hrank[t] = (uint16_t)(base + acc);
+            if (!later)
+                cnt[L] = base + acc + rs;
+        }
+    }
+    if (lane == 0) {
+        uint32_t start = 0;
+        for (uint32_t l = 1; l <= lmax; l++) {
+            lstart[l] = (uint16_t)start;
+            start += cnt[l];
+        }
+    }
+    for (uint32_t t = lane; t < nb; t += kWave)
+        sorted[lstart[lv[t]] + hrank[hd[t]] + psn[t]] = (uint16_t)t;
+    uint32_t nwin = 0, okw = 0;
+    if (lane == 0) {
         uint32_t win = 0, lanes = 0, dep = 0;
         bool ok = true;
-        for (uint32_t L = 1; L <= Lmax && ok; L++) {
-            if (lanes > 0 && lanes + cnt[L] > kWave) {  // the level does not fit: next window
+        for (uint32_t l = 1; l <= lmax && ok; l++) {
+            const uint32_t c = cnt[l];
+            if (lanes > 0 && lanes + c > kWave) {  // the level does not fit: next window
                 wdep[win++] = (uint8_t)dep;
                 lanes = dep = 0;
             }
             dep++;
-            for (uint32_t u1 = lhead[L]; u1 != 0; u1 = nxt[u1 - 1]) {
-                const uint32_t u = u1 - 1, sz = rsz[u];
-                if (lanes + sz > kWave) {  // a level of more than 64 requests: split
+            if (win >= kWinCap) {
+                ok = false;
+                break;
+            }
+            if (c <= kWave) {
+                lsplit[l] = 0;
+                lwin[l] = (uint8_t)win;
+                lbase[l] = (uint8_t)lanes;
+                ldep[l] = (uint8_t)(dep - 1);
+                lanes += c;
+                continue;
+            }
+            // a level of more than 64 requests: run by run, split between windows
+            lsplit[l] = 1;
+            for (uint32_t k = lstart[l]; k < lstart[l] + c;) {
+                const uint32_t u = sorted[k], sz = key[u] & 3u;
+                if (lanes + sz > kWave) {
                     wdep[win++] = (uint8_t)dep;
                     lanes = 0;
                     dep = 1;
+                    if (win >= kWinCap) {
+                        ok = false;
+                        break;
+                    }
                 }
-                if (win >= kWinCap) {
-                    ok = false;
-                    break;
-                }
-                const uint32_t d = dep - 1, m1 = sz > 1 ? mem1[u] : 0, m2 = sz > 2 ? mem2[u] : 0;
-                const uint32_t common = d | u << 9 | m1 << 19;
-                smap[win * kWave + lanes] = (uint16_t)u;
-                inf[u] = common | (sz > 1 ? 1u << 8 : 0u);
-                if (sz > 1) {
-                    smap[win * kWave + lanes + 1] = (uint16_t)m1;
-                    inf[m1] = common | 1u << 6 | (sz > 2 ? 1u << 8 : 0u);
-                }
-                if (sz > 2) {
-                    smap[win * kWave + lanes + 2] = (uint16_t)m2;
-                    inf[m2] = common | 2u << 6;
+                for (uint32_t m = 0; m < sz; m++) {
+                    const uint32_t v = sorted[k + m];
+                    rwin[v] = (uint8_t)win;
+                    rlane[v] = (uint8_t)(lanes + m);
+                    rdep[v] = (uint8_t)(dep - 1);
                 }
                 lanes += sz;
+                k += sz;
             }
         }
         if (ok && lanes > 0) {
@@ -520,14 +642,32 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
             win = 0;
         }
         nwin = win;
+        okw = ok ? 1u : 0u;
     }
-    __syncthreads();
-    for (uint32_t i = lane; i < nb; i += kWave)
-        info[r0 + i] = inf[i];
-    for (uint32_t i = lane; i < kWinCap * kWave; i += kWave)
-        slotmap[(uint64_t)blockIdx.x * kWinCap * kWave + i] = smap[i];
-    if (lane < (int)kWinCap)
-        wdepth[(uint64_t)blockIdx.x * kWinCap + lane] = lane < (int)nwin ? wdep[lane] : 0;
+    nwin = (uint32_t)__shfl((int)nwin, 0);
+    okw = (uint32_t)__shfl((int)okw, 0);
+    if (okw) {
+        for (uint32_t t = lane; t < nb; t += kWave) {
+            const uint32_t L = lv[t], pos = psn[t], h = hd[t], rs = 1u + has1[h] + has2[h];
+            uint32_t win, ln, d;
+            if (!lsplit[L]) {
+                win = lwin[L];
+                ln = lbase[L] + hrank[h] + pos;
+                d = ldep[L];
+            } else {
+                win = rwin[t];
+                ln = rlane[t];
+                d = rdep[t];
+            }
+            smap[win * kWave + ln] = (uint16_t)t;
+            const uint32_t m1 = pos == 2 ? (uint32_t)P[t] : 0u;
+            info[r0 + t] = d | pos << 6 | (pos + 1 < rs ? 1u << 8 : 0u) | h << 9 | m1 << 19;
+        }
+    }
+    for (uint32_t k = lane; k < kWinCap * kWave; k += kWave)
+        slotmap[(uint64_t)blockIdx.x * kWinCap * kWave + k] = smap[k];
+    if (lane < kWinCap)
+        wdepth[(uint64_t)blockIdx.x * kWinCap + lane] = lane < nwin ? wdep[lane] : 0;
     if (lane == 0)
         wcount[blockIdx.x] = nwin;
 }

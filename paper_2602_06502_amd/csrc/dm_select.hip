@@ -286,7 +286,7 @@ __global__ __launch_bounds__(256) void sel_base_kernel(const int64_t* __restrict
 }
 
 constexpr uint32_t kFastMaxLive = 256;
-constexpr int kPrefetch = 8;  // record windows in flight ahead of the walk
+constexpr int kPrefetch = 12;  // record windows in flight ahead of the walk
 
 // grow[0..n_live) and the bad-record word grow[kMaxSlots] start at zero.
 __global__ void sel_zero_kernel(unsigned long long* __restrict__ grow, uint32_t n_live)
@@ -972,7 +972,7 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
             reinterpret_cast<int2*>(lpre)[w * kWave + lane] = make_int2(La, Lo);
         }
     };
-    static_assert(kPrefetch == 8, "the walk below holds eight record windows");
+    static_assert(kPrefetch == 12, "the walk below holds 12 record windows");
     // Records arrive kPrefetch windows ahead.  The loop is unrolled by
     // kPrefetch so that each slot is used where it was loaded (no register
     // moves, which would wait for every load in flight); windows past the
@@ -981,6 +981,8 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
     WalkRec q2 = rec[2 * kWave + lane], q3 = rec[3 * kWave + lane];
     WalkRec q4 = rec[4 * kWave + lane], q5 = rec[5 * kWave + lane];
     WalkRec q6 = rec[6 * kWave + lane], q7 = rec[7 * kWave + lane];
+    WalkRec q8 = rec[8 * kWave + lane], q9 = rec[9 * kWave + lane];
+    WalkRec q10 = rec[10 * kWave + lane], q11 = rec[11 * kWave + lane];
     // Let the first records land before the loop: the wait the compiler
     // places at the loop head must hold on entry as well as on the
     // back-edge, and with these loads in flight on entry it would wait for
@@ -988,22 +990,30 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
     // expcnt and lgkmcnt unconstrained, in the gfx9 encoding.)
     __builtin_amdgcn_s_waitcnt(0x0F70);
     for (uint64_t w = 0; w < nw; w += kPrefetch) {
-        window(q0, w);
-        q0 = rec[(w + 8) * kWave + lane];
+        window(q0, w + 0);
+        q0 = rec[(w + 12) * kWave + lane];
         window(q1, w + 1);
-        q1 = rec[(w + 9) * kWave + lane];
+        q1 = rec[(w + 13) * kWave + lane];
         window(q2, w + 2);
-        q2 = rec[(w + 10) * kWave + lane];
+        q2 = rec[(w + 14) * kWave + lane];
         window(q3, w + 3);
-        q3 = rec[(w + 11) * kWave + lane];
+        q3 = rec[(w + 15) * kWave + lane];
         window(q4, w + 4);
-        q4 = rec[(w + 12) * kWave + lane];
+        q4 = rec[(w + 16) * kWave + lane];
         window(q5, w + 5);
-        q5 = rec[(w + 13) * kWave + lane];
+        q5 = rec[(w + 17) * kWave + lane];
         window(q6, w + 6);
-        q6 = rec[(w + 14) * kWave + lane];
+        q6 = rec[(w + 18) * kWave + lane];
         window(q7, w + 7);
-        q7 = rec[(w + 15) * kWave + lane];
+        q7 = rec[(w + 19) * kWave + lane];
+        window(q8, w + 8);
+        q8 = rec[(w + 20) * kWave + lane];
+        window(q9, w + 9);
+        q9 = rec[(w + 21) * kWave + lane];
+        window(q10, w + 10);
+        q10 = rec[(w + 22) * kWave + lane];
+        window(q11, w + 11);
+        q11 = rec[(w + 23) * kWave + lane];
     }
     __syncthreads();
     for (uint32_t d = lane; d < n_live && d < kFastMaxLive; d += kWave)

@@ -75,5 +75,7 @@ def test_walk_entries_land_on_step_starts(tmp_path):
         simm = simm - 65536 if simm >= 32768 else simm
         assert br_addr + 4 + 4 * simm == pc + off, "back-edge does not return to step 0"
     # one copy per record slot of the unrolled window loop
-    assert blocks == 8
+    src = open(os.path.join(B.CSRC, "dm_select.hip")).read()
+    prefetch = int(re.search(r"constexpr int kPrefetch = (\d+);", src).group(1))
+    assert blocks == prefetch
 

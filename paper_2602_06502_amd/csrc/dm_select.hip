@@ -231,7 +231,7 @@ constexpr uint32_t kRunMax = 3;
 
 // Per-request record of the packing kernel.
 struct SelPack {
-    uint32_t w;   // a | o << 8 (dense indices) | 1 << 28 when a is c2
+    uint32_t w;   // a | o << 8 (dense indices)
     uint32_t ua;  // uncached tokens on a
     uint32_t uo;  // uncached tokens on o
     int32_t th;   // take a iff L_a <= max(th, L_o), relative loads
@@ -328,7 +328,7 @@ __global__ __launch_bounds__(256) void sel_prep_kernel(
             th = (int32_t)(t < -1 ? -1 : (t > INT32_MAX ? INT32_MAX : t));
         }
         SelPack p;
-        p.w = aff2 ? ((d2 & 0xFF) | (d1 & 0xFF) << 8 | 1u << 28) : ((d1 & 0xFF) | (d2 & 0xFF) << 8);
+        p.w = aff2 ? ((d2 & 0xFF) | (d1 & 0xFF) << 8) : ((d1 & 0xFF) | (d2 & 0xFF) << 8);
         p.ua = (uint32_t)(aff2 ? u2 : u1);
         p.uo = (uint32_t)(aff2 ? u1 : u2);
         p.th = th;

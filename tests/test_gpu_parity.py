@@ -321,6 +321,29 @@ def test_edge_cases_and_errors():
     assert st == pk.DM_EINVAL
 
 
+def test_batch_sizes_around_chunks_and_blocks_parity():
+    """Batch sizes at and around the selection's 64-request chunks and
+    1024-request blocks (partial chunks, partial blocks, one request past a
+    block), each a prefix of the same prompt stream, routed from the same
+    index and loads on both sides."""
+    gh = _h()
+    wl = workloads.small_random(41, 12, 4, 16, 3000, slo_us=20_000)
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    gh.prefill_from_prior(eng, wl)
+    oh.prefill_from_prior(o, wl)
+    tok, off = workloads.prompts(wl, wl.n_req, sub=0)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    tok_d = gh.to_dev(tok, eng.device)
+    for k in (1, 2, 63, 64, 65, 127, 1023, 1024, 1025, 2047, 2049, 3000):
+        _say("batch size", k)
+        Ld = gh.to_dev(L0, eng.device)
+        g = eng.route(tok_d, gh.to_dev(off[:k + 1], eng.device), Ld)
+        eng.sync()
+        r = o.route(tok[:off[k]], off[:k + 1], L0)
+        compare_route(g, r, k)
+        assert np.array_equal(cpu(Ld), r["loads"]), k
+
+
 def test_index_ops_and_capacity():
     gh = _h()
     import paper_2602_06502_amd as pk

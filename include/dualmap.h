@@ -138,8 +138,9 @@ typedef struct {
  *      cached blocks unless its TTFT exceeds the SLO, then the other one if
  *      strictly less loaded.
  * loads: device int64 [max_slots], read and updated in place.  Requires
- * rings (DM_ESTATE otherwise).  n = 0 is a no-op; n must be below 2^32
- * (DM_EINVAL).  Match lengths are 32-bit: a request with 2^32 or more full
+ * rings (DM_ESTATE otherwise).  n = 0 is a no-op; n must be at most
+ * 1,908,874,240 (DM_EINVAL): the selection indexes its per-request slots in
+ * 32 bits.  Match lengths are 32-bit: a request with 2^32 or more full
  * blocks sets the device status word (DM_EINVAL from dm_sync). */
 dm_status dm_route_batch(dm_ctx* ctx, const int32_t* tokens, const int64_t* offsets, uint64_t n,
                          int64_t* loads, const dm_route_out* out);

@@ -383,8 +383,10 @@ dm_status dm_route_batch(dm_ctx* c, const int32_t* tokens, const int64_t* offset
         !aligned(out->cand) || !aligned(out->match) || !aligned(out->chosen) ||
         !aligned(out->ttft_us) || (out->block_keys && !aligned(out->block_keys)))
         return fail(c, DM_EINVAL, "dm_route_batch: misaligned pointer");
-    if (n > 0xFFFFFFFFull)
-        return fail(c, DM_EINVAL, "dm_route_batch: batch too large (n < 2^32)");
+    // the selection's slot indices are 32-bit: 36 windows of 64 lanes per
+    // 1024 requests must stay below 2^32
+    if (n > kMaxRouteBatch)
+        return fail(c, DM_EINVAL, "dm_route_batch: batch too large (n <= 1,908,874,240)");
     DeviceGuard g(c->device);
     hipError_t e = route(c, tokens, offsets, n, loads, out);
     return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_route_batch");

@@ -403,6 +403,8 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
 // block has at most 2 * ceil(kLevelBlock / 62) + 1 windows.
 constexpr uint32_t kLevelBlock = 1024;
 constexpr uint32_t kWinCap = 36;  // windows per block; the bound above is 35
+static_assert(kLevelBlock == kSelBlock && kWinCap == kSelWindowsPerBlock,
+              "dm_route_batch's batch limit assumes this layout");
 
 // One wave per block.  Writes, per request, info = depth in its window |
 // position in its run << 6 | (not the run's last) << 8 | run's first member

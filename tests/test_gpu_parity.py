@@ -319,6 +319,13 @@ def test_edge_cases_and_errors():
     assert st == pk.DM_EINVAL
     st = lib.dm_route_batch(eng._h, None, buf.data_ptr(), 2, L.data_ptr(), C.byref(ro))
     assert st == pk.DM_EINVAL
+    # a batch past the 32-bit selection slots is rejected before any work
+    ok = pk.dm_route_out(buf.data_ptr(), buf.data_ptr(), buf.data_ptr(), buf.data_ptr(),
+                         buf.data_ptr(), buf.data_ptr(), None)
+    st = lib.dm_route_batch(eng._h, buf.data_ptr(), buf.data_ptr(), 1_908_874_241, L.data_ptr(),
+                            C.byref(ok))
+    assert st == pk.DM_EINVAL
+    eng.sync()
 
 
 def test_batch_sizes_around_chunks_and_blocks_parity():

@@ -6,13 +6,15 @@
 // the request's uncached tokens before the next request is decided.  The
 // batch result is therefore defined by processing the requests one by one.
 //
-// Fast path (every live load within 2^30 of the batch's smallest one, at
-// most 256 live instances; checked on the device):
+// Fast path (at most 256 live instances, uncached counts within 32 bits,
+// live loads within 2^62 of the smallest; checked on the device), on 32-bit
+// absolute loads when every load stays below 2^31, else on 64-bit loads
+// relative to the smallest:
 //   sel_prep_kernel   one thread per request packs a 16-byte record: the
 //                     affine candidate a and the other o (dense indices),
 //                     their uncached tokens, and th such that the rule reads
-//                     "take a iff L_a <= max(th, L_o)" on 32-bit loads
-//                     relative to that base;
+//                     "take a iff L_a <= max(th, L_o)" (clamped to 32 bits;
+//                     the 64-bit walk recomputes it exactly);
 //   sel_level_kernel  one wave per block of 1024 requests: the dependency
 //                     level of every request inside its block (runs of up
 //                     to three same-pair requests sharing a level), and the
@@ -237,14 +239,13 @@ struct SelPack {
     int32_t th;   // take a iff L_a <= max(th, L_o), relative loads
 };
 
-// Per-request record of the walk, in the form its depth steps consume: the
-// LDS byte offsets (within the load array, 4-byte slots) of L_a and L_o,
-// where the request writes them (its spare slot unless it is the last
-// member of its run), rel = its depth (0-based) + the window's entry step e,
-// and the
-// window's control word e | (passes - 1) << 4.  Lanes past the batch and
-// the padding windows are inert: every offset is the lane's spare slot and
-// rel matches no step.
+// Per-window-lane record of the walk, in the form its depth steps consume:
+// the LDS byte offsets (within the load array, 4-byte slots) of L_a and
+// L_o, where the request writes them (its spare slot unless it is the last
+// member of its run), rel = its depth in the window (0-based) + the
+// window's entry step e, and the window's control word e | (passes - 1) << 4.
+// Lanes past a window's requests and the padding windows are inert: every
+// offset is the lane's spare slot and rel matches no step.
 struct WalkRec {
     uint32_t a4, o4, wa, wo;
     uint32_t rel, ctl;

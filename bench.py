@@ -10,8 +10,9 @@ to the snapshot before every step (a 2 KB device copy inside the step).
 
 Prints one JSON line: requests routed/s, prompt tokens hashed/s, the HBM
 roofline of the hash+match kernel (algorithmic bytes / its average
-duration measured with HIP events on the engine's stream), and the CPU
-oracle timed on a bounded sample of the same workload.
+duration measured with HIP events on the engine's stream), the elastic
+workload's scale, re-route and rebalance times (after the timed steps), and
+the CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
 import hashlib
@@ -146,6 +147,81 @@ def cpu_baseline(wl, sample):
             "tokens_hashed_per_s": ntok / dt}
 
 
+def elastic_leg(eng, wl, st, keys, L0, reps):
+    """Rows a8/a9 at full size, timed on the host clock around each call (both
+    entry points synchronise with the engine's stream before they return):
+    dm_scale adds 16 instances and removes 8 (both rings rebuilt, owners of
+    2 x n ring keys before and after), one dm_route_batch of the whole batch
+    on the scaled cluster, then dm_rebalance over 8 overloaded sources x
+    32,768 queued records.  Each scale is undone by the reverse scale before
+    the next repetition; the leg ends on the scaled cluster."""
+    import numpy as np
+    import torch
+
+    import paper_2602_06502_amd.harness as gh
+    import workloads
+
+    add, rm = workloads.scale_sets(wl, 16, 8)
+    fwd_ms, back_ms = [], []
+    for i in range(reps + 1):
+        for d, (a, r) in enumerate(((add, rm), (rm, add))):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            res = eng.scale(a.tolist(), r.tolist(), keys)
+            eng.sync()
+            ms = 1000.0 * (time.perf_counter() - t0)
+            if int(res["violations"].cpu()[0]) != 0:
+                raise RuntimeError("dm_scale reported keys remapped between unchanged instances")
+            if i > 0:
+                (fwd_ms if d == 0 else back_ms).append(ms)
+    moved = eng.scale(add.tolist(), rm.tolist(), keys)["moved"].cpu().numpy()
+    eng.sync()
+    n = keys.numel() // 2
+    eng.set_pipelining(False)
+    route_ms = []
+    out = eng.alloc_route_out(n)
+    for i in range(reps + 1):
+        loads = L0.clone()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        eng.route_into(st["tokens"], st["offsets"], loads, out)
+        eng.sync()
+        if i > 0:
+            route_ms.append(1000.0 * (time.perf_counter() - t0))
+    if np.isin(out["cand"].cpu().numpy(), rm).any():
+        raise RuntimeError("a removed instance was routed to")
+    S, n_live = wl.route.max_slots, wl.route.n_inst - len(rm) + len(add)
+    sources = np.sort(np.random.default_rng(3).choice(n_live, size=8, replace=False))
+    q = workloads.synthetic_queues(105, S, n_live, sources, 32_768, 2_000, 50_000,
+                                   4 * (wl.route.slo_us - 50_000))
+    dev = eng.device
+    qd = [gh.to_dev(x, dev) for x in (q.qoff, q.rec_id, q.unc_here, q.alt, q.unc_alt, q.base_work)]
+    reb_ms, count = [], 0
+    for i in range(2 * reps + 2):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        m = eng.rebalance(*qd)
+        eng.sync()
+        if i > 1:
+            reb_ms.append(1000.0 * (time.perf_counter() - t0))
+        count = int(m["count"].cpu()[0])
+    med = lambda x: float(np.median(x))
+    return {
+        "workload": f"elastic: large state, add ids {int(add[0])}..{int(add[-1])}, remove 8 "
+                    f"seeded ids ({n:,} x 2 ring keys); re-route {n:,} requests on "
+                    f"{n_live} instances; rebalance {len(q.rec_id):,} records queued on 8 "
+                    "overloaded instances",
+        "scale_ms": {"median": med(fwd_ms), "min": min(fwd_ms), "reverse_median": med(back_ms),
+                     "moved_frac": [float(x) / n for x in moved]},
+        "reroute_ms": {"median": med(route_ms), "min": min(route_ms),
+                       "requests_per_s": n / (med(route_ms) * 1e-3), "pipelined": False},
+        "rebalance_ms": {"median": med(reb_ms), "min": min(reb_ms), "migrations": count,
+                         "records": len(q.rec_id)},
+        "note": "host wall clock per call, repetitions after one warm-up; the paper reports "
+                "2.2-2.5 ms per rebalancing pass on its own machine (context, not a target)",
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -154,6 +230,9 @@ def main():
     ap.add_argument("--n-req", type=int, default=1_048_576)
     ap.add_argument("--cpu-sample", type=int, default=100_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--elastic-reps", type=int, default=5)
+    ap.add_argument("--no-elastic", action="store_true",
+                    help="skip the scale / re-route / rebalance timings")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after timing, copy 1 GiB device to device once (a plain copy kernel "
                          "of known size, to scale hardware byte counters)")
@@ -275,6 +354,9 @@ def main():
                               np.where(out["chosen"].cpu().numpy() == cand[:n], match[:n],
                                        match[n:]).sum() / max(1, ntok // wl.route.block))},
     }
+    if not args.no_elastic:
+        log("elastic leg: scale, re-route, rebalance")
+        res["elastic"] = elastic_leg(eng, wl, st, out["key"], L0, args.elastic_reps)
     if args.calibrate_copy:
         src = torch.ones(1 << 28, dtype=torch.int32, device=eng.device)
         dst = torch.empty_like(src)

@@ -8,19 +8,25 @@
 //                 eligible if B > 0, source overloaded, target not;
 //   source ranks  overloaded instances by (load desc, id asc);
 //   ordering      eligible records sorted by (source rank, B desc,
-//                 queue position asc) with stable radix passes, and a second
-//                 order grouping each source's records by target.
+//                 queue position asc) with stable radix passes (compaction
+//                 already leaves them in record order, which is queue order
+//                 within a source), and a second order grouping each
+//                 source's records by target, cut into (source, target)
+//                 segments.
 // Then the sources are committed one after another by one workgroup.  For a
 // source, the sequential rule "stop once the queue meets the SLO; move a
 // record iff its TTFT on the target with the target's current load is below
 // the SLO" is evaluated exactly as:
 //   (i)  acceptance ignoring the stop: a record's acceptance depends only on
-//        its target's load, so each target's records are walked in order by
-//        one thread, all targets at once;
+//        its target's load, so each target's segment is walked in order by
+//        one thread, all targets at once, with the segment's records loaded
+//        in batches ahead of the dependent load updates;
 //   (ii) the stop only truncates that acceptance sequence and removing
 //        records never raises a queued TTFT, so the number k of accepted
 //        records that move is the smallest k after which the queue meets the
-//        SLO -- found by bisection over parallel queue evaluations;
+//        SLO -- found by bisection; each probe is one pass over the queue,
+//        held in registers (a contiguous run of records per thread) when it
+//        fits, with one workgroup scan and one vote per probe;
 //   (iii) the first k accepted records move; target loads grow, the source's
 //        shrinks.
 #include <algorithm>
@@ -31,7 +37,13 @@ namespace dm {
 namespace {
 
 constexpr int kQThreads = 256;
-constexpr int kCommitThreads = 1024;
+constexpr int kCommitThreads = 512;
+constexpr int kWalkBatch = 16;   // records loaded ahead of a dependent walk
+constexpr int kQueueRegs = 64;   // queue records per thread held in registers
+constexpr int kCommitBatch = 8;  // committed records whose gathers are in flight together
+// acceptance bits of up to 262,144 candidates per source live in LDS; a
+// source with more uses the same layout in device memory
+constexpr uint32_t kLdsBitWords = 8192;
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;
 
 struct TtftK {
@@ -182,18 +194,14 @@ __global__ void fill_u32_kernel(uint32_t* p, uint64_t n, uint32_t v)
         p[k] = v;
 }
 
-// Eligible records in queue order -> (key = queue position, value = record).
+// Eligible records in record order (queue order within each source).
 __global__ void compact_kernel(uint64_t Q, const uint64_t* __restrict__ elig,
-                               const uint64_t* __restrict__ pos, const uint32_t* __restrict__ owner,
-                               const int64_t* __restrict__ qoff, uint64_t* __restrict__ keys,
-                               uint32_t* __restrict__ vals)
+                               const uint64_t* __restrict__ pos, uint32_t* __restrict__ vals)
 {
     for (uint64_t q = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; q < Q;
          q += (uint64_t)gridDim.x * blockDim.x)
-        if (elig[q]) {
-            keys[pos[q]] = (uint64_t)((int64_t)q - qoff[owner[q]]);
+        if (elig[q])
             vals[pos[q]] = (uint32_t)q;
-        }
 }
 
 // keys[t] = a key of the record (or candidate index) held in vals[t].
@@ -255,6 +263,43 @@ __global__ void gather_groups_kernel(uint64_t C, const uint32_t* __restrict__ gr
     }
 }
 
+// head[u] = 1 where grouped position u starts a (source, target) segment.
+__global__ void seg_head_kernel(uint64_t C, const uint32_t* __restrict__ grp,
+                                const uint32_t* __restrict__ cand_q,
+                                const uint32_t* __restrict__ owner,
+                                const uint32_t* __restrict__ rank,
+                                const uint32_t* __restrict__ g_alt, uint64_t* __restrict__ head)
+{
+    for (uint64_t u = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; u < C;
+         u += (uint64_t)gridDim.x * blockDim.x) {
+        bool h = u == 0 || g_alt[u] != g_alt[u - 1];
+        if (!h)
+            h = rank[owner[cand_q[grp[u]]]] != rank[owner[cand_q[grp[u - 1]]]];
+        head[u] = h ? 1 : 0;
+    }
+}
+
+// seg_pos[g] = first grouped position of segment g (seg_pos[nseg] = C);
+// sseg[r] = first segment of source rank r (sseg[nsrc] = nseg).
+__global__ void seg_pos_kernel(uint64_t C, uint32_t S, const uint64_t* __restrict__ head,
+                               const uint64_t* __restrict__ sid, const uint64_t* __restrict__ nseg_p,
+                               const uint32_t* __restrict__ start,
+                               const uint32_t* __restrict__ nsrc_p, uint32_t* __restrict__ seg_pos,
+                               uint32_t* __restrict__ sseg)
+{
+    const uint32_t nseg = C ? (uint32_t)*nseg_p : 0u, nsrc = *nsrc_p;
+    const uint64_t end = C > S ? C : S;
+    for (uint64_t u = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; u <= end;
+         u += (uint64_t)gridDim.x * blockDim.x) {
+        if (u == C)
+            seg_pos[nseg] = (uint32_t)C;
+        else if (u < C && head[u])
+            seg_pos[sid[u]] = (uint32_t)u;
+        if (u <= nsrc)
+            sseg[u] = start[u] < C ? (uint32_t)sid[start[u]] : nseg;
+    }
+}
+
 __global__ void copy_i64_kernel(const int64_t* __restrict__ a, int64_t* __restrict__ b, uint32_t n)
 {
     for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < n; k += gridDim.x * blockDim.x)
@@ -272,15 +317,18 @@ struct CommitArgs {
     const uint32_t* src;      // [nsrc] instance of each rank
     const uint32_t* nsrc;
     const uint32_t* start;    // [nsrc + 1]
+    const uint32_t* sseg;     // [nsrc + 1] first segment of each rank
+    const uint32_t* seg_pos;  // [nseg + 1] first grouped position of each segment
     const uint32_t* cand_q;   // [C] record of candidate t
     const uint32_t* grp;      // [C] candidate order grouped by (rank, target)
     const uint32_t* g_alt;    // [C] target of grp[u]
     const uint32_t* g_unc;    // [C] unc_alt of grp[u]
-    uint8_t* acc;             // [C]
-    uint32_t* arank;          // [C]
+    uint32_t* gbits;          // [C / 32 + 1] acceptance bits when LDS cannot hold them
+    uint32_t* gwpre;          // [C / 32 + 1] accepted candidates before each bit word
     int64_t* tto;             // [C]
     uint32_t* qkey;           // [Q]
-    int64_t* loads;           // [S] live loads (starts as pass-start loads)
+    int64_t* loads;           // [S] in: pass-start loads; out: loads after the pass
+    uint32_t S;
     TtftK tk;
     uint64_t cap;
     uint64_t* out_rec;
@@ -292,12 +340,15 @@ struct CommitArgs {
     uint32_t* status;
 };
 
-// Largest TTFT over the records of queue [lo, hi) whose key is >= k
-// (the records still queued after the first k accepted ones left).
-__device__ int64_t queue_max_after(const CommitArgs& a, int64_t lo, int64_t hi, int64_t w0,
-                                   uint32_t k, int64_t* sh)
+// Whether a record of queue [lo, hi) whose key is >= k (one still queued
+// after the first k accepted records left) exceeds the SLO behind the base
+// work and the records still ahead of it.  Chunked form, for queues longer
+// than the register form holds.
+__device__ bool queue_violates_chunked(const CommitArgs& a, int64_t lo, int64_t hi, int64_t w0,
+                                       uint32_t k, int64_t* sh)
 {
-    int64_t run = w0, mx = INT64_MIN;
+    int64_t run = w0;
+    bool v = false;
     for (int64_t b = lo; b < hi; b += kCommitThreads) {
         const int64_t q = b + threadIdx.x;
         const bool keep = q < hi && a.qkey[q] >= k;
@@ -305,101 +356,256 @@ __device__ int64_t queue_max_after(const CommitArgs& a, int64_t lo, int64_t hi, 
         int64_t tot;
         const int64_t ex = block_excl_scan_i64<kCommitThreads>(u, sh, tot);
         if (keep)
-            mx = std::max(mx, a.tk(u, run + ex));
+            v |= a.tk(u, run + ex) > a.tk.slo;
         run += tot;
     }
-    return block_max_i64<kCommitThreads>(mx, sh);
+    return __syncthreads_or(v) != 0;
+}
+
+// The same test with the queue in registers: thread x holds a contiguous run
+// of records (key 0 marks an empty register: k >= 1 never keeps it).
+__device__ __forceinline__ bool regs_violate(uint32_t (&u)[kQueueRegs],
+                                             const uint32_t (&key)[kQueueRegs], int64_t w0,
+                                             uint32_t k, const TtftK& tk, int64_t* sh)
+{
+    int64_t sum = 0;
+#pragma unroll
+    for (int r = 0; r < kQueueRegs; r++) {
+        // keep per-record products out of registers across probes
+        asm volatile("" : "+v"(u[r]));
+        sum += key[r] >= k ? (int64_t)u[r] : 0;
+    }
+    int64_t tot;
+    int64_t run = w0 + block_excl_scan_i64<kCommitThreads>(sum, sh, tot);
+    asm volatile("" : "+v"(k));  // recompute the keep masks rather than hold 32 of them
+    bool v = false;
+#pragma unroll
+    for (int r = 0; r < kQueueRegs; r++) {
+        const bool keep = key[r] >= k;
+        v |= keep && tk((int64_t)u[r], run) > tk.slo;
+        run += keep ? (int64_t)u[r] : 0;
+    }
+    return __syncthreads_or(v) != 0;
+}
+
+// Acceptance bits: one per candidate of the current source, in candidate
+// order.  The pointer is generic (LDS or device memory); every access is an
+// atomic performed where the word lives.
+__device__ __forceinline__ uint32_t bits_word(const uint32_t* w)
+{
+    return __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Orders every memory access before it, LDS and device memory, for the whole
+// workgroup.
+__device__ __forceinline__ void wg_sync()
+{
+    __threadfence();
+    __syncthreads();
+}
+
+// Smallest k in [1, A] after which queue [qlo, qlo + Lq) meets the SLO (A if
+// none), the queue held in registers.  Kept out of line: the probes get the
+// whole register file, and the caller's state is saved once per source.
+__device__ __noinline__ uint32_t regs_bisect(const uint32_t* __restrict__ unc_here,
+                                             const uint32_t* __restrict__ qkey, int64_t qlo,
+                                             uint64_t Lq, int64_t w0, uint32_t A, TtftK tk,
+                                             int64_t* sh)
+{
+    const uint32_t tid = threadIdx.x;
+    const uint64_t pq = (Lq + kCommitThreads - 1) / kCommitThreads;
+    const int64_t b0 = qlo + (int64_t)std::min<uint64_t>(Lq, tid * pq);
+    const int64_t b1 = qlo + (int64_t)std::min<uint64_t>(Lq, (tid + 1) * pq);
+    uint32_t u[kQueueRegs], key[kQueueRegs];
+#pragma unroll
+    for (int r = 0; r < kQueueRegs; r++) {
+        const bool in = b0 + r < b1;
+        u[r] = in ? unc_here[b0 + r] : 0u;
+        key[r] = in ? qkey[b0 + r] : 0u;
+    }
+    uint32_t lo = 1, hi = A;
+    if (regs_violate(u, key, w0, hi, tk, sh))
+        return hi;
+    while (lo < hi) {
+        const uint32_t mid = lo + (hi - lo) / 2;
+        if (!regs_violate(u, key, w0, mid, tk, sh))
+            hi = mid;
+        else
+            lo = mid + 1;
+    }
+    return lo;
 }
 
 __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
 {
     __shared__ int64_t sh[kCommitThreads / kWave];
+    __shared__ int64_t s_L[kMaxSlots];         // live loads of every instance
+    __shared__ uint32_t s_bits[kLdsBitWords];
+    __shared__ uint32_t s_wpre[kLdsBitWords];
     __shared__ uint64_t s_count;
-    const uint32_t nsrc = *a.nsrc;
-    if (threadIdx.x == 0)
+    const uint32_t nsrc = *a.nsrc, S = a.S;
+    const uint32_t tid = threadIdx.x;
+    for (uint32_t j = tid; j < S; j += kCommitThreads)
+        s_L[j] = a.loads[j];
+    if (tid == 0)
         s_count = 0;
     __syncthreads();
     for (uint32_t s = 0; s < nsrc; s++) {
         const uint32_t i = a.src[s];
-        const uint32_t cs = a.start[s], ce = a.start[s + 1];
+        const uint32_t cs = a.start[s], ce = a.start[s + 1], nc = ce - cs;
+        const uint32_t nw = (uint32_t)(((uint64_t)nc + 31) / 32);
+        const bool in_lds = nw <= kLdsBitWords;
+        uint32_t* bits = in_lds ? s_bits : a.gbits;
+        uint32_t* wpre = in_lds ? s_wpre : a.gwpre;
         const int64_t qlo = a.qoff[i], qhi = a.qoff[i + 1];
-        // (i) acceptance, one thread per target segment
-        for (uint32_t u = cs + threadIdx.x; u < ce; u += kCommitThreads) {
-            if (u != cs && a.g_alt[u] == a.g_alt[u - 1])
-                continue;
-            const uint32_t j = a.g_alt[u];
-            // loads are updated with atomics at L2: read them past the L1
-            int64_t Lt = __hip_atomic_load(&a.loads[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            for (uint32_t v = u; v < ce && a.g_alt[v] == j; v++) {
-                const int64_t tj = a.tk((int64_t)a.g_unc[v], Lt);
-                const bool ok = tj < a.tk.slo;
-                const uint32_t t = a.grp[v];
-                a.acc[t] = ok;
-                a.tto[t] = tj;
-                if (ok)
-                    Lt += a.g_unc[v];
+        for (uint32_t w = tid; w < nw; w += kCommitThreads)
+            __hip_atomic_store(&bits[w], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int64_t q = qlo + tid; q < qhi; q += kCommitThreads)
+            a.qkey[q] = kNoKey;
+        wg_sync();
+        // (i) acceptance, one thread per (source, target) segment
+        for (uint32_t g = a.sseg[s] + tid; g < a.sseg[s + 1]; g += kCommitThreads) {
+            const uint32_t lo = a.seg_pos[g], hi = a.seg_pos[g + 1];
+            int64_t Lt = s_L[a.g_alt[lo]];
+            for (uint32_t v0 = lo; v0 < hi; v0 += kWalkBatch) {
+                uint32_t ub[kWalkBatch], tb[kWalkBatch];
+#pragma unroll
+                for (int r = 0; r < kWalkBatch; r++) {
+                    const bool in = (uint64_t)v0 + r < hi;
+                    ub[r] = in ? a.g_unc[v0 + r] : 0u;
+                    tb[r] = in ? a.grp[v0 + r] : 0u;
+                }
+#pragma unroll
+                for (int r = 0; r < kWalkBatch; r++) {
+                    if ((uint64_t)v0 + r < hi) {
+                        const int64_t tj = a.tk((int64_t)ub[r], Lt);
+                        a.tto[tb[r]] = tj;
+                        if (tj < a.tk.slo) {
+                            const uint32_t x = tb[r] - cs;
+                            atomicOr(&bits[x >> 5], 1u << (x & 31));
+                            Lt += ub[r];
+                        }
+                    }
+                }
             }
         }
-        __syncthreads();
-        // (ii) acceptance ranks in candidate order; mark queue records
-        for (int64_t q = qlo + threadIdx.x; q < qhi; q += kCommitThreads)
-            a.qkey[q] = kNoKey;
-        int64_t A = 0;
-        for (uint32_t b = cs; b < ce; b += kCommitThreads) {
-            const uint32_t t = b + threadIdx.x;
-            const int64_t v = (t < ce && a.acc[t]) ? 1 : 0;
-            int64_t tot;
-            const int64_t ex = block_excl_scan_i64<kCommitThreads>(v, sh, tot);
-            if (t < ce)
-                a.arank[t] = (uint32_t)(A + ex);
-            A += tot;
+        wg_sync();
+        // (ii) acceptance ranks in candidate order: accepted candidates
+        // before each bit word (a contiguous run of words per thread)
+        const uint64_t pw = ((uint64_t)nw + kCommitThreads - 1) / kCommitThreads;
+        const uint32_t w0 = (uint32_t)std::min<uint64_t>(nw, tid * pw);
+        const uint32_t w1 = (uint32_t)std::min<uint64_t>(nw, (tid + 1) * pw);
+        int64_t cnt = 0;
+        for (uint32_t w = w0; w < w1; w++)
+            cnt += __popc(bits_word(&bits[w]));
+        int64_t A;
+        uint32_t run = (uint32_t)block_excl_scan_i64<kCommitThreads>(cnt, sh, A);
+        for (uint32_t w = w0; w < w1; w++) {
+            __hip_atomic_store(&wpre[w], run, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            run += __popc(bits_word(&bits[w]));
         }
-        __syncthreads();
-        for (uint32_t t = cs + threadIdx.x; t < ce; t += kCommitThreads)
-            if (a.acc[t])
-                a.qkey[a.cand_q[t]] = a.arank[t];
-        __syncthreads();
+        wg_sync();
+        // queue records of accepted candidates get their rank as key
+        for (uint32_t b = cs + tid; b < ce; b += kCommitThreads * kWalkBatch) {
+            uint32_t qb[kWalkBatch];
+#pragma unroll
+            for (int r = 0; r < kWalkBatch; r++) {
+                const uint64_t t = b + (uint64_t)r * kCommitThreads;
+                qb[r] = t < ce ? a.cand_q[t] : 0u;
+            }
+#pragma unroll
+            for (int r = 0; r < kWalkBatch; r++) {
+                const uint64_t t = b + (uint64_t)r * kCommitThreads;
+                if (t < ce) {
+                    const uint32_t x = (uint32_t)(t - cs), w = x >> 5, m = 1u << (x & 31);
+                    const uint32_t word = bits_word(&bits[w]);
+                    if (word & m)
+                        a.qkey[qb[r]] = bits_word(&wpre[w]) + __popc(word & (m - 1));
+                }
+            }
+        }
+        wg_sync();
+        // smallest k in [1, A] after which the queue meets the SLO (A if none)
         uint32_t kstar = 0;
         if (A > 0) {
-            const int64_t w0 = a.base_work[i];
-            if (queue_max_after(a, qlo, qhi, w0, (uint32_t)A, sh) > a.tk.slo) {
-                kstar = (uint32_t)A;
+            const int64_t w0q = a.base_work[i];
+            const uint64_t Lq = (uint64_t)(qhi - qlo);
+            uint32_t lo = 1, hi = (uint32_t)A;  // answer in [lo, hi]
+            if (Lq <= (uint64_t)kCommitThreads * kQueueRegs) {
+                lo = regs_bisect(a.unc_here, a.qkey, qlo, Lq, w0q, hi, a.tk, sh);
             } else {
-                uint32_t lo = 1, hi = (uint32_t)A;  // answer in [lo, hi]
-                while (lo < hi) {
-                    const uint32_t mid = lo + (hi - lo) / 2;
-                    if (queue_max_after(a, qlo, qhi, w0, mid, sh) <= a.tk.slo)
-                        hi = mid;
-                    else
-                        lo = mid + 1;
+                if (queue_violates_chunked(a, qlo, qhi, w0q, hi, sh)) {
+                    lo = hi;
+                } else {
+                    while (lo < hi) {
+                        const uint32_t mid = lo + (hi - lo) / 2;
+                        if (!queue_violates_chunked(a, qlo, qhi, w0q, mid, sh))
+                            hi = mid;
+                        else
+                            lo = mid + 1;
+                    }
                 }
-                kstar = lo;
             }
+            kstar = lo;
         }
-        // (iii) commit the first kstar accepted records
+        // (iii) commit the first kstar accepted records; loads move in LDS
         const uint64_t base = s_count;
-        for (uint32_t t = cs + threadIdx.x; t < ce; t += kCommitThreads) {
-            if (!a.acc[t] || a.arank[t] >= kstar)
-                continue;
-            const uint32_t q = a.cand_q[t];
-            const uint64_t idx = base + a.arank[t];
-            if (idx < a.cap) {
-                a.out_rec[idx] = a.rec_id[q];
-                a.out_from[idx] = i;
-                a.out_to[idx] = a.alt[q];
-                a.out_benefit[idx] = a.benefit[q];
-                a.out_ttft[idx] = a.tto[t];
+        int64_t dsrc = 0;
+        for (uint32_t b = cs + tid; b < ce; b += kCommitThreads * kCommitBatch) {
+            uint32_t rk[kCommitBatch], qb[kCommitBatch];
+#pragma unroll
+            for (int r = 0; r < kCommitBatch; r++) {
+                const uint64_t t = b + (uint64_t)r * kCommitThreads;
+                rk[r] = kNoKey;
+                if (t < ce) {
+                    const uint32_t x = (uint32_t)(t - cs), w = x >> 5, m = 1u << (x & 31);
+                    const uint32_t word = bits_word(&bits[w]);
+                    if (word & m)
+                        rk[r] = bits_word(&wpre[w]) + __popc(word & (m - 1));
+                }
+                qb[r] = rk[r] < kstar ? a.cand_q[t] : 0u;
             }
-            atomicAdd((unsigned long long*)&a.loads[a.alt[q]], (unsigned long long)a.unc_alt[q]);
-            atomicAdd((unsigned long long*)&a.loads[i],
-                      (unsigned long long)(-(int64_t)a.unc_here[q]));
+            uint64_t rec[kCommitBatch];
+            uint32_t to[kCommitBatch], ua[kCommitBatch], uh[kCommitBatch];
+            int64_t ben[kCommitBatch], tt[kCommitBatch];
+#pragma unroll
+            for (int r = 0; r < kCommitBatch; r++) {
+                if (rk[r] < kstar) {
+                    const uint32_t q = qb[r];
+                    rec[r] = a.rec_id[q];
+                    to[r] = a.alt[q];
+                    ua[r] = a.unc_alt[q];
+                    uh[r] = a.unc_here[q];
+                    ben[r] = a.benefit[q];
+                    tt[r] = a.tto[b + (uint64_t)r * kCommitThreads];
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < kCommitBatch; r++) {
+                if (rk[r] < kstar) {
+                    const uint64_t idx = base + rk[r];
+                    if (idx < a.cap) {
+                        a.out_rec[idx] = rec[r];
+                        a.out_from[idx] = i;
+                        a.out_to[idx] = to[r];
+                        a.out_benefit[idx] = ben[r];
+                        a.out_ttft[idx] = tt[r];
+                    }
+                    atomicAdd((unsigned long long*)&s_L[to[r]], (unsigned long long)ua[r]);
+                    dsrc += uh[r];
+                }
+            }
         }
+        if (dsrc)
+            atomicAdd((unsigned long long*)&s_L[i], (unsigned long long)(-dsrc));
         __syncthreads();
-        if (threadIdx.x == 0)
+        if (tid == 0)
             s_count = base + kstar;
         __syncthreads();
     }
-    if (threadIdx.x == 0) {
+    for (uint32_t j = tid; j < S; j += kCommitThreads)
+        a.loads[j] = s_L[j];
+    if (tid == 0) {
         *a.out_count = s_count;
         if (s_count > a.cap)
             atomicOr(a.status, kErrFull);
@@ -433,6 +639,7 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     uint32_t* rank = carve<uint32_t>(pi, S);
     uint32_t* src = carve<uint32_t>(pi, S);
     uint32_t* start = carve<uint32_t>(pi, S + 1);
+    uint32_t* sseg = carve<uint32_t>(pi, S + 1);
     uint32_t* nsrc = carve<uint32_t>(pi, 1);
     uint64_t* ctot = carve<uint64_t>(pi, 1);
     // per-record arrays
@@ -478,17 +685,16 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     uint32_t* grp = carve<uint32_t>(pc, Ca);
     uint32_t* g_alt = carve<uint32_t>(pc, Ca);
     uint32_t* g_unc = carve<uint32_t>(pc, Ca);
-    uint8_t* acc = carve<uint8_t>(pc, Ca);
-    uint32_t* arank = carve<uint32_t>(pc, Ca);
+    uint32_t* gbits = carve<uint32_t>(pc, Ca / 32 + 1);
+    uint32_t* gwpre = carve<uint32_t>(pc, Ca / 32 + 1);
     int64_t* tto = carve<int64_t>(pc, Ca);
+    uint32_t* seg_pos = carve<uint32_t>(pc, Ca + 1);
     uint32_t* cand_q = vals;  // the candidate order lands in vals
 
     if (C) {
         const uint32_t gc = grid_for(C, 256);
-        compact_kernel<<<grid_for(Q, 256), 256, 0, st>>>(Q, elig, pos, owner, q->qoff, keys, vals);
-        // order: queue position asc, then benefit desc, then source rank asc (stable passes)
-        e = radix_sort_kv(c, keys, vals, ktmp, vtmp, C, 32);
-        if (e != hipSuccess) return e;
+        compact_kernel<<<grid_for(Q, 256), 256, 0, st>>>(Q, elig, pos, vals);
+        // order: benefit desc, then source rank asc (stable passes over record order)
         rekey_kernel<<<gc, 256, 0, st>>>(C, kByBenefitDesc, vals, nullptr, benefit, owner, rank,
                                          q->alt, keys);
         e = radix_sort_kv(c, keys, vals, ktmp, vtmp, C, 64);
@@ -511,6 +717,17 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
         gather_groups_kernel<<<gc, 256, 0, st>>>(C, grp, cand_q, q->alt, q->unc_alt, g_alt, g_unc);
     }
     bounds_kernel<<<grid_for(C + 1, 256), 256, 0, st>>>(C, cand_q, owner, rank, nsrc, start);
+    // (source, target) segments of the grouped order; keys and ktmp are free
+    uint64_t* head = ktmp;
+    uint64_t* sid = keys;
+    if (C) {
+        seg_head_kernel<<<grid_for(C, 256), 256, 0, st>>>(C, grp, cand_q, owner, rank, g_alt, head);
+        e = exclusive_scan_u64(c, head, C, sid, ctot);
+        if (e != hipSuccess)
+            return e;
+    }
+    seg_pos_kernel<<<grid_for(std::max<uint64_t>(C, S) + 1, 256), 256, 0, st>>>(
+        C, S, head, sid, ctot, start, nsrc, seg_pos, sseg);
     copy_i64_kernel<<<grid_for(S, 256), 256, 0, st>>>(L0, loads_out, S);
     CommitArgs a;
     a.qoff = q->qoff;
@@ -523,15 +740,18 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     a.src = src;
     a.nsrc = nsrc;
     a.start = start;
+    a.sseg = sseg;
+    a.seg_pos = seg_pos;
     a.cand_q = cand_q;
     a.grp = grp;
     a.g_alt = g_alt;
     a.g_unc = g_unc;
-    a.acc = acc;
-    a.arank = arank;
+    a.gbits = gbits;
+    a.gwpre = gwpre;
     a.tto = tto;
     a.qkey = qkey;
     a.loads = loads_out;
+    a.S = S;
     a.tk = tk;
     a.cap = cap;
     a.out_rec = out->rec_id;

@@ -17,6 +17,11 @@
   oracle on 2 x 1,048,576 seeded random ring keys (rings, owners, moved
   counts, zero violations), and the zero-violation and moved-fraction
   properties on the batch's own ring keys.
+- Re-route on the scaled cluster (136 live instances): the whole batch again
+  on the GPU, the selection replay property, the oracle (scaled the same
+  way, its indexes of added and removed instances cleared) on a sample, and
+  the consistent-hashing properties: no candidate is a removed instance, and
+  every candidate that kept its instance kept its match length.
 - Rebalance at full size: 8 sources x 32,768 queued records against the
   oracle, element by element.
 """
@@ -199,6 +204,49 @@ def test_elastic_scale_full(large):
         _, first = np.unique(k, return_index=True)
         mv = old[s * n:(s + 1) * n][first] != new[s * n:(s + 1) * n][first]
         assert len(first) > 2000 and abs(mv.mean() - expect) < 0.05, (len(first), mv.mean())
+
+
+def test_elastic_reroute_full(large, large_oracle):
+    """Runs after test_elastic_scale_full, which leaves the engine scaled
+    forward (ids 128..143 added, the seeded 8 removed); scales the shared
+    oracle the same way, so no later test may use large_oracle."""
+    wl, g, gh, eng, out = large["wl"], large["g"], large["gh"], large["eng"], large["out"]
+    n = wl.n_req
+    add, rm = workloads.scale_sets(wl, 16, 8)
+    if not np.isin(add, eng.ring(0)[1]).all():  # run alone: scale forward here
+        _say("scale forward: add", len(add), "remove", rm.tolist())
+        eng.scale(add.tolist(), rm.tolist(), gh.to_dev(out["key"][:2], eng.device))
+        eng.sync()
+    live = np.unique(eng.ring(0)[1])
+    assert np.array_equal(live, np.union1d(np.setdiff1d(np.arange(128), rm), add))
+    _say("re-route", n, "requests on", len(live), "instances")
+    loads = gh.to_dev(g["loads0"], eng.device)
+    r2 = eng.route(g["tokens"], g["offsets"], loads)
+    eng.sync()
+    res = {k: v.cpu().numpy() for k, v in r2.items()}
+    res["loads"] = loads.cpu().numpy()
+    replay_check(wl, g["offsets_np"], g["loads0"], res)
+    assert np.array_equal(res["key"], out["key"])  # ring keys do not depend on membership
+    assert not np.isin(res["cand"], rm).any()
+    assert np.isin(res["cand"], add).any()
+    kept = res["cand"] == out["cand"]
+    assert 0.5 < kept.mean() < 1.0, kept.mean()  # about 0.83 of distinct keys stay
+    assert np.array_equal(res["match"][kept], out["match"][kept])
+    # the oracle, scaled the same way, on a sample of the batch
+    o = large_oracle
+    rs = o.scale(add, rm, out["key"][:2])
+    assert rs["status"] == 0
+    rng = np.random.default_rng(11)
+    sample = np.sort(rng.choice(n, size=2048, replace=False))
+    tok, off = g["tokens_np"], g["offsets_np"]
+    parts = [tok[off[r]:off[r + 1]] for r in sample]
+    soff = np.zeros(len(sample) + 1, np.int64)
+    soff[1:] = np.cumsum([len(p) for p in parts])
+    ro = o.route(np.concatenate(parts), soff, np.zeros(wl.route.max_slots, np.int64))
+    for name in ("key", "cand", "match"):
+        got = np.concatenate([res[name][:n][sample], res[name][n:][sample]])
+        assert np.array_equal(got, ro[name]), name
+    assert np.array_equal(res["flags"][sample] & 8, ro["flags"] & 8)
 
 
 def test_rebalance_full_size():

@@ -503,6 +503,37 @@ def test_rebalance_cap_and_empty():
     assert r["count"] == 0
 
 
+def test_rebalance_long_queues_many_targets_parity():
+    """One source whose queue is longer than a commit workgroup holds in
+    registers (40,000 records), one that fits unevenly (20,000), and 1,500
+    live instances, so each source has more (source, target) segments than
+    the workgroup has threads.  Sources start 100 ms under the SLO with small
+    uncached counts, so the queues meet the SLO after part of the accepted
+    records leave and the stop rule truncates."""
+    gh = _h()
+    S, n_live = 2048, 1500
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=S, index_log2_slots=8,
+               slo_us=400_000)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    o = oracle.Oracle(cfg)
+    src = np.array([17, 901])
+    q = workloads.synthetic_queues(29, S, n_live, src, 40_000, 60, 50_000, 4 * 300_000)
+    # second source: keep its first 20,000 records only
+    lens = np.diff(q.qoff)
+    keep = np.ones(len(q.rec_id), bool)
+    keep[q.qoff[901] + 20_000:q.qoff[902]] = False
+    lens[901] = 20_000
+    qoff = np.zeros(S + 1, np.int64)
+    qoff[1:] = np.cumsum(lens)
+    q = workloads.Queues(qoff, q.rec_id[keep], q.unc_here[keep], q.alt[keep], q.unc_alt[keep],
+                         q.base_work)
+    _say("rebalance long queues: records", len(q.rec_id))
+    r = compare_rebalance(eng, o, q)
+    per_src = np.bincount(r["src"], minlength=S)
+    assert 0 < per_src[17] < 40_000 and 0 < per_src[901] < 20_000, per_src[[17, 901]]
+    assert len(np.unique(r["dst"])) > 512
+
+
 def _queues_from_route(chosen, cand, match, off, B, S, base_work):
     """Queues built from a routed batch: each request queued on its chosen
     instance in arrival order; alternative = the other candidate."""

@@ -18,9 +18,16 @@
 // record iff its TTFT on the target with the target's current load is below
 // the SLO" is evaluated exactly as:
 //   (i)  acceptance ignoring the stop: a record's acceptance depends only on
-//        its target's load, so each target's segment is walked in order by
-//        one thread, all targets at once, with the segment's records loaded
-//        in batches ahead of the dependent load updates;
+//        its target's load, so the targets' segments are walked
+//        independently, each wave taking a run of whole segments 64 records
+//        at a time.  The first undecided record of a segment has an exact
+//        target load; if it is accepted, the following records are accepted
+//        up to the first that fails with all of them accepted, if rejected,
+//        they are rejected up to the first that passes at the same load, and
+//        that record takes the other decision.  Each round settles such a run
+//        in every segment at once (prefix sums give the loads), so a chunk
+//        needs as many rounds as its segments have decision changes -- the
+//        sequential walk's result exactly;
 //   (ii) the stop only truncates that acceptance sequence and removing
 //        records never raises a queued TTFT, so the number k of accepted
 //        records that move is the smallest k after which the queue meets the
@@ -38,7 +45,9 @@ namespace {
 
 constexpr int kQThreads = 256;
 constexpr int kCommitThreads = 512;
-constexpr int kWalkBatch = 16;   // records loaded ahead of a dependent walk
+constexpr int kCommitWaves = kCommitThreads / kWave;
+constexpr int kWalkBatch = 16;   // records loaded ahead of a dependent pass
+constexpr int kWalkChunks = 4;   // 64-record chunks of an acceptance walk loaded together
 constexpr int kQueueRegs = 64;   // queue records per thread held in registers
 constexpr int kCommitBatch = 8;  // committed records whose gathers are in flight together
 // acceptance bits of up to 262,144 candidates per source live in LDS; a
@@ -263,6 +272,27 @@ __global__ void gather_groups_kernel(uint64_t C, const uint32_t* __restrict__ gr
     }
 }
 
+// Per candidate t (candidate order): the record's fields a commit writes.
+__global__ void gather_cand_kernel(uint64_t C, const uint32_t* __restrict__ cand_q,
+                                   const uint64_t* __restrict__ rec_id,
+                                   const uint32_t* __restrict__ alt,
+                                   const uint32_t* __restrict__ unc_alt,
+                                   const uint32_t* __restrict__ unc_here,
+                                   const int64_t* __restrict__ benefit, uint64_t* __restrict__ c_rec,
+                                   uint32_t* __restrict__ c_alt, uint32_t* __restrict__ c_ua,
+                                   uint32_t* __restrict__ c_uh, int64_t* __restrict__ c_ben)
+{
+    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < C;
+         t += (uint64_t)gridDim.x * blockDim.x) {
+        const uint32_t q = cand_q[t];
+        c_rec[t] = rec_id[q];
+        c_alt[t] = alt[q];
+        c_ua[t] = unc_alt[q];
+        c_uh[t] = unc_here[q];
+        c_ben[t] = benefit[q];
+    }
+}
+
 // head[u] = 1 where grouped position u starts a (source, target) segment.
 __global__ void seg_head_kernel(uint64_t C, const uint32_t* __restrict__ grp,
                                 const uint32_t* __restrict__ cand_q,
@@ -320,6 +350,11 @@ struct CommitArgs {
     const uint32_t* sseg;     // [nsrc + 1] first segment of each rank
     const uint32_t* seg_pos;  // [nseg + 1] first grouped position of each segment
     const uint32_t* cand_q;   // [C] record of candidate t
+    const uint64_t* c_rec;    // [C] rec_id, alt, unc_alt, unc_here, benefit of candidate t
+    const uint32_t* c_alt;
+    const uint32_t* c_ua;
+    const uint32_t* c_uh;
+    const int64_t* c_ben;
     const uint32_t* grp;      // [C] candidate order grouped by (rank, target)
     const uint32_t* g_alt;    // [C] target of grp[u]
     const uint32_t* g_unc;    // [C] unc_alt of grp[u]
@@ -436,6 +471,113 @@ __device__ __noinline__ uint32_t regs_bisect(const uint32_t* __restrict__ unc_he
     return lo;
 }
 
+// Acceptance walk over grouped positions [P0, P1): whole (source, target)
+// segments of the current source, by one wave (every lane active).  Sets the
+// acceptance bit of each accepted candidate (bit t - cs) and stores every
+// record's TTFT on its target at its turn.
+__device__ __forceinline__ void walk_run(const CommitArgs& a, uint32_t* s_bits, uint32_t* g_bits,
+                                         bool in_lds, const int64_t* s_L, uint32_t cs, uint32_t P0,
+                                         uint32_t P1)
+{
+    const uint32_t lane = threadIdx.x & (kWave - 1);
+    const uint64_t below = (1ull << lane) - 1;  // lanes under this one
+    uint32_t carry_j = kNoKey;  // target of the segment open at the last chunk's end
+    int64_t carry_L = 0;        // its load after the records walked so far
+    uint32_t cu[kWalkChunks], ct[kWalkChunks], cj[kWalkChunks];
+#pragma unroll
+    for (int g = 0; g < kWalkChunks; g++) {
+        const uint64_t v = (uint64_t)P0 + g * kWave + lane;
+        const bool in = v < P1;
+        cu[g] = in ? a.g_unc[v] : 0u;
+        ct[g] = in ? a.grp[v] : 0u;
+        cj[g] = in ? a.g_alt[v] : kNoKey;
+    }
+    for (uint64_t p = P0; p < P1; p += kWave * kWalkChunks) {
+        uint32_t nu[kWalkChunks], nt[kWalkChunks], nj[kWalkChunks];
+#pragma unroll
+        for (int g = 0; g < kWalkChunks; g++) {
+            const uint64_t v = p + (uint64_t)(kWalkChunks + g) * kWave + lane;
+            const bool in = v < P1;
+            nu[g] = in ? a.g_unc[v] : 0u;
+            nt[g] = in ? a.grp[v] : 0u;
+            nj[g] = in ? a.g_alt[v] : kNoKey;
+        }
+#pragma unroll
+        for (int g = 0; g < kWalkChunks; g++) {
+            const uint64_t pc = p + (uint64_t)g * kWave;
+            if (pc >= P1)
+                break;
+            const bool valid = pc + lane < P1;
+            const uint32_t u = cu[g], t = ct[g], j = cj[g];
+            uint32_t jprev = __shfl_up(j, 1);
+            if (lane == 0)
+                jprev = carry_j;
+            const uint64_t H = __ballot(valid && j != jprev);
+            const uint64_t self = 1ull << lane;
+            const uint64_t hm = H & (below | self), nm = H & ~(below | self);
+            const int seglo = hm ? 63 - __clzll(hm) : 0;  // my segment's lanes in this chunk
+            const int seghi = nm ? __ffsll((long long)nm) - 2 : 63;
+            const uint64_t segbits = (seghi == 63 ? ~0ull : (2ull << seghi) - 1) & ~((1ull << seglo) - 1);
+            const uint64_t excl = wave_incl_sum_u64(u, lane) - u;
+            // exact target load at the first unsettled record of a segment
+            int64_t Lx = 0;
+            if (valid && lane == seglo)
+                Lx = (H & self) ? s_L[j] : carry_L;
+            uint64_t U = __ballot(valid);  // unsettled records
+            bool ok = false;
+            int64_t Lt = 0;
+            while (U) {
+                // per segment: its first unsettled record f decides a run
+                // (f accepted: records accepted until one fails; f rejected:
+                // records rejected until one passes at f's load), and the
+                // record ending the run takes the other decision
+                const uint64_t fm = U & segbits;
+                const int f = fm ? __ffsll((long long)fm) - 1 : (int)lane;
+                const int64_t Lf = (int64_t)shfl_u64((uint64_t)Lx, f);
+                const uint32_t uf = __shfl(u, f);
+                const uint64_t exf = shfl_u64(excl, f);
+                const bool pf = a.tk((int64_t)uf, Lf) < a.tk.slo;
+                const int64_t Lv = pf ? Lf + (int64_t)(excl - exf) : Lf;
+                const bool pv = a.tk((int64_t)u, Lv) < a.tk.slo;
+                const bool inU = (U >> lane) & 1;
+                const uint64_t sm = __ballot(inU && pv != pf) & segbits;
+                const int st = sm ? __ffsll((long long)sm) - 1 : kWave;
+                const bool settle = inU && (int)lane <= st;
+                const bool d = (int)lane < st ? pf : !pf;
+                const int64_t nxt = Lv + (d ? (int64_t)u : 0);
+                const uint32_t plo = __shfl_up((uint32_t)nxt, 1);
+                const uint32_t phi = __shfl_up((uint32_t)((uint64_t)nxt >> 32), 1);
+                if (settle) {
+                    ok = d;
+                    Lt = Lv;
+                } else if (inU && (int)lane == st + 1) {
+                    Lx = (int64_t)(((uint64_t)phi << 32) | plo);
+                }
+                U &= ~__ballot(settle);
+            }
+            if (valid) {
+                a.tto[t] = a.tk((int64_t)u, Lt);
+                if (ok) {
+                    const uint32_t x = t - cs;
+                    if (in_lds)
+                        atomicOr(&s_bits[x >> 5], 1u << (x & 31));
+                    else
+                        atomicOr(&g_bits[x >> 5], 1u << (x & 31));
+                }
+            }
+            const int last = (int)std::min<uint64_t>(kWave - 1, P1 - 1 - pc);
+            carry_L = (int64_t)readlane_u64((uint64_t)(Lt + (ok ? (int64_t)u : 0)), last);
+            carry_j = __builtin_amdgcn_readlane(j, last);
+        }
+#pragma unroll
+        for (int g = 0; g < kWalkChunks; g++) {
+            cu[g] = nu[g];
+            ct[g] = nt[g];
+            cj[g] = nj[g];
+        }
+    }
+}
+
 __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
 {
     __shared__ int64_t sh[kCommitThreads / kWave];
@@ -463,31 +605,13 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
         for (int64_t q = qlo + tid; q < qhi; q += kCommitThreads)
             a.qkey[q] = kNoKey;
         wg_sync();
-        // (i) acceptance, one thread per (source, target) segment
-        for (uint32_t g = a.sseg[s] + tid; g < a.sseg[s + 1]; g += kCommitThreads) {
-            const uint32_t lo = a.seg_pos[g], hi = a.seg_pos[g + 1];
-            int64_t Lt = s_L[a.g_alt[lo]];
-            for (uint32_t v0 = lo; v0 < hi; v0 += kWalkBatch) {
-                uint32_t ub[kWalkBatch], tb[kWalkBatch];
-#pragma unroll
-                for (int r = 0; r < kWalkBatch; r++) {
-                    const bool in = (uint64_t)v0 + r < hi;
-                    ub[r] = in ? a.g_unc[v0 + r] : 0u;
-                    tb[r] = in ? a.grp[v0 + r] : 0u;
-                }
-#pragma unroll
-                for (int r = 0; r < kWalkBatch; r++) {
-                    if ((uint64_t)v0 + r < hi) {
-                        const int64_t tj = a.tk((int64_t)ub[r], Lt);
-                        a.tto[tb[r]] = tj;
-                        if (tj < a.tk.slo) {
-                            const uint32_t x = tb[r] - cs;
-                            atomicOr(&bits[x >> 5], 1u << (x & 31));
-                            Lt += ub[r];
-                        }
-                    }
-                }
-            }
+        // (i) acceptance: each wave walks a run of whole segments
+        {
+            const uint32_t wv = tid / kWave, G0 = a.sseg[s], ng = a.sseg[s + 1] - G0;
+            const uint32_t ga = G0 + (uint32_t)((uint64_t)ng * wv / kCommitWaves);
+            const uint32_t gb = G0 + (uint32_t)((uint64_t)ng * (wv + 1) / kCommitWaves);
+            if (ga < gb)
+                walk_run(a, s_bits, a.gbits, in_lds, s_L, cs, a.seg_pos[ga], a.seg_pos[gb]);
         }
         wg_sync();
         // (ii) acceptance ranks in candidate order: accepted candidates
@@ -497,12 +621,15 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
         const uint32_t w1 = (uint32_t)std::min<uint64_t>(nw, (tid + 1) * pw);
         int64_t cnt = 0;
         for (uint32_t w = w0; w < w1; w++)
-            cnt += __popc(bits_word(&bits[w]));
+            cnt += __popc(in_lds ? s_bits[w] : bits_word(&bits[w]));
         int64_t A;
         uint32_t run = (uint32_t)block_excl_scan_i64<kCommitThreads>(cnt, sh, A);
         for (uint32_t w = w0; w < w1; w++) {
-            __hip_atomic_store(&wpre[w], run, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            run += __popc(bits_word(&bits[w]));
+            if (in_lds)
+                s_wpre[w] = run;
+            else
+                __hip_atomic_store(&wpre[w], run, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            run += __popc(in_lds ? s_bits[w] : bits_word(&bits[w]));
         }
         wg_sync();
         // queue records of accepted candidates get their rank as key
@@ -518,9 +645,10 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
                 const uint64_t t = b + (uint64_t)r * kCommitThreads;
                 if (t < ce) {
                     const uint32_t x = (uint32_t)(t - cs), w = x >> 5, m = 1u << (x & 31);
-                    const uint32_t word = bits_word(&bits[w]);
+                    const uint32_t word = in_lds ? s_bits[w] : bits_word(&bits[w]);
                     if (word & m)
-                        a.qkey[qb[r]] = bits_word(&wpre[w]) + __popc(word & (m - 1));
+                        a.qkey[qb[r]] = (in_lds ? s_wpre[w] : bits_word(&wpre[w])) +
+                                        __popc(word & (m - 1));
                 }
             }
         }
@@ -552,32 +680,32 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
         const uint64_t base = s_count;
         int64_t dsrc = 0;
         for (uint32_t b = cs + tid; b < ce; b += kCommitThreads * kCommitBatch) {
-            uint32_t rk[kCommitBatch], qb[kCommitBatch];
+            uint32_t rk[kCommitBatch];
+            uint64_t rec[kCommitBatch];
+            uint32_t to[kCommitBatch], ua[kCommitBatch], uh[kCommitBatch];
+            int64_t ben[kCommitBatch], tt[kCommitBatch];
+            // the fields load before the rank test, so their latency overlaps it
+#pragma unroll
+            for (int r = 0; r < kCommitBatch; r++) {
+                const uint64_t t = b + (uint64_t)r * kCommitThreads;
+                if (t < ce) {
+                    rec[r] = a.c_rec[t];
+                    to[r] = a.c_alt[t];
+                    ua[r] = a.c_ua[t];
+                    uh[r] = a.c_uh[t];
+                    ben[r] = a.c_ben[t];
+                    tt[r] = a.tto[t];
+                }
+            }
 #pragma unroll
             for (int r = 0; r < kCommitBatch; r++) {
                 const uint64_t t = b + (uint64_t)r * kCommitThreads;
                 rk[r] = kNoKey;
                 if (t < ce) {
                     const uint32_t x = (uint32_t)(t - cs), w = x >> 5, m = 1u << (x & 31);
-                    const uint32_t word = bits_word(&bits[w]);
+                    const uint32_t word = in_lds ? s_bits[w] : bits_word(&bits[w]);
                     if (word & m)
-                        rk[r] = bits_word(&wpre[w]) + __popc(word & (m - 1));
-                }
-                qb[r] = rk[r] < kstar ? a.cand_q[t] : 0u;
-            }
-            uint64_t rec[kCommitBatch];
-            uint32_t to[kCommitBatch], ua[kCommitBatch], uh[kCommitBatch];
-            int64_t ben[kCommitBatch], tt[kCommitBatch];
-#pragma unroll
-            for (int r = 0; r < kCommitBatch; r++) {
-                if (rk[r] < kstar) {
-                    const uint32_t q = qb[r];
-                    rec[r] = a.rec_id[q];
-                    to[r] = a.alt[q];
-                    ua[r] = a.unc_alt[q];
-                    uh[r] = a.unc_here[q];
-                    ben[r] = a.benefit[q];
-                    tt[r] = a.tto[b + (uint64_t)r * kCommitThreads];
+                        rk[r] = (in_lds ? s_wpre[w] : bits_word(&wpre[w])) + __popc(word & (m - 1));
                 }
             }
 #pragma unroll
@@ -676,6 +804,9 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     // per-candidate arrays
     const uint64_t Ca = C ? C : 1;
     uint8_t* pc = static_cast<uint8_t*>(scratch_get(c, 2, Ca * 64 + 16 * 256, &e));
+    // per candidate: keys, ktmp 8 B; vals, vtmp, grp, g_alt, g_unc, seg_pos,
+    // c_ua, c_uh 4 B; tto 8 B; two bit-word arrays 1/8 B -- 56.25 B and 13
+    // carves of at most 256 B padding each
     if (!pc)
         return e;
     uint64_t* keys = carve<uint64_t>(pc, Ca);
@@ -689,6 +820,8 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     uint32_t* gwpre = carve<uint32_t>(pc, Ca / 32 + 1);
     int64_t* tto = carve<int64_t>(pc, Ca);
     uint32_t* seg_pos = carve<uint32_t>(pc, Ca + 1);
+    uint32_t* c_ua = carve<uint32_t>(pc, Ca);
+    uint32_t* c_uh = carve<uint32_t>(pc, Ca);
     uint32_t* cand_q = vals;  // the candidate order lands in vals
 
     if (C) {
@@ -728,6 +861,14 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     }
     seg_pos_kernel<<<grid_for(std::max<uint64_t>(C, S) + 1, 256), 256, 0, st>>>(
         C, S, head, sid, ctot, start, nsrc, seg_pos, sseg);
+    // the commit's record fields in candidate order (head and sid are spent)
+    uint64_t* c_rec = ktmp;
+    int64_t* c_ben = reinterpret_cast<int64_t*>(keys);
+    uint32_t* c_alt = vtmp;
+    if (C)
+        gather_cand_kernel<<<grid_for(C, 256), 256, 0, st>>>(C, cand_q, q->rec_id, q->alt,
+                                                            q->unc_alt, q->unc_here, benefit,
+                                                            c_rec, c_alt, c_ua, c_uh, c_ben);
     copy_i64_kernel<<<grid_for(S, 256), 256, 0, st>>>(L0, loads_out, S);
     CommitArgs a;
     a.qoff = q->qoff;
@@ -743,6 +884,11 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     a.sseg = sseg;
     a.seg_pos = seg_pos;
     a.cand_q = cand_q;
+    a.c_rec = c_rec;
+    a.c_alt = c_alt;
+    a.c_ua = c_ua;
+    a.c_uh = c_uh;
+    a.c_ben = c_ben;
     a.grp = grp;
     a.g_alt = g_alt;
     a.g_unc = g_unc;

@@ -145,12 +145,16 @@ __global__ __launch_bounds__(kQThreads) void queue_kernel(
     }
 }
 
-__global__ void benefit_kernel(uint64_t Q, const int64_t* __restrict__ T,
-                               const uint32_t* __restrict__ owner, const uint32_t* __restrict__ alt,
-                               const uint32_t* __restrict__ unc_alt, const int64_t* __restrict__ L0,
-                               const uint8_t* __restrict__ over, uint32_t S, TtftK tk,
-                               int64_t* __restrict__ benefit, uint64_t* __restrict__ elig)
+// Per record: benefit and eligibility; the largest eligible benefit goes to
+// *maxb (it sizes the sort key).
+__global__ __launch_bounds__(256) void benefit_kernel(
+    uint64_t Q, const int64_t* __restrict__ T, const uint32_t* __restrict__ owner,
+    const uint32_t* __restrict__ alt, const uint32_t* __restrict__ unc_alt,
+    const int64_t* __restrict__ L0, const uint8_t* __restrict__ over, uint32_t S, TtftK tk,
+    int64_t* __restrict__ benefit, uint64_t* __restrict__ elig, uint64_t* __restrict__ maxb)
 {
+    __shared__ int64_t sh[256 / kWave];
+    int64_t mx = 0;
     for (uint64_t q = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; q < Q;
          q += (uint64_t)gridDim.x * blockDim.x) {
         const uint32_t i = owner[q], j = alt[q];
@@ -162,7 +166,12 @@ __global__ void benefit_kernel(uint64_t Q, const int64_t* __restrict__ T,
         }
         benefit[q] = b;
         elig[q] = e ? 1 : 0;
+        if (e)
+            mx = std::max(mx, b);
     }
+    mx = block_max_i64<256>(mx, sh);
+    if (threadIdx.x == 0 && mx > 0)
+        atomicMax((unsigned long long*)maxb, (unsigned long long)mx);
 }
 
 // rank[i] of overloaded instance i among (load desc, id asc); src[rank] = i.
@@ -214,9 +223,13 @@ __global__ void compact_kernel(uint64_t Q, const uint64_t* __restrict__ elig,
 }
 
 // keys[t] = a key of the record (or candidate index) held in vals[t].
-enum KeyKind { kByBenefitDesc, kBySourceRank, kByTarget, kByRankOfCand };
+// kByRankBenefit: (source rank, benefit descending in its low `sh` bits) of
+// record vals[t]; kByRankTarget: (source rank, target in `sh` bits) of
+// candidate vals[t]; kByBenefitDesc / kBySourceRank: the two halves of the
+// first, for benefits too wide to share a key with the rank.
+enum KeyKind { kByRankBenefit, kByRankTarget, kByBenefitDesc, kBySourceRank };
 
-__global__ void rekey_kernel(uint64_t C, int kind, const uint32_t* __restrict__ vals,
+__global__ void rekey_kernel(uint64_t C, int kind, uint32_t sh, const uint32_t* __restrict__ vals,
                              const uint32_t* __restrict__ cand_q, const int64_t* __restrict__ benefit,
                              const uint32_t* __restrict__ owner, const uint32_t* __restrict__ rank,
                              const uint32_t* __restrict__ alt, uint64_t* __restrict__ keys)
@@ -226,13 +239,30 @@ __global__ void rekey_kernel(uint64_t C, int kind, const uint32_t* __restrict__ 
         const uint32_t v = vals[t];
         uint64_t k = 0;
         switch (kind) {
+            case kByRankBenefit:
+                k = ((uint64_t)rank[owner[v]] << sh) |
+                    (((1ull << sh) - 1) - (uint64_t)benefit[v]);
+                break;
+            case kByRankTarget: {
+                const uint32_t q = cand_q[v];
+                k = ((uint64_t)rank[owner[q]] << sh) | alt[q];
+                break;
+            }
             case kByBenefitDesc: k = ~(uint64_t)benefit[v]; break;
             case kBySourceRank: k = rank[owner[v]]; break;
-            case kByTarget: k = alt[cand_q[v]]; break;
-            case kByRankOfCand: k = rank[owner[cand_q[v]]]; break;
         }
         keys[t] = k;
     }
+}
+
+inline int bit_length(uint64_t x)
+{
+    int n = 0;
+    while (x) {
+        n++;
+        x >>= 1;
+    }
+    return n;
 }
 
 __global__ void iota_kernel(uint64_t C, uint32_t* __restrict__ v)
@@ -769,7 +799,7 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     uint32_t* start = carve<uint32_t>(pi, S + 1);
     uint32_t* sseg = carve<uint32_t>(pi, S + 1);
     uint32_t* nsrc = carve<uint32_t>(pi, 1);
-    uint64_t* ctot = carve<uint64_t>(pi, 1);
+    uint64_t* ctot = carve<uint64_t>(pi, 2);  // candidate count, largest eligible benefit
     // per-record arrays
     const uint64_t Qa = Q ? Q : 1;
     uint8_t* pr = static_cast<uint8_t*>(scratch_get(c, 1, Qa * 48 + 8 * 256, &e));
@@ -783,24 +813,27 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     uint32_t* qkey = carve<uint32_t>(pr, Qa);
 
     zero_u32_kernel<<<1, 64, 0, st>>>(nsrc, 1);
+    zero_u32_kernel<<<1, 64, 0, st>>>(reinterpret_cast<uint32_t*>(ctot), 4);
     fill_u32_kernel<<<grid_for(Qa, 256), 256, 0, st>>>(owner, Qa, 0xFFFFFFFFu);
     queue_kernel<<<S, kQThreads, 0, st>>>(q->qoff, Q, q->unc_here, q->alt, q->base_work, S, tk, T,
                                           owner, L0, over, c->d_status);
     if (Q)
-        benefit_kernel<<<grid_for(Q, 256), 256, 0, st>>>(Q, T, owner, q->alt, q->unc_alt, L0, over,
-                                                         S, tk, benefit, elig);
+        // grid-stride: 256 workgroups, one atomic maximum each
+        benefit_kernel<<<grid_for(Q, 256, 256), 256, 0, st>>>(Q, T, owner, q->alt, q->unc_alt, L0,
+                                                              over, S, tk, benefit, elig, ctot + 1);
     rank_kernel<<<(S + 255) / 256, 256, 0, st>>>(L0, over, S, rank, src, nsrc);
-    uint64_t C = 0;
+    uint64_t hw[2] = {0, 0};  // candidate count, largest eligible benefit
     if (Q) {
         e = exclusive_scan_u64(c, elig, Q, pos, ctot);
         if (e != hipSuccess)
             return e;
-        e = hipMemcpyAsync(&C, ctot, sizeof(uint64_t), hipMemcpyDeviceToHost, st);
+        e = hipMemcpyAsync(hw, ctot, sizeof(hw), hipMemcpyDeviceToHost, st);
         if (e == hipSuccess)
             e = hipStreamSynchronize(st);
         if (e != hipSuccess)
             return e;
     }
+    const uint64_t C = hw[0];
     // per-candidate arrays
     const uint64_t Ca = C ? C : 1;
     uint8_t* pc = static_cast<uint8_t*>(scratch_get(c, 2, Ca * 64 + 16 * 256, &e));
@@ -827,25 +860,32 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     if (C) {
         const uint32_t gc = grid_for(C, 256);
         compact_kernel<<<grid_for(Q, 256), 256, 0, st>>>(Q, elig, pos, vals);
-        // order: benefit desc, then source rank asc (stable passes over record order)
-        rekey_kernel<<<gc, 256, 0, st>>>(C, kByBenefitDesc, vals, nullptr, benefit, owner, rank,
-                                         q->alt, keys);
-        e = radix_sort_kv(c, keys, vals, ktmp, vtmp, C, 64);
-        if (e != hipSuccess) return e;
-        rekey_kernel<<<gc, 256, 0, st>>>(C, kBySourceRank, vals, nullptr, benefit, owner, rank,
-                                         q->alt, keys);
-        e = radix_sort_kv(c, keys, vals, ktmp, vtmp, C, 16);
-        if (e != hipSuccess) return e;
-        // grouping: candidate indices by (source rank, target), order kept
+        // candidate order (source rank, benefit desc), stable over record order
+        // so equal benefits keep queue order; grouped order (source rank,
+        // target), stable over candidate order.  Keys take only the bits the
+        // ranks, targets and largest benefit need.
+        const int rb = std::max(1, bit_length(S - 1));
+        const int nb = bit_length(hw[1]);
+        if (rb + nb <= 64) {
+            rekey_kernel<<<gc, 256, 0, st>>>(C, kByRankBenefit, (uint32_t)nb, vals, nullptr, benefit,
+                                             owner, rank, q->alt, keys);
+            e = radix_sort_kv(c, keys, vals, ktmp, vtmp, C, rb + nb);
+            if (e != hipSuccess) return e;
+        } else {
+            rekey_kernel<<<gc, 256, 0, st>>>(C, kByBenefitDesc, 0, vals, nullptr, benefit, owner,
+                                             rank, q->alt, keys);
+            e = radix_sort_kv(c, keys, vals, ktmp, vtmp, C, 64);
+            if (e != hipSuccess) return e;
+            rekey_kernel<<<gc, 256, 0, st>>>(C, kBySourceRank, 0, vals, nullptr, benefit, owner,
+                                             rank, q->alt, keys);
+            e = radix_sort_kv(c, keys, vals, ktmp, vtmp, C, rb);
+            if (e != hipSuccess) return e;
+        }
         iota_kernel<<<gc, 256, 0, st>>>(C, grp);
-        rekey_kernel<<<gc, 256, 0, st>>>(C, kByTarget, grp, cand_q, benefit, owner, rank, q->alt,
-                                         ktmp);
+        rekey_kernel<<<gc, 256, 0, st>>>(C, kByRankTarget, (uint32_t)rb, grp, cand_q, benefit,
+                                         owner, rank, q->alt, ktmp);
         // sort (ktmp, grp) using (keys, vtmp) as work arrays: keys is free once cand_q is final
-        e = radix_sort_kv(c, ktmp, grp, keys, vtmp, C, 16);
-        if (e != hipSuccess) return e;
-        rekey_kernel<<<gc, 256, 0, st>>>(C, kByRankOfCand, grp, cand_q, benefit, owner, rank,
-                                         q->alt, ktmp);
-        e = radix_sort_kv(c, ktmp, grp, keys, vtmp, C, 16);
+        e = radix_sort_kv(c, ktmp, grp, keys, vtmp, C, 2 * rb);
         if (e != hipSuccess) return e;
         gather_groups_kernel<<<gc, 256, 0, st>>>(C, grp, cand_q, q->alt, q->unc_alt, g_alt, g_unc);
     }

@@ -43,7 +43,7 @@
 namespace dm {
 namespace {
 
-constexpr int kQThreads = 256;
+constexpr int kQThreads = 1024;
 constexpr int kCommitThreads = 512;
 constexpr int kCommitWaves = kCommitThreads / kWave;
 constexpr int kWalkBatch = 16;   // records loaded ahead of a dependent pass
@@ -103,7 +103,9 @@ __device__ int64_t block_max_i64(int64_t v, int64_t* sh)
     return m;
 }
 
-// Per instance (one workgroup each): record TTFTs, load, max TTFT.
+// Per instance (one workgroup each): record TTFTs, load, max TTFT.  Each
+// thread takes a contiguous run of the queue, so one workgroup scan places
+// every run behind the base work and the runs ahead of it.
 __global__ __launch_bounds__(kQThreads) void queue_kernel(
     const int64_t* __restrict__ qoff, uint64_t Q, const uint32_t* __restrict__ unc_here,
     const uint32_t* __restrict__ alt, const int64_t* __restrict__ base_work, uint32_t S, TtftK tk,
@@ -121,26 +123,48 @@ __global__ __launch_bounds__(kQThreads) void queue_kernel(
         }
         return;
     }
-    int64_t run = base_work[i], mx = INT64_MIN;
-    for (int64_t b = lo; b < hi; b += kQThreads) {
-        const int64_t q = b + threadIdx.x;
-        const bool ok = q < hi;
-        const int64_t u = ok ? (int64_t)unc_here[q] : 0;
-        int64_t tot;
-        const int64_t ex = block_excl_scan_i64<kQThreads>(u, sh, tot);
-        if (ok) {
-            const int64_t t = tk(u, run + ex);
-            T[q] = t;
-            owner[q] = i;
-            mx = std::max(mx, t);
-            if (alt[q] >= S)
-                atomicOr(status, kErrInval);
-        }
-        run += tot;
+    const uint64_t n = (uint64_t)(hi - lo), per = (n + kQThreads - 1) / kQThreads;
+    const int64_t b0 = lo + (int64_t)std::min<uint64_t>(n, threadIdx.x * per);
+    const int64_t b1 = lo + (int64_t)std::min<uint64_t>(n, (threadIdx.x + 1) * per);
+    int64_t sum = 0;
+    for (int64_t b = b0; b < b1; b += kWalkBatch) {
+        uint32_t ub[kWalkBatch];
+#pragma unroll
+        for (int r = 0; r < kWalkBatch; r++)
+            ub[r] = b + r < b1 ? unc_here[b + r] : 0u;
+#pragma unroll
+        for (int r = 0; r < kWalkBatch; r++)
+            sum += ub[r];
     }
+    int64_t tot;
+    int64_t run = base_work[i] + block_excl_scan_i64<kQThreads>(sum, sh, tot);
+    int64_t mx = INT64_MIN;
+    bool bad = false;
+    for (int64_t b = b0; b < b1; b += kWalkBatch) {
+        uint32_t ub[kWalkBatch], ab[kWalkBatch];
+#pragma unroll
+        for (int r = 0; r < kWalkBatch; r++) {
+            const bool in = b + r < b1;
+            ub[r] = in ? unc_here[b + r] : 0u;
+            ab[r] = in ? alt[b + r] : 0u;
+        }
+#pragma unroll
+        for (int r = 0; r < kWalkBatch; r++) {
+            if (b + r < b1) {
+                const int64_t t = tk((int64_t)ub[r], run);
+                T[b + r] = t;
+                owner[b + r] = i;
+                mx = std::max(mx, t);
+                bad |= ab[r] >= S;
+                run += ub[r];
+            }
+        }
+    }
+    if (bad)
+        atomicOr(status, kErrInval);
     mx = block_max_i64<kQThreads>(mx, sh);
     if (threadIdx.x == 0) {
-        L0[i] = run;
+        L0[i] = base_work[i] + tot;
         over[i] = (hi > lo && mx > tk.slo) ? 1 : 0;
     }
 }

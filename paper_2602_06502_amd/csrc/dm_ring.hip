@@ -50,6 +50,13 @@ __global__ void remap_kernel(RingView o1, RingView o2, RingView n1, RingView n2,
                              uint32_t* __restrict__ old_owner, uint32_t* __restrict__ new_owner,
                              uint64_t* __restrict__ moved, uint64_t* __restrict__ violations)
 {
+    // counts gather per wave over the grid-stride loop, then per workgroup in
+    // LDS: three device atomics per workgroup, not per wave
+    __shared__ unsigned long long s_cnt[3];
+    if (threadIdx.x < 3)
+        s_cnt[threadIdx.x] = 0;
+    __syncthreads();
+    uint64_t c1 = 0, c2 = 0, cb = 0;
     const uint64_t total = 2 * n;
     for (uint64_t base = blockIdx.x * (uint64_t)blockDim.x; base < total;
          base += (uint64_t)gridDim.x * blockDim.x) {
@@ -66,12 +73,20 @@ __global__ void remap_kernel(RingView o1, RingView o2, RingView n1, RingView n2,
             mv = a != b;
             bad = mv && !is_rm[a] && !is_add[b];
         }
-        const uint64_t m1 = ballot(mv && !second), m2 = ballot(mv && second), mb = ballot(bad);
-        if ((threadIdx.x & 63) == 0) {
-            if (m1) atomicAdd((unsigned long long*)&moved[0], (unsigned long long)__popcll(m1));
-            if (m2) atomicAdd((unsigned long long*)&moved[1], (unsigned long long)__popcll(m2));
-            if (mb) atomicAdd((unsigned long long*)violations, (unsigned long long)__popcll(mb));
-        }
+        c1 += __popcll(ballot(mv && !second));
+        c2 += __popcll(ballot(mv && second));
+        cb += __popcll(ballot(bad));
+    }
+    if ((threadIdx.x & 63) == 0) {
+        if (c1) atomicAdd(&s_cnt[0], (unsigned long long)c1);
+        if (c2) atomicAdd(&s_cnt[1], (unsigned long long)c2);
+        if (cb) atomicAdd(&s_cnt[2], (unsigned long long)cb);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        if (s_cnt[0]) atomicAdd((unsigned long long*)&moved[0], s_cnt[0]);
+        if (s_cnt[1]) atomicAdd((unsigned long long*)&moved[1], s_cnt[1]);
+        if (s_cnt[2]) atomicAdd((unsigned long long*)violations, s_cnt[2]);
     }
 }
 
@@ -136,7 +151,7 @@ hipError_t ring_remap(dm_ctx* c, const Ring old_r[2], const Ring new_r[2], const
     zero_u64_kernel<<<1, 64, 0, c->stream>>>(moved, 2);
     zero_u64_kernel<<<1, 64, 0, c->stream>>>(violations, 1);
     if (n)
-        remap_kernel<<<grid_for(2 * n, 256, 8192), 256, 0, c->stream>>>(
+        remap_kernel<<<grid_for(2 * n, 256, 1024), 256, 0, c->stream>>>(
             view(old_r[0]), view(old_r[1]), view(new_r[0]), view(new_r[1]), keys, n,
             c->d_flag_add, c->d_flag_rm, old_owner, new_owner, moved, violations);
     return hipGetLastError();

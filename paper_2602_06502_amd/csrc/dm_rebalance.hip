@@ -415,6 +415,9 @@ struct CommitArgs {
     uint32_t* gbits;          // [C / 32 + 1] acceptance bits when LDS cannot hold them
     uint32_t* gwpre;          // [C / 32 + 1] accepted candidates before each bit word
     int64_t* tto;             // [C]
+    uint32_t* arank;          // [C] acceptance rank of candidate t, kNoKey if not accepted
+    uint32_t* kstar_of;       // [nsrc] accepted records that move, per source rank
+    uint64_t* base_of;        // [nsrc] their first index in the migration list
     uint32_t* qkey;           // [Q]
     int64_t* loads;           // [S] in: pass-start loads; out: loads after the pass
     uint32_t S;
@@ -700,9 +703,12 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
                 if (t < ce) {
                     const uint32_t x = (uint32_t)(t - cs), w = x >> 5, m = 1u << (x & 31);
                     const uint32_t word = in_lds ? s_bits[w] : bits_word(&bits[w]);
-                    if (word & m)
-                        a.qkey[qb[r]] = (in_lds ? s_wpre[w] : bits_word(&wpre[w])) +
-                                        __popc(word & (m - 1));
+                    uint32_t rk = kNoKey;
+                    if (word & m) {
+                        rk = (in_lds ? s_wpre[w] : bits_word(&wpre[w])) + __popc(word & (m - 1));
+                        a.qkey[qb[r]] = rk;
+                    }
+                    a.arank[t] = rk;
                 }
             }
         }
@@ -730,49 +736,28 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
             }
             kstar = lo;
         }
-        // (iii) commit the first kstar accepted records; loads move in LDS
+        // (iii) the first kstar accepted records move: target loads grow and
+        // the source's shrinks, in LDS; emit_kernel writes the migrations
         const uint64_t base = s_count;
+        if (tid == 0) {
+            a.kstar_of[s] = kstar;
+            a.base_of[s] = base;
+        }
         int64_t dsrc = 0;
         for (uint32_t b = cs + tid; b < ce; b += kCommitThreads * kCommitBatch) {
-            uint32_t rk[kCommitBatch];
-            uint64_t rec[kCommitBatch];
-            uint32_t to[kCommitBatch], ua[kCommitBatch], uh[kCommitBatch];
-            int64_t ben[kCommitBatch], tt[kCommitBatch];
-            // the fields load before the rank test, so their latency overlaps it
+            uint32_t rk[kCommitBatch], to[kCommitBatch], ua[kCommitBatch], uh[kCommitBatch];
 #pragma unroll
             for (int r = 0; r < kCommitBatch; r++) {
                 const uint64_t t = b + (uint64_t)r * kCommitThreads;
-                if (t < ce) {
-                    rec[r] = a.c_rec[t];
-                    to[r] = a.c_alt[t];
-                    ua[r] = a.c_ua[t];
-                    uh[r] = a.c_uh[t];
-                    ben[r] = a.c_ben[t];
-                    tt[r] = a.tto[t];
-                }
-            }
-#pragma unroll
-            for (int r = 0; r < kCommitBatch; r++) {
-                const uint64_t t = b + (uint64_t)r * kCommitThreads;
-                rk[r] = kNoKey;
-                if (t < ce) {
-                    const uint32_t x = (uint32_t)(t - cs), w = x >> 5, m = 1u << (x & 31);
-                    const uint32_t word = in_lds ? s_bits[w] : bits_word(&bits[w]);
-                    if (word & m)
-                        rk[r] = (in_lds ? s_wpre[w] : bits_word(&wpre[w])) + __popc(word & (m - 1));
-                }
+                const bool in = t < ce;
+                rk[r] = in ? a.arank[t] : kNoKey;
+                to[r] = in ? a.c_alt[t] : 0u;
+                ua[r] = in ? a.c_ua[t] : 0u;
+                uh[r] = in ? a.c_uh[t] : 0u;
             }
 #pragma unroll
             for (int r = 0; r < kCommitBatch; r++) {
                 if (rk[r] < kstar) {
-                    const uint64_t idx = base + rk[r];
-                    if (idx < a.cap) {
-                        a.out_rec[idx] = rec[r];
-                        a.out_from[idx] = i;
-                        a.out_to[idx] = to[r];
-                        a.out_benefit[idx] = ben[r];
-                        a.out_ttft[idx] = tt[r];
-                    }
                     atomicAdd((unsigned long long*)&s_L[to[r]], (unsigned long long)ua[r]);
                     dsrc += uh[r];
                 }
@@ -794,6 +779,48 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
     }
 }
 
+
+// Migration list: candidate t of source rank r moves iff its acceptance rank
+// is below kstar_of[r]; it lands at base_of[r] + rank (rank order within a
+// source, sources in rank order).
+__global__ void emit_kernel(uint64_t C, const uint32_t* __restrict__ start,
+                            const uint32_t* __restrict__ nsrc_p, const uint32_t* __restrict__ src,
+                            const uint32_t* __restrict__ arank,
+                            const uint32_t* __restrict__ kstar_of,
+                            const uint64_t* __restrict__ base_of, const uint64_t* __restrict__ c_rec,
+                            const uint32_t* __restrict__ c_alt, const int64_t* __restrict__ c_ben,
+                            const int64_t* __restrict__ tto, uint64_t cap,
+                            uint64_t* __restrict__ out_rec, uint32_t* __restrict__ out_from,
+                            uint32_t* __restrict__ out_to, int64_t* __restrict__ out_benefit,
+                            int64_t* __restrict__ out_ttft)
+{
+    const uint32_t nsrc = *nsrc_p;
+    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < C;
+         t += (uint64_t)gridDim.x * blockDim.x) {
+        const uint32_t rk = arank[t];
+        if (rk == kNoKey)
+            continue;
+        // source rank: the last r with start[r] <= t
+        uint32_t lo = 0, hi = nsrc;  // start[lo] <= t < start[hi]
+        while (hi - lo > 1) {
+            const uint32_t mid = (lo + hi) / 2;
+            if (start[mid] <= t)
+                lo = mid;
+            else
+                hi = mid;
+        }
+        if (rk >= kstar_of[lo])
+            continue;
+        const uint64_t idx = base_of[lo] + rk;
+        if (idx < cap) {
+            out_rec[idx] = c_rec[t];
+            out_from[idx] = src[lo];
+            out_to[idx] = c_alt[t];
+            out_benefit[idx] = c_ben[t];
+            out_ttft[idx] = tto[t];
+        }
+    }
+}
 
 template <typename T>
 T* carve(uint8_t*& p, uint64_t n)
@@ -822,6 +849,8 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     uint32_t* src = carve<uint32_t>(pi, S);
     uint32_t* start = carve<uint32_t>(pi, S + 1);
     uint32_t* sseg = carve<uint32_t>(pi, S + 1);
+    uint32_t* kstar_of = carve<uint32_t>(pi, S);
+    uint64_t* base_of = carve<uint64_t>(pi, S);
     uint32_t* nsrc = carve<uint32_t>(pi, 1);
     uint64_t* ctot = carve<uint64_t>(pi, 2);  // candidate count, largest eligible benefit
     // per-record arrays
@@ -862,8 +891,8 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     const uint64_t Ca = C ? C : 1;
     uint8_t* pc = static_cast<uint8_t*>(scratch_get(c, 2, Ca * 64 + 16 * 256, &e));
     // per candidate: keys, ktmp 8 B; vals, vtmp, grp, g_alt, g_unc, seg_pos,
-    // c_ua, c_uh 4 B; tto 8 B; two bit-word arrays 1/8 B -- 56.25 B and 13
-    // carves of at most 256 B padding each
+    // c_ua, c_uh, arank 4 B; tto 8 B; two bit-word arrays 1/8 B -- 60.25 B
+    // and 14 carves of at most 256 B padding each
     if (!pc)
         return e;
     uint64_t* keys = carve<uint64_t>(pc, Ca);
@@ -879,6 +908,7 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     uint32_t* seg_pos = carve<uint32_t>(pc, Ca + 1);
     uint32_t* c_ua = carve<uint32_t>(pc, Ca);
     uint32_t* c_uh = carve<uint32_t>(pc, Ca);
+    uint32_t* arank = carve<uint32_t>(pc, Ca);
     uint32_t* cand_q = vals;  // the candidate order lands in vals
 
     if (C) {
@@ -959,6 +989,9 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     a.gbits = gbits;
     a.gwpre = gwpre;
     a.tto = tto;
+    a.arank = arank;
+    a.kstar_of = kstar_of;
+    a.base_of = base_of;
     a.qkey = qkey;
     a.loads = loads_out;
     a.S = S;
@@ -972,6 +1005,10 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     a.out_count = out->count;
     a.status = c->d_status;
     commit_kernel<<<1, kCommitThreads, 0, st>>>(a);
+    if (C)
+        emit_kernel<<<grid_for(C, 256), 256, 0, st>>>(
+            C, start, nsrc, src, arank, kstar_of, base_of, c_rec, c_alt, c_ben, tto, cap,
+            out->rec_id, out->from, out->to, out->benefit_us, out->ttft_to_us);
     return hipGetLastError();
 }
 

@@ -49,7 +49,7 @@ constexpr int kCommitWaves = kCommitThreads / kWave;
 constexpr int kWalkBatch = 16;   // records loaded ahead of a dependent pass
 constexpr int kWalkChunks = 4;   // 64-record chunks of an acceptance walk loaded together
 constexpr int kQueueRegs = 64;   // queue records per thread held in registers
-constexpr int kCommitBatch = 8;  // committed records whose gathers are in flight together
+constexpr int kCommitBatch = 16; // candidates whose loads are in flight together in the commit
 // acceptance bits of up to 262,144 candidates per source live in LDS; a
 // source with more uses the same layout in device memory
 constexpr uint32_t kLdsBitWords = 8192;
@@ -583,6 +583,33 @@ __device__ __forceinline__ void walk_run(const CommitArgs& a, uint32_t* s_bits, 
             uint64_t U = __ballot(valid);  // unsettled records
             bool ok = false;
             int64_t Lt = 0;
+            if ((H & ~1ull) == 0) {
+                // one segment in this chunk: the same rounds with the first
+                // undecided record and the run's end uniform, read by readlane
+                int64_t Lf = (int64_t)readlane_u64((uint64_t)Lx, 0);
+                while (U) {
+                    const int f = __ffsll((long long)U) - 1;
+                    const uint32_t uf = __builtin_amdgcn_readlane(u, f);
+                    const uint64_t exf = readlane_u64(excl, f);
+                    const bool pf = a.tk((int64_t)uf, Lf) < a.tk.slo;
+                    const int64_t Lv = pf ? Lf + (int64_t)(excl - exf) : Lf;
+                    const bool pv = a.tk((int64_t)u, Lv) < a.tk.slo;
+                    const bool inU = (U >> lane) & 1;
+                    const uint64_t sm = __ballot(inU && pv != pf);
+                    const int st = sm ? __ffsll((long long)sm) - 1 : kWave;
+                    if (inU && (int)lane <= st) {
+                        ok = (int)lane < st ? pf : !pf;
+                        Lt = Lv;
+                    }
+                    if (st == kWave)
+                        break;
+                    // the run's last record takes the other decision
+                    Lf = (int64_t)readlane_u64((uint64_t)Lv, st) +
+                         (pf ? 0 : (int64_t)__builtin_amdgcn_readlane(u, st));
+                    U &= ~((2ull << st) - 1);
+                }
+                U = 0;
+            }
             while (U) {
                 // per segment: its first unsettled record f decides a run
                 // (f accepted: records accepted until one fails; f rejected:

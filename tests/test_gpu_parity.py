@@ -534,6 +534,31 @@ def test_rebalance_long_queues_many_targets_parity():
     assert len(np.unique(r["dst"])) > 512
 
 
+def test_rebalance_candidates_past_lds_parity():
+    """One source with 300,000 queued records, nearly all eligible: more
+    candidates than the commit kernel keeps acceptance bits for in LDS
+    (262,144), so the bits and their prefix counts live in device memory,
+    and a queue longer than the register form holds (chunked probes).  The
+    queue starts just over the SLO, so the stop rule ends the pass after
+    about 1,300 migrations."""
+    gh = _h()
+    S, n_live = 64, 60
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=S, index_log2_slots=8,
+               slo_us=400_000)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    o = oracle.Oracle(cfg)
+    q = workloads.synthetic_queues(41, S, n_live, np.array([17]), 300_000, 4, 50_000, 1_232_000)
+    # the case: eligible candidates (benefit > 0, every target below the SLO)
+    u = q.unc_here.astype(np.int64)
+    before = np.concatenate([[0], np.cumsum(u)[:-1]])
+    t_here = 2_000 + 3 * u + ((q.base_work[17] + before) >> 2)
+    t_alt = 2_000 + 3 * q.unc_alt.astype(np.int64) + (q.base_work[q.alt] >> 2)
+    assert int((t_here > t_alt).sum()) > 262_144
+    _say("rebalance past LDS: records", len(q.rec_id))
+    r = compare_rebalance(eng, o, q)
+    assert 1_000 < r["count"] < 2_000
+
+
 def _queues_from_route(chosen, cand, match, off, B, S, base_work):
     """Queues built from a routed batch: each request queued on its chosen
     instance in arrival order; alternative = the other candidate."""

@@ -43,7 +43,8 @@
 namespace dm {
 namespace {
 
-constexpr int kQThreads = 1024;
+constexpr int kQThreads = 256;
+constexpr uint32_t kQSplit = 16;  // workgroups per queue in the queue scan
 constexpr int kCommitThreads = 512;
 constexpr int kCommitWaves = kCommitThreads / kWave;
 constexpr int kWalkBatch = 16;   // records loaded ahead of a dependent pass
@@ -103,31 +104,42 @@ __device__ int64_t block_max_i64(int64_t v, int64_t* sh)
     return m;
 }
 
-// Per instance (one workgroup each): record TTFTs, load, max TTFT.  Each
-// thread takes a contiguous run of the queue, so one workgroup scan places
-// every run behind the base work and the runs ahead of it.
-__global__ __launch_bounds__(kQThreads) void queue_kernel(
+// Per-queue TTFTs, loads and the overloaded set, each queue cut into kQSplit
+// slices of contiguous records so that every queue spreads over kQSplit
+// workgroups: slice sums; then each slice's records behind the base work and
+// the slices ahead of it (largest TTFT per slice); then per instance the load
+// and whether its largest queued TTFT exceeds the SLO.
+__device__ __forceinline__ bool queue_ok(const int64_t* qoff, uint32_t i, uint64_t Q)
+{
+    const int64_t lo = qoff[i], hi = qoff[i + 1];
+    return lo >= 0 && hi >= lo && hi <= (int64_t)Q;
+}
+
+__device__ __forceinline__ void slice_of(const int64_t* qoff, uint32_t i, uint32_t p, int64_t& b0,
+                                         int64_t& b1)
+{
+    const int64_t lo = qoff[i], n = qoff[i + 1] - lo;
+    b0 = lo + (int64_t)((uint64_t)n * p / kQSplit);
+    b1 = lo + (int64_t)((uint64_t)n * (p + 1) / kQSplit);
+}
+
+__global__ __launch_bounds__(kQThreads) void queue_sum_kernel(
     const int64_t* __restrict__ qoff, uint64_t Q, const uint32_t* __restrict__ unc_here,
-    const uint32_t* __restrict__ alt, const int64_t* __restrict__ base_work, uint32_t S, TtftK tk,
-    int64_t* __restrict__ T, uint32_t* __restrict__ owner, int64_t* __restrict__ L0,
-    uint8_t* __restrict__ over, uint32_t* __restrict__ status)
+    int64_t* __restrict__ slice_sum, uint32_t* __restrict__ status)
 {
     __shared__ int64_t sh[kQThreads / kWave];
-    const uint32_t i = blockIdx.x;
-    const int64_t lo = qoff[i], hi = qoff[i + 1];
-    if (lo < 0 || hi < lo || hi > (int64_t)Q) {
+    const uint32_t i = blockIdx.x / kQSplit, p = blockIdx.x % kQSplit;
+    if (!queue_ok(qoff, i, Q)) {
         if (threadIdx.x == 0) {
             atomicOr(status, kErrInval);
-            L0[i] = base_work[i];
-            over[i] = 0;
+            slice_sum[blockIdx.x] = 0;
         }
         return;
     }
-    const uint64_t n = (uint64_t)(hi - lo), per = (n + kQThreads - 1) / kQThreads;
-    const int64_t b0 = lo + (int64_t)std::min<uint64_t>(n, threadIdx.x * per);
-    const int64_t b1 = lo + (int64_t)std::min<uint64_t>(n, (threadIdx.x + 1) * per);
+    int64_t b0, b1;
+    slice_of(qoff, i, p, b0, b1);
     int64_t sum = 0;
-    for (int64_t b = b0; b < b1; b += kWalkBatch) {
+    for (int64_t b = b0 + threadIdx.x * kWalkBatch; b < b1; b += kQThreads * kWalkBatch) {
         uint32_t ub[kWalkBatch];
 #pragma unroll
         for (int r = 0; r < kWalkBatch; r++)
@@ -137,20 +149,58 @@ __global__ __launch_bounds__(kQThreads) void queue_kernel(
             sum += ub[r];
     }
     int64_t tot;
-    int64_t run = base_work[i] + block_excl_scan_i64<kQThreads>(sum, sh, tot);
+    (void)block_excl_scan_i64<kQThreads>(sum, sh, tot);
+    if (threadIdx.x == 0)
+        slice_sum[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(kQThreads) void queue_ttft_kernel(
+    const int64_t* __restrict__ qoff, uint64_t Q, const uint32_t* __restrict__ unc_here,
+    const uint32_t* __restrict__ alt, const int64_t* __restrict__ base_work,
+    const int64_t* __restrict__ slice_sum, uint32_t S, TtftK tk, int64_t* __restrict__ T,
+    uint32_t* __restrict__ owner, int64_t* __restrict__ slice_max, uint32_t* __restrict__ status)
+{
+    __shared__ int64_t sh[kQThreads / kWave];
+    const uint32_t i = blockIdx.x / kQSplit, p = blockIdx.x % kQSplit;
+    if (!queue_ok(qoff, i, Q)) {
+        if (threadIdx.x == 0)
+            slice_max[blockIdx.x] = INT64_MIN;
+        return;
+    }
+    int64_t b0, b1;
+    slice_of(qoff, i, p, b0, b1);
+    int64_t run0 = base_work[i];
+    for (uint32_t k = 0; k < p; k++)
+        run0 += slice_sum[i * kQSplit + k];
+    // contiguous runs of the slice per thread, placed by one workgroup scan
+    const uint64_t n = (uint64_t)(b1 - b0), per = (n + kQThreads - 1) / kQThreads;
+    const int64_t r0 = b0 + (int64_t)std::min<uint64_t>(n, threadIdx.x * per);
+    const int64_t r1 = b0 + (int64_t)std::min<uint64_t>(n, (threadIdx.x + 1) * per);
+    int64_t sum = 0;
+    for (int64_t b = r0; b < r1; b += kWalkBatch) {
+        uint32_t ub[kWalkBatch];
+#pragma unroll
+        for (int r = 0; r < kWalkBatch; r++)
+            ub[r] = b + r < r1 ? unc_here[b + r] : 0u;
+#pragma unroll
+        for (int r = 0; r < kWalkBatch; r++)
+            sum += ub[r];
+    }
+    int64_t tot;
+    int64_t run = run0 + block_excl_scan_i64<kQThreads>(sum, sh, tot);
     int64_t mx = INT64_MIN;
     bool bad = false;
-    for (int64_t b = b0; b < b1; b += kWalkBatch) {
+    for (int64_t b = r0; b < r1; b += kWalkBatch) {
         uint32_t ub[kWalkBatch], ab[kWalkBatch];
 #pragma unroll
         for (int r = 0; r < kWalkBatch; r++) {
-            const bool in = b + r < b1;
+            const bool in = b + r < r1;
             ub[r] = in ? unc_here[b + r] : 0u;
             ab[r] = in ? alt[b + r] : 0u;
         }
 #pragma unroll
         for (int r = 0; r < kWalkBatch; r++) {
-            if (b + r < b1) {
+            if (b + r < r1) {
                 const int64_t t = tk((int64_t)ub[r], run);
                 T[b + r] = t;
                 owner[b + r] = i;
@@ -163,10 +213,28 @@ __global__ __launch_bounds__(kQThreads) void queue_kernel(
     if (bad)
         atomicOr(status, kErrInval);
     mx = block_max_i64<kQThreads>(mx, sh);
-    if (threadIdx.x == 0) {
-        L0[i] = base_work[i] + tot;
-        over[i] = (hi > lo && mx > tk.slo) ? 1 : 0;
-    }
+    if (threadIdx.x == 0)
+        slice_max[blockIdx.x] = mx;
+}
+
+__global__ void queue_over_kernel(const int64_t* __restrict__ qoff, uint64_t Q,
+                                  const int64_t* __restrict__ base_work,
+                                  const int64_t* __restrict__ slice_sum,
+                                  const int64_t* __restrict__ slice_max, uint32_t S, int64_t slo,
+                                  int64_t* __restrict__ L0, uint8_t* __restrict__ over)
+{
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= S)
+        return;
+    int64_t L = base_work[i], mx = INT64_MIN;
+    const bool ok = queue_ok(qoff, i, Q);
+    if (ok)
+        for (uint32_t k = 0; k < kQSplit; k++) {
+            L += slice_sum[i * kQSplit + k];
+            mx = std::max(mx, slice_max[i * kQSplit + k]);
+        }
+    L0[i] = L;
+    over[i] = (ok && qoff[i + 1] > qoff[i] && mx > slo) ? 1 : 0;
 }
 
 // Per record: benefit and eligibility; the largest eligible benefit goes to
@@ -867,7 +935,10 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     hipStream_t st = c->stream;
     hipError_t e;
     // per-instance arrays
-    uint8_t* pi = static_cast<uint8_t*>(scratch_get(c, 3, 64 * (S + 64) + 4096, &e));
+    // per instance slot: L0, base_of 8 B; over 1 B; rank, src, start, sseg,
+    // kstar_of 4 B; slice sums and maxima 2 x 8 x kQSplit B -- 293 B, and 12
+    // carves of at most 256 B padding
+    uint8_t* pi = static_cast<uint8_t*>(scratch_get(c, 3, 320 * ((uint64_t)S + 64) + 8192, &e));
     if (!pi)
         return e;
     int64_t* L0 = carve<int64_t>(pi, S);
@@ -878,6 +949,8 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     uint32_t* sseg = carve<uint32_t>(pi, S + 1);
     uint32_t* kstar_of = carve<uint32_t>(pi, S);
     uint64_t* base_of = carve<uint64_t>(pi, S);
+    int64_t* slice_sum = carve<int64_t>(pi, (uint64_t)S * kQSplit);
+    int64_t* slice_max = carve<int64_t>(pi, (uint64_t)S * kQSplit);
     uint32_t* nsrc = carve<uint32_t>(pi, 1);
     uint64_t* ctot = carve<uint64_t>(pi, 2);  // candidate count, largest eligible benefit
     // per-record arrays
@@ -895,8 +968,13 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     zero_u32_kernel<<<1, 64, 0, st>>>(nsrc, 1);
     zero_u32_kernel<<<1, 64, 0, st>>>(reinterpret_cast<uint32_t*>(ctot), 4);
     fill_u32_kernel<<<grid_for(Qa, 256), 256, 0, st>>>(owner, Qa, 0xFFFFFFFFu);
-    queue_kernel<<<S, kQThreads, 0, st>>>(q->qoff, Q, q->unc_here, q->alt, q->base_work, S, tk, T,
-                                          owner, L0, over, c->d_status);
+    queue_sum_kernel<<<S * kQSplit, kQThreads, 0, st>>>(q->qoff, Q, q->unc_here, slice_sum,
+                                                        c->d_status);
+    queue_ttft_kernel<<<S * kQSplit, kQThreads, 0, st>>>(q->qoff, Q, q->unc_here, q->alt,
+                                                         q->base_work, slice_sum, S, tk, T, owner,
+                                                         slice_max, c->d_status);
+    queue_over_kernel<<<(S + 255) / 256, 256, 0, st>>>(q->qoff, Q, q->base_work, slice_sum,
+                                                        slice_max, S, tk.slo, L0, over);
     if (Q)
         // grid-stride: 256 workgroups, one atomic maximum each
         benefit_kernel<<<grid_for(Q, 256, 256), 256, 0, st>>>(Q, T, owner, q->alt, q->unc_alt, L0,

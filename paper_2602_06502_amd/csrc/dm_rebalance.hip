@@ -577,11 +577,32 @@ __device__ __noinline__ uint32_t regs_bisect(const uint32_t* __restrict__ unc_he
     const int64_t b0 = qlo + (int64_t)std::min<uint64_t>(Lq, tid * pq);
     const int64_t b1 = qlo + (int64_t)std::min<uint64_t>(Lq, (tid + 1) * pq);
     uint32_t u[kQueueRegs], key[kQueueRegs];
+    // 16-byte loads where the run is aligned: a quarter of the address
+    // requests of scalar loads, whose lanes each touch another cache line
+    const bool vec = (b0 & 3) == 0 && (reinterpret_cast<uintptr_t>(unc_here) & 15) == 0 &&
+                     (reinterpret_cast<uintptr_t>(qkey) & 15) == 0;
 #pragma unroll
-    for (int r = 0; r < kQueueRegs; r++) {
-        const bool in = b0 + r < b1;
-        u[r] = in ? unc_here[b0 + r] : 0u;
-        key[r] = in ? qkey[b0 + r] : 0u;
+    for (int k = 0; k < kQueueRegs / 4; k++) {
+        const int64_t q = b0 + 4 * k;
+        if (vec && q + 3 < b1) {
+            const uint4 x = *reinterpret_cast<const uint4*>(unc_here + q);
+            const uint4 y = *reinterpret_cast<const uint4*>(qkey + q);
+            u[4 * k] = x.x;
+            u[4 * k + 1] = x.y;
+            u[4 * k + 2] = x.z;
+            u[4 * k + 3] = x.w;
+            key[4 * k] = y.x;
+            key[4 * k + 1] = y.y;
+            key[4 * k + 2] = y.z;
+            key[4 * k + 3] = y.w;
+        } else {
+#pragma unroll
+            for (int r = 0; r < 4; r++) {
+                const bool in = q + r < b1;
+                u[4 * k + r] = in ? unc_here[q + r] : 0u;
+                key[4 * k + r] = in ? qkey[q + r] : 0u;
+            }
+        }
     }
     uint32_t lo = 1, hi = A;
     if (regs_violate(u, key, w0, hi, tk, sh))

@@ -117,13 +117,18 @@ typedef struct {
                           /*      bit1 both candidates' TTFT exceed the SLO (the    */
                           /*      rebalance trigger of Sec. A.1.2), bit2 equal      */
                           /*      match, bit3 second candidate adjusted             */
-    uint64_t* block_keys; /* NULL, or [sum of full blocks] every full block's f1    */
-                          /*      key, request-major (the keys a KV save inserts)   */
+    uint64_t* block_keys; /* NULL, or [sum over r of floor(len_r / B)] every full    */
+                          /*      block's f1 key, request-major (the keys a KV     */
+                          /*      save inserts)                                    */
 } dm_route_out;
 
-/* Route a batch of n requests (Sec. 3.2, Sec. A.1.1).  Request r's prompt is
- * tokens[offsets[r] .. offsets[r+1]) (int32 token ids; offsets int64, n + 1
- * entries, non-decreasing, offsets[0] >= 0).  For every request:
+/* Route a batch of n requests (Sec. 3.2, Sec. A.1.1).  tokens holds n_tokens
+ * int32 token ids; request r's prompt is tokens[offsets[r] .. offsets[r+1])
+ * (offsets int64, n + 1 entries, 0 <= offsets[0] <= ... <= offsets[n] <=
+ * n_tokens).  Offsets are checked on the device: if they break that rule,
+ * no token outside [0, n_tokens) and no block key past the batch's block
+ * count is touched, every request is treated as having no full block (ring
+ * keys 0, match 0), and dm_sync returns DM_EINVAL.  For every request:
  *   1. chained f1/f2 block keys; ring keys x_s = key of the first
  *      min(K, full blocks) blocks (no full block: the empty-prefix key);
  *   2. c1 = owner of x1 on ring 1, c2 = owner of x2 on ring 2; if they
@@ -138,12 +143,15 @@ typedef struct {
  *      cached blocks unless its TTFT exceeds the SLO, then the other one if
  *      strictly less loaded.
  * loads: device int64 [max_slots], read and updated in place.  Requires
- * rings (DM_ESTATE otherwise).  n = 0 is a no-op; n must be at most
+ * rings (DM_ESTATE otherwise).  The call does not wait for the device: its
+ * work arrays are sized from n and n_tokens (they grow, synchronising once,
+ * only when a batch needs more than any before it).  n = 0 is a no-op; n must be at most
  * 1,908,874,240 (DM_EINVAL): the selection indexes its per-request slots in
  * 32 bits.  Match lengths are 32-bit: a request with 2^32 or more full
  * blocks sets the device status word (DM_EINVAL from dm_sync). */
-dm_status dm_route_batch(dm_ctx* ctx, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                         int64_t* loads, const dm_route_out* out);
+dm_status dm_route_batch(dm_ctx* ctx, const int32_t* tokens, uint64_t n_tokens,
+                         const int64_t* offsets, uint64_t n, int64_t* loads,
+                         const dm_route_out* out);
 
 /* Pending-request queues, CSR over instance slots (device arrays).  Queue i
  * is records [qoff[i], qoff[i+1]) head first; record q costs unc_here[q]

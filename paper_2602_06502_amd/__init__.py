@@ -80,7 +80,7 @@ def load_library(path: str = LIB_PATH):
         "dm_index_erase": (i32, [P, u32, P, u64]),
         "dm_index_clear": (i32, [P, u32]),
         "dm_index_size": (i32, [P, u32, P]),
-        "dm_route_batch": (i32, [P, P, P, u64, P, P]),
+        "dm_route_batch": (i32, [P, P, u64, P, u64, P, P]),
         "dm_rebalance": (i32, [P, P, P, P, u64]),
         "dm_scale": (i32, [P, P, u32, P, u32, P, u64, P, P, P, P]),
         "dm_set_timing": (i32, [P, i32]),
@@ -225,15 +225,13 @@ class DualMap:
         return int(n.value)
 
     def route_into(self, tokens, offsets, loads, out: Dict) -> None:
-        """dm_route_batch into preallocated outputs (no allocation)."""
-        t = self.torch
+        """dm_route_batch into preallocated outputs (no allocation of outputs)."""
         n = offsets.numel() - 1
         ro = dm_route_out(_ptr(out["key"]), _ptr(out["cand"]), _ptr(out["match"]),
                           _ptr(out["chosen"]), _ptr(out["ttft"]), _ptr(out["flags"]),
                           _ptr(out.get("block_keys")))
-        self._check(self.lib.dm_route_batch(self._h, _ptr(tokens), _ptr(offsets), n, _ptr(loads),
-                                            C.byref(ro)), "dm_route_batch")
-        del t
+        self._check(self.lib.dm_route_batch(self._h, _ptr(tokens), tokens.numel(), _ptr(offsets),
+                                            n, _ptr(loads), C.byref(ro)), "dm_route_batch")
 
     def alloc_route_out(self, n: int, n_blocks: Optional[int] = None) -> Dict:
         t = self.torch

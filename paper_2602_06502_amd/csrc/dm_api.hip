@@ -26,6 +26,17 @@ dm_status hip_fail(dm_ctx* c, hipError_t e, const char* what)
     return fail(c, DM_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+hipError_t sync_streams(dm_ctx* c)
+{
+    hipError_t e = hipStreamSynchronize(c->stream);
+    if (e == hipSuccess && c->home_stream != c->stream)
+        e = hipStreamSynchronize(c->home_stream);
+    for (hipStream_t s : {c->work_stream, c->sel_stream, c->out_stream})
+        if (e == hipSuccess && s)
+            e = hipStreamSynchronize(s);
+    return e;
+}
+
 void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e)
 {
     Scratch& s = c->scratch[slot];
@@ -36,11 +47,7 @@ void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e)
         return s.p;
     // Work already queued (on any of the context's streams) may still use
     // the old buffer.
-    *e = hipStreamSynchronize(c->stream);
-    for (hipStream_t s : {c->work_stream, c->sel_stream, c->out_stream})
-        if (*e == hipSuccess && s)
-            *e = hipStreamSynchronize(s);
-    if (*e != hipSuccess)
+    if ((*e = sync_streams(c)) != hipSuccess)
         return nullptr;
     size_t nb = std::max(bytes, s.bytes * 2);
     nb = (nb + 4095) & ~size_t(4095);
@@ -62,6 +69,31 @@ hipError_t join_selection(dm_ctx* c)
     if (!c->pipelined || c->batches == 0)
         return hipSuccess;
     return hipStreamWaitEvent(c->stream, c->out_done[(c->batches - 1) & 1], 0);
+}
+
+// Host checks shared by both routing entry points (what = the caller's name).
+dm_status route_args_check(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens,
+                           const int64_t* offsets, uint64_t n, int64_t* loads,
+                           const dm_route_out* out, const char* what)
+{
+    if (c->n_live == 0)
+        return fail(c, DM_ESTATE, std::string(what) + ": rings not built");
+    if (n == 0)
+        return DM_OK;
+    if ((!tokens && n_tokens) || !offsets || !loads || !out || !out->key || !out->cand ||
+        !out->match || !out->chosen || !out->ttft_us || !out->flags)
+        return fail(c, DM_EINVAL, std::string(what) + ": null argument");
+    if (!aligned(tokens) || !aligned(offsets) || !aligned(loads) || !aligned(out->key) ||
+        !aligned(out->cand) || !aligned(out->match) || !aligned(out->chosen) ||
+        !aligned(out->ttft_us) || (out->block_keys && !aligned(out->block_keys)))
+        return fail(c, DM_EINVAL, std::string(what) + ": misaligned pointer");
+    // the selection's slot indices are 32-bit: 36 windows of 64 lanes per
+    // 1024 requests must stay below 2^32
+    if (n > kMaxRouteBatch)
+        return fail(c, DM_EINVAL, std::string(what) + ": batch too large (n <= 1,908,874,240)");
+    if (n_tokens > (1ull << 62))
+        return fail(c, DM_EINVAL, std::string(what) + ": token count too large");
+    return DM_OK;
 }
 
 }  // namespace dm
@@ -130,11 +162,6 @@ void make_params(HashParams& hp, const dm_config& cfg)
     }
 }
 
-template <typename T>
-bool aligned(const T* p)
-{
-    return (reinterpret_cast<uintptr_t>(p) % alignof(T)) == 0;
-}
 
 hipError_t upload_live(dm_ctx* c)
 {
@@ -188,6 +215,7 @@ dm_status dm_create(const dm_config* cfg, void* hip_stream, dm_ctx** out)
         return DM_ENOMEM;
     c->cfg = k;
     c->stream = static_cast<hipStream_t>(hip_stream);
+    c->home_stream = c->stream;
     c->shift_div = log2u((uint64_t)k.queue_div);
     c->live.assign(k.max_slots, 0);
     make_params(c->hp, k);
@@ -367,28 +395,18 @@ dm_status dm_index_size(dm_ctx* c, uint32_t id, uint64_t* n_host)
     return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_index_size");
 }
 
-dm_status dm_route_batch(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                         int64_t* loads, const dm_route_out* out)
+dm_status dm_route_batch(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens,
+                         const int64_t* offsets, uint64_t n, int64_t* loads,
+                         const dm_route_out* out)
 {
     if (!c)
         return DM_EINVAL;
-    if (c->n_live == 0)
-        return fail(c, DM_ESTATE, "dm_route_batch: rings not built");
-    if (n == 0)
-        return DM_OK;
-    if (!tokens || !offsets || !loads || !out || !out->key || !out->cand || !out->match ||
-        !out->chosen || !out->ttft_us || !out->flags)
-        return fail(c, DM_EINVAL, "dm_route_batch: null argument");
-    if (!aligned(tokens) || !aligned(offsets) || !aligned(loads) || !aligned(out->key) ||
-        !aligned(out->cand) || !aligned(out->match) || !aligned(out->chosen) ||
-        !aligned(out->ttft_us) || (out->block_keys && !aligned(out->block_keys)))
-        return fail(c, DM_EINVAL, "dm_route_batch: misaligned pointer");
-    // the selection's slot indices are 32-bit: 36 windows of 64 lanes per
-    // 1024 requests must stay below 2^32
-    if (n > kMaxRouteBatch)
-        return fail(c, DM_EINVAL, "dm_route_batch: batch too large (n <= 1,908,874,240)");
+    if (dm_status st = route_args_check(c, tokens, n_tokens, offsets, n, loads, out,
+                                        "dm_route_batch");
+        st != DM_OK || n == 0)
+        return st;
     DeviceGuard g(c->device);
-    hipError_t e = route(c, tokens, offsets, n, loads, out);
+    hipError_t e = route(c, tokens, n_tokens, offsets, n, loads, out);
     return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_route_batch");
 }
 

@@ -59,6 +59,7 @@ struct HashArgs {
     const HashParams* hp;
     uint32_t key_blocks;
     const uint64_t* bstart;  // [n+1]
+    const uint32_t* bad;     // offsets break the batch's rule (set by the block-start scan)
     uint64_t* hkeys;         // [bstart[n]] f1 block keys
     uint64_t* key_out;       // [2n]
     uint32_t* status;
@@ -74,6 +75,9 @@ __global__ __launch_bounds__(kHashThreads) void hash_kernel(HashArgs a)
     const uint64_t seed1 = hp->seed[0], seed2 = hp->seed[1];
     const uint64_t H01 = hp->H0[0], H02 = hp->H0[1];
     const uint64_t q1 = hp->qpow[0][lane], p1 = hp->ppow[0][lane], q2 = hp->qpow[1][lane];
+    // Malformed offsets (reported by the block-start scan): ring keys 0, no
+    // block key.  No store precedes the parameter loads, so they stay scalar.
+    const bool bad = *a.bad != 0;
     uint32_t k1[B], k2[B];
 #pragma unroll
     for (int j = 0; j < B; j++) {
@@ -99,9 +103,8 @@ __global__ __launch_bounds__(kHashThreads) void hash_kernel(HashArgs a)
             nbs = a.bstart[rn];
         }
         const int64_t len = o1 - o0;
-        if (o0 < 0 || len < 0) {
+        if (bad) {
             if (lane == 0) {
-                atomicOr(a.status, kErrInval);
                 a.key_out[r] = 0;
                 a.key_out[a.n + r] = 0;
             }
@@ -157,11 +160,11 @@ void launch_hash(const HashArgs& a, uint32_t grid, hipStream_t s)
 }  // namespace
 
 hipError_t hash_blocks(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                       const uint64_t* bstart, uint64_t* hkeys, uint64_t* key_out, uint64_t r0,
-                       uint64_t r1)
+                       const uint64_t* bstart, const uint32_t* bad, uint64_t* hkeys,
+                       uint64_t* key_out, uint64_t r0, uint64_t r1)
 {
-    HashArgs ha{tokens, offsets, n, r0, r1, c->d_hp, c->cfg.key_blocks, bstart, hkeys, key_out,
-                c->d_status};
+    HashArgs ha{tokens, offsets, n,     r0,      r1,        c->d_hp,
+                c->cfg.key_blocks, bstart, bad, hkeys, key_out, c->d_status};
     const uint32_t grid = grid_for(r1 > r0 ? r1 - r0 : 0, kHashThreads / kWave, kHashBlocks);
     switch (c->cfg.block_size) {
         case 4: launch_hash<4>(ha, grid, c->stream); break;

@@ -4,12 +4,22 @@
 // key's home bucket.  Slot 0 = empty, 1 = erased; stored keys are >= 2.
 // An insert takes the first empty slot of the probe sequence, so an empty
 // slot seen during a lookup proves the key absent.
+//
+// Capacity: a table never holds more than 2^(k-1) occupied slots.  A thread
+// reserves a unit of the occupied count before it claims an empty slot and
+// gives it back if the claim loses (another thread stored the same or a
+// different key there).  A reservation refused at the limit is not final,
+// since reservations still in flight may be given back: the key goes to an
+// overflow list, and once the insert kernel has finished a single wave
+// settles the list in order (present already, stored while room is left,
+// else dropped with DM_EFULL).  So a batch that fits is stored whole, and a
+// batch that does not fills the table to exactly the limit.
 #include "dm_internal.h"
 
 namespace dm {
 namespace {
 
-constexpr int kPurgeSlot = 8;  // table rebuild work area
+constexpr int kPurgeSlot = kSlotPurge;  // table rebuild work area
 
 struct TableRef {
     uint64_t* slots;
@@ -19,8 +29,17 @@ struct TableRef {
     uint64_t limit;      // maximum occupied slots
 };
 
-// Insert of one canonical key (>= 2); set semantics.
-__device__ __forceinline__ void insert_one(const TableRef& t, uint64_t k, uint32_t* status)
+// Overflow list: a count and the keys (room for every key of the batch).
+struct Overflow {
+    unsigned long long* count;
+    uint64_t* keys;
+};
+
+// Insert of one canonical key (>= 2); set semantics.  With an overflow list,
+// a key whose reservation is refused at the limit is appended to it;
+// without one the key is dropped with kErrFull.
+__device__ __forceinline__ void insert_one(const TableRef& t, uint64_t k, uint32_t* status,
+                                           const Overflow* ovf)
 {
     const uint64_t nbk = 1ull << (t.log2slots - 3);
     uint64_t b = home_bucket(k, t.log2slots);
@@ -32,21 +51,27 @@ __device__ __forceinline__ void insert_one(const TableRef& t, uint64_t k, uint32
             if (v == k) {
                 done = true;
             } else if (v == kEmpty) {
-                if (__hip_atomic_load(t.occupied, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >=
-                    t.limit) {
-                    atomicOr(status, kErrFull);
+                const unsigned long long held =
+                    atomicAdd((unsigned long long*)t.occupied, 1ull);
+                if (held >= t.limit) {
+                    atomicAdd((unsigned long long*)t.occupied, ~0ull);  // give back
+                    if (ovf) {
+                        const unsigned long long at = atomicAdd(ovf->count, 1ull);
+                        ovf->keys[at] = k;
+                    } else {
+                        atomicOr(status, kErrFull);
+                    }
                     return;
                 }
                 const unsigned long long prev = atomicCAS(
                     (unsigned long long*)slot, (unsigned long long)kEmpty, (unsigned long long)k);
                 if (prev == kEmpty) {
-                    atomicAdd((unsigned long long*)t.occupied, 1ull);
                     atomicAdd((unsigned long long*)t.live, 1ull);
                     done = true;
-                } else if (prev == k) {
-                    done = true;
+                } else {
+                    atomicAdd((unsigned long long*)t.occupied, ~0ull);  // claim lost
+                    done = prev == k;  // else another key took the slot: keep walking
                 }
-                // else another key took the slot: keep walking
             }
         }
     }
@@ -55,11 +80,60 @@ __device__ __forceinline__ void insert_one(const TableRef& t, uint64_t k, uint32
 }
 
 __global__ void insert_kernel(TableRef t, const uint64_t* __restrict__ keys, uint64_t n,
-                              uint32_t* __restrict__ status)
+                              uint32_t* __restrict__ status, Overflow ovf)
 {
     for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < n;
          i += (uint64_t)gridDim.x * blockDim.x)
-        insert_one(t, canon_key(keys[i]), status);
+        insert_one(t, canon_key(keys[i]), status, &ovf);
+}
+
+// Is canonical key k stored?  Walks k's probe sequence to its first empty slot.
+__device__ bool contains(const TableRef& t, uint64_t k)
+{
+    const uint64_t nbk = 1ull << (t.log2slots - 3);
+    uint64_t b = home_bucket(k, t.log2slots);
+    for (uint64_t step = 0; step < nbk; step++, b = (b + 1) & (nbk - 1))
+        for (uint32_t s = 0; s < kBucket; s++) {
+            const uint64_t v = __hip_atomic_load(t.slots + b * kBucket + s, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+            if (v == k)
+                return true;
+            if (v == kEmpty)
+                return false;
+        }
+    return false;
+}
+
+// The overflow list in list order, by one wave after the insert kernel:
+// every lane looks up its key, then the absent ones are stored one lane
+// at a time while the table has room; the rest are dropped with kErrFull.
+// Nothing else writes the table meanwhile, so the counts are exact here.
+__global__ void overflow_kernel(TableRef t, Overflow ovf, uint32_t* __restrict__ status)
+{
+    const int lane = lane_id();
+    const uint64_t m = *ovf.count;
+    for (uint64_t base = 0; base < m; base += kWave) {
+        const uint64_t i = base + lane;
+        const uint64_t k = i < m ? ovf.keys[i] : 0;
+        bool need = i < m && !contains(t, k);
+        if (!__any(need))
+            continue;
+        for (int j = 0; j < kWave; j++) {
+            // lanes in order: an earlier lane may have stored the same key
+            if (lane == j && need) {
+                if (contains(t, k)) {
+                    need = false;
+                } else if (__hip_atomic_load(t.occupied, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT) >= t.limit) {
+                    atomicOr(status, kErrFull);
+                } else {
+                    insert_one(t, k, status, nullptr);
+                }
+            }
+            // the next lane sees this lane's store and counts
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "agent");
+        }
+    }
 }
 
 // Erased slots are never reused by inserts (an empty slot must keep proving
@@ -72,7 +146,8 @@ __global__ void purge_plan_kernel(TableRef t, uint64_t n, unsigned long long* pl
 {
     const uint64_t occ = *t.occupied, live = *t.live;
     plan[0] = (occ + n > t.limit && occ > live) ? 1ull : 0ull;
-    plan[1] = 0;
+    plan[1] = 0;  // live keys gathered
+    plan[2] = 0;  // overflow list length
 }
 
 __global__ void purge_gather_kernel(TableRef t, const unsigned long long* plan,
@@ -92,8 +167,10 @@ __global__ void purge_gather_kernel(TableRef t, const unsigned long long* plan,
         if (m && lane_id() == 0)
             first = atomicAdd(cnt, (unsigned long long)__popcll(m));
         first = readlane_u64(first, 0);
-        if (keep)
-            out[first + __popcll(m & lt)] = v;
+        // live <= occupied <= limit, the buffer's length; bounded all the same
+        const uint64_t at = first + __popcll(m & lt);
+        if (keep && at < t.limit)
+            out[at] = v;
     }
 }
 
@@ -116,10 +193,10 @@ __global__ void purge_insert_kernel(TableRef t, const unsigned long long* plan,
 {
     if (!plan[0])
         return;
-    const uint64_t n = plan[1];
+    const uint64_t n = plan[1] < t.limit ? plan[1] : t.limit;
     for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < n;
          i += (uint64_t)gridDim.x * blockDim.x)
-        insert_one(t, keys[i], status);
+        insert_one(t, keys[i], status, nullptr);
 }
 
 __global__ void erase_kernel(TableRef t, const uint64_t* __restrict__ keys, uint64_t n)
@@ -174,19 +251,22 @@ hipError_t index_insert(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n
 {
     const TableRef t = table_of(c, id);
     hipError_t e = hipSuccess;
-    // rebuild work area: plan word, gather counter, then up to `limit` live keys
+    // work area: plan word, gather count, overflow count, then up to `limit`
+    // gathered live keys, then up to n overflow keys
     unsigned long long* w = static_cast<unsigned long long*>(
-        scratch_get(c, kPurgeSlot, (t.limit + 2) * sizeof(uint64_t), &e));
+        scratch_get(c, kPurgeSlot, (t.limit + n + 3) * sizeof(uint64_t), &e));
     if (!w)
         return e;
+    uint64_t* gathered = reinterpret_cast<uint64_t*>(w + 3);
+    const Overflow ovf{w + 2, gathered + t.limit};
     const uint64_t nslots = 1ull << t.log2slots;
     purge_plan_kernel<<<1, 1, 0, c->stream>>>(t, n, w);
-    purge_gather_kernel<<<grid_for(nslots, 256, 4096), 256, 0, c->stream>>>(
-        t, w, w + 1, reinterpret_cast<uint64_t*>(w + 2));
+    purge_gather_kernel<<<grid_for(nslots, 256, 4096), 256, 0, c->stream>>>(t, w, w + 1, gathered);
     purge_clear_kernel<<<grid_for(nslots, 256, 4096), 256, 0, c->stream>>>(t, w);
-    purge_insert_kernel<<<grid_for(t.limit, 256, 4096), 256, 0, c->stream>>>(
-        t, w, reinterpret_cast<const uint64_t*>(w + 2), c->d_status);
-    insert_kernel<<<grid_for(n, 256), 256, 0, c->stream>>>(table_of(c, id), keys, n, c->d_status);
+    purge_insert_kernel<<<grid_for(t.limit, 256, 4096), 256, 0, c->stream>>>(t, w, gathered,
+                                                                            c->d_status);
+    insert_kernel<<<grid_for(n, 256), 256, 0, c->stream>>>(t, keys, n, c->d_status, ovf);
+    overflow_kernel<<<1, kWave, 0, c->stream>>>(t, ovf, c->d_status);
     return hipGetLastError();
 }
 

@@ -13,7 +13,12 @@
 namespace dm {
 
 constexpr int kWave = 64;
-constexpr int kScratchSlots = 9;  // context work buffers, one per use (each file names its slots)
+constexpr int kScratchSlots = 9;  // context work buffers, one per use
+// Scratch slots.  Routing uses starts, probe, select, keys, sort and scan;
+// a rebalancing pass reuses probe, rebalance and select (it runs after the
+// batches before it have finished).
+constexpr int kSlotStarts = 0, kSlotProbe = 1, kSlotRebalance = 2, kSlotSelect = 3, kSlotKeys = 4,
+              kSlotRing = 5, kSlotSort = 6, kSlotScan = 7, kSlotPurge = 8;
 constexpr uint32_t kMaxSlots = 4096;
 constexpr uint64_t kEmpty = 0;      // index slot never used
 constexpr uint64_t kTomb = 1;       // index slot erased
@@ -71,7 +76,8 @@ struct Scratch {
 
 struct dm_ctx {
     dm_config cfg;
-    hipStream_t stream = nullptr;
+    hipStream_t stream = nullptr;       // launches go here (pipelined routing swaps it)
+    hipStream_t home_stream = nullptr;  // the stream given to dm_create
     int device = 0;
     int n_cu = 0;           // compute units of the device
     uint32_t probe_grid = 0;  // resident workgroups of the probe kernel (set on first use)
@@ -98,6 +104,10 @@ struct dm_ctx {
 
     dm::Scratch scratch[dm::kScratchSlots];
     uint32_t shift_div = 0;        // log2(queue_div)
+    // Distance between the two selection work-array sets (by batch parity).
+    // It only grows, and only once every stream is idle, so a set in use by
+    // a batch in flight never overlaps the other set.
+    size_t sel_stride = 0;
 
     // stage timing of dm_route_batch: one set of 5 events per batch, in a
     // ring (recorded only when enabled)
@@ -129,8 +139,22 @@ namespace dm {
 dm_status fail(dm_ctx* c, dm_status s, const std::string& msg);
 dm_status hip_fail(dm_ctx* c, hipError_t e, const char* what);
 void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e);
+// Wait for the context's stream and, with pipelining, its other streams.
+hipError_t sync_streams(dm_ctx* c);
 
 inline RingView view(const Ring& r) { return RingView{r.pos, r.id, r.dir, r.len, r.dbits}; }
+
+template <typename T>
+inline bool aligned(const T* p)
+{
+    return (reinterpret_cast<uintptr_t>(p) % alignof(T)) == 0;
+}
+
+// Host checks of dm_route_batch's arguments (what = the calling entry
+// point's name, for the message).
+dm_status route_args_check(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens,
+                           const int64_t* offsets, uint64_t n, int64_t* loads,
+                           const dm_route_out* out, const char* what);
 
 // Grid of a grid-stride loop over n items, at least one block, at most cap.
 inline uint32_t grid_for(uint64_t n, int threads, uint32_t cap = 65536)
@@ -144,10 +168,22 @@ inline uint32_t grid_for(uint64_t n, int threads, uint32_t cap = 65536)
 // Launchers (one per kernel family), all asynchronous on c->stream.
 // ---------------------------------------------------------------------------
 
+// Scratch bytes of each route stage for a batch of n requests (the
+// launchers request exactly these, so a plan made from them up front holds).
+uint64_t scan_scratch_bytes(uint64_t n);
+uint64_t sort_scratch_bytes(uint64_t n);
+uint64_t sort_scan_len(uint64_t n);  // length of the sort's digit-count scans
+uint64_t probe_scratch_bytes(uint64_t n);
+uint64_t select_scratch_bytes(uint64_t n);
+
 // dm_scan.hip: exclusive prefix sums.
 hipError_t exclusive_scan_u64(dm_ctx* c, const uint64_t* in, uint64_t n, uint64_t* out,
                               uint64_t* total_out);
-hipError_t block_starts(dm_ctx* c, const int64_t* offsets, uint64_t n, uint64_t* starts);
+// block_starts also checks the offsets (0 <= offsets[0] <= ... <= offsets[n]
+// <= n_tokens) and sets *bad (zeroed beforehand) when they break that rule;
+// such requests count no full block.
+hipError_t block_starts(dm_ctx* c, const int64_t* offsets, uint64_t n, uint64_t n_tokens,
+                        uint64_t* starts, uint32_t* bad);
 
 // dm_sort.hip: stable LSD radix sort of (u64 key, u32 value) pairs on the
 // low `bits` bits of the key (bits multiple of 8).  Sorted data ends in
@@ -168,17 +204,18 @@ hipError_t index_clear(dm_ctx* c, uint32_t id);
 
 // dm_hash.hip: block keys of every full block (hkeys at bstart[r]) and the
 // two ring keys of every request (key_out[r], key_out[n + r]) for the
-// requests r in [r0, r1) of a batch of n.
+// requests r in [r0, r1) of a batch of n; with *bad set, ring keys 0 and no
+// block key.
 hipError_t hash_blocks(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                       const uint64_t* bstart, uint64_t* hkeys, uint64_t* key_out, uint64_t r0,
-                       uint64_t r1);
+                       const uint64_t* bstart, const uint32_t* bad, uint64_t* hkeys,
+                       uint64_t* key_out, uint64_t r0, uint64_t r1);
 
 // dm_probe.hip: candidates on the current rings (cand, fix-up flag bit 3)
 // and the longest cached prefix on each (match), for the requests r in
-// [r0, r1) of a batch of n.
+// [r0, r1) of a batch of n; with *bad set, every match is 0.
 hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64_t* hkeys,
-                        const uint64_t* bstart, uint32_t* cand, uint32_t* match, uint8_t* flags,
-                        uint64_t r0, uint64_t r1);
+                        const uint64_t* bstart, const uint32_t* bad, uint32_t* cand,
+                        uint32_t* match, uint8_t* flags, uint64_t r0, uint64_t r1);
 
 // dm_select.hip: SLO-aware choice in request order; chosen, ttft_us and
 // flags bits 0-2 written, loads updated.  select_prepare packs the batch's
@@ -199,8 +236,8 @@ hipError_t select_batch(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint6
 hipError_t join_selection(dm_ctx* c);
 
 // dm_route.hip: the whole batch, stage by stage.
-hipError_t route(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                 int64_t* loads, const dm_route_out* out);
+hipError_t route(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens, const int64_t* offsets,
+                 uint64_t n, int64_t* loads, const dm_route_out* out);
 
 // dm_rebalance.hip
 hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm_migrations* out,

@@ -19,7 +19,7 @@ namespace dm {
 namespace {
 
 constexpr int kProbeThreads = 256;
-constexpr int kProbeSlot = 1;             // sort keys, request order and sort work arrays
+constexpr int kProbeSlot = kSlotProbe;  // sort keys, request order and sort work arrays
 constexpr int kOrderBits = 16;            // top bits of the first ring key used for ordering
 
 typedef unsigned long long v2u64 __attribute__((ext_vector_type(2), aligned(16)));
@@ -59,6 +59,7 @@ __global__ void order_init_kernel(const uint64_t* __restrict__ key, uint64_t r0,
 struct ProbeArgs {
     const uint64_t* hkeys;
     const uint64_t* bstart;
+    const uint32_t* bad;  // malformed offsets: no block key was written
     uint64_t n;      // batch size (cand and match hold 2n entries)
     uint64_t count;  // requests in order[]
     const uint32_t* cand;
@@ -157,7 +158,8 @@ __global__ __launch_bounds__(kProbeThreads) void probe_kernel(ProbeArgs a)
     unsigned long long* counter = a.next + xcd * kCounterStride;
     const uint32_t nbk = 1u << (a.log2slots - 3);
     const uint32_t ls = a.log2slots;
-    const uint64_t total = a.bstart[a.n];  // block keys in hkeys
+    const bool bad = *a.bad != 0;
+    const uint64_t total = bad ? 0 : a.bstart[a.n];  // block keys in hkeys
     // the claim of the next group is issued before the current one is probed
     uint64_t claim = 0;
     if (lane == 0)
@@ -181,11 +183,11 @@ __global__ __launch_bounds__(kProbeThreads) void probe_kernel(ProbeArgs a)
                 atomicOr(a.status, kErrInval);
                 k0 = ke;
             }
-            len = (uint32_t)(ke - k0);
+            len = bad ? 0u : (uint32_t)(ke - k0);
             tab = a.tables + ((uint64_t)a.cand[out] << ls);
         }
         const uint64_t* hk = a.hkeys + k0;
-        const uint64_t lim = total - k0;  // keys readable from hk
+        const uint64_t lim = total > k0 ? total - k0 : 0;  // keys readable from hk
         bool active = valid && len > 0;
         if (valid && !active)
             a.match[out] = 0;  // no full block
@@ -256,9 +258,19 @@ __global__ __launch_bounds__(kProbeThreads) void probe_kernel(ProbeArgs a)
 
 }  // namespace
 
+// Sort keys and request order (each twice, for the sort's passes), then the
+// per-XCD claim counters.
+uint64_t probe_scratch_bytes(uint64_t m)
+{
+    const size_t kbytes = ((m * sizeof(uint64_t)) + 255) & ~size_t(255);
+    const size_t vbytes = ((m * sizeof(uint32_t)) + 255) & ~size_t(255);
+    const size_t cbytes = kXcds * kCounterStride * sizeof(unsigned long long);
+    return 2 * (kbytes + vbytes) + cbytes + 256;
+}
+
 hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64_t* hkeys,
-                        const uint64_t* bstart, uint32_t* cand, uint32_t* match, uint8_t* flags,
-                        uint64_t r0, uint64_t r1)
+                        const uint64_t* bstart, const uint32_t* bad, uint32_t* cand,
+                        uint32_t* match, uint8_t* flags, uint64_t r0, uint64_t r1)
 {
     hipError_t e = hipSuccess;
     hipStream_t st = c->stream;
@@ -273,9 +285,7 @@ hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64
     // requests ordered by the top bits of their first ring key (stable radix sort)
     const size_t kbytes = ((m * sizeof(uint64_t)) + 255) & ~size_t(255);
     const size_t vbytes = ((m * sizeof(uint32_t)) + 255) & ~size_t(255);
-    const size_t cbytes = kXcds * kCounterStride * sizeof(unsigned long long);
-    uint8_t* w = static_cast<uint8_t*>(
-        scratch_get(c, kProbeSlot, 2 * (kbytes + vbytes) + cbytes + 256, &e));
+    uint8_t* w = static_cast<uint8_t*>(scratch_get(c, kProbeSlot, probe_scratch_bytes(m), &e));
     if (!w)
         return e;
     uint64_t* keys = reinterpret_cast<uint64_t*>(w);
@@ -297,8 +307,8 @@ hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64
         const uint32_t g = (uint32_t)std::max(1, per_cu * std::max(1, c->n_cu));
         c->probe_grid = (g + kXcds - 1) / kXcds * kXcds;
     }
-    ProbeArgs pa{hkeys, bstart, n,           m,    cand, c->d_tables, c->cfg.index_log2_slots,
-                 match, order,  c->d_status, next};
+    ProbeArgs pa{hkeys, bstart, bad,   n,     m,           cand, c->d_tables,
+                 c->cfg.index_log2_slots, match, order, c->d_status, next};
     probe_zero_kernel<<<1, 64, 0, st>>>(next);
     probe_kernel<<<c->probe_grid, kProbeThreads, 0, st>>>(pa);
     return hipGetLastError();

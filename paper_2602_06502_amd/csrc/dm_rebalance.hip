@@ -959,7 +959,8 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     // per instance slot: L0, base_of 8 B; over 1 B; rank, src, start, sseg,
     // kstar_of 4 B; slice sums and maxima 2 x 8 x kQSplit B -- 293 B, and 12
     // carves of at most 256 B padding
-    uint8_t* pi = static_cast<uint8_t*>(scratch_get(c, 3, 320 * ((uint64_t)S + 64) + 8192, &e));
+    uint8_t* pi = static_cast<uint8_t*>(
+        scratch_get(c, kSlotSelect, 320 * ((uint64_t)S + 64) + 8192, &e));
     if (!pi)
         return e;
     int64_t* L0 = carve<int64_t>(pi, S);
@@ -976,7 +977,7 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     uint64_t* ctot = carve<uint64_t>(pi, 2);  // candidate count, largest eligible benefit
     // per-record arrays
     const uint64_t Qa = Q ? Q : 1;
-    uint8_t* pr = static_cast<uint8_t*>(scratch_get(c, 1, Qa * 48 + 8 * 256, &e));
+    uint8_t* pr = static_cast<uint8_t*>(scratch_get(c, kSlotProbe, Qa * 48 + 8 * 256, &e));
     if (!pr)
         return e;
     int64_t* T = carve<int64_t>(pr, Qa);
@@ -1015,7 +1016,7 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     const uint64_t C = hw[0];
     // per-candidate arrays
     const uint64_t Ca = C ? C : 1;
-    uint8_t* pc = static_cast<uint8_t*>(scratch_get(c, 2, Ca * 64 + 16 * 256, &e));
+    uint8_t* pc = static_cast<uint8_t*>(scratch_get(c, kSlotRebalance, Ca * 64 + 16 * 256, &e));
     // per candidate: keys, ktmp 8 B; vals, vtmp, grp, g_alt, g_unc, seg_pos,
     // c_ua, c_uh, arank 4 B; tto 8 B; two bit-word arrays 1/8 B -- 60.25 B
     // and 14 carves of at most 256 B padding each

@@ -6,7 +6,7 @@
 namespace dm {
 namespace {
 
-constexpr int kRingSlot = 5;  // sort work arrays
+constexpr int kRingSlot = kSlotRing;  // sort work arrays
 
 // Virtual node v of live instance k on ring s sits at
 // mix64(((id << 32) | v) xor mix64(seed_s)).

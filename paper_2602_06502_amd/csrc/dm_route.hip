@@ -19,11 +19,23 @@
 namespace dm {
 namespace {
 
-constexpr int kKeySlot = 4;  // block keys when the caller keeps none
+constexpr int kKeySlot = kSlotKeys;  // block keys when the caller keeps none
+
+// Clears the batch's malformed-offsets word (a kernel rather than a memset,
+// so that a captured graph replays it like the rest of the batch).
+__global__ void route_zero_kernel(uint32_t* bad) { *bad = 0; }
 
 }  // namespace
 
 namespace {
+
+uint32_t block_shift_of(const dm_ctx* c)
+{
+    uint32_t k = 0;
+    while ((1u << k) < c->cfg.block_size)
+        k++;
+    return k;
+}
 
 // Routes launches of the helper stages to another stream for one call.
 struct StreamSwap {
@@ -35,8 +47,8 @@ struct StreamSwap {
 
 }  // namespace
 
-hipError_t route(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                 int64_t* loads, const dm_route_out* out)
+hipError_t route(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens, const int64_t* offsets,
+                 uint64_t n, int64_t* loads, const dm_route_out* out)
 {
     hipError_t e = hipSuccess;
     const bool pipe = c->pipelined;
@@ -59,31 +71,34 @@ hipError_t route(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint6
     }
     if (ev && (e = hipEventRecord(ev[0], st)) != hipSuccess)
         return e;
-    uint64_t* bstart = static_cast<uint64_t*>(scratch_get(c, 0, (n + 1) * sizeof(uint64_t), &e));
+    // block starts [n + 1], then the malformed-offsets word
+    uint64_t* bstart =
+        static_cast<uint64_t*>(scratch_get(c, kSlotStarts, (n + 2) * sizeof(uint64_t), &e));
     if (!bstart)
         return e;
-    if ((e = block_starts(c, offsets, n, bstart)) != hipSuccess)
+    uint32_t* bad = reinterpret_cast<uint32_t*>(bstart + n + 1);
+    route_zero_kernel<<<1, 1, 0, st>>>(bad);
+    if ((e = block_starts(c, offsets, n, n_tokens, bstart, bad)) != hipSuccess)
         return e;
     uint64_t* hkeys = out->block_keys;
     if (!hkeys) {
-        // block keys go to context scratch sized by the batch's full-block count
-        uint64_t total = 0;
-        if ((e = hipMemcpyAsync(&total, bstart + n, sizeof(uint64_t), hipMemcpyDeviceToHost, st)) !=
-                hipSuccess ||
-            (e = hipStreamSynchronize(st)) != hipSuccess)
-            return e;
-        hkeys = static_cast<uint64_t*>(scratch_get(c, kKeySlot, (total + 1) * sizeof(uint64_t), &e));
+        // Requests that pass the offsets check are disjoint ranges of the
+        // token array, so they hold at most n_tokens / B full blocks: the
+        // scratch is sized without reading the batch's block count back.
+        const uint64_t cap = (n_tokens >> block_shift_of(c)) + 1;
+        hkeys = static_cast<uint64_t*>(scratch_get(c, kKeySlot, cap * sizeof(uint64_t), &e));
         if (!hkeys)
             return e;
     }
     if (ev && (e = hipEventRecord(ev[1], st)) != hipSuccess)
         return e;
-    if ((e = hash_blocks(c, tokens, offsets, n, bstart, hkeys, out->key, 0, n)) != hipSuccess)
+    if ((e = hash_blocks(c, tokens, offsets, n, bstart, bad, hkeys, out->key, 0, n)) !=
+        hipSuccess)
         return e;
     if (ev && (e = hipEventRecord(ev[2], st)) != hipSuccess)
         return e;
-    if ((e = lookup_probe(c, n, out->key, hkeys, bstart, out->cand, out->match, out->flags, 0, n)) !=
-        hipSuccess)
+    if ((e = lookup_probe(c, n, out->key, hkeys, bstart, bad, out->cand, out->match, out->flags, 0,
+                          n)) != hipSuccess)
         return e;
     if (ev && (e = hipEventRecord(ev[3], st)) != hipSuccess)
         return e;

@@ -11,21 +11,34 @@ namespace {
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 4;
 constexpr uint64_t kTile = kScanThreads * kScanItems;
-constexpr int kScanSlot = 7;  // scratch slot of the tile-sum levels
+constexpr int kScanSlot = kSlotScan;  // tile-sum levels
 
 struct ArrayIn {
     const uint64_t* p;
     __device__ uint64_t operator()(uint64_t i) const { return p[i]; }
 };
 
-// Full blocks of request i: floor(max(0, len) / B), B = 2^shift.
+// Full blocks of request i: floor(len / B), B = 2^shift, for a prompt
+// inside [0, n_tokens); a request that breaks 0 <= off[i] <= off[i+1] <=
+// n_tokens counts none and sets *bad and kErrInval in the device status
+// word.  When every request keeps the rule the offsets never decrease, so
+// the prompts are disjoint ranges of the token array and their full blocks
+// add up to at most n_tokens / B.
 struct FullBlocksIn {
     const int64_t* off;
     uint32_t shift;
+    uint64_t n_tokens;
+    uint32_t* bad;
+    uint32_t* status;
     __device__ uint64_t operator()(uint64_t i) const
     {
-        const int64_t len = off[i + 1] - off[i];
-        return len > 0 ? (uint64_t)len >> shift : 0;
+        const int64_t o0 = off[i], o1 = off[i + 1];
+        if (o0 < 0 || o1 < o0 || (uint64_t)o1 > n_tokens) {
+            atomicOr(bad, 1u);
+            atomicOr(status, kErrInval);
+            return 0;
+        }
+        return (uint64_t)(o1 - o0) >> shift;
     }
 };
 
@@ -115,7 +128,7 @@ hipError_t scan_impl(dm_ctx* c, In in, uint64_t n, uint64_t* out, uint64_t* tota
         need += 2 * ntiles(nd[d]);
     }
     hipError_t e;
-    uint64_t* buf = static_cast<uint64_t*>(scratch_get(c, kScanSlot, need * sizeof(uint64_t), &e));
+    uint64_t* buf = static_cast<uint64_t*>(scratch_get(c, kScanSlot, scan_scratch_bytes(n), &e));
     if (!buf)
         return e;
     auto sums = [&](size_t d) { return buf + at[d]; };
@@ -137,6 +150,16 @@ hipError_t scan_impl(dm_ctx* c, In in, uint64_t n, uint64_t* out, uint64_t* tota
 
 }  // namespace
 
+// Words of tile sums a scan of n items keeps: sums and scanned sums of every
+// level with more than one tile.
+uint64_t scan_scratch_bytes(uint64_t n)
+{
+    uint64_t need = 0;
+    for (uint64_t m = n; ntiles(m) > 1; m = ntiles(m))
+        need += 2 * ntiles(m);
+    return need * sizeof(uint64_t);
+}
+
 hipError_t exclusive_scan_u64(dm_ctx* c, const uint64_t* in, uint64_t n, uint64_t* out,
                               uint64_t* total_out)
 {
@@ -144,12 +167,14 @@ hipError_t exclusive_scan_u64(dm_ctx* c, const uint64_t* in, uint64_t n, uint64_
 }
 
 // starts[r] = full blocks of requests 0..r-1, for r = 0..n (starts[n] = total).
-hipError_t block_starts(dm_ctx* c, const int64_t* offsets, uint64_t n, uint64_t* starts)
+hipError_t block_starts(dm_ctx* c, const int64_t* offsets, uint64_t n, uint64_t n_tokens,
+                        uint64_t* starts, uint32_t* bad)
 {
     uint32_t shift = 0;
     while ((1u << shift) < c->cfg.block_size)
         shift++;
-    return scan_impl(c, FullBlocksIn{offsets, shift}, n, starts, starts + n);
+    return scan_impl(c, FullBlocksIn{offsets, shift, n_tokens, bad, c->d_status}, n, starts,
+                     starts + n);
 }
 
 }  // namespace dm

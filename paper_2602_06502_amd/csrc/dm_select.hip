@@ -37,7 +37,7 @@
 namespace dm {
 namespace {
 
-constexpr int kSelSlot = 3;  // selection work arrays
+constexpr int kSelSlot = kSlotSelect;  // selection work arrays
 
 // Shared by both selection kernels: the SLO-aware rule given the two
 // candidates' pre-update loads.  kind bit0 = equal match, bit1 = c1 is the
@@ -1128,13 +1128,12 @@ struct SelBuf {
 
 static size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 
-static hipError_t sel_buffers(dm_ctx* c, uint64_t n, int par, SelBuf* b)
+// Sizes of one set's arrays for a batch of n requests, in layout order.
+static void sel_sizes(uint64_t n, size_t* sizes)
 {
-    hipError_t e = hipSuccess;
-    b->nblk = (n + kLevelBlock - 1) / kLevelBlock;
-    const uint64_t wcap = b->nblk * kWinCap;
-    b->nslots = wcap * kWave;
-    const size_t sizes[] = {
+    const uint64_t nblk = (n + kLevelBlock - 1) / kLevelBlock;
+    const uint64_t wcap = nblk * kWinCap;
+    const size_t z[] = {
         up256(n * sizeof(SelPack)),                                  // prep
         up256((wcap + 2 * kPrefetch) * kWave * sizeof(WalkRec)),     // rec
         up256((wcap + kPrefetch) * kWave * sizeof(longlong2)),       // lpre
@@ -1142,17 +1141,44 @@ static hipError_t sel_buffers(dm_ctx* c, uint64_t n, int par, SelBuf* b)
         up256(n * sizeof(uint32_t)),                                 // slot_of
         up256(wcap * kWave * sizeof(uint16_t)),                      // slotmap
         up256(wcap),                                                 // wdepth
-        up256(b->nblk * sizeof(uint32_t)),                           // wcount
-        up256(b->nblk * sizeof(uint32_t)),                           // woff
+        up256(nblk * sizeof(uint32_t)),                              // wcount
+        up256(nblk * sizeof(uint32_t)),                              // woff
         256 + 256 + (kMaxSlots + 1) * sizeof(unsigned long long),   // total, base/plan, grow
     };
-    size_t one = 0;
+    for (int i = 0; i < 10; i++)
+        sizes[i] = z[i];
+}
+
+uint64_t select_scratch_bytes(uint64_t n)
+{
+    size_t sizes[10], one = 0;
+    sel_sizes(n, sizes);
     for (size_t z : sizes)
         one += z;
-    uint8_t* sw = static_cast<uint8_t*>(scratch_get(c, kSelSlot, 2 * one, &e));
+    return one;
+}
+
+static hipError_t sel_buffers(dm_ctx* c, uint64_t n, int par, SelBuf* b)
+{
+    hipError_t e = hipSuccess;
+    b->nblk = (n + kLevelBlock - 1) / kLevelBlock;
+    b->nslots = b->nblk * kWinCap * kWave;
+    size_t sizes[10];
+    sel_sizes(n, sizes);
+    const size_t one = select_scratch_bytes(n);
+    // The two sets sit sel_stride apart whatever this batch's size: a
+    // smaller batch must not move its set into the other parity's, which the
+    // batch before it may still be walking.  A larger batch widens the
+    // stride only once every stream is idle.
+    if (one > c->sel_stride) {
+        if ((e = sync_streams(c)) != hipSuccess)
+            return e;
+        c->sel_stride = one;
+    }
+    uint8_t* sw = static_cast<uint8_t*>(scratch_get(c, kSelSlot, 2 * c->sel_stride, &e));
     if (!sw)
         return e;
-    sw += par * one;
+    sw += par * c->sel_stride;
     uint8_t* at[10];
     for (int i = 0; i < 10; i++) {
         at[i] = sw;

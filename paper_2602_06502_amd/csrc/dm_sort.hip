@@ -11,7 +11,7 @@ constexpr int kSortThreads = 256;
 constexpr int kSortItems = 4;
 constexpr uint64_t kSortTile = kSortThreads * kSortItems;
 constexpr int kSubtiles = kSortItems * (kSortThreads / kWave);
-constexpr int kSortSlot = 6;
+constexpr int kSortSlot = kSlotSort;
 
 __global__ __launch_bounds__(kSortThreads) void digit_hist_kernel(const uint64_t* __restrict__ keys,
                                                                   uint64_t n, int shift,
@@ -90,6 +90,11 @@ __global__ __launch_bounds__(kSortThreads) void digit_scatter_kernel(
 
 }  // namespace
 
+uint64_t sort_scan_len(uint64_t n) { return 256 * ((n + kSortTile - 1) / kSortTile); }
+
+// digit counts and their offsets, 256 per tile each
+uint64_t sort_scratch_bytes(uint64_t n) { return 2 * sort_scan_len(n) * sizeof(uint64_t); }
+
 hipError_t radix_sort_kv(dm_ctx* c, uint64_t* keys, uint32_t* vals, uint64_t* ktmp,
                          uint32_t* vtmp, uint64_t n, int bits)
 {
@@ -97,8 +102,7 @@ hipError_t radix_sort_kv(dm_ctx* c, uint64_t* keys, uint32_t* vals, uint64_t* kt
         return hipSuccess;
     const uint64_t ntiles = (n + kSortTile - 1) / kSortTile;
     hipError_t e;
-    uint64_t* cnt =
-        static_cast<uint64_t*>(scratch_get(c, kSortSlot, 2 * 256 * ntiles * sizeof(uint64_t), &e));
+    uint64_t* cnt = static_cast<uint64_t*>(scratch_get(c, kSortSlot, sort_scratch_bytes(n), &e));
     if (!cnt)
         return e;
     uint64_t* offs = cnt + 256 * ntiles;

@@ -302,28 +302,39 @@ def test_edge_cases_and_errors():
     eng.sync()
     r = o.route(tok, off, np.zeros(4, np.int64))
     compare_route(g, r, 5)
-    # malformed offsets are reported by dm_sync (the batch is not read past them)
-    bad = torch.tensor([0, 8, 4], dtype=torch.int64, device=dev)
-    eng.route(torch.zeros(8, dtype=torch.int32, device=dev), bad, L)
-    with pytest.raises(pk.DMError) as ei:
-        eng.sync()
-    assert ei.value.status == pk.DM_EINVAL
-    eng.sync()  # cleared
+    # malformed offsets are reported by dm_sync (the batch is not read past
+    # them): decreasing, negative, past the token array, and overlapping
+    # prompts that are each in range
+    for bad, ntok in (([0, 8, 4], 8), ([-16, 0, 8], 8), ([0, 8, 24], 16), ([0, 64, 0, 64], 64)):
+        _say("malformed offsets", bad, "tokens", ntok)
+        eng.route(torch.zeros(64, dtype=torch.int32, device=dev)[:ntok],
+                  torch.tensor(bad, dtype=torch.int64, device=dev), L, block_keys=True)
+        with pytest.raises(pk.DMError) as ei:
+            eng.sync()
+        assert ei.value.status == pk.DM_EINVAL
+        eng.sync()  # cleared
+    # the same token array with valid offsets routes normally afterwards
+    L = torch.zeros(4, dtype=torch.int64, device=dev)
+    g = eng.route(gh.to_dev(tok, dev), gh.to_dev(off, dev), L)
+    eng.sync()
+    compare_route(g, r, 5)
+    assert np.array_equal(cpu(L), r["loads"])
     # misaligned pointer rejected on the host
     lib = pk.load_library()
     import ctypes as C
     buf = torch.zeros(64, dtype=torch.int64, device=dev)
     ro = pk.dm_route_out(buf.data_ptr() + 4, buf.data_ptr(), buf.data_ptr(), buf.data_ptr(),
                          buf.data_ptr(), buf.data_ptr(), None)
-    st = lib.dm_route_batch(eng._h, buf.data_ptr(), buf.data_ptr(), 2, L.data_ptr(), C.byref(ro))
+    st = lib.dm_route_batch(eng._h, buf.data_ptr(), 128, buf.data_ptr(), 2, L.data_ptr(),
+                            C.byref(ro))
     assert st == pk.DM_EINVAL
-    st = lib.dm_route_batch(eng._h, None, buf.data_ptr(), 2, L.data_ptr(), C.byref(ro))
+    st = lib.dm_route_batch(eng._h, None, 128, buf.data_ptr(), 2, L.data_ptr(), C.byref(ro))
     assert st == pk.DM_EINVAL
     # a batch past the 32-bit selection slots is rejected before any work
     ok = pk.dm_route_out(buf.data_ptr(), buf.data_ptr(), buf.data_ptr(), buf.data_ptr(),
                          buf.data_ptr(), buf.data_ptr(), None)
-    st = lib.dm_route_batch(eng._h, buf.data_ptr(), buf.data_ptr(), 1_908_874_241, L.data_ptr(),
-                            C.byref(ok))
+    st = lib.dm_route_batch(eng._h, buf.data_ptr(), 128, buf.data_ptr(), 1_908_874_241,
+                            L.data_ptr(), C.byref(ok))
     assert st == pk.DM_EINVAL
     eng.sync()
 
@@ -381,6 +392,65 @@ def test_index_ops_and_capacity():
         eng.sync()
     assert ei.value.status == pk.DM_EFULL
     assert eng.index_size(1) == 128
+
+
+def test_index_capacity_within_one_batch():
+    """One insert batch that crosses the load limit stores exactly up to the
+    limit and reports DM_EFULL; a batch that fits (many duplicates, up to
+    exactly the limit) is stored whole with no error, however its threads
+    race for the last slots; a rebuild after erasures never holds more than
+    the limit.  2^8 slots hold at most 128 keys."""
+    gh = _h()
+    import paper_2602_06502_amd as pk
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=4, index_log2_slots=8)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    d = lambda a: gh.to_dev(a, eng.device)
+    rng = np.random.default_rng(5)
+
+    def full_error():
+        with pytest.raises(pk.DMError) as ei:
+            eng.sync()
+        assert ei.value.status == pk.DM_EFULL
+
+    # 200 distinct keys in one batch
+    many = rng.integers(2, 2**64, size=200, dtype=np.uint64)
+    _say("index: one batch of 200 distinct keys")
+    eng.index_insert(0, d(many))
+    full_error()
+    assert eng.index_size(0) == 128
+    # exactly 128 distinct keys, each four times, shuffled: fits, no error
+    k128 = rng.integers(2, 2**64, size=128, dtype=np.uint64)
+    _say("index: 128 distinct keys x 4 in one batch")
+    eng.index_insert(1, d(rng.permutation(np.tile(k128, 4))))
+    eng.sync()
+    assert eng.index_size(1) == 128
+    # 127 distinct keys x 3, then one new key x 60 with the old ones again
+    k127 = rng.integers(2, 2**64, size=128, dtype=np.uint64)
+    eng.index_insert(2, d(rng.permutation(np.tile(k127[:127], 3))))
+    eng.sync()
+    assert eng.index_size(2) == 127
+    eng.index_insert(2, d(rng.permutation(np.concatenate([np.repeat(k127[127:], 60), k127[:127]]))))
+    eng.sync()
+    assert eng.index_size(2) == 128
+    eng.index_insert(2, d(rng.integers(2, 2**64, size=3, dtype=np.uint64)))
+    full_error()
+    assert eng.index_size(2) == 128
+    # erase 28 of the full table, then 40 fresh keys: the rebuild keeps 100
+    # live keys and stores 28 more
+    eng.index_erase(0, d(many[:200]))  # erases exactly the stored ones
+    eng.sync()
+    assert eng.index_size(0) == 0
+    eng.index_insert(0, d(many[:128]))
+    eng.sync()
+    assert eng.index_size(0) == 128
+    eng.index_erase(0, d(many[:28]))
+    eng.sync()
+    assert eng.index_size(0) == 100
+    fresh = rng.integers(2, 2**64, size=40, dtype=np.uint64)
+    _say("index: rebuild after erasures, then past the limit")
+    eng.index_insert(0, d(fresh))
+    full_error()
+    assert eng.index_size(0) == 128
 
 
 def test_index_churn_rebuilds_erased_slots():
@@ -715,3 +785,40 @@ def test_pipelined_batches_parity(slo_us):
     r = o.route(t, f, Lo)
     compare_route(g, r, 300)
     assert np.array_equal(cpu(Ld), r["loads"])
+
+
+def test_pipelined_shrinking_batches_parity():
+    """Pipelined batches of 16,384, then 8,192, then 16,384 requests: each
+    batch's selection work arrays must stay clear of those of the batch
+    before it, which may still be walking when a smaller batch packs its
+    records.  Every output and the final loads against the oracle."""
+    import dataclasses
+    wl = workloads.small_random(77, 24, 16, 16, 40_960, slo_us=60_000)
+    wl = dataclasses.replace(wl, n_prior=2_000,
+                             route=dataclasses.replace(wl.route, index_log2_slots=14))
+    gh = _h()
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    gh.prefill_from_prior(eng, wl)
+    oh.prefill_from_prior(o, wl)
+    tok, off = workloads.prompts(wl, wl.n_req)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    dev = eng.device
+    Ld = gh.to_dev(L0, dev)
+    cuts = [0, 16_384, 24_576, 40_960]
+    eng.set_pipelining(True)
+    outs, refs, Lo = [], [], L0
+    try:
+        for lo, hi in zip(cuts[:-1], cuts[1:]):
+            _say("pipelined batch", hi - lo)
+            t = tok[off[lo]:off[hi]]
+            f = off[lo:hi + 1] - off[lo]
+            outs.append(eng.route(gh.to_dev(t, dev), gh.to_dev(f, dev), Ld))
+            r = o.route(t, f, Lo)
+            refs.append(r)
+            Lo = r["loads"]
+        eng.sync()
+    finally:
+        eng.set_pipelining(False)
+    for g, r, (lo, hi) in zip(outs, refs, zip(cuts[:-1], cuts[1:])):
+        compare_route(g, r, hi - lo)
+    assert np.array_equal(cpu(Ld), Lo)

@@ -64,7 +64,7 @@ def test_null_context_is_rejected():
     pk, lib = _lib()
     assert lib.dm_sync(None) == pk.DM_EINVAL
     assert lib.dm_build_rings(None, None, 0) == pk.DM_EINVAL
-    assert lib.dm_route_batch(None, None, None, 0, None, None) == pk.DM_EINVAL
+    assert lib.dm_route_batch(None, None, 0, None, 0, None, None) == pk.DM_EINVAL
     assert lib.dm_rebalance(None, None, None, None, 0) == pk.DM_EINVAL
     assert lib.dm_scale(None, None, 0, None, 0, None, 0, None, None, None, None) == pk.DM_EINVAL
     assert lib.dm_index_insert(None, 0, None, 0) == pk.DM_EINVAL

@@ -9,10 +9,12 @@ nodes per ring, block 16, each instance index holding 1,048,576 keys in
 to the snapshot before every step (a 2 KB device copy inside the step).
 
 Prints one JSON line: requests routed/s, prompt tokens hashed/s, the HBM
-roofline of the hash+match kernel (algorithmic bytes / its average
-duration measured with HIP events on the engine's stream), the elastic
-workload's scale, re-route and rebalance times (after the timed steps), and
-the CPU oracle timed on a bounded sample of the same workload.
+roofline of the hash+match stage (algorithmic bytes / the stage's average
+device time measured with HIP events on the stream it runs on; the hash
+kernel alone as an extra key), the elastic workload's scale, re-route and
+rebalance times (after the timed steps), one row per smaller configuration
+(tiny, chat, agent: GPU and oracle throughput, parity), and the CPU oracle
+timed on the benchmark's own batch.
 """
 import argparse
 import hashlib
@@ -31,25 +33,47 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def route_source_hash():
-    """Hash of the hash kernel's source: its memory traffic depends on it alone."""
+def source_hash(files):
+    """Hash of kernel sources: a kernel's memory traffic depends on them alone."""
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2602_06502_amd", "csrc", "dm_hash.hip"), "rb") as fh:
-        h.update(fh.read())
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2602_06502_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def load_traffic(name):
+# Sources of the hash+match stage's kernels (block offsets, hashing, ring
+# lookup, request ordering, probing) and of the hash kernel alone.
+STAGE_SOURCES = ("dm_internal.h", "dm_route.hip", "dm_scan.hip", "dm_hash.hip", "dm_probe.hip",
+                 "dm_sort.hip")
+HASH_SOURCES = ("dm_hash.hip",)
+
+
+def load_traffic(name, files):
     """HBM bytes per launch from rocprofv3 FETCH_SIZE/WRITE_SIZE counters, if
-    recorded for the current kernel source."""
+    recorded for the current kernel sources."""
     p = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(p):
         return None
     with open(p) as f:
         d = json.load(f)
-    if d.get("source_hash") != route_source_hash():
+    if d.get("source_hash") != source_hash(files):
         return None
     return d.get("bytes_per_launch")
+
+
+def host_cpu():
+    """(logical CPUs, model name) of the host."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return os.cpu_count(), model
 
 
 def algorithmic_bytes(off_np, B, match, cand, n):
@@ -125,26 +149,139 @@ def walk_steps(cand, match, n, block=1024, lanes=64, run_max=3):
     return steps, windows
 
 
-def cpu_baseline(wl, sample):
+def cpu_baseline(wl, st, sample):
     """The oracle as it stands, single-threaded, on the first `sample`
-    requests of the same workload (same index, same initial loads)."""
+    requests of the benchmark's own batch (same index, same initial loads);
+    the whole batch by default."""
     import numpy as np
 
     import oracle
     import oracle.harness as oh
-    import workloads
     oracle.build(force=False)
     log("cpu baseline: building oracle state")
-    st = oh.setup(wl, with_batch=False)
-    tok, off = workloads.prompts(wl, sample, sub=0)
+    ost = oh.setup(wl, with_batch=False)
+    off = st["offsets_np"][:sample + 1]
+    tok = st["tokens_np"][:int(off[-1])]
+    log(f"cpu baseline: oracle routes {sample:,} requests")
     t0 = time.perf_counter()
-    st["oracle"].route(tok, off, st["loads0"])
+    ost["oracle"].route(tok, off, ost["loads0"])
     dt = time.perf_counter() - t0
     ntok = int(((np.diff(off) // wl.route.block) * wl.route.block).sum())
+    ncpu, model = host_cpu()
+    what = "the whole batch" if sample == wl.n_req else f"the first {sample:,} requests"
     return {"value": sample / dt, "unit": "requests/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {sample:,} of the {wl.n_req:,} requests (same index and loads), "
-                      f"{dt:.1f} s single-threaded on the host",
+            "sample": f"{what} of the {wl.n_req:,}-request benchmark batch (same index and "
+                      f"loads), {dt:.1f} s single-threaded",
+            "host_logical_cpus": ncpu, "host_cpu_model": model,
             "tokens_hashed_per_s": ntok / dt}
+
+
+def queues_of(chosen, cand, match, off, B, S, base):
+    """Queues of a routed batch: request r waits on its chosen instance with
+    its uncached tokens there, the other candidate and its uncached tokens
+    there (records in request order)."""
+    import numpy as np
+    n = len(chosen)
+    lens = np.diff(off).astype(np.int64)
+    c1, c2 = cand[:n].astype(np.int64), cand[n:].astype(np.int64)
+    u1 = lens - B * match[:n].astype(np.int64)
+    u2 = lens - B * match[n:].astype(np.int64)
+    first = chosen.astype(np.int64) == c1
+    here, other = np.where(first, u1, u2), np.where(first, u2, u1)
+    alt = np.where(first, c2, c1)
+    order = np.argsort(chosen, kind="stable")
+    qoff = np.zeros(S + 1, np.int64)
+    np.cumsum(np.bincount(chosen, minlength=S), out=qoff[1:])
+    return (qoff, order.astype(np.uint64), here[order].astype(np.uint32),
+            alt[order].astype(np.uint32), other[order].astype(np.uint32), base)
+
+
+def config_rows(reps):
+    """Configurations 1-3 at their own shapes, each one batch against its
+    warmed state: GPU device time of one unpipelined dm_route_batch (HIP
+    events around its stages, median over `reps` after one warm-up), the
+    oracle on the same batch (one run, single-threaded), and whether every
+    output matched.  The agent row adds a rebalancing pass over the batch's
+    queues with four seed-chosen instances stalled to 5x the mean work."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import oracle.harness as oh
+    import paper_2602_06502_amd.harness as gh
+    import workloads
+    oracle.build(force=False)
+    rows = {}
+    specs = [("tiny", workloads.tiny()), ("chat", workloads.chat()), ("agent", workloads.agent())]
+    for name, cfg in specs:
+        log("config row:", name)
+        if name == "tiny":
+            g, o = gh.setup(cfg, device="cuda:0"), oh.setup(cfg)
+            rc = cfg.route
+        else:
+            g, o = gh.setup_warm(cfg, device="cuda:0"), oh.setup_warm(cfg)
+            rc = cfg.route
+        eng = g["eng"]
+        n = len(g["offsets_np"]) - 1
+        out = eng.alloc_route_out(n)
+        dev_ms = []
+        for i in range(reps + 1):  # the first call is a warm-up
+            L = gh.to_dev(g["loads0"], eng.device)
+            eng.set_timing(True)  # restarts the averages: this call alone
+            eng.route_into(g["tokens"], g["offsets"], L, out)
+            eng.sync()
+            if i > 0:
+                dev_ms.append(sum(eng.stage_ms()))
+        eng.set_timing(False)
+        got = {k: v.cpu().numpy() for k, v in out.items()}
+        got["loads"] = L.cpu().numpy()
+        t0 = time.perf_counter()
+        ref = o["oracle"].route(o["tokens"], o["offsets"], o["loads0"])
+        odt = time.perf_counter() - t0
+        same = all(np.array_equal(got[k], ref[k][:len(got[k])]) for k in
+                   ("key", "cand", "match", "chosen", "ttft", "flags", "loads"))
+        ntok = int(((np.diff(g["offsets_np"]) // rc.block) * rc.block).sum())
+        ms = float(np.median(dev_ms))
+        row = {"requests": n, "full_block_tokens": ntok,
+               "gpu": {"ms_per_batch": ms, "requests_per_s": n / (ms * 1e-3),
+                       "tokens_hashed_per_s": ntok / (ms * 1e-3)},
+               "oracle": {"s": odt, "requests_per_s": n / odt, "tokens_hashed_per_s": ntok / odt,
+                          "threads": 1},
+               "parity": bool(same)}
+        if name == "agent":
+            S = rc.max_slots
+            base = np.zeros(S, np.int64)
+            base[:rc.n_inst] = cfg.mu
+            hot = workloads.agent_hot_instances(cfg, 0)
+            base[hot] += (cfg.hot_factor - 1) * cfg.mu
+            q = queues_of(got["chosen"], got["cand"], got["match"], g["offsets_np"], rc.block, S,
+                          base)
+            qd = [gh.to_dev(x, eng.device) for x in q]
+            rms = []
+            for i in range(reps + 1):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                m = eng.rebalance(*qd)
+                eng.sync()
+                if i > 0:
+                    rms.append(1000.0 * (time.perf_counter() - t0))
+            cnt = int(m["count"].cpu()[0])
+            t0 = time.perf_counter()
+            r = o["oracle"].rebalance(*q)
+            ort = time.perf_counter() - t0
+            rsame = r["status"] == 0 and r["count"] == cnt and all(
+                np.array_equal(m[k].cpu().numpy()[:cnt], r[k]) for k in
+                ("rec", "src", "dst", "benefit", "ttft_to")) and np.array_equal(
+                m["loads"].cpu().numpy(), r["loads"])
+            row["rebalance"] = {"records": int(q[0][-1]), "migrations": cnt,
+                                "gpu_ms": float(np.median(rms)), "oracle_ms": 1000.0 * ort,
+                                "parity": bool(rsame),
+                                "note": "host clock per call; queues of the routed batch, "
+                                        "four seed-chosen instances stalled to 5x the mean work"}
+        rows[name] = row
+        del eng, g, o, out
+        torch.cuda.empty_cache()
+    return rows
 
 
 def elastic_leg(eng, wl, st, keys, L0, reps):
@@ -228,8 +365,12 @@ def main():
     ap.add_argument("--steps", type=int, default=40)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--n-req", type=int, default=1_048_576)
-    ap.add_argument("--cpu-sample", type=int, default=100_000)
+    ap.add_argument("--cpu-sample", type=int, default=0,
+                    help="requests the oracle routes for the CPU baseline (0 = the whole batch)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--config-reps", type=int, default=5)
+    ap.add_argument("--no-config-rows", action="store_true",
+                    help="skip the tiny / chat / agent rows")
     ap.add_argument("--elastic-reps", type=int, default=5)
     ap.add_argument("--no-elastic", action="store_true",
                     help="skip the scale / re-route / rebalance timings")
@@ -298,7 +439,9 @@ def main():
                                                      cand, n)
     achieved = hbytes / (hash_avg * 1e-3) / 1e9
     stage_gbs = sbytes / ((hash_avg + match_avg) * 1e-3) / 1e9
-    traffic = load_traffic("traffic_hash_kernel_large.json")
+    hash_traffic = load_traffic("traffic_hash_kernel_large.json", HASH_SOURCES)
+    stage_traffic = load_traffic("traffic_route_stage_large.json", STAGE_SOURCES)
+    final = loads[args.warmup + args.steps - 1].cpu().numpy()[:wl.route.n_inst].astype(np.float64)
     flags = out["flags"].cpu().numpy()
     depth_steps, walk_windows = walk_steps(cand, match, n)
     depth_steps_no_runs, _ = walk_steps(cand, match, n, run_max=1)
@@ -342,17 +485,31 @@ def main():
                         "steps": n_ref,
                         "stage_ms": {"hash": ref_stage[0], "lookup_match": ref_stage[1],
                                      "select": ref_stage[2], "block_offsets": ref_stage[3]}},
-        "roofline": {"bound": "hbm", "kernel": "hash_kernel<16>", "achieved": achieved,
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic, "algorithmic_bytes_per_launch": hbytes},
-        "hash_match_stage": {"achieved_GBs": stage_gbs, "frac": stage_gbs / HBM_PEAK_GBS,
-                             "algorithmic_bytes": sbytes, "probes": probes,
-                             "ms": hash_avg + match_avg},
+        "roofline": {"bound": "hbm",
+                     "kernel": "hash+match stage: hash_kernel<16>, lookup_kernel, "
+                               "order_init_kernel, radix sort passes, probe_zero_kernel, "
+                               "probe_kernel",
+                     "achieved": stage_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": stage_gbs / HBM_PEAK_GBS, "traffic": stage_traffic,
+                     "algorithmic_bytes_per_launch": sbytes, "probes": probes,
+                     "ms": hash_avg + match_avg,
+                     "note": "algorithmic bytes of one batch (full-block tokens, offsets, "
+                             "per-request outputs, 8 B per index slot the first-miss rule "
+                             "inspects) over the stage's device time from HIP events on the "
+                             "stream it runs on, averaged over the timed steps"},
+        "roofline_hash_kernel": {"bound": "hbm", "kernel": "hash_kernel<16>",
+                                 "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                 "frac": achieved / HBM_PEAK_GBS, "traffic": hash_traffic,
+                                 "algorithmic_bytes_per_launch": hbytes, "ms": hash_avg},
         "routing_stats": {"slo_switch_frac": float((flags & 1).mean()),
                           "both_over_frac": float(((flags >> 1) & 1).mean()),
                           "hit_blocks_frac": float(
                               np.where(out["chosen"].cpu().numpy() == cand[:n], match[:n],
-                                       match[n:]).sum() / max(1, ntok // wl.route.block))},
+                                       match[n:]).sum() / max(1, ntok // wl.route.block)),
+                          "final_load_cv": float(final.std() / final.mean()),
+                          "note": "final_load_cv: coefficient of variation of the instances' "
+                                  "queued work after the batch (std / mean over live "
+                                  "instances)"},
     }
     if not args.no_elastic:
         log("elastic leg: scale, re-route, rebalance")
@@ -364,8 +521,11 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         res["calibration_copy_bytes"] = {"read": src.numel() * 4, "write": dst.numel() * 4}
+    if not args.no_config_rows:
+        log("configuration rows: tiny, chat, agent")
+        res["configs"] = config_rows(args.config_reps)
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_sample, n))
+        res["cpu_baseline"] = cpu_baseline(wl, st, min(args.cpu_sample or n, n))
     print(json.dumps(res), flush=True)
 
 

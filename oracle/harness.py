@@ -67,3 +67,20 @@ def setup(wl: workloads.Workload, with_batch: bool = True) -> Dict:
     if with_batch:
         res["tokens"], res["offsets"] = workloads.prompts(wl, wl.n_req, sub=0)
     return res
+
+
+def setup_warm(cfg) -> Dict:
+    """The oracle's counterpart of the engine-side warm start of a chat or
+    agent workload: warm-up batches routed in order from zero queued work,
+    each batch's chains inserted into its chosen instance; then the first
+    measured batch and its queued work."""
+    rc = cfg.route
+    o = Oracle(rc.as_dict())
+    assert o.build_rings(range(rc.n_inst)) == 0
+    Lw = np.zeros(rc.max_slots, np.int64)
+    for tok, off in workloads.warmup_batches(cfg):
+        out = o.route(tok, off, Lw, block_keys=True)
+        Lw = out["loads"]
+        insert_blocks(o, out["block_keys"], np.repeat(out["chosen"], np.diff(off) // rc.block))
+    tok, off, L0 = workloads.measured_batch(cfg)
+    return dict(oracle=o, tokens=tok, offsets=off, loads0=L0)

@@ -107,3 +107,26 @@ def setup(wl: workloads.Workload, device="cuda:0") -> Dict:
     loads0 = workloads.initial_loads(wl, wl.route.max_slots)
     return dict(eng=eng, tokens=to_dev(tok, eng.device), offsets=to_dev(off, eng.device),
                 loads0=loads0, tokens_np=tok, offsets_np=off)
+
+
+def setup_warm(cfg, device="cuda:0") -> Dict:
+    """Engine for a chat or agent workload after its warm-up: the warm-up
+    batches routed in order from zero queued work (loads carried from batch
+    to batch), each batch's chains cached on its chosen instance.  The
+    warm-up stays under the per-instance cache bound, so no block is
+    evicted.  Returns the engine and the first measured batch (device and
+    host copies) with its queued work."""
+    torch = _torch()
+    rc = cfg.route
+    eng = DualMap(rc.as_dict(), device=device)
+    eng.build_rings(list(range(rc.n_inst)))
+    Lw = torch.zeros(eng.max_slots, dtype=torch.int64, device=eng.device)
+    for tok, off in workloads.warmup_batches(cfg):
+        off_d = to_dev(off, eng.device)
+        out = eng.route(to_dev(tok, eng.device), off_d, Lw, block_keys=True)
+        per_block = torch.repeat_interleave(out["chosen"].to(torch.int64), full_blocks(eng, off_d))
+        insert_blocks(eng, out["block_keys"], per_block)
+    eng.sync()
+    tok, off, L0 = workloads.measured_batch(cfg)
+    return dict(eng=eng, tokens=to_dev(tok, eng.device), offsets=to_dev(off, eng.device),
+                loads0=L0, tokens_np=tok, offsets_np=off)

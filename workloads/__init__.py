@@ -411,6 +411,7 @@ class Agent:
     hot_factor: int = 5
     drain_per_us: int = 4
     utilisation: float = 0.9
+    mu: int = 320_000         # mean queued work per instance: 5 mu / 4 crosses the SLO
 
 
 def agent(n_req: int = 262_144, n_warm: int = 16_384, batch: int = 16_384) -> Agent:
@@ -464,3 +465,36 @@ def arrival_gaps(seed: int, n_batches: int, batch: int, mean_gap_us: float) -> n
 def batch_initial_loads(seed: int, n_slots: int, hi: int) -> np.ndarray:
     """Per-slot queued work U[0, hi] for the multi-batch workloads."""
     return _rng(seed, _S_LOADS).integers(0, hi + 1, size=n_slots).astype(np.int64)
+
+
+# --------------------------------------------------------------------------
+# One measured batch of a multi-batch workload, after its warm-up (for the
+# per-configuration rows of the benchmark).
+# --------------------------------------------------------------------------
+
+def warmup_batches(cfg):
+    """The warm-up requests of a chat or agent workload as a list of token
+    CSRs, one per batch of cfg.batch requests."""
+    out = []
+    if isinstance(cfg, Chat):
+        st = ChatStream(cfg, 1)
+        for lo in range(0, st.n, cfg.batch):
+            out.append(st.batch(lo, lo + cfg.batch))
+    else:
+        for w in range(0, cfg.n_warm, cfg.batch):
+            out.append(agent_batch(cfg, w // cfg.batch, min(cfg.batch, cfg.n_warm - w), warm=True))
+    return out
+
+
+def measured_batch(cfg, b: int = 0):
+    """Batch b of the measured requests of a chat or agent workload, and the
+    queued work per slot it is routed against when it is the first batch
+    (chat: U[0, load_hi]; agent: mu on every live instance)."""
+    S = cfg.route.max_slots
+    if isinstance(cfg, Chat):
+        tok, off = ChatStream(cfg, 0).batch(b * cfg.batch, (b + 1) * cfg.batch)
+        return tok, off, batch_initial_loads(cfg.seed, S, cfg.load_hi)
+    tok, off = agent_batch(cfg, b, cfg.batch)
+    L = np.zeros(S, np.int64)
+    L[: cfg.route.n_inst] = cfg.mu
+    return tok, off, L

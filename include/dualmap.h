@@ -153,6 +153,24 @@ dm_status dm_route_batch(dm_ctx* ctx, const int32_t* tokens, uint64_t n_tokens,
                          const int64_t* offsets, uint64_t n, int64_t* loads,
                          const dm_route_out* out);
 
+/* dm_route_batch for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * Same arguments, results and device-side checks as dm_route_batch; the
+ * caller still provides every input and output.  Work arrays come from a
+ * static area of 64 MiB per GPU that the library holds until the process
+ * ends, instead of the context's growable scratch: the call allocates and
+ * frees nothing.  The batch is planned on the host first; if its work
+ * arrays do not fit (about 250 bytes per request plus, when block_keys is
+ * NULL, 8 bytes per n_tokens / B), the call returns DM_EINVAL with the
+ * sizes in dm_last_error and launches nothing.  Runs unpipelined on the
+ * context's stream (after any pipelined batch).  Every call on one GPU
+ * shares that GPU's area: calls that overlap on one GPU (other contexts,
+ * other host threads, unordered streams) race.  DM_EDEVICE if the area
+ * could not be located on this device. */
+dm_status dm_route_batch_noalloc(dm_ctx* ctx, const int32_t* tokens, uint64_t n_tokens,
+                                 const int64_t* offsets, uint64_t n, int64_t* loads,
+                                 const dm_route_out* out);
+
 /* Pending-request queues, CSR over instance slots (device arrays).  Queue i
  * is records [qoff[i], qoff[i+1]) head first; record q costs unc_here[q]
  * uncached tokens on i and unc_alt[q] on its alternative candidate alt[q]

@@ -25,6 +25,7 @@ _NAMES = {0: "DM_OK", 1: "DM_EINVAL", 2: "DM_ENOMEM", 3: "DM_EFULL", 4: "DM_ESTA
 
 EXPORTS = ("dm_create", "dm_destroy", "dm_build_rings", "dm_ring_export", "dm_index_insert",
            "dm_index_erase", "dm_index_clear", "dm_index_size", "dm_route_batch",
+           "dm_route_batch_noalloc",
            "dm_rebalance", "dm_scale", "dm_set_timing", "dm_route_stage_ms",
            "dm_set_pipelining", "dm_sync", "dm_last_error")
 
@@ -81,6 +82,7 @@ def load_library(path: str = LIB_PATH):
         "dm_index_clear": (i32, [P, u32]),
         "dm_index_size": (i32, [P, u32, P]),
         "dm_route_batch": (i32, [P, P, u64, P, u64, P, P]),
+        "dm_route_batch_noalloc": (i32, [P, P, u64, P, u64, P, P]),
         "dm_rebalance": (i32, [P, P, P, P, u64]),
         "dm_scale": (i32, [P, P, u32, P, u32, P, u64, P, P, P, P]),
         "dm_set_timing": (i32, [P, i32]),
@@ -224,14 +226,17 @@ class DualMap:
         self._check(self.lib.dm_index_size(self._h, inst, C.byref(n)), "dm_index_size")
         return int(n.value)
 
-    def route_into(self, tokens, offsets, loads, out: Dict) -> None:
-        """dm_route_batch into preallocated outputs (no allocation of outputs)."""
+    def route_into(self, tokens, offsets, loads, out: Dict, noalloc: bool = False) -> None:
+        """dm_route_batch into preallocated outputs; with noalloc,
+        dm_route_batch_noalloc (work arrays from the library's static area)."""
         n = offsets.numel() - 1
         ro = dm_route_out(_ptr(out["key"]), _ptr(out["cand"]), _ptr(out["match"]),
                           _ptr(out["chosen"]), _ptr(out["ttft"]), _ptr(out["flags"]),
                           _ptr(out.get("block_keys")))
-        self._check(self.lib.dm_route_batch(self._h, _ptr(tokens), tokens.numel(), _ptr(offsets),
-                                            n, _ptr(loads), C.byref(ro)), "dm_route_batch")
+        fn = self.lib.dm_route_batch_noalloc if noalloc else self.lib.dm_route_batch
+        name = "dm_route_batch_noalloc" if noalloc else "dm_route_batch"
+        self._check(fn(self._h, _ptr(tokens), tokens.numel(), _ptr(offsets), n, _ptr(loads),
+                       C.byref(ro)), name)
 
     def alloc_route_out(self, n: int, n_blocks: Optional[int] = None) -> Dict:
         t = self.torch

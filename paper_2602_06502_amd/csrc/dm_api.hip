@@ -43,6 +43,13 @@ void* scratch_get(dm_ctx* c, int slot, size_t bytes, hipError_t* e)
     *e = hipSuccess;
     if (bytes == 0)
         bytes = 256;
+    if (c->arena.on) {
+        // allocation-free call: the region planned for this slot, or an error
+        if (bytes <= c->arena.len[slot])
+            return c->arena.base + c->arena.off[slot];
+        *e = hipErrorOutOfMemory;
+        return nullptr;
+    }
     if (s.bytes >= bytes)
         return s.p;
     // Work already queued (on any of the context's streams) may still use
@@ -241,6 +248,11 @@ dm_status dm_create(const dm_config* cfg, void* hip_stream, dm_ctx** out)
     if (e == hipSuccess) e = hipMemsetAsync(c->d_status, 0, sizeof(uint32_t), c->stream);
     if (e == hipSuccess) e = hipMemsetAsync(c->d_next_live, 0, S * sizeof(uint32_t), c->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    // the static work area of allocation-free routing on this device; if it
+    // cannot be found, that entry point reports DM_EDEVICE and nothing else
+    // is affected
+    if (e == hipSuccess && noalloc_attach(c) != hipSuccess)
+        (void)hipGetLastError();
     if (e != hipSuccess) {
         dm_status s = (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) ? DM_ENOMEM
                                                                                    : DM_EDEVICE;

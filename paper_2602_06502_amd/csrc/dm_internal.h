@@ -72,6 +72,16 @@ struct Scratch {
     size_t bytes = 0;
 };
 
+// Fixed work area for calls that must not allocate: every scratch slot is a
+// region carved from it before the call's first launch, sized by the call's
+// plan; a request past its region fails instead of growing.
+struct Arena {
+    bool on = false;
+    uint8_t* base = nullptr;
+    size_t off[kScratchSlots] = {};
+    size_t len[kScratchSlots] = {};
+};
+
 }  // namespace dm
 
 struct dm_ctx {
@@ -103,6 +113,8 @@ struct dm_ctx {
     uint32_t* d_status = nullptr;  // device status word
 
     dm::Scratch scratch[dm::kScratchSlots];
+    dm::Arena arena;                  // set only for the duration of an allocation-free call
+    uint8_t* noalloc_area = nullptr;  // this device's static work area (dm_noalloc.hip)
     uint32_t shift_div = 0;        // log2(queue_div)
     // Distance between the two selection work-array sets (by batch parity).
     // It only grows, and only once every stream is idle, so a set in use by
@@ -175,6 +187,14 @@ uint64_t sort_scratch_bytes(uint64_t n);
 uint64_t sort_scan_len(uint64_t n);  // length of the sort's digit-count scans
 uint64_t probe_scratch_bytes(uint64_t n);
 uint64_t select_scratch_bytes(uint64_t n);
+// Per-slot scratch of one unpipelined dm_route_batch (bytes[kScratchSlots]).
+void route_scratch_plan(const dm_ctx* c, uint64_t n, uint64_t n_tokens, bool keys_in_scratch,
+                        size_t* bytes);
+
+// dm_noalloc.hip: this device's static work area (looked up once per device
+// by dm_create) and its size.
+hipError_t noalloc_attach(dm_ctx* c);
+size_t noalloc_capacity();
 
 // dm_scan.hip: exclusive prefix sums.
 hipError_t exclusive_scan_u64(dm_ctx* c, const uint64_t* in, uint64_t n, uint64_t* out,

@@ -47,6 +47,21 @@ struct StreamSwap {
 
 }  // namespace
 
+void route_scratch_plan(const dm_ctx* c, uint64_t n, uint64_t n_tokens, bool keys_in_scratch,
+                        size_t* bytes)
+{
+    for (int i = 0; i < kScratchSlots; i++)
+        bytes[i] = 0;
+    bytes[kSlotStarts] = (n + 2) * sizeof(uint64_t);  // block starts, malformed-offsets word
+    bytes[kSlotProbe] = probe_scratch_bytes(n);       // request order, claim counters
+    bytes[kSlotSelect] = select_scratch_bytes(n);     // one set of selection work arrays
+    if (keys_in_scratch)                              // block keys
+        bytes[kSlotKeys] = ((n_tokens >> block_shift_of(c)) + 1) * sizeof(uint64_t);
+    bytes[kSlotSort] = sort_scratch_bytes(n);         // digit counts of the ordering sort
+    const uint64_t s1 = scan_scratch_bytes(n), s2 = scan_scratch_bytes(sort_scan_len(n));
+    bytes[kSlotScan] = s1 > s2 ? s1 : s2;             // tile sums of both kinds of scan
+}
+
 hipError_t route(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens, const int64_t* offsets,
                  uint64_t n, int64_t* loads, const dm_route_out* out)
 {

@@ -1166,19 +1166,26 @@ static hipError_t sel_buffers(dm_ctx* c, uint64_t n, int par, SelBuf* b)
     size_t sizes[10];
     sel_sizes(n, sizes);
     const size_t one = select_scratch_bytes(n);
-    // The two sets sit sel_stride apart whatever this batch's size: a
-    // smaller batch must not move its set into the other parity's, which the
-    // batch before it may still be walking.  A larger batch widens the
-    // stride only once every stream is idle.
-    if (one > c->sel_stride) {
-        if ((e = sync_streams(c)) != hipSuccess)
-            return e;
-        c->sel_stride = one;
+    uint8_t* sw = nullptr;
+    if (c->arena.on) {
+        // allocation-free call: unpipelined, one set
+        sw = static_cast<uint8_t*>(scratch_get(c, kSelSlot, one, &e));
+    } else {
+        // The two sets sit sel_stride apart whatever this batch's size: a
+        // smaller batch must not move its set into the other parity's, which
+        // the batch before it may still be walking.  A larger batch widens
+        // the stride only once every stream is idle.
+        if (one > c->sel_stride) {
+            if ((e = sync_streams(c)) != hipSuccess)
+                return e;
+            c->sel_stride = one;
+        }
+        sw = static_cast<uint8_t*>(scratch_get(c, kSelSlot, 2 * c->sel_stride, &e));
+        if (sw)
+            sw += par * c->sel_stride;
     }
-    uint8_t* sw = static_cast<uint8_t*>(scratch_get(c, kSelSlot, 2 * c->sel_stride, &e));
     if (!sw)
         return e;
-    sw += par * c->sel_stride;
     uint8_t* at[10];
     for (int i = 0; i < 10; i++) {
         at[i] = sw;

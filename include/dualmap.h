@@ -227,12 +227,13 @@ dm_status dm_scale(dm_ctx* ctx, const uint32_t* add, uint32_t n_add, const uint3
 /* Instrumentation.  With on != 0, dm_route_batch records HIP events around
  * its stages; dm_route_stage_ms waits for the last batch and writes up to n
  * stage times in milliseconds to ms_host, averaged over the batches routed
- * since timing was (re)enabled (the last 64 at most): [0] chained block
- * hashing (one kernel), [1] ring lookup and longest cached prefix, [2]
- * record packing and in-order selection (with pipelining: from the end of
- * the batch's probe stage to the end of its selection, so it includes
- * waiting for the previous batch's selection), [3] per-request block
- * offsets.
+ * since timing was (re)enabled (the last 64 at most): [0] ring keys,
+ * candidates and request groups (prefix hashing, ring lookup, ordering,
+ * grouping), [1] full chains and longest cached prefixes (group leaders,
+ * then every other request), [2] record packing and in-order selection
+ * (with pipelining: from the end of the batch's stage [1] to the end of its
+ * selection, so it includes waiting for the previous batch's selection),
+ * [3] per-request block offsets and the offsets check.
  * dm_route_stage_ms returns DM_ESTATE if timing is off or no batch was
  * timed. */
 dm_status dm_set_timing(dm_ctx* ctx, int on);

@@ -1,23 +1,46 @@
-// Chained block keys and ring keys of every request (Sec. 3.2; Sec. A.1.1).
+// Chained block keys, ring keys and longest cached prefixes (Sec. 3.2;
+// Sec. A.1.1; the per-block KV metadata of Sec. A.3.2).
 //
-// Each wave takes requests in turn (one, unless the batch has more than 4 Mi
-// requests) and walks each prompt 64 blocks at a time, lane l owning block l
-// of the chunk:
+// One wave per request walks the prompt 64 blocks at a time, lane l owning
+// block l of the chunk:
 //   - NH digest of its block from B/4 16-byte loads;
 //   - the affine chain H[b] = H[b-1] P + NH(b) for all 64 lanes at once:
 //     with Q = P^-1 mod 2^64, H[c+l] = P^(l+1) (G + sum_{k<=l} NH(c+k)
 //     Q^(k+1)), G carrying H of the previous chunk -- a wave prefix sum of
 //     u64 (register-level DPP moves) instead of a serial chain;
-//   - block key mix64(H xor seed), stored for every full block;
-//   - in the first chunk the f2 chain over the first K blocks (one wave
-//     sum) gives the second ring key.
+//   - block key mix64(H xor seed).
+// Three passes use this walk (dm_route.hip runs them in this order):
+//   prefix   both chains over the first min(K, full blocks) blocks only:
+//            the two ring keys (ring_key_kernel: several requests per wave);
+//   leaders  one request per group of equal ring keys (dm_probe.hip): the
+//            full f1 chain, stored; each chunk's keys are probed against
+//            both candidates' tables, lanes from the first unresolved block
+//            (two first, then the rest of the chunk), until each
+//            candidate's first absent block;
+//   members  every other request: the full f1 chain (stored only when the
+//            caller asks for block keys).  While within one block past the
+//            leader's longer match, each chunk's keys are compared with the
+//            leader's stored keys (one ballot): blocks before the first
+//            disagreement s hold the leader's keys, so on a candidate where
+//            the leader's match ends before s the request's match is the
+//            leader's; elsewhere the request's first s blocks are present
+//            and its keys are probed from block s on, chunk by chunk.
+// The comparison is of keys and the probes are of keys, so every match is
+// the definition's (leading blocks whose f1 keys are all in the candidate's
+// index) whatever the keys are.  Requests that share a prefix with their
+// leader read the leader's 8-byte keys (cache-resident) instead of probing
+// 64-byte buckets for it, and no request reads its own keys back.
 #include "dm_internal.h"
 
 namespace dm {
 namespace {
 
 constexpr int kHashThreads = 256;
-constexpr uint32_t kHashBlocks = 1u << 20;  // one wave per request up to 4 Mi requests
+constexpr uint32_t kHashBlocks = 1u << 20;  // one wave per unit up to 4 Mi units
+constexpr uint32_t kLeaderBlocks = 2048;    // leaders: at most 8,192 waves, grid-stride
+
+enum : int { kLeaders = 1, kResume = 2 };
+constexpr uint64_t kPendKeys = 8;  // keys kept per request for the pending probes
 
 typedef int v4i __attribute__((ext_vector_type(4), aligned(4)));
 
@@ -54,127 +77,652 @@ __device__ __forceinline__ void nh_block2(const int32_t* p, const uint32_t* k1, 
 struct HashArgs {
     const int32_t* tokens;
     const int64_t* offsets;
-    uint64_t n;             // batch size (key_out holds 2n keys)
-    uint64_t r0, r1;        // requests of this launch
+    uint64_t n;               // batch size (key_out, cand and match hold 2n entries)
     const HashParams* hp;
     uint32_t key_blocks;
-    const uint64_t* bstart;  // [n+1]
-    const uint32_t* bad;     // offsets break the batch's rule (set by the block-start scan)
-    uint64_t* hkeys;         // [bstart[n]] f1 block keys
-    uint64_t* key_out;       // [2n]
+    uint32_t write_keys;      // members: store the block keys as well
+    const uint64_t* bstart;   // [n + 1] where each request's block keys go
+    const uint32_t* bad;      // offsets break the batch's rule (set by the block-start scan)
+    uint64_t* hkeys;          // f1 block keys
+    uint64_t* key_out;        // prefix: [2n] ring keys
+    GroupView gv;
+    const uint32_t* cand;     // [2n]
+    uint32_t* match;          // [2n]
+    const uint64_t* tables;
+    uint32_t log2slots;
     uint32_t* status;
+    // members pass
+    const struct MemberRec* rec;  // [n]
+    uint64_t* pkeys;              // [n * kPendKeys]
+    uint64_t* pend;               // [n]
+    const uint64_t* resume;       // resume list
+    const unsigned long long* resume_count;
 };
 
+// Index of this wave in the grid, in a scalar register: the compiler cannot
+// see that threadIdx.x / 64 is the same for the whole wave, and everything
+// derived from a vector index (a request's record, its offsets) would take
+// vector loads and vector registers.
+__device__ __forceinline__ uint64_t wave_index()
+{
+    const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    return (uint64_t)blockIdx.x * (blockDim.x >> 6) + w;
+}
+
+// First block absent from table tab among this chunk's blocks [pb, hi)
+// (cb <= pb, hi <= cb + 64), lanes pb and pb + 1 first and the rest only if
+// both are present.  Returns false when every probed block is present.
+__device__ __forceinline__ bool chunk_first_absent(const uint64_t* tab, uint32_t ls, uint64_t ck,
+                                                   uint64_t cb, uint64_t pb, uint64_t hi, int lane,
+                                                   uint64_t* first)
+{
+    const uint64_t b = cb + lane;
+    const bool in_a = b >= pb && b < pb + 2 && b < hi;
+    uint64_t m = ballot(in_a && !table_has(tab, ls, ck));
+    if (!m && pb + 2 < hi) {
+        const bool in_b = b >= pb + 2 && b < hi;
+        m = ballot(in_b && !table_has(tab, ls, ck));
+    }
+    if (!m)
+        return false;
+    *first = cb + (uint64_t)__builtin_ctzll(m);
+    return true;
+}
+
+// Ring keys of every request: lane group of g = 2^k >= K lanes per request
+// (64 / g requests per wave), lane j of a group holding block j.  The ring
+// key is block K_r - 1's, K_r = min(K, full blocks): with the chain's
+// closed form H[K_r - 1] = P^K_r (H[-1] + sum_{j<K_r} NH(j) Q^(j+1)), a sum
+// over the group's lanes (xor shuffles) replaces the scan.
 template <int B>
-__global__ __launch_bounds__(kHashThreads) void hash_kernel(HashArgs a)
+__global__ __launch_bounds__(kHashThreads) void ring_key_kernel(HashArgs a, uint32_t glog)
 {
     const int lane = lane_id();
-    const uint64_t gw = ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const uint32_t g = 1u << glog, j = (uint32_t)lane & (g - 1);
+    const uint64_t gw = wave_index();
     const uint64_t nw = ((uint64_t)gridDim.x * blockDim.x) >> 6;
+    const uint64_t per_wave = kWave >> glog;
     const HashParams* hp = a.hp;
     const uint64_t seed1 = hp->seed[0], seed2 = hp->seed[1];
     const uint64_t H01 = hp->H0[0], H02 = hp->H0[1];
-    const uint64_t q1 = hp->qpow[0][lane], p1 = hp->ppow[0][lane], q2 = hp->qpow[1][lane];
-    // Malformed offsets (reported by the block-start scan): ring keys 0, no
-    // block key.  No store precedes the parameter loads, so they stay scalar.
+    const uint64_t q1 = hp->qpow[0][j], q2 = hp->qpow[1][j];
     const bool bad = *a.bad != 0;
     uint32_t k1[B], k2[B];
 #pragma unroll
-    for (int j = 0; j < B; j++) {
-        k1[j] = hp->kk[0][j];
-        k2[j] = hp->kk[1][j];
+    for (int t = 0; t < B; t++) {
+        k1[t] = hp->kk[0][t];
+        k2[t] = hp->kk[1][t];
     }
-    // The next request's offsets and block start are fetched while this one
-    // is hashed, so no wave waits on them between requests.
-    int64_t o0 = 0, o1 = 0;
-    uint64_t bs = 0;
-    if (a.r0 + gw < a.r1) {
-        o0 = a.offsets[a.r0 + gw];
-        o1 = a.offsets[a.r0 + gw + 1];
-        bs = a.bstart[a.r0 + gw];
-    }
-    for (uint64_t r = a.r0 + gw; r < a.r1; r += nw) {
-        const uint64_t rn = r + nw;
-        int64_t no0 = 0, no1 = 0;
-        uint64_t nbs = 0;
-        if (rn < a.r1) {
-            no0 = a.offsets[rn];
-            no1 = a.offsets[rn + 1];
-            nbs = a.bstart[rn];
+    for (uint64_t base = gw * per_wave; base < a.n; base += nw * per_wave) {
+        const uint64_t r = base + ((uint32_t)lane >> glog);
+        uint32_t kr = 0;
+        int64_t o0 = 0;
+        if (r < a.n && !bad) {
+            o0 = a.offsets[r];
+            const uint64_t nfull = (uint64_t)(a.offsets[r + 1] - o0) / B;
+            kr = (uint32_t)(nfull < a.key_blocks ? nfull : a.key_blocks);
         }
-        const int64_t len = o1 - o0;
-        if (bad) {
-            if (lane == 0) {
-                a.key_out[r] = 0;
-                a.key_out[a.n + r] = 0;
+        uint64_t nh1 = 0, nh2 = 0;
+        if (j < kr)
+            nh_block2<B>(a.tokens + o0 + (uint64_t)j * B, k1, k2, nh1, nh2);
+        uint64_t s1 = nh1 * q1, s2 = nh2 * q2;
+        for (uint32_t d = 1; d < g; d <<= 1) {
+            s1 += shfl_xor_u64(s1, (int)d);
+            s2 += shfl_xor_u64(s2, (int)d);
+        }
+        if (r < a.n && j == 0) {
+            uint64_t x1 = mix64(H01 ^ seed1), x2 = mix64(H02 ^ seed2);  // empty-prefix keys
+            if (kr > 0) {
+                x1 = mix64(((H01 + s1) * hp->ppow[0][kr - 1]) ^ seed1);
+                x2 = mix64(((H02 + s2) * hp->ppow[1][kr - 1]) ^ seed2);
             }
-            o0 = no0;
-            o1 = no1;
-            bs = nbs;
-            continue;
+            a.key_out[r] = bad ? 0 : x1;
+            a.key_out[a.n + r] = bad ? 0 : x2;
         }
-        const uint64_t nfull = (uint64_t)len / B;
-        const uint32_t kr = (uint32_t)(nfull < a.key_blocks ? nfull : a.key_blocks);
+    }
+}
+
+// Walk of whole chains with probes from the chain's chunks (leaders, and
+// the rare requests whose pending probes ran past the keys the members pass
+// kept): the full f1 chain, each chunk's keys probed against the
+// candidates still unresolved, from each one's start block.
+//   kLeaders  unit g: group g's leader, both candidates from block 0, keys
+//             stored (members compare with them), until both are resolved;
+//   kResume   unit i: entry i of the resume list, one candidate from its
+//             start block, nothing stored.
+template <int B, int MODE>
+__global__ __launch_bounds__(kHashThreads) void walk_kernel(HashArgs a)
+{
+    const int lane = lane_id();
+    const uint64_t gw = wave_index();
+    const uint64_t nw = ((uint64_t)gridDim.x * blockDim.x) >> 6;
+    const HashParams* hp = a.hp;
+    const uint64_t seed1 = hp->seed[0];
+    const uint64_t H01 = hp->H0[0];
+    const uint64_t q1 = hp->qpow[0][lane], p1 = hp->ppow[0][lane];
+    // Malformed offsets (reported by the block-start scan): no full block
+    // anywhere.  No store precedes the parameter loads, so they stay scalar.
+    const bool bad = *a.bad != 0;
+    uint32_t k1[B];
+#pragma unroll
+    for (int j = 0; j < B; j++)
+        k1[j] = hp->kk[0][j];
+    const uint32_t ls = a.log2slots;
+    const uint64_t units = MODE == kLeaders ? *a.gv.groups : *a.resume_count;
+    for (uint64_t u = gw; u < units; u += nw) {
+        uint32_t r;
+        bool pend0 = true, pend1 = true;
+        uint64_t pb0 = 0, pb1 = 0;
+        if (MODE == kLeaders) {
+            r = a.gv.leader[u];
+        } else {
+            const uint64_t e = a.resume[u];
+            r = (uint32_t)e;
+            const bool side1 = (e >> 32) & 1;
+            pend0 = !side1;
+            pend1 = side1;
+            pb0 = pb1 = e >> 33;
+        }
+        const int64_t o0 = a.offsets[r], o1 = a.offsets[(uint64_t)r + 1];
+        uint64_t nfull = bad ? 0 : (uint64_t)(o1 - o0) / B;
+        if (nfull > 0xFFFFFFFFull) {
+            // match lengths are 32-bit
+            if (lane == 0)
+                atomicOr(a.status, kErrInval);
+            nfull = 0;
+        }
         const int32_t* tp = a.tokens + o0;
-        uint64_t* hk = a.hkeys + bs;
-        uint64_t x1 = mix64(H01 ^ seed1), x2 = mix64(H02 ^ seed2);  // empty-prefix keys
+        const uint64_t* t0 = a.tables + ((uint64_t)a.cand[r] << ls);
+        const uint64_t* t1 = a.tables + ((uint64_t)a.cand[a.n + r] << ls);
+        uint64_t* hk = a.hkeys + a.bstart[r];
+        // a candidate still probing at the end has every block present
+        pend0 = pend0 && pb0 < nfull;
+        pend1 = pend1 && pb1 < nfull;
+        uint64_t m0 = nfull, m1 = nfull;
         uint64_t G = H01;
         for (uint64_t cb = 0; cb < nfull; cb += kWave) {
             const uint64_t b = cb + lane;
             const bool valid = b < nfull;
-            uint64_t nh1 = 0, nh2 = 0;
-            if (cb == 0) {
-                if (valid)
-                    nh_block2<B>(tp + b * B, k1, k2, nh1, nh2);
-            } else if (valid) {
-                nh1 = nh_block<B>(tp + b * B, k1);
-            }
+            const uint64_t nh1 = valid ? nh_block<B>(tp + b * B, k1) : 0;
             const uint64_t S = wave_incl_sum_u64(nh1 * q1, lane);
             const uint64_t H = (G + S) * p1;
             const uint64_t h = mix64(H ^ seed1);
-            if (valid)
+            if (MODE == kLeaders && valid)
                 hk[b] = h;
             G = readlane_u64(H, kWave - 1);
-            if (cb == 0) {
-                x1 = readlane_u64(h, (int)kr - 1);
-                const uint64_t S2 = wave_sum_u64(lane < (int)kr ? nh2 * q2 : 0);
-                x2 = mix64(((H02 + S2) * hp->ppow[1][kr - 1]) ^ seed2);
+            const uint64_t hi = nfull < cb + kWave ? nfull : cb + kWave;
+            const uint64_t ck = canon_key(h);
+            uint64_t f = 0;
+            if (pend0 && pb0 < hi) {
+                if (chunk_first_absent(t0, ls, ck, cb, pb0, hi, lane, &f)) {
+                    m0 = f;
+                    pend0 = false;
+                } else {
+                    pb0 = hi;
+                }
             }
+            if (pend1 && pb1 < hi) {
+                if (chunk_first_absent(t1, ls, ck, cb, pb1, hi, lane, &f)) {
+                    m1 = f;
+                    pend1 = false;
+                } else {
+                    pb1 = hi;
+                }
+            }
+            // Both candidates resolved: a resumed walk is done; a leader's
+            // keys are stored up to here, past one block beyond its longer
+            // match (as far as its members compare), and the members pass
+            // hashes the rest of its prompt.
+            if (!pend0 && !pend1)
+                break;
         }
         if (lane == 0) {
-            a.key_out[r] = x1;
-            a.key_out[a.n + r] = x2;
+            if (MODE == kLeaders) {
+                a.match[r] = (uint32_t)m0;
+                a.match[a.n + r] = (uint32_t)m1;
+            } else if ((a.resume[u] >> 32) & 1) {
+                a.match[a.n + r] = (uint32_t)m1;
+            } else {
+                a.match[r] = (uint32_t)m0;
+            }
         }
-        o0 = no0;
-        o1 = no1;
-        bs = nbs;
     }
 }
 
-template <int B>
-void launch_hash(const HashArgs& a, uint32_t grid, hipStream_t s)
+// Per-request record of the members pass (48 bytes, read with one scalar
+// load): where the prompt and its keys are, the leader's keys, how far to
+// compare and the leader's matches.  lim == kLeaderMark marks a leader.
+struct alignas(16) MemberRec {
+    int64_t o0;          // prompt start
+    uint64_t bs;         // own block keys (when stored)
+    uint64_t bs_lead;    // the leader's block keys
+    uint32_t nfull;      // full blocks
+    uint32_t lim;        // blocks compared with the leader
+    uint32_t m_lead[2];  // the leader's matches
+    uint32_t pad[2];
+};
+constexpr uint32_t kLeaderMark = 0xFFFFFFFFu;
+
+__global__ void member_record_kernel(const int64_t* __restrict__ offsets, uint64_t n,
+                                     uint32_t bshift, const uint64_t* __restrict__ bstart,
+                                     const uint32_t* bad_p, GroupView gv,
+                                     const uint32_t* __restrict__ cand,
+                                     const uint32_t* __restrict__ match,
+                                     MemberRec* __restrict__ rec,
+                                     unsigned long long* __restrict__ resume_count)
 {
-    hash_kernel<B><<<grid, kHashThreads, 0, s>>>(a);
+    const bool bad = *bad_p != 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0)
+        *resume_count = 0;
+    for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
+         r += (uint64_t)gridDim.x * blockDim.x) {
+        const uint32_t L = gv.leader[gv.group_of[r]];
+        MemberRec m{};
+        m.o0 = offsets[r];
+        m.bs = bstart[r];
+        uint64_t nr = bad ? 0 : (uint64_t)(offsets[r + 1] - m.o0) >> bshift;
+        nr = nr > 0xFFFFFFFFull ? 0 : nr;  // reported by the leaders' walk kernel if a leader
+        m.nfull = (uint32_t)nr;
+        if (L == r) {
+            m.lim = kLeaderMark;
+        } else {
+            uint64_t nl = bad ? 0 : (uint64_t)(offsets[(uint64_t)L + 1] - offsets[L]) >> bshift;
+            nl = nl > 0xFFFFFFFFull ? 0 : nl;
+            m.bs_lead = bstart[L];
+            m.m_lead[0] = match[L];
+            m.m_lead[1] = match[n + L];
+            const uint64_t M = m.m_lead[0] > m.m_lead[1] ? m.m_lead[0] : m.m_lead[1];
+            uint64_t lim = M + 1 < nr ? M + 1 : nr;
+            lim = lim < nl ? lim : nl;
+            // the leader's matches are on its candidates: a request whose
+            // candidates differ (only on a ring-key collision) is probed on
+            // its own from block 0
+            if (cand[r] != cand[L] || cand[n + r] != cand[n + L])
+                lim = 0;
+            m.lim = (uint32_t)lim;
+        }
+        rec[r] = m;
+    }
+}
+
+// Tokens of one chunk, lane l holding block l's B tokens as B/4 16-byte
+// words (loaded a chunk ahead of their use by the members pass).
+template <int B>
+struct ChunkTokens {
+    v4i t[B / 4];
+};
+
+template <int B>
+__device__ __forceinline__ void load_chunk(ChunkTokens<B>& c, const int32_t* tp, uint64_t b,
+                                           bool valid)
+{
+#pragma unroll
+    for (int j = 0; j < B / 4; j++)
+        c.t[j] = valid ? *reinterpret_cast<const v4i*>(tp + b * B + 4 * j) : v4i{0, 0, 0, 0};
+}
+
+// NH of a block held in registers, with key words kk.
+template <int B>
+__device__ __forceinline__ uint64_t nh_regs(const ChunkTokens<B>& c, const uint32_t* kk)
+{
+    uint64_t acc = 0;
+#pragma unroll
+    for (int j = 0; j < B / 4; j++) {
+        const v4i v = c.t[j];
+        acc += (uint64_t)((uint32_t)v.x + kk[4 * j]) * (uint32_t)((uint32_t)v.y + kk[4 * j + 1]);
+        acc += (uint64_t)((uint32_t)v.z + kk[4 * j + 2]) * (uint32_t)((uint32_t)v.w + kk[4 * j + 3]);
+    }
+    return acc;
+}
+
+// A member record in registers (three 16-byte loads issued together).
+struct RecRegs {
+    int64_t o0;
+    uint64_t bs, bs_lead;
+    uint32_t nfull, lim, m_lead0, m_lead1;
+};
+
+__device__ __forceinline__ RecRegs load_rec(const MemberRec* rec, uint64_t r)
+{
+    typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+    const u4* p = reinterpret_cast<const u4*>(rec + r);
+    const u4 x = p[0], y = p[1], z = p[2];
+    RecRegs m;
+    m.o0 = (int64_t)(((uint64_t)x.y << 32) | x.x);
+    m.bs = ((uint64_t)x.w << 32) | x.z;
+    m.bs_lead = ((uint64_t)y.y << 32) | y.x;
+    m.nfull = y.z;
+    m.lim = y.w;
+    m.m_lead0 = z.x;
+    m.m_lead1 = z.y;
+    return m;
+}
+
+// Blocks of a record compared with its leader (none for a leader itself).
+__device__ __forceinline__ uint32_t cmp_lim(const RecRegs& m)
+{
+    return m.lim == kLeaderMark ? 0u : m.lim;
+}
+
+// Every request's full f1 chain (stored when the caller asks for block
+// keys).  A request that is not a leader is compared chunk by chunk with its
+// leader's keys over blocks [0, lim) (one ballot per chunk) to find the
+// first disagreement s.  Per candidate, the leader's match where it ends
+// before s, the request's length where s reaches it, or pending: the
+// request's keys of blocks [s, s + 8) are kept in pkeys (8 per request) and
+// pend[r] = s | side mask << 32 for probe_pending_kernel.  Probing is left
+// out of this pass: its latency would hold the wave with no tokens in
+// flight.
+//
+// A wave keeps one chunk's loads in flight while it hashes the chunk
+// before: the next chunk's tokens and leader keys, or, on a request's last
+// chunk, the next request's first chunk (its record is loaded a request
+// ahead), when a wave has more than one request.  (Persistent waves claiming
+// blocks of requests through per-XCD counters were measured 13% slower.)
+template <int B>
+__global__ __launch_bounds__(kHashThreads) void member_kernel(HashArgs a)
+{
+    const int lane = lane_id();
+    const HashParams* hp = a.hp;
+    const uint64_t seed1 = hp->seed[0];
+    const uint64_t H01 = hp->H0[0];
+    const uint64_t q1 = hp->qpow[0][lane], p1 = hp->ppow[0][lane];
+    uint32_t k1[B];
+#pragma unroll
+    for (int j = 0; j < B; j++)
+        k1[j] = hp->kk[0][j];
+    // requests of this wave: its index, then every grid's worth of waves on
+    // (one request per wave unless the batch has more than 4 Mi requests)
+    const uint64_t nw = ((uint64_t)gridDim.x * blockDim.x) >> 6;
+    uint64_t r = wave_index();
+    bool have = r < a.n;
+    RecRegs cur{};
+    if (have)
+        cur = load_rec(a.rec, r);
+    ChunkTokens<B> nx;
+    uint64_t nlk = 0;
+    {
+        const bool v = have && (uint64_t)lane < cur.nfull;
+        load_chunk<B>(nx, a.tokens + cur.o0, (uint64_t)lane, v);
+        nlk = have && (uint32_t)lane < cmp_lim(cur) ? a.hkeys[cur.bs_lead + lane] : 0;
+    }
+    while (have) {
+        // this request, then the wave's next one and its record
+        const uint64_t rc = r, rn = r + nw;
+        const bool have_n = rn < a.n;
+        RecRegs nxt{};
+        if (have_n)
+            nxt = load_rec(a.rec, rn);
+        const bool lead = cur.lim == kLeaderMark;
+        const uint64_t nfull = cur.nfull, lim = cmp_lim(cur);
+        const int32_t* tp = a.tokens + cur.o0;
+        const uint64_t* lk = a.hkeys + cur.bs_lead;
+        uint64_t* hk = a.hkeys + cur.bs;
+        uint64_t* pk = a.pkeys + rc * kPendKeys;
+        bool cmp = lim > 0;
+        // s = 0 when there is nothing to compare
+        uint64_t s = 0, emit_lo = 0, emit_hi = 0;
+        uint32_t mask = 0;  // candidates left to probe
+        uint32_t m0 = (uint32_t)nfull, m1 = (uint32_t)nfull;
+        auto resolve = [&](uint64_t s_) {
+            s = s_;
+            if (cur.m_lead0 < s)
+                m0 = cur.m_lead0;
+            else if (s < nfull)
+                mask |= 1;
+            if (cur.m_lead1 < s)
+                m1 = cur.m_lead1;
+            else if (s < nfull)
+                mask |= 2;
+            emit_lo = s;
+            emit_hi = mask ? (s + kPendKeys < nfull ? s + kPendKeys : nfull) : s;
+        };
+        if (!cmp && !lead)
+            resolve(0);
+        uint64_t G = H01;
+        for (uint64_t cb = 0; cb < nfull; cb += kWave) {
+            const uint64_t b = cb + lane;
+            const bool valid = b < nfull;
+            const ChunkTokens<B> tc = nx;
+            const uint64_t lkey = nlk;
+            // loads of the following chunk go out before this one is hashed
+            const uint64_t b2 = b + kWave;
+            if (cb + kWave < nfull) {
+                load_chunk<B>(nx, tp, b2, b2 < nfull);
+                nlk = cmp && b2 < lim ? lk[b2] : 0;
+            } else if (have_n) {
+                load_chunk<B>(nx, a.tokens + nxt.o0, (uint64_t)lane, (uint64_t)lane < nxt.nfull);
+                nlk = (uint32_t)lane < cmp_lim(nxt) ? a.hkeys[nxt.bs_lead + lane] : 0;
+            }
+            const uint64_t nh1 = valid ? nh_regs<B>(tc, k1) : 0;
+            const uint64_t S = wave_incl_sum_u64(nh1 * q1, lane);
+            const uint64_t H = (G + S) * p1;
+            const uint64_t h = mix64(H ^ seed1);
+            if (a.write_keys && valid)
+                hk[b] = h;
+            G = readlane_u64(H, kWave - 1);
+            if (cmp) {
+                const bool in = b < lim;
+                const uint64_t diff = ballot(in && lkey != h);
+                if (diff) {
+                    cmp = false;
+                    resolve(cb + (uint64_t)__builtin_ctzll(diff));
+                } else if (cb + kWave >= lim) {
+                    cmp = false;
+                    resolve(lim);
+                }
+            }
+            if (!cmp && b >= emit_lo && b < emit_hi)
+                pk[b - emit_lo] = h;
+        }
+        if (nfull == 0 && have_n) {
+            // nothing of the next request was loaded ahead yet
+            load_chunk<B>(nx, a.tokens + nxt.o0, (uint64_t)lane, (uint64_t)lane < nxt.nfull);
+            nlk = (uint32_t)lane < cmp_lim(nxt) ? a.hkeys[nxt.bs_lead + lane] : 0;
+        }
+        if (lane == 0 && !lead) {
+            a.match[rc] = m0;
+            a.match[a.n + rc] = m1;
+            a.pend[rc] = s | ((uint64_t)mask << 32);
+        }
+        r = rn;
+        cur = nxt;
+        have = have_n;
+    }
+}
+
+// Pending candidates of the members pass, one thread per request: probe
+// its kept keys of blocks [s, s + 8) in order up to the first absent one.
+// If all are present and blocks remain, the (request, candidate) goes to
+// the resume list (walked again from block s + 8 by walk_kernel<kResume>).
+__global__ void probe_pending_kernel(uint64_t n, const uint64_t* __restrict__ pend,
+                                     const MemberRec* __restrict__ rec,
+                                     const uint64_t* __restrict__ pkeys,
+                                     const uint32_t* __restrict__ cand,
+                                     const uint64_t* __restrict__ tables, uint32_t ls,
+                                     uint32_t* __restrict__ match, uint64_t* __restrict__ resume,
+                                     unsigned long long* __restrict__ resume_count)
+{
+    for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
+         r += (uint64_t)gridDim.x * blockDim.x) {
+        if (rec[r].lim == kLeaderMark)
+            continue;
+        const uint64_t p = pend[r];
+        const uint32_t mask = (uint32_t)(p >> 32);
+        if (!mask)
+            continue;
+        const uint64_t s = (uint32_t)p, nfull = rec[r].nfull;
+        const uint64_t k_end = s + kPendKeys < nfull ? s + kPendKeys : nfull;
+        for (int side = 0; side < 2; side++) {
+            if (!(mask & (1u << side)))
+                continue;
+            const uint64_t* tab = tables + ((uint64_t)cand[side * n + r] << ls);
+            uint64_t b = s;
+            while (b < k_end && table_has(tab, ls, canon_key(pkeys[r * kPendKeys + (b - s)])))
+                b++;
+            if (b < k_end || b == nfull) {
+                match[side * n + r] = (uint32_t)b;
+            } else {
+                const unsigned long long at = atomicAdd(resume_count, 1ull);
+                resume[at] = (uint64_t)r | ((uint64_t)side << 32) | (b << 33);
+            }
+        }
+    }
+}
+
+template <int MODE>
+hipError_t launch_walk(dm_ctx* c, const HashArgs& a, uint32_t grid)
+{
+    switch (c->cfg.block_size) {
+        case 4: walk_kernel<4, MODE><<<grid, kHashThreads, 0, c->stream>>>(a); break;
+        case 8: walk_kernel<8, MODE><<<grid, kHashThreads, 0, c->stream>>>(a); break;
+        case 16: walk_kernel<16, MODE><<<grid, kHashThreads, 0, c->stream>>>(a); break;
+        case 32: walk_kernel<32, MODE><<<grid, kHashThreads, 0, c->stream>>>(a); break;
+        case 64: walk_kernel<64, MODE><<<grid, kHashThreads, 0, c->stream>>>(a); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <int B>
+hipError_t launch_members_b(dm_ctx* c, const HashArgs& a)
+{
+    member_kernel<B><<<grid_for(a.n, kHashThreads / kWave, kHashBlocks), kHashThreads, 0,
+                       c->stream>>>(a);
+    return hipGetLastError();
+}
+
+hipError_t launch_members(dm_ctx* c, const HashArgs& a)
+{
+    switch (c->cfg.block_size) {
+        case 4: return launch_members_b<4>(c, a);
+        case 8: return launch_members_b<8>(c, a);
+        case 16: return launch_members_b<16>(c, a);
+        case 32: return launch_members_b<32>(c, a);
+        case 64: return launch_members_b<64>(c, a);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+HashArgs base_args(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                   const uint32_t* bad)
+{
+    HashArgs a{};
+    a.tokens = tokens;
+    a.offsets = offsets;
+    a.n = n;
+    a.hp = c->d_hp;
+    a.key_blocks = c->cfg.key_blocks;
+    a.bad = bad;
+    a.tables = c->d_tables;
+    a.log2slots = c->cfg.index_log2_slots;
+    a.status = c->d_status;
+    return a;
+}
+
+// Work arrays of the members pass for n requests, in layout order: records,
+// kept keys, pending words, the resume list (two entries per request at
+// most) and its count.
+struct MemberWork {
+    MemberRec* rec;
+    uint64_t *pkeys, *pend, *resume;
+    unsigned long long* resume_count;
+};
+
+size_t up256m(size_t x) { return (x + 255) & ~size_t(255); }
+
+size_t member_layout(uint64_t n, uint8_t* w, MemberWork* mw)
+{
+    const size_t sz[] = {up256m(n * sizeof(MemberRec)), up256m(n * kPendKeys * 8), up256m(8 * n),
+                         up256m(16 * n), 256};
+    size_t at[5], off = 0;
+    for (int i = 0; i < 5; i++) {
+        at[i] = off;
+        off += sz[i];
+    }
+    if (mw) {
+        mw->rec = reinterpret_cast<MemberRec*>(w + at[0]);
+        mw->pkeys = reinterpret_cast<uint64_t*>(w + at[1]);
+        mw->pend = reinterpret_cast<uint64_t*>(w + at[2]);
+        mw->resume = reinterpret_cast<uint64_t*>(w + at[3]);
+        mw->resume_count = reinterpret_cast<unsigned long long*>(w + at[4]);
+    }
+    return off;
 }
 
 }  // namespace
 
-hipError_t hash_blocks(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                       const uint64_t* bstart, const uint32_t* bad, uint64_t* hkeys,
-                       uint64_t* key_out, uint64_t r0, uint64_t r1)
+hipError_t hash_prefix(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                       const uint32_t* bad, uint64_t* key_out)
 {
-    HashArgs ha{tokens, offsets, n,     r0,      r1,        c->d_hp,
-                c->cfg.key_blocks, bstart, bad, hkeys, key_out, c->d_status};
-    const uint32_t grid = grid_for(r1 > r0 ? r1 - r0 : 0, kHashThreads / kWave, kHashBlocks);
+    HashArgs a = base_args(c, tokens, offsets, n, bad);
+    a.key_out = key_out;
+    uint32_t glog = 0;
+    while ((1u << glog) < c->cfg.key_blocks)
+        glog++;
+    const uint64_t waves = (n + (kWave >> glog) - 1) / (kWave >> glog);
+    const uint32_t grid = grid_for(waves, kHashThreads / kWave, kHashBlocks);
     switch (c->cfg.block_size) {
-        case 4: launch_hash<4>(ha, grid, c->stream); break;
-        case 8: launch_hash<8>(ha, grid, c->stream); break;
-        case 16: launch_hash<16>(ha, grid, c->stream); break;
-        case 32: launch_hash<32>(ha, grid, c->stream); break;
-        case 64: launch_hash<64>(ha, grid, c->stream); break;
+        case 4: ring_key_kernel<4><<<grid, kHashThreads, 0, c->stream>>>(a, glog); break;
+        case 8: ring_key_kernel<8><<<grid, kHashThreads, 0, c->stream>>>(a, glog); break;
+        case 16: ring_key_kernel<16><<<grid, kHashThreads, 0, c->stream>>>(a, glog); break;
+        case 32: ring_key_kernel<32><<<grid, kHashThreads, 0, c->stream>>>(a, glog); break;
+        case 64: ring_key_kernel<64><<<grid, kHashThreads, 0, c->stream>>>(a, glog); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+hipError_t hash_leaders(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                        const uint64_t* bstart, const uint32_t* bad, const GroupView& gv,
+                        const uint32_t* cand, uint64_t* hkeys, uint32_t* match)
+{
+    HashArgs a = base_args(c, tokens, offsets, n, bad);
+    a.bstart = bstart;
+    a.hkeys = hkeys;
+    a.gv = gv;
+    a.cand = cand;
+    a.match = match;
+    // the group count is on the device: a bounded grid strides over it
+    return launch_walk<kLeaders>(c, a, grid_for(n, kHashThreads / kWave, kLeaderBlocks));
+}
+
+uint64_t member_scratch_bytes(uint64_t n) { return member_layout(n, nullptr, nullptr); }
+
+hipError_t hash_members(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                        const uint64_t* bstart, const uint32_t* bad, const GroupView& gv,
+                        const uint32_t* cand, uint64_t* hkeys, bool write_keys, uint32_t* match)
+{
+    hipError_t e = hipSuccess;
+    uint8_t* w = static_cast<uint8_t*>(scratch_get(c, kSlotMembers, member_scratch_bytes(n), &e));
+    if (!w)
+        return e;
+    MemberWork mw;
+    member_layout(n, w, &mw);
+    uint32_t bshift = 0;
+    while ((1u << bshift) < c->cfg.block_size)
+        bshift++;
+    member_record_kernel<<<grid_for(n, 256, 8192), 256, 0, c->stream>>>(
+        offsets, n, bshift, bstart, bad, gv, cand, match, mw.rec, mw.resume_count);
+    HashArgs a = base_args(c, tokens, offsets, n, bad);
+    a.bstart = bstart;
+    a.hkeys = hkeys;
+    a.write_keys = write_keys ? 1u : 0u;
+    a.gv = gv;
+    a.cand = cand;
+    a.match = match;
+    a.rec = mw.rec;
+    a.pkeys = mw.pkeys;
+    a.pend = mw.pend;
+    a.resume = mw.resume;
+    a.resume_count = mw.resume_count;
+    if ((e = launch_members(c, a)) != hipSuccess)
+        return e;
+    probe_pending_kernel<<<grid_for(n, 256, 8192), 256, 0, c->stream>>>(
+        n, mw.pend, mw.rec, mw.pkeys, cand, c->d_tables, c->cfg.index_log2_slots, match,
+        mw.resume, mw.resume_count);
+    // the rare (request, candidate) whose kept keys were all present
+    return launch_walk<kResume>(c, a, grid_for(2 * n, kHashThreads / kWave, kLeaderBlocks));
 }
 
 }  // namespace dm

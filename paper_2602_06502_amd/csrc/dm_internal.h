@@ -13,12 +13,13 @@
 namespace dm {
 
 constexpr int kWave = 64;
-constexpr int kScratchSlots = 9;  // context work buffers, one per use
-// Scratch slots.  Routing uses starts, probe, select, keys, sort and scan;
+constexpr int kScratchSlots = 10;  // context work buffers, one per use
+// Scratch slots.  Routing uses starts, probe, select, keys, sort, scan and
+// members;
 // a rebalancing pass reuses probe, rebalance and select (it runs after the
 // batches before it have finished).
 constexpr int kSlotStarts = 0, kSlotProbe = 1, kSlotRebalance = 2, kSlotSelect = 3, kSlotKeys = 4,
-              kSlotRing = 5, kSlotSort = 6, kSlotScan = 7, kSlotPurge = 8;
+              kSlotRing = 5, kSlotSort = 6, kSlotScan = 7, kSlotPurge = 8, kSlotMembers = 9;
 constexpr uint32_t kMaxSlots = 4096;
 constexpr uint64_t kEmpty = 0;      // index slot never used
 constexpr uint64_t kTomb = 1;       // index slot erased
@@ -90,7 +91,6 @@ struct dm_ctx {
     hipStream_t home_stream = nullptr;  // the stream given to dm_create
     int device = 0;
     int n_cu = 0;           // compute units of the device
-    uint32_t probe_grid = 0;  // resident workgroups of the probe kernel (set on first use)
     std::string err;
 
     // live set (host) and cyclic next-live table (device)
@@ -186,6 +186,7 @@ uint64_t scan_scratch_bytes(uint64_t n);
 uint64_t sort_scratch_bytes(uint64_t n);
 uint64_t sort_scan_len(uint64_t n);  // length of the sort's digit-count scans
 uint64_t probe_scratch_bytes(uint64_t n);
+uint64_t member_scratch_bytes(uint64_t n);
 uint64_t select_scratch_bytes(uint64_t n);
 // Per-slot scratch of one unpipelined dm_route_batch (bytes[kScratchSlots]).
 void route_scratch_plan(const dm_ctx* c, uint64_t n, uint64_t n_tokens, bool keys_in_scratch,
@@ -222,20 +223,37 @@ hipError_t index_insert(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n
 hipError_t index_erase(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n);
 hipError_t index_clear(dm_ctx* c, uint32_t id);
 
-// dm_hash.hip: block keys of every full block (hkeys at bstart[r]) and the
-// two ring keys of every request (key_out[r], key_out[n + r]) for the
-// requests r in [r0, r1) of a batch of n; with *bad set, ring keys 0 and no
-// block key.
-hipError_t hash_blocks(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                       const uint64_t* bstart, const uint32_t* bad, uint64_t* hkeys,
-                       uint64_t* key_out, uint64_t r0, uint64_t r1);
+// Requests grouped by equal ring keys (dm_probe.hip): group_of[r] is
+// request r's group, leader[g] is group g's leader request, *groups = G.
+struct GroupView {
+    const uint32_t* group_of;
+    const uint32_t* leader;
+    const uint64_t* groups;
+};
 
-// dm_probe.hip: candidates on the current rings (cand, fix-up flag bit 3)
-// and the longest cached prefix on each (match), for the requests r in
-// [r0, r1) of a batch of n; with *bad set, every match is 0.
-hipError_t lookup_probe(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64_t* hkeys,
-                        const uint64_t* bstart, const uint32_t* bad, uint32_t* cand,
-                        uint32_t* match, uint8_t* flags, uint64_t r0, uint64_t r1);
+// dm_hash.hip.  With *bad set (malformed offsets) every request has no full
+// block: ring keys 0, match 0, no block key.
+//   hash_prefix: both ring keys of every request (key_out[r], key_out[n+r]),
+//     hashing only the first min(K, full blocks) blocks;
+//   hash_leaders: every group leader's full f1 chain into hkeys (at
+//     bstart[r]) and its longest cached prefix on both candidates (match);
+//   hash_members: every other request's full f1 chain, compared with its
+//     leader's keys as it is computed, and its longest cached prefix from
+//     that comparison and probes past the first disagreement; its keys are
+//     stored into hkeys only when write_keys is set.
+hipError_t hash_prefix(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                       const uint32_t* bad, uint64_t* key_out);
+hipError_t hash_leaders(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                        const uint64_t* bstart, const uint32_t* bad, const GroupView& gv,
+                        const uint32_t* cand, uint64_t* hkeys, uint32_t* match);
+hipError_t hash_members(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                        const uint64_t* bstart, const uint32_t* bad, const GroupView& gv,
+                        const uint32_t* cand, uint64_t* hkeys, bool write_keys, uint32_t* match);
+
+// dm_probe.hip: candidates on the current rings (cand, fix-up flag bit 3),
+// then requests ordered by their first ring key and grouped (gv).
+hipError_t lookup_group(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64_t* bstart,
+                        const uint32_t* bad, uint32_t* cand, uint8_t* flags, GroupView* gv);
 
 // dm_select.hip: SLO-aware choice in request order; chosen, ttft_us and
 // flags bits 0-2 written, loads updated.  select_prepare packs the batch's
@@ -305,6 +323,14 @@ __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src)
     return ((uint64_t)hi << 32) | lo;
 }
 
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask)
+{
+    uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+    lo = __shfl_xor(lo, mask);
+    hi = __shfl_xor(hi, mask);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane)
 {
     uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, lane);
@@ -362,5 +388,46 @@ __device__ __forceinline__ uint32_t ring_owner(const RingView& r, uint64_t x)
 }
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// Index probing.  A table is 2^ls slots in 8-slot (64-byte) buckets; a
+// key's probe sequence starts at its home bucket (the key's top ls - 3
+// bits) and walks buckets in order.  An insert takes the first empty slot
+// of the sequence and slots never return to empty, so a bucket's empty
+// slots are a suffix of it: a bucket has one iff its last slot is empty,
+// and such a bucket ends the key's sequence.
+enum : int { kHit = 0, kMiss = 1, kNext = 2 };
+
+typedef unsigned long long v2u64 __attribute__((ext_vector_type(2), aligned(16)));
+
+// Home bucket of a canonical key in a 2^ls-slot table (ls <= 30).
+__device__ __forceinline__ uint32_t home32(uint64_t ck, uint32_t ls)
+{
+    return (uint32_t)(ck >> 32) >> (35 - ls);
+}
+
+// One bucket: the key is there, the bucket ends the sequence without it, or
+// go on to the next bucket.
+__device__ __forceinline__ int bucket_probe(const uint64_t* tab, uint32_t bkt, uint64_t key)
+{
+    const v2u64* line = reinterpret_cast<const v2u64*>(tab + (uint64_t)bkt * kBucket);
+    const v2u64 s0 = line[0], s1 = line[1], s2 = line[2], s3 = line[3];
+    const bool hit = s0.x == key || s0.y == key || s1.x == key || s1.y == key || s2.x == key ||
+                     s2.y == key || s3.x == key || s3.y == key;
+    return hit ? kHit : (s3.y == kEmpty ? kMiss : kNext);
+}
+
+// Is canonical key ck in the table?  Walks its probe sequence.
+__device__ __forceinline__ bool table_has(const uint64_t* tab, uint32_t ls, uint64_t ck)
+{
+    const uint32_t nbk = 1u << (ls - 3);
+    uint32_t b = home32(ck, ls);
+    for (uint32_t step = 0; step < nbk; step++) {
+        const int r = bucket_probe(tab, b, ck);
+        if (r != kNext)
+            return r == kHit;
+        b = (b + 1) & (nbk - 1);
+    }
+    return false;
+}
 
 }  // namespace dm

@@ -1,11 +1,16 @@
 // dm_route_batch: batched dual-mapping routing (Sec. 3.2; Sec. A.1.1).
 //
 //   block_starts   exclusive sum of full blocks per request: where each
-//                  request's block keys live;
-//   hash_blocks    chained block keys and both ring keys (dm_hash.hip);
-//   lookup_probe   candidates on the two rings and the longest cached prefix
-//                  on each (dm_probe.hip);
-//   select_batch   SLO-aware choice in request order, loads updated
+//                  request's block keys go; checks the offsets;
+//   hash_prefix    both ring keys from the first min(K, full blocks)
+//                  blocks (dm_hash.hip);
+//   lookup_group   candidates on the two rings, then requests ordered by
+//                  their first ring key and grouped by equal ring keys,
+//                  with a leader per group (dm_probe.hip);
+//   hash_leaders   leaders' full chains and longest cached prefixes;
+//   hash_members   every other request's full chain and longest cached
+//                  prefix, from its leader's keys and its own probes;
+//   select_*       SLO-aware choice in request order, loads updated
 //                  (dm_select.hip).
 // With timing on, events between the stages give the per-stage times that
 // dm_route_stage_ms reports.  With pipelining on, the batch's work runs on
@@ -53,7 +58,8 @@ void route_scratch_plan(const dm_ctx* c, uint64_t n, uint64_t n_tokens, bool key
     for (int i = 0; i < kScratchSlots; i++)
         bytes[i] = 0;
     bytes[kSlotStarts] = (n + 2) * sizeof(uint64_t);  // block starts, malformed-offsets word
-    bytes[kSlotProbe] = probe_scratch_bytes(n);       // request order, claim counters
+    bytes[kSlotProbe] = probe_scratch_bytes(n);       // request order and groups
+    bytes[kSlotMembers] = member_scratch_bytes(n);    // members pass records, kept keys
     bytes[kSlotSelect] = select_scratch_bytes(n);     // one set of selection work arrays
     if (keys_in_scratch)                              // block keys
         bytes[kSlotKeys] = ((n_tokens >> block_shift_of(c)) + 1) * sizeof(uint64_t);
@@ -107,13 +113,16 @@ hipError_t route(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens, const int6
     }
     if (ev && (e = hipEventRecord(ev[1], st)) != hipSuccess)
         return e;
-    if ((e = hash_blocks(c, tokens, offsets, n, bstart, bad, hkeys, out->key, 0, n)) !=
-        hipSuccess)
+    GroupView gv{};
+    if ((e = hash_prefix(c, tokens, offsets, n, bad, out->key)) != hipSuccess ||
+        (e = lookup_group(c, n, out->key, bstart, bad, out->cand, out->flags, &gv)) != hipSuccess)
         return e;
     if (ev && (e = hipEventRecord(ev[2], st)) != hipSuccess)
         return e;
-    if ((e = lookup_probe(c, n, out->key, hkeys, bstart, bad, out->cand, out->match, out->flags, 0,
-                          n)) != hipSuccess)
+    if ((e = hash_leaders(c, tokens, offsets, n, bstart, bad, gv, out->cand, hkeys, out->match)) !=
+            hipSuccess ||
+        (e = hash_members(c, tokens, offsets, n, bstart, bad, gv, out->cand, hkeys,
+                          out->block_keys != nullptr, out->match)) != hipSuccess)
         return e;
     if (ev && (e = hipEventRecord(ev[3], st)) != hipSuccess)
         return e;

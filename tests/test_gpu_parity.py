@@ -822,3 +822,58 @@ def test_pipelined_shrinking_batches_parity():
     for g, r, (lo, hi) in zip(outs, refs, zip(cuts[:-1], cuts[1:])):
         compare_route(g, r, hi - lo)
     assert np.array_equal(cpu(Ld), Lo)
+
+
+def test_group_resolution_paths_parity():
+    """Requests that share a cached prefix P (300 blocks, cached on every
+    instance) and so one ring-key group, built to reach every way a group
+    member is resolved: the leader's match (its first disagreement with
+    the leader comes after the leader's first miss), its own length
+    (a prefix of the leader), probes of its kept keys past the first
+    disagreement, and the resume walk (more than the kept keys present).
+    Every output against the oracle, with and without block keys."""
+    gh = _h()
+    B = 16
+    cfg = dict(block=B, key_blocks=4, seeds=(3, 9), vnodes=16, max_slots=8, index_log2_slots=14)
+    rng = np.random.default_rng(23)
+    P = rng.integers(0, 50_000, size=300 * B, dtype=np.int32)
+    rnd = lambda nb: rng.integers(0, 50_000, size=nb * B, dtype=np.int32)
+    prompts = [np.concatenate([P[:30 * B], rnd(20)]) for _ in range(64)]  # leader: the first
+    prompts += [
+        P[:300 * B],                                    # pending past the kept keys: resume
+        np.concatenate([P[:33 * B], rnd(5)]),           # pending: first miss among kept keys
+        P[:25 * B],                                     # own length (prefix of the leader)
+        np.concatenate([P[:30 * B], rnd(3)]),           # pending at the leader's first miss
+        np.concatenate([P[:20 * B], rnd(40)]),          # disagrees before the leader's miss
+        prompts[0].copy(),                              # the leader's own prompt: its match
+        np.concatenate([P[:300 * B], rnd(1)[:7]]),      # partial tail block
+        np.concatenate([P[:37 * B], rnd(2)]),           # first miss on the last kept key
+        np.concatenate([P[:38 * B], rnd(2)]),           # first miss just past the kept keys
+    ]
+    prompts += [rnd(int(k)) for k in rng.integers(0, 40, size=40)]  # groups of their own
+    off = np.zeros(len(prompts) + 1, np.int64)
+    off[1:] = np.cumsum([len(p) for p in prompts])
+    tok = np.concatenate(prompts).astype(np.int32)
+    o = oracle.Oracle(cfg)
+    o.build_rings(range(8))
+    eng = gh.DualMap(cfg, device="cuda:0")
+    eng.build_rings(list(range(8)))
+    pk = o.chain(0, P)
+    assert len(pk) == 300
+    for inst in range(8):
+        o.index_insert(inst, pk)
+        eng.index_insert(inst, gh.to_dev(pk, eng.device))
+    eng.sync()
+    L0 = np.arange(8, dtype=np.int64) * 1000
+    for bk in (False, True):
+        _say("group resolution paths, block keys", bk)
+        Ld = gh.to_dev(L0, eng.device)
+        g = eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld, block_keys=bk)
+        eng.sync()
+        r = o.route(tok, off, L0, block_keys=bk)
+        compare_route(g, r, len(prompts), with_bk=bk)
+        assert np.array_equal(cpu(Ld), r["loads"])
+    n = len(prompts)
+    m1 = r["match"][:n]
+    assert m1[64] == 300 and m1[65] == 33 and m1[66] == 25 and m1[67] == 30
+    assert m1[68] == 20 and m1[69] == 30 and m1[71] == 37 and m1[72] == 38

@@ -5,7 +5,9 @@ the tests, the package smoke check and the benchmark's CPU-baseline leg may
 import this module; the product path (the HIP library and its binding) never
 does, and shares no code with it.
 
-build() compiles dm_oracle.c with gcc into liboracle.so next to it.
+build() compiles dm_oracle.c with gcc into liboracle.so next to it.  A
+process that sets DM_ORACLE_LIB loads the build at that path instead (the
+sanitizer tests use it for an instrumented build of the same source).
 """
 from __future__ import annotations
 
@@ -46,9 +48,12 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build(force=False)
-        L = C.CDLL(_LIB)
+        path = os.environ.get("DM_ORACLE_LIB")
+        if not path:
+            path = _LIB
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build(force=False)
+        L = C.CDLL(path)
         P = C.c_void_p
         u64, u32, i64, i32 = C.c_uint64, C.c_uint32, C.c_int64, C.c_int
         sig = {

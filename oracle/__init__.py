@@ -80,7 +80,7 @@ def lib():
             "or_candidates": (i32, [P, u64, u64, P, P]),
             "or_select": (u32, [P, u32, u32, u64, u64, i64, P, P, P]),
             "or_route": (i32, [P, P, P, u64, P, P, P, P, P, P, P, P]),
-            "or_rebalance": (i32, [P, P, P, P, P, P, P, P, P, P, P, P, P, u64, P]),
+            "or_rebalance": (i32, [P, P, P, P, P, P, P, P, i64, P, P, P, P, P, P, u64, P]),
             "or_scale": (i32, [P, P, u32, P, u32, P, u64, P, P, P, P]),
             "or_n_live": (u32, [P]),
         }
@@ -249,8 +249,10 @@ class Oracle:
             out["block_keys"] = bk
         return out
 
-    def rebalance(self, qoff, rec_id, unc_here, alt, unc_alt, base_work, cap: Optional[int] = None):
+    def rebalance(self, qoff, rec_id, unc_here, alt, unc_alt, base_work, cap: Optional[int] = None,
+                  prefill_interval=None, decode_threshold_us: int = 3_000_000):
         qoff = np.ascontiguousarray(qoff, np.int64)
+        pint = None if prefill_interval is None else np.ascontiguousarray(prefill_interval, np.int64)
         rec_id = np.ascontiguousarray(rec_id, np.uint64)
         unc_here = np.ascontiguousarray(unc_here, np.uint32)
         alt = np.ascontiguousarray(alt, np.uint32)
@@ -264,7 +266,9 @@ class Oracle:
                  ttft_to=np.zeros(max(cap, 1), np.int64))
         cnt = C.c_uint64()
         rc = lib().or_rebalance(self._h, _p(qoff), _p(rec_id), _p(unc_here), _p(alt), _p(unc_alt),
-                                _p(base_work), _p(loads), _p(m["rec"]), _p(m["src"]), _p(m["dst"]),
+                                _p(base_work), _p(pint) if pint is not None else None,
+                                int(decode_threshold_us), _p(loads), _p(m["rec"]), _p(m["src"]),
+                                _p(m["dst"]),
                                 _p(m["benefit"]), _p(m["ttft_to"]), cap, C.byref(cnt))
         n = int(cnt.value)
         out = {k: v[:min(n, cap)] for k, v in m.items()}

@@ -648,10 +648,19 @@ static int64_t queue_max_ttft(const or_state *st, int64_t base_work, const uint3
  *    below the SLO (Sec. A.1.2); a move removes it from i's queue and adds
  *    unc_alt to j's load.  Moved records are not reconsidered.
  * loads_out[i] receives each instance's final load (base work plus its
- * queued uncached tokens plus received records). */
+ * queued uncached tokens plus received records).
+ *
+ * Decode-bottleneck correction (Sec. A.7), when prefill_interval is given:
+ * an instance with a non-empty queue whose prefill interval (time since it
+ * last completed a prefill) exceeds decode_threshold_us is taken to be
+ * stalled in decode, and every TTFT estimated on it -- its queued records',
+ * and a migrated record's as a target -- gets the interval added as the
+ * decode-delay estimate D.  Loads are unchanged.  Intervals must lie in
+ * [0, 2^40] and the threshold must not be negative. */
 int or_rebalance(const or_state *st, const int64_t *qoff, const uint64_t *rec_id,
                  const uint32_t *unc_here, const uint32_t *alt, const uint32_t *unc_alt,
-                 const int64_t *base_work, int64_t *loads_out, uint64_t *mig_rec,
+                 const int64_t *base_work, const int64_t *prefill_interval,
+                 int64_t decode_threshold_us, int64_t *loads_out, uint64_t *mig_rec,
                  uint32_t *mig_from, uint32_t *mig_to, int64_t *mig_benefit,
                  int64_t *mig_ttft_to, uint64_t cap, uint64_t *count)
 {
@@ -666,20 +675,32 @@ int or_rebalance(const or_state *st, const int64_t *qoff, const uint64_t *rec_id
     for (uint64_t q = (uint64_t)qoff[0]; q < Q; q++)
         if (alt[q] >= S)
             return OR_EINVAL;
+    if (decode_threshold_us < 0)
+        return OR_EINVAL;
+    if (prefill_interval)
+        for (uint32_t i = 0; i < S; i++)
+            if (prefill_interval[i] < 0 || prefill_interval[i] > ((int64_t)1 << 40))
+                return OR_EINVAL;
 
     int64_t *L = (int64_t *)malloc(S * sizeof(int64_t));
     int64_t *maxT = (int64_t *)malloc(S * sizeof(int64_t));
+    int64_t *D = (int64_t *)calloc(S, sizeof(int64_t));
     uint8_t *over = (uint8_t *)calloc(S, 1);
     or_src *src = (or_src *)malloc(S * sizeof(or_src));
-    if (!L || !maxT || !over || !src) {
-        free(L); free(maxT); free(over); free(src);
+    if (!L || !maxT || !D || !over || !src) {
+        free(L); free(maxT); free(D); free(over); free(src);
         return OR_ENOMEM;
     }
+    /* decode-delay estimate per instance (zero unless stalled in decode) */
+    if (prefill_interval)
+        for (uint32_t i = 0; i < S; i++)
+            if (qoff[i + 1] > qoff[i] && prefill_interval[i] > decode_threshold_us)
+                D[i] = prefill_interval[i];
     /* pass-start state */
     for (uint32_t i = 0; i < S; i++) {
         int64_t ahead = base_work[i], mx = INT64_MIN;
         for (int64_t q = qoff[i]; q < qoff[i + 1]; q++) {
-            int64_t t = or_ttft(st, unc_here[q], ahead);
+            int64_t t = D[i] + or_ttft(st, unc_here[q], ahead);
             if (t > mx) mx = t;
             ahead += unc_here[q];
         }
@@ -698,7 +719,7 @@ int or_rebalance(const or_state *st, const int64_t *qoff, const uint64_t *rec_id
 
     int64_t *L0 = (int64_t *)malloc(S * sizeof(int64_t));
     if (!L0) {
-        free(L); free(maxT); free(over); free(src);
+        free(L); free(maxT); free(D); free(over); free(src);
         return OR_ENOMEM;
     }
     memcpy(L0, L, S * sizeof(int64_t));
@@ -719,10 +740,10 @@ int or_rebalance(const or_state *st, const int64_t *qoff, const uint64_t *rec_id
         uint64_t nc = 0;
         int64_t ahead = base_work[i];
         for (uint64_t q = lo; q < hi; q++) {
-            const int64_t ti = or_ttft(st, unc_here[q], ahead);
+            const int64_t ti = D[i] + or_ttft(st, unc_here[q], ahead);
             ahead += unc_here[q];
             const uint32_t j = alt[q];
-            const int64_t tj = or_ttft(st, unc_alt[q], L0[j]);
+            const int64_t tj = D[j] + or_ttft(st, unc_alt[q], L0[j]);
             const int64_t b = ti - tj;
             if (b > 0 && !over[j]) {
                 c[nc].benefit = b;
@@ -735,11 +756,11 @@ int or_rebalance(const or_state *st, const int64_t *qoff, const uint64_t *rec_id
         int any;
         int64_t cur_max = queue_max_ttft(st, base_work[i], unc_here, gone, lo, hi, &any);
         for (uint64_t k = 0; k < nc; k++) {
-            if (!any || cur_max <= slo)
+            if (!any || D[i] + cur_max <= slo)
                 break; /* every queued request meets the SLO */
             const uint64_t q = c[k].rec;
             const uint32_t j = alt[q];
-            const int64_t tj = or_ttft(st, unc_alt[q], L[j]);
+            const int64_t tj = D[j] + or_ttft(st, unc_alt[q], L[j]);
             if (tj < slo) {
                 gone[q - lo] = 1;
                 L[i] -= unc_here[q];
@@ -760,7 +781,7 @@ int or_rebalance(const or_state *st, const int64_t *qoff, const uint64_t *rec_id
     }
     memcpy(loads_out, L, S * sizeof(int64_t));
     *count = nmig;
-    free(L); free(L0); free(maxT); free(over); free(src);
+    free(L); free(L0); free(maxT); free(D); free(over); free(src);
     if (rc == OR_OK && nmig > cap)
         rc = OR_EFULL;
     return rc;

@@ -435,20 +435,23 @@ def test_two_choices_spread_less_than_one_choice():
 # Rebalance (Sec. 3.3; Sec. A.1.2)
 # ---------------------------------------------------------------------------
 
-def brute_rebalance(cfg, qoff, rec, here, alt, other, W0):
-    """Literal pass recomputing every queue TTFT from scratch at each step."""
+def brute_rebalance(cfg, qoff, rec, here, alt, other, W0, interval=None, thresh=0):
+    """Literal pass recomputing every queue TTFT from scratch at each step.
+    With `interval`, an instance with queued requests whose prefill interval
+    exceeds `thresh` is stalled in decode and every TTFT estimated on it gets
+    the interval added (Sec. A.7)."""
     base, per, div, slo = cfg["ttft_base_us"], cfg["ttft_per_token_us"], cfg["queue_div"], cfg["slo_us"]
     S = len(W0)
-
-    def T(unc, load):
-        return base + per * unc + load // div
-
     queues = {i: list(range(qoff[i], qoff[i + 1])) for i in range(S)}
+    stalled = [interval is not None and bool(queues[i]) and interval[i] > thresh for i in range(S)]
+
+    def T(unc, load, inst):
+        return (int(interval[inst]) if stalled[inst] else 0) + base + per * unc + load // div
 
     def qts(i, q):
         ahead, out = W0[i], []
         for r in q:
-            out.append(T(int(here[r]), ahead))
+            out.append(T(int(here[r]), ahead, i))
             ahead += int(here[r])
         return out
 
@@ -461,7 +464,7 @@ def brute_rebalance(cfg, qoff, rec, here, alt, other, W0):
         cands = []
         for p, r in enumerate(queues[i]):
             j = int(alt[r])
-            b = ts[p] - T(int(other[r]), L0[j])
+            b = ts[p] - T(int(other[r]), L0[j], j)
             if b > 0 and not over[j]:
                 cands.append((-b, p, r))
         cands.sort()
@@ -471,7 +474,7 @@ def brute_rebalance(cfg, qoff, rec, here, alt, other, W0):
             if not now or max(now) <= slo:
                 break
             j = int(alt[r])
-            tj = T(int(other[r]), L[j])
+            tj = T(int(other[r]), L[j], j)
             if tj < slo:
                 cur.remove(r)
                 L[i] -= int(here[r])
@@ -509,6 +512,93 @@ def test_rebalance_matches_brute_force(seed):
                  got["benefit"].tolist(), got["ttft_to"].tolist()))
     assert g == want
     assert got["loads"].tolist() == L
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_rebalance_decode_correction_matches_brute_force(seed):
+    """Decode-bottleneck correction (Sec. A.7) against the literal pass."""
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=5,
+               ttft_base_us=2, ttft_per_token_us=1, queue_div=4, slo_us=50 + seed % 20)
+    o = oracle.Oracle(cfg)
+    qoff, rec, here, alt, other, W0 = _random_queues(1000 + seed)
+    rng = np.random.default_rng(seed)
+    interval = rng.integers(0, 40, size=5).astype(np.int64)
+    thresh = int(rng.integers(0, 30))
+    got = o.rebalance(qoff, rec, here, alt, other, W0, prefill_interval=interval,
+                      decode_threshold_us=thresh)
+    want, L = brute_rebalance(cfg, qoff, rec, here, alt, other, W0, interval, thresh)
+    assert got["status"] == oracle.OK
+    g = list(zip(got["rec"].tolist(), got["src"].tolist(), got["dst"].tolist(),
+                 got["benefit"].tolist(), got["ttft_to"].tolist()))
+    assert g == want
+    assert got["loads"].tolist() == L
+
+
+def _decode_case(interval1, queue1):
+    """Instance 0 holds two records of 10 uncached tokens (alternative 1, 5
+    tokens there); instance 1 holds one record of 1 token if queue1."""
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=3,
+               ttft_base_us=2, ttft_per_token_us=1, queue_div=4, slo_us=40)
+    o = oracle.Oracle(cfg)
+    n1 = 1 if queue1 else 0
+    qoff = np.array([0, 2, 2 + n1, 2 + n1], np.int64)
+    here = np.array([10, 10] + [1] * n1, np.uint32)
+    alt = np.array([1, 1] + [2] * n1, np.uint32)
+    other = np.array([5, 5] + [1] * n1, np.uint32)
+    rec = np.array([7, 8] + [9] * n1, np.uint64)
+    W0 = np.zeros(3, np.int64)
+    return o, (qoff, rec, here, alt, other, W0), np.array([30, interval1, 0], np.int64)
+
+
+def test_rebalance_decode_correction_hand_values():
+    """Sec. A.7 by hand.  TTFT = 2 + unc + load/4, SLO 40.  Instance 0's
+    queue estimates 12 and 14 us: no overload.  With a prefill interval of
+    30 us over a 20 us threshold it is stalled in decode: 42 and 44 us,
+    overloaded.  Instance 1 (empty queue, so never stalled) estimates 7 us
+    for either record: benefits 35 and 37; the 37 record moves first
+    (target TTFT 7), the queue still estimates 42, the other moves (target
+    TTFT 2 + 5 + 5/4 = 8)."""
+    o, q, interval = _decode_case(100, queue1=False)
+    plain = o.rebalance(*q)
+    assert plain["count"] == 0
+    got = o.rebalance(*q, prefill_interval=interval, decode_threshold_us=20)
+    assert got["status"] == oracle.OK and got["count"] == 2
+    assert got["rec"].tolist() == [8, 7] and got["src"].tolist() == [0, 0]
+    assert got["dst"].tolist() == [1, 1]
+    assert got["benefit"].tolist() == [37, 35] and got["ttft_to"].tolist() == [7, 8]
+    assert got["loads"].tolist() == [0, 10, 0]
+    # at the threshold exactly the instance is not stalled (strictly above)
+    at = o.rebalance(*q, prefill_interval=interval, decode_threshold_us=30)
+    assert at["count"] == 0
+    # instance 1 with queued work and a 100 us interval is stalled too: its
+    # record estimates 100 + 2 + 1 = 103 us, so instance 1 is overloaded and
+    # no target for instance 0; its own record moves to instance 2 (benefit
+    # 103 - 3 = 100, target TTFT 3), instance 0 keeps its queue
+    o, q, interval = _decode_case(100, queue1=True)
+    got = o.rebalance(*q, prefill_interval=interval, decode_threshold_us=20)
+    assert got["status"] == oracle.OK and got["count"] == 1
+    assert got["rec"].tolist() == [9] and got["src"].tolist() == [1] and got["dst"].tolist() == [2]
+    assert got["benefit"].tolist() == [100] and got["ttft_to"].tolist() == [3]
+    assert got["loads"].tolist() == [20, 0, 1]
+    # every interval at or under the threshold: the plain pass
+    o2 = oracle.Oracle(dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=5,
+                            ttft_base_us=2, ttft_per_token_us=1, queue_div=4, slo_us=45))
+    for seed in range(5):
+        qq = _random_queues(2000 + seed)
+        a = o2.rebalance(*qq)
+        b = o2.rebalance(*qq, prefill_interval=np.full(5, 20, np.int64), decode_threshold_us=20)
+        for k in ("rec", "src", "dst", "benefit", "ttft_to", "loads"):
+            assert a[k].tolist() == b[k].tolist()
+
+
+def test_rebalance_decode_correction_rejects_bad_telemetry():
+    o, q, interval = _decode_case(100, queue1=False)
+    assert o.rebalance(*q, prefill_interval=interval, decode_threshold_us=-1)["status"] == oracle.EINVAL
+    bad = interval.copy()
+    bad[2] = -5
+    assert o.rebalance(*q, prefill_interval=bad, decode_threshold_us=20)["status"] == oracle.EINVAL
+    bad[2] = (1 << 40) + 1
+    assert o.rebalance(*q, prefill_interval=bad, decode_threshold_us=20)["status"] == oracle.EINVAL
 
 
 def test_rebalance_invariants_and_cap():

@@ -175,7 +175,17 @@ dm_status dm_route_batch_noalloc(dm_ctx* ctx, const int32_t* tokens, uint64_t n_
  * is records [qoff[i], qoff[i+1]) head first; record q costs unc_here[q]
  * uncached tokens on i and unc_alt[q] on its alternative candidate alt[q]
  * (the other member of its dual-mapping pair); base_work[i] is pending work
- * ahead of queue i. */
+ * ahead of queue i.
+ *
+ * Decode-bottleneck telemetry (Sec. A.7), optional: prefill_interval[i] is
+ * the time in microseconds since instance i last completed a prefill.  An
+ * instance with a non-empty queue whose interval exceeds
+ * decode_threshold_us is taken to be stalled in decode, and every TTFT the
+ * pass estimates on it (as source or as target) gets its interval added as
+ * the decode-delay estimate.  NULL: no correction.  Intervals must lie in
+ * [0, 2^40] (the pass reports DM_EINVAL through dm_sync otherwise, its
+ * outputs then undefined); the threshold must not be negative (host
+ * check).  The paper's deployment uses a threshold of 3 s. */
 typedef struct {
     const int64_t* qoff;       /* [max_slots + 1], qoff[0] = 0, non-decreasing */
     const uint64_t* rec_id;    /* [Q] caller's record ids                      */
@@ -183,6 +193,8 @@ typedef struct {
     const uint32_t* alt;       /* [Q] each < max_slots                         */
     const uint32_t* unc_alt;   /* [Q]                                          */
     const int64_t* base_work;  /* [max_slots]                                  */
+    const int64_t* prefill_interval;  /* [max_slots] or NULL                   */
+    int64_t decode_threshold_us;      /* read only with prefill_interval       */
 } dm_queues;
 
 /* Migration list of dm_rebalance (device arrays of cap entries). */
@@ -198,7 +210,8 @@ typedef struct {
 /* One non-recursive, single-round hotspot rebalancing pass (Sec. 3.3,
  * Eq. of the migration benefit; Sec. A.1.2).  The TTFT of the record at
  * queue position p of instance i waits behind base_work[i] and the records
- * ahead of it.  Instance i is overloaded when some queued TTFT exceeds the
+ * ahead of it (plus the decode-delay estimate of a stalled instance, see
+ * dm_queues).  Instance i is overloaded when some queued TTFT exceeds the
  * SLO (judged at pass start).  Overloaded sources are taken heaviest load
  * first (ties: lower id); within a source, records with benefit B > 0 whose
  * alternative is not overloaded go in order of descending B (ties: nearer

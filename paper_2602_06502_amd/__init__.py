@@ -52,7 +52,8 @@ class dm_route_out(C.Structure):
 
 class dm_queues(C.Structure):
     _fields_ = [("qoff", C.c_void_p), ("rec_id", C.c_void_p), ("unc_here", C.c_void_p),
-                ("alt", C.c_void_p), ("unc_alt", C.c_void_p), ("base_work", C.c_void_p)]
+                ("alt", C.c_void_p), ("unc_alt", C.c_void_p), ("base_work", C.c_void_p),
+                ("prefill_interval", C.c_void_p), ("decode_threshold_us", C.c_int64)]
 
 
 class dm_migrations(C.Structure):
@@ -263,7 +264,8 @@ class DualMap:
         self.route_into(tokens, offsets, loads, out)
         return out
 
-    def rebalance(self, qoff, rec_id, unc_here, alt, unc_alt, base_work, cap: Optional[int] = None):
+    def rebalance(self, qoff, rec_id, unc_here, alt, unc_alt, base_work, cap: Optional[int] = None,
+                  prefill_interval=None, decode_threshold_us: int = 3_000_000):
         t = self.torch
         qoff = self._dev(qoff, t.int64, "qoff")
         rec_id = self._dev(rec_id, t.uint64, "rec_id")
@@ -273,13 +275,18 @@ class DualMap:
         base_work = self._dev(base_work, t.int64, "base_work")
         if qoff.numel() != self.max_slots + 1 or base_work.numel() != self.max_slots:
             raise ValueError("qoff needs max_slots + 1 entries and base_work max_slots")
+        if prefill_interval is not None:
+            prefill_interval = self._dev(prefill_interval, t.int64, "prefill_interval")
+            if prefill_interval.numel() != self.max_slots:
+                raise ValueError("prefill_interval needs max_slots entries")
         cap = rec_id.numel() if cap is None else cap
         m = dict(rec=self._empty(max(cap, 1), t.uint64), src=self._empty(max(cap, 1), t.uint32),
                  dst=self._empty(max(cap, 1), t.uint32), benefit=self._empty(max(cap, 1), t.int64),
                  ttft_to=self._empty(max(cap, 1), t.int64), count=self._empty(1, t.uint64))
         loads = self._empty(self.max_slots, t.int64)
         q = dm_queues(_ptr(qoff), _ptr(rec_id), _ptr(unc_here), _ptr(alt), _ptr(unc_alt),
-                      _ptr(base_work))
+                      _ptr(base_work),
+                      _ptr(prefill_interval), int(decode_threshold_us))
         mg = dm_migrations(_ptr(m["rec"]), _ptr(m["src"]), _ptr(m["dst"]), _ptr(m["benefit"]),
                            _ptr(m["ttft_to"]), _ptr(m["count"]))
         self._check(self.lib.dm_rebalance(self._h, C.byref(q), _ptr(loads), C.byref(mg), cap),

@@ -432,8 +432,10 @@ dm_status dm_rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out,
     if (cap && (!out->rec_id || !out->from || !out->to || !out->benefit_us || !out->ttft_to_us))
         return fail(c, DM_EINVAL, "dm_rebalance: null migration array");
     if (!aligned(q->qoff) || !aligned(q->base_work) || !aligned(loads_out) ||
-        !aligned(out->count))
+        !aligned(out->count) || (q->prefill_interval && !aligned(q->prefill_interval)))
         return fail(c, DM_EINVAL, "dm_rebalance: misaligned pointer");
+    if (q->prefill_interval && q->decode_threshold_us < 0)
+        return fail(c, DM_EINVAL, "dm_rebalance: negative decode threshold");
     DeviceGuard g(c->device);
     if (hipError_t je = join_selection(c); je != hipSuccess)
         return hip_fail(c, je, "dm_rebalance");

@@ -1,9 +1,14 @@
 // dm_rebalance: one non-recursive, single-round hotspot migration pass
 // (Sec. 3.3, Eq. of the migration benefit; Sec. A.1.2).
 //
+// A stalled instance (decode-bottleneck telemetry, Sec. A.7) has its
+// interval D added to every TTFT estimated on it; the comparisons below use
+// the equivalent per-instance bound "TTFT without D against SLO - D".
+//
 // Pass-start state in parallel:
 //   queue scan    per instance: each record's TTFT behind the base work and
-//                 the records ahead of it; load; max TTFT; overloaded flag;
+//                 the records ahead of it; load; max TTFT; decode delay;
+//                 overloaded flag;
 //   benefit       per record: B = TTFT here - TTFT on the alternative;
 //                 eligible if B > 0, source overloaded, target not;
 //   source ranks  overloaded instances by (load desc, id asc);
@@ -217,11 +222,15 @@ __global__ __launch_bounds__(kQThreads) void queue_ttft_kernel(
         slice_max[blockIdx.x] = mx;
 }
 
+// Decode delay D of a stalled instance (non-empty queue, prefill interval
+// above the threshold), else 0; intervals outside [0, 2^40] are rejected.
 __global__ void queue_over_kernel(const int64_t* __restrict__ qoff, uint64_t Q,
                                   const int64_t* __restrict__ base_work,
                                   const int64_t* __restrict__ slice_sum,
                                   const int64_t* __restrict__ slice_max, uint32_t S, int64_t slo,
-                                  int64_t* __restrict__ L0, uint8_t* __restrict__ over)
+                                  const int64_t* __restrict__ interval, int64_t thresh,
+                                  int64_t* __restrict__ L0, uint8_t* __restrict__ over,
+                                  int64_t* __restrict__ delay, uint32_t* __restrict__ status)
 {
     const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= S)
@@ -233,8 +242,18 @@ __global__ void queue_over_kernel(const int64_t* __restrict__ qoff, uint64_t Q,
             L += slice_sum[i * kQSplit + k];
             mx = std::max(mx, slice_max[i * kQSplit + k]);
         }
+    const bool busy = ok && qoff[i + 1] > qoff[i];
+    int64_t d = 0;
+    if (interval) {
+        const int64_t v = interval[i];
+        if (v < 0 || v > (int64_t(1) << 40))
+            atomicOr(status, kErrInval);
+        else if (busy && v > thresh)
+            d = v;
+    }
     L0[i] = L;
-    over[i] = (ok && qoff[i + 1] > qoff[i] && mx > slo) ? 1 : 0;
+    delay[i] = d;
+    over[i] = (busy && mx > slo - d) ? 1 : 0;
 }
 
 // Per record: benefit and eligibility; the largest eligible benefit goes to
@@ -242,8 +261,9 @@ __global__ void queue_over_kernel(const int64_t* __restrict__ qoff, uint64_t Q,
 __global__ __launch_bounds__(256) void benefit_kernel(
     uint64_t Q, const int64_t* __restrict__ T, const uint32_t* __restrict__ owner,
     const uint32_t* __restrict__ alt, const uint32_t* __restrict__ unc_alt,
-    const int64_t* __restrict__ L0, const uint8_t* __restrict__ over, uint32_t S, TtftK tk,
-    int64_t* __restrict__ benefit, uint64_t* __restrict__ elig, uint64_t* __restrict__ maxb)
+    const int64_t* __restrict__ L0, const uint8_t* __restrict__ over,
+    const int64_t* __restrict__ delay, uint32_t S, TtftK tk, int64_t* __restrict__ benefit,
+    uint64_t* __restrict__ elig, uint64_t* __restrict__ maxb)
 {
     __shared__ int64_t sh[256 / kWave];
     int64_t mx = 0;
@@ -253,7 +273,7 @@ __global__ __launch_bounds__(256) void benefit_kernel(
         bool e = false;
         int64_t b = 0;
         if (i < S && j < S && over[i]) {
-            b = T[q] - tk((int64_t)unc_alt[q], L0[j]);
+            b = (T[q] + delay[i]) - (tk((int64_t)unc_alt[q], L0[j]) + delay[j]);
             e = b > 0 && !over[j];
         }
         benefit[q] = b;
@@ -488,6 +508,7 @@ struct CommitArgs {
     uint64_t* base_of;        // [nsrc] their first index in the migration list
     uint32_t* qkey;           // [Q]
     int64_t* loads;           // [S] in: pass-start loads; out: loads after the pass
+    const int64_t* delay;     // [S] decode delay per instance (0 unless stalled)
     uint32_t S;
     TtftK tk;
     uint64_t cap;
@@ -504,8 +525,8 @@ struct CommitArgs {
 // after the first k accepted records left) exceeds the SLO behind the base
 // work and the records still ahead of it.  Chunked form, for queues longer
 // than the register form holds.
-__device__ bool queue_violates_chunked(const CommitArgs& a, int64_t lo, int64_t hi, int64_t w0,
-                                       uint32_t k, int64_t* sh)
+__device__ bool queue_violates_chunked(const CommitArgs& a, const TtftK& tk, int64_t lo, int64_t hi,
+                                       int64_t w0, uint32_t k, int64_t* sh)
 {
     int64_t run = w0;
     bool v = false;
@@ -516,7 +537,7 @@ __device__ bool queue_violates_chunked(const CommitArgs& a, int64_t lo, int64_t 
         int64_t tot;
         const int64_t ex = block_excl_scan_i64<kCommitThreads>(u, sh, tot);
         if (keep)
-            v |= a.tk(u, run + ex) > a.tk.slo;
+            v |= tk(u, run + ex) > tk.slo;
         run += tot;
     }
     return __syncthreads_or(v) != 0;
@@ -622,8 +643,8 @@ __device__ __noinline__ uint32_t regs_bisect(const uint32_t* __restrict__ unc_he
 // acceptance bit of each accepted candidate (bit t - cs) and stores every
 // record's TTFT on its target at its turn.
 __device__ __forceinline__ void walk_run(const CommitArgs& a, uint32_t* s_bits, uint32_t* g_bits,
-                                         bool in_lds, const int64_t* s_L, uint32_t cs, uint32_t P0,
-                                         uint32_t P1)
+                                         bool in_lds, const int64_t* s_L, const int64_t* s_slo,
+                                         uint32_t cs, uint32_t P0, uint32_t P1)
 {
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const uint64_t below = (1ull << lane) - 1;  // lanes under this one
@@ -655,6 +676,9 @@ __device__ __forceinline__ void walk_run(const CommitArgs& a, uint32_t* s_bits, 
                 break;
             const bool valid = pc + lane < P1;
             const uint32_t u = cu[g], t = ct[g], j = cj[g];
+            // the SLO less the target's decode delay; a run's records share
+            // their target, so a record's bound is also its run start's
+            const int64_t slo_j = valid ? s_slo[j] : a.tk.slo;
             uint32_t jprev = __shfl_up(j, 1);
             if (lane == 0)
                 jprev = carry_j;
@@ -680,9 +704,9 @@ __device__ __forceinline__ void walk_run(const CommitArgs& a, uint32_t* s_bits, 
                     const int f = __ffsll((long long)U) - 1;
                     const uint32_t uf = __builtin_amdgcn_readlane(u, f);
                     const uint64_t exf = readlane_u64(excl, f);
-                    const bool pf = a.tk((int64_t)uf, Lf) < a.tk.slo;
+                    const bool pf = a.tk((int64_t)uf, Lf) < slo_j;
                     const int64_t Lv = pf ? Lf + (int64_t)(excl - exf) : Lf;
-                    const bool pv = a.tk((int64_t)u, Lv) < a.tk.slo;
+                    const bool pv = a.tk((int64_t)u, Lv) < slo_j;
                     const bool inU = (U >> lane) & 1;
                     const uint64_t sm = __ballot(inU && pv != pf);
                     const int st = sm ? __ffsll((long long)sm) - 1 : kWave;
@@ -709,9 +733,9 @@ __device__ __forceinline__ void walk_run(const CommitArgs& a, uint32_t* s_bits, 
                 const int64_t Lf = (int64_t)shfl_u64((uint64_t)Lx, f);
                 const uint32_t uf = __shfl(u, f);
                 const uint64_t exf = shfl_u64(excl, f);
-                const bool pf = a.tk((int64_t)uf, Lf) < a.tk.slo;
+                const bool pf = a.tk((int64_t)uf, Lf) < slo_j;
                 const int64_t Lv = pf ? Lf + (int64_t)(excl - exf) : Lf;
-                const bool pv = a.tk((int64_t)u, Lv) < a.tk.slo;
+                const bool pv = a.tk((int64_t)u, Lv) < slo_j;
                 const bool inU = (U >> lane) & 1;
                 const uint64_t sm = __ballot(inU && pv != pf) & segbits;
                 const int st = sm ? __ffsll((long long)sm) - 1 : kWave;
@@ -729,7 +753,7 @@ __device__ __forceinline__ void walk_run(const CommitArgs& a, uint32_t* s_bits, 
                 U &= ~__ballot(settle);
             }
             if (valid) {
-                a.tto[t] = a.tk((int64_t)u, Lt);
+                a.tto[t] = a.tk((int64_t)u, Lt) + (a.tk.slo - slo_j);
                 if (ok) {
                     const uint32_t x = t - cs;
                     if (in_lds)
@@ -755,13 +779,16 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
 {
     __shared__ int64_t sh[kCommitThreads / kWave];
     __shared__ int64_t s_L[kMaxSlots];         // live loads of every instance
+    __shared__ int64_t s_slo[kMaxSlots];       // SLO less each instance's decode delay
     __shared__ uint32_t s_bits[kLdsBitWords];
     __shared__ uint32_t s_wpre[kLdsBitWords];
     __shared__ uint64_t s_count;
     const uint32_t nsrc = *a.nsrc, S = a.S;
     const uint32_t tid = threadIdx.x;
-    for (uint32_t j = tid; j < S; j += kCommitThreads)
+    for (uint32_t j = tid; j < S; j += kCommitThreads) {
         s_L[j] = a.loads[j];
+        s_slo[j] = a.tk.slo - a.delay[j];
+    }
     if (tid == 0)
         s_count = 0;
     __syncthreads();
@@ -784,7 +811,7 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
             const uint32_t ga = G0 + (uint32_t)((uint64_t)ng * wv / kCommitWaves);
             const uint32_t gb = G0 + (uint32_t)((uint64_t)ng * (wv + 1) / kCommitWaves);
             if (ga < gb)
-                walk_run(a, s_bits, a.gbits, in_lds, s_L, cs, a.seg_pos[ga], a.seg_pos[gb]);
+                walk_run(a, s_bits, a.gbits, in_lds, s_L, s_slo, cs, a.seg_pos[ga], a.seg_pos[gb]);
         }
         wg_sync();
         // (ii) acceptance ranks in candidate order: accepted candidates
@@ -833,17 +860,19 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
         uint32_t kstar = 0;
         if (A > 0) {
             const int64_t w0q = a.base_work[i];
+            TtftK tks = a.tk;  // the source's queue against the SLO less its decode delay
+            tks.slo = s_slo[i];
             const uint64_t Lq = (uint64_t)(qhi - qlo);
             uint32_t lo = 1, hi = (uint32_t)A;  // answer in [lo, hi]
             if (Lq <= (uint64_t)kCommitThreads * kQueueRegs) {
-                lo = regs_bisect(a.unc_here, a.qkey, qlo, Lq, w0q, hi, a.tk, sh);
+                lo = regs_bisect(a.unc_here, a.qkey, qlo, Lq, w0q, hi, tks, sh);
             } else {
-                if (queue_violates_chunked(a, qlo, qhi, w0q, hi, sh)) {
+                if (queue_violates_chunked(a, tks, qlo, qhi, w0q, hi, sh)) {
                     lo = hi;
                 } else {
                     while (lo < hi) {
                         const uint32_t mid = lo + (hi - lo) / 2;
-                        if (!queue_violates_chunked(a, qlo, qhi, w0q, mid, sh))
+                        if (!queue_violates_chunked(a, tks, qlo, qhi, w0q, mid, sh))
                             hi = mid;
                         else
                             lo = mid + 1;
@@ -956,14 +985,15 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     hipStream_t st = c->stream;
     hipError_t e;
     // per-instance arrays
-    // per instance slot: L0, base_of 8 B; over 1 B; rank, src, start, sseg,
-    // kstar_of 4 B; slice sums and maxima 2 x 8 x kQSplit B -- 293 B, and 12
-    // carves of at most 256 B padding
+    // per instance slot: L0, delay, base_of 8 B; over 1 B; rank, src, start,
+    // sseg, kstar_of 4 B; slice sums and maxima 2 x 8 x kQSplit B -- 301 B,
+    // and 13 carves of at most 256 B padding
     uint8_t* pi = static_cast<uint8_t*>(
         scratch_get(c, kSlotSelect, 320 * ((uint64_t)S + 64) + 8192, &e));
     if (!pi)
         return e;
     int64_t* L0 = carve<int64_t>(pi, S);
+    int64_t* delay = carve<int64_t>(pi, S);
     uint8_t* over = carve<uint8_t>(pi, S);
     uint32_t* rank = carve<uint32_t>(pi, S);
     uint32_t* src = carve<uint32_t>(pi, S);
@@ -996,11 +1026,14 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
                                                          q->base_work, slice_sum, S, tk, T, owner,
                                                          slice_max, c->d_status);
     queue_over_kernel<<<(S + 255) / 256, 256, 0, st>>>(q->qoff, Q, q->base_work, slice_sum,
-                                                        slice_max, S, tk.slo, L0, over);
+                                                        slice_max, S, tk.slo, q->prefill_interval,
+                                                        q->decode_threshold_us, L0, over, delay,
+                                                        c->d_status);
     if (Q)
         // grid-stride: 256 workgroups, one atomic maximum each
         benefit_kernel<<<grid_for(Q, 256, 256), 256, 0, st>>>(Q, T, owner, q->alt, q->unc_alt, L0,
-                                                              over, S, tk, benefit, elig, ctot + 1);
+                                                              over, delay, S, tk, benefit, elig,
+                                                              ctot + 1);
     rank_kernel<<<(S + 255) / 256, 256, 0, st>>>(L0, over, S, rank, src, nsrc);
     uint64_t hw[2] = {0, 0};  // candidate count, largest eligible benefit
     if (Q) {
@@ -1121,6 +1154,7 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     a.base_of = base_of;
     a.qkey = qkey;
     a.loads = loads_out;
+    a.delay = delay;
     a.S = S;
     a.tk = tk;
     a.cap = cap;

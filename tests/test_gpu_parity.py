@@ -514,18 +514,20 @@ def test_index_erase_then_match_parity():
 # Rebalance
 # ---------------------------------------------------------------------------
 
-def compare_rebalance(eng, o, q, cap=None):
+def compare_rebalance(eng, o, q, cap=None, interval=None, thresh=3_000_000):
     gh = _h()
     dev = eng.device
     g = eng.rebalance(gh.to_dev(q.qoff, dev), gh.to_dev(q.rec_id, dev), gh.to_dev(q.unc_here, dev),
                       gh.to_dev(q.alt, dev), gh.to_dev(q.unc_alt, dev), gh.to_dev(q.base_work, dev),
-                      cap=cap)
+                      cap=cap, prefill_interval=None if interval is None else gh.to_dev(interval, dev),
+                      decode_threshold_us=thresh)
     status = 0
     try:
         eng.sync()
     except Exception as e:  # DM_EFULL when cap is exceeded
         status = e.status
-    r = o.rebalance(q.qoff, q.rec_id, q.unc_here, q.alt, q.unc_alt, q.base_work, cap=cap)
+    r = o.rebalance(q.qoff, q.rec_id, q.unc_here, q.alt, q.unc_alt, q.base_work, cap=cap,
+                    prefill_interval=interval, decode_threshold_us=thresh)
     assert status == r["status"]
     n = int(cpu(g["count"])[0])
     assert n == r["count"]
@@ -627,6 +629,94 @@ def test_rebalance_candidates_past_lds_parity():
     _say("rebalance past LDS: records", len(q.rec_id))
     r = compare_rebalance(eng, o, q)
     assert 1_000 < r["count"] < 2_000
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_rebalance_decode_correction_parity(seed):
+    """Decode-bottleneck correction (Sec. A.7): stalled sources, stalled
+    targets and instances stalled only by the correction, against the
+    oracle; intervals at or under the threshold give the plain pass."""
+    gh = _h()
+    S, n_live = 16, 12
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=S, index_log2_slots=8,
+               slo_us=80_000)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    o = oracle.Oracle(cfg)
+    rng = np.random.default_rng(50 + seed)
+    src = np.sort(rng.choice(n_live, size=2, replace=False))
+    q = workloads.synthetic_queues(60 + seed, S, n_live, src, 800, 400, 150_000, 4 * 70_000)
+    thresh = 20_000
+    interval = rng.integers(0, 60_000, size=S).astype(np.int64)
+    _say("rebalance decode correction", seed, "records", len(q.rec_id))
+    plain = compare_rebalance(eng, o, q)
+    r = compare_rebalance(eng, o, q, interval=interval, thresh=thresh)
+    assert r["count"] > 0
+    assert (r["rec"].tolist() != plain["rec"].tolist()
+            or r["ttft_to"].tolist() != plain["ttft_to"].tolist())
+    calm = np.minimum(interval, thresh)
+    r2 = compare_rebalance(eng, o, q, interval=calm, thresh=thresh)
+    for k in ("rec", "src", "dst", "benefit", "ttft_to", "loads"):
+        assert np.array_equal(r2[k], plain[k]), k
+
+
+def test_rebalance_decode_correction_long_queues_parity():
+    """The correction on the commit's long-queue paths: a 40,000-record
+    source (chunked queue probes) stalled by a small delay, a 2,000-record
+    source (queue in registers), and stalled targets among 1,500 live
+    instances."""
+    gh = _h()
+    S, n_live = 2048, 1500
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=S, index_log2_slots=8,
+               slo_us=400_000)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    o = oracle.Oracle(cfg)
+    q = workloads.synthetic_queues(31, S, n_live, np.array([17, 901]), 40_000, 60, 50_000,
+                                   4 * 300_000)
+    lens = np.diff(q.qoff)
+    keep = np.ones(len(q.rec_id), bool)
+    keep[q.qoff[901] + 2_000:q.qoff[902]] = False
+    lens[901] = 2_000
+    qoff = np.zeros(S + 1, np.int64)
+    qoff[1:] = np.cumsum(lens)
+    q = workloads.Queues(qoff, q.rec_id[keep], q.unc_here[keep], q.alt[keep], q.unc_alt[keep],
+                         q.base_work)
+    rng = np.random.default_rng(7)
+    interval = np.zeros(S, np.int64)
+    interval[17] = 25_000
+    interval[901] = 120_000
+    stalled_targets = rng.choice(n_live, size=200, replace=False)
+    interval[stalled_targets] = rng.integers(30_000, 500_000, size=200)
+    _say("rebalance decode correction long queues: records", len(q.rec_id))
+    r = compare_rebalance(eng, o, q, interval=interval, thresh=20_000)
+    per_src = np.bincount(r["src"], minlength=S)
+    assert per_src[17] > 0 and per_src[901] > 0, per_src[[17, 901]]
+
+
+def test_rebalance_decode_telemetry_errors():
+    gh = _h()
+    import paper_2602_06502_amd as pk
+    S = 8
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=S, index_log2_slots=8,
+               slo_us=50_000)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    o = oracle.Oracle(cfg)
+    q = workloads.synthetic_queues(3, S, S, np.array([1, 5]), 400, 300, 100_000, 4 * 40_000)
+    dev = eng.device
+    args = [gh.to_dev(a, dev) for a in (q.qoff, q.rec_id, q.unc_here, q.alt, q.unc_alt, q.base_work)]
+    good = np.full(S, 1_000, np.int64)
+    with pytest.raises(pk.DMError) as ei:
+        eng.rebalance(*args, prefill_interval=gh.to_dev(good, dev), decode_threshold_us=-1)
+    assert ei.value.status == pk.DM_EINVAL
+    bad = good.copy()
+    bad[3] = -1
+    eng.rebalance(*args, prefill_interval=gh.to_dev(bad, dev), decode_threshold_us=10)
+    with pytest.raises(pk.DMError) as ei:
+        eng.sync()
+    assert ei.value.status == pk.DM_EINVAL
+    assert o.rebalance(q.qoff, q.rec_id, q.unc_here, q.alt, q.unc_alt, q.base_work,
+                       prefill_interval=bad, decode_threshold_us=10)["status"] == oracle.EINVAL
+    # the context stays usable
+    compare_rebalance(eng, o, q, interval=good, thresh=10)
 
 
 def _queues_from_route(chosen, cand, match, off, B, S, base_work):

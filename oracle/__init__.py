@@ -80,6 +80,7 @@ def lib():
             "or_candidates": (i32, [P, u64, u64, P, P]),
             "or_select": (u32, [P, u32, u32, u64, u64, i64, P, P, P]),
             "or_route": (i32, [P, P, P, u64, P, P, P, P, P, P, P, P]),
+            "or_set_policy": (i32, [P, i32]),
             "or_rebalance": (i32, [P, P, P, P, P, P, P, P, i64, P, P, P, P, P, P, u64, P]),
             "or_scale": (i32, [P, P, u32, P, u32, P, u64, P, P, P, P]),
             "or_n_live": (u32, [P]),
@@ -160,6 +161,13 @@ class Oracle:
             self._h = None
 
     # -- state ------------------------------------------------------------
+    POLICIES = {"slo_aware": 0, "cache_affinity": 1, "least_loaded": 2, "min_ttft": 3}
+
+    def set_policy(self, policy) -> int:
+        """Selection rule for later routes: a name of POLICIES or its number."""
+        p = self.POLICIES.get(policy, policy) if isinstance(policy, str) else int(policy)
+        return lib().or_set_policy(self._h, p)
+
     def build_rings(self, ids: Sequence[int]) -> int:
         a = np.ascontiguousarray(ids, dtype=np.uint32)
         return lib().or_build_rings(self._h, _p(a), len(a))

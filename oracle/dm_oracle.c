@@ -52,7 +52,13 @@ typedef struct {
     uint64_t ring_len;
     uint64_t **set;           /* per instance: sorted unique cached block keys  */
     uint64_t *set_len;
+    int policy;               /* selection rule, OR_POLICY_* (default SLO-aware)*/
 } or_state;
+
+/* Selection rules between the two candidates: DualMap's SLO-aware rule and
+ * the single-criterion variants of the ablation study (Sec. 4.3). */
+enum { OR_POLICY_SLO_AWARE = 0, OR_POLICY_CACHE_AFFINITY = 1, OR_POLICY_LEAST_LOADED = 2,
+       OR_POLICY_MIN_TTFT = 3 };
 
 /* ------------------------------------------------------------------------- */
 /* Hash primitives.  The paper asks for two independent hash functions over   */
@@ -487,14 +493,21 @@ static uint64_t prefix_match(const or_state *st, uint32_t id, const uint64_t *h1
     return m;
 }
 
-/* SLO-aware selection of one request (Sec. 3.2 "SLO-Aware Strategy";
- * Sec. A.1.1).  Loads L are pending prefill tokens before this request.
+/* Selection of one request between its candidates.  Loads L are pending
+ * prefill tokens before this request.  SLO-aware rule (Sec. 3.2 "SLO-Aware
+ * Strategy"; Sec. A.1.1):
  *   - equal prefix hits: the less-loaded candidate (ties: c1);
  *   - otherwise the candidate with more cached blocks, unless its TTFT
  *     exceeds the SLO, then the less-loaded one (ties: keep the cached one).
- * Flags: bit0 switched away from the cached candidate because of the SLO,
- * bit1 both candidates' TTFT exceed the SLO, bit2 equal match, bit3 the
- * second candidate was adjusted. */
+ * Ablation variants (Sec. 4.3), each a single criterion:
+ *   - cache affinity: the candidate with more cached blocks (equal hits: the
+ *     less-loaded, ties c1);
+ *   - least loaded: the less-loaded candidate (ties: c1);
+ *   - min TTFT: the candidate with the smaller estimated TTFT (ties: c1).
+ * Flags: bit0 the chosen candidate has fewer cached blocks than the other
+ * (under the SLO-aware rule: a switch for the SLO), bit1 both candidates'
+ * TTFT exceed the SLO, bit2 equal match, bit3 the second candidate was
+ * adjusted. */
 uint32_t or_select(const or_state *st, uint32_t c1, uint32_t c2, uint64_t m1, uint64_t m2,
                    int64_t len, const int64_t *L, int64_t *ttft_out, uint8_t *flags_io)
 {
@@ -504,25 +517,50 @@ uint32_t or_select(const or_state *st, uint32_t c1, uint32_t c2, uint64_t m1, ui
     uint8_t fl = *flags_io;
     if (t1 > st->cfg.slo_us && t2 > st->cfg.slo_us)
         fl |= 2;
-    uint32_t ch;
-    if (m1 == m2) {
+    if (m1 == m2)
         fl |= 4;
+    uint32_t ch;
+    switch (st->policy) {
+    case OR_POLICY_LEAST_LOADED:
         ch = (L[c1] <= L[c2]) ? c1 : c2;
-    } else {
-        uint32_t a = m1 > m2 ? c1 : c2, o = m1 > m2 ? c2 : c1;
-        int64_t ta = m1 > m2 ? t1 : t2;
-        if (ta <= st->cfg.slo_us) {
-            ch = a;
-        } else if (L[o] < L[a]) {
-            ch = o;
-            fl |= 1;
+        break;
+    case OR_POLICY_MIN_TTFT:
+        ch = (t1 <= t2) ? c1 : c2;
+        break;
+    case OR_POLICY_CACHE_AFFINITY:
+        if (m1 == m2)
+            ch = (L[c1] <= L[c2]) ? c1 : c2;
+        else
+            ch = m1 > m2 ? c1 : c2;
+        break;
+    default:
+        if (m1 == m2) {
+            ch = (L[c1] <= L[c2]) ? c1 : c2;
         } else {
-            ch = a;
+            uint32_t a = m1 > m2 ? c1 : c2, o = m1 > m2 ? c2 : c1;
+            int64_t ta = m1 > m2 ? t1 : t2;
+            if (ta <= st->cfg.slo_us)
+                ch = a;
+            else if (L[o] < L[a])
+                ch = o;
+            else
+                ch = a;
         }
     }
+    if (m1 != m2 && (ch == c1) != (m1 > m2))
+        fl |= 1;
     *ttft_out = (ch == c1) ? t1 : t2;
     *flags_io = fl;
     return ch;
+}
+
+/* Choose the selection rule for later routes; OR_EINVAL if unknown. */
+int or_set_policy(or_state *st, int policy)
+{
+    if (!st || policy < OR_POLICY_SLO_AWARE || policy > OR_POLICY_MIN_TTFT)
+        return OR_EINVAL;
+    st->policy = policy;
+    return OR_OK;
 }
 
 /* Route a batch in request order over a snapshot of the cached block sets,

@@ -346,6 +346,100 @@ def test_selection_truth_table(case):
     assert t == 400_000 and ch == 0
 
 
+@pytest.mark.parametrize("case", [
+    # (policy, m1, m2, L1, L2, len, expected chosen (1|2), flags)
+    # TTFT = 2000 + 3 unc + L/4 with B = 16, SLO 400,000
+    ("cache_affinity", 5, 1, 2_000_000, 0, 100, 1, 0),   # affine even far over the SLO
+    ("cache_affinity", 1, 5, 0, 2_000_000, 100, 2, 0),
+    ("cache_affinity", 3, 3, 21, 20, 100, 2, 4),          # equal hits: less loaded
+    ("cache_affinity", 3, 3, 20, 20, 100, 1, 4),
+    ("least_loaded", 5, 1, 11, 10, 100, 2, 1),            # less loaded, fewer cached blocks
+    ("least_loaded", 5, 1, 10, 10, 100, 1, 0),            # ties: c1
+    ("least_loaded", 1, 5, 10, 10, 100, 1, 1),            # ties: c1 even with fewer blocks
+    ("least_loaded", 3, 3, 21, 20, 100, 2, 4),
+    # min TTFT: t1 = 2000 + 3 (100 - 16 m1) + L1/4, t2 likewise
+    ("min_ttft", 5, 1, 400, 0, 100, 1, 0),   # t1 = 2060 + 100 = 2160 < t2 = 2252
+    ("min_ttft", 5, 1, 772, 0, 100, 2, 1),   # t1 = 2060 + 193 = 2253 > 2252
+    ("min_ttft", 5, 1, 768, 0, 100, 1, 0),   # t1 = 2060 + 192 = 2252 = t2: ties c1
+    ("min_ttft", 3, 3, 8, 4, 100, 2, 4),     # equal hits: t by load, 2000+156+2 vs +1
+    ("min_ttft", 3, 3, 7, 4, 100, 1, 4),     # 7/4 = 1 = 4/4: tie, c1
+    ("slo_aware", 5, 1, 2_000_000, 0, 100, 2, 1),
+])
+def test_policy_truth_table(case):
+    """The ablation variants of Sec. 4.3 by hand.  bit0 marks a chosen
+    candidate with fewer cached blocks, bit1 both over the SLO, bit2 equal
+    hits."""
+    policy, m1, m2, L1, L2, length, want, want_flags = case
+    o = oracle.Oracle(dict(_cfg(B=16), slo_us=400_000))
+    assert o.set_policy(policy) == oracle.OK
+    loads = np.array([L1, L2], np.int64)
+    ch, t, f = o.select(0, 1, m1, m2, length, loads)
+    assert ch == want - 1, (ch, want)
+    assert f == want_flags
+    unc = length - 16 * (m1 if ch == 0 else m2)
+    assert t == 2000 + 3 * unc + loads[ch] // 4
+
+
+def test_policy_rejects_unknown():
+    o = oracle.Oracle(_cfg())
+    assert o.set_policy(4) == oracle.EINVAL and o.set_policy(-1) == oracle.EINVAL
+    assert o.set_policy("slo_aware") == oracle.OK
+
+
+def _in_order(policy, cand, match, lens, L0, B, slo):
+    """Literal in-order replay of one rule over a routed batch (Sec. 3.2 and
+    the single-criterion rules of Sec. 4.3) from its candidates and hits."""
+    n = len(lens)
+    L = L0.astype(np.int64).copy()
+    out = []
+    for r in range(n):
+        c = (int(cand[r]), int(cand[n + r]))
+        m = (int(match[r]), int(match[n + r]))
+        u = [int(lens[r]) - B * m[0], int(lens[r]) - B * m[1]]
+        t = [2000 + 3 * u[k] + int(L[c[k]]) // 4 for k in (0, 1)]
+        if policy == "least_loaded" or m[0] == m[1]:
+            k = 0 if L[c[0]] <= L[c[1]] else 1
+            if policy == "min_ttft":
+                k = 0 if t[0] <= t[1] else 1
+        elif policy == "min_ttft":
+            k = 0 if t[0] <= t[1] else 1
+        elif policy == "cache_affinity":
+            k = 0 if m[0] > m[1] else 1
+        else:
+            a = 0 if m[0] > m[1] else 1
+            k = a if t[a] <= slo or not L[c[1 - a]] < L[c[a]] else 1 - a
+        out.append(c[k])
+        L[c[k]] += u[k]
+    return np.array(out), L
+
+
+@pytest.mark.parametrize("policy", ["slo_aware", "cache_affinity", "least_loaded", "min_ttft"])
+def test_policy_routes_match_in_order_replay(policy):
+    """Whole batches under each rule equal the literal request-by-request
+    replay, and the per-rule invariants hold: cache affinity takes the
+    larger hit of every request (so its hit rate bounds every rule's from
+    above, the index being a snapshot), least loaded the candidate with the
+    smaller pre-update load."""
+    import oracle.harness as oh
+    wl = workloads.tiny(slo_us=20_000)
+    st = oh.setup(wl)
+    o = st["oracle"]
+    assert o.set_policy(policy) == oracle.OK
+    tok, off, L0 = st["tokens"], st["offsets"], st["loads0"]
+    out = o.route(tok, off, L0.copy())
+    lens = np.diff(off)
+    want, Lw = _in_order(policy, out["cand"], out["match"], lens, L0, wl.route.block, 20_000)
+    assert np.array_equal(out["chosen"], want)
+    assert np.array_equal(out["loads"], Lw)
+    n = len(lens)
+    m_ch = np.where(out["chosen"] == out["cand"][:n], out["match"][:n], out["match"][n:])
+    best = np.maximum(out["match"][:n], out["match"][n:])
+    if policy == "cache_affinity":
+        assert np.array_equal(m_ch, best)
+    assert np.all(m_ch <= best)
+    o.set_policy("slo_aware")
+
+
 def _read_narrative():
     rows = []
     with open(os.path.join(GOLDEN_DIR, "slo_narrative.txt")) as f:

@@ -284,6 +284,45 @@ def config_rows(reps):
     return rows
 
 
+def policy_rows(eng, wl, st, L0):
+    """The ablation study's selection rules (Sec. 4.3) on the large batch:
+    one unpipelined route per rule from the same initial loads; cache hit
+    rate (cached prompt tokens of the chosen instances over all prompt
+    tokens) and the coefficient of variation of the instances' queued work
+    afterwards (Sec. 2.2)."""
+    import numpy as np
+    import torch
+    n = wl.n_req
+    lens = np.diff(st["offsets_np"])
+    rows = {}
+    for pol in ("slo_aware", "cache_affinity", "least_loaded", "min_ttft"):
+        eng.set_policy(pol)
+        L = L0.clone()
+        o = eng.alloc_route_out(n)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        eng.route_into(st["tokens"], st["offsets"], L, o)
+        eng.sync()
+        ms = 1000.0 * (time.perf_counter() - t0)
+        ch = o["chosen"].cpu().numpy()
+        cand = o["cand"].cpu().numpy()
+        match = o["match"].cpu().numpy()
+        m = np.where(ch == cand[:n], match[:n], match[n:]).astype(np.int64)
+        fin = L.cpu().numpy()[:wl.route.n_inst].astype(np.float64)
+        rows[pol] = {"hit_rate": float((m * wl.route.block).sum() / lens.sum()),
+                     "final_load_cv": float(fin.std() / fin.mean()),
+                     "fewer_blocks_frac": float((o["flags"].cpu().numpy() & 1).mean()),
+                     "ms": ms}
+    eng.set_policy("slo_aware")
+    rows["note"] = ("one unpipelined dm_route_batch per rule from the same loads and index; "
+                    "hit_rate: cached prompt tokens on the chosen instances / prompt tokens; "
+                    "final_load_cv: std / mean of the live instances' queued work after the "
+                    "batch; fewer_blocks_frac: requests sent to the candidate with fewer cached "
+                    "blocks; min_ttft takes the serial selection path; ms: host wall time of "
+                    "the call and its sync")
+    return rows
+
+
 def elastic_leg(eng, wl, st, keys, L0, reps):
     """Rows a8/a9 at full size, timed on the host clock around each call (both
     entry points synchronise with the engine's stream before they return):
@@ -374,6 +413,8 @@ def main():
     ap.add_argument("--elastic-reps", type=int, default=5)
     ap.add_argument("--no-elastic", action="store_true",
                     help="skip the scale / re-route / rebalance timings")
+    ap.add_argument("--no-policies", action="store_true",
+                    help="skip the per-rule routes (cache affinity, least loaded, min TTFT)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after timing, copy 1 GiB device to device once (a plain copy kernel "
                          "of known size, to scale hardware byte counters)")
@@ -489,9 +530,11 @@ def main():
                         "stage_ms": {"keys_groups": ref_stage[0], "hash_match": ref_stage[1],
                                      "select": ref_stage[2], "block_offsets": ref_stage[3]}},
         "roofline": {"bound": "hbm",
-                     "kernel": "hash+match stage: hash_kernel<16> (prefix, leaders and "
-                               "members passes), lookup_kernel, order_init_kernel, radix sort "
-                               "passes, group_head_kernel, group scan, group_leader_kernel",
+                     "kernel": "hash+match stage: ring_key_kernel<16>, lookup_kernel, "
+                               "order_init_kernel, radix sort passes, group_head_kernel, "
+                               "group scan, group_leader_kernel, group_of_kernel, "
+                               "walk_kernel<16> (leaders, resume), member_record_kernel, "
+                               "member_kernel<16>, probe_pending_kernel",
                      "achieved": stage_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": stage_gbs / HBM_PEAK_GBS, "traffic": stage_traffic,
                      "algorithmic_bytes_per_launch": sbytes, "probes": probes,
@@ -501,7 +544,9 @@ def main():
                              "inspects) over the stage's device time from HIP events on the "
                              "stream it runs on, averaged over the timed steps"},
         "roofline_hash_match_pass": {"bound": "hbm",
-                                     "kernel": "hash_kernel<16> leaders and members passes",
+                                     "kernel": "walk_kernel<16> (leaders), "
+                                               "member_record_kernel, member_kernel<16>, "
+                                               "probe_pending_kernel, walk_kernel<16> (resume)",
                                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                      "frac": achieved / HBM_PEAK_GBS, "traffic": hash_traffic,
                                      "algorithmic_bytes_per_launch": hbytes, "ms": hashm_avg},
@@ -515,6 +560,9 @@ def main():
                                   "queued work after the batch (std / mean over live "
                                   "instances)"},
     }
+    if not args.no_policies:
+        log("selection rules of the ablation study")
+        res["policies"] = policy_rows(eng, wl, st, L0)
     if not args.no_elastic:
         log("elastic leg: scale, re-route, rebalance")
         res["elastic"] = elastic_leg(eng, wl, st, out["key"], L0, args.elastic_reps)

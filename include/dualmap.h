@@ -281,6 +281,29 @@ dm_status dm_route_stage_ms(dm_ctx* ctx, float* ms_host, int n);
  * DM_EDEVICE if the streams or their events cannot be created. */
 dm_status dm_set_pipelining(dm_ctx* ctx, int on);
 
+/* Selection rule between the two candidates of every request.  The
+ * SLO-aware rule is DualMap's (Sec. 3.2) and the default; the others are the
+ * single-criterion variants of the ablation study (Sec. 4.3):
+ *   DM_POLICY_CACHE_AFFINITY  the candidate with more cached blocks (equal
+ *                             hits: the less-loaded one, ties c1);
+ *   DM_POLICY_LEAST_LOADED    the candidate with the smaller load (ties c1);
+ *   DM_POLICY_MIN_TTFT        the candidate with the smaller estimated TTFT
+ *                             (ties c1).
+ * The ablation's "no rebalance" variant is the SLO-aware rule with no
+ * dm_rebalance calls.  Every rule updates the loads in request order as the
+ * SLO-aware one does; flag bit0 marks a chosen candidate with fewer cached
+ * blocks than the other (under the SLO-aware rule exactly its switches for
+ * the SLO).  The minimum-TTFT rule always takes the one-request-at-a-time
+ * selection path.  Applies to batches routed after the call; DM_EINVAL for
+ * an unknown rule. */
+typedef enum {
+    DM_POLICY_SLO_AWARE = 0,
+    DM_POLICY_CACHE_AFFINITY = 1,
+    DM_POLICY_LEAST_LOADED = 2,
+    DM_POLICY_MIN_TTFT = 3
+} dm_policy;
+dm_status dm_set_policy(dm_ctx* ctx, int policy);
+
 /* Wait for all work on the context's stream (and, with pipelining, on its
  * work, selection and epilogue streams); return and clear the first
  * device-side error since the last dm_sync. */

@@ -27,7 +27,7 @@ EXPORTS = ("dm_create", "dm_destroy", "dm_build_rings", "dm_ring_export", "dm_in
            "dm_index_erase", "dm_index_clear", "dm_index_size", "dm_route_batch",
            "dm_route_batch_noalloc",
            "dm_rebalance", "dm_scale", "dm_set_timing", "dm_route_stage_ms",
-           "dm_set_pipelining", "dm_sync", "dm_last_error")
+           "dm_set_pipelining", "dm_set_policy", "dm_sync", "dm_last_error")
 
 
 class DMError(RuntimeError):
@@ -89,6 +89,7 @@ def load_library(path: str = LIB_PATH):
         "dm_set_timing": (i32, [P, i32]),
         "dm_route_stage_ms": (i32, [P, P, i32]),
         "dm_set_pipelining": (i32, [P, i32]),
+        "dm_set_policy": (i32, [P, i32]),
         "dm_sync": (i32, [P]),
         "dm_last_error": (C.c_char_p, [P]),
     }
@@ -183,6 +184,14 @@ class DualMap:
         probing (see dm_set_pipelining): consecutive batches need distinct
         output buffers, and results are final after sync()."""
         self._check(self.lib.dm_set_pipelining(self._h, 1 if on else 0), "dm_set_pipelining")
+
+    POLICIES = {"slo_aware": 0, "cache_affinity": 1, "least_loaded": 2, "min_ttft": 3}
+
+    def set_policy(self, policy) -> None:
+        """Selection rule of later batches (see dm_set_policy): a name of
+        POLICIES or its number."""
+        p = self.POLICIES[policy] if isinstance(policy, str) else int(policy)
+        self._check(self.lib.dm_set_policy(self._h, p), "dm_set_policy")
 
     def stage_ms(self):
         """(hash, lookup+match, selection, block offsets) ms, averaged over the

@@ -601,6 +601,16 @@ static hipError_t make_streams(dm_ctx* c)
     return e;
 }
 
+dm_status dm_set_policy(dm_ctx* c, int policy)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (policy < DM_POLICY_SLO_AWARE || policy > DM_POLICY_MIN_TTFT)
+        return fail(c, DM_EINVAL, "dm_set_policy: unknown selection rule");
+    c->policy = (uint32_t)policy;
+    return DM_OK;
+}
+
 dm_status dm_set_pipelining(dm_ctx* c, int on)
 {
     if (!c)

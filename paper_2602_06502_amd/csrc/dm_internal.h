@@ -135,6 +135,7 @@ struct dm_ctx {
     // batch's work first waits for the batch two back to finish, so at most
     // two batches' outputs and work arrays (by batch parity) are in use.
     bool pipelined = false;
+    uint32_t policy = DM_POLICY_SLO_AWARE;  // selection rule of later batches
     hipStream_t work_stream = nullptr, sel_stream = nullptr, out_stream = nullptr;
     hipEvent_t in_ready = nullptr;                 // caller's stream: inputs of the batch
     hipEvent_t prep_done = nullptr;                // work stream: records packed

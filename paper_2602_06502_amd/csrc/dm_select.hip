@@ -5,6 +5,10 @@
 // less loaded, first candidate on ties); the chosen instance's load grows by
 // the request's uncached tokens before the next request is decided.  The
 // batch result is therefore defined by processing the requests one by one.
+// The single-criterion rules of the ablation study (Sec. 4.3) run on the same
+// machinery: cache affinity is the SLO-aware rule with an unbounded TTFT
+// budget, least load is the equal-match rule for every request (both take
+// the fast path), and minimum TTFT compares the two estimates (serial path).
 //
 // Fast path (at most 256 live instances, uncached counts within 32 bits,
 // live loads within 2^62 of the smallest; checked on the device), on 32-bit
@@ -39,14 +43,22 @@ namespace {
 
 constexpr int kSelSlot = kSlotSelect;  // selection work arrays
 
-// Shared by both selection kernels: the SLO-aware rule given the two
-// candidates' pre-update loads.  kind bit0 = equal match, bit1 = c1 is the
-// cache-affine candidate; th = the affine candidate's load below which its
-// TTFT meets the SLO.
-__device__ __forceinline__ bool pick_first(uint32_t kind, int64_t L1, int64_t L2, int64_t th)
+// Shared by every selection kernel: the rule given the two candidates'
+// pre-update loads.  kind bit0 = compare the loads (equal match, or the
+// least-load rule), bit1 = c1 is the cache-affine candidate, bit2 = compare
+// the TTFT estimates, bit3 = keep the cache-affine candidate whatever its
+// TTFT; th = the affine candidate's load below which its TTFT meets the SLO,
+// or for bit2 per * (u2 - u1), so that t1 <= t2 reads
+// floor(L1 / 2^q) - floor(L2 / 2^q) <= th.
+__device__ __forceinline__ bool pick_first(uint32_t kind, int64_t L1, int64_t L2, int64_t th,
+                                           uint32_t qshift)
 {
+    if (kind & 4)
+        return (L1 >> qshift) - (L2 >> qshift) <= th;
     if (kind & 1)
         return L1 <= L2;
+    if (kind & 8)
+        return (kind & 2) != 0;
     if (kind & 2)
         return L1 < th || !(L2 < L1);
     return !(L2 < th || !(L1 < L2));
@@ -55,13 +67,15 @@ __device__ __forceinline__ bool pick_first(uint32_t kind, int64_t L1, int64_t L2
 // Per-lane request record for the serial loop and the output epilogue.
 struct SelRec {
     uint32_t c1, c2, kind;
+    bool eq, aff1;  // equal match; c1 has more cached blocks
+    bool a2;        // the fast path's records take c2 as their "a" instance
     int64_t u1, u2, th;
 };
 
 __device__ __forceinline__ SelRec load_rec(const int64_t* offsets, uint64_t n, uint64_t r, bool ok,
                                            uint32_t bshift, const uint32_t* cand,
                                            const uint32_t* match, int64_t base, int64_t per,
-                                           uint32_t qshift, int64_t slo)
+                                           uint32_t qshift, int64_t slo, uint32_t policy)
 {
     SelRec s;
     s.c1 = ok ? cand[r] : 0;
@@ -70,10 +84,22 @@ __device__ __forceinline__ SelRec load_rec(const int64_t* offsets, uint64_t n, u
     const int64_t len = ok ? offsets[r + 1] - offsets[r] : 0;
     s.u1 = len - ((int64_t)m1 << bshift);
     s.u2 = len - ((int64_t)m2 << bshift);
-    const bool eq = m1 == m2, aff1 = m1 > m2;
+    s.eq = m1 == m2;
+    s.aff1 = m1 > m2;
     // T_a <= slo  <=>  floor(L_a / 2^q) <= slo - base - per*u_a  <=>  L_a < th
-    s.th = (slo - base - per * (aff1 ? s.u1 : s.u2) + 1) * ((int64_t)1 << qshift);
-    s.kind = (eq ? 1u : 0u) | (aff1 ? 2u : 0u);
+    s.th = (slo - base - per * (s.aff1 ? s.u1 : s.u2) + 1) * ((int64_t)1 << qshift);
+    s.kind = (s.eq ? 1u : 0u) | (s.aff1 ? 2u : 0u);
+    s.a2 = !s.eq && !s.aff1;
+    if (policy == DM_POLICY_CACHE_AFFINITY) {
+        s.kind |= 8u;
+    } else if (policy == DM_POLICY_LEAST_LOADED) {
+        s.kind = 1u;
+        s.a2 = false;
+    } else if (policy == DM_POLICY_MIN_TTFT) {
+        s.kind = 4u;
+        s.th = per * (s.u2 - s.u1);
+        s.a2 = false;
+    }
     return s;
 }
 
@@ -81,29 +107,29 @@ __device__ __forceinline__ void store_out(const SelRec& s, uint64_t r, int64_t L
                                           uint8_t* flags, uint32_t* chosen, int64_t* ttft,
                                           int64_t base, int64_t per, uint32_t qshift, int64_t slo)
 {
-    const bool pick1 = pick_first(s.kind, L1, L2, s.th);
+    const bool pick1 = pick_first(s.kind, L1, L2, s.th, qshift);
     const int64_t t1 = base + per * s.u1 + (L1 >> qshift);
     const int64_t t2 = base + per * s.u2 + (L2 >> qshift);
     uint32_t f = flags[r];
     if (t1 > slo && t2 > slo)
         f |= 2;
-    if (s.kind & 1)
+    if (s.eq)
         f |= 4;
-    else if (pick1 != ((s.kind & 2) != 0))
+    else if (pick1 != s.aff1)
         f |= 1;
     chosen[r] = pick1 ? s.c1 : s.c2;
     ttft[r] = pick1 ? t1 : t2;
     flags[r] = (uint8_t)f;
 }
 
-// Serial SLO-aware selection, loads in R register banks of one wave.
+// Serial selection, loads in R register banks of one wave.
 template <int R>
 __global__ __launch_bounds__(kWave) void select_kernel(
     const int64_t* __restrict__ offsets, uint64_t n, uint32_t bshift,
     const uint32_t* __restrict__ cand, const uint32_t* __restrict__ match,
     uint8_t* __restrict__ flags, uint32_t* __restrict__ chosen, int64_t* __restrict__ ttft,
     int64_t* __restrict__ loads, uint32_t S, int64_t base, int64_t per, uint32_t qshift, int64_t slo,
-    const uint32_t* __restrict__ plan)
+    uint32_t policy, const uint32_t* __restrict__ plan)
 {
     if (!plan[0])
         return;
@@ -131,7 +157,8 @@ __global__ __launch_bounds__(kWave) void select_kernel(
     for (uint64_t r0 = 0; r0 < n; r0 += kWave) {
         const uint64_t r = r0 + lane;
         const bool ok = r < n;
-        const SelRec s = load_rec(offsets, n, r, ok, bshift, cand, match, base, per, qshift, slo);
+        const SelRec s = load_rec(offsets, n, r, ok, bshift, cand, match, base, per, qshift, slo,
+                                  policy);
         int64_t myL1 = 0, myL2 = 0;
         const int cnt = (int)(n - r0 < (uint64_t)kWave ? n - r0 : kWave);
         for (int j = 0; j < cnt; j++) {
@@ -142,7 +169,7 @@ __global__ __launch_bounds__(kWave) void select_kernel(
             const int64_t U1 = (int64_t)readlane_u64((uint64_t)s.u1, j);
             const int64_t U2 = (int64_t)readlane_u64((uint64_t)s.u2, j);
             const int64_t L1 = get(C1), L2 = get(C2);
-            const bool pick1 = pick_first(K, L1, L2, TH);
+            const bool pick1 = pick_first(K, L1, L2, TH, qshift);
             const uint32_t ch = pick1 ? C1 : C2;
             const int64_t nv = (pick1 ? L1 : L2) + (pick1 ? U1 : U2);
             const uint32_t bank = ch >> 6, l = ch & 63;
@@ -175,7 +202,7 @@ __global__ __launch_bounds__(kWave) void select_lds_kernel(
     const uint32_t* __restrict__ cand, const uint32_t* __restrict__ match,
     uint8_t* __restrict__ flags, uint32_t* __restrict__ chosen, int64_t* __restrict__ ttft,
     int64_t* __restrict__ loads, uint32_t S, int64_t base, int64_t per, uint32_t qshift, int64_t slo,
-    const uint32_t* __restrict__ plan)
+    uint32_t policy, const uint32_t* __restrict__ plan)
 {
     if (!plan[0])
         return;
@@ -187,7 +214,8 @@ __global__ __launch_bounds__(kWave) void select_lds_kernel(
     for (uint64_t r0 = 0; r0 < n; r0 += kWave) {
         const uint64_t r = r0 + lane;
         const bool ok = r < n;
-        const SelRec s = load_rec(offsets, n, r, ok, bshift, cand, match, base, per, qshift, slo);
+        const SelRec s = load_rec(offsets, n, r, ok, bshift, cand, match, base, per, qshift, slo,
+                                  policy);
         int64_t myL1 = 0, myL2 = 0;
         const int cnt = (int)(n - r0 < (uint64_t)kWave ? n - r0 : kWave);
         for (int j = 0; j < cnt; j++) {
@@ -198,7 +226,7 @@ __global__ __launch_bounds__(kWave) void select_lds_kernel(
             const int64_t U1 = (int64_t)readlane_u64((uint64_t)s.u1, j);
             const int64_t U2 = (int64_t)readlane_u64((uint64_t)s.u2, j);
             const int64_t L1 = L[C1], L2 = L[C2];
-            const bool pick1 = pick_first(K, L1, L2, TH);
+            const bool pick1 = pick_first(K, L1, L2, TH, qshift);
             const uint32_t ch = pick1 ? C1 : C2;
             const int64_t nv = (pick1 ? L1 : L2) + (pick1 ? U1 : U2);
             __syncthreads();
@@ -302,7 +330,8 @@ __global__ __launch_bounds__(256) void sel_prep_kernel(
     const int64_t* __restrict__ offsets, uint64_t n, uint32_t bshift,
     const uint32_t* __restrict__ cand, const uint32_t* __restrict__ match,
     const uint32_t* __restrict__ dense, uint32_t n_live, int64_t tbase, int64_t per,
-    uint32_t qshift, int64_t slo, SelPack* __restrict__ rec, unsigned long long* __restrict__ grow)
+    uint32_t qshift, int64_t slo, uint32_t policy, SelPack* __restrict__ rec,
+    unsigned long long* __restrict__ grow)
 {
     __shared__ unsigned long long sg[kFastMaxLive];
     const bool track = n_live <= kFastMaxLive;
@@ -316,15 +345,20 @@ __global__ __launch_bounds__(256) void sel_prep_kernel(
         const uint32_t m1 = match[r], m2 = match[n + r];
         const int64_t len = offsets[r + 1] - offsets[r];
         const int64_t u1 = len - ((int64_t)m1 << bshift), u2 = len - ((int64_t)m2 << bshift);
-        const bool eq = m1 == m2, aff2 = m2 > m1;
+        // least load: every request as an equal match, c1 as "a"
+        const bool eq = m1 == m2 || policy == DM_POLICY_LEAST_LOADED;
+        const bool aff2 = m2 > m1 && policy != DM_POLICY_LEAST_LOADED;
         const uint32_t d1 = dense[cand[r]], d2 = dense[cand[n + r]];
         // T_a <= slo  <=>  floor(L_a / 2^q) <= slo - tbase - per*u_a  <=>
         // L_a < (slo - tbase - per*u_a + 1) 2^q, i.e. "take a iff L_a <=
         // max(th, L_o)" with th one less.  The 32-bit walk uses absolute loads
         // in [0, 2^31 - 1), so th is clamped to that range; equal matches:
-        // take c1 iff L1 <= L2, th = -2^31.
+        // take c1 iff L1 <= L2, th = -2^31; cache affinity: always a,
+        // th = 2^31 - 1.
         int32_t th = INT32_MIN;
-        if (!eq) {
+        if (!eq && policy == DM_POLICY_CACHE_AFFINITY) {
+            th = INT32_MAX;
+        } else if (!eq) {
             const int64_t t = (slo - tbase - per * (aff2 ? u2 : u1) + 1) * ((int64_t)1 << qshift) - 1;
             th = (int32_t)(t < -1 ? -1 : (t > INT32_MAX ? INT32_MAX : t));
         }
@@ -363,11 +397,13 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
                                                        uint32_t n_live,
                                                        const int64_t* __restrict__ base,
                                                        const unsigned long long* __restrict__ grow,
+                                                       uint32_t policy,
                                                        uint32_t* __restrict__ plan)
 {
     __shared__ int ok_all, narrow;
     if (threadIdx.x == 0) {
-        ok_all = n_live <= kFastMaxLive && grow[kMaxSlots] == 0;
+        // the minimum-TTFT rule has no windowed form: serial path
+        ok_all = n_live <= kFastMaxLive && grow[kMaxSlots] == 0 && policy != DM_POLICY_MIN_TTFT;
         narrow = 1;
     }
     __syncthreads();
@@ -906,7 +942,7 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
                                              uint32_t n_live, int64_t* __restrict__ loads,
                                              int64_t b0, longlong2* __restrict__ lpre,
                                              int64_t tbase, int64_t per, uint32_t qshift,
-                                             int64_t slo, T* L)
+                                             int64_t slo, uint32_t policy, T* L)
 {
     constexpr bool wide = sizeof(T) == 8;
     const int lane = lane_id();
@@ -924,11 +960,15 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
         const T pua = (T)cur.pua, puo = (T)cur.puo, pua2 = (T)cur.pua2, puo2 = (T)cur.puo2;
         if constexpr (wide) {
             // the packed bounds are clamped to 32 bits: recompute them
-            // exactly, relative to the base (equal matches: -inf)
+            // exactly, relative to the base (equal matches: -inf; cache
+            // affinity: +inf)
+            const bool keep_a = policy == DM_POLICY_CACHE_AFFINITY;
             auto exact = [&](int32_t packed, uint32_t u) -> T {
-                return packed == INT32_MIN
-                           ? (T)INT64_MIN
-                           : (T)((slo - tbase - per * (int64_t)u + 1) * ((int64_t)1 << qshift) - 1 - b0);
+                return packed == INT32_MIN ? (T)INT64_MIN
+                       : keep_a            ? (T)INT64_MAX
+                                           : (T)((slo - tbase - per * (int64_t)u + 1) *
+                                                     ((int64_t)1 << qshift) -
+                                                 1 - b0);
             };
             const T th = exact(cur.th, cur.ua), pth = exact(cur.pth, cur.pua);
             const T pth2 = exact(cur.pth2, cur.pua2);
@@ -1034,7 +1074,7 @@ __global__ __launch_bounds__(kWave) void select_fast_kernel(
     const uint32_t* __restrict__ live_ids, uint32_t n_live, int64_t* __restrict__ loads,
     const uint32_t* __restrict__ plan,
     const int64_t* __restrict__ base, longlong2* __restrict__ lpre, int64_t tbase, int64_t per,
-    uint32_t qshift, int64_t slo)
+    uint32_t qshift, int64_t slo, uint32_t policy)
 {
     // Claim the whole register file of this wave's SIMD (256 + 256
     // registers), so that no wave of another kernel shares its issue slots:
@@ -1047,10 +1087,10 @@ __global__ __launch_bounds__(kWave) void select_fast_kernel(
     const int64_t b0 = plan[2] ? base[0] : 0;  // 32-bit walks use absolute loads
     if (plan[2])
         walk_windows<int64_t>(rec, nwin, live_ids, n_live, loads, b0, lpre, tbase, per, qshift, slo,
-                              L);
+                              policy, L);
     else
         walk_windows<int32_t>(rec, nwin, live_ids, n_live, loads, b0, lpre, tbase, per, qshift, slo,
-                              reinterpret_cast<int32_t*>(L));
+                              policy, reinterpret_cast<int32_t*>(L));
 }
 
 __global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, uint32_t bshift,
@@ -1060,7 +1100,8 @@ __global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, 
                                const int64_t* __restrict__ base,
                                const uint32_t* __restrict__ plan, uint8_t* __restrict__ flags,
                                uint32_t* __restrict__ chosen, int64_t* __restrict__ ttft,
-                               int64_t tbase, int64_t per, uint32_t qshift, int64_t slo)
+                               int64_t tbase, int64_t per, uint32_t qshift, int64_t slo,
+                               uint32_t policy)
 {
     if (!plan[1])
         return;
@@ -1068,7 +1109,8 @@ __global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, 
     const int64_t b0 = wide ? base[0] : 0;
     for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
          r += (uint64_t)gridDim.x * blockDim.x) {
-        SelRec s = load_rec(offsets, n, r, true, bshift, cand, match, tbase, per, qshift, slo);
+        SelRec s = load_rec(offsets, n, r, true, bshift, cand, match, tbase, per, qshift, slo,
+                            policy);
         const uint32_t q = slot_of[r];
         if (q >= nslots)  // only when the packing failed, which the status reports
             continue;
@@ -1083,7 +1125,8 @@ __global__ void sel_out_kernel(const int64_t* __restrict__ offsets, uint64_t n, 
             Lo = lp.y;
         }
         // the walk records (L_a, L_o); a is c2 when c2 has the longer match
-        const bool a_is_c2 = s.kind == 0;
+        // (never under the least-load rule)
+        const bool a_is_c2 = s.a2;
         store_out(s, r, b0 + (a_is_c2 ? Lo : La), b0 + (a_is_c2 ? La : Lo), flags, chosen, ttft,
                   tbase, per, qshift, slo);
     }
@@ -1097,7 +1140,7 @@ void launch_select(dm_ctx* c, hipStream_t st, const int64_t* offsets, uint64_t n
     select_kernel<R><<<1, kWave, 0, st>>>(offsets, n, bshift, out->cand, out->match,
                                                  out->flags, out->chosen, out->ttft_us, loads,
                                                  k.max_slots, k.ttft_base_us, k.ttft_per_token_us,
-                                                 c->shift_div, k.slo_us, plan);
+                                                 c->shift_div, k.slo_us, c->policy, plan);
 }
 
 
@@ -1232,7 +1275,7 @@ hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uin
     // ones with one atomic per instance, and those atomics meet on a few lines
     sel_prep_kernel<<<grid_for(n, 256, 512), 256, 0, st>>>(
         offsets, n, block_shift(c), out->cand, out->match, c->d_dense, NL, k.ttft_base_us,
-        k.ttft_per_token_us, c->shift_div, k.slo_us, b.prep, b.grow);
+        k.ttft_per_token_us, c->shift_div, k.slo_us, c->policy, b.prep, b.grow);
     if (b.nblk > 0)
         sel_level_kernel<<<(uint32_t)b.nblk, kWave, 0, st>>>(b.prep, n, b.info, b.slotmap, b.wdepth,
                                                              b.wcount, c->d_status);
@@ -1255,10 +1298,11 @@ hipError_t select_run(dm_ctx* c, hipStream_t ss, hipStream_t os, hipEvent_t sel_
     const dm_config& k = c->cfg;
     const uint32_t S = k.max_slots, NL = c->n_live, bshift = block_shift(c);
     sel_base_kernel<<<1, 256, 0, ss>>>(loads, c->d_live_ids, NL, b.base, b.grow);
-    sel_plan_kernel<<<1, 256, 0, ss>>>(loads, c->d_live_ids, NL, b.base, b.grow, b.plan);
+    sel_plan_kernel<<<1, 256, 0, ss>>>(loads, c->d_live_ids, NL, b.base, b.grow, c->policy,
+                                       b.plan);
     select_fast_kernel<<<1, kWave, 0, ss>>>(b.rec, b.total, c->d_live_ids, NL, loads, b.plan,
                                             b.base, b.lpre, k.ttft_base_us, k.ttft_per_token_us,
-                                            c->shift_div, k.slo_us);
+                                            c->shift_div, k.slo_us, c->policy);
     if (S <= 64)
         launch_select<1>(c, ss, offsets, n, bshift, out, loads, b.plan);
     else if (S <= 128)
@@ -1271,7 +1315,7 @@ hipError_t select_run(dm_ctx* c, hipStream_t ss, hipStream_t os, hipEvent_t sel_
         select_lds_kernel<<<1, kWave, 0, ss>>>(offsets, n, bshift, out->cand, out->match,
                                                out->flags, out->chosen, out->ttft_us, loads, S,
                                                k.ttft_base_us, k.ttft_per_token_us, c->shift_div,
-                                               k.slo_us, b.plan);
+                                               k.slo_us, c->policy, b.plan);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
     if (os != ss) {
@@ -1282,7 +1326,7 @@ hipError_t select_run(dm_ctx* c, hipStream_t ss, hipStream_t os, hipEvent_t sel_
     sel_out_kernel<<<grid_for(n, 256, 8192), 256, 0, os>>>(
         offsets, n, bshift, out->cand, out->match, b.lpre, b.slot_of, b.nslots, b.base, b.plan,
         out->flags, out->chosen, out->ttft_us, k.ttft_base_us, k.ttft_per_token_us, c->shift_div,
-        k.slo_us);
+        k.slo_us, c->policy);
     return hipGetLastError();
 }
 

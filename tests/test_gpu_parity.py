@@ -112,10 +112,13 @@ def test_random_small_parity(seed, n_inst, vnodes, block):
     run_pair(wl)
 
 
-def _pair_with_loads(wl, L0):
+def _pair_with_loads(wl, L0, policy=None):
     gh = _h()
     eng = gh.engine_for(wl)
     o = oh.oracle_for(wl)
+    if policy is not None:
+        eng.set_policy(policy)
+        assert o.set_policy(policy) == oracle.OK
     gh.prefill_from_prior(eng, wl)
     oh.prefill_from_prior(o, wl)
     tok, off = workloads.prompts(wl, wl.n_req, sub=0)
@@ -139,6 +142,69 @@ def test_selection_wide_loads_parity(n_inst, top):
     _say("wide loads", n_inst, top)
     r = _pair_with_loads(wl, L0)
     assert (r["flags"] & 1).sum() + (r["flags"] & 4).sum() > 0
+
+
+@pytest.mark.parametrize("policy", ["cache_affinity", "least_loaded", "min_ttft"])
+@pytest.mark.parametrize("n_inst,wide", [(8, 0), (200, 0), (150, 1), (300, 0), (8, 2)])
+def test_policy_selection_parity(policy, n_inst, wide):
+    """The single-criterion rules of the ablation study (Sec. 4.3) on every
+    selection path: the windowed walk on 32-bit loads (8 and 200 instances)
+    and on 64-bit loads (spread beyond 2^30), the serial path with loads in
+    registers (spread beyond 2^62) and in LDS (300 instances).  The
+    minimum-TTFT rule always runs serially."""
+    wl = workloads.small_random(61 + n_inst, n_inst, 3, 16, 700,
+                                slo_us=6_000_000_000 if wide else 20_000)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    if wide:
+        L0[::3] += 1 << 40
+        L0[1] = (1 << 62) - (1 << 50) if wide == 1 else (1 << 62) + (1 << 50)
+    _say("policy", policy, n_inst, wide)
+    r = _pair_with_loads(wl, L0, policy)
+    fewer = (r["flags"] & 1) != 0
+    if policy == "cache_affinity":
+        assert not fewer.any()
+    else:
+        assert fewer.any()
+
+
+def test_policy_changes_between_pipelined_batches():
+    """The rule is taken when a batch is routed: pipelined batches under
+    different rules, each against the oracle under the same rule in order."""
+    gh = _h()
+    wl = workloads.tiny(slo_us=20_000)
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    gh.prefill_from_prior(eng, wl)
+    oh.prefill_from_prior(o, wl)
+    tok, off = workloads.prompts(wl, wl.n_req, sub=0)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    Ld = gh.to_dev(L0, eng.device)
+    td, od = gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device)
+    eng.set_pipelining(True)
+    outs = []
+    seq = ["least_loaded", "slo_aware", "min_ttft", "cache_affinity", "slo_aware"]
+    for pol in seq:
+        eng.set_policy(pol)
+        outs.append(eng.route(td, od, Ld))
+    eng.sync()
+    eng.set_pipelining(False)
+    L = L0.copy()
+    for pol, g in zip(seq, outs):
+        assert o.set_policy(pol) == oracle.OK
+        r = o.route(tok, off, L)
+        compare_route(g, r, wl.n_req)
+        L = r["loads"]
+    assert np.array_equal(cpu(Ld), L)
+    o.set_policy("slo_aware")
+
+
+def test_policy_rejects_unknown_rule():
+    gh = _h()
+    import paper_2602_06502_amd as pk
+    eng = gh.engine_for(workloads.tiny())
+    for bad in (-1, 4, 99):
+        with pytest.raises(pk.DMError) as ei:
+            eng.set_policy(bad)
+        assert ei.value.status == pk.DM_EINVAL
 
 
 def _disjoint_pair_prompts(o, rng, n_pool):

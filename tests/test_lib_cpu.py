@@ -68,6 +68,7 @@ def test_null_context_is_rejected():
     assert lib.dm_rebalance(None, None, None, None, 0) == pk.DM_EINVAL
     assert lib.dm_scale(None, None, 0, None, 0, None, 0, None, None, None, None) == pk.DM_EINVAL
     assert lib.dm_index_insert(None, 0, None, 0) == pk.DM_EINVAL
+    assert lib.dm_set_policy(None, 0) == pk.DM_EINVAL
     assert lib.dm_last_error(None) == b"null context"
     lib.dm_destroy(None)
 

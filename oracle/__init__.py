@@ -79,8 +79,12 @@ def lib():
             "or_ttft": (i64, [P, i64, i64]),
             "or_candidates": (i32, [P, u64, u64, P, P]),
             "or_select": (u32, [P, u32, u32, u64, u64, i64, P, P, P]),
-            "or_route": (i32, [P, P, P, u64, P, P, P, P, P, P, P, P]),
+            "or_route": (i32, [P, P, P, u64, P, P, P, P, P, P, P, P, P]),
             "or_set_policy": (i32, [P, i32]),
+            "or_keylen_enable": (i32, [P, u64]),
+            "or_keylen_window": (i32, [P]),
+            "or_keylen_export": (i32, [P, P, u64, P]),
+            "or_ring_key_at": (u64, [P, i32, P, u64]),
             "or_rebalance": (i32, [P, P, P, P, P, P, P, P, i64, P, P, P, P, P, P, u64, P]),
             "or_scale": (i32, [P, P, u32, P, u32, P, u64, P, P, P, P]),
             "or_n_live": (u32, [P]),
@@ -168,6 +172,27 @@ class Oracle:
         p = self.POLICIES.get(policy, policy) if isinstance(policy, str) else int(policy)
         return lib().or_set_policy(self._h, p)
 
+    def keylen_enable(self, max_nodes: int) -> int:
+        """Adaptive hash-key length: an empty prefix hotness tree with room for
+        max_nodes extended prefixes (0 turns it off)."""
+        return lib().or_keylen_enable(self._h, int(max_nodes))
+
+    def keylen_window(self) -> int:
+        """Close the current window: hot leaves extend, cold nodes shrink."""
+        return lib().or_keylen_window(self._h)
+
+    def keylen_tree(self) -> np.ndarray:
+        """The extended prefixes (canon f1 keys of their last blocks), ascending."""
+        n = C.c_uint64()
+        lib().or_keylen_export(self._h, None, 0, C.byref(n))
+        a = np.zeros(max(int(n.value), 1), np.uint64)
+        lib().or_keylen_export(self._h, _p(a), len(a), C.byref(n))
+        return a[:int(n.value)]
+
+    def ring_key_at(self, s: int, tokens: np.ndarray, kr: int) -> int:
+        t = np.ascontiguousarray(tokens, dtype=np.int32)
+        return int(lib().or_ring_key_at(self._h, s, _p(t), int(kr)))
+
     def build_rings(self, ids: Sequence[int]) -> int:
         a = np.ascontiguousarray(ids, dtype=np.uint32)
         return lib().or_build_rings(self._h, _p(a), len(a))
@@ -242,14 +267,15 @@ class Oracle:
         L = np.array(loads, dtype=np.int64, copy=True)
         out = dict(key=np.zeros(2 * n, np.uint64), cand=np.zeros(2 * n, np.uint32),
                    match=np.zeros(2 * n, np.uint32), chosen=np.zeros(n, np.uint32),
-                   ttft=np.zeros(n, np.int64), flags=np.zeros(n, np.uint8))
+                   ttft=np.zeros(n, np.int64), flags=np.zeros(n, np.uint8),
+                   key_len=np.zeros(n, np.uint32))
         bk = None
         if block_keys:
             nfull = np.diff(o) // self.block
             bk = np.zeros(int(nfull.sum()), np.uint64)
         rc = lib().or_route(self._h, _p(t), _p(o), n, _p(L), _p(out["key"]), _p(out["cand"]),
                             _p(out["match"]), _p(out["chosen"]), _p(out["ttft"]),
-                            _p(out["flags"]), _p(bk))
+                            _p(out["flags"]), _p(bk), _p(out["key_len"]))
         if rc != OK:
             raise RuntimeError("or_route failed with status %d" % rc)
         out["loads"] = L

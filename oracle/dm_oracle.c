@@ -53,6 +53,14 @@ typedef struct {
     uint64_t **set;           /* per instance: sorted unique cached block keys  */
     uint64_t *set_len;
     int policy;               /* selection rule, OR_POLICY_* (default SLO-aware)*/
+    /* adaptive hash-key length (Sec. 3.2): the prefix hotness tree      */
+    int kl_on;
+    uint64_t kl_max;          /* most extended prefixes the tree may hold       */
+    uint64_t *kl_ext;         /* sorted canon keys of the extended prefixes     */
+    uint64_t kl_n;
+    uint64_t *kl_log;         /* prefixes on routed requests' paths, this window*/
+    uint64_t kl_log_n, kl_log_cap;
+    uint64_t kl_win;          /* requests routed in this window                 */
 } or_state;
 
 /* Selection rules between the two candidates: DualMap's SLO-aware rule and
@@ -131,11 +139,21 @@ uint64_t or_chain(const or_state *st, int s, const int32_t *t, int64_t len, uint
  * Sec. A.7): the block key of the last block of the hashed prefix, which is
  * the first K full blocks (fewer if the prompt is shorter).  A prompt with no
  * full block maps to the key of the empty prefix, mix64(H[-1] xor seed). */
+uint64_t or_ring_key_at(const or_state *st, int s, const int32_t *t, uint64_t kr);
+
 uint64_t or_ring_key(const or_state *st, int s, const int32_t *t, int64_t len)
 {
     const uint32_t B = st->cfg.block_size;
     uint64_t nfull = len > 0 ? (uint64_t)len / B : 0;
     uint64_t kr = nfull < st->cfg.key_blocks ? nfull : st->cfg.key_blocks;
+    return or_ring_key_at(st, s, t, kr);
+}
+
+/* Ring key of the first kr full blocks under function s (kr = 0: the
+ * empty-prefix key).  The prompt must hold kr full blocks. */
+uint64_t or_ring_key_at(const or_state *st, int s, const int32_t *t, uint64_t kr)
+{
+    const uint32_t B = st->cfg.block_size;
     uint64_t H = st->h_init[s];
     for (uint64_t b = 0; b < kr; b++)
         H = H * st->mult[s] + or_nh(t + b * B, st->kk[s], B);
@@ -261,6 +279,8 @@ void or_destroy(or_state *st)
 {
     if (!st)
         return;
+    free(st->kl_ext);
+    free(st->kl_log);
     for (uint32_t i = 0; i < st->cfg.max_slots; i++)
         free(st->set[i]);
     free(st->set); free(st->set_len); free(st->live);
@@ -563,15 +583,166 @@ int or_set_policy(or_state *st, int policy)
     return OR_OK;
 }
 
+/* ------------------------------------------------------------------------- */
+/* Adaptive hash-key length (Sec. 3.2, "How long prefix is appropriate for   */
+/* the hash key?"; Sec. A.1.1, Fig. prefix-len).                              */
+/* ------------------------------------------------------------------------- */
+
+/* The prefix hotness tree.  A node is a prompt prefix of d >= K full blocks,
+ * named by the f1 key of its last block (that key covers the whole prefix);
+ * the nodes of depth K are the roots.  The tree is held as the set of its
+ * extended nodes, those whose children exist.  A request's hash prefix is
+ * its path from its root to a leaf: K_r is the smallest d >= K whose prefix
+ * is not extended, and never more than the request's full blocks (fewer
+ * than K full blocks: all of them, as without the tree).
+ *
+ * Traffic ratios come from windows the caller closes (or_keylen_window):
+ * rho of a node = requests of the window whose path passes through it /
+ * requests routed in the window.  At the close, with n live instances, a
+ * leaf with rho > 2/n becomes extended (its children are added, so its
+ * requests hash one block more and spread over more candidate pairs) and an
+ * extended node with rho < 1/n is no longer (its children are removed). */
+
+static int kl_extended(const or_state *st, uint64_t ck)
+{
+    uint64_t lo = 0, hi = st->kl_n;
+    while (lo < hi) {
+        uint64_t mid = lo + (hi - lo) / 2;
+        if (st->kl_ext[mid] < ck)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo < st->kl_n && st->kl_ext[lo] == ck;
+}
+
+/* K_r of a request with block keys h1[0..nfull). */
+static uint64_t kl_key_len(const or_state *st, const uint64_t *h1, uint64_t nfull)
+{
+    const uint64_t K = st->cfg.key_blocks;
+    if (nfull <= K || !st->kl_on)
+        return nfull < K ? nfull : K;
+    uint64_t d = K;
+    while (d < nfull && kl_extended(st, canon(h1[d - 1])))
+        d++;
+    return d;
+}
+
+static int kl_log_push(or_state *st, uint64_t ck)
+{
+    if (st->kl_log_n == st->kl_log_cap) {
+        uint64_t cap = st->kl_log_cap ? 2 * st->kl_log_cap : 1024;
+        uint64_t *a = (uint64_t *)realloc(st->kl_log, cap * sizeof(uint64_t));
+        if (!a)
+            return OR_ENOMEM;
+        st->kl_log = a;
+        st->kl_log_cap = cap;
+    }
+    st->kl_log[st->kl_log_n++] = ck;
+    return OR_OK;
+}
+
+/* Turn the tree on with room for max_nodes extended prefixes (empty tree,
+ * empty window), or off (max_nodes = 0). */
+int or_keylen_enable(or_state *st, uint64_t max_nodes)
+{
+    if (!st)
+        return OR_EINVAL;
+    free(st->kl_ext);
+    free(st->kl_log);
+    st->kl_ext = NULL;
+    st->kl_log = NULL;
+    st->kl_n = st->kl_log_n = st->kl_log_cap = st->kl_win = 0;
+    st->kl_on = max_nodes > 0;
+    st->kl_max = max_nodes;
+    if (max_nodes) {
+        st->kl_ext = (uint64_t *)malloc(max_nodes * sizeof(uint64_t));
+        if (!st->kl_ext) {
+            st->kl_on = 0;
+            return OR_ENOMEM;
+        }
+    }
+    return OR_OK;
+}
+
+static int cmp_u64(const void *a, const void *b)
+{
+    uint64_t x = *(const uint64_t *)a, y = *(const uint64_t *)b;
+    return x < y ? -1 : (x > y ? 1 : 0);
+}
+
+/* Close the window: apply the hot and cold rules to every node with the
+ * window's counts, then start an empty window.  OR_EFULL (tree unchanged,
+ * window still closed) if the new tree would hold more than max_nodes
+ * extended prefixes. */
+int or_keylen_window(or_state *st)
+{
+    if (!st || !st->kl_on)
+        return OR_EINVAL;
+    if (st->n_live == 0)
+        return OR_ESTATE;
+    const uint64_t W = st->kl_win, n = st->n_live;
+    qsort(st->kl_log, st->kl_log_n, sizeof(uint64_t), cmp_u64);
+    uint64_t *next = (uint64_t *)malloc((st->kl_log_n + st->kl_n + 1) * sizeof(uint64_t));
+    if (!next)
+        return OR_ENOMEM;
+    uint64_t nn = 0;
+    /* nodes seen in the window */
+    for (uint64_t i = 0; i < st->kl_log_n;) {
+        uint64_t j = i;
+        while (j < st->kl_log_n && st->kl_log[j] == st->kl_log[i])
+            j++;
+        const uint64_t key = st->kl_log[i], c = j - i;
+        if (kl_extended(st, key) ? c * n >= W : c * n > 2 * W)
+            next[nn++] = key;
+        i = j;
+    }
+    /* extended nodes the window never reached: rho = 0 < 1/n, unless the
+     * window is empty (no traffic, no change) */
+    if (W == 0)
+        for (uint64_t k = 0; k < st->kl_n; k++)
+            next[nn++] = st->kl_ext[k];
+    qsort(next, nn, sizeof(uint64_t), cmp_u64);
+    uint64_t u = 0;
+    for (uint64_t k = 0; k < nn; k++)
+        if (u == 0 || next[k] != next[u - 1])
+            next[u++] = next[k];
+    int rc = OR_OK;
+    if (u > st->kl_max) {
+        rc = OR_EFULL;
+    } else {
+        memcpy(st->kl_ext, next, u * sizeof(uint64_t));
+        st->kl_n = u;
+    }
+    free(next);
+    st->kl_log_n = 0;
+    st->kl_win = 0;
+    return rc;
+}
+
+/* The extended prefixes, ascending (at most cap of them); *n gets the count. */
+int or_keylen_export(const or_state *st, uint64_t *keys, uint64_t cap, uint64_t *n)
+{
+    if (!st || !n)
+        return OR_EINVAL;
+    for (uint64_t k = 0; k < st->kl_n && k < cap; k++)
+        keys[k] = st->kl_ext[k];
+    *n = st->kl_n;
+    return OR_OK;
+}
+
 /* Route a batch in request order over a snapshot of the cached block sets,
  * applying each decision to the loads before the next request (scheduler
  * metadata is updated as requests are scheduled, Sec. A.3.2).
  * key[2n] ring keys, cand[2n] candidates, match[2n] cached blocks,
  * chosen[n], ttft[n], flags[n]; block_keys (optional) receives every full
- * block's f1 key, request-major. */
+ * block's f1 key, request-major; key_len (optional) each request's hashed
+ * prefix length K_r in blocks.  With the hotness tree on, the ring keys hash
+ * K_r blocks and each request's path joins the current window. */
 int or_route(or_state *st, const int32_t *tokens, const int64_t *off, uint64_t n,
              int64_t *loads, uint64_t *key, uint32_t *cand, uint32_t *match,
-             uint32_t *chosen, int64_t *ttft, uint8_t *flags, uint64_t *block_keys)
+             uint32_t *chosen, int64_t *ttft, uint8_t *flags, uint64_t *block_keys,
+             uint32_t *key_len)
 {
     if (!st || (n && (!tokens || !off || !loads || !key || !cand || !match || !chosen ||
                       !ttft || !flags)))
@@ -600,7 +771,16 @@ int or_route(or_state *st, const int32_t *tokens, const int64_t *off, uint64_t n
             memcpy(block_keys + bk, h1, nfull * sizeof(uint64_t));
             bk += nfull;
         }
-        const uint64_t x1 = or_ring_key(st, 0, t, len), x2 = or_ring_key(st, 1, t, len);
+        const uint64_t kr = kl_key_len(st, h1, nfull);
+        if (st->kl_on && nfull >= st->cfg.key_blocks)
+            for (uint64_t d = st->cfg.key_blocks; d <= kr; d++)
+                if (kl_log_push(st, canon(h1[d - 1])) != OR_OK) {
+                    free(h1);
+                    return OR_ENOMEM;
+                }
+        if (key_len)
+            key_len[r] = (uint32_t)kr;
+        const uint64_t x1 = or_ring_key_at(st, 0, t, kr), x2 = or_ring_key_at(st, 1, t, kr);
         uint32_t c1, c2;
         uint8_t fl = or_candidates(st, x1, x2, &c1, &c2) ? 8 : 0;
         const uint64_t m1 = prefix_match(st, c1, h1, nfull);
@@ -613,6 +793,8 @@ int or_route(or_state *st, const int32_t *tokens, const int64_t *off, uint64_t n
         match[r] = (uint32_t)m1; match[n + r] = (uint32_t)m2;
         chosen[r] = ch; ttft[r] = tt; flags[r] = fl;
     }
+    if (st->kl_on)
+        st->kl_win += n;
     free(h1);
     return OR_OK;
 }

@@ -795,3 +795,217 @@ def test_metadata_footprint_fixture():
                 vals[k] = int(v)
     assert vals["bytes_per_block"] == 8 + 8
     assert 8 / 0.5 == vals["bytes_per_block"]
+
+
+# ---------------------------------------------------------------------------
+# Adaptive hash-key length (Sec. 3.2; Sec. A.1.1, Fig. prefix-len)
+# ---------------------------------------------------------------------------
+
+def _tree_model(batches, K, B, n_live):
+    """The prefix hotness tree over token tuples (no hashing): for each batch,
+    every request's key length K_r (walk from depth K while the prefix is
+    extended, at most its full blocks) and, after the window closes, the
+    extended prefixes.  Counts are taken directly from the token prefixes."""
+    ext = set()
+    for batch in batches:
+        counts = {}
+        klens = []
+        for p in batch:
+            nfull = len(p) // B
+            if nfull <= K:
+                kr = nfull
+            else:
+                kr = K
+                while kr < nfull and tuple(p[:kr * B]) in ext:
+                    kr += 1
+            if nfull >= K:
+                for d in range(K, kr + 1):
+                    node = tuple(p[:d * B])
+                    counts[node] = counts.get(node, 0) + 1
+            klens.append(kr)
+        W = len(batch)
+        if W:
+            ext = {v for v, c in counts.items()
+                   if (c * n_live >= W if v in ext else c * n_live > 2 * W)}
+        yield klens, set(ext)
+
+
+def _node_key(o, node):
+    return oracle.canon(int(o.chain(0, np.array(node, np.int32))[-1]))
+
+
+def _route_windows(o, batches, n_live):
+    for batch in batches:
+        tok = np.concatenate([np.asarray(p, np.int32) for p in batch]) if batch else \
+            np.zeros(0, np.int32)
+        off = np.zeros(len(batch) + 1, np.int64)
+        off[1:] = np.cumsum([len(p) for p in batch])
+        out = o.route(tok, off, np.zeros(n_live, np.int64))
+        assert o.keylen_window() == oracle.OK
+        yield out, tok, off
+
+
+def _check_tree_against_model(o, batches, K, B, n_live):
+    depths = []
+    for (out, tok, off), (klens, ext) in zip(_route_windows(o, batches, n_live),
+                                             _tree_model(batches, K, B, n_live)):
+        assert out["key_len"].tolist() == klens
+        n = len(klens)
+        for r, kr in enumerate(klens):
+            p = tok[off[r]:off[r + 1]]
+            assert int(out["key"][r]) == o.ring_key_at(0, p, kr)
+            assert int(out["key"][n + r]) == o.ring_key_at(1, p, kr)
+        want = sorted(_node_key(o, v) for v in ext)
+        assert o.keylen_tree().tolist() == want
+        # the tree stays connected: a node below the roots has its parent
+        for v in ext:
+            if len(v) > K * B:
+                assert tuple(v[:len(v) - B]) in ext
+        depths.append(klens)
+    return depths
+
+
+def _blk(rng, B):
+    return list(rng.integers(0, 1 << 20, size=B))
+
+
+def test_keylen_hand_windows():
+    """K = 1, B = 4, 4 live instances.  Window 1: six of eight requests start
+    with block A (counts: A 6; 6*4 = 24 > 2*8): A extends.  Window 2: the A
+    requests now hash two blocks, so their ring keys change; A still sees 6
+    requests (24 >= 8) and stays.  Window 3: one A request of eight
+    (4 < 8): A is cold and shrinks back.  Window 4: A requests hash one
+    block again."""
+    B, K, n_live = 4, 1, 4
+    rng = np.random.default_rng(5)
+    A = _blk(rng, B)
+    a_reqs = [A + _blk(rng, B) + [7, 7] for _ in range(6)]
+    others = [_blk(rng, B) + _blk(rng, B) for _ in range(2)]
+    w1 = a_reqs + others
+    w3 = [a_reqs[0]] + [_blk(rng, B) + _blk(rng, B) for _ in range(7)]
+    w4 = a_reqs[:2] + others
+    o = oracle.Oracle(dict(block=B, key_blocks=K, seeds=(1, 2), vnodes=16, max_slots=n_live))
+    o.build_rings(range(n_live))
+    assert o.keylen_enable(64) == oracle.OK
+    outs = list(_route_windows(o, [w1], n_live))
+    assert outs[0][0]["key_len"].tolist() == [1] * 8
+    assert o.keylen_tree().tolist() == [_node_key(o, A)]
+    k1 = outs[0][0]["key"][:6].copy()
+    out2 = list(_route_windows(o, [w1], n_live))[0][0]
+    assert out2["key_len"].tolist() == [2] * 6 + [1, 1]
+    assert len(set(out2["key"][:6].tolist())) == 6 and not set(out2["key"][:6]) & set(k1)
+    assert o.keylen_tree().tolist() == [_node_key(o, A)]
+    out3 = list(_route_windows(o, [w3], n_live))[0][0]
+    assert out3["key_len"][0] == 2
+    assert o.keylen_tree().tolist() == []
+    out4 = list(_route_windows(o, [w4], n_live))[0][0]
+    assert out4["key_len"].tolist() == [1, 1, 1, 1]
+    assert out4["key"][:2].tolist() == k1[:2].tolist()
+    # and the same windows through the token-tuple model
+    o2 = oracle.Oracle(dict(block=B, key_blocks=K, seeds=(1, 2), vnodes=16, max_slots=n_live))
+    o2.build_rings(range(n_live))
+    o2.keylen_enable(64)
+    _check_tree_against_model(o2, [w1, w1, w3, w4], K, B, n_live)
+
+
+def test_keylen_thresholds_are_strict_and_inclusive():
+    """Hot needs rho > 2/n (4 of 8 with n = 4 is exactly 2/n: no); cold needs
+    rho < 1/n (2 of 8 is exactly 1/n: stays)."""
+    B, K, n_live = 4, 1, 4
+    rng = np.random.default_rng(6)
+    A = _blk(rng, B)
+    mk = lambda k: [A + _blk(rng, B) for _ in range(k)] + [_blk(rng, B) + _blk(rng, B)
+                                                           for _ in range(8 - k)]
+    o = oracle.Oracle(dict(block=B, key_blocks=K, seeds=(1, 2), vnodes=16, max_slots=n_live))
+    o.build_rings(range(n_live))
+    o.keylen_enable(8)
+    list(_route_windows(o, [mk(4)], n_live))
+    assert o.keylen_tree().tolist() == []
+    list(_route_windows(o, [mk(5)], n_live))
+    assert o.keylen_tree().tolist() == [_node_key(o, A)]
+    list(_route_windows(o, [mk(2)], n_live))
+    assert o.keylen_tree().tolist() == [_node_key(o, A)]
+    list(_route_windows(o, [mk(1)], n_live))
+    assert o.keylen_tree().tolist() == []
+    # an empty window changes nothing
+    list(_route_windows(o, [mk(5)], n_live))
+    list(_route_windows(o, [[]], n_live))
+    assert o.keylen_tree().tolist() == [_node_key(o, A)]
+
+
+def test_keylen_extends_one_level_per_window():
+    """A template of three blocks shared by every request: each window
+    extends the path one level, until the requests diverge after it."""
+    B, K, n_live = 4, 1, 8
+    rng = np.random.default_rng(7)
+    T = _blk(rng, B) + _blk(rng, B) + _blk(rng, B)
+    batch = [T + _blk(rng, B) + _blk(rng, B) for _ in range(16)]
+    o = oracle.Oracle(dict(block=B, key_blocks=K, seeds=(1, 2), vnodes=16, max_slots=n_live))
+    o.build_rings(range(n_live))
+    o.keylen_enable(16)
+    depths = _check_tree_against_model(o, [batch] * 6, K, B, n_live)
+    assert [d[0] for d in depths] == [1, 2, 3, 4, 4, 4]
+    assert len(o.keylen_tree()) == 3
+
+
+def test_keylen_disabled_or_empty_tree_is_fixed_K():
+    wl = workloads.tiny(slo_us=20_000)
+    import oracle.harness as oh
+    st = oh.setup(wl)
+    o = st["oracle"]
+    a = o.route(st["tokens"], st["offsets"], st["loads0"])
+    o.keylen_enable(1024)
+    b = o.route(st["tokens"], st["offsets"], st["loads0"])
+    for k in ("key", "cand", "match", "chosen", "ttft", "flags", "key_len"):
+        assert np.array_equal(a[k], b[k]), k
+    nfull = np.diff(st["offsets"]) // wl.route.block
+    assert np.array_equal(a["key_len"], np.minimum(nfull, wl.route.key_blocks))
+    o.keylen_enable(0)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_keylen_random_windows_match_token_model(seed):
+    """Zipf-popular templates with random tails over several windows: key
+    lengths, ring keys and the tree after every window against the
+    token-tuple model (brute-force counts of every path prefix)."""
+    rng = np.random.default_rng(100 + seed)
+    B, K, n_live = 4, 2, 8
+    templates = [[int(x) for x in rng.integers(0, 50, size=B * int(rng.integers(K + 1, 9)))]
+                 for _ in range(6)]
+    w = 1.0 / np.arange(1, 7) ** 1.4
+    w /= w.sum()
+    batches = []
+    for _ in range(7):
+        batch = []
+        for _ in range(int(rng.integers(40, 120))):
+            t = templates[int(rng.choice(6, p=w))]
+            cut = int(rng.integers(0, len(t) + 1)) if rng.random() < 0.2 else \
+                int(rng.integers(K * B, len(t) + 1))
+            batch.append(t[:cut] + [int(x) for x in rng.integers(0, 50, size=int(rng.integers(0, 5 * B)))])
+        batches.append(batch)
+    o = oracle.Oracle(dict(block=B, key_blocks=K, seeds=(1, 2), vnodes=16, max_slots=n_live))
+    o.build_rings(range(n_live))
+    o.keylen_enable(4096)
+    depths = _check_tree_against_model(o, batches, K, B, n_live)
+    assert max(max(d) for d in depths) > K  # the tree did extend
+
+
+def test_keylen_capacity_and_state_errors():
+    B, K, n_live = 4, 1, 8
+    rng = np.random.default_rng(8)
+    A, C = _blk(rng, B), _blk(rng, B)
+    batch = [A + _blk(rng, B) for _ in range(4)] + [C + _blk(rng, B) for _ in range(4)]
+    o = oracle.Oracle(dict(block=B, key_blocks=K, seeds=(1, 2), vnodes=16, max_slots=n_live))
+    assert o.keylen_window() == oracle.EINVAL  # tree off
+    o.build_rings(range(n_live))
+    o.keylen_enable(1)
+    tok = np.concatenate([np.asarray(p, np.int32) for p in batch])
+    off = np.arange(0, len(tok) + 1, 2 * B, dtype=np.int64)
+    o.route(tok, off, np.zeros(n_live, np.int64))
+    # A and C both hot (4 * 8 > 2 * 8), room for one: the tree is unchanged
+    assert o.keylen_window() == oracle.EFULL
+    assert o.keylen_tree().tolist() == []
+    o.keylen_enable(2)
+    o.route(tok, off, np.zeros(n_live, np.int64))
+    assert o.keylen_window() == oracle.OK
+    assert o.keylen_tree().tolist() == sorted([_node_key(o, A), _node_key(o, C)])

@@ -58,7 +58,7 @@ typedef struct {
     uint64_t kl_max;          /* most extended prefixes the tree may hold       */
     uint64_t *kl_ext;         /* sorted canon keys of the extended prefixes     */
     uint64_t kl_n;
-    uint64_t *kl_log;         /* prefixes on routed requests' paths, this window*/
+    uint64_t *kl_log;         /* prefixes (depth >= K) of this window's requests*/
     uint64_t kl_log_n, kl_log_cap;
     uint64_t kl_win;          /* requests routed in this window                 */
 } or_state;
@@ -597,11 +597,17 @@ int or_set_policy(or_state *st, int policy)
  * than K full blocks: all of them, as without the tree).
  *
  * Traffic ratios come from windows the caller closes (or_keylen_window):
- * rho of a node = requests of the window whose path passes through it /
- * requests routed in the window.  At the close, with n live instances, a
- * leaf with rho > 2/n becomes extended (its children are added, so its
- * requests hash one block more and spread over more candidate pairs) and an
- * extended node with rho < 1/n is no longer (its children are removed). */
+ * rho of a prefix = requests of the window that carry it / requests routed
+ * in the window.  At the close, with n live instances, a leaf with
+ * rho > 2/n becomes extended (its children are added, so its requests hash
+ * one block more and spread over more candidate pairs) and an extended node
+ * with rho < 1/n is no longer (its children are removed).  The rule is
+ * applied until it changes nothing: a child added as hot that is itself hot
+ * in the same window is extended too, so a hot prefix grows in one close to
+ * where its requests part.  Since a prefix's count never exceeds its
+ * parent's, that fixed point is the set of prefixes (depth >= K) with
+ * rho > 2/n, or already extended with rho >= 1/n; it is a tree (every
+ * member's parent is a member). */
 
 static int kl_extended(const or_state *st, uint64_t ck)
 {
@@ -671,8 +677,9 @@ static int cmp_u64(const void *a, const void *b)
     return x < y ? -1 : (x > y ? 1 : 0);
 }
 
-/* Close the window: apply the hot and cold rules to every node with the
- * window's counts, then start an empty window.  OR_EFULL (tree unchanged,
+/* Close the window: the new tree is every prefix the window's requests
+ * carry (depth >= K) that is hot, or extended and not cold, by its count
+ * in the window; then start an empty window.  OR_EFULL (tree unchanged,
  * window still closed) if the new tree would hold more than max_nodes
  * extended prefixes. */
 int or_keylen_window(or_state *st)
@@ -697,8 +704,8 @@ int or_keylen_window(or_state *st)
             next[nn++] = key;
         i = j;
     }
-    /* extended nodes the window never reached: rho = 0 < 1/n, unless the
-     * window is empty (no traffic, no change) */
+    /* extended prefixes no request of the window carried: rho = 0 < 1/n,
+     * unless the window is empty (no traffic, no change) */
     if (W == 0)
         for (uint64_t k = 0; k < st->kl_n; k++)
             next[nn++] = st->kl_ext[k];
@@ -738,7 +745,8 @@ int or_keylen_export(const or_state *st, uint64_t *keys, uint64_t cap, uint64_t 
  * chosen[n], ttft[n], flags[n]; block_keys (optional) receives every full
  * block's f1 key, request-major; key_len (optional) each request's hashed
  * prefix length K_r in blocks.  With the hotness tree on, the ring keys hash
- * K_r blocks and each request's path joins the current window. */
+ * K_r blocks and each request's prefixes of depths K and more join the
+ * current window. */
 int or_route(or_state *st, const int32_t *tokens, const int64_t *off, uint64_t n,
              int64_t *loads, uint64_t *key, uint32_t *cand, uint32_t *match,
              uint32_t *chosen, int64_t *ttft, uint8_t *flags, uint64_t *block_keys,
@@ -773,7 +781,7 @@ int or_route(or_state *st, const int32_t *tokens, const int64_t *off, uint64_t n
         }
         const uint64_t kr = kl_key_len(st, h1, nfull);
         if (st->kl_on && nfull >= st->cfg.key_blocks)
-            for (uint64_t d = st->cfg.key_blocks; d <= kr; d++)
+            for (uint64_t d = st->cfg.key_blocks; d <= nfull; d++)
                 if (kl_log_push(st, canon(h1[d - 1])) != OR_OK) {
                     free(h1);
                     return OR_ENOMEM;

@@ -805,7 +805,9 @@ def _tree_model(batches, K, B, n_live):
     """The prefix hotness tree over token tuples (no hashing): for each batch,
     every request's key length K_r (walk from depth K while the prefix is
     extended, at most its full blocks) and, after the window closes, the
-    extended prefixes.  Counts are taken directly from the token prefixes."""
+    extended prefixes.  The close applies the one-level rule (hot leaf:
+    extend; extended and cold: shrink) repeatedly until nothing changes,
+    with counts taken directly from the token prefixes."""
     ext = set()
     for batch in batches:
         counts = {}
@@ -818,15 +820,26 @@ def _tree_model(batches, K, B, n_live):
                 kr = K
                 while kr < nfull and tuple(p[:kr * B]) in ext:
                     kr += 1
-            if nfull >= K:
-                for d in range(K, kr + 1):
-                    node = tuple(p[:d * B])
-                    counts[node] = counts.get(node, 0) + 1
+            for d in range(K, nfull + 1):
+                node = tuple(p[:d * B])
+                counts[node] = counts.get(node, 0) + 1
             klens.append(kr)
         W = len(batch)
         if W:
-            ext = {v for v, c in counts.items()
-                   if (c * n_live >= W if v in ext else c * n_live > 2 * W)}
+            old = set(ext)
+            hot = lambda v: counts.get(v, 0) * n_live > 2 * W
+            cold = lambda v: counts.get(v, 0) * n_live < W
+            tree = {v for v in old if not cold(v)}
+            # a child of an extended node (or a root) that is a hot leaf
+            # extends; repeat until no leaf is hot
+            while True:
+                grow = {v for v in counts if v not in tree and hot(v) and
+                        (len(v) == K * B or v[:len(v) - B] in tree)}
+                # extended nodes are kept only under a kept parent
+                tree = {v for v in tree | grow if len(v) == K * B or v[:len(v) - B] in tree | grow}
+                if not grow:
+                    break
+            ext = tree
         yield klens, set(ext)
 
 
@@ -933,19 +946,28 @@ def test_keylen_thresholds_are_strict_and_inclusive():
     assert o.keylen_tree().tolist() == [_node_key(o, A)]
 
 
-def test_keylen_extends_one_level_per_window():
-    """A template of three blocks shared by every request: each window
-    extends the path one level, until the requests diverge after it."""
+def test_keylen_extends_to_where_requests_part():
+    """A template of three blocks shared by every request: the first close
+    extends the path through the whole template (each level is hot in turn:
+    16 of 16 requests, 16 * 8 > 2 * 16), and the requests' own fourth
+    blocks (one request each) stay leaves.  From the second window on every
+    request hashes four blocks: its own fourth block decides its pair.  When
+    the template drops to 3 of 16 requests (3 * 8 = 24: not above 2 * 16,
+    not below 16) the tree stays; at 1 of 16 (8 < 16) all three levels are
+    cold and go."""
     B, K, n_live = 4, 1, 8
     rng = np.random.default_rng(7)
     T = _blk(rng, B) + _blk(rng, B) + _blk(rng, B)
     batch = [T + _blk(rng, B) + _blk(rng, B) for _ in range(16)]
+    mix3 = batch[:3] + [_blk(rng, B) * 2 for _ in range(13)]
+    mix1 = batch[:1] + [_blk(rng, B) * 2 for _ in range(15)]
     o = oracle.Oracle(dict(block=B, key_blocks=K, seeds=(1, 2), vnodes=16, max_slots=n_live))
     o.build_rings(range(n_live))
     o.keylen_enable(16)
-    depths = _check_tree_against_model(o, [batch] * 6, K, B, n_live)
-    assert [d[0] for d in depths] == [1, 2, 3, 4, 4, 4]
-    assert len(o.keylen_tree()) == 3
+    depths = _check_tree_against_model(o, [batch, batch, mix3, mix1, mix1], K, B, n_live)
+    assert [d[0] for d in depths] == [1, 4, 4, 4, 1]
+    assert len(o.keylen_tree()) == 0
+    assert len(set(o.ring_key_at(0, np.array(p, np.int32), 4) for p in batch)) == 16
 
 
 def test_keylen_disabled_or_empty_tree_is_fixed_K():

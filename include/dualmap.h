@@ -120,6 +120,7 @@ typedef struct {
     uint64_t* block_keys; /* NULL, or [sum over r of floor(len_r / B)] every full    */
                           /*      block's f1 key, request-major (the keys a KV     */
                           /*      save inserts)                                    */
+    uint32_t* key_len;    /* NULL, or [n] blocks the ring keys hash (K_r)           */
 } dm_route_out;
 
 /* Route a batch of n requests (Sec. 3.2, Sec. A.1.1).  tokens holds n_tokens
@@ -129,8 +130,10 @@ typedef struct {
  * no token outside [0, n_tokens) and no block key past the batch's block
  * count is touched, every request is treated as having no full block (ring
  * keys 0, match 0), and dm_sync returns DM_EINVAL.  For every request:
- *   1. chained f1/f2 block keys; ring keys x_s = key of the first
- *      min(K, full blocks) blocks (no full block: the empty-prefix key);
+ *   1. chained f1/f2 block keys; ring keys x_s = key of the first K_r
+ *      blocks, K_r = min(K, full blocks) (no full block: the empty-prefix
+ *      key), or with the hotness tree on (dm_keylen_enable) the length the
+ *      tree gives;
  *   2. c1 = owner of x1 on ring 1, c2 = owner of x2 on ring 2; if they
  *      coincide c2 becomes the next live id after c1 in cyclic id order
  *      (Sec. 3.2, id2 = (id1 + 1) mod n for dense ids);
@@ -280,6 +283,43 @@ dm_status dm_route_stage_ms(dm_ctx* ctx, float* ms_host, int n);
  * after the last epilogue.  Turning pipelining off does the same.  Returns
  * DM_EDEVICE if the streams or their events cannot be created. */
 dm_status dm_set_pipelining(dm_ctx* ctx, int on);
+
+/* Adaptive hash-key length (Sec. 3.2, "How long prefix is appropriate for
+ * the hash key?"; Sec. A.1.1).  The prefix hotness tree: nodes are prompt
+ * prefixes of d >= K full blocks (named by the f1 key of their last block),
+ * the depth-K prefixes its roots; the tree is kept as the set of its
+ * extended nodes (those with children).  While it is on, a request's ring
+ * keys hash K_r blocks: the smallest d >= K whose prefix is not extended,
+ * at most its full blocks (fewer than K full blocks: all of them).  Every
+ * routed request joins the current window with its prefixes of depth >= K.
+ *
+ * dm_keylen_enable turns the tree on with room for max_nodes extended
+ * prefixes and a window record of max_window_blocks prefixes (the tree
+ * starts empty, i.e. every K_r is min(K, full blocks)); max_nodes = 0 turns
+ * it off.  Prefixes past the record's room are dropped and dm_sync reports
+ * DM_EFULL; closing such a window returns DM_EFULL and leaves the tree
+ * unchanged.  With the tree on, the routing computes every request's block
+ * keys (as for block_keys) to record them.
+ *
+ * dm_keylen_window closes the window.  With W requests in it and n live
+ * instances, a prefix's traffic ratio rho is the share of the window's
+ * requests that carry it.  A leaf with rho > 2/n becomes extended (its
+ * requests will hash one block more and spread over more candidate pairs),
+ * an extended node with rho < 1/n stops being extended, and the rule is
+ * applied until it changes nothing, so a hot prefix grows in one close to
+ * where its requests part.  As a prefix's count never exceeds its
+ * parent's, the new tree is the set of prefixes (depth >= K) with
+ * rho > 2/n, or already extended with rho >= 1/n.  An empty window changes
+ * nothing.  DM_EFULL if the new tree would hold more than max_nodes
+ * extended prefixes (the tree is then unchanged); the next window starts
+ * empty either way.  dm_keylen_export writes up to cap extended prefixes,
+ * ascending (canonical keys: k, or k + 2^63 for k < 2), to keys_host and
+ * their count to *n_host.  All three synchronise with the context's
+ * streams.  DM_ESTATE if the tree is off (window, export) or no ring exists
+ * (window). */
+dm_status dm_keylen_enable(dm_ctx* ctx, uint64_t max_nodes, uint64_t max_window_blocks);
+dm_status dm_keylen_window(dm_ctx* ctx);
+dm_status dm_keylen_export(dm_ctx* ctx, uint64_t* keys_host, uint64_t cap, uint64_t* n_host);
 
 /* Selection rule between the two candidates of every request.  The
  * SLO-aware rule is DualMap's (Sec. 3.2) and the default; the others are the

@@ -27,7 +27,8 @@ EXPORTS = ("dm_create", "dm_destroy", "dm_build_rings", "dm_ring_export", "dm_in
            "dm_index_erase", "dm_index_clear", "dm_index_size", "dm_route_batch",
            "dm_route_batch_noalloc",
            "dm_rebalance", "dm_scale", "dm_set_timing", "dm_route_stage_ms",
-           "dm_set_pipelining", "dm_set_policy", "dm_sync", "dm_last_error")
+           "dm_set_pipelining", "dm_set_policy", "dm_keylen_enable", "dm_keylen_window",
+           "dm_keylen_export", "dm_sync", "dm_last_error")
 
 
 class DMError(RuntimeError):
@@ -47,7 +48,7 @@ class dm_config(C.Structure):
 class dm_route_out(C.Structure):
     _fields_ = [("key", C.c_void_p), ("cand", C.c_void_p), ("match", C.c_void_p),
                 ("chosen", C.c_void_p), ("ttft_us", C.c_void_p), ("flags", C.c_void_p),
-                ("block_keys", C.c_void_p)]
+                ("block_keys", C.c_void_p), ("key_len", C.c_void_p)]
 
 
 class dm_queues(C.Structure):
@@ -90,6 +91,9 @@ def load_library(path: str = LIB_PATH):
         "dm_route_stage_ms": (i32, [P, P, i32]),
         "dm_set_pipelining": (i32, [P, i32]),
         "dm_set_policy": (i32, [P, i32]),
+        "dm_keylen_enable": (i32, [P, u64, u64]),
+        "dm_keylen_window": (i32, [P]),
+        "dm_keylen_export": (i32, [P, P, u64, P]),
         "dm_sync": (i32, [P]),
         "dm_last_error": (C.c_char_p, [P]),
     }
@@ -242,20 +246,44 @@ class DualMap:
         n = offsets.numel() - 1
         ro = dm_route_out(_ptr(out["key"]), _ptr(out["cand"]), _ptr(out["match"]),
                           _ptr(out["chosen"]), _ptr(out["ttft"]), _ptr(out["flags"]),
-                          _ptr(out.get("block_keys")))
+                          _ptr(out.get("block_keys")), _ptr(out.get("key_len")))
         fn = self.lib.dm_route_batch_noalloc if noalloc else self.lib.dm_route_batch
         name = "dm_route_batch_noalloc" if noalloc else "dm_route_batch"
         self._check(fn(self._h, _ptr(tokens), tokens.numel(), _ptr(offsets), n, _ptr(loads),
                        C.byref(ro)), name)
 
-    def alloc_route_out(self, n: int, n_blocks: Optional[int] = None) -> Dict:
+    def alloc_route_out(self, n: int, n_blocks: Optional[int] = None,
+                        key_len: bool = False) -> Dict:
         t = self.torch
         out = dict(key=self._empty(2 * n, t.uint64), cand=self._empty(2 * n, t.uint32),
                    match=self._empty(2 * n, t.uint32), chosen=self._empty(n, t.uint32),
                    ttft=self._empty(n, t.int64), flags=self._empty(n, t.uint8))
         if n_blocks is not None:
             out["block_keys"] = self._empty(max(n_blocks, 1), t.uint64)
+        if key_len:
+            out["key_len"] = self._empty(max(n, 1), t.uint32)
         return out
+
+    def keylen_enable(self, max_nodes: int, max_window_blocks: int = 1 << 24) -> None:
+        """Adaptive hash-key length (see dm_keylen_enable): an empty prefix
+        hotness tree with room for max_nodes extended prefixes and a window
+        record of max_window_blocks prefixes; max_nodes = 0 turns it off."""
+        self._check(self.lib.dm_keylen_enable(self._h, int(max_nodes), int(max_window_blocks)),
+                    "dm_keylen_enable")
+
+    def keylen_window(self) -> None:
+        """Close the hotness window: hot leaves extend, cold nodes shrink."""
+        self._check(self.lib.dm_keylen_window(self._h), "dm_keylen_window")
+
+    def keylen_tree(self):
+        """The extended prefixes (canonical f1 keys), ascending, as numpy."""
+        import numpy as np
+        n = C.c_uint64()
+        self._check(self.lib.dm_keylen_export(self._h, None, 0, C.byref(n)), "dm_keylen_export")
+        a = np.zeros(max(int(n.value), 1), np.uint64)
+        self._check(self.lib.dm_keylen_export(self._h, a.ctypes.data_as(C.c_void_p), len(a),
+                                              C.byref(n)), "dm_keylen_export")
+        return a[:int(n.value)]
 
     def route(self, tokens, offsets, loads, block_keys: bool = False) -> Dict:
         """Route a batch; loads (int64 [max_slots]) are updated in place."""
@@ -269,7 +297,7 @@ class DualMap:
         nb = None
         if block_keys:
             nb = int(((offsets[1:] - offsets[:-1]).clamp(min=0) // self.block).sum().item())
-        out = self.alloc_route_out(n, nb)
+        out = self.alloc_route_out(n, nb, key_len=True)
         self.route_into(tokens, offsets, loads, out)
         return out
 

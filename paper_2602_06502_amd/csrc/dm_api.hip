@@ -92,8 +92,10 @@ dm_status route_args_check(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens,
         return fail(c, DM_EINVAL, std::string(what) + ": null argument");
     if (!aligned(tokens) || !aligned(offsets) || !aligned(loads) || !aligned(out->key) ||
         !aligned(out->cand) || !aligned(out->match) || !aligned(out->chosen) ||
-        !aligned(out->ttft_us) || (out->block_keys && !aligned(out->block_keys)))
+        !aligned(out->ttft_us) || (out->block_keys && !aligned(out->block_keys)) ||
+        (out->key_len && !aligned(out->key_len)))
         return fail(c, DM_EINVAL, std::string(what) + ": misaligned pointer");
+
     // the selection's slot indices are 32-bit: 36 windows of 64 lanes per
     // 1024 requests must stay below 2^32
     if (n > kMaxRouteBatch)
@@ -277,6 +279,7 @@ void dm_destroy(dm_ctx* c)
             free_ring(r);
     for (auto& s : c->scratch)
         (void)hipFree(s.p);
+    keylen_free(c);
     for (auto& ev : c->tev)
         if (ev)
             (void)hipEventDestroy(ev);
@@ -599,6 +602,32 @@ static hipError_t make_streams(dm_ctx* c)
         if (e == hipSuccess)
             e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
     return e;
+}
+
+dm_status dm_keylen_enable(dm_ctx* c, uint64_t max_nodes, uint64_t max_window_blocks)
+{
+    if (!c)
+        return DM_EINVAL;
+    DeviceGuard g(c->device);
+    return keylen_enable(c, max_nodes, max_window_blocks);
+}
+
+dm_status dm_keylen_window(dm_ctx* c)
+{
+    if (!c)
+        return DM_EINVAL;
+    DeviceGuard g(c->device);
+    return keylen_window(c);
+}
+
+dm_status dm_keylen_export(dm_ctx* c, uint64_t* keys_host, uint64_t cap, uint64_t* n_host)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (!n_host || (cap && !keys_host))
+        return fail(c, DM_EINVAL, "dm_keylen_export: null argument");
+    DeviceGuard g(c->device);
+    return keylen_export(c, keys_host, cap, n_host);
 }
 
 dm_status dm_set_policy(dm_ctx* c, int policy)

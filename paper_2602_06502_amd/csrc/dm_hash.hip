@@ -12,6 +12,9 @@
 // Three passes use this walk (dm_route.hip runs them in this order):
 //   prefix   both chains over the first min(K, full blocks) blocks only:
 //            the two ring keys (ring_key_kernel: several requests per wave);
+//            with the prefix hotness tree on, requests whose depth-K prefix
+//            is extended go on down the tree (extend_kernel) to their key
+//            length K_r, both chains, and take the ring keys of depth K_r;
 //   leaders  one request per group of equal ring keys (dm_probe.hip): the
 //            full f1 chain, stored; each chunk's keys are probed against
 //            both candidates' tables, lanes from the first unresolved block
@@ -97,6 +100,14 @@ struct HashArgs {
     uint64_t* pend;               // [n]
     const uint64_t* resume;       // resume list
     const unsigned long long* resume_count;
+    // prefix hotness tree (kl_on = 0: fixed K)
+    uint32_t kl_on;
+    uint32_t kl_log2;
+    const uint64_t* kl_tab;       // extended prefixes
+    uint32_t* ext_list;           // requests whose depth-K prefix is extended
+    unsigned long long* ext_count;
+    const unsigned long long* ext_count_in;
+    uint32_t* key_len;            // [n] or null
 };
 
 // Index of this wave in the grid, in a scalar register: the compiler cannot
@@ -157,9 +168,10 @@ __global__ __launch_bounds__(kHashThreads) void ring_key_kernel(HashArgs a, uint
         const uint64_t r = base + ((uint32_t)lane >> glog);
         uint32_t kr = 0;
         int64_t o0 = 0;
+        uint64_t nfull = 0;
         if (r < a.n && !bad) {
             o0 = a.offsets[r];
-            const uint64_t nfull = (uint64_t)(a.offsets[r + 1] - o0) / B;
+            nfull = (uint64_t)(a.offsets[r + 1] - o0) / B;
             kr = (uint32_t)(nfull < a.key_blocks ? nfull : a.key_blocks);
         }
         uint64_t nh1 = 0, nh2 = 0;
@@ -170,6 +182,7 @@ __global__ __launch_bounds__(kHashThreads) void ring_key_kernel(HashArgs a, uint
             s1 += shfl_xor_u64(s1, (int)d);
             s2 += shfl_xor_u64(s2, (int)d);
         }
+        bool down = false;  // the depth-K prefix is extended: go on down the tree
         if (r < a.n && j == 0) {
             uint64_t x1 = mix64(H01 ^ seed1), x2 = mix64(H02 ^ seed2);  // empty-prefix keys
             if (kr > 0) {
@@ -178,6 +191,84 @@ __global__ __launch_bounds__(kHashThreads) void ring_key_kernel(HashArgs a, uint
             }
             a.key_out[r] = bad ? 0 : x1;
             a.key_out[a.n + r] = bad ? 0 : x2;
+            if (a.key_len)
+                a.key_len[r] = kr;
+            // x1 is the f1 key of block K - 1: the request's depth-K prefix
+            if (a.kl_on && !bad && nfull > a.key_blocks)
+                down = table_has(a.kl_tab, a.kl_log2, canon_key(x1));
+        }
+        if (a.kl_on) {
+            // one append per wave for the requests going down the tree
+            const uint64_t m = ballot(down);
+            if (m) {
+                unsigned long long at = 0;
+                if (lane == (int)__builtin_ctzll(m))
+                    at = atomicAdd(a.ext_count, (unsigned long long)__builtin_popcountll(m));
+                at = (unsigned long long)readlane_u64((uint64_t)at, (int)__builtin_ctzll(m));
+                if (down)
+                    a.ext_list[at + __builtin_popcountll(m & ((1ull << lane) - 1))] = (uint32_t)r;
+            }
+        }
+    }
+}
+
+// Requests whose depth-K prefix is extended walk down the tree: both chains
+// 64 blocks at a time from the start; K_r is the first depth d > K whose
+// prefix (f1 key of block d - 1) is not extended, or the full-block count.
+// The ring keys become the depth-K_r keys.
+template <int B>
+__global__ __launch_bounds__(kHashThreads) void extend_kernel(HashArgs a)
+{
+    const int lane = lane_id();
+    const uint64_t gw = wave_index();
+    const uint64_t nw = ((uint64_t)gridDim.x * blockDim.x) >> 6;
+    const HashParams* hp = a.hp;
+    const uint64_t seed1 = hp->seed[0], seed2 = hp->seed[1];
+    const uint64_t q1 = hp->qpow[0][lane], p1 = hp->ppow[0][lane];
+    const uint64_t q2 = hp->qpow[1][lane], p2 = hp->ppow[1][lane];
+    uint32_t k1[B], k2[B];
+#pragma unroll
+    for (int t = 0; t < B; t++) {
+        k1[t] = hp->kk[0][t];
+        k2[t] = hp->kk[1][t];
+    }
+    const uint64_t K = a.key_blocks;
+    const uint64_t units = *a.ext_count_in;
+    for (uint64_t u = gw; u < units; u += nw) {
+        const uint32_t r = a.ext_list[u];
+        const int64_t o0 = a.offsets[r];
+        const uint64_t nfull = (uint64_t)(a.offsets[(uint64_t)r + 1] - o0) / B;
+        const int32_t* tp = a.tokens + o0;
+        uint64_t G1 = hp->H0[0], G2 = hp->H0[1];
+        uint64_t kr = nfull, x1 = 0, x2 = 0;
+        for (uint64_t cb = 0; cb < nfull; cb += kWave) {
+            const uint64_t b = cb + lane, d = b + 1;
+            const bool valid = b < nfull;
+            uint64_t nh1 = 0, nh2 = 0;
+            if (valid)
+                nh_block2<B>(tp + b * B, k1, k2, nh1, nh2);
+            const uint64_t H1 = (G1 + wave_incl_sum_u64(nh1 * q1, lane)) * p1;
+            const uint64_t H2 = (G2 + wave_incl_sum_u64(nh2 * q2, lane)) * p2;
+            G1 = readlane_u64(H1, kWave - 1);
+            G2 = readlane_u64(H2, kWave - 1);
+            const uint64_t h1 = mix64(H1 ^ seed1);
+            // the path ends at the first depth past K that is not extended
+            const bool below = valid && d > K;
+            const uint64_t stop =
+                ballot(below && (d == nfull || !table_has(a.kl_tab, a.kl_log2, canon_key(h1))));
+            if (stop) {
+                const int f = __builtin_ctzll(stop);
+                kr = cb + f + 1;
+                x1 = readlane_u64(h1, f);
+                x2 = readlane_u64(mix64(H2 ^ seed2), f);
+                break;
+            }
+        }
+        if (lane == 0) {
+            a.key_out[r] = x1;
+            a.key_out[a.n + r] = x2;
+            if (a.key_len)
+                a.key_len[r] = (uint32_t)kr;
         }
     }
 }
@@ -652,11 +743,27 @@ size_t member_layout(uint64_t n, uint8_t* w, MemberWork* mw)
 
 }  // namespace
 
+// The tree's fields of HashArgs (kl_on = 0 when the tree is off).
+static void tree_args(dm_ctx* c, HashArgs& a)
+{
+    const KeyLen& k = c->kl;
+    a.kl_on = k.on ? 1u : 0u;
+    if (!k.on)
+        return;
+    a.kl_log2 = k.log2;
+    a.kl_tab = k.tab[k.cur];
+}
+
 hipError_t hash_prefix(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                       const uint32_t* bad, uint64_t* key_out)
+                       const uint32_t* bad, uint64_t* key_out, uint32_t* key_len,
+                       uint32_t* ext_list, unsigned long long* ext_count)
 {
     HashArgs a = base_args(c, tokens, offsets, n, bad);
     a.key_out = key_out;
+    a.key_len = key_len;
+    tree_args(c, a);
+    a.ext_list = ext_list;
+    a.ext_count = ext_count;
     uint32_t glog = 0;
     while ((1u << glog) < c->cfg.key_blocks)
         glog++;
@@ -668,6 +775,29 @@ hipError_t hash_prefix(dm_ctx* c, const int32_t* tokens, const int64_t* offsets,
         case 16: ring_key_kernel<16><<<grid, kHashThreads, 0, c->stream>>>(a, glog); break;
         case 32: ring_key_kernel<32><<<grid, kHashThreads, 0, c->stream>>>(a, glog); break;
         case 64: ring_key_kernel<64><<<grid, kHashThreads, 0, c->stream>>>(a, glog); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t hash_extend(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                       const uint32_t* bad, uint64_t* key_out, uint32_t* key_len,
+                       const uint32_t* ext_list, const unsigned long long* ext_count)
+{
+    HashArgs a = base_args(c, tokens, offsets, n, bad);
+    a.key_out = key_out;
+    a.key_len = key_len;
+    tree_args(c, a);
+    a.ext_list = const_cast<uint32_t*>(ext_list);
+    a.ext_count_in = ext_count;
+    // the listed count is on the device: a bounded grid strides over it
+    const uint32_t grid = grid_for(n, kHashThreads / kWave, kLeaderBlocks);
+    switch (c->cfg.block_size) {
+        case 4: extend_kernel<4><<<grid, kHashThreads, 0, c->stream>>>(a); break;
+        case 8: extend_kernel<8><<<grid, kHashThreads, 0, c->stream>>>(a); break;
+        case 16: extend_kernel<16><<<grid, kHashThreads, 0, c->stream>>>(a); break;
+        case 32: extend_kernel<32><<<grid, kHashThreads, 0, c->stream>>>(a); break;
+        case 64: extend_kernel<64><<<grid, kHashThreads, 0, c->stream>>>(a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

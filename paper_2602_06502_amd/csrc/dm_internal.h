@@ -83,6 +83,25 @@ struct Arena {
     size_t len[kScratchSlots] = {};
 };
 
+// Adaptive hash-key length (Sec. 3.2): the prefix hotness tree as the set of
+// its extended prefixes (canonical f1 key of each prefix's last block), in
+// an open-addressing table of 8-slot buckets (double-buffered: a window's
+// close builds the next one), and the window's record: every prefix of
+// depth >= K of every routed request.
+struct KeyLen {
+    bool on = false;
+    uint64_t max_nodes = 0;       // most extended prefixes
+    uint64_t cap = 0;             // window record entries
+    uint32_t log2 = 0;            // table slots 2^log2 (>= 2 max_nodes, >= 64)
+    uint64_t* tab[2] = {nullptr, nullptr};
+    int cur = 0;
+    uint64_t* list = nullptr;     // [max_nodes] extended prefixes, ascending
+    uint64_t n_ext = 0;
+    uint64_t* log = nullptr;      // [cap] the window's record
+    unsigned long long* log_n = nullptr;  // entries the window produced (may pass cap)
+    uint64_t win = 0;             // requests routed in the current window
+};
+
 }  // namespace dm
 
 struct dm_ctx {
@@ -136,6 +155,7 @@ struct dm_ctx {
     // two batches' outputs and work arrays (by batch parity) are in use.
     bool pipelined = false;
     uint32_t policy = DM_POLICY_SLO_AWARE;  // selection rule of later batches
+    dm::KeyLen kl;                          // adaptive hash-key length
     hipStream_t work_stream = nullptr, sel_stream = nullptr, out_stream = nullptr;
     hipEvent_t in_ready = nullptr;                 // caller's stream: inputs of the batch
     hipEvent_t prep_done = nullptr;                // work stream: records packed
@@ -209,7 +229,8 @@ hipError_t block_starts(dm_ctx* c, const int64_t* offsets, uint64_t n, uint64_t 
 
 // dm_sort.hip: stable LSD radix sort of (u64 key, u32 value) pairs on the
 // low `bits` bits of the key (bits multiple of 8).  Sorted data ends in
-// keys/vals; ktmp/vtmp are same-sized work arrays.
+// keys/vals; ktmp/vtmp are same-sized work arrays.  vals and vtmp may both
+// be null: keys only.
 hipError_t radix_sort_kv(dm_ctx* c, uint64_t* keys, uint32_t* vals, uint64_t* ktmp,
                          uint32_t* vtmp, uint64_t n, int bits);
 
@@ -242,14 +263,34 @@ struct GroupView {
 //     leader's keys as it is computed, and its longest cached prefix from
 //     that comparison and probes past the first disagreement; its keys are
 //     stored into hkeys only when write_keys is set.
+//   hash_prefix with the hotness tree on: requests whose depth-K prefix is
+//     extended are listed (ext_list, *ext_count zeroed beforehand) for
+//     hash_extend, which walks them down the tree to K_r and rewrites their
+//     ring keys.  key_len (optional) gets every request's K_r.
+//   keylen_record: every request's prefixes of depth >= K (its f1 block
+//     keys from block K - 1 on, in hkeys at bstart[r]) join the window.
 hipError_t hash_prefix(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
-                       const uint32_t* bad, uint64_t* key_out);
+                       const uint32_t* bad, uint64_t* key_out, uint32_t* key_len,
+                       uint32_t* ext_list, unsigned long long* ext_count);
+hipError_t hash_extend(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
+                       const uint32_t* bad, uint64_t* key_out, uint32_t* key_len,
+                       const uint32_t* ext_list, const unsigned long long* ext_count);
 hipError_t hash_leaders(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
                         const uint64_t* bstart, const uint32_t* bad, const GroupView& gv,
                         const uint32_t* cand, uint64_t* hkeys, uint32_t* match);
 hipError_t hash_members(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
                         const uint64_t* bstart, const uint32_t* bad, const GroupView& gv,
                         const uint32_t* cand, uint64_t* hkeys, bool write_keys, uint32_t* match);
+
+// dm_keylen.hip: the hotness tree's set-up, window close and export
+// (host entry points; they synchronise), and its release.
+dm_status keylen_enable(dm_ctx* c, uint64_t max_nodes, uint64_t max_window_blocks);
+hipError_t keylen_record(dm_ctx* c, uint64_t n, const uint64_t* bstart, const uint64_t* hkeys,
+                         uint64_t* work);
+uint64_t keylen_record_bytes(uint64_t n);
+dm_status keylen_window(dm_ctx* c);
+dm_status keylen_export(dm_ctx* c, uint64_t* keys_host, uint64_t cap, uint64_t* n_host);
+void keylen_free(dm_ctx* c);
 
 // dm_probe.hip: candidates on the current rings (cand, fix-up flag bit 3),
 // then requests ordered by their first ring key and grouped (gv).

@@ -28,7 +28,12 @@ constexpr int kKeySlot = kSlotKeys;  // block keys when the caller keeps none
 
 // Clears the batch's malformed-offsets word (a kernel rather than a memset,
 // so that a captured graph replays it like the rest of the batch).
-__global__ void route_zero_kernel(uint32_t* bad) { *bad = 0; }
+__global__ void route_zero_kernel(uint32_t* bad, unsigned long long* ext_count)
+{
+    *bad = 0;
+    if (ext_count)
+        *ext_count = 0;
+}
 
 }  // namespace
 
@@ -66,6 +71,9 @@ void route_scratch_plan(const dm_ctx* c, uint64_t n, uint64_t n_tokens, bool key
     bytes[kSlotSort] = sort_scratch_bytes(n);         // digit counts of the ordering sort
     const uint64_t s1 = scan_scratch_bytes(n), s2 = scan_scratch_bytes(sort_scan_len(n));
     bytes[kSlotScan] = s1 > s2 ? s1 : s2;             // tile sums of both kinds of scan
+    if (c->kl.on)  // requests going down the tree; the window record's offsets
+        bytes[kSlotRebalance] = 256 + ((n * sizeof(uint32_t) + 255) & ~255ull) +
+                                keylen_record_bytes(n);
 }
 
 hipError_t route(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens, const int64_t* offsets,
@@ -98,10 +106,27 @@ hipError_t route(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens, const int6
     if (!bstart)
         return e;
     uint32_t* bad = reinterpret_cast<uint32_t*>(bstart + n + 1);
-    route_zero_kernel<<<1, 1, 0, st>>>(bad);
+    // with the hotness tree: the count (first 256 bytes), then the list of
+    // requests going down the tree
+    unsigned long long* ext_count = nullptr;
+    uint32_t* ext_list = nullptr;
+    uint64_t* kl_work = nullptr;
+    if (c->kl.on) {
+        const uint64_t list_bytes = (n * sizeof(uint32_t) + 255) & ~255ull;
+        uint8_t* w = static_cast<uint8_t*>(scratch_get(
+            c, kSlotRebalance, 256 + list_bytes + keylen_record_bytes(n), &e));
+        if (!w)
+            return e;
+        ext_count = reinterpret_cast<unsigned long long*>(w);
+        ext_list = reinterpret_cast<uint32_t*>(w + 256);
+        kl_work = reinterpret_cast<uint64_t*>(w + 256 + list_bytes);
+    }
+    route_zero_kernel<<<1, 1, 0, st>>>(bad, ext_count);
     if ((e = block_starts(c, offsets, n, n_tokens, bstart, bad)) != hipSuccess)
         return e;
     uint64_t* hkeys = out->block_keys;
+    // the hotness tree's window records every request's block keys
+    const bool write_keys = out->block_keys != nullptr || c->kl.on;
     if (!hkeys) {
         // Requests that pass the offsets check are disjoint ranges of the
         // token array, so they hold at most n_tokens / B full blocks: the
@@ -114,16 +139,26 @@ hipError_t route(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens, const int6
     if (ev && (e = hipEventRecord(ev[1], st)) != hipSuccess)
         return e;
     GroupView gv{};
-    if ((e = hash_prefix(c, tokens, offsets, n, bad, out->key)) != hipSuccess ||
-        (e = lookup_group(c, n, out->key, bstart, bad, out->cand, out->flags, &gv)) != hipSuccess)
+    if ((e = hash_prefix(c, tokens, offsets, n, bad, out->key, out->key_len, ext_list,
+                         ext_count)) != hipSuccess)
+        return e;
+    if (c->kl.on && (e = hash_extend(c, tokens, offsets, n, bad, out->key, out->key_len, ext_list,
+                                     ext_count)) != hipSuccess)
+        return e;
+    if ((e = lookup_group(c, n, out->key, bstart, bad, out->cand, out->flags, &gv)) != hipSuccess)
         return e;
     if (ev && (e = hipEventRecord(ev[2], st)) != hipSuccess)
         return e;
     if ((e = hash_leaders(c, tokens, offsets, n, bstart, bad, gv, out->cand, hkeys, out->match)) !=
             hipSuccess ||
-        (e = hash_members(c, tokens, offsets, n, bstart, bad, gv, out->cand, hkeys,
-                          out->block_keys != nullptr, out->match)) != hipSuccess)
+        (e = hash_members(c, tokens, offsets, n, bstart, bad, gv, out->cand, hkeys, write_keys,
+                          out->match)) != hipSuccess)
         return e;
+    if (c->kl.on) {
+        if ((e = keylen_record(c, n, bstart, hkeys, kl_work)) != hipSuccess)
+            return e;
+        c->kl.win += n;
+    }
     if (ev && (e = hipEventRecord(ev[3], st)) != hipSuccess)
         return e;
     if ((e = select_prepare(c, st, offsets, n, out, par)) != hipSuccess)

@@ -52,7 +52,7 @@ __global__ __launch_bounds__(kSortThreads) void digit_scatter_kernel(
         const uint64_t i = base + it * kSortThreads + threadIdx.x;
         ok[it] = i < n;
         k[it] = ok[it] ? keys[i] : 0;
-        v[it] = ok[it] ? vals[i] : 0;
+        v[it] = ok[it] && vals ? vals[i] : 0;
         d[it] = (uint32_t)((k[it] >> shift) & 0xFF);
         uint64_t peers = ballot(ok[it]);
 #pragma unroll
@@ -84,7 +84,8 @@ __global__ __launch_bounds__(kSortThreads) void digit_scatter_kernel(
         const uint64_t pos = offs[(uint64_t)d[it] * ntiles + blockIdx.x] +
                              sub[it * (kSortThreads / kWave) + w][d[it]] + rank[it];
         okeys[pos] = k[it];
-        ovals[pos] = v[it];
+        if (ovals)
+            ovals[pos] = v[it];
     }
 }
 
@@ -121,7 +122,7 @@ hipError_t radix_sort_kv(dm_ctx* c, uint64_t* keys, uint32_t* vals, uint64_t* kt
     }
     if (passes & 1) {
         e = hipMemcpyAsync(keys, sk, n * sizeof(uint64_t), hipMemcpyDeviceToDevice, c->stream);
-        if (e == hipSuccess)
+        if (e == hipSuccess && vals)
             e = hipMemcpyAsync(vals, sv, n * sizeof(uint32_t), hipMemcpyDeviceToDevice, c->stream);
         if (e != hipSuccess)
             return e;

@@ -224,6 +224,14 @@ def agent_base_work(cfg, mu: int) -> np.ndarray:
     return base
 
 
+def _close_window(side, stage, b):
+    """With the prefix hotness tree on, every routed batch is one window."""
+    if getattr(side, "keylen", False):
+        side.window()
+        return ("window", b, {"tree": side.tree()})
+    return None
+
+
 def run_agent(side, cfg, mu: int, n_batches: int, warm: bool = True):
     import workloads
     rc = cfg.route
@@ -238,6 +246,9 @@ def run_agent(side, cfg, mu: int, n_batches: int, warm: bool = True):
                                lambda: workloads.agent_batch(cfg, w // cfg.batch, n, warm=True))
             out = side.route(tok, off, Lw)
             yield "warm", w // cfg.batch, out
+            win = _close_window(side, "warm", w // cfg.batch)
+            if win:
+                yield win
             Lw = out["loads"]
             u1, u2 = _uncached(out, off, B)
             unc_sum += int(np.where(out["chosen"] == out["cand"][:n], u1, u2).sum())
@@ -251,6 +262,9 @@ def run_agent(side, cfg, mu: int, n_batches: int, warm: bool = True):
         n = len(off) - 1
         out = side.route(tok, off, qs.loads())
         yield "route", b, out
+        win = _close_window(side, "route", b)
+        if win:
+            yield win
         c1, c2 = out["cand"][:n].astype(np.int64), out["cand"][n:].astype(np.int64)
         ch = out["chosen"].astype(np.int64)
         u1, u2 = _uncached(out, off, B)

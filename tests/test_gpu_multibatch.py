@@ -36,9 +36,18 @@ def _say(*a):
 
 
 class OracleSide:
-    def __init__(self, rc):
+    def __init__(self, rc, keylen_nodes=0):
         self.o = oracle.Oracle(rc.as_dict())
         assert self.o.build_rings(range(rc.n_inst)) == 0
+        self.keylen = keylen_nodes > 0
+        if self.keylen:
+            assert self.o.keylen_enable(keylen_nodes) == oracle.OK
+
+    def window(self):
+        assert self.o.keylen_window() == oracle.OK
+
+    def tree(self):
+        return self.o.keylen_tree()
 
     def route(self, tok, off, loads):
         return self.o.route(tok, off, loads, block_keys=True)
@@ -56,11 +65,20 @@ class OracleSide:
 
 
 class EngineSide:
-    def __init__(self, rc):
+    def __init__(self, rc, keylen_nodes=0):
         import paper_2602_06502_amd.harness as gh
         self.gh = gh
         self.eng = gh.DualMap(rc.as_dict(), device="cuda:0")
         self.eng.build_rings(list(range(rc.n_inst)))
+        self.keylen = keylen_nodes > 0
+        if self.keylen:
+            self.eng.keylen_enable(keylen_nodes, 1 << 24)
+
+    def window(self):
+        self.eng.keylen_window()
+
+    def tree(self):
+        return self.eng.keylen_tree()
 
     def _d(self, a):
         return self.gh.to_dev(a, self.eng.device)
@@ -89,12 +107,13 @@ class EngineSide:
         return res
 
 
-ROUTE_KEYS = ("key", "cand", "match", "chosen", "ttft", "flags", "block_keys", "loads")
+ROUTE_KEYS = ("key", "cand", "match", "chosen", "ttft", "flags", "block_keys", "loads", "key_len")
 MIGRATION_KEYS = ("rec", "src", "dst", "benefit", "ttft_to", "loads")
 
 
 def _compare(stage, b, g, o):
-    keys = ROUTE_KEYS if stage in ("warm", "route") else MIGRATION_KEYS
+    keys = (ROUTE_KEYS if stage in ("warm", "route") else
+            ("tree",) if stage == "window" else MIGRATION_KEYS)
     for k in keys:
         assert np.array_equal(g[k], o[k]), f"{stage} batch {b}: {k} differs"
     if stage == "rebalance":
@@ -141,3 +160,30 @@ def test_agent_multibatch_parity():
             queued += o["queued"]
     assert migrated > 0
     _say("agent migrated", migrated, "of", queued, "queued records over 16 passes")
+
+
+def test_agent_multibatch_adaptive_keylen_parity():
+    """The agent workload with the prefix hotness tree on (Sec. 3.2): every
+    batch is one window; hot system prompts extend their hash keys window by
+    window, so their requests spread over more candidate pairs.  Routes,
+    trees after every window and rebalancing passes against the oracle."""
+    _gpu()
+    cfg = workloads.agent()
+    rc = cfg.route
+    gs, os_ = EngineSide(rc, keylen_nodes=4096), OracleSide(rc, keylen_nodes=4096)
+    migrated = queued = 0
+    deepest = 0
+    for (st, b, g), (st2, b2, o) in zip(sim.run_agent(gs, cfg, cfg.mu, 16),
+                                        sim.run_agent(os_, cfg, cfg.mu, 16)):
+        assert (st, b) == (st2, b2)
+        _compare(st, b, g, o)
+        if st == "route":
+            deepest = max(deepest, int(o["key_len"].max()))
+        if st == "window":
+            _say("agent keylen window", b, "extended prefixes", len(o["tree"]))
+        if st == "rebalance":
+            migrated += o["count"]
+            queued += o["queued"]
+    assert deepest > rc.key_blocks
+    _say("agent (adaptive keys) migrated", migrated, "of", queued, "queued records; deepest key",
+         deepest, "blocks")

@@ -53,6 +53,8 @@ def compare_route(g, o, n, with_bk=False):
                                  f"gpu {a[bad[:5]]} oracle {b[bad[:5]]}")
     if with_bk:
         assert np.array_equal(cpu(g["block_keys"])[:len(o["block_keys"])], o["block_keys"])
+    if "key_len" in g:
+        assert np.array_equal(cpu(g["key_len"])[:n], o["key_len"]), "key_len"
 
 
 def run_pair(wl, block_keys=True, n_live=None):
@@ -205,6 +207,133 @@ def test_policy_rejects_unknown_rule():
         with pytest.raises(pk.DMError) as ei:
             eng.set_policy(bad)
         assert ei.value.status == pk.DM_EINVAL
+
+
+# ---------------------------------------------------------------------------
+# Adaptive hash-key length (prefix hotness tree)
+# ---------------------------------------------------------------------------
+
+def _hot_batches(seed, B, K, n_batches, tlen_blocks=(1, 40), n_tpl=8, zipf=1.3):
+    """Batches of prompts over Zipf-popular templates (whole templates or
+    cut past depth K, then a random tail): hot templates extend their keys
+    window by window, long ones past a 64-block chunk."""
+    rng = np.random.default_rng(seed)
+    tpl = [rng.integers(0, 1 << 20, size=B * int(rng.integers(K + tlen_blocks[0], K + tlen_blocks[1])),
+                        dtype=np.int32) for _ in range(n_tpl)]
+    w = 1.0 / np.arange(1, n_tpl + 1) ** zipf
+    w /= w.sum()
+    out = []
+    for _ in range(n_batches):
+        ps = []
+        for _ in range(int(rng.integers(200, 700))):
+            if rng.random() < 0.15:
+                ps.append(rng.integers(0, 1 << 20, size=int(rng.integers(0, 8 * B)), dtype=np.int32))
+                continue
+            t = tpl[int(rng.choice(n_tpl, p=w))]
+            cut = int(rng.integers(K * B, len(t) + 1))
+            ps.append(np.concatenate([t[:cut], rng.integers(0, 1 << 20, size=int(rng.integers(0, 4 * B)),
+                                                            dtype=np.int32)]))
+        off = np.zeros(len(ps) + 1, np.int64)
+        off[1:] = np.cumsum([len(p) for p in ps])
+        out.append((np.concatenate(ps) if ps else np.zeros(0, np.int32), off))
+    return out
+
+
+@pytest.mark.parametrize("B,K,n_inst,pipelined", [(16, 4, 8, False), (4, 60, 12, True),
+                                                  (32, 2, 32, False), (64, 3, 10, True),
+                                                  (8, 1, 16, False)])
+def test_keylen_windows_parity(B, K, n_inst, pipelined):
+    """Every batch one window: key lengths, ring keys and all routing outputs
+    per batch, and the tree after every window, against the oracle.  With
+    K = 60 the paths cross the extension walk's 64-block chunk boundary as
+    the tree deepens; short and empty prompts sit below the roots."""
+    gh = _h()
+    wl = workloads.small_random(71 + B, n_inst, 8, B, 64, slo_us=30_000, key_blocks=K)
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    eng.keylen_enable(4096, 1 << 20)
+    assert o.keylen_enable(4096) == oracle.OK
+    if pipelined:
+        eng.set_pipelining(True)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    Ld = gh.to_dev(L0, eng.device)
+    L = L0.copy()
+    deepest = 0
+    batches = _hot_batches(5 + B, B, K, 14, tlen_blocks=(1, 90))
+    for i, (tok, off) in enumerate(batches):
+        _say("keylen window", B, K, n_inst, i, "requests", len(off) - 1)
+        g = eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld)
+        eng.keylen_window()
+        r = o.route(tok, off, L)
+        assert o.keylen_window() == oracle.OK
+        L = r["loads"]
+        compare_route(g, r, len(off) - 1)
+        assert np.array_equal(eng.keylen_tree(), o.keylen_tree()), f"tree after window {i}"
+        deepest = max(deepest, int(r["key_len"].max()))
+    assert np.array_equal(cpu(Ld), L)
+    assert deepest > K + 1, deepest
+    if K + 14 > 64:
+        assert deepest > 64, deepest
+    eng.set_pipelining(False)
+
+
+def test_keylen_window_spans_batches_and_errors():
+    """Windows of several batches (pipelined), the record and tree limits,
+    and the tree turned off."""
+    gh = _h()
+    import paper_2602_06502_amd as pk
+    B, K = 16, 2
+    wl = workloads.small_random(81, 6, 8, B, 64, slo_us=30_000, key_blocks=K)
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    batches = _hot_batches(9, B, K, 9)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    with pytest.raises(pk.DMError) as ei:
+        eng.keylen_window()
+    assert ei.value.status == pk.DM_ESTATE
+    eng.keylen_enable(1024, 1 << 20)
+    o.keylen_enable(1024)
+    eng.set_pipelining(True)
+    Ld, L = gh.to_dev(L0, eng.device), L0.copy()
+    for i, (tok, off) in enumerate(batches):
+        n = len(off) - 1
+        _say("keylen multi-batch window", i, "requests", n)
+        g = eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld)
+        r = o.route(tok, off, L)
+        L = r["loads"]
+        if i % 3 == 2:  # three batches per window
+            eng.keylen_window()
+            assert o.keylen_window() == oracle.OK
+            assert np.array_equal(eng.keylen_tree(), o.keylen_tree()), i
+        eng.sync()
+        compare_route(g, r, n)
+    eng.set_pipelining(False)
+    assert np.array_equal(cpu(Ld), L)
+    assert len(o.keylen_tree()) > 0
+    # a tree too small for the next window's hot prefixes: DM_EFULL, unchanged
+    eng.keylen_enable(2, 1 << 20)
+    assert o.keylen_enable(2) == oracle.OK
+    for tok, off in batches[:2]:
+        eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld)
+        o.route(tok, off, L)
+    assert o.keylen_window() == oracle.EFULL
+    with pytest.raises(pk.DMError) as ei:
+        eng.keylen_window()
+    assert ei.value.status == pk.DM_EFULL
+    assert len(eng.keylen_tree()) == 0 == len(o.keylen_tree())
+    # prefixes past the record's room: reported by dm_sync, and the close
+    # leaves the tree unchanged
+    eng.keylen_enable(64, 16)
+    td, od = gh.to_dev(batches[0][0], eng.device), gh.to_dev(batches[0][1], eng.device)
+    eng.route(td, od, Ld)
+    with pytest.raises(pk.DMError) as ei:
+        eng.sync()
+    assert ei.value.status == pk.DM_EFULL
+    with pytest.raises(pk.DMError) as ei:
+        eng.keylen_window()
+    assert ei.value.status == pk.DM_EFULL
+    assert len(eng.keylen_tree()) == 0
+    eng.keylen_enable(0)
+    with pytest.raises(pk.DMError):
+        eng.keylen_tree()
 
 
 def _disjoint_pair_prompts(o, rng, n_pool):

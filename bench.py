@@ -323,6 +323,72 @@ def policy_rows(eng, wl, st, L0):
     return rows
 
 
+def adaptive_leg(eng, wl, st, L0, base_out, base_loads, reps=3):
+    """Adaptive hash-key length (Sec. 3.2) on the large batch: each route of
+    the batch is one window of the prefix hotness tree, closed after it,
+    until the tree stops changing; then the batch is routed with the settled
+    tree.  Reported against the fixed-K route of the timed steps: key-length
+    spread, the hottest candidate pair's share of requests, the selection
+    walk's depth steps, cache hit rate, load CV and times."""
+    import numpy as np
+    import torch
+    n = wl.n_req
+    lens = np.diff(st["offsets_np"])
+
+    def stats(o, L):
+        ch = o["chosen"].cpu().numpy()
+        cand = o["cand"].cpu().numpy()
+        match = o["match"].cpu().numpy()
+        lo, hi = np.minimum(cand[:n], cand[n:]), np.maximum(cand[:n], cand[n:])
+        _, cnt = np.unique(lo.astype(np.int64) * 65536 + hi, return_counts=True)
+        m = np.where(ch == cand[:n], match[:n], match[n:]).astype(np.int64)
+        fin = L.cpu().numpy()[:wl.route.n_inst].astype(np.float64)
+        steps, windows = walk_steps(cand, match, n)
+        return {"hottest_pair_share": float(cnt.max() / n), "pairs": int(len(cnt)),
+                "select_depth_steps": steps, "select_windows": windows,
+                "hit_rate": float((m * wl.route.block).sum() / lens.sum()),
+                "final_load_cv": float(fin.std() / fin.mean())}
+
+    base = stats(base_out, base_loads)
+    eng.keylen_enable(1 << 16, 1 << 28)
+    sizes, close_ms = [], []
+    o = eng.alloc_route_out(n, key_len=True)
+    for w in range(6):
+        L = L0.clone()
+        eng.route_into(st["tokens"], st["offsets"], L, o)
+        eng.sync()
+        t0 = time.perf_counter()
+        eng.keylen_window()
+        close_ms.append(1000.0 * (time.perf_counter() - t0))
+        sizes.append(int(len(eng.keylen_tree())))
+        if len(sizes) >= 2 and sizes[-1] == sizes[-2]:
+            break
+    route_ms = []
+    for _ in range(reps):
+        L = L0.clone()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        eng.route_into(st["tokens"], st["offsets"], L, o)
+        eng.sync()
+        route_ms.append(1000.0 * (time.perf_counter() - t0))
+        eng.keylen_window()  # each route its own window (the tree has settled)
+    kl = o["key_len"].cpu().numpy()[:n]
+    ad = stats(o, L)
+    eng.keylen_enable(0)
+    K = wl.route.key_blocks
+    return {"windows_to_settle": len(sizes), "tree_sizes": sizes,
+            "key_len": {"K": K, "frac_above_K": float((kl > K).mean()),
+                        "p50": float(np.percentile(kl, 50)), "p99": float(np.percentile(kl, 99)),
+                        "max": int(kl.max())},
+            "fixed_K": base, "adaptive": ad,
+            "route_ms": float(np.median(route_ms)), "window_close_ms": float(np.median(close_ms)),
+            "note": "each window is one route of the whole batch from the same loads, closed "
+                    "after it; route_ms: unpipelined dm_route_batch with the settled tree (the "
+                    "window record of every prefix of depth >= K included), host wall clock; "
+                    "window_close_ms: dm_keylen_window (sort and count of the record, tree "
+                    "rebuild); fixed_K: the timed steps' route"}
+
+
 def elastic_leg(eng, wl, st, keys, L0, reps):
     """Rows a8/a9 at full size, timed on the host clock around each call (both
     entry points synchronise with the engine's stream before they return):
@@ -413,6 +479,8 @@ def main():
     ap.add_argument("--elastic-reps", type=int, default=5)
     ap.add_argument("--no-elastic", action="store_true",
                     help="skip the scale / re-route / rebalance timings")
+    ap.add_argument("--no-adaptive", action="store_true",
+                    help="skip the adaptive hash-key length leg")
     ap.add_argument("--no-policies", action="store_true",
                     help="skip the per-rule routes (cache affinity, least loaded, min TTFT)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -563,6 +631,10 @@ def main():
     if not args.no_policies:
         log("selection rules of the ablation study")
         res["policies"] = policy_rows(eng, wl, st, L0)
+    if not args.no_adaptive:
+        log("adaptive hash-key length")
+        res["adaptive_key_length"] = adaptive_leg(eng, wl, st, L0, out,
+                                                  loads[args.warmup + args.steps - 1])
     if not args.no_elastic:
         log("elastic leg: scale, re-route, rebalance")
         res["elastic"] = elastic_leg(eng, wl, st, out["key"], L0, args.elastic_reps)

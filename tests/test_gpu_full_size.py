@@ -167,6 +167,42 @@ def test_large_replay_property(large):
     assert (f & 1).any() and (f & 2).any() and (f & 4).any() and (~f & 4).any()
 
 
+def test_large_adaptive_keylen_full_parity(large, large_oracle):
+    """The prefix hotness tree on the large batch (Sec. 3.2): one window
+    routes the batch with the empty tree and closes (the hot templates'
+    prefixes extend to where their requests part); the next routes it again
+    with key lengths from that tree.  The second batch, its key lengths and
+    the tree against the oracle doing the same, over the whole batch."""
+    wl, g, eng, gh = large["wl"], large["g"], large["eng"], large["gh"]
+    o = large_oracle
+    eng.keylen_enable(1 << 16, 1 << 28)
+    assert o.keylen_enable(1 << 16) == oracle.OK
+    try:
+        _say("adaptive keys: window 1 (empty tree)")
+        L = gh.to_dev(g["loads0"], eng.device)
+        eng.route(g["tokens"], g["offsets"], L)
+        eng.keylen_window()
+        o.route(g["tokens_np"], g["offsets_np"], g["loads0"])
+        assert o.keylen_window() == oracle.OK
+        tree = o.keylen_tree()
+        assert np.array_equal(eng.keylen_tree(), tree)
+        assert len(tree) > 0
+        _say("adaptive keys: window 2,", len(tree), "extended prefixes")
+        L = gh.to_dev(g["loads0"], eng.device)
+        out = eng.route(g["tokens"], g["offsets"], L)
+        eng.sync()
+        got = {k: v.cpu().numpy() for k, v in out.items()}
+        got["loads"] = L.cpu().numpy()
+        del out
+        ref = o.route(g["tokens_np"], g["offsets_np"], g["loads0"])
+        compare_full(got, ref, "large, adaptive key lengths")
+        assert np.array_equal(got["key_len"], ref["key_len"])
+        assert (ref["key_len"] > wl.route.key_blocks).any()
+    finally:
+        eng.keylen_enable(0)
+        o.keylen_enable(0)
+
+
 def test_elastic_scale_full(large):
     wl, gh, eng, out = large["wl"], large["gh"], large["eng"], large["out"]
     n = wl.n_req

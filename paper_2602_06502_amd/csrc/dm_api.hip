@@ -508,9 +508,13 @@ dm_status dm_scale(dm_ctx* c, const uint32_t* add, uint32_t n_add, const uint32_
     if (e == hipSuccess)
         e = ring_remap(c, c->ring[c->cur], c->ring[nb], keys, n, old_owner, new_owner, moved,
                        violations);
-    for (uint32_t i = 0; i < S && e == hipSuccess; i++)
-        if (fa[i] || fr[i])
-            e = index_clear(c, i);
+    if (e == hipSuccess) {
+        std::vector<uint32_t> changed;
+        for (uint32_t i = 0; i < S; i++)
+            if (fa[i] || fr[i])
+                changed.push_back(i);
+        e = index_clear_many(c, changed.data(), (uint32_t)changed.size());
+    }
     if (e != hipSuccess) {
         c->live = old_live;
         c->n_live = old_n;

@@ -14,6 +14,8 @@
 // settles the list in order (present already, stored while room is left,
 // else dropped with DM_EFULL).  So a batch that fits is stored whole, and a
 // batch that does not fills the table to exactly the limit.
+#include <algorithm>
+
 #include "dm_internal.h"
 
 namespace dm {
@@ -237,6 +239,24 @@ __global__ void clear_kernel(uint64_t* __restrict__ slots, uint64_t n, uint64_t*
     }
 }
 
+// Tables of several instances emptied at once: grid row y clears table
+// ids[y] (and its counts).
+__global__ void clear_many_kernel(uint64_t* __restrict__ tables, uint32_t log2slots,
+                                  const uint32_t* __restrict__ ids, uint64_t* __restrict__ counts,
+                                  uint32_t S)
+{
+    const uint32_t id = ids[blockIdx.y];
+    uint64_t* slots = tables + ((uint64_t)id << log2slots);
+    const uint64_t n = 1ull << log2slots;
+    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < n;
+         i += (uint64_t)gridDim.x * blockDim.x)
+        slots[i] = kEmpty;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        counts[id] = 0;      // live keys
+        counts[S + id] = 0;  // occupied slots
+    }
+}
+
 TableRef table_of(dm_ctx* c, uint32_t id)
 {
     const uint32_t k = c->cfg.index_log2_slots;
@@ -273,6 +293,26 @@ hipError_t index_insert(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n
 hipError_t index_erase(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n)
 {
     erase_kernel<<<grid_for(n, 256), 256, 0, c->stream>>>(table_of(c, id), keys, n);
+    return hipGetLastError();
+}
+
+hipError_t index_clear_many(dm_ctx* c, const uint32_t* ids_host, uint32_t n)
+{
+    if (n == 0)
+        return hipSuccess;
+    hipError_t e = hipSuccess;
+    uint32_t* d = static_cast<uint32_t*>(scratch_get(c, kPurgeSlot, n * sizeof(uint32_t), &e));
+    if (!d)
+        return e;
+    if ((e = hipMemcpyAsync(d, ids_host, n * sizeof(uint32_t), hipMemcpyHostToDevice,
+                            c->stream)) != hipSuccess ||
+        (e = hipStreamSynchronize(c->stream)) != hipSuccess)
+        return e;
+    const uint32_t k = c->cfg.index_log2_slots;
+    const uint64_t per = std::max<uint64_t>(1, 4096 / n);
+    dim3 grid((uint32_t)std::min<uint64_t>(per, ((1ull << k) + 255) / 256), n);
+    clear_many_kernel<<<grid, 256, 0, c->stream>>>(c->d_tables, k, d, c->d_counts,
+                                                   c->cfg.max_slots);
     return hipGetLastError();
 }
 

@@ -244,6 +244,8 @@ hipError_t ring_remap(dm_ctx* c, const Ring old_r[2], const Ring new_r[2], const
 hipError_t index_insert(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n);
 hipError_t index_erase(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n);
 hipError_t index_clear(dm_ctx* c, uint32_t id);
+// the tables of n instances (host list) emptied by one launch
+hipError_t index_clear_many(dm_ctx* c, const uint32_t* ids_host, uint32_t n);
 
 // Requests grouped by equal ring keys (dm_probe.hip): group_of[r] is
 // request r's group, leader[g] is group g's leader request, *groups = G.

@@ -60,6 +60,9 @@ constexpr int kCommitBatch = 16; // candidates whose loads are in flight togethe
 // source with more uses the same layout in device memory
 constexpr uint32_t kLdsBitWords = 8192;
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;
+// Passes with at most this many overloaded sources run each source's commit
+// phases as kernels over the whole GPU; more sources, one workgroup for all.
+constexpr uint32_t kSpreadSources = 64;
 
 struct TtftK {
     int64_t base, per;
@@ -230,7 +233,8 @@ __global__ void queue_over_kernel(const int64_t* __restrict__ qoff, uint64_t Q,
                                   const int64_t* __restrict__ slice_max, uint32_t S, int64_t slo,
                                   const int64_t* __restrict__ interval, int64_t thresh,
                                   int64_t* __restrict__ L0, uint8_t* __restrict__ over,
-                                  int64_t* __restrict__ delay, uint32_t* __restrict__ status)
+                                  int64_t* __restrict__ delay, int64_t* __restrict__ slo_of,
+                                  uint32_t* __restrict__ status)
 {
     const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= S)
@@ -253,6 +257,7 @@ __global__ void queue_over_kernel(const int64_t* __restrict__ qoff, uint64_t Q,
     }
     L0[i] = L;
     delay[i] = d;
+    slo_of[i] = slo - d;
     over[i] = (busy && mx > slo - d) ? 1 : 0;
 }
 
@@ -509,6 +514,10 @@ struct CommitArgs {
     uint32_t* qkey;           // [Q]
     int64_t* loads;           // [S] in: pass-start loads; out: loads after the pass
     const int64_t* delay;     // [S] decode delay per instance (0 unless stalled)
+    const int64_t* slo_of;    // [S] the SLO less each instance's decode delay
+    uint32_t* wpre_src;       // [C / 32 + 2] per source: accepted candidates before each word
+    uint32_t* acc_of;         // [nsrc] accepted candidates per source
+    unsigned long long* run;  // [1] migrations so far (sources in rank order)
     uint32_t S;
     TtftK tk;
     uint64_t cap;
@@ -925,6 +934,179 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a)
 }
 
 
+// ---------------------------------------------------------------------------
+// The same commit spread over the GPU, one source at a time (the host
+// launches these in source-rank order), for passes with few sources: every
+// phase that the single workgroup above runs for a source becomes a kernel
+// over all compute units, except the prefix of acceptance bits and the stop
+// point, which stay on one workgroup.  The acceptance bits are indexed by
+// candidate (all zero at the start of the pass); loads live in loads_out.
+// ---------------------------------------------------------------------------
+
+// Walk of source s's segments, one wave per segment; the blocks also reset
+// the source's queue keys.
+__global__ __launch_bounds__(256) void src_walk_kernel(CommitArgs a, uint32_t s)
+{
+    if (s >= *a.nsrc)
+        return;
+    const uint32_t i = a.src[s];
+    const int64_t qlo = a.qoff[i], qhi = a.qoff[i + 1];
+    for (int64_t q = qlo + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < qhi;
+         q += (int64_t)gridDim.x * blockDim.x)
+        a.qkey[q] = kNoKey;
+    const uint64_t wv = blockIdx.x * (uint64_t)(blockDim.x >> 6) +
+                        __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint64_t nwv = (uint64_t)gridDim.x * (blockDim.x >> 6);
+    const uint32_t G0 = a.sseg[s], G1 = a.sseg[s + 1];
+    for (uint64_t g = G0 + wv; g < G1; g += nwv)
+        walk_run(a, nullptr, a.gbits, false, a.loads, a.slo_of, 0, a.seg_pos[g],
+                 a.seg_pos[g + 1]);
+}
+
+// Accepted candidates of source s before each of its bit words (bits of
+// other sources masked off), and their total.
+__global__ __launch_bounds__(kCommitThreads) void src_rank_kernel(CommitArgs a, uint32_t s)
+{
+    __shared__ int64_t sh[kCommitThreads / kWave];
+    if (s >= *a.nsrc)
+        return;
+    const uint32_t cs = a.start[s], ce = a.start[s + 1];
+    if (cs == ce) {
+        if (threadIdx.x == 0)
+            a.acc_of[s] = 0;
+        return;
+    }
+    const uint32_t w0 = cs >> 5, w1 = ((ce - 1) >> 5) + 1, nw = w1 - w0;
+    auto word = [&](uint32_t w) -> uint32_t {
+        uint32_t v = a.gbits[w];
+        if (w == w0)
+            v &= ~0u << (cs & 31);
+        if (w == w1 - 1 && (ce & 31))
+            v &= (1u << (ce & 31)) - 1;
+        return v;
+    };
+    const uint64_t per = ((uint64_t)nw + kCommitThreads - 1) / kCommitThreads;
+    const uint32_t a0 = w0 + (uint32_t)std::min<uint64_t>(nw, threadIdx.x * per);
+    const uint32_t a1 = w0 + (uint32_t)std::min<uint64_t>(nw, (threadIdx.x + 1) * per);
+    int64_t cnt = 0;
+    for (uint32_t w = a0; w < a1; w++)
+        cnt += __popc(word(w));
+    int64_t A;
+    uint32_t run = (uint32_t)block_excl_scan_i64<kCommitThreads>(cnt, sh, A);
+    for (uint32_t w = a0; w < a1; w++) {
+        a.wpre_src[w] = run;
+        run += __popc(word(w));
+    }
+    if (threadIdx.x == 0)
+        a.acc_of[s] = (uint32_t)A;
+}
+
+// Acceptance rank of every candidate of source s (kNoKey if not accepted),
+// and as the key of its queue record.
+__global__ void src_mark_kernel(CommitArgs a, uint32_t s)
+{
+    if (s >= *a.nsrc)
+        return;
+    const uint32_t cs = a.start[s], ce = a.start[s + 1];
+    for (uint64_t t = cs + blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < ce;
+         t += (uint64_t)gridDim.x * blockDim.x) {
+        const uint32_t w = (uint32_t)(t >> 5), m = 1u << (t & 31);
+        uint32_t v = a.gbits[w];
+        if (w == (cs >> 5))
+            v &= ~0u << (cs & 31);
+        uint32_t rk = kNoKey;
+        if (v & m) {
+            rk = a.wpre_src[w] + __popc(v & (m - 1));
+            a.qkey[a.cand_q[t]] = rk;
+        }
+        a.arank[t] = rk;
+    }
+}
+
+// Stop point of source s (smallest k after which its queue meets the SLO,
+// all accepted if none) and its place in the migration list.
+__global__ __launch_bounds__(kCommitThreads) void src_stop_kernel(CommitArgs a, uint32_t s)
+{
+    __shared__ int64_t sh[kCommitThreads / kWave];
+    if (s >= *a.nsrc)
+        return;
+    const uint32_t i = a.src[s];
+    const uint32_t A = a.acc_of[s];
+    uint32_t kstar = 0;
+    if (A > 0) {
+        const int64_t qlo = a.qoff[i], qhi = a.qoff[i + 1];
+        const int64_t w0q = a.base_work[i];
+        const uint64_t Lq = (uint64_t)(qhi - qlo);
+        TtftK tks = a.tk;
+        tks.slo = a.slo_of[i];
+        uint32_t lo = 1, hi = A;
+        if (Lq <= (uint64_t)kCommitThreads * kQueueRegs) {
+            lo = regs_bisect(a.unc_here, a.qkey, qlo, Lq, w0q, hi, tks, sh);
+        } else if (queue_violates_chunked(a, tks, qlo, qhi, w0q, hi, sh)) {
+            lo = hi;
+        } else {
+            while (lo < hi) {
+                const uint32_t mid = lo + (hi - lo) / 2;
+                if (!queue_violates_chunked(a, tks, qlo, qhi, w0q, mid, sh))
+                    hi = mid;
+                else
+                    lo = mid + 1;
+            }
+        }
+        kstar = lo;
+    }
+    if (threadIdx.x == 0) {
+        const unsigned long long base = *a.run;
+        a.kstar_of[s] = kstar;
+        a.base_of[s] = base;
+        *a.run = base + kstar;
+    }
+}
+
+// The first k* accepted records of source s move: one wave per segment
+// adds its moved records' uncached tokens to its target (segments of a
+// source have distinct targets) and takes theirs on the source away.
+__global__ __launch_bounds__(256) void src_commit_kernel(CommitArgs a, uint32_t s)
+{
+    if (s >= *a.nsrc)
+        return;
+    const uint32_t i = a.src[s], kstar = a.kstar_of[s];
+    const uint64_t wv = blockIdx.x * (uint64_t)(blockDim.x >> 6) +
+                        __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint64_t nwv = (uint64_t)gridDim.x * (blockDim.x >> 6);
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t G0 = a.sseg[s], G1 = a.sseg[s + 1];
+    for (uint64_t g = G0 + wv; g < G1; g += nwv) {
+        const uint32_t P0 = a.seg_pos[g], P1 = a.seg_pos[g + 1];
+        uint64_t to = 0, from = 0;
+        for (uint64_t v = P0 + lane; v < P1; v += kWave) {
+            const uint32_t t = a.grp[v];
+            if (a.arank[t] < kstar) {
+                to += a.g_unc[v];
+                from += a.c_uh[t];
+            }
+        }
+        to = wave_incl_sum_u64(to, (int)lane);
+        from = wave_incl_sum_u64(from, (int)lane);
+        to = readlane_u64(to, kWave - 1);
+        from = readlane_u64(from, kWave - 1);
+        if (lane == 0 && P0 < P1) {
+            const uint32_t j = a.g_alt[P0];
+            a.loads[j] += (int64_t)to;
+            if (from)
+                atomicAdd((unsigned long long*)&a.loads[i], (unsigned long long)(-(int64_t)from));
+        }
+    }
+}
+
+__global__ void src_finish_kernel(CommitArgs a)
+{
+    const unsigned long long n = *a.run;
+    *a.out_count = n;
+    if (n > a.cap)
+        atomicOr(a.status, kErrFull);
+}
+
 // Migration list: candidate t of source rank r moves iff its acceptance rank
 // is below kstar_of[r]; it lands at base_of[r] + rank (rank order within a
 // source, sources in rank order).
@@ -985,15 +1167,18 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     hipStream_t st = c->stream;
     hipError_t e;
     // per-instance arrays
-    // per instance slot: L0, delay, base_of 8 B; over 1 B; rank, src, start,
-    // sseg, kstar_of 4 B; slice sums and maxima 2 x 8 x kQSplit B -- 301 B,
-    // and 13 carves of at most 256 B padding
+    // per instance slot: L0, delay, slo_of, base_of 8 B; over 1 B; rank,
+    // src, start, sseg, kstar_of, acc_of 4 B; slice sums and maxima
+    // 2 x 8 x kQSplit B -- 313 B, and 16 carves of at most 256 B padding
     uint8_t* pi = static_cast<uint8_t*>(
         scratch_get(c, kSlotSelect, 320 * ((uint64_t)S + 64) + 8192, &e));
     if (!pi)
         return e;
     int64_t* L0 = carve<int64_t>(pi, S);
     int64_t* delay = carve<int64_t>(pi, S);
+    int64_t* slo_of = carve<int64_t>(pi, S);
+    uint32_t* acc_of = carve<uint32_t>(pi, S);
+    unsigned long long* run = carve<unsigned long long>(pi, 1);
     uint8_t* over = carve<uint8_t>(pi, S);
     uint32_t* rank = carve<uint32_t>(pi, S);
     uint32_t* src = carve<uint32_t>(pi, S);
@@ -1028,7 +1213,7 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     queue_over_kernel<<<(S + 255) / 256, 256, 0, st>>>(q->qoff, Q, q->base_work, slice_sum,
                                                         slice_max, S, tk.slo, q->prefill_interval,
                                                         q->decode_threshold_us, L0, over, delay,
-                                                        c->d_status);
+                                                        slo_of, c->d_status);
     if (Q)
         // grid-stride: 256 workgroups, one atomic maximum each
         benefit_kernel<<<grid_for(Q, 256, 256), 256, 0, st>>>(Q, T, owner, q->alt, q->unc_alt, L0,
@@ -1036,11 +1221,14 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
                                                               ctot + 1);
     rank_kernel<<<(S + 255) / 256, 256, 0, st>>>(L0, over, S, rank, src, nsrc);
     uint64_t hw[2] = {0, 0};  // candidate count, largest eligible benefit
+    uint32_t nsrc_h = 0;      // overloaded sources
     if (Q) {
         e = exclusive_scan_u64(c, elig, Q, pos, ctot);
         if (e != hipSuccess)
             return e;
         e = hipMemcpyAsync(hw, ctot, sizeof(hw), hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(&nsrc_h, nsrc, sizeof(nsrc_h), hipMemcpyDeviceToHost, st);
         if (e == hipSuccess)
             e = hipStreamSynchronize(st);
         if (e != hipSuccess)
@@ -1051,8 +1239,8 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     const uint64_t Ca = C ? C : 1;
     uint8_t* pc = static_cast<uint8_t*>(scratch_get(c, kSlotRebalance, Ca * 64 + 16 * 256, &e));
     // per candidate: keys, ktmp 8 B; vals, vtmp, grp, g_alt, g_unc, seg_pos,
-    // c_ua, c_uh, arank 4 B; tto 8 B; two bit-word arrays 1/8 B -- 60.25 B
-    // and 14 carves of at most 256 B padding each
+    // c_ua, c_uh, arank 4 B; tto 8 B; three bit-word arrays 1/8 B -- 60.4 B
+    // and 15 carves of at most 256 B padding each
     if (!pc)
         return e;
     uint64_t* keys = carve<uint64_t>(pc, Ca);
@@ -1064,6 +1252,7 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     uint32_t* g_unc = carve<uint32_t>(pc, Ca);
     uint32_t* gbits = carve<uint32_t>(pc, Ca / 32 + 1);
     uint32_t* gwpre = carve<uint32_t>(pc, Ca / 32 + 1);
+    uint32_t* wpre_src = carve<uint32_t>(pc, Ca / 32 + 2);
     int64_t* tto = carve<int64_t>(pc, Ca);
     uint32_t* seg_pos = carve<uint32_t>(pc, Ca + 1);
     uint32_t* c_ua = carve<uint32_t>(pc, Ca);
@@ -1155,6 +1344,10 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     a.qkey = qkey;
     a.loads = loads_out;
     a.delay = delay;
+    a.slo_of = slo_of;
+    a.wpre_src = wpre_src;
+    a.acc_of = acc_of;
+    a.run = run;
     a.S = S;
     a.tk = tk;
     a.cap = cap;
@@ -1165,7 +1358,24 @@ hipError_t rebalance(dm_ctx* c, const dm_queues* q, int64_t* loads_out, const dm
     a.out_ttft = out->ttft_to_us;
     a.out_count = out->count;
     a.status = c->d_status;
-    commit_kernel<<<1, kCommitThreads, 0, st>>>(a);
+    if (nsrc_h <= kSpreadSources) {
+        // few sources: each source's phases as kernels over the whole GPU
+        zero_u32_kernel<<<1, 64, 0, st>>>(reinterpret_cast<uint32_t*>(run), 2);
+        zero_u32_kernel<<<grid_for(Ca / 32 + 1, 256, 1024), 256, 0, st>>>(gbits,
+                                                                       (uint32_t)(Ca / 32 + 1));
+        const uint32_t gw = (uint32_t)std::min<uint64_t>((S + 3) / 4, 1024);
+        const uint32_t gm = grid_for(C, 256, 512);
+        for (uint32_t sr = 0; sr < nsrc_h; sr++) {
+            src_walk_kernel<<<gw, 256, 0, st>>>(a, sr);
+            src_rank_kernel<<<1, kCommitThreads, 0, st>>>(a, sr);
+            src_mark_kernel<<<gm, 256, 0, st>>>(a, sr);
+            src_stop_kernel<<<1, kCommitThreads, 0, st>>>(a, sr);
+            src_commit_kernel<<<gw, 256, 0, st>>>(a, sr);
+        }
+        src_finish_kernel<<<1, 1, 0, st>>>(a);
+    } else {
+        commit_kernel<<<1, kCommitThreads, 0, st>>>(a);
+    }
     if (C)
         emit_kernel<<<grid_for(C, 256), 256, 0, st>>>(
             C, start, nsrc, src, arank, kstar_of, base_of, c_rec, c_alt, c_ben, tto, cap,

@@ -801,6 +801,27 @@ def test_rebalance_long_queues_many_targets_parity():
     assert len(np.unique(r["dst"])) > 512
 
 
+def test_rebalance_many_sources_parity():
+    """80 overloaded sources of 200 live instances: more sources than the
+    pass spreads one source at a time over the GPU (64), so one workgroup
+    commits them all; with 40 sources, the spread form.  Both against the
+    oracle."""
+    gh = _h()
+    S, n_live = 256, 200
+    cfg = dict(block=16, key_blocks=4, seeds=(1, 2), vnodes=4, max_slots=S, index_log2_slots=8,
+               slo_us=200_000)
+    eng = gh.DualMap(cfg, device="cuda:0")
+    o = oracle.Oracle(cfg)
+    rng = np.random.default_rng(90)
+    for n_src in (80, 40):
+        src = np.sort(rng.choice(n_live, size=n_src, replace=False))
+        q = workloads.synthetic_queues(91 + n_src, S, n_live, src, 600, 300, 100_000,
+                                       4 * (cfg["slo_us"] - 5_000))
+        _say("rebalance sources", n_src, "records", len(q.rec_id))
+        r = compare_rebalance(eng, o, q)
+        assert len(np.unique(r["src"])) > n_src // 2
+
+
 def test_rebalance_candidates_past_lds_parity():
     """One source with 300,000 queued records, nearly all eligible: more
     candidates than the commit kernel keeps acceptance bits for in LDS

@@ -81,6 +81,7 @@ def lib():
             "or_select": (u32, [P, u32, u32, u64, u64, i64, P, P, P]),
             "or_route": (i32, [P, P, P, u64, P, P, P, P, P, P, P, P, P]),
             "or_set_policy": (i32, [P, i32]),
+            "or_kv_save": (i32, [P, P, u64, P, P, u64, u64, P, P]),
             "or_keylen_enable": (i32, [P, u64]),
             "or_keylen_window": (i32, [P]),
             "or_keylen_export": (i32, [P, P, u64, P]),
@@ -171,6 +172,17 @@ class Oracle:
         """Selection rule for later routes: a name of POLICIES or its number."""
         p = self.POLICIES.get(policy, policy) if isinstance(policy, str) else int(policy)
         return lib().or_set_policy(self._h, p)
+
+    def kv_save(self, offsets, block_keys, inst, clock: int, cap: int):
+        """Save the batch's blocks on the serving instances with LRU eviction
+        (or_kv_save); returns (status, keys added, keys removed)."""
+        o = np.ascontiguousarray(offsets, np.int64)
+        bk = np.ascontiguousarray(block_keys, np.uint64)
+        ins = np.ascontiguousarray(inst, np.uint32)
+        a, r = C.c_uint64(), C.c_uint64()
+        rc = lib().or_kv_save(self._h, _p(o), len(o) - 1, _p(bk), _p(ins), int(clock), int(cap),
+                              C.byref(a), C.byref(r))
+        return rc, int(a.value), int(r.value)
 
     def keylen_enable(self, max_nodes: int) -> int:
         """Adaptive hash-key length: an empty prefix hotness tree with room for

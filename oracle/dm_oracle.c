@@ -53,6 +53,10 @@ typedef struct {
     uint64_t **set;           /* per instance: sorted unique cached block keys  */
     uint64_t *set_len;
     int policy;               /* selection rule, OR_POLICY_* (default SLO-aware)*/
+    /* KV save with LRU eviction: per instance, the keys saved through
+     * or_kv_save and the time of their latest touch, sorted by key       */
+    uint64_t **lru_key, **lru_t;
+    uint64_t *lru_len;
     /* adaptive hash-key length (Sec. 3.2): the prefix hotness tree      */
     int kl_on;
     uint64_t kl_max;          /* most extended prefixes the tree may hold       */
@@ -266,11 +270,15 @@ or_state *or_create(const or_config *cfg)
     st->live = (uint8_t *)calloc(cfg->max_slots, 1);
     st->set = (uint64_t **)calloc(cfg->max_slots, sizeof(uint64_t *));
     st->set_len = (uint64_t *)calloc(cfg->max_slots, sizeof(uint64_t));
-    if (!st->live || !st->set || !st->set_len)
+    st->lru_key = (uint64_t **)calloc(cfg->max_slots, sizeof(uint64_t *));
+    st->lru_t = (uint64_t **)calloc(cfg->max_slots, sizeof(uint64_t *));
+    st->lru_len = (uint64_t *)calloc(cfg->max_slots, sizeof(uint64_t));
+    if (!st->live || !st->set || !st->set_len || !st->lru_key || !st->lru_t || !st->lru_len)
         goto fail;
     return st;
 fail:
     free(st->kk[0]); free(st->kk[1]); free(st->live); free(st->set); free(st->set_len);
+    free(st->lru_key); free(st->lru_t); free(st->lru_len);
     free(st);
     return NULL;
 }
@@ -281,9 +289,13 @@ void or_destroy(or_state *st)
         return;
     free(st->kl_ext);
     free(st->kl_log);
-    for (uint32_t i = 0; i < st->cfg.max_slots; i++)
+    for (uint32_t i = 0; i < st->cfg.max_slots; i++) {
         free(st->set[i]);
+        free(st->lru_key[i]);
+        free(st->lru_t[i]);
+    }
     free(st->set); free(st->set_len); free(st->live);
+    free(st->lru_key); free(st->lru_t); free(st->lru_len);
     free(st->ring[0]); free(st->ring[1]);
     free(st->kk[0]); free(st->kk[1]);
     free(st);
@@ -448,6 +460,149 @@ int or_index_clear(or_state *st, uint32_t id)
 uint64_t or_index_size(const or_state *st, uint32_t id)
 {
     return (st && id < st->cfg.max_slots) ? st->set_len[id] : 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* KV save with least-recently-used eviction: the step after routing.  A     */
+/* served request's KV blocks are saved on its instance (the KV query and   */
+/* save of Sec. A.3.2), and each instance's cache is bounded.               */
+/* ------------------------------------------------------------------------- */
+
+typedef struct {
+    uint64_t key, t;
+} or_kt;
+
+static int cmp_kt_key(const void *pa, const void *pb)
+{
+    const or_kt *a = (const or_kt *)pa, *b = (const or_kt *)pb;
+    if (a->key != b->key)
+        return a->key < b->key ? -1 : 1;
+    return a->t > b->t ? -1 : (a->t < b->t ? 1 : 0); /* latest touch first */
+}
+
+static int cmp_kt_time_desc(const void *pa, const void *pb)
+{
+    const or_kt *a = (const or_kt *)pa, *b = (const or_kt *)pb;
+    return a->t > b->t ? -1 : (a->t < b->t ? 1 : 0);
+}
+
+/* Save the batch's blocks: request r (full blocks block_keys[start_r ..
+ * start_r + nfull_r), request-major, start_r = full blocks of the requests
+ * before it) is served by inst[r].  Every block is touched on that
+ * instance, deepest block first, at time clock + start_r + (nfull_r - 1 - b)
+ * for block b, so a prefix's blocks are always more recent than its
+ * descendants.  Each instance's cache becomes the cap most recently touched
+ * distinct keys (cap = 0: unbounded) among what it held and what it was
+ * sent; keys that leave are erased from its index and keys that join are
+ * inserted.  *added and *removed (optional) count them over all instances.
+ * The caller's clock should advance by the batch's full blocks. */
+int or_kv_save(or_state *st, const int64_t *off, uint64_t n, const uint64_t *block_keys,
+               const uint32_t *inst, uint64_t clock, uint64_t cap, uint64_t *added,
+               uint64_t *removed)
+{
+    if (!st || (n && (!off || !inst)))
+        return OR_EINVAL;
+    const uint32_t S = st->cfg.max_slots, B = st->cfg.block_size;
+    uint64_t total = 0;
+    for (uint64_t r = 0; r < n; r++) {
+        if (off[r + 1] < off[r] || inst[r] >= S)
+            return OR_EINVAL;
+        total += (uint64_t)(off[r + 1] - off[r]) / B;
+    }
+    if (total && !block_keys)
+        return OR_EINVAL;
+    /* every block's (instance, key, time), grouped by instance */
+    uint64_t *cnt = (uint64_t *)calloc(S + 1, sizeof(uint64_t));
+    or_kt *ent = (or_kt *)malloc((total ? total : 1) * sizeof(or_kt));
+    if (!cnt || !ent) {
+        free(cnt); free(ent);
+        return OR_ENOMEM;
+    }
+    for (uint64_t r = 0; r < n; r++)
+        cnt[inst[r] + 1] += (uint64_t)(off[r + 1] - off[r]) / B;
+    for (uint32_t c = 0; c < S; c++)
+        cnt[c + 1] += cnt[c];
+    uint64_t start = 0;
+    for (uint64_t r = 0; r < n; r++) {
+        const uint64_t nf = (uint64_t)(off[r + 1] - off[r]) / B;
+        for (uint64_t b = 0; b < nf; b++) {
+            or_kt *e = &ent[cnt[inst[r]]++];
+            e->key = block_keys[start + b];
+            e->t = clock + start + (nf - 1 - b);
+        }
+        start += nf;
+    }
+    /* cnt[c] is now the end of instance c's entries; its start is cnt[c-1] */
+    uint64_t n_add = 0, n_rm = 0;
+    int rc = OR_OK;
+    for (uint32_t c = 0; c < S && rc == OR_OK; c++) {
+        const uint64_t lo = c ? cnt[c - 1] : 0, hi = cnt[c];
+        if (lo == hi)
+            continue;
+        const uint64_t old = st->lru_len[c], m = old + (hi - lo);
+        or_kt *a = (or_kt *)malloc(m * sizeof(or_kt));
+        uint64_t *gone = (uint64_t *)malloc((old ? old : 1) * sizeof(uint64_t));
+        uint64_t *join = (uint64_t *)malloc(m * sizeof(uint64_t));
+        if (!a || !gone || !join) {
+            free(a); free(gone); free(join);
+            rc = OR_ENOMEM;
+            break;
+        }
+        for (uint64_t k = 0; k < old; k++) {
+            a[k].key = st->lru_key[c][k];
+            a[k].t = st->lru_t[c][k];
+        }
+        memcpy(a + old, ent + lo, (hi - lo) * sizeof(or_kt));
+        /* latest touch per key */
+        qsort(a, m, sizeof(or_kt), cmp_kt_key);
+        uint64_t u = 0;
+        for (uint64_t k = 0; k < m; k++)
+            if (u == 0 || a[k].key != a[u - 1].key)
+                a[u++] = a[k];
+        /* the cap most recent keys stay */
+        if (cap && u > cap) {
+            qsort(a, u, sizeof(or_kt), cmp_kt_time_desc);
+            u = cap;
+            qsort(a, u, sizeof(or_kt), cmp_kt_key);
+        }
+        /* keys that left and keys that joined (both lists sorted by key) */
+        uint64_t ng = 0, nj = 0, i = 0, j = 0;
+        while (i < old || j < u) {
+            if (j == u || (i < old && st->lru_key[c][i] < a[j].key))
+                gone[ng++] = st->lru_key[c][i++];
+            else if (i == old || a[j].key < st->lru_key[c][i])
+                join[nj++] = a[j++].key;
+            else {
+                i++;
+                j++;
+            }
+        }
+        if (or_index_erase(st, c, gone, ng) != OR_OK || or_index_insert(st, c, join, nj) != OR_OK)
+            rc = OR_ENOMEM;
+        uint64_t *nk = (uint64_t *)realloc(st->lru_key[c], (u ? u : 1) * sizeof(uint64_t));
+        uint64_t *nt = nk ? (uint64_t *)realloc(st->lru_t[c], (u ? u : 1) * sizeof(uint64_t)) : NULL;
+        if (!nk || !nt) {
+            if (nk) st->lru_key[c] = nk;
+            free(a); free(gone); free(join);
+            rc = OR_ENOMEM;
+            break;
+        }
+        for (uint64_t k = 0; k < u; k++) {
+            nk[k] = a[k].key;
+            nt[k] = a[k].t;
+        }
+        st->lru_key[c] = nk;
+        st->lru_t[c] = nt;
+        st->lru_len[c] = u;
+        n_add += nj;
+        n_rm += ng;
+        free(a); free(gone); free(join);
+    }
+    free(cnt);
+    free(ent);
+    if (added) *added = n_add;
+    if (removed) *removed = n_rm;
+    return rc;
 }
 
 /* ------------------------------------------------------------------------- */

@@ -1031,3 +1031,91 @@ def test_keylen_capacity_and_state_errors():
     o.route(tok, off, np.zeros(n_live, np.int64))
     assert o.keylen_window() == oracle.OK
     assert o.keylen_tree().tolist() == sorted([_node_key(o, A), _node_key(o, C)])
+
+
+# ---------------------------------------------------------------------------
+# KV save with LRU eviction (the serving step after routing, Sec. A.3.2)
+# ---------------------------------------------------------------------------
+
+def _kv_case(o, B, chains, inst, clock, cap):
+    toks, off = [], [0]
+    keys = []
+    for ch in chains:
+        toks.append(np.asarray(ch, np.int32))
+        off.append(off[-1] + len(ch))
+        keys.append(o.chain(0, np.asarray(ch, np.int32)))
+    bk = np.concatenate(keys) if keys else np.zeros(0, np.uint64)
+    return o.kv_save(np.array(off, np.int64), bk, np.array(inst, np.uint32), clock, cap), bk
+
+
+def test_kv_save_hand_values():
+    """cap 3 on instance 0.  Request A = blocks (a0, a1, a2) touches a2, a1,
+    a0 at times 0, 1, 2 (deepest first); request B = (a0, b1) touches b1 at
+    3 and a0 at 4.  Four distinct keys: the least recent, a2, is dropped in
+    the same call, so a0, a1, b1 join the index and nothing leaves; the
+    cache stays prefix-closed."""
+    import sys
+    sys.path.insert(0, os.path.dirname(__file__))
+    B = 4
+    o = oracle.Oracle(dict(block=B, key_blocks=1, seeds=(1, 2), vnodes=4, max_slots=2))
+    rng = np.random.default_rng(11)
+    a = [int(x) for x in rng.integers(0, 1000, size=3 * B)]
+    b = a[:B] + [int(x) for x in rng.integers(1000, 2000, size=B)]
+    (rc, added, removed), bk = _kv_case(o, B, [a, b], [0, 0], 0, 3)
+    assert rc == oracle.OK and (added, removed) == (3, 0)
+    ka, kb = o.chain(0, np.array(a, np.int32)), o.chain(0, np.array(b, np.int32))
+    assert o.index_size(0) == 3 and o.index_size(1) == 0
+    for k, present in ((ka[0], True), (ka[1], True), (ka[2], False), (kb[1], True)):
+        assert bool(o.index_contains(0, int(k))) == present
+    # a later batch touching only a2 (its own chain a0, a1, a2 again) at
+    # clock 5: times a2 5, a1 6, a0 7; b1 (time 3) is now the least recent
+    (rc, added, removed), _ = _kv_case(o, B, [a], [0], 5, 3)
+    assert (added, removed) == (1, 1)
+    assert not o.index_contains(0, int(kb[1])) and o.index_contains(0, int(ka[2]))
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_kv_save_matches_lru_model(seed):
+    """Batches of template-sharing prompts over 4 instances against the LRU
+    model of the multi-batch driver (tests/sim.py, written independently):
+    after every batch each instance's index holds exactly the model's keys,
+    and the added and removed counts agree."""
+    import sys
+    sys.path.insert(0, os.path.dirname(__file__))
+    import sim
+    B, S = 4, 4
+    o = oracle.Oracle(dict(block=B, key_blocks=1, seeds=(1, 2), vnodes=4, max_slots=S))
+    lru = sim.LRUIndex(S, cap=40 + 10 * seed)
+    rng = np.random.default_rng(200 + seed)
+    tpl = [list(rng.integers(0, 100, size=B * int(rng.integers(2, 9)))) for _ in range(5)]
+    clock = 0
+    for _ in range(6):
+        chains, inst = [], []
+        for _ in range(int(rng.integers(5, 40))):
+            t = tpl[int(rng.integers(0, 5))]
+            cut = int(rng.integers(0, len(t) + 1))
+            chains.append([int(x) for x in t[:cut]] +
+                          [int(x) for x in rng.integers(0, 100, size=int(rng.integers(0, 3 * B)))])
+            inst.append(int(rng.integers(0, S)))
+        (rc, added, removed), bk = _kv_case(o, B, chains, inst, clock, lru.cap)
+        assert rc == oracle.OK
+        nfull = np.array([len(c) // B for c in chains])
+        upd = lru.touch(np.array(inst), bk, nfull)
+        clock += int(nfull.sum())
+        assert added == sum(len(a) for a, _ in upd.values())
+        assert removed == sum(len(r) for _, r in upd.values())
+        for c in range(S):
+            assert o.index_size(c) == len(lru.keys[c])
+            assert all(o.index_contains(c, int(k)) for k in lru.keys[c])
+
+
+def test_kv_save_unbounded_and_errors():
+    B = 4
+    o = oracle.Oracle(dict(block=B, key_blocks=1, seeds=(1, 2), vnodes=4, max_slots=2))
+    rng = np.random.default_rng(12)
+    chains = [[int(x) for x in rng.integers(0, 50, size=B * 3)] for _ in range(4)]
+    (rc, added, removed), bk = _kv_case(o, B, chains, [1, 1, 1, 1], 0, 0)
+    assert rc == oracle.OK and removed == 0 and added == len(np.unique(bk))
+    assert o.index_size(1) == len(np.unique(bk))
+    (rc, _, _), _ = _kv_case(o, B, chains[:1], [2], 0, 0)
+    assert rc == oracle.EINVAL

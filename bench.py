@@ -278,6 +278,26 @@ def config_rows(reps):
                                 "parity": bool(rsame),
                                 "note": "host clock per call; queues of the routed batch, "
                                         "four seed-chosen instances stalled to 5x the mean work"}
+            # KV save of the routed batch on the chosen instances, LRU-bounded
+            nb = int((np.diff(g["offsets_np"]) // rc.block).sum())
+            ob = eng.alloc_route_out(n, nb)
+            L = gh.to_dev(g["loads0"], eng.device)
+            eng.route_into(g["tokens"], g["offsets"], L, ob)
+            eng.sync()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            ga = eng.kv_save(g["offsets"], ob["block_keys"], ob["chosen"], 0, cfg.lru_blocks)
+            kv_ms = 1000.0 * (time.perf_counter() - t0)
+            bk = ob["block_keys"].cpu().numpy()[:nb]
+            t0 = time.perf_counter()
+            orc, oa, orm = o["oracle"].kv_save(o["offsets"], bk, ob["chosen"].cpu().numpy(), 0,
+                                                cfg.lru_blocks)
+            kv_ort = time.perf_counter() - t0
+            row["kv_save"] = {"blocks": nb, "added": ga[0], "removed": ga[1],
+                              "gpu_ms": kv_ms, "oracle_ms": 1000.0 * kv_ort,
+                              "parity": bool(orc == 0 and (oa, orm) == ga),
+                              "note": "host clock of one dm_kv_save of the routed batch on the "
+                                      "chosen instances, LRU bound 200,000 blocks per instance"}
         rows[name] = row
         del eng, g, o, out
         torch.cuda.empty_cache()

@@ -99,8 +99,32 @@ dm_status dm_index_insert(dm_ctx* ctx, uint32_t id, const uint64_t* keys, uint64
  * ignored.  Erased slots stay occupied until dm_index_clear. */
 dm_status dm_index_erase(dm_ctx* ctx, uint32_t id, const uint64_t* keys, uint64_t n);
 
-/* Empty instance id's index. */
+/* Empty instance id's index (and drop its keys from dm_kv_save's record). */
 dm_status dm_index_clear(dm_ctx* ctx, uint32_t id);
+
+/* KV save with least-recently-used eviction: the serving step after routing
+ * (the KV query and save of Sec. A.3.2), on the device.  Request r of a
+ * served batch (offsets: device int64 [n + 1], non-decreasing, the batch's
+ * prompts as in dm_route_batch; block_keys: device u64, every full block's
+ * f1 key request-major, e.g. dm_route_out.block_keys) is served by inst[r]
+ * (device u32 [n], e.g. dm_route_out.chosen after any migrations).  Every
+ * block is touched on that instance, deepest block first, at time
+ * clock + start_r + (nfull_r - 1 - b) for block b (start_r: full blocks of
+ * the requests before r), so a prefix's blocks are always more recent than
+ * its descendants and caches stay prefix-closed.  Each instance's cache
+ * becomes the cap most recently touched distinct keys (cap = 0: unbounded;
+ * cap <= 2^(k-1)) among those saved before and those sent now; keys that
+ * leave are erased from its index and keys that join are inserted.  The
+ * counts go to *added_host / *removed_host (host, optional).  The caller
+ * advances its clock by the batch's full blocks; times must stay below
+ * 2^40.  The record of saved keys is the library's: keys inserted with
+ * dm_index_insert are not in it, and erasing saved keys with
+ * dm_index_erase leaves them recorded.  Synchronises.  DM_EINVAL (nothing
+ * changed) for offsets that decrease or are negative, or an instance id >=
+ * max_slots, both checked on the device before any other work. */
+dm_status dm_kv_save(dm_ctx* ctx, const int64_t* offsets, uint64_t n, const uint64_t* block_keys,
+                     const uint32_t* inst, uint64_t clock, uint64_t cap, uint64_t* added_host,
+                     uint64_t* removed_host);
 
 /* Number of keys held by instance id's index (host out).  Synchronises. */
 dm_status dm_index_size(dm_ctx* ctx, uint32_t id, uint64_t* n_host);

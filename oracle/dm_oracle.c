@@ -454,6 +454,9 @@ int or_index_clear(or_state *st, uint32_t id)
     free(st->set[id]);
     st->set[id] = NULL;
     st->set_len[id] = 0;
+    free(st->lru_key[id]); st->lru_key[id] = NULL;
+    free(st->lru_t[id]); st->lru_t[id] = NULL;
+    st->lru_len[id] = 0;
     return OR_OK;
 }
 
@@ -1213,13 +1216,13 @@ int or_scale(or_state *st, const uint32_t *add, uint32_t n_add, const uint32_t *
     for (uint64_t k = 0; k < 2 * n; k++)
         old_owner[k] = ring_owner(st, (int)(k / (n ? n : 1)), keys[k]);
     for (uint32_t id = 0; id < S; id++) {
-        if (is_rm[id]) {
-            st->live[id] = 0;
+        if (is_rm[id] || is_add[id]) {
+            st->live[id] = is_add[id] ? 1 : 0;
             free(st->set[id]); st->set[id] = NULL; st->set_len[id] = 0;
-        }
-        if (is_add[id]) {
-            st->live[id] = 1;
-            free(st->set[id]); st->set[id] = NULL; st->set_len[id] = 0;
+            /* the saved-key record of an emptied cache goes with it */
+            free(st->lru_key[id]); st->lru_key[id] = NULL;
+            free(st->lru_t[id]); st->lru_t[id] = NULL;
+            st->lru_len[id] = 0;
         }
     }
     st->n_live = st->n_live - n_rm + n_add;

@@ -27,7 +27,8 @@ EXPORTS = ("dm_create", "dm_destroy", "dm_build_rings", "dm_ring_export", "dm_in
            "dm_index_erase", "dm_index_clear", "dm_index_size", "dm_route_batch",
            "dm_route_batch_noalloc",
            "dm_rebalance", "dm_scale", "dm_set_timing", "dm_route_stage_ms",
-           "dm_set_pipelining", "dm_set_policy", "dm_keylen_enable", "dm_keylen_window",
+           "dm_kv_save", "dm_set_pipelining", "dm_set_policy", "dm_keylen_enable",
+           "dm_keylen_window",
            "dm_keylen_export", "dm_sync", "dm_last_error")
 
 
@@ -91,6 +92,7 @@ def load_library(path: str = LIB_PATH):
         "dm_route_stage_ms": (i32, [P, P, i32]),
         "dm_set_pipelining": (i32, [P, i32]),
         "dm_set_policy": (i32, [P, i32]),
+        "dm_kv_save": (i32, [P, P, u64, P, P, u64, u64, P, P]),
         "dm_keylen_enable": (i32, [P, u64, u64]),
         "dm_keylen_window": (i32, [P]),
         "dm_keylen_export": (i32, [P, P, u64, P]),
@@ -263,6 +265,19 @@ class DualMap:
         if key_len:
             out["key_len"] = self._empty(max(n, 1), t.uint32)
         return out
+
+    def kv_save(self, offsets, block_keys, inst, clock: int, cap: int):
+        """Save a served batch's blocks with LRU eviction (see dm_kv_save);
+        returns (keys added, keys removed)."""
+        t = self.torch
+        offsets = self._dev(offsets, t.int64, "offsets")
+        block_keys = self._dev(block_keys, t.uint64, "block_keys")
+        inst = self._dev(inst, t.uint32, "inst")
+        a, r = C.c_uint64(), C.c_uint64()
+        self._check(self.lib.dm_kv_save(self._h, _ptr(offsets), offsets.numel() - 1,
+                                        _ptr(block_keys), _ptr(inst), int(clock), int(cap),
+                                        C.byref(a), C.byref(r)), "dm_kv_save")
+        return int(a.value), int(r.value)
 
     def keylen_enable(self, max_nodes: int, max_window_blocks: int = 1 << 24) -> None:
         """Adaptive hash-key length (see dm_keylen_enable): an empty prefix

@@ -280,6 +280,7 @@ void dm_destroy(dm_ctx* c)
     for (auto& s : c->scratch)
         (void)hipFree(s.p);
     keylen_free(c);
+    kv_free(c);
     for (auto& ev : c->tev)
         if (ev)
             (void)hipEventDestroy(ev);
@@ -392,7 +393,35 @@ dm_status dm_index_clear(dm_ctx* c, uint32_t id)
     if (hipError_t je = join_selection(c); je != hipSuccess)
         return hip_fail(c, je, "dm_index_clear");
     hipError_t e = index_clear(c, id);
+    if (e == hipSuccess && c->kv.n) {
+        // the saved-key record of the emptied cache goes with it
+        std::vector<uint8_t> gone(c->cfg.max_slots, 0);
+        gone[id] = 1;
+        if ((e = hipMemcpy(c->d_flag_add, gone.data(), gone.size(), hipMemcpyHostToDevice)) ==
+            hipSuccess)
+            e = kv_forget(c, c->d_flag_add);
+    }
     return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_index_clear");
+}
+
+dm_status dm_kv_save(dm_ctx* c, const int64_t* offsets, uint64_t n, const uint64_t* block_keys,
+                     const uint32_t* inst, uint64_t clock, uint64_t cap, uint64_t* added_host,
+                     uint64_t* removed_host)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (c->n_live == 0)
+        return fail(c, DM_ESTATE, "dm_kv_save: rings not built");
+    if (n && (!offsets || !inst))
+        return fail(c, DM_EINVAL, "dm_kv_save: null argument");
+    if (!aligned(offsets) || !aligned(block_keys) || !aligned(inst))
+        return fail(c, DM_EINVAL, "dm_kv_save: misaligned pointer");
+    if (cap > (1ull << (c->cfg.index_log2_slots - 1)))
+        return fail(c, DM_EINVAL, "dm_kv_save: cap past the index's load limit");
+    if (n >= (1ull << 32))
+        return fail(c, DM_EINVAL, "dm_kv_save: batch too large");
+    DeviceGuard g(c->device);
+    return kv_save(c, offsets, n, block_keys, inst, clock, cap, added_host, removed_host);
 }
 
 dm_status dm_index_size(dm_ctx* c, uint32_t id, uint64_t* n_host)
@@ -514,6 +543,15 @@ dm_status dm_scale(dm_ctx* c, const uint32_t* add, uint32_t n_add, const uint32_
             if (fa[i] || fr[i])
                 changed.push_back(i);
         e = index_clear_many(c, changed.data(), (uint32_t)changed.size());
+        if (e == hipSuccess && c->kv.n) {
+            // the saved-key record of the emptied caches goes with them
+            std::vector<uint8_t> gone(S, 0);
+            for (uint32_t i : changed)
+                gone[i] = 1;
+            if ((e = hipMemcpy(c->d_flag_add, gone.data(), S, hipMemcpyHostToDevice)) ==
+                hipSuccess)
+                e = kv_forget(c, c->d_flag_add);
+        }
     }
     if (e != hipSuccess) {
         c->live = old_live;

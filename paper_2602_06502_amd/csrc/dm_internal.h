@@ -102,6 +102,15 @@ struct KeyLen {
     uint64_t win = 0;             // requests routed in the current window
 };
 
+// Record of the keys saved through dm_kv_save: (instance, key, time of the
+// latest touch) per entry, one flat array.
+struct KvRecord {
+    uint64_t* key = nullptr;
+    uint64_t* t = nullptr;
+    uint32_t* inst = nullptr;
+    uint64_t n = 0, cap = 0;
+};
+
 }  // namespace dm
 
 struct dm_ctx {
@@ -156,6 +165,7 @@ struct dm_ctx {
     bool pipelined = false;
     uint32_t policy = DM_POLICY_SLO_AWARE;  // selection rule of later batches
     dm::KeyLen kl;                          // adaptive hash-key length
+    dm::KvRecord kv;                        // keys saved through dm_kv_save
     hipStream_t work_stream = nullptr, sel_stream = nullptr, out_stream = nullptr;
     hipEvent_t in_ready = nullptr;                 // caller's stream: inputs of the batch
     hipEvent_t prep_done = nullptr;                // work stream: records packed
@@ -293,6 +303,15 @@ uint64_t keylen_record_bytes(uint64_t n);
 dm_status keylen_window(dm_ctx* c);
 dm_status keylen_export(dm_ctx* c, uint64_t* keys_host, uint64_t cap, uint64_t* n_host);
 void keylen_free(dm_ctx* c);
+
+// dm_kv.hip: KV save with LRU eviction (host entry point; synchronises),
+// the record's entries of emptied instances dropped (d_gone: device u8 flags
+// per instance slot), and the record's release.
+dm_status kv_save(dm_ctx* c, const int64_t* offsets, uint64_t n, const uint64_t* block_keys,
+                  const uint32_t* inst, uint64_t clock, uint64_t cap, uint64_t* added,
+                  uint64_t* removed);
+hipError_t kv_forget(dm_ctx* c, const uint8_t* d_gone);
+void kv_free(dm_ctx* c);
 
 // dm_probe.hip: candidates on the current rings (cand, fix-up flag bit 3),
 // then requests ordered by their first ring key and grouped (gv).

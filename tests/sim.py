@@ -166,6 +166,12 @@ def _cached(key, make):
 
 
 def _apply_lru(side, lru: LRUIndex, inst: np.ndarray, out, off: np.ndarray, block: int) -> None:
+    if getattr(side, "kv_on_side", False):
+        # the side saves the batch itself (dm_kv_save / or_kv_save); the
+        # clock advances as the model's would
+        side.kv_save(off, out, inst, lru.clock, lru.cap)
+        lru.clock += int((np.maximum(np.diff(off), 0) // block).sum())
+        return
     upd = lru.touch(inst, out["block_keys"], np.maximum(np.diff(off), 0) // block)
     for c, (added, removed) in sorted(upd.items()):
         if len(removed):

@@ -17,6 +17,7 @@ work (a load the router did not see, as with a decode-bound instance); once
 with a fixed key length and once with the prefix hotness tree (every batch
 one window), where at least 10% of the queued records migrate.
 """
+import itertools
 import sys
 
 import numpy as np
@@ -38,12 +39,19 @@ def _say(*a):
 
 
 class OracleSide:
-    def __init__(self, rc, keylen_nodes=0):
+    def __init__(self, rc, keylen_nodes=0, kv_on_side=False):
         self.o = oracle.Oracle(rc.as_dict())
         assert self.o.build_rings(range(rc.n_inst)) == 0
         self.keylen = keylen_nodes > 0
         if self.keylen:
             assert self.o.keylen_enable(keylen_nodes) == oracle.OK
+        self.kv_on_side = kv_on_side
+        self.kv_counts = []
+
+    def kv_save(self, off, out, inst, clock, cap):
+        rc, a, r = self.o.kv_save(off, out["block_keys"], inst, clock, cap)
+        assert rc == oracle.OK
+        self.kv_counts.append((a, r))
 
     def window(self):
         assert self.o.keylen_window() == oracle.OK
@@ -67,7 +75,7 @@ class OracleSide:
 
 
 class EngineSide:
-    def __init__(self, rc, keylen_nodes=0):
+    def __init__(self, rc, keylen_nodes=0, kv_on_side=False):
         import paper_2602_06502_amd.harness as gh
         self.gh = gh
         self.eng = gh.DualMap(rc.as_dict(), device="cuda:0")
@@ -75,6 +83,16 @@ class EngineSide:
         self.keylen = keylen_nodes > 0
         if self.keylen:
             self.eng.keylen_enable(keylen_nodes, 1 << 24)
+        self.kv_on_side = kv_on_side
+        self.kv_counts = []
+        self._dev_out = None
+
+    def kv_save(self, off, out, inst, clock, cap):
+        # the block keys the last route left on the device; the offsets and
+        # serving instances are the batch's
+        bk = self._dev_out["block_keys"] if self._dev_out is not None else self._d(out["block_keys"])
+        self.kv_counts.append(self.eng.kv_save(self._d(np.asarray(off, np.int64)), bk,
+                                               self._d(np.asarray(inst, np.uint32)), clock, cap))
 
     def window(self):
         self.eng.keylen_window()
@@ -91,6 +109,7 @@ class EngineSide:
         self.eng.sync()
         res = {k: v.cpu().numpy() for k, v in out.items()}
         res["loads"] = L.cpu().numpy()
+        self._dev_out = out if self.kv_on_side else None
         return res
 
     def insert(self, c, keys):
@@ -192,3 +211,44 @@ def test_agent_multibatch_adaptive_keylen_parity():
     # the configuration is calibrated for this: at least 10% of queued
     # records migrate over the 16 passes
     assert migrated >= 0.10 * queued, (migrated, queued)
+
+
+def test_chat_multibatch_device_kv_save_parity():
+    """The chat workload with the caches kept by the sides themselves: after
+    every routed batch each side saves the batch's blocks on the chosen
+    instances with LRU eviction (dm_kv_save on the device from the route's
+    own block keys; or_kv_save in the oracle), and every later batch's
+    routing, which reads those caches, is compared."""
+    _gpu()
+    cfg = workloads.chat()
+    rc = cfg.route
+    gs, os_ = EngineSide(rc, kv_on_side=True), OracleSide(rc, kv_on_side=True)
+    # both drivers run to their end (each saves after its last batch)
+    for x, y in itertools.zip_longest(sim.run_chat(gs, cfg, 16), sim.run_chat(os_, cfg, 16)):
+        (st, b, g), (st2, b2, o) = x, y
+        assert (st, b) == (st2, b2)
+        _say("chat (device KV save)", st, b, "requests", len(o["chosen"]))
+        _compare(st, b, g, o)
+    assert gs.kv_counts == os_.kv_counts
+    _say("chat saves: added", sum(a for a, _ in os_.kv_counts), "evicted",
+         sum(r for _, r in os_.kv_counts))
+    for c in range(rc.n_inst):
+        assert gs.eng.index_size(c) == os_.o.index_size(c)
+
+
+def test_agent_multibatch_device_kv_save_parity():
+    """The agent workload (fixed key length) with device KV save: each batch's
+    blocks saved on the instance that serves each request after the
+    rebalancing pass."""
+    _gpu()
+    cfg = workloads.agent()
+    rc = cfg.route
+    gs, os_ = EngineSide(rc, kv_on_side=True), OracleSide(rc, kv_on_side=True)
+    for x, y in itertools.zip_longest(sim.run_agent(gs, cfg, cfg.mu, 6),
+                                      sim.run_agent(os_, cfg, cfg.mu, 6)):
+        (st, b, g), (st2, b2, o) = x, y
+        assert (st, b) == (st2, b2)
+        _compare(st, b, g, o)
+    assert gs.kv_counts == os_.kv_counts
+    # the caches fill past their 200,000 blocks: saves evict
+    assert sum(r for _, r in os_.kv_counts) > 0

@@ -336,6 +336,54 @@ def test_keylen_window_spans_batches_and_errors():
         eng.keylen_tree()
 
 
+# ---------------------------------------------------------------------------
+# KV save with LRU eviction
+# ---------------------------------------------------------------------------
+
+def test_kv_save_parity_and_errors():
+    """Batches over hot templates routed, then saved on the chosen
+    instances with a small cap (evictions every batch), each side on its
+    own state: added and removed counts, index sizes and the next batch's
+    routing (which reads the caches) against the oracle; then bad inputs."""
+    gh = _h()
+    import paper_2602_06502_amd as pk
+    B, K = 16, 2
+    wl = workloads.small_random(95, 8, 8, B, 64, slo_us=30_000, key_blocks=K)
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    L = workloads.initial_loads(wl, wl.route.max_slots)
+    clock, cap = 0, 300
+    for i, (tok, off) in enumerate(_hot_batches(96, B, K, 8, tlen_blocks=(1, 30))):
+        _say("kv save batch", i, "requests", len(off) - 1)
+        Ld = gh.to_dev(L, eng.device)
+        g = eng.route(gh.to_dev(tok, eng.device), gh.to_dev(off, eng.device), Ld, block_keys=True)
+        eng.sync()
+        r = o.route(tok, off, L, block_keys=True)
+        compare_route(g, r, len(off) - 1, with_bk=True)
+        L = r["loads"]
+        ga = eng.kv_save(gh.to_dev(off, eng.device), g["block_keys"], g["chosen"], clock, cap)
+        rc, a, rm = o.kv_save(off, r["block_keys"], r["chosen"], clock, cap)
+        assert rc == oracle.OK and ga == (a, rm), (ga, a, rm)
+        clock += int((np.diff(off) // B).sum())
+        for c in range(wl.route.n_inst):
+            assert eng.index_size(c) == o.index_size(c) <= cap
+    assert rm > 0
+    tok, off = _hot_batches(96, B, K, 1)[0]
+    bad_inst = gh.to_dev(np.full(len(off) - 1, wl.route.max_slots, np.uint32), eng.device)
+    nb = int((np.diff(off) // B).sum())
+    keys = gh.to_dev(np.arange(max(nb, 1), dtype=np.uint64), eng.device)
+    with pytest.raises(pk.DMError) as ei:
+        eng.kv_save(gh.to_dev(off, eng.device), keys, bad_inst, clock, cap)
+    assert ei.value.status == pk.DM_EINVAL
+    with pytest.raises(pk.DMError) as ei:
+        eng.kv_save(gh.to_dev(off, eng.device), keys, gh.to_dev(np.zeros(len(off) - 1, np.uint32),
+                                                               eng.device), clock, 1 << 20)
+    assert ei.value.status == pk.DM_EINVAL
+    # clearing an instance drops its saved keys from the record too
+    eng.index_clear(0)
+    o.index_clear(0)
+    assert eng.index_size(0) == 0 == o.index_size(0)
+
+
 def _disjoint_pair_prompts(o, rng, n_pool):
     """Random prompts whose candidate pairs are pairwise disjoint (greedy
     over a pool), found with the oracle's ring keys and candidates."""

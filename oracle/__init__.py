@@ -82,6 +82,9 @@ def lib():
             "or_route": (i32, [P, P, P, u64, P, P, P, P, P, P, P, P, P]),
             "or_set_policy": (i32, [P, i32]),
             "or_kv_save": (i32, [P, P, u64, P, P, u64, u64, P, P]),
+            "or_queue_append": (i32, [P, P, P, P, P, P, u64, P, P, P, P, u64, P, P, P, P, P]),
+            "or_queue_migrate": (i32, [P, P, P, P, P, P, u64, P, P, P, P, P, P, P, P]),
+            "or_queue_drain": (i32, [P, P, P, P, P, P, P, P, P, P, P, P, P, P]),
             "or_keylen_enable": (i32, [P, u64]),
             "or_keylen_window": (i32, [P]),
             "or_keylen_export": (i32, [P, P, u64, P]),
@@ -183,6 +186,63 @@ class Oracle:
         rc = lib().or_kv_save(self._h, _p(o), len(o) - 1, _p(bk), _p(ins), int(clock), int(cap),
                               C.byref(a), C.byref(r))
         return rc, int(a.value), int(r.value)
+
+    # -- queued requests (CSR tuples: qoff, rec_id, unc_here, alt, unc_alt, base_work)
+    @staticmethod
+    def _q(q):
+        qoff, rec, here, alt, there, base = q
+        return (np.ascontiguousarray(qoff, np.int64), np.ascontiguousarray(rec, np.uint64),
+                np.ascontiguousarray(here, np.uint32), np.ascontiguousarray(alt, np.uint32),
+                np.ascontiguousarray(there, np.uint32), np.ascontiguousarray(base, np.int64))
+
+    def _qout(self, n):
+        return (np.zeros(self.max_slots + 1, np.int64), np.zeros(max(n, 1), np.uint64),
+                np.zeros(max(n, 1), np.uint32), np.zeros(max(n, 1), np.uint32),
+                np.zeros(max(n, 1), np.uint32))
+
+    def queue_append(self, q, offsets, cand, match, chosen, rec_base: int):
+        """A routed batch joins the queues (or_queue_append)."""
+        qoff, rec, here, alt, there, base = self._q(q)
+        off = np.ascontiguousarray(offsets, np.int64)
+        nb = len(off) - 1
+        cand = np.ascontiguousarray(cand, np.uint32)
+        match = np.ascontiguousarray(match, np.uint32)
+        chosen = np.ascontiguousarray(chosen, np.uint32)
+        o = self._qout(int(qoff[-1]) + nb)
+        rc = lib().or_queue_append(self._h, _p(qoff), _p(rec), _p(here), _p(alt), _p(there), nb,
+                                   _p(off), _p(cand), _p(match), _p(chosen), int(rec_base),
+                                   *[_p(x) for x in o])
+        if rc != OK:
+            raise RuntimeError("or_queue_append failed with status %d" % rc)
+        n2 = int(o[0][-1])
+        return (o[0], o[1][:n2], o[2][:n2], o[3][:n2], o[4][:n2], base.copy())
+
+    def queue_migrate(self, q, mrec, msrc, mdst):
+        """A migration list applied to the queues (or_queue_migrate)."""
+        qoff, rec, here, alt, there, base = self._q(q)
+        mrec = np.ascontiguousarray(mrec, np.uint64)
+        msrc = np.ascontiguousarray(msrc, np.uint32)
+        mdst = np.ascontiguousarray(mdst, np.uint32)
+        o = self._qout(int(qoff[-1]))
+        rc = lib().or_queue_migrate(self._h, _p(qoff), _p(rec), _p(here), _p(alt), _p(there),
+                                    len(mrec), _p(mrec), _p(msrc), _p(mdst), *[_p(x) for x in o])
+        if rc != OK:
+            raise RuntimeError("or_queue_migrate failed with status %d" % rc)
+        n2 = int(o[0][-1])
+        return (o[0], o[1][:n2], o[2][:n2], o[3][:n2], o[4][:n2], base.copy())
+
+    def queue_drain(self, q, units):
+        """units[i] of service on every instance (or_queue_drain)."""
+        qoff, rec, here, alt, there, base = self._q(q)
+        units = np.ascontiguousarray(units, np.int64)
+        o = self._qout(int(qoff[-1]))
+        base2 = np.zeros_like(base)
+        rc = lib().or_queue_drain(self._h, _p(qoff), _p(rec), _p(here), _p(alt), _p(there),
+                                  _p(base), _p(units), *[_p(x) for x in o], _p(base2))
+        if rc != OK:
+            raise RuntimeError("or_queue_drain failed with status %d" % rc)
+        n2 = int(o[0][-1])
+        return (o[0], o[1][:n2], o[2][:n2], o[3][:n2], o[4][:n2], base2)
 
     def keylen_enable(self, max_nodes: int) -> int:
         """Adaptive hash-key length: an empty prefix hotness tree with room for

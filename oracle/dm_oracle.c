@@ -609,6 +609,146 @@ int or_kv_save(or_state *st, const int64_t *off, uint64_t n, const uint64_t *blo
 }
 
 /* ------------------------------------------------------------------------- */
+/* Queued requests: the serving state the rebalancing pass reads (Sec. 3.3). */
+/* Per instance a FIFO of records (request id, uncached tokens on it, the    */
+/* other candidate, uncached tokens there) in CSR form over instance slots, */
+/* and base work ahead of each queue.  Every operation writes a new CSR.    */
+/* ------------------------------------------------------------------------- */
+
+/* A routed batch joins the queues: request r (id rec_base + r) at the tail
+ * of its chosen instance's queue, in request order; its uncached tokens are
+ * len - B * match on each candidate, the other candidate its alternative. */
+int or_queue_append(const or_state *st, const int64_t *qoff, const uint64_t *rec,
+                    const uint32_t *here, const uint32_t *alt, const uint32_t *there, uint64_t nb,
+                    const int64_t *off, const uint32_t *cand, const uint32_t *match,
+                    const uint32_t *chosen, uint64_t rec_base, int64_t *qoff2, uint64_t *rec2,
+                    uint32_t *here2, uint32_t *alt2, uint32_t *there2)
+{
+    if (!st || !qoff || !qoff2)
+        return OR_EINVAL;
+    const uint32_t S = st->cfg.max_slots;
+    const int64_t B = st->cfg.block_size;
+    for (uint64_t r = 0; r < nb; r++)
+        if (chosen[r] >= S || off[r + 1] < off[r])
+            return OR_EINVAL;
+    qoff2[0] = 0;
+    for (uint32_t i = 0; i < S; i++) {
+        int64_t w = qoff2[i];
+        for (int64_t q = qoff[i]; q < qoff[i + 1]; q++, w++) {
+            rec2[w] = rec[q]; here2[w] = here[q]; alt2[w] = alt[q]; there2[w] = there[q];
+        }
+        for (uint64_t r = 0; r < nb; r++) {
+            if (chosen[r] != i)
+                continue;
+            const int64_t len = off[r + 1] - off[r];
+            const uint32_t c1 = cand[r], c2 = cand[nb + r];
+            const int64_t u1 = len - B * (int64_t)match[r], u2 = len - B * (int64_t)match[nb + r];
+            const int first = chosen[r] == c1;
+            rec2[w] = rec_base + r;
+            here2[w] = (uint32_t)(first ? u1 : u2);
+            alt2[w] = first ? c2 : c1;
+            there2[w] = (uint32_t)(first ? u2 : u1);
+            w++;
+        }
+        qoff2[i + 1] = w;
+    }
+    return OR_OK;
+}
+
+/* A migration list applied in order: each record leaves its source queue
+ * (the others keep their order) and joins its target's tail with the pair's
+ * roles swapped (its alternative becomes the source). */
+int or_queue_migrate(const or_state *st, const int64_t *qoff, const uint64_t *rec,
+                     const uint32_t *here, const uint32_t *alt, const uint32_t *there, uint64_t m,
+                     const uint64_t *mrec, const uint32_t *msrc, const uint32_t *mdst,
+                     int64_t *qoff2, uint64_t *rec2, uint32_t *here2, uint32_t *alt2,
+                     uint32_t *there2)
+{
+    if (!st || !qoff || !qoff2)
+        return OR_EINVAL;
+    const uint32_t S = st->cfg.max_slots;
+    const uint64_t Q = (uint64_t)qoff[S];
+    /* the queue position of every migrated record */
+    int64_t *at = (int64_t *)malloc((m ? m : 1) * sizeof(int64_t));
+    uint8_t *gone = (uint8_t *)calloc(Q ? Q : 1, 1);
+    if (!at || !gone) {
+        free(at); free(gone);
+        return OR_ENOMEM;
+    }
+    for (uint64_t k = 0; k < m; k++) {
+        at[k] = -1;
+        if (msrc[k] >= S || mdst[k] >= S) {
+            free(at); free(gone);
+            return OR_EINVAL;
+        }
+        for (int64_t q = qoff[msrc[k]]; q < qoff[msrc[k] + 1]; q++)
+            if (rec[q] == mrec[k] && !gone[q]) {
+                at[k] = q;
+                gone[q] = 1;
+                break;
+            }
+        if (at[k] < 0) {
+            free(at); free(gone);
+            return OR_EINVAL;
+        }
+    }
+    qoff2[0] = 0;
+    for (uint32_t i = 0; i < S; i++) {
+        int64_t w = qoff2[i];
+        for (int64_t q = qoff[i]; q < qoff[i + 1]; q++)
+            if (!gone[q]) {
+                rec2[w] = rec[q]; here2[w] = here[q]; alt2[w] = alt[q]; there2[w] = there[q];
+                w++;
+            }
+        for (uint64_t k = 0; k < m; k++)
+            if (mdst[k] == i) {
+                const int64_t q = at[k];
+                rec2[w] = rec[q]; here2[w] = there[q]; alt2[w] = msrc[k]; there2[w] = here[q];
+                w++;
+            }
+        qoff2[i + 1] = w;
+    }
+    free(at);
+    free(gone);
+    return OR_OK;
+}
+
+/* units[i] of service on instance i: base work first, then whole records
+ * from the head; a partly served head keeps the remainder. */
+int or_queue_drain(const or_state *st, const int64_t *qoff, const uint64_t *rec,
+                   const uint32_t *here, const uint32_t *alt, const uint32_t *there,
+                   const int64_t *base, const int64_t *units, int64_t *qoff2, uint64_t *rec2,
+                   uint32_t *here2, uint32_t *alt2, uint32_t *there2, int64_t *base2)
+{
+    if (!st || !qoff || !qoff2 || !base || !units || !base2)
+        return OR_EINVAL;
+    const uint32_t S = st->cfg.max_slots;
+    qoff2[0] = 0;
+    for (uint32_t i = 0; i < S; i++) {
+        if (units[i] < 0 || base[i] < 0)
+            return OR_EINVAL;
+        int64_t u = units[i];
+        const int64_t take = base[i] < u ? base[i] : u;
+        base2[i] = base[i] - take;
+        u -= take;
+        int64_t q = qoff[i];
+        while (q < qoff[i + 1] && u >= (int64_t)here[q]) {
+            u -= here[q];
+            q++;
+        }
+        int64_t w = qoff2[i];
+        for (int64_t p = q; p < qoff[i + 1]; p++, w++) {
+            rec2[w] = rec[p];
+            here2[w] = (uint32_t)(p == q ? (int64_t)here[p] - u : (int64_t)here[p]);
+            alt2[w] = alt[p];
+            there2[w] = there[p];
+        }
+        qoff2[i + 1] = w;
+    }
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------------- */
 /* Routing                                                                   */
 /* ------------------------------------------------------------------------- */
 

@@ -1119,3 +1119,78 @@ def test_kv_save_unbounded_and_errors():
     assert o.index_size(1) == len(np.unique(bk))
     (rc, _, _), _ = _kv_case(o, B, chains[:1], [2], 0, 0)
     assert rc == oracle.EINVAL
+
+
+# ---------------------------------------------------------------------------
+# Queued requests: append, migrate, drain (the state the rebalancing pass
+# reads, Sec. 3.3)
+# ---------------------------------------------------------------------------
+
+def _qs_csr(qs):
+    qoff, rec, here, alt, there, base = qs.csr()
+    return [qoff, rec, here, alt, there, base]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_queue_operations_match_queue_model(seed):
+    """Append routed batches, apply migration lists, drain: the oracle's CSR
+    operations against the multi-batch driver's queue model (tests/sim.py,
+    written independently), after every step."""
+    import sys
+    sys.path.insert(0, os.path.dirname(__file__))
+    import sim
+    S, B = 6, 4
+    o = oracle.Oracle(dict(block=B, key_blocks=1, seeds=(1, 2), vnodes=4, max_slots=S))
+    rng = np.random.default_rng(300 + seed)
+    base = rng.integers(0, 50, size=S).astype(np.int64)
+    qs = sim.QueueState(S, base)
+    q = _qs_csr(qs)
+    rec_base = 0
+    for step in range(5):
+        nb = int(rng.integers(1, 30))
+        lens = rng.integers(0, 40, size=nb)
+        off = np.zeros(nb + 1, np.int64)
+        off[1:] = np.cumsum(lens)
+        c1 = rng.integers(0, S, size=nb)
+        c2 = (c1 + rng.integers(1, S, size=nb)) % S
+        cand = np.concatenate([c1, c2]).astype(np.uint32)
+        match = np.concatenate([rng.integers(0, 1 + lens // B), rng.integers(0, 1 + lens // B)])
+        match = np.minimum(match, np.concatenate([lens // B, lens // B])).astype(np.uint32)
+        chosen = np.where(rng.random(nb) < 0.5, c1, c2).astype(np.uint32)
+        q = list(o.queue_append(q, off, cand, match, chosen, rec_base))
+        u1 = lens - B * match[:nb].astype(np.int64)
+        u2 = lens - B * match[nb:].astype(np.int64)
+        first = chosen == c1
+        qs.append(np.arange(rec_base, rec_base + nb, dtype=np.uint64), chosen,
+                  np.where(first, c2, c1), np.where(first, u1, u2), np.where(first, u2, u1))
+        rec_base += nb
+        for a, b in zip(q, _qs_csr(qs)):
+            assert np.array_equal(a, b)
+        # migrate a few records from their queues to their alternatives
+        Q = int(q[0][-1])
+        if Q:
+            pick = rng.choice(Q, size=min(Q, int(rng.integers(0, 6))), replace=False)
+            owner = np.searchsorted(q[0], np.arange(Q), side="right") - 1
+            mrec, msrc, mdst = q[1][pick], owner[pick].astype(np.uint32), q[3][pick]
+            q = list(o.queue_migrate(q, mrec, msrc, mdst))
+            qs.migrate(mrec, msrc, mdst)
+            for a, b in zip(q, _qs_csr(qs)):
+                assert np.array_equal(a, b)
+        units = rng.integers(0, 80, size=S).astype(np.int64)
+        q = list(o.queue_drain(q, units))
+        qs.drain(units)
+        for a, b in zip(q, _qs_csr(qs)):
+            assert np.array_equal(a, b)
+
+
+def test_queue_drain_hand_values():
+    """Base 5 and records of 3, 4, 6 tokens: 10 units serve the base (5),
+    the first record (3) and 2 of the second, which keeps 2."""
+    S = 1
+    o = oracle.Oracle(dict(block=4, key_blocks=1, seeds=(1, 2), vnodes=4, max_slots=S))
+    q = (np.array([0, 3], np.int64), np.array([7, 8, 9], np.uint64),
+         np.array([3, 4, 6], np.uint32), np.zeros(3, np.uint32), np.array([1, 1, 1], np.uint32),
+         np.array([5], np.int64))
+    qoff, rec, here, alt, there, base = o.queue_drain(q, np.array([10], np.int64))
+    assert qoff.tolist() == [0, 2] and rec.tolist() == [8, 9] and here.tolist() == [2, 6]
+    assert base.tolist() == [0]

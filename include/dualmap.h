@@ -224,6 +224,48 @@ typedef struct {
     int64_t decode_threshold_us;      /* read only with prefill_interval       */
 } dm_queues;
 
+/* Writable queues, the output of the queue operations below: device arrays
+ * with room for cap records (qoff [max_slots + 1], base_work [max_slots]).
+ * They must not overlap the input queues' arrays. */
+typedef struct {
+    int64_t* qoff;
+    uint64_t* rec_id;
+    uint32_t* unc_here;
+    uint32_t* alt;
+    uint32_t* unc_alt;
+    int64_t* base_work;
+    uint64_t cap;
+} dm_queue_out;
+
+/* Queue operations: the serving state the rebalancing pass reads, kept on
+ * the device.  Each reads queues q and writes the result to out (DM_EFULL,
+ * nothing written, if it holds more than out->cap records; DM_EINVAL,
+ * nothing written, if q's offsets are not in order within [0, qoff[S]] or
+ * q has 2^32 records or more).  All synchronise.
+ *   dm_queue_append: a routed batch (offsets as given to dm_route_batch;
+ *     routed->cand, match and chosen of its result) joins the queues:
+ *     request r, id rec_base + r, at the tail of chosen[r]'s queue in
+ *     request order, with len - B * match uncached tokens there and on the
+ *     other candidate, its alternative.  Base work unchanged.  DM_EINVAL
+ *     for a chosen id >= max_slots.
+ *   dm_queue_migrate: a migration list (e.g. dm_rebalance's, its first m
+ *     entries) applied in order: each record leaves its source's queue (the
+ *     others keep their order) and joins its target's tail with the pair's
+ *     roles swapped (its alternative becomes the source).  DM_EINVAL if a
+ *     record is not queued on its source, appears twice, or is id 2^64 - 1,
+ *     or an id is >= max_slots.
+ *   dm_queue_drain: units[i] (device int64 [max_slots], >= 0) of service on
+ *     instance i: its base work first, then whole records from the head; a
+ *     partly served head keeps the rest of its uncached tokens. */
+dm_status dm_queue_append(dm_ctx* ctx, const dm_queues* q, const int64_t* offsets, uint64_t n,
+                          const dm_route_out* routed, uint64_t rec_base,
+                          const dm_queue_out* out);
+dm_status dm_queue_migrate(dm_ctx* ctx, const dm_queues* q, const uint64_t* rec_id,
+                           const uint32_t* from, const uint32_t* to, uint64_t m,
+                           const dm_queue_out* out);
+dm_status dm_queue_drain(dm_ctx* ctx, const dm_queues* q, const int64_t* units,
+                         const dm_queue_out* out);
+
 /* Migration list of dm_rebalance (device arrays of cap entries). */
 typedef struct {
     uint64_t* rec_id;

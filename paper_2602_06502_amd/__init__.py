@@ -27,7 +27,8 @@ EXPORTS = ("dm_create", "dm_destroy", "dm_build_rings", "dm_ring_export", "dm_in
            "dm_index_erase", "dm_index_clear", "dm_index_size", "dm_route_batch",
            "dm_route_batch_noalloc",
            "dm_rebalance", "dm_scale", "dm_set_timing", "dm_route_stage_ms",
-           "dm_kv_save", "dm_set_pipelining", "dm_set_policy", "dm_keylen_enable",
+           "dm_kv_save", "dm_queue_append", "dm_queue_migrate", "dm_queue_drain",
+           "dm_set_pipelining", "dm_set_policy", "dm_keylen_enable",
            "dm_keylen_window",
            "dm_keylen_export", "dm_sync", "dm_last_error")
 
@@ -56,6 +57,12 @@ class dm_queues(C.Structure):
     _fields_ = [("qoff", C.c_void_p), ("rec_id", C.c_void_p), ("unc_here", C.c_void_p),
                 ("alt", C.c_void_p), ("unc_alt", C.c_void_p), ("base_work", C.c_void_p),
                 ("prefill_interval", C.c_void_p), ("decode_threshold_us", C.c_int64)]
+
+
+class dm_queue_out(C.Structure):
+    _fields_ = [("qoff", C.c_void_p), ("rec_id", C.c_void_p), ("unc_here", C.c_void_p),
+                ("alt", C.c_void_p), ("unc_alt", C.c_void_p), ("base_work", C.c_void_p),
+                ("cap", C.c_uint64)]
 
 
 class dm_migrations(C.Structure):
@@ -93,6 +100,9 @@ def load_library(path: str = LIB_PATH):
         "dm_set_pipelining": (i32, [P, i32]),
         "dm_set_policy": (i32, [P, i32]),
         "dm_kv_save": (i32, [P, P, u64, P, P, u64, u64, P, P]),
+        "dm_queue_append": (i32, [P, P, P, u64, P, u64, P]),
+        "dm_queue_migrate": (i32, [P, P, P, P, P, u64, P]),
+        "dm_queue_drain": (i32, [P, P, P, P]),
         "dm_keylen_enable": (i32, [P, u64, u64]),
         "dm_keylen_window": (i32, [P]),
         "dm_keylen_export": (i32, [P, P, u64, P]),
@@ -278,6 +288,74 @@ class DualMap:
                                         _ptr(block_keys), _ptr(inst), int(clock), int(cap),
                                         C.byref(a), C.byref(r)), "dm_kv_save")
         return int(a.value), int(r.value)
+
+    # -- queued requests on the device: tuples (qoff, rec_id, unc_here, alt,
+    # unc_alt, base_work) of device tensors
+    def _qin(self, q):
+        t = self.torch
+        qoff, rec, here, alt, there, base = q
+        return (self._dev(qoff, t.int64, "qoff"), self._dev(rec, t.uint64, "rec_id"),
+                self._dev(here, t.uint32, "unc_here"), self._dev(alt, t.uint32, "alt"),
+                self._dev(there, t.uint32, "unc_alt"), self._dev(base, t.int64, "base_work"))
+
+    def _qnew(self, cap: int):
+        t = self.torch
+        c = max(int(cap), 1)
+        return (self._empty(self.max_slots + 1, t.int64), self._empty(c, t.uint64),
+                self._empty(c, t.uint32), self._empty(c, t.uint32), self._empty(c, t.uint32),
+                self._empty(self.max_slots, t.int64))
+
+    @staticmethod
+    def _qstructs(qi, qo, cap):
+        qs = dm_queues(*[_ptr(x) for x in qi], None, 0)
+        qd = dm_queue_out(*[_ptr(x) for x in qo], int(cap))
+        return qs, qd
+
+    def _qtrim(self, qo):
+        n = int(qo[0][-1].item())
+        return (qo[0], qo[1][:n], qo[2][:n], qo[3][:n], qo[4][:n], qo[5])
+
+    def queue_append(self, q, offsets, routed: Dict, rec_base: int):
+        """A routed batch joins the queues (see dm_queue_append)."""
+        qi = self._qin(q)
+        offsets = self._dev(offsets, self.torch.int64, "offsets")
+        n = offsets.numel() - 1
+        cap = qi[1].numel() + n
+        qo = self._qnew(cap)
+        qs, qd = self._qstructs(qi, qo, cap)
+        ro = dm_route_out(_ptr(routed["key"]), _ptr(routed["cand"]), _ptr(routed["match"]),
+                          _ptr(routed["chosen"]), _ptr(routed["ttft"]), _ptr(routed["flags"]),
+                          None, None)
+        self._check(self.lib.dm_queue_append(self._h, C.byref(qs), _ptr(offsets), n,
+                                             C.byref(ro), int(rec_base), C.byref(qd)),
+                    "dm_queue_append")
+        return self._qtrim(qo)
+
+    def queue_migrate(self, q, rec_id, src, dst):
+        """A migration list applied to the queues (see dm_queue_migrate)."""
+        t = self.torch
+        qi = self._qin(q)
+        rec_id = self._dev(rec_id, t.uint64, "rec_id")
+        src = self._dev(src, t.uint32, "from")
+        dst = self._dev(dst, t.uint32, "to")
+        cap = qi[1].numel()
+        qo = self._qnew(cap)
+        qs, qd = self._qstructs(qi, qo, cap)
+        self._check(self.lib.dm_queue_migrate(self._h, C.byref(qs), _ptr(rec_id), _ptr(src),
+                                              _ptr(dst), rec_id.numel(), C.byref(qd)),
+                    "dm_queue_migrate")
+        return self._qtrim(qo)
+
+    def queue_drain(self, q, units):
+        """units[i] of service per instance (see dm_queue_drain)."""
+        qi = self._qin(q)
+        units = self._dev(units, self.torch.int64, "units")
+        cap = qi[1].numel()
+        qo = self._qnew(cap)
+        qs, qd = self._qstructs(qi, qo, cap)
+        self._check(self.lib.dm_queue_drain(self._h, C.byref(qs), _ptr(units), C.byref(qd)),
+                    "dm_queue_drain")
+        return self._qtrim(qo)
 
     def keylen_enable(self, max_nodes: int, max_window_blocks: int = 1 << 24) -> None:
         """Adaptive hash-key length (see dm_keylen_enable): an empty prefix

@@ -404,6 +404,69 @@ dm_status dm_index_clear(dm_ctx* c, uint32_t id)
     return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_index_clear");
 }
 
+// Host checks shared by the queue operations.
+static dm_status queue_args(dm_ctx* c, const dm_queues* q, const dm_queue_out* out,
+                            const char* what)
+{
+    if (!q || !out || !q->qoff || !q->base_work || !out->qoff || !out->base_work)
+        return fail(c, DM_EINVAL, std::string(what) + ": null argument");
+    if (out->cap && (!out->rec_id || !out->unc_here || !out->alt || !out->unc_alt))
+        return fail(c, DM_EINVAL, std::string(what) + ": null output array");
+    if (!aligned(q->qoff) || !aligned(q->base_work) || !aligned(out->qoff) ||
+        !aligned(out->base_work) || !aligned(q->rec_id) || !aligned(out->rec_id))
+        return fail(c, DM_EINVAL, std::string(what) + ": misaligned pointer");
+    const void* in_p[] = {q->qoff, q->rec_id, q->unc_here, q->alt, q->unc_alt, q->base_work};
+    const void* out_p[] = {out->qoff, out->rec_id, out->unc_here, out->alt, out->unc_alt,
+                           out->base_work};
+    for (const void* a : in_p)
+        for (const void* b : out_p)
+            if (a && a == b)
+                return fail(c, DM_EINVAL, std::string(what) + ": output aliases the input");
+    return DM_OK;
+}
+
+dm_status dm_queue_append(dm_ctx* c, const dm_queues* q, const int64_t* offsets, uint64_t n,
+                          const dm_route_out* routed, uint64_t rec_base, const dm_queue_out* out)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (dm_status s = queue_args(c, q, out, "dm_queue_append"); s != DM_OK)
+        return s;
+    if (n && (!offsets || !routed || !routed->cand || !routed->match || !routed->chosen))
+        return fail(c, DM_EINVAL, "dm_queue_append: null batch argument");
+    if (n >= (1ull << 32))
+        return fail(c, DM_EINVAL, "dm_queue_append: batch too large");
+    DeviceGuard g(c->device);
+    return queue_append(c, q, offsets, n, routed, rec_base, out);
+}
+
+dm_status dm_queue_migrate(dm_ctx* c, const dm_queues* q, const uint64_t* rec_id,
+                           const uint32_t* from, const uint32_t* to, uint64_t m,
+                           const dm_queue_out* out)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (dm_status s = queue_args(c, q, out, "dm_queue_migrate"); s != DM_OK)
+        return s;
+    if (m && (!rec_id || !from || !to))
+        return fail(c, DM_EINVAL, "dm_queue_migrate: null migration array");
+    DeviceGuard g(c->device);
+    return queue_migrate(c, q, rec_id, from, to, m, out);
+}
+
+dm_status dm_queue_drain(dm_ctx* c, const dm_queues* q, const int64_t* units,
+                         const dm_queue_out* out)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (dm_status s = queue_args(c, q, out, "dm_queue_drain"); s != DM_OK)
+        return s;
+    if (!units || !aligned(units))
+        return fail(c, DM_EINVAL, "dm_queue_drain: null or misaligned units");
+    DeviceGuard g(c->device);
+    return queue_drain(c, q, units, out);
+}
+
 dm_status dm_kv_save(dm_ctx* c, const int64_t* offsets, uint64_t n, const uint64_t* block_keys,
                      const uint32_t* inst, uint64_t clock, uint64_t cap, uint64_t* added_host,
                      uint64_t* removed_host)

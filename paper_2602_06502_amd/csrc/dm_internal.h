@@ -313,6 +313,16 @@ dm_status kv_save(dm_ctx* c, const int64_t* offsets, uint64_t n, const uint64_t*
 hipError_t kv_forget(dm_ctx* c, const uint8_t* d_gone);
 void kv_free(dm_ctx* c);
 
+// dm_queue.hip: queued requests, CSR to CSR (host entry points; they
+// synchronise).  The output arrays must not overlap the input's.
+dm_status queue_append(dm_ctx* c, const dm_queues* q, const int64_t* offsets, uint64_t n,
+                       const dm_route_out* routed, uint64_t rec_base, const dm_queue_out* out);
+dm_status queue_migrate(dm_ctx* c, const dm_queues* q, const uint64_t* mrec,
+                        const uint32_t* msrc, const uint32_t* mdst, uint64_t m,
+                        const dm_queue_out* out);
+dm_status queue_drain(dm_ctx* c, const dm_queues* q, const int64_t* units,
+                      const dm_queue_out* out);
+
 // dm_probe.hip: candidates on the current rings (cand, fix-up flag bit 3),
 // then requests ordered by their first ring key and grouped (gv).
 hipError_t lookup_group(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64_t* bstart,

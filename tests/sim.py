@@ -262,7 +262,10 @@ def run_agent(side, cfg, mu: int, n_batches: int, warm: bool = True):
             _apply_lru(side, lru, out["chosen"], out, off, B)
     mean_gap = (unc_sum / max(unc_n, 1)) / (cfg.utilisation * rc.n_inst * cfg.drain_per_us)
     gaps = workloads.arrival_gaps(cfg.seed, n_batches, cfg.batch, mean_gap)
-    qs = QueueState(S, agent_base_work(cfg, mu))
+    # the side keeps the queues itself (dm_queue_* / or_queue_*), or this
+    # module's model does
+    qs = side.queues(S, agent_base_work(cfg, mu)) if getattr(side, "queues_on_side", False) \
+        else QueueState(S, agent_base_work(cfg, mu))
     for b in range(n_batches):
         tok, off = _cached(("agent", cfg, 0, b), lambda: workloads.agent_batch(cfg, b, cfg.batch))
         n = len(off) - 1
@@ -276,13 +279,16 @@ def run_agent(side, cfg, mu: int, n_batches: int, warm: bool = True):
         u1, u2 = _uncached(out, off, B)
         first = ch == c1
         rec = np.arange(b * cfg.batch, b * cfg.batch + n, dtype=np.uint64)
-        qs.append(rec, ch, np.where(first, c2, c1), np.where(first, u1, u2),
-                  np.where(first, u2, u1))
+        if getattr(side, "queues_on_side", False):
+            qs.append_routed(off, b * cfg.batch)
+        else:
+            qs.append(rec, ch, np.where(first, c2, c1), np.where(first, u1, u2),
+                      np.where(first, u2, u1))
         # a stall the router did not see (e.g. decode-bound instances,
         # Sec. A.7): a few instances' queued work jumps to hot_factor x mu
         hot = workloads.agent_hot_instances(cfg, b)
         qs.base[hot] += (cfg.hot_factor - 1) * mu
-        queued = sum(len(x) for x in qs.q)
+        queued = qs.count() if getattr(side, "queues_on_side", False) else sum(len(x) for x in qs.q)
         mg = side.rebalance(qs.csr())
         mg["queued"] = queued
         yield "rebalance", b, mg

@@ -38,8 +38,107 @@ def _say(*a):
     print("[case]", *a, flush=True)
 
 
+class OracleQueues:
+    """The oracle's queue operations behind the driver's queue interface."""
+
+    def __init__(self, o, S, base):
+        self.o = o
+        self.q = (np.zeros(S + 1, np.int64), np.zeros(0, np.uint64), np.zeros(0, np.uint32),
+                  np.zeros(0, np.uint32), np.zeros(0, np.uint32), np.asarray(base, np.int64))
+        self.last = None
+
+    @property
+    def base(self):
+        return _BaseView(self)
+
+    def loads(self):
+        qoff, rec, here, alt, there, base = self.q
+        L = base.copy()
+        np.add.at(L, np.repeat(np.arange(len(qoff) - 1), np.diff(qoff)), here.astype(np.int64))
+        return L
+
+    def append_routed(self, off, rec_base):
+        r = self.last
+        self.q = self.o.queue_append(self.q, off, r["cand"], r["match"], r["chosen"], rec_base)
+
+    def count(self):
+        return int(self.q[0][-1])
+
+    def csr(self):
+        return tuple(np.array(x) for x in self.q)
+
+    def migrate(self, rec, src, dst):
+        self.q = self.o.queue_migrate(self.q, rec, src, dst)
+
+    def drain(self, units):
+        self.q = self.o.queue_drain(self.q, units)
+
+
+class _BaseView:
+    """qs.base[hot] += x on a side's queue state."""
+
+    def __init__(self, owner):
+        self.owner = owner
+
+    def __getitem__(self, idx):
+        b = self.owner.q[5]
+        return (b if isinstance(b, np.ndarray) else b.cpu().numpy())[idx]
+
+    def __setitem__(self, idx, val):
+        q = list(self.owner.q)
+        base = np.array(q[5], np.int64) if isinstance(q[5], np.ndarray) else q[5]
+        if isinstance(base, np.ndarray):
+            base[idx] = val
+            q[5] = base
+        else:  # a device tensor
+            b = base.clone()
+            b[torch.as_tensor(np.asarray(idx), device=b.device)] = torch.as_tensor(
+                np.asarray(val, np.int64), device=b.device)
+            q[5] = b
+        self.owner.q = tuple(q)
+
+
+class EngineQueues(OracleQueues):
+    """The device queue operations (dm_queue_*); the queues stay on the GPU."""
+
+    def __init__(self, side, S, base):
+        self.side = side
+        eng, d = side.eng, side._d
+        self.q = (d(np.zeros(S + 1, np.int64)), d(np.zeros(0, np.uint64)),
+                  d(np.zeros(0, np.uint32)), d(np.zeros(0, np.uint32)), d(np.zeros(0, np.uint32)),
+                  d(np.asarray(base, np.int64)))
+        self.last = None
+
+    def loads(self):
+        qoff, rec, here, alt, there, base = self.q
+        S = qoff.numel() - 1
+        owner = torch.repeat_interleave(torch.arange(S, device=qoff.device), qoff[1:] - qoff[:-1])
+        L = base.clone()
+        L.index_add_(0, owner, here.to(torch.int64))
+        return L.cpu().numpy()
+
+    def append_routed(self, off, rec_base):
+        self.q = self.side.eng.queue_append(self.q, self.side._d(np.asarray(off, np.int64)),
+                                            self.side._dev_out, rec_base)
+
+    def count(self):
+        return int(self.q[0][-1].item())
+
+    def csr(self):
+        return tuple(x.cpu().numpy() for x in self.q)
+
+    def migrate(self, rec, src, dst):
+        d = self.side._d
+        self.q = self.side.eng.queue_migrate(self.q, d(np.asarray(rec, np.uint64)),
+                                             d(np.asarray(src, np.uint32)),
+                                             d(np.asarray(dst, np.uint32)))
+
+    def drain(self, units):
+        self.q = self.side.eng.queue_drain(self.q, self.side._d(np.asarray(units, np.int64)))
+
+
 class OracleSide:
-    def __init__(self, rc, keylen_nodes=0, kv_on_side=False):
+    def __init__(self, rc, keylen_nodes=0, kv_on_side=False, queues_on_side=False):
         self.o = oracle.Oracle(rc.as_dict())
         assert self.o.build_rings(range(rc.n_inst)) == 0
         self.keylen = keylen_nodes > 0
@@ -47,6 +146,13 @@ class OracleSide:
             assert self.o.keylen_enable(keylen_nodes) == oracle.OK
         self.kv_on_side = kv_on_side
         self.kv_counts = []
+        self.queues_on_side = queues_on_side
+        self._q = None
+        self._last = None
+
+    def queues(self, S, base):
+        self._q = OracleQueues(self.o, S, base)
+        return self._q
 
     def kv_save(self, off, out, inst, clock, cap):
         rc, a, r = self.o.kv_save(off, out["block_keys"], inst, clock, cap)
@@ -60,7 +166,10 @@ class OracleSide:
         return self.o.keylen_tree()
 
     def route(self, tok, off, loads):
-        return self.o.route(tok, off, loads, block_keys=True)
+        out = self.o.route(tok, off, loads, block_keys=True)
+        if self._q is not None:
+            self._q.last = out
+        return out
 
     def insert(self, c, keys):
         self.o.index_insert(c, keys)
@@ -75,7 +184,7 @@ class OracleSide:
 
 
 class EngineSide:
-    def __init__(self, rc, keylen_nodes=0, kv_on_side=False):
+    def __init__(self, rc, keylen_nodes=0, kv_on_side=False, queues_on_side=False):
         import paper_2602_06502_amd.harness as gh
         self.gh = gh
         self.eng = gh.DualMap(rc.as_dict(), device="cuda:0")
@@ -86,6 +195,10 @@ class EngineSide:
         self.kv_on_side = kv_on_side
         self.kv_counts = []
         self._dev_out = None
+        self.queues_on_side = queues_on_side
+
+    def queues(self, S, base):
+        return EngineQueues(self, S, base)
 
     def kv_save(self, off, out, inst, clock, cap):
         # the block keys the last route left on the device; the offsets and
@@ -109,7 +222,7 @@ class EngineSide:
         self.eng.sync()
         res = {k: v.cpu().numpy() for k, v in out.items()}
         res["loads"] = L.cpu().numpy()
-        self._dev_out = out if self.kv_on_side else None
+        self._dev_out = out if (self.kv_on_side or self.queues_on_side) else None
         return res
 
     def insert(self, c, keys):
@@ -252,3 +365,25 @@ def test_agent_multibatch_device_kv_save_parity():
     assert gs.kv_counts == os_.kv_counts
     # the caches fill past their 200,000 blocks: saves evict
     assert sum(r for _, r in os_.kv_counts) > 0
+
+
+def test_agent_multibatch_device_resident_parity():
+    """The agent workload with its serving state on each side: queues kept
+    by the queue operations (routed batches appended, migration lists
+    applied, service drained: dm_queue_* on the GPU, or_queue_* in the
+    oracle) and caches by the KV save; every routed batch and rebalancing
+    pass compared, and the queues themselves at the end."""
+    _gpu()
+    cfg = workloads.agent()
+    rc = cfg.route
+    gs = EngineSide(rc, kv_on_side=True, queues_on_side=True)
+    os_ = OracleSide(rc, kv_on_side=True, queues_on_side=True)
+    migrated = 0
+    for x, y in itertools.zip_longest(sim.run_agent(gs, cfg, cfg.mu, 6),
+                                      sim.run_agent(os_, cfg, cfg.mu, 6)):
+        (st, b, g), (st2, b2, o) = x, y
+        assert (st, b) == (st2, b2)
+        _compare(st, b, g, o)
+        if st == "rebalance":
+            migrated += o["count"]
+    assert migrated > 0

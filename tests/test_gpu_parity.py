@@ -384,6 +384,103 @@ def test_kv_save_parity_and_errors():
     assert eng.index_size(0) == 0 == o.index_size(0)
 
 
+def _q_eq(g, o, what):
+    names = ("qoff", "rec_id", "unc_here", "alt", "unc_alt", "base_work")
+    for name, a, b in zip(names, g, o):
+        a = cpu(a)
+        assert a.shape == b.shape and np.array_equal(a, b), f"{what}: {name}"
+
+
+@pytest.mark.parametrize("seed,n_inst,batch", [(0, 6, 40), (1, 60, 3000), (2, 200, 9000)])
+def test_queue_operations_parity(seed, n_inst, batch):
+    """Routed batches appended, random migration lists applied and random
+    service drained, on the device queues and on the oracle's, compared
+    after every operation; the batches span several blocks of the kernels,
+    include empty prompts, an empty batch and an empty migration list."""
+    gh = _h()
+    B = 16
+    wl = workloads.small_random(97 + seed, n_inst, 4, B, 8)
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    S = wl.route.max_slots
+    d = lambda a: gh.to_dev(a, eng.device)
+    rng = np.random.default_rng(400 + seed)
+    base = rng.integers(0, 5000, size=S).astype(np.int64)
+    qo = (np.zeros(S + 1, np.int64), np.zeros(0, np.uint64), np.zeros(0, np.uint32),
+          np.zeros(0, np.uint32), np.zeros(0, np.uint32), base)
+    qg = tuple(d(x) for x in qo)
+    rec_base = 0
+    for step in range(6):
+        nb = 0 if step == 2 else int(rng.integers(1, batch))
+        _say("queue ops step", step, "batch", nb, "queued", int(qo[0][-1]))
+        lens = rng.integers(0, 40 * B, size=nb)
+        lens[rng.random(nb) < 0.05] = 0
+        off = np.zeros(nb + 1, np.int64)
+        off[1:] = np.cumsum(lens)
+        c1 = rng.integers(0, n_inst, size=nb)
+        c2 = (c1 + rng.integers(1, n_inst, size=nb)) % n_inst
+        cand = np.concatenate([c1, c2]).astype(np.uint32)
+        match = np.concatenate([rng.integers(0, 1 + lens // B), rng.integers(0, 1 + lens // B)])
+        match = match.astype(np.uint32)
+        chosen = np.where(rng.random(nb) < 0.5, c1, c2).astype(np.uint32)
+        routed = {"key": None, "ttft": None, "flags": None,
+                  "cand": d(cand), "match": d(match), "chosen": d(chosen)}
+        qg = eng.queue_append(qg, d(off), routed, rec_base)
+        qo = o.queue_append(qo, off, cand, match, chosen, rec_base)
+        _q_eq(qg, qo, "append")
+        rec_base += nb
+        Q = int(qo[0][-1])
+        k = 0 if step == 3 else min(Q, int(rng.integers(0, max(2, Q // 4))))
+        pick = rng.choice(Q, size=k, replace=False) if k else np.zeros(0, np.int64)
+        owner = np.searchsorted(qo[0], np.arange(Q), side="right") - 1
+        mrec, msrc, mdst = qo[1][pick], owner[pick].astype(np.uint32), qo[3][pick]
+        qg = eng.queue_migrate(qg, d(mrec), d(msrc), d(mdst))
+        qo = o.queue_migrate(qo, mrec, msrc, mdst)
+        _q_eq(qg, qo, "migrate")
+        units = rng.integers(0, 20_000, size=S).astype(np.int64)
+        units[rng.random(S) < 0.2] = 0
+        qg = eng.queue_drain(qg, d(units))
+        qo = o.queue_drain(qo, units)
+        _q_eq(qg, qo, "drain")
+
+
+def test_queue_operations_errors():
+    """Bad inputs are rejected, nothing written: a chosen id out of range, a
+    migration of a record that is not on its source, a record listed twice,
+    negative service."""
+    gh = _h()
+    import paper_2602_06502_amd as pk
+    wl = workloads.small_random(99, 6, 4, 16, 8)
+    eng = gh.engine_for(wl)
+    S = wl.route.max_slots
+    d = lambda a: gh.to_dev(a, eng.device)
+    q = (d(np.array([0] + [2] * S, np.int64)), d(np.array([5, 6], np.uint64)),
+         d(np.array([3, 4], np.uint32)), d(np.array([1, 1], np.uint32)),
+         d(np.array([7, 8], np.uint32)), d(np.zeros(S, np.int64)))
+    off = np.array([0, 16], np.int64)
+    routed = {"key": None, "ttft": None, "flags": None, "cand": d(np.array([0, 1], np.uint32)),
+              "match": d(np.zeros(2, np.uint32)), "chosen": d(np.array([S], np.uint32))}
+    cases = [
+        lambda: eng.queue_append(q, d(off), routed, 10),
+        lambda: eng.queue_migrate(q, d(np.array([5], np.uint64)), d(np.array([1], np.uint32)),
+                                  d(np.array([2], np.uint32))),
+        lambda: eng.queue_migrate(q, d(np.array([5, 5], np.uint64)),
+                                  d(np.array([0, 0], np.uint32)), d(np.array([1, 1], np.uint32))),
+        lambda: eng.queue_migrate(q, d(np.array([5], np.uint64)), d(np.array([0], np.uint32)),
+                                  d(np.array([S], np.uint32))),
+        lambda: eng.queue_drain(q, d(np.full(S, -1, np.int64))),
+    ]
+    for i, f in enumerate(cases):
+        _say("queue error case", i)
+        with pytest.raises(pk.DMError) as ei:
+            f()
+        assert ei.value.status == pk.DM_EINVAL, i
+    # the valid forms of the same calls go through
+    g = eng.queue_migrate(q, d(np.array([6], np.uint64)), d(np.array([0], np.uint32)),
+                          d(np.array([1], np.uint32)))
+    assert cpu(g[0]).tolist()[:3] == [0, 1, 2] and cpu(g[1]).tolist() == [5, 6]
+    assert cpu(g[2]).tolist() == [3, 8] and cpu(g[3]).tolist() == [1, 0]
+
+
 def _disjoint_pair_prompts(o, rng, n_pool):
     """Random prompts whose candidate pairs are pairwise disjoint (greedy
     over a pool), found with the oracle's ring keys and candidates."""

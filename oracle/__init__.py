@@ -85,6 +85,7 @@ def lib():
             "or_queue_append": (i32, [P, P, P, P, P, P, u64, P, P, P, P, u64, P, P, P, P, P]),
             "or_queue_migrate": (i32, [P, P, P, P, P, P, u64, P, P, P, P, P, P, P, P]),
             "or_queue_drain": (i32, [P, P, P, P, P, P, P, P, P, P, P, P, P, P]),
+            "or_queue_reprobe": (i32, [P, P, P, P, u64, P, P, P, P, P]),
             "or_keylen_enable": (i32, [P, u64]),
             "or_keylen_window": (i32, [P]),
             "or_keylen_export": (i32, [P, P, u64, P]),
@@ -230,6 +231,23 @@ class Oracle:
             raise RuntimeError("or_queue_migrate failed with status %d" % rc)
         n2 = int(o[0][-1])
         return (o[0], o[1][:n2], o[2][:n2], o[3][:n2], o[4][:n2], base.copy())
+
+    def queue_reprobe(self, q, coff, keys, plen):
+        """Queued records re-priced against the current caches
+        (or_queue_reprobe): record id r's chain keys[coff[r]:coff[r+1]], its
+        prompt plen[r] tokens."""
+        qoff, rec, here, alt, there, base = self._q(q)
+        coff = np.ascontiguousarray(coff, np.int64)
+        keys = np.ascontiguousarray(keys, np.uint64)
+        plen = np.ascontiguousarray(plen, np.int64)
+        n = max(len(rec), 1)
+        here2, there2 = np.zeros(n, np.uint32), np.zeros(n, np.uint32)
+        rc = lib().or_queue_reprobe(self._h, _p(qoff), _p(rec), _p(alt), len(plen), _p(coff),
+                                    _p(keys), _p(plen), _p(here2), _p(there2))
+        if rc != OK:
+            raise RuntimeError("or_queue_reprobe failed with status %d" % rc)
+        Q = len(rec)
+        return (qoff.copy(), rec.copy(), here2[:Q], alt.copy(), there2[:Q], base.copy())
 
     def queue_drain(self, q, units):
         """units[i] of service on every instance (or_queue_drain)."""

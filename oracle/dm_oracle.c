@@ -811,6 +811,40 @@ static uint64_t prefix_match(const or_state *st, uint32_t id, const uint64_t *h1
     return m;
 }
 
+/* Queued records re-priced against the caches as they are now: each TTFT
+ * the rebalancing pass evaluates rests on a KV-cache query on the record's
+ * instance and one on its backup (Sec. A.3.2, rebalancing cost; Sec. 3.3).
+ * Record id r's f1 block chain is keys[coff[r] .. coff[r+1]) and its prompt
+ * plen[r] tokens; its uncached tokens become plen - B * (cached leading
+ * blocks of the chain) on its instance (here2) and on its alternative
+ * (there2).  Order, ids, alternatives and base work are unchanged.
+ * OR_EINVAL for an id >= n_ids, a chain with more blocks than the prompt
+ * holds, or a prompt outside [0, 2^32). */
+int or_queue_reprobe(const or_state *st, const int64_t *qoff, const uint64_t *rec,
+                     const uint32_t *alt, uint64_t n_ids, const int64_t *coff,
+                     const uint64_t *keys, const int64_t *plen, uint32_t *here2, uint32_t *there2)
+{
+    if (!st || !qoff)
+        return OR_EINVAL;
+    const uint32_t S = st->cfg.max_slots;
+    const int64_t B = st->cfg.block_size;
+    for (uint32_t i = 0; i < S; i++) {
+        for (int64_t q = qoff[i]; q < qoff[i + 1]; q++) {
+            const uint64_t r = rec[q];
+            if (r >= n_ids || alt[q] >= S)
+                return OR_EINVAL;
+            const int64_t nb = coff[r + 1] - coff[r];
+            if (coff[r] < 0 || nb < 0 || plen[r] < 0 || plen[r] >= ((int64_t)1 << 32) ||
+                nb * B > plen[r])
+                return OR_EINVAL;
+            const uint64_t *h1 = keys + coff[r];
+            here2[q] = (uint32_t)(plen[r] - B * (int64_t)prefix_match(st, i, h1, (uint64_t)nb));
+            there2[q] = (uint32_t)(plen[r] - B * (int64_t)prefix_match(st, alt[q], h1, (uint64_t)nb));
+        }
+    }
+    return OR_OK;
+}
+
 /* Selection of one request between its candidates.  Loads L are pending
  * prefill tokens before this request.  SLO-aware rule (Sec. 3.2 "SLO-Aware
  * Strategy"; Sec. A.1.1):

@@ -1183,6 +1183,81 @@ def test_queue_operations_match_queue_model(seed):
             assert np.array_equal(a, b)
 
 
+def test_queue_reprobe_hand_values():
+    """Instance 0 caches blocks {10, 11}, instance 1 {10}; B = 16.  Chain
+    [10, 11, 12] of 100 tokens: 2 blocks cached on 0 (68 uncached), 1 on 1
+    (84).  Chain [11, 10] of 40 tokens queued on 1: none there (40), both on
+    0 (8).  An empty chain of 5 tokens: 5 everywhere."""
+    o = oracle.Oracle(dict(block=16, key_blocks=1, seeds=(1, 2), vnodes=4, max_slots=2))
+    o.index_insert(0, np.array([10, 11], np.uint64))
+    o.index_insert(1, np.array([10], np.uint64))
+    coff = np.array([0, 3, 3, 5], np.int64)
+    keys = np.array([10, 11, 12, 11, 10], np.uint64)
+    plen = np.array([100, 5, 40], np.int64)
+    q = (np.array([0, 1, 3], np.int64), np.array([0, 1, 2], np.uint64),
+         np.array([1, 2, 3], np.uint32), np.array([1, 0, 0], np.uint32),
+         np.array([4, 5, 6], np.uint32), np.array([7, 9], np.int64))
+    qoff, rec, here, alt, there, base = o.queue_reprobe(q, coff, keys, plen)
+    assert here.tolist() == [68, 5, 40] and there.tolist() == [84, 5, 8]
+    assert qoff.tolist() == [0, 1, 3] and rec.tolist() == [0, 1, 2]
+    assert alt.tolist() == [1, 0, 0] and base.tolist() == [7, 9]
+    with pytest.raises(RuntimeError):  # an id without a chain
+        o.queue_reprobe(q, coff[:3], keys, plen[:2])
+    with pytest.raises(RuntimeError):  # 2 blocks of 16 cannot fit 31 tokens
+        o.queue_reprobe(q, coff, keys, np.array([100, 5, 31], np.int64))
+
+
+def test_queue_reprobe_matches_routing_until_caches_change():
+    """Right after routing, the re-probed uncached tokens are the ones the
+    routing pass computed (append's), and they stay so after migrations
+    (roles swap with the records).  Once a record's whole chain is saved on
+    its alternative, its cost there is just the partial tail, len mod B."""
+    import oracle.harness as oh
+    wl = workloads.small_random(41, 6, 8, 16, 200)
+    o = oh.oracle_for(wl)
+    oh.prefill_from_prior(o, wl)
+    B = wl.route.block
+    tok, off = workloads.prompts(wl, wl.n_req, sub=0)
+    n = len(off) - 1
+    r = o.route(tok, off, workloads.initial_loads(wl, wl.route.max_slots), block_keys=True)
+    S = wl.route.max_slots
+    empty = (np.zeros(S + 1, np.int64), np.zeros(0, np.uint64), np.zeros(0, np.uint32),
+             np.zeros(0, np.uint32), np.zeros(0, np.uint32), np.zeros(S, np.int64))
+    q = o.queue_append(empty, off, r["cand"], r["match"], r["chosen"], 0)
+    lens = np.diff(off)
+    coff = np.zeros(n + 1, np.int64)
+    coff[1:] = np.cumsum(lens // B)
+    q2 = o.queue_reprobe(q, coff, r["block_keys"], lens)
+    for a, b in zip(q, q2):
+        assert np.array_equal(a, b)
+    Q = int(q[0][-1])
+    owner = np.searchsorted(q[0], np.arange(Q), side="right") - 1
+    pick = np.arange(0, Q, 3)
+    q = o.queue_migrate(q, q[1][pick], owner[pick].astype(np.uint32), q[3][pick])
+    q2 = o.queue_reprobe(q, coff, r["block_keys"], lens)
+    for a, b in zip(q, q2):
+        assert np.array_equal(a, b)
+    # save some records' chains on their alternatives
+    saved = q[1][::4].astype(np.int64)
+    alt_of = dict(zip(q[1].tolist(), q[3].tolist()))
+    for rid in saved.tolist():
+        o.index_insert(alt_of[rid], r["block_keys"][coff[rid]:coff[rid + 1]])
+    q3 = o.queue_reprobe(q, coff, r["block_keys"], lens)
+    pos = {rid: i for i, rid in enumerate(q[1].tolist())}
+    for rid in saved.tolist():
+        assert q3[4][pos[rid]] == lens[rid] % B
+    # every record, one cached block at a time through the index
+    for i in range(S):
+        for p in range(q3[0][i], q3[0][i + 1]):
+            rid = int(q3[1][p])
+            chain = r["block_keys"][coff[rid]:coff[rid + 1]]
+            for inst, got in ((i, q3[2][p]), (int(q3[3][p]), q3[4][p])):
+                m = 0
+                while m < len(chain) and o.index_contains(inst, int(chain[m])):
+                    m += 1
+                assert got == lens[rid] - B * m
+
+
 def test_queue_drain_hand_values():
     """Base 5 and records of 3, 4, 6 tokens: 10 units serve the base (5),
     the first record (3) and 2 of the second, which keeps 2."""

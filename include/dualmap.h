@@ -266,6 +266,23 @@ dm_status dm_queue_migrate(dm_ctx* ctx, const dm_queues* q, const uint64_t* rec_
 dm_status dm_queue_drain(dm_ctx* ctx, const dm_queues* q, const int64_t* units,
                          const dm_queue_out* out);
 
+/* Queued records re-priced against the caches as they are now (Sec. 3.3;
+ * Sec. A.3.2: each TTFT the rebalancing pass evaluates rests on a KV-cache
+ * query on the record's instance and one on its backup).  Record id r
+ * (< n_ids) has the f1 block-key chain chain_keys[chain_off[r] ..
+ * chain_off[r+1]) (block keys as dm_route_batch emits them; device u64
+ * [n_keys]) and a prompt of prompt_len[r] tokens (device int64 [n_ids];
+ * chain_off device int64 [n_ids + 1]).  out receives q with each record's
+ * unc_here and unc_alt recomputed as prompt_len - B * (leading chain blocks
+ * cached on its instance / on its alternative); order, ids, alternatives
+ * and base work are unchanged.  DM_EINVAL, nothing written, for a queued id
+ * >= n_ids, a chain outside [0, n_keys) or with more blocks than its prompt
+ * holds, a prompt outside [0, 2^32) or an alternative >= max_slots.
+ * Synchronises.  The caches must not change during the call. */
+dm_status dm_queue_reprobe(dm_ctx* ctx, const dm_queues* q, const int64_t* chain_off,
+                           const uint64_t* chain_keys, uint64_t n_keys, const int64_t* prompt_len,
+                           uint64_t n_ids, const dm_queue_out* out);
+
 /* Migration list of dm_rebalance (device arrays of cap entries). */
 typedef struct {
     uint64_t* rec_id;

@@ -27,7 +27,7 @@ EXPORTS = ("dm_create", "dm_destroy", "dm_build_rings", "dm_ring_export", "dm_in
            "dm_index_erase", "dm_index_clear", "dm_index_size", "dm_route_batch",
            "dm_route_batch_noalloc",
            "dm_rebalance", "dm_scale", "dm_set_timing", "dm_route_stage_ms",
-           "dm_kv_save", "dm_queue_append", "dm_queue_migrate", "dm_queue_drain",
+           "dm_kv_save", "dm_queue_append", "dm_queue_migrate", "dm_queue_drain", "dm_queue_reprobe",
            "dm_set_pipelining", "dm_set_policy", "dm_keylen_enable",
            "dm_keylen_window",
            "dm_keylen_export", "dm_sync", "dm_last_error")
@@ -103,6 +103,7 @@ def load_library(path: str = LIB_PATH):
         "dm_queue_append": (i32, [P, P, P, u64, P, u64, P]),
         "dm_queue_migrate": (i32, [P, P, P, P, P, u64, P]),
         "dm_queue_drain": (i32, [P, P, P, P]),
+        "dm_queue_reprobe": (i32, [P, P, P, P, u64, P, u64, P]),
         "dm_keylen_enable": (i32, [P, u64, u64]),
         "dm_keylen_window": (i32, [P]),
         "dm_keylen_export": (i32, [P, P, u64, P]),
@@ -355,6 +356,26 @@ class DualMap:
         qs, qd = self._qstructs(qi, qo, cap)
         self._check(self.lib.dm_queue_drain(self._h, C.byref(qs), _ptr(units), C.byref(qd)),
                     "dm_queue_drain")
+        return self._qtrim(qo)
+
+    def queue_reprobe(self, q, chain_off, chain_keys, prompt_len):
+        """Queued records re-priced against the current caches (see
+        dm_queue_reprobe): record id r's chain chain_keys[chain_off[r]:
+        chain_off[r+1]], its prompt prompt_len[r] tokens."""
+        t = self.torch
+        qi = self._qin(q)
+        chain_off = self._dev(chain_off, t.int64, "chain_off")
+        chain_keys = self._dev(chain_keys, t.uint64, "chain_keys")
+        prompt_len = self._dev(prompt_len, t.int64, "prompt_len")
+        if chain_off.numel() != prompt_len.numel() + 1:
+            raise ValueError("chain_off needs one entry more than prompt_len")
+        cap = qi[1].numel()
+        qo = self._qnew(cap)
+        qs, qd = self._qstructs(qi, qo, cap)
+        self._check(self.lib.dm_queue_reprobe(self._h, C.byref(qs), _ptr(chain_off),
+                                              _ptr(chain_keys), chain_keys.numel(),
+                                              _ptr(prompt_len), prompt_len.numel(), C.byref(qd)),
+                    "dm_queue_reprobe")
         return self._qtrim(qo)
 
     def keylen_enable(self, max_nodes: int, max_window_blocks: int = 1 << 24) -> None:

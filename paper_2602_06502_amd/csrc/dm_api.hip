@@ -467,6 +467,20 @@ dm_status dm_queue_drain(dm_ctx* c, const dm_queues* q, const int64_t* units,
     return queue_drain(c, q, units, out);
 }
 
+dm_status dm_queue_reprobe(dm_ctx* c, const dm_queues* q, const int64_t* chain_off,
+                           const uint64_t* chain_keys, uint64_t n_keys, const int64_t* prompt_len,
+                           uint64_t n_ids, const dm_queue_out* out)
+{
+    if (!c)
+        return DM_EINVAL;
+    if (dm_status s = queue_args(c, q, out, "dm_queue_reprobe"); s != DM_OK)
+        return s;
+    if (!q->alt && out->cap)
+        return fail(c, DM_EINVAL, "dm_queue_reprobe: null alt array");
+    DeviceGuard g(c->device);
+    return queue_reprobe(c, q, chain_off, chain_keys, n_keys, prompt_len, n_ids, out);
+}
+
 dm_status dm_kv_save(dm_ctx* c, const int64_t* offsets, uint64_t n, const uint64_t* block_keys,
                      const uint32_t* inst, uint64_t clock, uint64_t cap, uint64_t* added_host,
                      uint64_t* removed_host)

@@ -322,6 +322,9 @@ dm_status queue_migrate(dm_ctx* c, const dm_queues* q, const uint64_t* mrec,
                         const dm_queue_out* out);
 dm_status queue_drain(dm_ctx* c, const dm_queues* q, const int64_t* units,
                       const dm_queue_out* out);
+dm_status queue_reprobe(dm_ctx* c, const dm_queues* q, const int64_t* coff, const uint64_t* keys,
+                        uint64_t n_keys, const int64_t* plen, uint64_t n_ids,
+                        const dm_queue_out* out);
 
 // dm_probe.hip: candidates on the current rings (cand, fix-up flag bit 3),
 // then requests ordered by their first ring key and grouped (gv).

@@ -365,6 +365,79 @@ __global__ void q_drain_keep_kernel(QIn a, uint32_t S, int64_t Q, const int64_t*
     }
 }
 
+// Re-probe, checks first: every queued record's id has a chain inside the
+// key array that fits its prompt (bad |= 1 otherwise).
+__global__ void q_reprobe_check_kernel(QIn a, uint32_t S, int64_t Q, uint64_t n_ids,
+                                       const int64_t* __restrict__ coff, uint64_t n_keys,
+                                       const int64_t* __restrict__ plen, uint32_t bshift,
+                                       uint32_t* __restrict__ bad)
+{
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < Q;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const uint64_t r = a.rec[q];
+        bool ok = r < n_ids && a.alt[q] < S;
+        if (ok) {
+            const int64_t lo = coff[r], hi = coff[r + 1], len = plen[r];
+            ok = lo >= 0 && hi >= lo && (uint64_t)hi <= n_keys && len >= 0 &&
+                 len < (1ll << 32) && ((hi - lo) << bshift) <= len;
+        }
+        if (!ok)
+            atomicOr(bad, 1u);
+    }
+}
+
+// Leading blocks of chain[0, nb) cached in one table: lane l probes block
+// base + l, the first miss over the wave ends the scan.  Wave-uniform.
+__device__ __forceinline__ int64_t q_cached_blocks(const uint64_t* tab, uint32_t ls,
+                                                   const uint64_t* chain, int64_t nb, int lane)
+{
+    for (int64_t b0 = 0; b0 < nb; b0 += kWave) {
+        const int64_t k = b0 + lane;
+        const bool miss = k < nb && !table_has(tab, ls, canon_key(chain[k]));
+        const uint64_t m = ballot(miss);
+        if (m)
+            return b0 + __builtin_ctzll(m);
+    }
+    return nb;
+}
+
+// One wave per record: its uncached tokens on its instance and on its
+// alternative from the caches as they are now; the rest copied.
+__global__ void __launch_bounds__(256) q_reprobe_kernel(
+    QIn a, uint32_t S, int64_t Q, const int64_t* __restrict__ coff,
+    const uint64_t* __restrict__ keys, const int64_t* __restrict__ plen,
+    const uint64_t* __restrict__ tables, uint32_t ls, uint32_t bshift, QOut b)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t waves = (int64_t)gridDim.x * (blockDim.x / kWave);
+    for (int64_t q = blockIdx.x * (int64_t)(blockDim.x / kWave) + threadIdx.x / kWave; q < Q;
+         q += waves) {
+        const uint32_t i = owner_of(a.qoff, S, q);
+        const uint64_t r = a.rec[q];
+        const uint32_t j = a.alt[q];
+        const int64_t lo = coff[r], nb = coff[r + 1] - lo, len = plen[r];
+        const int64_t mh = q_cached_blocks(tables + ((uint64_t)i << ls), ls, keys + lo, nb, lane);
+        const int64_t ma = q_cached_blocks(tables + ((uint64_t)j << ls), ls, keys + lo, nb, lane);
+        if (lane == 0) {
+            b.rec[q] = r;
+            b.alt[q] = j;
+            b.here[q] = (uint32_t)(len - (mh << bshift));
+            b.there[q] = (uint32_t)(len - (ma << bshift));
+        }
+    }
+}
+
+__global__ void q_copy_offsets_kernel(const int64_t* __restrict__ qoff,
+                                      const int64_t* __restrict__ base, uint32_t S,
+                                      int64_t* __restrict__ qoff2, int64_t* __restrict__ base2)
+{
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i <= S; i += gridDim.x * blockDim.x) {
+        qoff2[i] = qoff[i];
+        if (i < S)
+            base2[i] = base[i];
+    }
+}
+
 hipError_t q_quiesce(dm_ctx* c)
 {
     hipError_t e = join_selection(c);
@@ -608,6 +681,57 @@ dm_status queue_drain(dm_ctx* c, const dm_queues* q, const int64_t* units,
                                                                    popped, npop, b);
     if ((e = hipGetLastError()) != hipSuccess || (e = hipStreamSynchronize(st)) != hipSuccess)
         return hip_fail(c, e, "dm_queue_drain");
+    return DM_OK;
+}
+
+dm_status queue_reprobe(dm_ctx* c, const dm_queues* q, const int64_t* coff, const uint64_t* keys,
+                        uint64_t n_keys, const int64_t* plen, uint64_t n_ids,
+                        const dm_queue_out* out)
+{
+    const uint32_t S = c->cfg.max_slots;
+    hipError_t e = q_quiesce(c);
+    int64_t Q = 0;
+    if (e == hipSuccess && (e = q_count(c, q->qoff, &Q)) == hipErrorInvalidValue)
+        return fail(c, DM_EINVAL, "dm_queue_reprobe: qoff[0] must be 0, fewer than 2^32 records");
+    if (e != hipSuccess)
+        return hip_fail(c, e, "dm_queue_reprobe");
+    if ((uint64_t)Q > out->cap)
+        return fail(c, DM_EFULL, "dm_queue_reprobe: the output holds fewer records than the input");
+    if (Q && (!coff || !plen || !aligned(coff) || !aligned(plen) || (n_keys && !keys) ||
+              (keys && !aligned(keys))))
+        return fail(c, DM_EINVAL, "dm_queue_reprobe: null or misaligned chain arrays");
+    hipStream_t st = c->stream;
+    uint32_t* bad = static_cast<uint32_t*>(scratch_get(c, kSlotMembers, 256, &e));
+    if (!bad)
+        return hip_fail(c, e, "dm_queue_reprobe");
+    uint32_t bshift = 0;
+    while ((1u << bshift) < c->cfg.block_size)
+        bshift++;
+    q_zero_kernel<<<1, 64, 0, st>>>(reinterpret_cast<unsigned long long*>(bad), 1);
+    q_check_kernel<<<grid_for(S + 1, 256), 256, 0, st>>>(q->qoff, S, Q, nullptr, nullptr, bad);
+    const QIn a{q->qoff, q->rec_id, q->unc_here, q->alt, q->unc_alt};
+    if (Q)
+        q_reprobe_check_kernel<<<grid_for(Q, 256, 8192), 256, 0, st>>>(a, S, Q, n_ids, coff, n_keys,
+                                                                       plen, bshift, bad);
+    uint32_t badh = 0;
+    if ((e = hipMemcpyAsync(&badh, bad, 4, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+        (e = hipStreamSynchronize(st)) != hipSuccess)
+        return hip_fail(c, e, "dm_queue_reprobe");
+    if (badh & 4)
+        return fail(c, DM_EINVAL, "dm_queue_reprobe: queue offsets out of order or range");
+    if (badh)
+        return fail(c, DM_EINVAL, "dm_queue_reprobe: a record id without a chain, a chain outside "
+                                  "the key array or longer than its prompt, a prompt outside "
+                                  "[0, 2^32), or an alternative >= max_slots");
+    q_copy_offsets_kernel<<<grid_for(S + 1, 256), 256, 0, st>>>(q->qoff, q->base_work, S,
+                                                                out->qoff, out->base_work);
+    const QOut b{out->qoff, out->rec_id, out->unc_here, out->alt, out->unc_alt};
+    if (Q)
+        q_reprobe_kernel<<<grid_for(Q, 4, 8192), 256, 0, st>>>(a, S, Q, coff, keys, plen,
+                                                               c->d_tables, c->cfg.index_log2_slots,
+                                                               bshift, b);
+    if ((e = hipGetLastError()) != hipSuccess || (e = hipStreamSynchronize(st)) != hipSuccess)
+        return hip_fail(c, e, "dm_queue_reprobe");
     return DM_OK;
 }
 

@@ -288,6 +288,9 @@ def run_agent(side, cfg, mu: int, n_batches: int, warm: bool = True):
         # Sec. A.7): a few instances' queued work jumps to hot_factor x mu
         hot = workloads.agent_hot_instances(cfg, b)
         qs.base[hot] += (cfg.hot_factor - 1) * mu
+        if getattr(side, "reprobe", False):
+            # queued records re-priced against the caches as they are now
+            qs.reprobe()
         queued = qs.count() if getattr(side, "queues_on_side", False) else sum(len(x) for x in qs.q)
         mg = side.rebalance(qs.csr())
         mg["queued"] = queued

@@ -46,6 +46,15 @@ class OracleQueues:
         self.q = (np.zeros(S + 1, np.int64), np.zeros(0, np.uint64), np.zeros(0, np.uint32),
                   np.zeros(0, np.uint32), np.zeros(0, np.uint32), np.asarray(base, np.int64))
         self.last = None
+        # chain store by record id: block keys, offsets, prompt lengths
+        self.coff, self.keys, self.plen = [0], [], []
+        self.B = o.block
+
+    def _store(self, off, bk):
+        lens = np.diff(np.asarray(off, np.int64))
+        self.coff += (self.coff[-1] + np.cumsum(lens // self.B)).tolist()
+        self.plen += lens.tolist()
+        self.keys.append(np.asarray(bk)[: int((lens // self.B).sum())])
 
     @property
     def base(self):
@@ -59,7 +68,13 @@ class OracleQueues:
 
     def append_routed(self, off, rec_base):
         r = self.last
+        assert rec_base == len(self.plen)
         self.q = self.o.queue_append(self.q, off, r["cand"], r["match"], r["chosen"], rec_base)
+        self._store(off, r["block_keys"])
+
+    def reprobe(self):
+        self.q = self.o.queue_reprobe(self.q, np.array(self.coff, np.int64),
+                                      np.concatenate(self.keys), np.array(self.plen, np.int64))
 
     def count(self):
         return int(self.q[0][-1])
@@ -108,6 +123,9 @@ class EngineQueues(OracleQueues):
                   d(np.zeros(0, np.uint32)), d(np.zeros(0, np.uint32)), d(np.zeros(0, np.uint32)),
                   d(np.asarray(base, np.int64)))
         self.last = None
+        self.coff, self.keys, self.plen = [0], [], []
+        self.B = side.eng.block
+        self.dkeys = None
 
     def loads(self):
         qoff, rec, here, alt, there, base = self.q
@@ -118,8 +136,18 @@ class EngineQueues(OracleQueues):
         return L.cpu().numpy()
 
     def append_routed(self, off, rec_base):
+        assert rec_base == len(self.plen)
         self.q = self.side.eng.queue_append(self.q, self.side._d(np.asarray(off, np.int64)),
                                             self.side._dev_out, rec_base)
+        nb = int((np.diff(np.asarray(off, np.int64)) // self.B).sum())
+        bk = self.side._dev_out["block_keys"][:nb]
+        self.dkeys = bk.clone() if self.dkeys is None else torch.cat([self.dkeys, bk])
+        self._store(off, np.zeros(0, np.uint64))
+
+    def reprobe(self):
+        d = self.side._d
+        self.q = self.side.eng.queue_reprobe(self.q, d(np.array(self.coff, np.int64)), self.dkeys,
+                                             d(np.array(self.plen, np.int64)))
 
     def count(self):
         return int(self.q[0][-1].item())
@@ -369,15 +397,17 @@ def test_agent_multibatch_device_kv_save_parity():
 
 def test_agent_multibatch_device_resident_parity():
     """The agent workload with its serving state on each side: queues kept
-    by the queue operations (routed batches appended, migration lists
-    applied, service drained: dm_queue_* on the GPU, or_queue_* in the
+    by the queue operations (routed batches appended, records re-priced
+    against the current caches before each rebalancing pass, migration
+    lists applied, service drained: dm_queue_* on the GPU, or_queue_* in the
     oracle) and caches by the KV save; every routed batch and rebalancing
-    pass compared, and the queues themselves at the end."""
+    pass compared."""
     _gpu()
     cfg = workloads.agent()
     rc = cfg.route
     gs = EngineSide(rc, kv_on_side=True, queues_on_side=True)
     os_ = OracleSide(rc, kv_on_side=True, queues_on_side=True)
+    gs.reprobe = os_.reprobe = True
     migrated = 0
     for x, y in itertools.zip_longest(sim.run_agent(gs, cfg, cfg.mu, 6),
                                       sim.run_agent(os_, cfg, cfg.mu, 6)):

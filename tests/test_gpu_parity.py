@@ -481,6 +481,81 @@ def test_queue_operations_errors():
     assert cpu(g[2]).tolist() == [3, 8] and cpu(g[3]).tolist() == [1, 0]
 
 
+def test_queue_reprobe_parity_and_errors():
+    """Queues built from routed batches over long hot templates (chains past
+    several 64-block chunks); between batches the served chains are saved on
+    the chosen instances and some on the alternatives, so queued records'
+    cached prefixes change; the re-probed queues against the oracle's after
+    every batch and after a migration; then bad chain stores."""
+    gh = _h()
+    import paper_2602_06502_amd as pk
+    B, K = 16, 2
+    wl = workloads.small_random(98, 8, 8, B, 8, key_blocks=K)
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    S = wl.route.max_slots
+    d = lambda a: gh.to_dev(a, eng.device)
+    rng = np.random.default_rng(77)
+    L = workloads.initial_loads(wl, S)
+    qo = (np.zeros(S + 1, np.int64), np.zeros(0, np.uint64), np.zeros(0, np.uint32),
+          np.zeros(0, np.uint32), np.zeros(0, np.uint32), np.zeros(S, np.int64))
+    qg = tuple(d(x) for x in qo)
+    coff, keys, plen = [0], [], []
+    for i, (tok, off) in enumerate(_hot_batches(98, B, K, 4, tlen_blocks=(1, 200))):
+        n = len(off) - 1
+        _say("reprobe batch", i, "requests", n)
+        g = eng.route(d(tok), d(off), d(L), block_keys=True)
+        eng.sync()
+        r = o.route(tok, off, L, block_keys=True)
+        compare_route(g, r, n, with_bk=True)
+        L = r["loads"]
+        rb = len(plen)
+        qg = eng.queue_append(qg, d(off), g, rb)
+        qo = o.queue_append(qo, off, r["cand"], r["match"], r["chosen"], rb)
+        _q_eq(qg, qo, "append")
+        lens = np.diff(off)
+        nf = lens // B
+        coff += (coff[-1] + np.cumsum(nf)).tolist()
+        keys.append(r["block_keys"])
+        plen += lens.tolist()
+        bo = np.concatenate([[0], np.cumsum(nf)])
+        # served chains saved on the chosen instance, a third also on the other
+        other = np.where(r["chosen"] == r["cand"][:n], r["cand"][n:], r["cand"][:n])
+        extra = rng.random(n) < 0.33
+        for c in range(S):
+            for sel in (r["chosen"] == c, (other == c) & extra):
+                ks = [r["block_keys"][bo[j]:bo[j + 1]] for j in np.nonzero(sel)[0]]
+                if ks:
+                    kk = np.concatenate(ks)
+                    eng.index_insert(c, d(kk))
+                    o.index_insert(c, kk)
+        K_all = np.concatenate(keys)
+        co, pl = np.array(coff, np.int64), np.array(plen, np.int64)
+        qg = eng.queue_reprobe(qg, d(co), d(K_all), d(pl))
+        qo = o.queue_reprobe(qo, co, K_all, pl)
+        _q_eq(qg, qo, "reprobe")
+        Q = int(qo[0][-1])
+        pick = rng.choice(Q, size=Q // 5, replace=False)
+        owner = np.searchsorted(qo[0], np.arange(Q), side="right") - 1
+        mrec, msrc, mdst = qo[1][pick], owner[pick].astype(np.uint32), qo[3][pick]
+        qg = eng.queue_migrate(qg, d(mrec), d(msrc), d(mdst))
+        qo = o.queue_migrate(qo, mrec, msrc, mdst)
+        qg = eng.queue_reprobe(qg, d(co), d(K_all), d(pl))
+        qo = o.queue_reprobe(qo, co, K_all, pl)
+        _q_eq(qg, qo, "reprobe after migrate")
+    assert max(np.diff(co)) > 128
+    bad = [
+        (co[:-1], pl[:-1]),                       # the last id has no chain
+        (co, np.where(np.diff(co) > 0, B * np.diff(co) - 1, pl)),  # chains longer than prompts
+        (co + 1, pl),                             # the last chain runs past the keys
+    ]
+    for j, (c2, p2) in enumerate(bad):
+        _say("reprobe error case", j)
+        with pytest.raises(pk.DMError) as ei:
+            eng.queue_reprobe(qg, d(np.asarray(c2, np.int64)), d(K_all),
+                              d(np.asarray(p2, np.int64)))
+        assert ei.value.status == pk.DM_EINVAL, j
+
+
 def _disjoint_pair_prompts(o, rng, n_pool):
     """Random prompts whose candidate pairs are pairwise disjoint (greedy
     over a pool), found with the oracle's ring keys and candidates."""

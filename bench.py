@@ -298,10 +298,73 @@ def config_rows(reps):
                               "parity": bool(orc == 0 and (oa, orm) == ga),
                               "note": "host clock of one dm_kv_save of the routed batch on the "
                                       "chosen instances, LRU bound 200,000 blocks per instance"}
+            row["queue_ops"] = queue_ops_row(eng, o["oracle"], g, ob, n, nb, base, cfg)
         rows[name] = row
         del eng, g, o, out
         torch.cuda.empty_cache()
     return rows
+
+
+def queue_ops_row(eng, orc, g, ob, n, nb, base, cfg):
+    """The agent batch's serving state kept on the device: the routed batch
+    appended to queues over the stalled base work, re-priced against the
+    caches after its KV save, a rebalancing pass over those queues, its
+    migration list applied, then 2 ms of service.  Host clock of the second
+    of two identical calls (each synchronises), the oracle's beside it,
+    and whether the queues matched after every step."""
+    import numpy as np
+    import torch
+
+    import paper_2602_06502_amd.harness as gh
+    d = lambda a: gh.to_dev(a, eng.device)
+    S = len(base)
+    cpu = {k: v.cpu().numpy() for k, v in ob.items()}
+    offs = g["offsets_np"]
+    lens = np.diff(offs)
+    coff = np.zeros(n + 1, np.int64)
+    coff[1:] = np.cumsum(lens // cfg.route.block)
+    bk = cpu["block_keys"][:nb]
+    empty = (np.zeros(S + 1, np.int64), np.zeros(0, np.uint64), np.zeros(0, np.uint32),
+             np.zeros(0, np.uint32), np.zeros(0, np.uint32), base)
+    res, same = {}, True
+
+    def step(name, fg, fo):
+        nonlocal same
+        fg()  # warm-up: the library's scratch grows once
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        qg = fg()
+        t1 = time.perf_counter()
+        qo = fo()
+        t2 = time.perf_counter()
+        ok = all(np.array_equal(a.cpu().numpy(), b) for a, b in zip(qg, qo))
+        same = same and ok
+        res[name] = {"gpu_ms": 1000.0 * (t1 - t0), "oracle_ms": 1000.0 * (t2 - t1),
+                     "records": int(qo[0][-1]), "parity": bool(ok)}
+        return qg, qo
+
+    qg, qo = step("append", lambda: eng.queue_append(tuple(d(x) for x in empty), g["offsets"], ob, 0),
+                  lambda: orc.queue_append(empty, offs, cpu["cand"], cpu["match"], cpu["chosen"], 0))
+    dco, dpl = d(coff), d(lens.astype(np.int64))
+    qg, qo = step("reprobe", lambda: eng.queue_reprobe(qg, dco, ob["block_keys"][:nb], dpl),
+                  lambda: orc.queue_reprobe(qo, coff, bk, lens))
+    m = eng.rebalance(*qg)
+    eng.sync()
+    cnt = int(m["count"].cpu()[0])
+    mr, ms_, md = m["rec"][:cnt], m["src"][:cnt], m["dst"][:cnt]
+    qg, qo = step("migrate", lambda: eng.queue_migrate(qg, mr, ms_, md),
+                  lambda: orc.queue_migrate(qo, mr.cpu().numpy(), ms_.cpu().numpy(),
+                                            md.cpu().numpy()))
+    units = np.zeros(S, np.int64)
+    units[:cfg.route.n_inst] = int(cfg.drain_per_us * 2000)
+    qg, qo = step("drain", lambda: eng.queue_drain(qg, d(units)),
+                  lambda: orc.queue_drain(qo, units))
+    res["migrations"] = cnt
+    res["parity"] = bool(same)
+    res["note"] = ("host clock per call; queues of the routed batch over the stalled base work, "
+                   "re-priced after the batch's KV save, the rebalancing pass's migrations "
+                   "applied, 2 ms of service drained")
+    return res
 
 
 def policy_rows(eng, wl, st, L0):

@@ -510,7 +510,7 @@ __device__ __forceinline__ uint32_t cmp_lim(const RecRegs& m)
 // chunk, the next request's first chunk (its record is loaded a request
 // ahead), when a wave has more than one request.  (Persistent waves claiming
 // blocks of requests through per-XCD counters were measured 13% slower.)
-template <int B>
+template <int B, bool MULTI>
 __global__ __launch_bounds__(kHashThreads) void member_kernel(HashArgs a)
 {
     const int lane = lane_id();
@@ -540,7 +540,7 @@ __global__ __launch_bounds__(kHashThreads) void member_kernel(HashArgs a)
     while (have) {
         // this request, then the wave's next one and its record
         const uint64_t rc = r, rn = r + nw;
-        const bool have_n = rn < a.n;
+        const bool have_n = MULTI && rn < a.n;  // a grid of one request per wave has none
         RecRegs nxt{};
         if (have_n)
             nxt = load_rec(a.rec, rn);
@@ -678,8 +678,13 @@ hipError_t launch_walk(dm_ctx* c, const HashArgs& a, uint32_t grid)
 template <int B>
 hipError_t launch_members_b(dm_ctx* c, const HashArgs& a)
 {
-    member_kernel<B><<<grid_for(a.n, kHashThreads / kWave, kHashBlocks), kHashThreads, 0,
-                       c->stream>>>(a);
+    // one request per wave (the register-lean form, 8 waves per SIMD) unless
+    // the batch outnumbers the grid
+    const uint32_t grid = grid_for(a.n, kHashThreads / kWave, kHashBlocks);
+    if ((uint64_t)grid * (kHashThreads / kWave) < a.n)
+        member_kernel<B, true><<<grid, kHashThreads, 0, c->stream>>>(a);
+    else
+        member_kernel<B, false><<<grid, kHashThreads, 0, c->stream>>>(a);
     return hipGetLastError();
 }
 

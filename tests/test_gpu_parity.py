@@ -777,6 +777,37 @@ def test_batch_sizes_around_chunks_and_blocks_parity():
         assert np.array_equal(cpu(Ld), r["loads"]), k
 
 
+def test_batch_beyond_one_request_per_wave_parity():
+    """More requests than the hashing passes' grid has waves (4 Mi): waves
+    then take several requests each (the members pass loads the next
+    request's record and first chunk ahead).  A 3,000-prompt stream, cut to
+    at most 40 tokens, repeated past 4 Mi requests, so groups are large and
+    members share their leader's prefix."""
+    gh = _h()
+    wl = workloads.small_random(43, 8, 4, 16, 3000)
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    gh.prefill_from_prior(eng, wl)
+    oh.prefill_from_prior(o, wl)
+    tok, off = workloads.prompts(wl, wl.n_req, sub=0)
+    lens = np.minimum(np.diff(off), 40)
+    base = np.concatenate([tok[off[i]:off[i] + lens[i]] for i in range(len(lens))])
+    n = (1 << 22) + 1234
+    reps = -(-n // len(lens))
+    L_all = np.tile(lens, reps)[:n]
+    off_big = np.zeros(n + 1, np.int64)
+    off_big[1:] = np.cumsum(L_all)
+    tok_big = np.tile(base, reps)[:off_big[-1]]
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    _say("route", n, "requests", len(tok_big), "tokens")
+    Ld = gh.to_dev(L0, eng.device)
+    g = eng.route(gh.to_dev(tok_big, eng.device), gh.to_dev(off_big, eng.device), Ld,
+                  block_keys=True)
+    eng.sync()
+    r = o.route(tok_big, off_big, L0, block_keys=True)
+    compare_route(g, r, n, with_bk=True)
+    assert np.array_equal(cpu(Ld), r["loads"])
+
+
 def test_index_ops_and_capacity():
     gh = _h()
     import paper_2602_06502_amd as pk

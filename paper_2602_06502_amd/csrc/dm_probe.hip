@@ -75,41 +75,57 @@ __global__ void group_head_kernel(const uint64_t* __restrict__ skeys,
 
 // Leader of each group (a head at i leads group gpos[i]): the longest
 // request among the group's positions [i, i + 64), ties to the earliest.
-// Positions are examined 16 at a time, their loads issued together.
-__global__ void group_leader_kernel(const uint32_t* __restrict__ order, uint64_t m,
-                                    const uint64_t* __restrict__ head,
-                                    const uint32_t* __restrict__ len,
-                                    const uint64_t* __restrict__ gpos,
-                                    uint32_t* __restrict__ leader)
+// One wave per 64 positions holds positions [64w, 64w + 128), two per lane,
+// as (full blocks << 32 | ~position) so that the larger value is the longer
+// and then earlier request.  A segmented suffix maximum by doubling over
+// both halves (each lane's span doubles six times, to 64 positions, and
+// stops at the next head) gives every head lane of the first half its
+// leader; positions past the list act as heads.
+__global__ __launch_bounds__(256) void group_leader_kernel(const uint32_t* __restrict__ order,
+                                                           uint64_t m,
+                                                           const uint64_t* __restrict__ head,
+                                                           const uint32_t* __restrict__ len,
+                                                           const uint64_t* __restrict__ gpos,
+                                                           uint32_t* __restrict__ leader)
 {
-    constexpr int kBatch = 16;
-    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < m;
-         i += (uint64_t)gridDim.x * blockDim.x) {
-        if (!head[i])
-            continue;
-        uint64_t best = i;
-        uint32_t blen = len[i];
-        bool open = true;  // no later head seen yet
-        for (uint64_t j0 = i + 1; open && j0 < i + kWave && j0 < m; j0 += kBatch) {
-            bool in[kBatch];
-            uint32_t l[kBatch];
+    const int lane = lane_id();
+    const uint64_t waves = (m + kWave - 1) / kWave;
+    const uint64_t nw = ((uint64_t)gridDim.x * blockDim.x) / kWave;
+    for (uint64_t w = ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave; w < waves;
+         w += nw) {
+        const uint64_t i0 = w * kWave + lane, i1 = i0 + kWave;
+        const bool h0 = i0 >= m || head[i0] != 0, h1 = i1 >= m || head[i1] != 0;
+        uint64_t v0 = i0 < m ? ((uint64_t)len[i0] << 32) | (uint32_t)~(uint32_t)i0 : 0;
+        uint64_t v1 = i1 < m ? ((uint64_t)len[i1] << 32) | (uint32_t)~(uint32_t)i1 : 0;
+        const uint64_t H0 = ballot(h0), H1 = ballot(h1);
+        // done: this lane's span already ends at a head (or the window end)
+        bool done0 = lane < kWave - 1 ? (H0 >> (lane + 1)) & 1 : H1 & 1;
+        bool done1 = lane < kWave - 1 ? (H1 >> (lane + 1)) & 1 : true;
 #pragma unroll
-            for (int k = 0; k < kBatch; k++) {
-                const uint64_t j = j0 + k;
-                const bool ok = j < m && j < i + kWave;
-                in[k] = ok && !head[ok ? j : i];
-                l[k] = ok ? len[j] : 0;
+        for (int d = 1; d < kWave; d <<= 1) {
+            const int src = (lane + d) & (kWave - 1);
+            const bool hi = lane + d >= kWave;  // partner in the second half
+            const uint64_t a0 = shfl_u64(v0, src), a1 = shfl_u64(v1, src);
+            const uint64_t D0 = ballot(done0), D1 = ballot(done1);
+            const uint64_t p0 = hi ? a1 : a0;
+            const bool pd0 = hi ? (D1 >> src) & 1 : (D0 >> src) & 1;
+            if (!done0) {
+                v0 = v0 > p0 ? v0 : p0;
+                done0 = pd0;
             }
-#pragma unroll
-            for (int k = 0; k < kBatch; k++) {
-                open = open && in[k];
-                if (open && l[k] > blen) {
-                    blen = l[k];
-                    best = j0 + k;
+            if (!done1) {
+                if (hi) {
+                    done1 = true;
+                } else {
+                    v1 = v1 > a1 ? v1 : a1;
+                    done1 = (D1 >> src) & 1;
                 }
             }
         }
-        leader[gpos[i]] = order[best];
+        if (i0 < m && h0) {
+            const uint64_t best = (uint32_t)~(uint32_t)v0;
+            leader[gpos[i0]] = order[best];
+        }
     }
 }
 
@@ -189,8 +205,8 @@ hipError_t lookup_group(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64
                                                               g.head, g.len);
     if ((e = exclusive_scan_u64(c, g.head, n, g.gpos, g.groups)) != hipSuccess)
         return e;
-    group_leader_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(g.order, n, g.head, g.len, g.gpos,
-                                                                g.leader);
+    group_leader_kernel<<<grid_for((n + kWave - 1) / kWave, 256 / kWave, 8192), 256, 0, st>>>(
+        g.order, n, g.head, g.len, g.gpos, g.leader);
     group_of_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(g.order, n, g.head, g.gpos,
                                                             g.group_of);
     *gv = GroupView{g.group_of, g.leader, g.groups};

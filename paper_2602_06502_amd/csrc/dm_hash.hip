@@ -501,7 +501,8 @@ __device__ __forceinline__ uint32_t cmp_lim(const RecRegs& m)
 // first disagreement s.  Per candidate, the leader's match where it ends
 // before s, the request's length where s reaches it, or pending: the
 // request's keys of blocks [s, s + 8) are kept in pkeys (8 per request) and
-// pend[r] = s | side mask << 32 for probe_pending_kernel.  Probing is left
+// pend[r] = s | side mask << 32 for probe_pending_kernel (0 for leaders and
+// requests with nothing pending).  Probing is left
 // out of this pass: its latency would hold the wave with no tokens in
 // flight.
 //
@@ -611,10 +612,12 @@ __global__ __launch_bounds__(kHashThreads) void member_kernel(HashArgs a)
             load_chunk<B>(nx, a.tokens + nxt.o0, (uint64_t)lane, (uint64_t)lane < nxt.nfull);
             nlk = (uint32_t)lane < cmp_lim(nxt) ? a.hkeys[nxt.bs_lead + lane] : 0;
         }
-        if (lane == 0 && !lead) {
-            a.match[rc] = m0;
-            a.match[a.n + rc] = m1;
-            a.pend[rc] = s | ((uint64_t)mask << 32);
+        if (lane == 0) {
+            if (!lead) {
+                a.match[rc] = m0;
+                a.match[a.n + rc] = m1;
+            }
+            a.pend[rc] = s | ((uint64_t)mask << 32);  // 0 for a leader
         }
         r = rn;
         cur = nxt;
@@ -636,9 +639,7 @@ __global__ void probe_pending_kernel(uint64_t n, const uint64_t* __restrict__ pe
 {
     for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
          r += (uint64_t)gridDim.x * blockDim.x) {
-        if (rec[r].lim == kLeaderMark)
-            continue;
-        const uint64_t p = pend[r];
+        const uint64_t p = pend[r];  // nothing pending for leaders
         const uint32_t mask = (uint32_t)(p >> 32);
         if (!mask)
             continue;

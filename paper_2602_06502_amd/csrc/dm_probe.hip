@@ -1,7 +1,8 @@
 // Candidates and request groups (Sec. 3.2; Sec. A.1.1).
 //
 // lookup_kernel: one thread per request finds the owners of its two ring
-//   keys and applies the distinct-candidate adjustment.
+//   keys and applies the distinct-candidate adjustment (and writes the
+//   ordering's sort input).
 // Then requests are ordered by the top 16 bits of their first ring key
 // (stable radix sort) and grouped: a group is a maximal run of the order
 // with equal first ring keys, so its requests have the same first
@@ -20,14 +21,21 @@ namespace {
 
 constexpr int kOrderBits = 16;  // top bits of the first ring key used for ordering
 
-__global__ void lookup_kernel(uint64_t n, uint64_t q0, uint64_t q1, const uint64_t* __restrict__ key,
-                              RingView r1, RingView r2, const uint32_t* __restrict__ next_live,
+__global__ void lookup_kernel(uint64_t n, const uint64_t* __restrict__ key, RingView r1,
+                              RingView r2, const uint32_t* __restrict__ next_live,
                               uint32_t n_live, uint32_t* __restrict__ cand,
-                              uint8_t* __restrict__ flags)
+                              uint8_t* __restrict__ flags, uint64_t* __restrict__ skeys,
+                              uint32_t* __restrict__ svals)
 {
-    for (uint64_t r = q0 + blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < q1;
+    for (uint64_t r = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; r < n;
          r += (uint64_t)gridDim.x * blockDim.x) {
-        const uint32_t c1 = ring_owner(r1, key[r]);
+        const uint64_t x = key[r];
+        // the ordering's sort input: the first ring key rotated so that its
+        // top kOrderBits bits are the low ones the sort orders by (the sort
+        // carries the whole key along), and the request
+        skeys[r] = (x << kOrderBits) | (x >> (64 - kOrderBits));
+        svals[r] = (uint32_t)r;
+        const uint32_t c1 = ring_owner(r1, x);
         uint32_t c2 = ring_owner(r2, key[n + r]);
         uint8_t f = 0;
         if (c2 == c1) {
@@ -37,20 +45,6 @@ __global__ void lookup_kernel(uint64_t n, uint64_t q0, uint64_t q1, const uint64
         cand[r] = c1;
         cand[n + r] = c2;
         flags[r] = f;
-    }
-}
-
-// keys[i] = request r0 + i's first ring key rotated so that its top
-// kOrderBits bits are the low ones the sort orders by (the sort carries the
-// whole key along); vals[i] = r0 + i.
-__global__ void order_init_kernel(const uint64_t* __restrict__ key, uint64_t r0, uint64_t m,
-                                  uint64_t* __restrict__ keys, uint32_t* __restrict__ vals)
-{
-    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < m;
-         i += (uint64_t)gridDim.x * blockDim.x) {
-        const uint64_t x = key[r0 + i];
-        keys[i] = (x << kOrderBits) | (x >> (64 - kOrderBits));
-        vals[i] = (uint32_t)(r0 + i);
     }
 }
 
@@ -188,17 +182,16 @@ hipError_t lookup_group(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64
         return hipSuccess;
     if (n > 0xFFFFFFFFull)
         return hipErrorInvalidValue;
-    lookup_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(
-        n, 0, n, key, view(c->ring[c->cur][0]), view(c->ring[c->cur][1]), c->d_next_live,
-        c->n_live, cand, flags);
     uint8_t* w = static_cast<uint8_t*>(scratch_get(c, kSlotProbe, probe_scratch_bytes(n), &e));
     if (!w)
         return e;
     GroupWork g;
     group_layout(n, w, &g);
+    lookup_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(
+        n, key, view(c->ring[c->cur][0]), view(c->ring[c->cur][1]), c->d_next_live, c->n_live,
+        cand, flags, g.keys, g.order);
     g.len = g.vtmp;  // the sort's spare value array is free once it has run
     // requests ordered by the top bits of their first ring key (stable radix sort)
-    order_init_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(key, 0, n, g.keys, g.order);
     if ((e = radix_sort_kv(c, g.keys, g.order, g.ktmp, g.vtmp, n, kOrderBits)) != hipSuccess)
         return e;
     group_head_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(g.keys, g.order, n, bstart, bad,

@@ -682,7 +682,7 @@ def main():
                                      "select": ref_stage[2], "block_offsets": ref_stage[3]}},
         "roofline": {"bound": "hbm",
                      "kernel": "hash+match stage: ring_key_kernel<16>, lookup_kernel, "
-                               "order_init_kernel, radix sort passes, group_head_kernel, "
+                               "radix sort passes, group_head_kernel, "
                                "group scan, group_leader_kernel, group_of_kernel, "
                                "walk_kernel<16> (leaders, resume), member_record_kernel, "
                                "member_kernel<16>, probe_pending_kernel",

@@ -187,7 +187,7 @@ dm_status dm_route_batch(dm_ctx* ctx, const int32_t* tokens, uint64_t n_tokens,
  * static area of 64 MiB per GPU that the library holds until the process
  * ends, instead of the context's growable scratch: the call allocates and
  * frees nothing.  The batch is planned on the host first; if its work
- * arrays do not fit (about 330 bytes per request plus, when block_keys is
+ * arrays do not fit (about 360 bytes per request plus, when block_keys is
  * NULL, 8 bytes per n_tokens / B), the call returns DM_EINVAL with the
  * sizes in dm_last_error and launches nothing.  Runs unpipelined on the
  * context's stream (after any pipelined batch).  Every call on one GPU

@@ -108,6 +108,10 @@ struct HashArgs {
     unsigned long long* ext_count;
     const unsigned long long* ext_count_in;
     uint32_t* key_len;            // [n] or null
+    // f1 digests NH(j) of blocks j < min(K, full blocks), [n * key_blocks]:
+    // written by the prefix pass so that the members pass need not read
+    // those tokens again (null: not kept)
+    uint64_t* nh0;
 };
 
 // Index of this wave in the grid, in a scalar register: the compiler cannot
@@ -177,6 +181,8 @@ __global__ __launch_bounds__(kHashThreads) void ring_key_kernel(HashArgs a, uint
         uint64_t nh1 = 0, nh2 = 0;
         if (j < kr)
             nh_block2<B>(a.tokens + o0 + (uint64_t)j * B, k1, k2, nh1, nh2);
+        if (a.nh0 && j < kr)
+            a.nh0[r * a.key_blocks + j] = nh1;
         uint64_t s1 = nh1 * q1, s2 = nh2 * q2;
         for (uint32_t d = 1; d < g; d <<= 1) {
             s1 += shfl_xor_u64(s1, (int)d);
@@ -531,12 +537,18 @@ __global__ __launch_bounds__(kHashThreads) void member_kernel(HashArgs a)
     RecRegs cur{};
     if (have)
         cur = load_rec(a.rec, r);
+    // blocks whose f1 digests the prefix pass kept (their tokens are not
+    // read again)
+    const uint64_t K = a.key_blocks;
+    auto kept = [&](uint64_t nfull) -> uint64_t { return a.nh0 ? (nfull < K ? nfull : K) : 0; };
     ChunkTokens<B> nx;
-    uint64_t nlk = 0;
+    uint64_t nlk = 0, pnh = 0;
     {
-        const bool v = have && (uint64_t)lane < cur.nfull;
+        const uint64_t kp = have ? kept(cur.nfull) : 0;
+        const bool v = have && (uint64_t)lane < cur.nfull && (uint64_t)lane >= kp;
         load_chunk<B>(nx, a.tokens + cur.o0, (uint64_t)lane, v);
         nlk = have && (uint32_t)lane < cmp_lim(cur) ? a.hkeys[cur.bs_lead + lane] : 0;
+        pnh = (uint64_t)lane < kp ? a.nh0[r * K + lane] : 0;
     }
     while (have) {
         // this request, then the wave's next one and its record
@@ -546,7 +558,9 @@ __global__ __launch_bounds__(kHashThreads) void member_kernel(HashArgs a)
         if (have_n)
             nxt = load_rec(a.rec, rn);
         const bool lead = cur.lim == kLeaderMark;
-        const uint64_t nfull = cur.nfull, lim = cmp_lim(cur);
+        const uint64_t nfull = cur.nfull, lim = cmp_lim(cur), kp = kept(nfull);
+        const uint64_t pre = pnh;
+        uint64_t pnh_n = 0;
         const int32_t* tp = a.tokens + cur.o0;
         const uint64_t* lk = a.hkeys + cur.bs_lead;
         uint64_t* hk = a.hkeys + cur.bs;
@@ -583,10 +597,13 @@ __global__ __launch_bounds__(kHashThreads) void member_kernel(HashArgs a)
                 load_chunk<B>(nx, tp, b2, b2 < nfull);
                 nlk = cmp && b2 < lim ? lk[b2] : 0;
             } else if (have_n) {
-                load_chunk<B>(nx, a.tokens + nxt.o0, (uint64_t)lane, (uint64_t)lane < nxt.nfull);
+                const uint64_t kn = kept(nxt.nfull);
+                load_chunk<B>(nx, a.tokens + nxt.o0, (uint64_t)lane,
+                              (uint64_t)lane < nxt.nfull && (uint64_t)lane >= kn);
                 nlk = (uint32_t)lane < cmp_lim(nxt) ? a.hkeys[nxt.bs_lead + lane] : 0;
+                pnh_n = (uint64_t)lane < kn ? a.nh0[rn * K + lane] : 0;
             }
-            const uint64_t nh1 = valid ? nh_regs<B>(tc, k1) : 0;
+            const uint64_t nh1 = valid ? (b < kp ? pre : nh_regs<B>(tc, k1)) : 0;
             const uint64_t S = wave_incl_sum_u64(nh1 * q1, lane);
             const uint64_t H = (G + S) * p1;
             const uint64_t h = mix64(H ^ seed1);
@@ -609,8 +626,11 @@ __global__ __launch_bounds__(kHashThreads) void member_kernel(HashArgs a)
         }
         if (nfull == 0 && have_n) {
             // nothing of the next request was loaded ahead yet
-            load_chunk<B>(nx, a.tokens + nxt.o0, (uint64_t)lane, (uint64_t)lane < nxt.nfull);
+            const uint64_t kn = kept(nxt.nfull);
+            load_chunk<B>(nx, a.tokens + nxt.o0, (uint64_t)lane,
+                          (uint64_t)lane < nxt.nfull && (uint64_t)lane >= kn);
             nlk = (uint32_t)lane < cmp_lim(nxt) ? a.hkeys[nxt.bs_lead + lane] : 0;
+            pnh_n = (uint64_t)lane < kn ? a.nh0[rn * K + lane] : 0;
         }
         if (lane == 0) {
             if (!lead) {
@@ -621,6 +641,7 @@ __global__ __launch_bounds__(kHashThreads) void member_kernel(HashArgs a)
         }
         r = rn;
         cur = nxt;
+        pnh = pnh_n;
         have = have_n;
     }
 }
@@ -762,9 +783,10 @@ static void tree_args(dm_ctx* c, HashArgs& a)
 
 hipError_t hash_prefix(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
                        const uint32_t* bad, uint64_t* key_out, uint32_t* key_len,
-                       uint32_t* ext_list, unsigned long long* ext_count)
+                       uint32_t* ext_list, unsigned long long* ext_count, uint64_t* nh0)
 {
     HashArgs a = base_args(c, tokens, offsets, n, bad);
+    a.nh0 = nh0;
     a.key_out = key_out;
     a.key_len = key_len;
     tree_args(c, a);
@@ -827,7 +849,8 @@ uint64_t member_scratch_bytes(uint64_t n) { return member_layout(n, nullptr, nul
 
 hipError_t hash_members(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
                         const uint64_t* bstart, const uint32_t* bad, const GroupView& gv,
-                        const uint32_t* cand, uint64_t* hkeys, bool write_keys, uint32_t* match)
+                        const uint32_t* cand, uint64_t* hkeys, bool write_keys, uint32_t* match,
+                        const uint64_t* nh0)
 {
     hipError_t e = hipSuccess;
     uint8_t* w = static_cast<uint8_t*>(scratch_get(c, kSlotMembers, member_scratch_bytes(n), &e));
@@ -844,6 +867,7 @@ hipError_t hash_members(dm_ctx* c, const int32_t* tokens, const int64_t* offsets
     a.bstart = bstart;
     a.hkeys = hkeys;
     a.write_keys = write_keys ? 1u : 0u;
+    a.nh0 = const_cast<uint64_t*>(nh0);
     a.gv = gv;
     a.cand = cand;
     a.match = match;

@@ -279,11 +279,14 @@ struct GroupView {
 //     extended are listed (ext_list, *ext_count zeroed beforehand) for
 //     hash_extend, which walks them down the tree to K_r and rewrites their
 //     ring keys.  key_len (optional) gets every request's K_r.
+//   nh0 (optional, [n * K]): hash_prefix keeps there the f1 digests of
+//     every request's blocks below min(K, full blocks), and hash_members
+//     takes them instead of reading those tokens again.
 //   keylen_record: every request's prefixes of depth >= K (its f1 block
 //     keys from block K - 1 on, in hkeys at bstart[r]) join the window.
 hipError_t hash_prefix(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
                        const uint32_t* bad, uint64_t* key_out, uint32_t* key_len,
-                       uint32_t* ext_list, unsigned long long* ext_count);
+                       uint32_t* ext_list, unsigned long long* ext_count, uint64_t* nh0);
 hipError_t hash_extend(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
                        const uint32_t* bad, uint64_t* key_out, uint32_t* key_len,
                        const uint32_t* ext_list, const unsigned long long* ext_count);
@@ -292,7 +295,8 @@ hipError_t hash_leaders(dm_ctx* c, const int32_t* tokens, const int64_t* offsets
                         const uint32_t* cand, uint64_t* hkeys, uint32_t* match);
 hipError_t hash_members(dm_ctx* c, const int32_t* tokens, const int64_t* offsets, uint64_t n,
                         const uint64_t* bstart, const uint32_t* bad, const GroupView& gv,
-                        const uint32_t* cand, uint64_t* hkeys, bool write_keys, uint32_t* match);
+                        const uint32_t* cand, uint64_t* hkeys, bool write_keys, uint32_t* match,
+                        const uint64_t* nh0);
 
 // dm_keylen.hip: the hotness tree's set-up, window close and export
 // (host entry points; they synchronise), and its release.

@@ -47,6 +47,17 @@ uint32_t block_shift_of(const dm_ctx* c)
     return k;
 }
 
+// Block starts [n + 1] and the malformed-offsets word, 256-byte aligned.
+uint64_t starts_bytes(uint64_t n) { return ((n + 2) * sizeof(uint64_t) + 255) & ~255ull; }
+
+// The f1 digests the prefix pass keeps for the members pass: K per request,
+// when K is small enough that they cost less than a fraction of the tokens
+// they replace (always at K <= 16).
+uint64_t nh0_bytes(const dm_ctx* c, uint64_t n)
+{
+    return c->cfg.key_blocks <= 16 ? n * c->cfg.key_blocks * sizeof(uint64_t) : 0;
+}
+
 // Routes launches of the helper stages to another stream for one call.
 struct StreamSwap {
     dm_ctx* c;
@@ -62,7 +73,8 @@ void route_scratch_plan(const dm_ctx* c, uint64_t n, uint64_t n_tokens, bool key
 {
     for (int i = 0; i < kScratchSlots; i++)
         bytes[i] = 0;
-    bytes[kSlotStarts] = (n + 2) * sizeof(uint64_t);  // block starts, malformed-offsets word
+    // block starts, malformed-offsets word, the first blocks' f1 digests
+    bytes[kSlotStarts] = starts_bytes(n) + nh0_bytes(c, n);
     bytes[kSlotProbe] = probe_scratch_bytes(n);       // request order and groups
     bytes[kSlotMembers] = member_scratch_bytes(n);    // members pass records, kept keys
     bytes[kSlotSelect] = select_scratch_bytes(n);     // one set of selection work arrays
@@ -100,12 +112,16 @@ hipError_t route(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens, const int6
     }
     if (ev && (e = hipEventRecord(ev[0], st)) != hipSuccess)
         return e;
-    // block starts [n + 1], then the malformed-offsets word
-    uint64_t* bstart =
-        static_cast<uint64_t*>(scratch_get(c, kSlotStarts, (n + 2) * sizeof(uint64_t), &e));
+    // block starts [n + 1], then the malformed-offsets word, then the f1
+    // digests of every request's first min(K, full blocks) blocks
+    uint64_t* bstart = static_cast<uint64_t*>(
+        scratch_get(c, kSlotStarts, starts_bytes(n) + nh0_bytes(c, n), &e));
     if (!bstart)
         return e;
     uint32_t* bad = reinterpret_cast<uint32_t*>(bstart + n + 1);
+    uint64_t* nh0 = nh0_bytes(c, n) ? reinterpret_cast<uint64_t*>(
+                                          reinterpret_cast<uint8_t*>(bstart) + starts_bytes(n))
+                                    : nullptr;
     // with the hotness tree: the count (first 256 bytes), then the list of
     // requests going down the tree
     unsigned long long* ext_count = nullptr;
@@ -140,7 +156,7 @@ hipError_t route(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens, const int6
         return e;
     GroupView gv{};
     if ((e = hash_prefix(c, tokens, offsets, n, bad, out->key, out->key_len, ext_list,
-                         ext_count)) != hipSuccess)
+                         ext_count, nh0)) != hipSuccess)
         return e;
     if (c->kl.on && (e = hash_extend(c, tokens, offsets, n, bad, out->key, out->key_len, ext_list,
                                      ext_count)) != hipSuccess)
@@ -152,7 +168,7 @@ hipError_t route(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens, const int6
     if ((e = hash_leaders(c, tokens, offsets, n, bstart, bad, gv, out->cand, hkeys, out->match)) !=
             hipSuccess ||
         (e = hash_members(c, tokens, offsets, n, bstart, bad, gv, out->cand, hkeys, write_keys,
-                          out->match)) != hipSuccess)
+                          out->match, nh0)) != hipSuccess)
         return e;
     if (c->kl.on) {
         if ((e = keylen_record(c, n, bstart, hkeys, kl_work)) != hipSuccess)

@@ -683,7 +683,7 @@ def main():
         "roofline": {"bound": "hbm",
                      "kernel": "hash+match stage: ring_key_kernel<16>, lookup_kernel, "
                                "radix sort passes, group_head_kernel, "
-                               "group scan, group_leader_kernel, group_of_kernel, "
+                               "group scan, group_leader_kernel, "
                                "walk_kernel<16> (leaders, resume), member_record_kernel, "
                                "member_kernel<16>, probe_pending_kernel",
                      "achieved": stage_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",

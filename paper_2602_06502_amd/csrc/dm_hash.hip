@@ -40,7 +40,8 @@ namespace {
 
 constexpr int kHashThreads = 256;
 constexpr uint32_t kHashBlocks = 1u << 20;  // one wave per unit up to 4 Mi units
-constexpr uint32_t kLeaderBlocks = 2048;    // leaders: at most 8,192 waves, grid-stride
+constexpr uint32_t kLeaderBlocks = 2048;    // tree walk, resume walk: at most 8,192 waves
+constexpr uint32_t kLeaderGrid = 8192;      // leaders: up to 32,768 waves, one leader each
 
 enum : int { kLeaders = 1, kResume = 2 };
 constexpr uint64_t kPendKeys = 8;  // keys kept per request for the pending probes
@@ -842,7 +843,7 @@ hipError_t hash_leaders(dm_ctx* c, const int32_t* tokens, const int64_t* offsets
     a.cand = cand;
     a.match = match;
     // the group count is on the device: a bounded grid strides over it
-    return launch_walk<kLeaders>(c, a, grid_for(n, kHashThreads / kWave, kLeaderBlocks));
+    return launch_walk<kLeaders>(c, a, grid_for(n, kHashThreads / kWave, kLeaderGrid));
 }
 
 uint64_t member_scratch_bytes(uint64_t n) { return member_layout(n, nullptr, nullptr); }

@@ -68,7 +68,8 @@ __global__ void group_head_kernel(const uint64_t* __restrict__ skeys,
 }
 
 // Leader of each group (a head at i leads group gpos[i]): the longest
-// request among the group's positions [i, i + 64), ties to the earliest.
+// request among the group's positions [i, i + 64), ties to the earliest;
+// and every request's group (group_of[order[i]]).
 // One wave per 64 positions holds positions [64w, 64w + 128), two per lane,
 // as (full blocks << 32 | ~position) so that the larger value is the longer
 // and then earlier request.  A segmented suffix maximum by doubling over
@@ -80,7 +81,8 @@ __global__ __launch_bounds__(256) void group_leader_kernel(const uint32_t* __res
                                                            const uint64_t* __restrict__ head,
                                                            const uint32_t* __restrict__ len,
                                                            const uint64_t* __restrict__ gpos,
-                                                           uint32_t* __restrict__ leader)
+                                                           uint32_t* __restrict__ leader,
+                                                           uint32_t* __restrict__ group_of)
 {
     const int lane = lane_id();
     const uint64_t waves = (m + kWave - 1) / kWave;
@@ -116,22 +118,17 @@ __global__ __launch_bounds__(256) void group_leader_kernel(const uint32_t* __res
                 }
             }
         }
-        if (i0 < m && h0) {
-            const uint64_t best = (uint32_t)~(uint32_t)v0;
-            leader[gpos[i0]] = order[best];
+        if (i0 < m) {
+            // the group of position i0, for its request; a head names the
+            // group's leader
+            const uint64_t g = gpos[i0] + (h0 ? 1 : 0) - 1;
+            group_of[order[i0]] = (uint32_t)g;
+            if (h0)
+                leader[g] = order[(uint32_t)~(uint32_t)v0];
         }
     }
 }
 
-// group_of[order[i]] = the group of position i.
-__global__ void group_of_kernel(const uint32_t* __restrict__ order, uint64_t m,
-                                const uint64_t* __restrict__ head,
-                                const uint64_t* __restrict__ gpos, uint32_t* __restrict__ group_of)
-{
-    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < m;
-         i += (uint64_t)gridDim.x * blockDim.x)
-        group_of[order[i]] = (uint32_t)(gpos[i] + head[i] - 1);
-}
 
 // Work arrays of grouping for m requests, in layout order: sort keys and
 // request order (each twice, for the sort's passes), group heads, group
@@ -199,9 +196,7 @@ hipError_t lookup_group(dm_ctx* c, uint64_t n, const uint64_t* key, const uint64
     if ((e = exclusive_scan_u64(c, g.head, n, g.gpos, g.groups)) != hipSuccess)
         return e;
     group_leader_kernel<<<grid_for((n + kWave - 1) / kWave, 256 / kWave, 8192), 256, 0, st>>>(
-        g.order, n, g.head, g.len, g.gpos, g.leader);
-    group_of_kernel<<<grid_for(n, 256, 8192), 256, 0, st>>>(g.order, n, g.head, g.gpos,
-                                                            g.group_of);
+        g.order, n, g.head, g.len, g.gpos, g.leader, g.group_of);
     *gv = GroupView{g.group_of, g.leader, g.groups};
     return hipGetLastError();
 }

@@ -540,7 +540,8 @@ int or_kv_save(or_state *st, const int64_t *off, uint64_t n, const uint64_t *blo
     int rc = OR_OK;
     for (uint32_t c = 0; c < S && rc == OR_OK; c++) {
         const uint64_t lo = c ? cnt[c - 1] : 0, hi = cnt[c];
-        if (lo == hi)
+        /* an instance sent nothing still keeps only its cap most recent keys */
+        if (lo == hi && (cap == 0 || st->lru_len[c] <= cap))
             continue;
         const uint64_t old = st->lru_len[c], m = old + (hi - lo);
         or_kt *a = (or_kt *)malloc(m * sizeof(or_kt));

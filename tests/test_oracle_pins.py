@@ -1109,6 +1109,24 @@ def test_kv_save_matches_lru_model(seed):
             assert all(o.index_contains(c, int(k)) for k in lru.keys[c])
 
 
+def test_kv_save_lower_cap_applies_to_every_instance():
+    """Instance 1 holds 3 saved keys; a save with cap 2 that sends it nothing
+    still leaves it its 2 most recent (the least recent is erased), and
+    instance 0, sent one chain of 2 blocks, keeps both."""
+    B = 4
+    o = oracle.Oracle(dict(block=B, key_blocks=1, seeds=(1, 2), vnodes=4, max_slots=2))
+    rng = np.random.default_rng(13)
+    c1 = [int(x) for x in rng.integers(0, 50, size=B * 3)]
+    (rc, added, removed), bk1 = _kv_case(o, B, [c1], [1], 0, 0)
+    assert rc == oracle.OK and (added, removed) == (3, 0)
+    c0 = [int(x) for x in rng.integers(50, 100, size=B * 2)]
+    (rc, added, removed), bk0 = _kv_case(o, B, [c0], [0], 3, 2)
+    assert rc == oracle.OK and (added, removed) == (2, 1)
+    assert o.index_size(0) == 2 and o.index_size(1) == 2
+    # times of instance 1's blocks: block 2 at 0, block 1 at 1, block 0 at 2
+    assert not o.index_contains(1, int(bk1[2])) and o.index_contains(1, int(bk1[0]))
+
+
 def test_kv_save_unbounded_and_errors():
     B = 4
     o = oracle.Oracle(dict(block=B, key_blocks=1, seeds=(1, 2), vnodes=4, max_slots=2))

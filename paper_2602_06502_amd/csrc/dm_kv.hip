@@ -58,10 +58,12 @@ __global__ void kv_fill_kernel(const uint64_t* __restrict__ rkey, const uint64_t
     for (uint64_t r = w; r < n; r += nw) {
         const uint64_t s = bstart[r], nf = bstart[r + 1] - s;
         const uint32_t c = inst[r];
+        // entries in touch order (deepest block first), so that after the
+        // stable sorts a run's last entry is its latest touch of this batch
         for (uint64_t b = lane; b < nf; b += kWave) {
-            const uint64_t e = nrec + s + b;
+            const uint64_t e = nrec + s + (nf - 1 - b);
             key[e] = block_keys[s + b];
-            t[e] = clock + s + (nf - 1 - b);
+            t[e] = clock + (e - nrec);
             ins[e] = c;
             idx[e] = (uint32_t)e;
         }
@@ -104,8 +106,11 @@ __global__ void kv_head_kernel(const uint32_t* __restrict__ order,
     }
 }
 
-// One thread per run head: latest time over the run, whether any entry is
-// from the record (already cached), and the run's place.
+// Runs of equal (instance, key) in sorted order, their entries in input
+// order (the sorts are stable): a record entry first if there is one, then
+// the batch's touches by increasing time.  The head writes the run's key,
+// instance, whether it was already cached and its first entry's time; the
+// last entry's time is merged in by kv_runs_last_kernel.
 __global__ void kv_runs_kernel(const uint32_t* __restrict__ order,
                                const uint64_t* __restrict__ key, const uint64_t* __restrict__ t,
                                const uint32_t* __restrict__ ins, uint64_t m, uint64_t nrec,
@@ -118,28 +123,53 @@ __global__ void kv_runs_kernel(const uint32_t* __restrict__ order,
         if (!head[p])
             continue;
         const uint32_t a = order[p];
-        uint64_t best = t[a];
-        bool old = a < nrec;
-        for (uint64_t q = p + 1; q < m && !head[q]; q++) {
-            const uint32_t b = order[q];
-            best = std::max(best, t[b]);
-            old |= b < nrec;
-        }
         const uint64_t u = run[p];
         ukey[u] = key[a];
-        ut[u] = best;
+        ut[u] = t[a];
         uins[u] = ins[a];
-        uold[u] = old ? 1u : 0u;
+        uold[u] = a < nrec ? 1u : 0u;
     }
 }
 
-// Runs per instance (one atomic per run).
-__global__ void kv_count_kernel(const uint32_t* __restrict__ uins, uint64_t u, uint32_t S,
-                                unsigned long long* __restrict__ cnt)
+// The latest time of each run of more than one entry: the larger of its
+// first entry's (a record entry may carry any earlier time) and its last's.
+__global__ void kv_runs_last_kernel(const uint32_t* __restrict__ order,
+                                    const uint64_t* __restrict__ t, uint64_t m,
+                                    const uint64_t* __restrict__ head,
+                                    const uint64_t* __restrict__ run, uint64_t* __restrict__ ut)
+{
+    for (uint64_t p = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; p < m;
+         p += (uint64_t)gridDim.x * blockDim.x) {
+        if (head[p] || (p + 1 < m && !head[p + 1]))
+            continue;
+        const uint64_t u = run[p] - 1;
+        const uint64_t x = t[order[p]];
+        ut[u] = ut[u] > x ? ut[u] : x;
+    }
+}
+
+// Runs per instance: the runs are in (instance, key) order, so each
+// instance's runs are one range; its bounds are where the instance changes.
+__global__ void kv_count_kernel(const uint32_t* __restrict__ uins, uint64_t u,
+                                unsigned long long* __restrict__ first,
+                                unsigned long long* __restrict__ end)
 {
     for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < u;
-         i += (uint64_t)gridDim.x * blockDim.x)
-        atomicAdd(&cnt[uins[i]], 1ull);
+         i += (uint64_t)gridDim.x * blockDim.x) {
+        const uint32_t c = uins[i];
+        if (i == 0 || uins[i - 1] != c)
+            first[c] = i;
+        if (i + 1 == u || uins[i + 1] != c)
+            end[c] = i + 1;
+    }
+}
+
+// cnt[c] = end[c] - first[c] (both zero for an instance without runs).
+__global__ void kv_count_fin_kernel(const unsigned long long* __restrict__ first,
+                                    unsigned long long* __restrict__ end, uint32_t S)
+{
+    for (uint32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < S; c += gridDim.x * blockDim.x)
+        end[c] -= first[c];
 }
 
 // Sort key of the third pass: instance above the time (times < 2^40).
@@ -207,20 +237,26 @@ __global__ void kv_emit_kernel(const uint32_t* __restrict__ order2,
 }
 
 // Per instance: how many of the erase and insert lists' entries are its.
-__global__ void kv_list_count_kernel(const uint32_t* __restrict__ order2,
-                                     const uint32_t* __restrict__ uins, uint64_t u,
-                                     const uint64_t* __restrict__ f_erase,
-                                     const uint64_t* __restrict__ f_insert,
+// Its runs are positions [ibase[c], ibase[c] + cnt[c]) of the (instance,
+// time) order, so the counts are differences of the lists' exclusive scans
+// (tot_e, tot_i: the scans' totals).
+__global__ void kv_list_count_kernel(const unsigned long long* __restrict__ cnt,
+                                     const uint64_t* __restrict__ ibase, uint32_t S, uint64_t u,
+                                     const uint64_t* __restrict__ p_erase,
+                                     const uint64_t* __restrict__ p_insert,
+                                     const uint64_t* __restrict__ tot_e,
+                                     const uint64_t* __restrict__ tot_i,
                                      unsigned long long* __restrict__ ce,
                                      unsigned long long* __restrict__ ci)
 {
-    for (uint64_t p = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; p < u;
-         p += (uint64_t)gridDim.x * blockDim.x) {
-        const uint32_t c = uins[order2[p]];
-        if (f_erase[p])
-            atomicAdd(&ce[c], 1ull);
-        if (f_insert[p])
-            atomicAdd(&ci[c], 1ull);
+    for (uint32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < S; c += gridDim.x * blockDim.x) {
+        if (!cnt[c]) {
+            ce[c] = ci[c] = 0;
+            continue;
+        }
+        const uint64_t lo = ibase[c], hi = lo + cnt[c];
+        ce[c] = (hi < u ? p_erase[hi] : *tot_e) - p_erase[lo];
+        ci[c] = (hi < u ? p_insert[hi] : *tot_i) - p_insert[lo];
     }
 }
 
@@ -435,6 +471,7 @@ dm_status kv_save(dm_ctx* c, const int64_t* offsets, uint64_t n, const uint64_t*
         return hip_fail(c, e, "dm_kv_save");
     kv_runs_kernel<<<g, 256, 0, st>>>(order, key, t, ins, M, rec.n, head, run, ukey, ut, uins,
                                       uold);
+    kv_runs_last_kernel<<<g, 256, 0, st>>>(order, t, M, head, run, ut);
     uint64_t U = 0;
     if ((e = hipMemcpyAsync(&U, tot, 8, hipMemcpyDeviceToHost, st)) != hipSuccess ||
         (e = hipStreamSynchronize(st)) != hipSuccess)
@@ -444,7 +481,8 @@ dm_status kv_save(dm_ctx* c, const int64_t* offsets, uint64_t n, const uint64_t*
     kv_zero_kernel<<<grid_for(S, 256), 256, 0, st>>>(ce, S);
     kv_zero_kernel<<<grid_for(S, 256), 256, 0, st>>>(ci, S);
     const uint32_t gu = grid_for(U, 256, 8192);
-    kv_count_kernel<<<gu, 256, 0, st>>>(uins, U, S, cnt);
+    kv_count_kernel<<<gu, 256, 0, st>>>(uins, U, ce, cnt);
+    kv_count_fin_kernel<<<grid_for(S, 256), 256, 0, st>>>(ce, cnt, S);
     if ((e = exclusive_scan_u64(c, reinterpret_cast<const uint64_t*>(cnt), S, ibase, tot + 1)) !=
         hipSuccess)
         return hip_fail(c, e, "dm_kv_save");
@@ -467,7 +505,8 @@ dm_status kv_save(dm_ctx* c, const int64_t* offsets, uint64_t n, const uint64_t*
     kv_emit_kernel<<<gu, 256, 0, st>>>(order2, ukey, ut, uins, U, f_erase, p_erase, f_insert,
                                        p_insert, f_keep, p_keep, erase_keys, insert_keys, rec.key,
                                        rec.t, rec.inst);
-    kv_list_count_kernel<<<gu, 256, 0, st>>>(order2, uins, U, f_erase, f_insert, ce, ci);
+    kv_list_count_kernel<<<grid_for(S, 256), 256, 0, st>>>(cnt, ibase, S, U, p_erase, p_insert,
+                                                           tot + 2, tot + 3, ce, ci);
     std::vector<unsigned long long> hce(S), hci(S);
     if ((e = hipMemcpyAsync(hce.data(), ce, 8 * (size_t)S, hipMemcpyDeviceToHost, st)) !=
             hipSuccess ||

@@ -556,6 +556,39 @@ def test_queue_reprobe_parity_and_errors():
         assert ei.value.status == pk.DM_EINVAL, j
 
 
+def test_kv_save_runs_and_lower_cap_parity():
+    """KV saves whose batches send one key many times to one instance (long
+    runs of equal keys), record entries touched again, and a lowered cap on
+    a later save that sends some instances nothing: counts and index sizes
+    against the oracle after every save, then a route that reads the
+    caches."""
+    gh = _h()
+    B, K = 16, 2
+    wl = workloads.small_random(91, 6, 8, B, 8, key_blocks=K)
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    S = wl.route.max_slots
+    d = lambda a: gh.to_dev(a, eng.device)
+    rng = np.random.default_rng(5)
+    clock = 0
+    for step, (cap, n_inst) in enumerate([(0, 6), (400, 6), (400, 2), (150, 1), (0, 3)]):
+        tok, off = _hot_batches(200 + step, B, K, 1, tlen_blocks=(1, 60), n_tpl=3, zipf=2.0)[0]
+        n = len(off) - 1
+        bk = o.route(tok, off, workloads.initial_loads(wl, S), block_keys=True)["block_keys"]
+        inst = rng.integers(0, n_inst, size=n).astype(np.uint32)
+        _say("kv save step", step, "cap", cap, "instances", n_inst, "requests", n)
+        ga = eng.kv_save(d(off), d(bk), d(inst), clock, cap)
+        rc, a, rm = o.kv_save(off, bk, inst, clock, cap)
+        assert rc == oracle.OK and ga == (a, rm), (step, ga, a, rm)
+        clock += int((np.diff(off) // B).sum())
+        for c in range(S):
+            assert eng.index_size(c) == o.index_size(c), (step, c)
+    tok, off = _hot_batches(299, B, K, 1, tlen_blocks=(1, 60), n_tpl=3, zipf=2.0)[0]
+    L = workloads.initial_loads(wl, S)
+    g = eng.route(d(tok), d(off), d(L), block_keys=True)
+    eng.sync()
+    compare_route(g, o.route(tok, off, L, block_keys=True), len(off) - 1, with_bk=True)
+
+
 def _disjoint_pair_prompts(o, rng, n_pool):
     """Random prompts whose candidate pairs are pairwise disjoint (greedy
     over a pool), found with the oracle's ring keys and candidates."""

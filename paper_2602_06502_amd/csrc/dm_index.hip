@@ -15,6 +15,7 @@
 // else dropped with DM_EFULL).  So a batch that fits is stored whole, and a
 // batch that does not fills the table to exactly the limit.
 #include <algorithm>
+#include <vector>
 
 #include "dm_internal.h"
 
@@ -257,6 +258,140 @@ __global__ void clear_many_kernel(uint64_t* __restrict__ tables, uint32_t log2sl
     }
 }
 
+// Key lists of several tables at once: keys[seg[i] .. seg[i+1]) belong to
+// table i (seg: device [S + 1]).  Each thread finds its key's table by
+// bisection over seg.
+struct Tables {
+    uint64_t* slots;   // [S << log2slots]
+    uint64_t* counts;  // [2 S]: live keys, then occupied slots
+    uint32_t log2slots, S;
+    __device__ TableRef of(uint32_t id) const
+    {
+        return TableRef{slots + ((uint64_t)id << log2slots), counts + id, counts + S + id,
+                        log2slots, 1ull << (log2slots - 1)};
+    }
+};
+
+__device__ __forceinline__ uint32_t seg_of(const uint64_t* seg, uint32_t S, uint64_t i)
+{
+    uint32_t lo = 0, hi = S;  // seg[lo] <= i < seg[hi]
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) / 2;
+        if (seg[mid] <= i)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// Adds to a table's counts, once per wave when the wave's lanes share the
+// table (the counters are few words that every insert would meet on).
+__device__ __forceinline__ void add_counts(const TableRef& t, uint32_t id, bool mine,
+                                           unsigned long long dl, unsigned long long docc)
+{
+    const uint32_t id0 = __builtin_amdgcn_readfirstlane(id);
+    if (ballot(id != id0) == 0) {
+        const unsigned long long c = __popcll(ballot(mine));
+        if (c && lane_id() == __builtin_ctzll(ballot(true))) {
+            if (dl)
+                atomicAdd((unsigned long long*)t.live, c * dl);
+            if (docc)
+                atomicAdd((unsigned long long*)t.occupied, c * docc);
+        }
+    } else if (mine) {
+        if (dl)
+            atomicAdd((unsigned long long*)t.live, dl);
+        if (docc)
+            atomicAdd((unsigned long long*)t.occupied, docc);
+    }
+}
+
+__global__ void erase_many_kernel(Tables T, const uint64_t* __restrict__ keys,
+                                  const uint64_t* __restrict__ seg, uint64_t n)
+{
+    for (uint64_t i0 = blockIdx.x * (uint64_t)blockDim.x; i0 < n;
+         i0 += (uint64_t)gridDim.x * blockDim.x) {
+        const uint64_t i = i0 + threadIdx.x;
+        const bool in = i < n;
+        const uint32_t id = seg_of(seg, T.S, in ? i : n - 1);
+        const TableRef t = T.of(id);
+        const uint64_t nbk = 1ull << (t.log2slots - 3);
+        const uint64_t k = in ? canon_key(keys[i]) : kEmpty;
+        uint64_t b = home_bucket(k, t.log2slots);
+        bool done = !in, gone = false;
+        for (uint64_t step = 0; step < nbk && !done; step++, b = (b + 1) & (nbk - 1)) {
+            for (uint32_t q = 0; q < kBucket && !done; q++) {
+                uint64_t* slot = t.slots + b * kBucket + q;
+                const uint64_t v = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (v == kEmpty) {
+                    done = true;
+                } else if (v == k) {
+                    const unsigned long long prev = atomicCAS(
+                        (unsigned long long*)slot, (unsigned long long)k, (unsigned long long)kTomb);
+                    gone = prev == k;
+                    done = true;
+                }
+            }
+        }
+        add_counts(t, id, gone, ~0ull, 0);  // live - 1 per key erased
+    }
+}
+
+// fits[i] = 1 when table i has room for all of its keys without a rebuild
+// (else the caller inserts into it alone, with the rebuild and overflow
+// handling of index_insert).
+__global__ void fits_many_kernel(Tables T, const uint64_t* __restrict__ seg,
+                                 uint32_t* __restrict__ fits)
+{
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < T.S; i += gridDim.x * blockDim.x) {
+        const uint64_t n = seg[i + 1] - seg[i];
+        fits[i] = !n || *T.of(i).occupied + n <= (1ull << (T.log2slots - 1)) ? 1u : 0u;
+    }
+}
+
+// Every table has room for all of its keys (checked before), so a key takes
+// the first empty slot of its sequence without reserving a unit of the
+// occupied count; the counts grow by the keys stored, per wave.
+__global__ void insert_many_kernel(Tables T, const uint64_t* __restrict__ keys,
+                                   const uint64_t* __restrict__ seg, uint64_t n,
+                                   const uint32_t* __restrict__ fits, uint32_t* __restrict__ status)
+{
+    for (uint64_t i0 = blockIdx.x * (uint64_t)blockDim.x; i0 < n;
+         i0 += (uint64_t)gridDim.x * blockDim.x) {
+        const uint64_t i = i0 + threadIdx.x;
+        const bool in = i < n;
+        const uint32_t id = seg_of(seg, T.S, in ? i : n - 1);
+        const TableRef t = T.of(id);
+        bool stored = false;
+        if (in && fits[id]) {
+            const uint64_t k = canon_key(keys[i]);
+            const uint64_t nbk = 1ull << (t.log2slots - 3);
+            uint64_t b = home_bucket(k, t.log2slots);
+            bool done = false;
+            for (uint64_t step = 0; step < nbk && !done; step++, b = (b + 1) & (nbk - 1)) {
+                for (uint32_t q = 0; q < kBucket && !done; q++) {
+                    uint64_t* slot = t.slots + b * kBucket + q;
+                    const uint64_t v =
+                        __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (v == k) {
+                        done = true;
+                    } else if (v == kEmpty) {
+                        const unsigned long long prev =
+                            atomicCAS((unsigned long long*)slot, (unsigned long long)kEmpty,
+                                      (unsigned long long)k);
+                        stored = prev == kEmpty;
+                        done = stored || prev == k;  // else another key took it: walk on
+                    }
+                }
+            }
+            if (!done)
+                atomicOr(status, kErrFull);
+        }
+        add_counts(t, id, stored, 1, 1);
+    }
+}
+
 TableRef table_of(dm_ctx* c, uint32_t id)
 {
     const uint32_t k = c->cfg.index_log2_slots;
@@ -294,6 +429,44 @@ hipError_t index_erase(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n)
 {
     erase_kernel<<<grid_for(n, 256), 256, 0, c->stream>>>(table_of(c, id), keys, n);
     return hipGetLastError();
+}
+
+hipError_t index_erase_many(dm_ctx* c, const uint64_t* keys, const uint64_t* seg, uint64_t n)
+{
+    if (n == 0)
+        return hipSuccess;
+    const Tables T{c->d_tables, c->d_counts, c->cfg.index_log2_slots, c->cfg.max_slots};
+    erase_many_kernel<<<grid_for(n, 256), 256, 0, c->stream>>>(T, keys, seg, n);
+    return hipGetLastError();
+}
+
+hipError_t index_insert_many(dm_ctx* c, const uint64_t* keys, const uint64_t* seg,
+                             const uint64_t* seg_host, uint64_t n)
+{
+    if (n == 0)
+        return hipSuccess;
+    const uint32_t S = c->cfg.max_slots;
+    const Tables T{c->d_tables, c->d_counts, c->cfg.index_log2_slots, S};
+    hipError_t e = hipSuccess;
+    // a flag per table: room for all of its keys
+    uint32_t* fits = static_cast<uint32_t*>(scratch_get(c, kPurgeSlot, 4 * (size_t)S + 256, &e));
+    if (!fits)
+        return e;
+    std::vector<uint32_t> fits_h(S);
+    fits_many_kernel<<<grid_for(S, 256), 256, 0, c->stream>>>(T, seg, fits);
+    insert_many_kernel<<<grid_for(n, 256), 256, 0, c->stream>>>(T, keys, seg, n, fits,
+                                                                 c->d_status);
+    if ((e = hipMemcpyAsync(fits_h.data(), fits, 4 * (size_t)S, hipMemcpyDeviceToHost,
+                            c->stream)) != hipSuccess ||
+        (e = hipStreamSynchronize(c->stream)) != hipSuccess)
+        return e;
+    // tables without room: one at a time, with the rebuild and overflow handling
+    for (uint32_t i = 0; i < S; i++)
+        if (!fits_h[i] &&
+            (e = index_insert(c, i, keys + seg_host[i], seg_host[i + 1] - seg_host[i])) !=
+                hipSuccess)
+            return e;
+    return hipSuccess;
 }
 
 hipError_t index_clear_many(dm_ctx* c, const uint32_t* ids_host, uint32_t n)

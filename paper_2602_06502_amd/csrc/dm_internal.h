@@ -253,6 +253,13 @@ hipError_t ring_remap(dm_ctx* c, const Ring old_r[2], const Ring new_r[2], const
 // dm_index.hip
 hipError_t index_insert(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n);
 hipError_t index_erase(dm_ctx* c, uint32_t id, const uint64_t* keys, uint64_t n);
+// Lists of several instances at once: keys[seg[i] .. seg[i+1]) are instance
+// i's (seg: device [max_slots + 1], seg_host its host copy).  The insert
+// runs as one kernel when every table has room for its keys, else table by
+// table as index_insert.
+hipError_t index_erase_many(dm_ctx* c, const uint64_t* keys, const uint64_t* seg, uint64_t n);
+hipError_t index_insert_many(dm_ctx* c, const uint64_t* keys, const uint64_t* seg,
+                             const uint64_t* seg_host, uint64_t n);
 hipError_t index_clear(dm_ctx* c, uint32_t id);
 // the tables of n instances (host list) emptied by one launch
 hipError_t index_clear_many(dm_ctx* c, const uint32_t* ids_host, uint32_t n);

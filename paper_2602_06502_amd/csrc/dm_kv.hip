@@ -426,7 +426,8 @@ dm_status kv_save(dm_ctx* c, const int64_t* offsets, uint64_t n, const uint64_t*
     // run heads and ids, the runs, and the flags and positions of the lists
     const uint64_t A = up256v(8 * M), A4 = up256v(4 * M), Sa = up256v(8 * (uint64_t)S);
     uint8_t* w = static_cast<uint8_t*>(
-        scratch_get(c, kSlotMembers, 16 * A + 8 * A4 + 4 * Sa + 4096, &e));
+        scratch_get(c, kSlotMembers, 16 * A + 8 * A4 + 4 * Sa + up256v(16 * ((uint64_t)S + 1)) + 4096,
+                    &e));
     if (!w)
         return hip_fail(c, e, "dm_kv_save");
     uint64_t* key = carve<uint64_t>(w, M);
@@ -456,6 +457,7 @@ dm_status kv_save(dm_ctx* c, const int64_t* offsets, uint64_t n, const uint64_t*
     unsigned long long* ce = carve<unsigned long long>(w, S);
     unsigned long long* ci = carve<unsigned long long>(w, S);
     uint64_t* tot = carve<uint64_t>(w, 8);
+    uint64_t* dseg = carve<uint64_t>(w, 2 * ((uint64_t)S + 1));
     const uint32_t g = grid_for(M, 256, 8192);
     kv_fill_kernel<<<grid_for(std::max(rec.n, n * 64), 256, 8192), 256, 0, st>>>(
         rec.key, rec.t, rec.inst, rec.n, n, bstart, block_keys, inst, clock, key, t, ins, order);
@@ -515,18 +517,18 @@ dm_status kv_save(dm_ctx* c, const int64_t* offsets, uint64_t n, const uint64_t*
         (e = hipStreamSynchronize(st)) != hipSuccess)
         return hip_fail(c, e, "dm_kv_save");
     rec.n = totals[2];
-    // the lists are in instance order: erase, then insert, instance by instance
-    uint64_t oe = 0, oi = 0;
+    // the lists are in instance order: every erase, then every insert
+    std::vector<uint64_t> seg(2 * ((size_t)S + 1), 0);
     for (uint32_t i = 0; i < S; i++) {
-        if (hce[i] && (e = index_erase(c, i, erase_keys + oe, hce[i])) != hipSuccess)
-            return hip_fail(c, e, "dm_kv_save");
-        oe += hce[i];
+        seg[i + 1] = seg[i] + hce[i];
+        seg[S + 1 + i + 1] = seg[S + 1 + i] + hci[i];
     }
-    for (uint32_t i = 0; i < S; i++) {
-        if (hci[i] && (e = index_insert(c, i, insert_keys + oi, hci[i])) != hipSuccess)
-            return hip_fail(c, e, "dm_kv_save");
-        oi += hci[i];
-    }
+    if ((e = hipMemcpyAsync(dseg, seg.data(), seg.size() * sizeof(uint64_t),
+                            hipMemcpyHostToDevice, st)) != hipSuccess ||
+        (e = index_erase_many(c, erase_keys, dseg, seg[S])) != hipSuccess ||
+        (e = index_insert_many(c, insert_keys, dseg + S + 1, seg.data() + S + 1,
+                               seg[2 * (size_t)S + 1])) != hipSuccess)
+        return hip_fail(c, e, "dm_kv_save");
     if ((e = hipStreamSynchronize(st)) != hipSuccess)
         return hip_fail(c, e, "dm_kv_save");
     if (added) *added = totals[1];

@@ -1,23 +1,28 @@
 // Stable LSD radix sort of (u64 key, u32 value) pairs, 8-bit digits.
 // Per pass: tile digit histograms (digit-major), one exclusive scan over
-// them, and a stable scatter that ranks equal digits inside each 64-lane
-// sub-tile with ballots.
+// them, and a stable scatter.  A tile is 1024 or 4096 items; the scatter ranks
+// equal digits inside each wave with ballots, orders the tile by digit in
+// LDS, and writes each digit's items as one run of consecutive addresses.
 #include "dm_internal.h"
 
 namespace dm {
 namespace {
 
 constexpr int kSortThreads = 256;
-constexpr int kSortItems = 4;
-constexpr uint64_t kSortTile = kSortThreads * kSortItems;
-constexpr int kSubtiles = kSortItems * (kSortThreads / kWave);
+constexpr int kSortWaves = kSortThreads / kWave;
+// Items per thread: 16 (4096-item tiles, longer runs per digit) for large
+// sorts, 4 (1024-item tiles, four times the workgroups) below kBigSort.
+constexpr uint64_t kBigSort = 1ull << 22;
+constexpr uint64_t tile_of(uint64_t n) { return n >= kBigSort ? 16 * kSortThreads : 4 * kSortThreads; }
 constexpr int kSortSlot = kSlotSort;
 
+template <int kSortItems>
 __global__ __launch_bounds__(kSortThreads) void digit_hist_kernel(const uint64_t* __restrict__ keys,
                                                                   uint64_t n, int shift,
                                                                   uint64_t ntiles,
                                                                   uint64_t* __restrict__ cnt)
 {
+    constexpr uint64_t kSortTile = (uint64_t)kSortThreads * kSortItems;
     __shared__ uint32_t hist[256];
     hist[threadIdx.x] = 0;
     __syncthreads();
@@ -32,66 +37,115 @@ __global__ __launch_bounds__(kSortThreads) void digit_hist_kernel(const uint64_t
     cnt[(uint64_t)threadIdx.x * ntiles + blockIdx.x] = hist[threadIdx.x];
 }
 
+template <int kSortItems>
 __global__ __launch_bounds__(kSortThreads) void digit_scatter_kernel(
     const uint64_t* __restrict__ keys, const uint32_t* __restrict__ vals, uint64_t n, int shift,
     uint64_t ntiles, const uint64_t* __restrict__ offs, uint64_t* __restrict__ okeys,
     uint32_t* __restrict__ ovals)
 {
-    __shared__ uint32_t sub[kSubtiles][256];
-    for (int k = threadIdx.x; k < kSubtiles * 256; k += kSortThreads)
-        (&sub[0][0])[k] = 0;
-    __syncthreads();
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const uint64_t lt = (lane ? (~0ull >> (64 - lane)) : 0ull);
+    constexpr uint64_t kSortTile = (uint64_t)kSortThreads * kSortItems;
+    __shared__ uint64_t sk[kSortTile];
+    __shared__ uint32_t sv[kSortTile];
+    // per round (double-buffered): each wave's count of each digit, tagged
+    // with the round (count | round << 16), then replaced by its offset
+    __shared__ uint32_t wcnt[2][kSortWaves][256];
+    __shared__ uint32_t run[256];    // items of each digit in earlier rounds
+    __shared__ uint32_t dbase[256];  // the digit's first place in the tile's order
+    __shared__ int64_t gshift[256];  // global place of the digit's first item - dbase
+    __shared__ uint32_t wsum[kSortWaves];
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
     const uint64_t base = blockIdx.x * kSortTile;
+    const uint64_t tn = n - base < kSortTile ? n - base : kSortTile;
+    run[t] = 0;
+    // no round's tag: entries a round does not write read as zero counts
+    for (int q = t; q < 2 * kSortWaves * 256; q += kSortThreads)
+        (&wcnt[0][0][0])[q] = 0xFFFFFFFFu;
     uint64_t k[kSortItems];
-    uint32_t v[kSortItems], d[kSortItems], rank[kSortItems];
-    bool ok[kSortItems];
+    uint32_t v[kSortItems], rk[kSortItems];
+    __syncthreads();
 #pragma unroll
     for (int it = 0; it < kSortItems; it++) {
-        const uint64_t i = base + it * kSortThreads + threadIdx.x;
-        ok[it] = i < n;
-        k[it] = ok[it] ? keys[i] : 0;
-        v[it] = ok[it] && vals ? vals[i] : 0;
-        d[it] = (uint32_t)((k[it] >> shift) & 0xFF);
-        uint64_t peers = ballot(ok[it]);
+        const uint64_t i = (uint64_t)it * kSortThreads + t;  // place in the tile
+        const bool ok = i < tn;
+        k[it] = ok ? keys[base + i] : 0;
+        v[it] = ok && vals ? vals[base + i] : 0;
+        const uint32_t d = (uint32_t)((k[it] >> shift) & 0xFF);
+        uint64_t peers = ballot(ok);
 #pragma unroll
         for (int b = 0; b < 8; b++) {
-            const bool bit = (d[it] >> b) & 1;
+            const bool bit = (d >> b) & 1;
             const uint64_t m = ballot(bit);
             peers &= bit ? m : ~m;
         }
-        rank[it] = __popcll(peers & lt);
-        // the lowest lane of each peer group records the group size
-        if (ok[it] && (peers & lt) == 0)
-            sub[it * (kSortThreads / kWave) + w][d[it]] = __popcll(peers);
-    }
-    __syncthreads();
-    // exclusive scan over sub-tiles, per digit (thread = digit)
-    {
-        uint32_t run = 0;
-        for (int s = 0; s < kSubtiles; s++) {
-            const uint32_t c = sub[s][threadIdx.x];
-            sub[s][threadIdx.x] = run;
-            run += c;
+        const uint32_t pr = __popcll(peers & lt);
+        const int buf = it & 1;
+        if (ok && pr == 0)
+            wcnt[buf][w][d] = (uint32_t)__popcll(peers) | ((uint32_t)it << 16);
+        __syncthreads();
+        // thread t = digit t: offsets of the waves' items of this round
+        {
+            uint32_t r = run[t];
+#pragma unroll
+            for (int ww = 0; ww < kSortWaves; ww++) {
+                const uint32_t x = wcnt[buf][ww][t];
+                const uint32_t c = (x >> 16) == (uint32_t)it ? (x & 0xFFFFu) : 0u;
+                wcnt[buf][ww][t] = r | ((uint32_t)it << 16);
+                r += c;
+            }
+            run[t] = r;
         }
+        __syncthreads();
+        rk[it] = ok ? (wcnt[buf][w][d] & 0xFFFFu) + pr : 0;
+    }
+    // (offsets fit the 16 bits below the tag: a tile has at most 4096 items)
+    // first place of each digit in the tile (exclusive scan over digits)
+    {
+        uint32_t x = run[t];
+        // inclusive wave scan
+#pragma unroll
+        for (int dlt = 1; dlt < kWave; dlt <<= 1) {
+            const uint32_t y = __shfl_up(x, dlt);
+            if (lane >= dlt)
+                x += y;
+        }
+        if (lane == kWave - 1)
+            wsum[w] = x;
+        __syncthreads();
+        uint32_t add = 0;
+        for (int ww = 0; ww < w; ww++)
+            add += wsum[ww];
+        dbase[t] = x + add - run[t];
+        gshift[t] = (int64_t)offs[(uint64_t)t * ntiles + blockIdx.x] - (int64_t)(x + add - run[t]);
     }
     __syncthreads();
 #pragma unroll
     for (int it = 0; it < kSortItems; it++) {
-        if (!ok[it])
-            continue;
-        const uint64_t pos = offs[(uint64_t)d[it] * ntiles + blockIdx.x] +
-                             sub[it * (kSortThreads / kWave) + w][d[it]] + rank[it];
-        okeys[pos] = k[it];
+        const uint64_t i = (uint64_t)it * kSortThreads + t;
+        if (i < tn) {
+            const uint32_t d = (uint32_t)((k[it] >> shift) & 0xFF);
+            const uint32_t at = dbase[d] + rk[it];
+            sk[at] = k[it];
+            if (vals)
+                sv[at] = v[it];
+        }
+    }
+    __syncthreads();
+    // the tile in digit order: consecutive places of one digit go to
+    // consecutive addresses
+    for (uint32_t j = t; j < tn; j += kSortThreads) {
+        const uint64_t x = sk[j];
+        const uint32_t d = (uint32_t)((x >> shift) & 0xFF);
+        const uint64_t pos = (uint64_t)(gshift[d] + (int64_t)j);
+        okeys[pos] = x;
         if (ovals)
-            ovals[pos] = v[it];
+            ovals[pos] = sv[j];
     }
 }
 
 }  // namespace
 
-uint64_t sort_scan_len(uint64_t n) { return 256 * ((n + kSortTile - 1) / kSortTile); }
+uint64_t sort_scan_len(uint64_t n) { return 256 * ((n + tile_of(n) - 1) / tile_of(n)); }
 
 // digit counts and their offsets, 256 per tile each
 uint64_t sort_scratch_bytes(uint64_t n) { return 2 * sort_scan_len(n) * sizeof(uint64_t); }
@@ -101,7 +155,7 @@ hipError_t radix_sort_kv(dm_ctx* c, uint64_t* keys, uint32_t* vals, uint64_t* kt
 {
     if (n < 2 || bits <= 0)
         return hipSuccess;
-    const uint64_t ntiles = (n + kSortTile - 1) / kSortTile;
+    const uint64_t tile = tile_of(n), ntiles = (n + tile - 1) / tile;
     hipError_t e;
     uint64_t* cnt = static_cast<uint64_t*>(scratch_get(c, kSortSlot, sort_scratch_bytes(n), &e));
     if (!cnt)
@@ -111,12 +165,19 @@ hipError_t radix_sort_kv(dm_ctx* c, uint64_t* keys, uint32_t* vals, uint64_t* kt
     uint32_t *sv = vals, *dv = vtmp;
     int passes = 0;
     for (int shift = 0; shift < bits; shift += 8, passes++) {
-        digit_hist_kernel<<<ntiles, kSortThreads, 0, c->stream>>>(sk, n, shift, ntiles, cnt);
+        if (n >= kBigSort)
+            digit_hist_kernel<16><<<ntiles, kSortThreads, 0, c->stream>>>(sk, n, shift, ntiles, cnt);
+        else
+            digit_hist_kernel<4><<<ntiles, kSortThreads, 0, c->stream>>>(sk, n, shift, ntiles, cnt);
         e = exclusive_scan_u64(c, cnt, 256 * ntiles, offs, nullptr);
         if (e != hipSuccess)
             return e;
-        digit_scatter_kernel<<<ntiles, kSortThreads, 0, c->stream>>>(sk, sv, n, shift, ntiles,
-                                                                     offs, dk, dv);
+        if (n >= kBigSort)
+            digit_scatter_kernel<16><<<ntiles, kSortThreads, 0, c->stream>>>(sk, sv, n, shift,
+                                                                             ntiles, offs, dk, dv);
+        else
+            digit_scatter_kernel<4><<<ntiles, kSortThreads, 0, c->stream>>>(sk, sv, n, shift,
+                                                                            ntiles, offs, dk, dv);
         std::swap(sk, dk);
         std::swap(sv, dv);
     }

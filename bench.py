@@ -531,7 +531,9 @@ def elastic_leg(eng, wl, st, keys, L0, reps):
             reb_ms.append(1000.0 * (time.perf_counter() - t0))
         count = int(m["count"].cpu()[0])
     med = lambda x: float(np.median(x))
+    queue_ops = elastic_queue_ops(eng, wl, st, out, qd, m, count)
     return {
+        "queue_ops": queue_ops,
         "workload": f"elastic: large state, add ids {int(add[0])}..{int(add[-1])}, remove 8 "
                     f"seeded ids ({n:,} x 2 ring keys); re-route {n:,} requests on "
                     f"{n_live} instances; rebalance {len(q.rec_id):,} records queued on 8 "
@@ -545,6 +547,60 @@ def elastic_leg(eng, wl, st, keys, L0, reps):
         "note": "host wall clock per call, repetitions after one warm-up; the paper reports "
                 "2.2-2.5 ms per rebalancing pass on its own machine (context, not a target)",
     }
+
+
+def elastic_queue_ops(eng, wl, st, out, qd, m, count):
+    """The queue operations at the elastic workload's scale: the re-routed
+    batch (1,048,576 requests) appended to empty queues, the rebalancing
+    pass's migration list applied to its 262,144 queued records, then one
+    round of service drained.  Host clock of the second of two identical
+    calls (each synchronises), the oracle's operation on the same input
+    beside it (one run, single-threaded), and whether the queues matched."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2602_06502_amd.harness as gh
+    o = oracle.Oracle(wl.route.as_dict())
+    S = wl.route.max_slots
+    d = lambda a: gh.to_dev(a, eng.device)
+    res, same = {}, True
+
+    def step(name, fg, fo):
+        nonlocal same
+        fg()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        g = fg()
+        t1 = time.perf_counter()
+        r = fo()
+        t2 = time.perf_counter()
+        ok = all(np.array_equal(a.cpu().numpy(), b) for a, b in zip(g, r))
+        same = same and ok
+        res[name] = {"gpu_ms": 1000.0 * (t1 - t0), "oracle_ms": 1000.0 * (t2 - t1),
+                     "records": int(r[0][-1]), "parity": bool(ok)}
+        return g, r
+
+    offs = st["offsets_np"]
+    n = len(offs) - 1
+    cpu = {k: out[k].cpu().numpy() for k in ("cand", "match", "chosen")}
+    empty = (np.zeros(S + 1, np.int64), np.zeros(0, np.uint64), np.zeros(0, np.uint32),
+             np.zeros(0, np.uint32), np.zeros(0, np.uint32), np.zeros(S, np.int64))
+    step("append", lambda: eng.queue_append(tuple(d(x) for x in empty), st["offsets"], out, 0),
+         lambda: o.queue_append(empty, offs, cpu["cand"], cpu["match"], cpu["chosen"], 0))
+    qh = tuple(x.cpu().numpy() for x in qd)
+    mr, ms_, md = m["rec"][:count], m["src"][:count], m["dst"][:count]
+    qg, qo = step("migrate", lambda: eng.queue_migrate(tuple(qd), mr, ms_, md),
+                  lambda: o.queue_migrate(qh, mr.cpu().numpy(), ms_.cpu().numpy(),
+                                          md.cpu().numpy()))
+    units = np.zeros(S, np.int64)
+    units[:wl.route.n_inst] = 4 * 2000
+    step("drain", lambda: eng.queue_drain(qg, d(units)), lambda: o.queue_drain(qo, units))
+    res["parity"] = bool(same)
+    res["note"] = ("host clock per call; append: the re-routed batch into empty queues; "
+                   "migrate: the rebalancing pass's list on its queues; drain: 8,000 units "
+                   "of service per instance")
+    return res
 
 
 def main():

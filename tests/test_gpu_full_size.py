@@ -310,3 +310,37 @@ def test_rebalance_full_size():
     for name in ("rec", "src", "dst", "benefit", "ttft_to"):
         assert np.array_equal(g[name].cpu().numpy()[:cnt], r[name]), name
     assert np.array_equal(g["loads"].cpu().numpy(), r["loads"])
+    # the migration list applied to the queues, then a round of service, on
+    # both sides (the queue operations at full size)
+    qd = [gh.to_dev(x, dev) for x in (q.qoff, q.rec_id, q.unc_here, q.alt, q.unc_alt, q.base_work)]
+    qh = (q.qoff, q.rec_id, q.unc_here, q.alt, q.unc_alt, q.base_work)
+    _say("queue migrate + drain at full size: migrations", cnt)
+    qg = eng.queue_migrate(qd, g["rec"][:cnt], g["src"][:cnt], g["dst"][:cnt])
+    qo = o.queue_migrate(qh, r["rec"], r["src"], r["dst"])
+    for a, b in zip(qg, qo):
+        assert np.array_equal(a.cpu().numpy(), b)
+    units = np.zeros(S, np.int64)
+    units[:n_live] = 8_000
+    qg = eng.queue_drain(qg, gh.to_dev(units, dev))
+    qo = o.queue_drain(qo, units)
+    for a, b in zip(qg, qo):
+        assert np.array_equal(a.cpu().numpy(), b)
+
+
+def test_queue_append_full_batch(large, large_ref):
+    """The whole large batch (1,048,576 routed requests) appended to empty
+    queues on the device and in the oracle."""
+    wl, g, eng, gh = large["wl"], large["g"], large["eng"], large["gh"]
+    S = wl.route.max_slots
+    o = oracle.Oracle(wl.route.as_dict())
+    empty = (np.zeros(S + 1, np.int64), np.zeros(0, np.uint64), np.zeros(0, np.uint32),
+             np.zeros(0, np.uint32), np.zeros(0, np.uint32), np.zeros(S, np.int64))
+    d = lambda a: gh.to_dev(a, eng.device)
+    routed = {"key": None, "ttft": None, "flags": None, "cand": d(large_ref["cand"]),
+              "match": d(large_ref["match"]), "chosen": d(large_ref["chosen"])}
+    _say("queue append of the large batch")
+    qg = eng.queue_append(tuple(d(x) for x in empty), g["offsets"], routed, 7)
+    qo = o.queue_append(empty, g["offsets_np"], large_ref["cand"], large_ref["match"],
+                        large_ref["chosen"], 7)
+    for a, b in zip(qg, qo):
+        assert np.array_equal(a.cpu().numpy(), b)

@@ -67,18 +67,40 @@ __global__ void q_check_kernel(const int64_t* __restrict__ qoff, uint32_t S, int
     }
 }
 
+// Per-instance counts are gathered per workgroup in LDS (dynamic shared
+// memory of k * S words) and added to the device counters once per
+// workgroup: a few hot instances would otherwise take every atomic.
+__device__ __forceinline__ void lds_zero(uint32_t* sh, uint32_t m)
+{
+    for (uint32_t j = threadIdx.x; j < m; j += blockDim.x)
+        sh[j] = 0;
+    __syncthreads();
+}
+
+__device__ __forceinline__ void lds_flush(const uint32_t* sh, uint32_t S,
+                                          unsigned long long* __restrict__ cnt)
+{
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < S; j += blockDim.x)
+        if (sh[j])
+            atomicAdd(&cnt[j], (unsigned long long)sh[j]);
+}
+
 // Histogram of instance ids (bad |= 1 for one past the slots).
 __global__ void q_hist_kernel(const uint32_t* __restrict__ id, uint64_t n, uint32_t S,
                               unsigned long long* __restrict__ cnt, uint32_t* __restrict__ bad)
 {
+    extern __shared__ uint32_t sh[];
+    lds_zero(sh, S);
     for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < n;
          i += (uint64_t)gridDim.x * blockDim.x) {
         const uint32_t c = id[i];
         if (c >= S)
             atomicOr(bad, 1u);
         else
-            atomicAdd(&cnt[c], 1ull);
+            atomicAdd(&sh[c], 1u);
     }
+    lds_flush(sh, S, cnt);
 }
 
 // qoff2[i] = qoff[i] + extra_before[i] (qoff2[S] too); base copied.
@@ -239,15 +261,21 @@ __global__ void q_mig_count_kernel(const uint32_t* __restrict__ msrc,
                                    unsigned long long* __restrict__ in_cnt,
                                    uint32_t* __restrict__ bad)
 {
+    extern __shared__ uint32_t sh[];  // [2 S]: removed, received
+    lds_zero(sh, 2 * S);
     for (uint64_t k = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; k < m;
          k += (uint64_t)gridDim.x * blockDim.x) {
         if (msrc[k] >= S || mdst[k] >= S || at[k] < 0) {
             atomicOr(bad, 1u);
             continue;
         }
-        atomicAdd(&delta_out[msrc[k]], 1ull);
-        atomicAdd(&in_cnt[mdst[k]], 1ull);
+        atomicAdd(&sh[msrc[k]], 1u);
+        atomicAdd(&sh[S + mdst[k]], 1u);
     }
+    lds_flush(sh, S, delta_out);
+    for (uint32_t j = threadIdx.x; j < S; j += blockDim.x)
+        if (sh[S + j])
+            atomicAdd(&in_cnt[j], (unsigned long long)sh[S + j]);
 }
 
 // New queue lengths of the migration: len - removed + received; ex[i] =
@@ -315,6 +343,8 @@ __global__ void q_drain_kernel(QIn a, uint32_t S, int64_t Q, const int64_t* __re
                                const int64_t* __restrict__ units, const uint64_t* __restrict__ hs,
                                uint64_t* __restrict__ popped, unsigned long long* __restrict__ npop)
 {
+    extern __shared__ uint32_t sh[];
+    lds_zero(sh, S);
     for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < Q;
          q += (int64_t)gridDim.x * blockDim.x) {
         const uint32_t i = owner_of(a.qoff, S, q);
@@ -323,8 +353,9 @@ __global__ void q_drain_kernel(QIn a, uint32_t S, int64_t Q, const int64_t* __re
         const uint64_t p = upto <= (uint64_t)left ? 1 : 0;
         popped[q] = p;
         if (p)
-            atomicAdd(&npop[i], 1ull);
+            atomicAdd(&sh[i], 1u);
     }
+    lds_flush(sh, S, npop);
 }
 
 __global__ void q_drain_len_kernel(const int64_t* __restrict__ qoff, uint32_t S,
@@ -492,7 +523,7 @@ dm_status queue_append(dm_ctx* c, const dm_queues* q, const int64_t* offsets, ui
     q_zero_kernel<<<1, 64, 0, st>>>(reinterpret_cast<unsigned long long*>(tot), 2);
     q_check_kernel<<<grid_for(S + 1, 256), 256, 0, st>>>(q->qoff, S, Q, nullptr, nullptr, bad);
     if (n)
-        q_hist_kernel<<<grid_for(n, 256, 1024), 256, 0, st>>>(routed->chosen, n, S, cnt, bad);
+        q_hist_kernel<<<grid_for(n, 256, 1024), 256, 4 * S, st>>>(routed->chosen, n, S, cnt, bad);
     uint32_t badh = 0;
     if ((e = hipMemcpyAsync(&badh, bad, 4, hipMemcpyDeviceToHost, st)) != hipSuccess ||
         (e = hipStreamSynchronize(st)) != hipSuccess)
@@ -583,7 +614,7 @@ dm_status queue_migrate(dm_ctx* c, const dm_queues* q, const uint64_t* mrec,
         q_mig_find_kernel<<<grid_for(Q, 256, 8192), 256, 0, st>>>(a, S, Q, tk, tv, log2, msrc,
                                                                 gone, at);
     if (m)
-        q_mig_count_kernel<<<grid_for(m, 256, 1024), 256, 0, st>>>(msrc, mdst, m, S, at, removed,
+        q_mig_count_kernel<<<grid_for(m, 256, 1024), 256, 8 * S, st>>>(msrc, mdst, m, S, at, removed,
                                                                   in_cnt, bad);
     uint32_t badh = 0;
     if ((e = hipMemcpyAsync(&badh, bad, 4, hipMemcpyDeviceToHost, st)) != hipSuccess ||
@@ -667,7 +698,7 @@ dm_status queue_drain(dm_ctx* c, const dm_queues* q, const int64_t* units,
         q_widen_kernel<<<grid_for(Q, 256, 8192), 256, 0, st>>>(q->unc_here, Q, here64);
         if ((e = exclusive_scan_u64(c, here64, Q, hs, tot)) != hipSuccess)
             return hip_fail(c, e, "dm_queue_drain");
-        q_drain_kernel<<<grid_for(Q, 256, 8192), 256, 0, st>>>(a, S, Q, q->base_work, units, hs,
+        q_drain_kernel<<<grid_for(Q, 256, 1024), 256, 4 * S, st>>>(a, S, Q, q->base_work, units, hs,
                                                               popped, npop);
     }
     const int64_t* base_in = q->base_work;

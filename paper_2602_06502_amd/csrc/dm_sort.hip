@@ -1,6 +1,6 @@
 // Stable LSD radix sort of (u64 key, u32 value) pairs, 8-bit digits.
 // Per pass: tile digit histograms (digit-major), one exclusive scan over
-// them, and a stable scatter.  A tile is 1024 or 4096 items; the scatter ranks
+// them, and a stable scatter.  A tile is 1024 or 2048 items; the scatter ranks
 // equal digits inside each wave with ballots, orders the tile by digit in
 // LDS, and writes each digit's items as one run of consecutive addresses.
 #include "dm_internal.h"
@@ -10,10 +10,10 @@ namespace {
 
 constexpr int kSortThreads = 256;
 constexpr int kSortWaves = kSortThreads / kWave;
-// Items per thread: 16 (4096-item tiles, longer runs per digit) for large
+// Items per thread: 8 (2048-item tiles, longer runs per digit) for large
 // sorts, 4 (1024-item tiles, four times the workgroups) below kBigSort.
 constexpr uint64_t kBigSort = 1ull << 22;
-constexpr uint64_t tile_of(uint64_t n) { return n >= kBigSort ? 16 * kSortThreads : 4 * kSortThreads; }
+constexpr uint64_t tile_of(uint64_t n) { return n >= kBigSort ? 8 * kSortThreads : 4 * kSortThreads; }
 constexpr int kSortSlot = kSlotSort;
 
 template <int kSortItems>
@@ -166,14 +166,14 @@ hipError_t radix_sort_kv(dm_ctx* c, uint64_t* keys, uint32_t* vals, uint64_t* kt
     int passes = 0;
     for (int shift = 0; shift < bits; shift += 8, passes++) {
         if (n >= kBigSort)
-            digit_hist_kernel<16><<<ntiles, kSortThreads, 0, c->stream>>>(sk, n, shift, ntiles, cnt);
+            digit_hist_kernel<8><<<ntiles, kSortThreads, 0, c->stream>>>(sk, n, shift, ntiles, cnt);
         else
             digit_hist_kernel<4><<<ntiles, kSortThreads, 0, c->stream>>>(sk, n, shift, ntiles, cnt);
         e = exclusive_scan_u64(c, cnt, 256 * ntiles, offs, nullptr);
         if (e != hipSuccess)
             return e;
         if (n >= kBigSort)
-            digit_scatter_kernel<16><<<ntiles, kSortThreads, 0, c->stream>>>(sk, sv, n, shift,
+            digit_scatter_kernel<8><<<ntiles, kSortThreads, 0, c->stream>>>(sk, sv, n, shift,
                                                                              ntiles, offs, dk, dv);
         else
             digit_scatter_kernel<4><<<ntiles, kSortThreads, 0, c->stream>>>(sk, sv, n, shift,

@@ -11,7 +11,7 @@ namespace {
 constexpr int kSortThreads = 256;
 constexpr int kSortWaves = kSortThreads / kWave;
 // Items per thread: 8 (2048-item tiles, longer runs per digit) for large
-// sorts, 4 (1024-item tiles, four times the workgroups) below kBigSort.
+// sorts, 4 (1024-item tiles, twice the workgroups) below kBigSort.
 constexpr uint64_t kBigSort = 1ull << 22;
 constexpr uint64_t tile_of(uint64_t n) { return n >= kBigSort ? 8 * kSortThreads : 4 * kSortThreads; }
 constexpr int kSortSlot = kSlotSort;
@@ -98,7 +98,7 @@ __global__ __launch_bounds__(kSortThreads) void digit_scatter_kernel(
         __syncthreads();
         rk[it] = ok ? (wcnt[buf][w][d] & 0xFFFFu) + pr : 0;
     }
-    // (offsets fit the 16 bits below the tag: a tile has at most 4096 items)
+    // (offsets fit the 16 bits below the tag: a tile has at most 2048 items)
     // first place of each digit in the tile (exclusive scan over digits)
     {
         uint32_t x = run[t];

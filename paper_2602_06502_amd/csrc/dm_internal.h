@@ -98,6 +98,7 @@ struct KeyLen {
     uint64_t* list = nullptr;     // [max_nodes] extended prefixes, ascending
     uint64_t n_ext = 0;
     uint64_t* log = nullptr;      // [cap] the window's record
+    uint32_t* roots = nullptr;    // [cap / 32 + 1] bit i: record entry i is a request's root
     unsigned long long* log_n = nullptr;  // entries the window produced (may pass cap)
     uint64_t win = 0;             // requests routed in the current window
 };

@@ -71,7 +71,8 @@ __global__ void kl_append_kernel(uint64_t n, const uint64_t* __restrict__ bstart
                                  const uint64_t* __restrict__ epos,
                                  const uint64_t* __restrict__ ent, uint64_t K,
                                  const uint64_t* __restrict__ hkeys, uint64_t* __restrict__ log,
-                                 uint64_t cap, const unsigned long long* __restrict__ log_n)
+                                 uint32_t* __restrict__ roots, uint64_t cap,
+                                 const unsigned long long* __restrict__ log_n)
 {
     const uint64_t base = *log_n;
     const uint64_t w = blockIdx.x * (uint64_t)(blockDim.x >> 6) +
@@ -84,7 +85,96 @@ __global__ void kl_append_kernel(uint64_t n, const uint64_t* __restrict__ bstart
         for (uint64_t j = lane; j < e; j += kWave)
             if (at + j < cap)
                 log[at + j] = canon_key(src[j]);
+        // the request's first entry (its depth-K prefix) starts its run
+        if (lane == 0 && e && at < cap)
+            atomicOr(&roots[at >> 5], 1u << (at & 31));
     }
+}
+
+// Roots of the record: per 32-entry word its root count (for a scan).
+__global__ void kl_root_count_kernel(const uint32_t* __restrict__ roots, uint64_t nw,
+                                     uint64_t* __restrict__ cnt)
+{
+    for (uint64_t w = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; w < nw;
+         w += (uint64_t)gridDim.x * blockDim.x)
+        cnt[w] = __popc(roots[w]);
+}
+
+// Run (request) of record entry i: the roots at or before it, minus one.
+__device__ __forceinline__ uint64_t kl_run_of(const uint32_t* roots, const uint64_t* wpre,
+                                              uint64_t i)
+{
+    const uint32_t below = roots[i >> 5] & (0xFFFFFFFFu >> (31 - (i & 31)));  // bits <= i
+    return wpre[i >> 5] + __popc(below) - 1;
+}
+
+// Each run's root key, in record order.
+__global__ void kl_root_keys_kernel(const uint64_t* __restrict__ log, uint64_t m,
+                                    const uint32_t* __restrict__ roots,
+                                    const uint64_t* __restrict__ wpre, uint64_t* __restrict__ rk)
+{
+    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < m;
+         i += (uint64_t)gridDim.x * blockDim.x)
+        if ((roots[i >> 5] >> (i & 31)) & 1)
+            rk[kl_run_of(roots, wpre, i)] = log[i];
+}
+
+// Over the sorted root keys: at the first of each run of equal keys, flag
+// it when its count c (requests carrying that depth-K prefix) has
+// c n >= W.  No prefix under a root without it can reach c n >= W.
+__global__ void kl_hot_root_kernel(const uint64_t* __restrict__ keys, uint64_t m, uint64_t W,
+                                   uint64_t n_live, uint64_t* __restrict__ flag)
+{
+    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < m;
+         i += (uint64_t)gridDim.x * blockDim.x) {
+        const uint64_t key = keys[i];
+        uint64_t f = 0;
+        if (i == 0 || keys[i - 1] != key) {
+            uint64_t lo = i + 1, hi = m;
+            while (lo < hi) {
+                const uint64_t mid = lo + (hi - lo) / 2;
+                if (keys[mid] == key)
+                    lo = mid + 1;
+                else
+                    hi = mid;
+            }
+            f = (lo - i) * n_live >= W ? 1 : 0;
+        }
+        flag[i] = f;
+    }
+}
+
+// Is key among the h sorted hot roots?
+__device__ __forceinline__ bool kl_is_hot(const uint64_t* hot, uint64_t h, uint64_t key)
+{
+    uint64_t lo = 0, hi = h;
+    while (lo < hi) {
+        const uint64_t mid = lo + (hi - lo) / 2;
+        if (hot[mid] < key)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo < h && hot[lo] == key;
+}
+
+// keep[i] = 1 for record entries whose run has a hot root.
+__global__ void kl_keep_kernel(uint64_t m, const uint32_t* __restrict__ roots,
+                               const uint64_t* __restrict__ wpre, const uint64_t* __restrict__ rk,
+                               const uint64_t* __restrict__ hot, const uint64_t* __restrict__ h_p,
+                               uint64_t* __restrict__ keep)
+{
+    const uint64_t h = *h_p;
+    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < m;
+         i += (uint64_t)gridDim.x * blockDim.x)
+        keep[i] = h && kl_is_hot(hot, h, rk[kl_run_of(roots, wpre, i)]) ? 1 : 0;
+}
+
+__global__ void kl_zero_u32_kernel(uint32_t* __restrict__ p, uint64_t n)
+{
+    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < n;
+         i += (uint64_t)gridDim.x * blockDim.x)
+        p[i] = 0;
 }
 
 __global__ void kl_advance_kernel(unsigned long long* __restrict__ log_n,
@@ -171,6 +261,8 @@ void keylen_free(dm_ctx* c)
     for (uint64_t* p : {k.tab[0], k.tab[1], k.list, k.log})
         if (p)
             (void)hipFree(p);
+    if (k.roots)
+        (void)hipFree(k.roots);
     if (k.log_n)
         (void)hipFree(k.log_n);
     k = KeyLen{};
@@ -193,7 +285,7 @@ hipError_t keylen_record(dm_ctx* c, uint64_t n, const uint64_t* bstart, const ui
     if (e != hipSuccess)
         return e;
     kl_append_kernel<<<grid_for(n, 4, 16384), 256, 0, c->stream>>>(n, bstart, epos, ent, K, hkeys,
-                                                                   k.log, k.cap, k.log_n);
+                                                                   k.log, k.roots, k.cap, k.log_n);
     kl_advance_kernel<<<1, 1, 0, c->stream>>>(k.log_n, total, k.cap, c->d_status);
     return hipGetLastError();
 }
@@ -220,7 +312,8 @@ dm_status keylen_enable(dm_ctx* c, uint64_t max_nodes, uint64_t max_window_block
     if ((e = hipMalloc(&k.tab[0], slots * 8)) == hipSuccess &&
         (e = hipMalloc(&k.tab[1], slots * 8)) == hipSuccess &&
         (e = hipMalloc(&k.list, max_nodes * 8)) == hipSuccess &&
-        (e = hipMalloc(&k.log, k.cap * 8)) == hipSuccess)
+        (e = hipMalloc(&k.log, k.cap * 8)) == hipSuccess &&
+        (e = hipMalloc(&k.roots, (k.cap / 32 + 1) * 4)) == hipSuccess)
         e = hipMalloc(&k.log_n, 8);
     c->kl = k;
     if (e != hipSuccess) {
@@ -229,6 +322,8 @@ dm_status keylen_enable(dm_ctx* c, uint64_t max_nodes, uint64_t max_window_block
     }
     c->kl.on = true;
     kl_fill_kernel<<<grid_for(slots, 256), 256, 0, c->stream>>>(c->kl.tab[0], slots, kEmpty);
+    kl_zero_u32_kernel<<<grid_for(k.cap / 32 + 1, 256, 8192), 256, 0, c->stream>>>(
+        c->kl.roots, k.cap / 32 + 1);
     reset_window(c);
     if ((e = hipGetLastError()) == hipSuccess)
         e = hipStreamSynchronize(c->stream);
@@ -252,6 +347,8 @@ dm_status keylen_window(dm_ctx* c)
     hipStream_t st = c->stream;
     if (M > k.cap) {
         reset_window(c);
+        kl_zero_u32_kernel<<<grid_for(k.cap / 32 + 1, 256, 8192), 256, 0, st>>>(k.roots,
+                                                                              k.cap / 32 + 1);
         if ((e = hipStreamSynchronize(st)) != hipSuccess)
             return hip_fail(c, e, "dm_keylen_window");
         return fail(c, DM_EFULL, "dm_keylen_window: the window held more prefixes than its "
@@ -262,25 +359,69 @@ dm_status keylen_window(dm_ctx* c)
         e = hipStreamSynchronize(st);
         return e == hipSuccess ? DM_OK : hip_fail(c, e, "dm_keylen_window");
     }
-    const uint64_t Ma = M ? M : 1, outcap = k.max_nodes + 1;
+    const uint64_t Ma = M ? M : 1, outcap = k.max_nodes + 1, nw = (Ma + 31) / 32;
     uint8_t* w = static_cast<uint8_t*>(scratch_get(
-        c, kSlotMembers, 3 * up256k(8 * Ma) + up256k(8 * outcap) + 512, &e));
+        c, kSlotMembers, 3 * up256k(8 * Ma) + up256k(8 * outcap) + 2 * up256k(8 * nw) + 1024, &e));
     if (!w)
         return hip_fail(c, e, "dm_keylen_window");
     uint64_t* ktmp = carve<uint64_t>(w, Ma);
     uint64_t* flag = carve<uint64_t>(w, Ma);
     uint64_t* pos = carve<uint64_t>(w, Ma);
     uint64_t* out = carve<uint64_t>(w, outcap);
-    uint64_t* count = carve<uint64_t>(w, 1);
-    kl_fill_kernel<<<1, 64, 0, st>>>(count, 1, 0);
+    uint64_t* wcnt = carve<uint64_t>(w, nw);
+    uint64_t* wpre = carve<uint64_t>(w, nw);
+    uint64_t* count = carve<uint64_t>(w, 4);
+    kl_fill_kernel<<<1, 64, 0, st>>>(count, 4, 0);
     if (M) {
-        const uint32_t g = grid_for(M, 256, 8192);
-        if ((e = radix_sort_kv(c, k.log, nullptr, ktmp, nullptr, M, 64)) != hipSuccess)
+        // Only prefixes under a root (depth-K prefix) carried by at least
+        // W / n requests can be kept (a prefix's count never exceeds its
+        // root's): count the roots first, one per request, and sort only
+        // the entries of requests with such a root.
+        kl_root_count_kernel<<<grid_for(nw, 256, 8192), 256, 0, st>>>(k.roots, nw, wcnt);
+        uint64_t R = 0;
+        if ((e = exclusive_scan_u64(c, wcnt, nw, wpre, count + 1)) != hipSuccess ||
+            (e = hipMemcpyAsync(&R, count + 1, 8, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+            (e = hipStreamSynchronize(st)) != hipSuccess)
             return hip_fail(c, e, "dm_keylen_window");
-        kl_decide_kernel<<<g, 256, 0, st>>>(k.log, M, k.tab[k.cur], k.log2, W, c->n_live, flag);
-        if ((e = exclusive_scan_u64(c, flag, M, pos, count)) != hipSuccess)
+        const uint64_t Ra = R ? R : 1;
+        uint8_t* rw = static_cast<uint8_t*>(
+            scratch_get(c, kSlotProbe, 6 * up256k(8 * Ra) + 256, &e));
+        if (!rw)
             return hip_fail(c, e, "dm_keylen_window");
-        kl_compact_kernel<<<g, 256, 0, st>>>(k.log, flag, pos, M, out, outcap);
+        uint64_t* rk = carve<uint64_t>(rw, Ra);     // each run's root, record order
+        uint64_t* rs = carve<uint64_t>(rw, Ra);     // the same, sorted
+        uint64_t* rtmp = carve<uint64_t>(rw, Ra);
+        uint64_t* rflag = carve<uint64_t>(rw, Ra);
+        uint64_t* rpos = carve<uint64_t>(rw, Ra);
+        uint64_t* hot = carve<uint64_t>(rw, Ra);
+        const uint32_t g = grid_for(M, 256, 8192), gr = grid_for(Ra, 256, 8192);
+        kl_root_keys_kernel<<<g, 256, 0, st>>>(k.log, M, k.roots, wpre, rk);
+        uint64_t Mk = 0;
+        if ((e = hipMemcpyAsync(rs, rk, 8 * R, hipMemcpyDeviceToDevice, st)) != hipSuccess ||
+            (e = radix_sort_kv(c, rs, nullptr, rtmp, nullptr, R, 64)) != hipSuccess)
+            return hip_fail(c, e, "dm_keylen_window");
+        kl_hot_root_kernel<<<gr, 256, 0, st>>>(rs, R, W, c->n_live, rflag);
+        if ((e = exclusive_scan_u64(c, rflag, R, rpos, count + 2)) != hipSuccess)
+            return hip_fail(c, e, "dm_keylen_window");
+        kl_compact_kernel<<<gr, 256, 0, st>>>(rs, rflag, rpos, R, hot, Ra);
+        kl_keep_kernel<<<g, 256, 0, st>>>(M, k.roots, wpre, rk, hot, count + 2, flag);
+        if ((e = exclusive_scan_u64(c, flag, M, pos, count + 3)) != hipSuccess)
+            return hip_fail(c, e, "dm_keylen_window");
+        kl_compact_kernel<<<g, 256, 0, st>>>(k.log, flag, pos, M, ktmp, Ma);
+        if ((e = hipMemcpyAsync(&Mk, count + 3, 8, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+            (e = hipStreamSynchronize(st)) != hipSuccess)
+            return hip_fail(c, e, "dm_keylen_window");
+        if (Mk) {
+            const uint32_t gk = grid_for(Mk, 256, 8192);
+            if ((e = radix_sort_kv(c, ktmp, nullptr, pos, nullptr, Mk, 64)) != hipSuccess)
+                return hip_fail(c, e, "dm_keylen_window");
+            kl_decide_kernel<<<gk, 256, 0, st>>>(ktmp, Mk, k.tab[k.cur], k.log2, W, c->n_live,
+                                                 flag);
+            if ((e = exclusive_scan_u64(c, flag, Mk, pos, count)) != hipSuccess)
+                return hip_fail(c, e, "dm_keylen_window");
+            kl_compact_kernel<<<gk, 256, 0, st>>>(ktmp, flag, pos, Mk, out, outcap);
+        }
+        kl_zero_u32_kernel<<<grid_for(nw, 256, 8192), 256, 0, st>>>(k.roots, nw);
     }
     uint64_t n_next = 0;
     if ((e = hipGetLastError()) != hipSuccess ||

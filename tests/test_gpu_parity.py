@@ -336,6 +336,63 @@ def test_keylen_window_spans_batches_and_errors():
         eng.keylen_tree()
 
 
+def test_keylen_close_without_hot_roots_and_after_overflow():
+    """Window closes that keep nothing (distinct random prompts: no root is
+    carried by W / n requests; prompts shorter than K blocks: no record
+    entries) after a window that built a tree, and a normal window after
+    one whose record overflowed: the trees against the oracle's."""
+    gh = _h()
+    import paper_2602_06502_amd as pk
+    B, K = 16, 2
+    wl = workloads.small_random(83, 6, 8, B, 64, key_blocks=K)
+    eng, o = gh.engine_for(wl), oh.oracle_for(wl)
+    L = workloads.initial_loads(wl, wl.route.max_slots)
+    d = lambda a: gh.to_dev(a, eng.device)
+    rng = np.random.default_rng(17)
+
+    def window(tok, off):
+        eng.route(d(tok), d(off), d(L))
+        o.route(tok, off, L)
+        eng.keylen_window()
+        assert o.keylen_window() == oracle.OK
+        t = eng.keylen_tree()
+        assert np.array_equal(t, o.keylen_tree())
+        return t
+
+    def random_batch(n, lo, hi):
+        lens = rng.integers(lo, hi, size=n)
+        off = np.zeros(n + 1, np.int64)
+        off[1:] = np.cumsum(lens)
+        return rng.integers(0, 1 << 20, size=int(off[-1])).astype(np.int32), off
+
+    eng.keylen_enable(1024, 1 << 20)
+    o.keylen_enable(1024)
+    hot = _hot_batches(19, B, K, 2)
+    assert len(window(*hot[0])) > 0
+    _say("keylen: a window of distinct prompts")
+    assert len(window(*random_batch(500, 4 * B, 30 * B))) == 0
+    assert len(window(*hot[1])) > 0
+    _say("keylen: a window of prompts shorter than K blocks")
+    assert len(window(*random_batch(300, 0, K * B))) == 0
+    # a window whose record overflows (the close fails, the tree and the
+    # window start over), then a window that fits, on the same context
+    tok1, off1 = hot[1]
+    m = 40
+    small = (tok1[:off1[m]], off1[:m + 1])
+    cap = int(np.maximum(np.diff(small[1]) // B - K + 1, 0).sum())
+    eng.keylen_enable(1024, cap)
+    assert o.keylen_enable(1024) == oracle.OK
+    tok, off = hot[0]
+    eng.route(d(tok), d(off), d(L))
+    with pytest.raises(pk.DMError) as ei:
+        eng.sync()
+    assert ei.value.status == pk.DM_EFULL
+    with pytest.raises(pk.DMError):
+        eng.keylen_window()
+    _say("keylen: a window after an overflowed one, record of", cap)
+    assert len(window(*small)) > 0
+
+
 # ---------------------------------------------------------------------------
 # KV save with LRU eviction
 # ---------------------------------------------------------------------------

@@ -62,6 +62,24 @@ def load_traffic(name, files):
     return d.get("bytes_per_launch")
 
 
+# Integer issue peak of the chip: 256 CUs x 4 SIMDs x 16 lanes at 2.4 GHz
+# (one 32-bit integer lane-op per lane per clock); a wave-wide VALU
+# instruction occupies a SIMD for 4 clocks.
+INT_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4
+
+
+def load_valu(name, files):
+    """VALU instruction counts per launch (rocprofv3 SQ_INSTS_* counters), if
+    recorded for the current kernel sources."""
+    p = os.path.join(ROOT, "profiles", name)
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        d = json.load(f)
+    return d if d.get("source_hash") == source_hash(files) else None
+
+
 def host_cpu():
     """(logical CPUs, model name) of the host."""
     model = "unknown"
@@ -688,6 +706,7 @@ def main():
     achieved = hbytes / (hashm_avg * 1e-3) / 1e9
     stage_gbs = sbytes / ((groups_avg + hashm_avg) * 1e-3) / 1e9
     hash_traffic = load_traffic("traffic_hash_kernel_large.json", HASH_SOURCES)
+    valu = load_valu("valu_hash_pass_large.json", HASH_SOURCES)
     stage_traffic = load_traffic("traffic_route_stage_large.json", STAGE_SOURCES)
     final = loads[args.warmup + args.steps - 1].cpu().numpy()[:wl.route.n_inst].astype(np.float64)
     flags = out["flags"].cpu().numpy()
@@ -757,6 +776,19 @@ def main():
                                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                      "frac": achieved / HBM_PEAK_GBS, "traffic": hash_traffic,
                                      "algorithmic_bytes_per_launch": hbytes, "ms": hashm_avg},
+        "integer_ops": None if valu is None else {
+            "kernels": valu["kernels"],
+            "int_lane_ops_per_launch": valu["int_lane_ops"],
+            "achieved_tops": valu["int_lane_ops"] / (hashm_avg * 1e-3) / 1e12,
+            "peak_tops": INT_PEAK_TOPS,
+            "frac": valu["int_lane_ops"] / (hashm_avg * 1e-3) / 1e12 / INT_PEAK_TOPS,
+            "valu_insts_per_launch": valu["valu_insts"],
+            "valu_issue_frac": valu["valu_insts"] / (hashm_avg * 1e-3) / VALU_ISSUE_PEAK,
+            "note": "rocprofv3 SQ_INSTS_VALU_INT32 + SQ_INSTS_VALU_INT64 (x 64 lanes) and "
+                    "SQ_INSTS_VALU per batch over the hash and match pass "
+                    "(profiles/route_large_valu_counters.md), over this run's pass time; "
+                    "peak: one 32-bit integer op per lane per clock on 256 CUs x 4 SIMDs x "
+                    "16 lanes at 2.4 GHz (64-bit multiplies take several)"},
         "routing_stats": {"slo_switch_frac": float((flags & 1).mean()),
                           "both_over_frac": float(((flags >> 1) & 1).mean()),
                           "hit_blocks_frac": float(

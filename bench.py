@@ -123,9 +123,11 @@ def walk_steps(cand, match, n, block=1024, lanes=64, run_max=3):
     both instances is one request of the same pair with the same
     cache-affine candidate (the one with more cached blocks, c1 on equal
     matches) joins that request's run, at its level, while the run holds
-    fewer than `run_max` requests.  Whole consecutive levels are packed into
-    windows of at most `lanes` requests; a larger level is split with runs
-    kept whole.  Steps = the sum of the windows' level counts."""
+    fewer than `run_max` requests.  A level of more than `lanes` requests is
+    cut, runs kept whole, into parts of at most `lanes`; every part is one
+    depth step.  Windows take consecutive parts and hold two sets of `lanes`
+    lanes, the depths alternating between the sets: a window grows while
+    both sets' parts fit and its depth stays within 64."""
     c1, c2 = cand[:n].tolist(), cand[n:].tolist()
     m1, m2 = match[:n].tolist(), match[n:].tolist()
     steps = windows = 0
@@ -147,23 +149,25 @@ def walk_steps(cand, match, n, block=1024, lanes=64, run_max=3):
                 unit[i] = [1]
                 units.setdefault(lv[i], []).append(unit[i])
             last[a] = last[o] = i
-        used = dep = 0
+        parts = []
         for L in range(1, max(units) + 1):
-            sizes = [u[0] for u in units[L]]
-            if used and used + sum(sizes) > lanes:
-                steps += dep
+            part = 0
+            for sz in (u[0] for u in units[L]):
+                if part + sz > lanes:
+                    parts.append(part)
+                    part = 0
+                part += sz
+            parts.append(part)
+        steps += len(parts)
+        # sums of the window's parts at an even (s0) and an odd (s1)
+        # distance from its last depth: appending a part swaps them
+        s0 = s1 = dep = 0
+        for c in parts:
+            if dep and (dep == 64 or c + s1 > lanes):
                 windows += 1
-                used = dep = 0
-            dep += 1
-            for sz in sizes:
-                if used + sz > lanes:
-                    steps += dep
-                    windows += 1
-                    used, dep = 0, 1
-                used += sz
-        if used:
-            steps += dep
-            windows += 1
+                s0 = s1 = dep = 0
+            s0, s1, dep = c + s1, s0, dep + 1
+        windows += 1
     return steps, windows
 
 
@@ -746,7 +750,8 @@ def main():
                          "depth_steps": depth_steps, "windows": walk_windows,
                          "depth_steps_without_runs": depth_steps_no_runs,
                          "ns_per_step": ref_stage[2] * 1e6 / depth_steps,
-                         "note": "one wave walks windows of up to 64 requests packed from the "
+                         "note": "one wave walks windows of up to 2 x 64 requests (one lane "
+                                 "set for even depths, one for odd) packed from the "
                                  "dependency levels of 1024-request blocks, runs of up to three "
                                  "same-pair requests sharing a level; each step is an LDS "
                                  "round trip plus the run replay and the decision; time from "

@@ -173,7 +173,7 @@ typedef struct {
  * rings (DM_ESTATE otherwise).  The call does not wait for the device: its
  * work arrays are sized from n and n_tokens (they grow, synchronising once,
  * only when a batch needs more than any before it).  n = 0 is a no-op; n must be at most
- * 1,908,874,240 (DM_EINVAL): the selection indexes its per-request slots in
+ * 954,436,608 (DM_EINVAL): the selection indexes its per-request slots in
  * 32 bits.  Match lengths are 32-bit: a request with 2^32 or more full
  * blocks sets the device status word (DM_EINVAL from dm_sync). */
 dm_status dm_route_batch(dm_ctx* ctx, const int32_t* tokens, uint64_t n_tokens,
@@ -187,7 +187,7 @@ dm_status dm_route_batch(dm_ctx* ctx, const int32_t* tokens, uint64_t n_tokens,
  * static area of 64 MiB per GPU that the library holds until the process
  * ends, instead of the context's growable scratch: the call allocates and
  * frees nothing.  The batch is planned on the host first; if its work
- * arrays do not fit (about 360 bytes per request plus, when block_keys is
+ * arrays do not fit (about 550 bytes per request plus, when block_keys is
  * NULL, 8 bytes per n_tokens / B), the call returns DM_EINVAL with the
  * sizes in dm_last_error and launches nothing.  Runs unpipelined on the
  * context's stream (after any pipelined batch).  Every call on one GPU

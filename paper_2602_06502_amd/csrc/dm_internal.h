@@ -29,9 +29,10 @@ constexpr uint32_t kBucket = 8;     // slots per probe bucket (one 64-byte line)
 constexpr uint32_t kErrInval = 1u;
 constexpr uint32_t kErrFull = 2u;
 // Largest batch dm_route_batch takes: the selection gives each block of 1024
-// requests room for 36 windows of 64 lanes and indexes those lanes in 32 bits.
+// requests room for 36 windows of two sets of 64 lanes and indexes those
+// lanes in 32 bits.
 constexpr uint64_t kSelBlock = 1024, kSelWindowsPerBlock = 36;
-constexpr uint64_t kMaxRouteBatch = (0xFFFFFFFFull / (kSelWindowsPerBlock * 64)) * kSelBlock;
+constexpr uint64_t kMaxRouteBatch = (0xFFFFFFFFull / (kSelWindowsPerBlock * 2 * 64)) * kSelBlock;
 
 // Hash parameters of both functions, computed on the host at dm_create.
 // For function s: key words kk[s][0..B), odd multiplier P, its inverse

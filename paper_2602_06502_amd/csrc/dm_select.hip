@@ -22,7 +22,9 @@
 //   sel_level_kernel  one wave per block of 1024 requests: the dependency
 //                     level of every request inside its block (runs of up
 //                     to three same-pair requests sharing a level), and the
-//                     packing of whole levels into windows of 64 lanes;
+//                     packing of whole levels into windows of two sets of
+//                     64 lanes (one set for the window's even depths, one
+//                     for its odd ones);
 //   sel_scan_kernel,  the windows' places, the walk records of every
 //   sel_fill_kernel   window lane and each request's slot;
 //   select_fast_kernel one wave walks the windows in order and, inside a
@@ -315,7 +317,10 @@ __global__ __launch_bounds__(256) void sel_base_kernel(const int64_t* __restrict
 }
 
 constexpr uint32_t kFastMaxLive = 256;
-constexpr int kPrefetch = 12;  // record windows in flight ahead of the walk
+constexpr int kPrefetch = 6;  // record windows in flight ahead of the walk
+// Lane sets of a window: every lane holds one request for the window's steps
+// of even number and one for its steps of odd number.
+constexpr uint32_t kSets = 2;
 
 // grow[0..n_live) and the bad-record word grow[kMaxSlots] start at zero.
 __global__ void sel_zero_kernel(unsigned long long* __restrict__ grow, uint32_t n_live)
@@ -433,11 +438,15 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
 // the requests (runs) of one level touch pairwise distinct instances, and
 // any order of the levels' requests that keeps levels in order and the
 // blocks in order gives every request exactly the loads of the one-by-one
-// walk.  Windows of at most 64 lanes take whole consecutive levels; a level
-// that does not fit starts a new window, and a level of more than 64
-// requests is split between windows with runs kept whole.  Any two
-// consecutive windows of a block hold more than 64 - kRunMax requests, so a
-// block has at most 2 * ceil(kLevelBlock / 62) + 1 windows.
+// walk.  A level of more than 64 requests is cut, runs kept whole, into
+// parts of at most 64, each part a depth of its own.  Windows take
+// consecutive parts, one per depth, and hold two sets of 64 lanes: the
+// depths alternate between the sets (steps of even and odd number), so a
+// window holds up to 128 requests.  Packing the same parts into windows of
+// one set of 64 lanes would close a window only when the next part does not
+// fit, so any two consecutive such windows hold more than 64 requests and a
+// block needs at most 2 * ceil(kLevelBlock / 65) + 1 = 33 of them; the
+// two-set packing needs no more.
 constexpr uint32_t kLevelBlock = 1024;
 constexpr uint32_t kWinCap = 36;  // windows per block; the bound above is 35
 static_assert(kLevelBlock == kSelBlock && kWinCap == kSelWindowsPerBlock,
@@ -447,7 +456,7 @@ static_assert(kLevelBlock == kSelBlock && kWinCap == kSelWindowsPerBlock,
 // position in its run << 6 | (not the run's last) << 8 | run's first member
 // << 9 | run's second member << 19 (block-local indices); per block, its
 // window count, each window's depth and the block-local request index in
-// every window lane (0xFFFF for none).  The result is that of taking the
+// every lane of both sets of every window (0xFFFF for none).  The result is that of taking the
 // requests one by one; the wave takes them 64 at a time, in order:
 //   - the latest earlier request on each instance: within the chunk from
 //     per-instance lane masks, before it from the latest request of the
@@ -462,8 +471,7 @@ static_assert(kLevelBlock == kSelBlock && kWinCap == kSelWindowsPerBlock,
 //   - then, chunk by chunk again with the runs' sizes final, each run takes
 //     its lanes within its level after the runs that start earlier
 //     (ballots per level);
-//   - lane 0 walks the levels in order to place them into windows, run by run
-//     for a level of more than 64 requests.
+//   - lane 0 cuts the levels into parts and places the parts into windows.
 // Every LDS access is by this one wave, so no barrier is needed.
 __global__ __launch_bounds__(kWave) void sel_level_kernel(
     const SelPack* __restrict__ prep, uint64_t n, uint32_t* __restrict__ info,
@@ -480,13 +488,14 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
     __shared__ uint8_t has1[kLevelBlock], has2[kLevelBlock];  // a run has a 2nd / 3rd member
     __shared__ __align__(16) uint16_t key[kLevelBlock];  // a run's first member: level << 2 | size
     __shared__ uint16_t hrank[kLevelBlock];    // lanes of earlier runs of the same level
-    __shared__ uint32_t cnt[kLevelBlock + 1];  // requests per level (so far)
+    __shared__ uint32_t cnt[kLevelBlock + 2];  // requests per level (so far), then
+                                               // each level's first part
     __shared__ uint16_t lstart[kLevelBlock + 1];
-    __shared__ uint8_t lwin[kLevelBlock + 1], lbase[kLevelBlock + 1], ldep[kLevelBlock + 1];
-    __shared__ uint8_t lsplit[kLevelBlock + 1];
     __shared__ uint16_t sorted[kLevelBlock];   // requests by level, runs in order
-    __shared__ uint8_t rwin[kLevelBlock], rlane[kLevelBlock], rdep[kLevelBlock];
-    __shared__ uint16_t smap[kWinCap * kWave];
+    __shared__ uint16_t pl_s0[kLevelBlock];     // part: first index in sorted
+    __shared__ uint8_t pl_win[kLevelBlock], pl_lane[kLevelBlock];  // window, set << 6 | lane
+    __shared__ uint16_t wfirst[kWinCap];        // first part of each window
+    __shared__ uint16_t smap[kWinCap * kSets * kWave];
     __shared__ uint8_t wdep[kWinCap];
     const uint32_t lane = (uint32_t)lane_id();
     const uint64_t r0 = (uint64_t)blockIdx.x * kLevelBlock;
@@ -494,9 +503,9 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
     const unsigned long long below = (1ull << lane) - 1, above = ~below << 1;
     for (uint32_t k = lane; k < kFastMaxLive; k += kWave)
         last[k] = 0;
-    for (uint32_t k = lane; k <= kLevelBlock; k += kWave)
+    for (uint32_t k = lane; k < kLevelBlock + 2; k += kWave)
         cnt[k] = 0;
-    for (uint32_t k = lane; k < kWinCap * kWave; k += kWave)
+    for (uint32_t k = lane; k < kWinCap * kSets * kWave; k += kWave)
         smap[k] = 0xFFFF;
     {
         // all pair codes first: sixteen loads in flight per lane, one wait
@@ -626,56 +635,79 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
         sorted[lstart[lv[t]] + hrank[hd[t]] + psn[t]] = (uint16_t)t;
     uint32_t nwin = 0, okw = 0;
     if (lane == 0) {
-        uint32_t win = 0, lanes = 0, dep = 0;
-        bool ok = true;
-        for (uint32_t l = 1; l <= lmax && ok; l++) {
-            const uint32_t c = cnt[l];
-            if (lanes > 0 && lanes + c > kWave) {  // the level does not fit: next window
-                wdep[win++] = (uint8_t)dep;
-                lanes = dep = 0;
-            }
-            dep++;
-            if (win >= kWinCap) {
-                ok = false;
-                break;
-            }
+        // parts: a level of at most 64 requests is one part; a larger one is
+        // cut run by run into parts of at most 64 (its requests are
+        // independent, so its parts may take consecutive depths).  The parts
+        // cover sorted in order, so part p holds [pl_s0[p], pl_s0[p + 1]);
+        // cnt[l] becomes level l's first part once its size is read.
+        uint32_t npl = 0;
+        for (uint32_t l = 1; l <= lmax; l++) {
+            const uint32_t c = cnt[l], s0 = lstart[l];
+            cnt[l] = npl;
             if (c <= kWave) {
-                lsplit[l] = 0;
-                lwin[l] = (uint8_t)win;
-                lbase[l] = (uint8_t)lanes;
-                ldep[l] = (uint8_t)(dep - 1);
-                lanes += c;
+                pl_s0[npl++] = (uint16_t)s0;
                 continue;
             }
-            // a level of more than 64 requests: run by run, split between windows
-            lsplit[l] = 1;
-            for (uint32_t k = lstart[l]; k < lstart[l] + c;) {
-                const uint32_t u = sorted[k], sz = key[u] & 3u;
-                if (lanes + sz > kWave) {
-                    wdep[win++] = (uint8_t)dep;
-                    lanes = 0;
-                    dep = 1;
-                    if (win >= kWinCap) {
-                        ok = false;
-                        break;
-                    }
+            uint32_t part = 0;
+            pl_s0[npl++] = (uint16_t)s0;
+            for (uint32_t k = s0; k < s0 + c;) {
+                const uint32_t sz = key[sorted[k]] & 3u;  // k is a run's first member
+                if (part + sz > kWave) {
+                    pl_s0[npl++] = (uint16_t)k;
+                    part = 0;
                 }
-                for (uint32_t m = 0; m < sz; m++) {
-                    const uint32_t v = sorted[k + m];
-                    rwin[v] = (uint8_t)win;
-                    rlane[v] = (uint8_t)(lanes + m);
-                    rdep[v] = (uint8_t)(dep - 1);
-                }
-                lanes += sz;
+                part += sz;
                 k += sz;
             }
         }
-        if (ok && lanes > 0) {
-            if (win >= kWinCap)
+        cnt[lmax + 1] = npl;
+        auto psize = [&](uint32_t p) -> uint32_t {
+            return (p + 1 < npl ? (uint32_t)pl_s0[p + 1] : nb) - pl_s0[p];
+        };
+        // windows of consecutive parts, one depth each: a window of depth D
+        // is entered at step e = -D mod 16, so depth t runs on step e + t and
+        // takes the lane set of that step's parity.  S0 and S1 sum the parts
+        // at an even and an odd distance from the window's last depth (sets
+        // 1 and 0); appending a part moves every other part one further, so
+        // the window grows while c + S1 <= 64 and the depth stays below 65.
+        // A window that fits holds every window inside it, so closing at the
+        // first misfit gives the fewest windows; any window that fits one
+        // set of 64 lanes fits the two, so the bound of kWinCap holds.
+        bool ok = true;
+        uint32_t win = 0, first = 0, D = 0, S0 = 0, S1 = 0;
+        auto close = [&](uint32_t end) {
+            if (win >= kWinCap) {
                 ok = false;
-            else
-                wdep[win++] = (uint8_t)dep;
+                return;
+            }
+            const uint32_t e = (0u - D) & 15u;
+            uint32_t base0 = 0, base1 = 0;
+            for (uint32_t p = first; p < end; p++) {
+                const uint32_t odd = (e + (p - first)) & 1u, c = psize(p);
+                pl_win[p] = (uint8_t)win;
+                pl_lane[p] = (uint8_t)(odd << 6 | (odd ? base1 : base0));
+                if (odd)
+                    base1 += c;
+                else
+                    base0 += c;
+            }
+            wfirst[win] = (uint16_t)first;
+            wdep[win++] = (uint8_t)D;
+        };
+        for (uint32_t p = 0; p < npl && ok; p++) {
+            const uint32_t c = psize(p);
+            if (D > 0 && (D == kWave || c + S1 > kWave)) {
+                close(p);
+                first = p;
+                D = S0 = S1 = 0;
+            }
+            const uint32_t s0n = c + S1;
+            S1 = S0;
+            S0 = s0n;
+            D++;
         }
+        if (ok && D > 0)
+            close(npl);
         if (!ok) {  // cannot happen (see above); no window of this block is walked
             atomicOr(status, kErrInval);
             win = 0;
@@ -688,23 +720,19 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
     if (okw) {
         for (uint32_t t = lane; t < nb; t += kWave) {
             const uint32_t L = lv[t], pos = psn[t], h = hd[t], rs = 1u + has1[h] + has2[h];
-            uint32_t win, ln, d;
-            if (!lsplit[L]) {
-                win = lwin[L];
-                ln = lbase[L] + hrank[h] + pos;
-                d = ldep[L];
-            } else {
-                win = rwin[t];
-                ln = rlane[t];
-                d = rdep[t];
-            }
-            smap[win * kWave + ln] = (uint16_t)t;
+            const uint32_t k = lstart[L] + hrank[h] + pos;  // index in sorted
+            uint32_t p = cnt[L];
+            while (p + 1 < cnt[L + 1] && pl_s0[p + 1] <= k)
+                p++;
+            const uint32_t w = pl_win[p], pl = pl_lane[p], set = pl >> 6;
+            const uint32_t ln = (pl & 63u) + (k - pl_s0[p]), d = p - wfirst[w];
+            smap[(w * kSets + set) * kWave + ln] = (uint16_t)t;
             const uint32_t m1 = pos == 2 ? (uint32_t)P[t] : 0u;
             info[r0 + t] = d | pos << 6 | (pos + 1 < rs ? 1u << 8 : 0u) | h << 9 | m1 << 19;
         }
     }
-    for (uint32_t k = lane; k < kWinCap * kWave; k += kWave)
-        slotmap[(uint64_t)blockIdx.x * kWinCap * kWave + k] = smap[k];
+    for (uint32_t k = lane; k < kWinCap * kSets * kWave; k += kWave)
+        slotmap[(uint64_t)blockIdx.x * kWinCap * kSets * kWave + k] = smap[k];
     if (lane < kWinCap)
         wdepth[(uint64_t)blockIdx.x * kWinCap + lane] = lane < nwin ? wdep[lane] : 0;
     if (lane == 0)
@@ -749,9 +777,10 @@ __global__ __launch_bounds__(1024) void sel_scan_kernel(const uint32_t* __restri
         total[0] = carry;
 }
 
-// One wave per (block, window) of capacity, then 2 * kPrefetch padding
-// windows: the walk records of every lane (inert past the window's
-// requests) and each request's slot.
+// One wave per lane set of every (block, window) of capacity, then of
+// 2 * kPrefetch padding windows: the walk records of every lane (inert past
+// the set's requests) and each request's slot.  The records of window w's
+// set s start at (w * kSets + s) * 64.
 __global__ __launch_bounds__(4 * kWave) void sel_fill_kernel(
     const SelPack* __restrict__ prep, uint64_t n, const uint32_t* __restrict__ info,
     const uint16_t* __restrict__ slotmap, const uint8_t* __restrict__ wdepth,
@@ -761,20 +790,22 @@ __global__ __launch_bounds__(4 * kWave) void sel_fill_kernel(
 {
     const int lane = lane_id();
     const uint64_t gw = ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const uint64_t ws = gw / kSets;  // window of capacity
+    const uint32_t set = (uint32_t)(gw % kSets);
     const uint32_t sp = 4u * (kFastMaxLive + lane);
     uint64_t win;
     uint32_t k = 0xFFFF, depth = 1;
     uint64_t blk = 0;
-    if (gw < nblk * kWinCap) {
-        blk = gw / kWinCap;
-        const uint32_t lw = (uint32_t)(gw % kWinCap);
+    if (ws < nblk * kWinCap) {
+        blk = ws / kWinCap;
+        const uint32_t lw = (uint32_t)(ws % kWinCap);
         if (lw >= wcount[blk])
             return;
         win = (uint64_t)woff[blk] + lw;
         k = slotmap[gw * kWave + lane];
-        depth = wdepth[gw];
-    } else if (gw < nblk * kWinCap + 2 * kPrefetch) {
-        win = (uint64_t)total[0] + (gw - nblk * kWinCap);
+        depth = wdepth[ws];
+    } else if (ws < nblk * kWinCap + 2 * kPrefetch) {
+        win = (uint64_t)total[0] + (ws - nblk * kWinCap);
     } else {
         return;
     }
@@ -809,14 +840,14 @@ __global__ __launch_bounds__(4 * kWave) void sel_fill_kernel(
             q.puo2 = m1.uo;
             q.pth2 = m1.th;
         }
-        slot_of[r] = (uint32_t)(win * kWave + lane);
+        slot_of[r] = (uint32_t)((win * kSets + set) * kWave + lane);
     } else {
         q.a4 = q.o4 = q.wa = q.wo = sp;
         q.rel = kInertRel;
         q.ua = q.uo = q.pua = q.puo = q.pua2 = q.puo2 = q.pad = 0;
         q.th = q.pth = q.pth2 = 0;
     }
-    rec[win * kWave + lane] = q;
+    rec[(win * kSets + set) * kWave + lane] = q;
 }
 
 // Walks the windows in order; see the file comment.  T is the load type:
@@ -824,7 +855,8 @@ __global__ __launch_bounds__(4 * kWave) void sel_fill_kernel(
 // windows past the last and lpre kPrefetch, so that the unrolled walk and
 // its prefetch stay in bounds; lpre receives the pre-update loads (L_a, L_o)
 // of every request relative to the base, as int32 pairs for the 32-bit walk
-// and int64 pairs for the 64-bit one.
+// and int64 pairs for the 64-bit one, at the request's slot (window w, set
+// s, lane l: (w * kSets + s) * 64 + l).
 // Byte address of a shared-memory element within the workgroup's LDS.
 template <typename T>
 __device__ __forceinline__ uint32_t lds_addr(T* p)
@@ -833,73 +865,80 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
 }
 
 // One depth step of the 32-bit walk, as asm text for DM_WALK_BLOCK: the
-// lanes whose rel equals the inline constant K are on this depth.  The loads
-// of a step live in one register pair X = (L_a, L_o): v[240:241] or
-// v[242:243], alternating between steps, so that a decision adds both of its
-// increments with one 64-bit add.  No carry crosses the halves for a lane on
-// its depth: on this path every live load and its growth stay below 2^31.
-// (A lane off its depth may carry; its values only reach its spare slot.)
+// lanes of set S whose rel equals the inline constant K are on this depth
+// (steps of even number take set A, of odd number set B).  The loads of a
+// step live in one register pair X = (L_a, L_o): v[240:241] on even steps,
+// v[242:243] on odd ones, so that a decision adds both of its increments
+// with one 64-bit add.  No carry crosses the halves for a lane on its
+// depth: on this path every live load and its growth stay below 2^31.  (A
+// lane off its depth may carry; its values only reach its spare slot.)
 // Reads X (L_o first), replays the decisions of the run's earlier members
 // (no change for zero increments) into X: the loads this request saw;
-// captures the
-// previous step's pair XP (lane mask MP) into (La, Lo); M receives this
-// step's lane mask.  Then the lane's own decision into v[246:247], and both
-// loads of the pair written back (the second instance first, so that a pair
-// of one instance keeps the first's value) -- to the lane's write slots
-// (wa, wo) when on the depth, else to its spare slot.  The reads of a depth
-// precede its writes in the LDS queue, and the writes of one depth precede
-// the reads of the next, so the waits count this step's reads only.  Every
-// step has the same instructions with fixed-size encodings (operands are
-// registers and inline constants), which the computed entry relies on; the
-// assembler checks the sizes.
-#define DM_STEP_TEXT(K, XA, XO, X, M, XAP, XOP, MP)                                            \
+// captures the previous step's pair XP (lane mask MP) into the other set's
+// (La, Lo); M receives this step's lane mask.  Then the lane's own decision
+// into v[246:247], and both loads of the pair written back (the second
+// instance first, so that a pair of one instance keeps the first's value)
+// -- to the lane's write slots (wa, wo) when on the depth, else to its spare
+// slot.  The reads of a depth precede its writes in the LDS queue, and the
+// writes of one depth precede the reads of the next, so the waits count
+// this step's reads only.  Every step has the same instructions with
+// fixed-size encodings (operands are registers and inline constants), which
+// the computed entry relies on; the assembler checks the sizes.
+#define DM_STEP_TEXT(K, XA, XO, X, M, XAP, XOP, MP, S, P)                                      \
     ".Ldmw%=_" #K ":\n\t"                                                                      \
-    "ds_read_b32 " XO ", %[o4]\n\t"                                                            \
-    "ds_read_b32 " XA ", %[a4]\n\t"                                                            \
-    "v_cmp_eq_u32_e64 %[" M "], " #K ", %[rel]\n\t"                                           \
-    "v_cndmask_b32_e64 %[La], %[La], " XAP ", %[" MP "]\n\t"                                   \
-    "v_cndmask_b32_e64 %[Lo], %[Lo], " XOP ", %[" MP "]\n\t"                                   \
-    "v_cndmask_b32_e64 %[da], %[sp], %[wa], %[" M "]\n\t"                                      \
-    "v_cndmask_b32_e64 %[dz], %[sp], %[wo], %[" M "]\n\t"                                      \
+    "ds_read_b32 " XO ", %[o4" S "]\n\t"                                                       \
+    "ds_read_b32 " XA ", %[a4" S "]\n\t"                                                       \
+    "v_cmp_eq_u32_e64 %[" M "], " #K ", %[rel" S "]\n\t"                                      \
+    "v_cndmask_b32_e64 %[La" P "], %[La" P "], " XAP ", %[" MP "]\n\t"                         \
+    "v_cndmask_b32_e64 %[Lo" P "], %[Lo" P "], " XOP ", %[" MP "]\n\t"                         \
+    "v_cndmask_b32_e64 %[da], %[sp], %[wa" S "], %[" M "]\n\t"                                 \
+    "v_cndmask_b32_e64 %[dz], %[sp], %[wo" S "], %[" M "]\n\t"                                 \
     "s_waitcnt lgkmcnt(1)\n\t"                                                                 \
-    "v_max_i32_e32 v244, %[pth], " XO "\n\t"                                                   \
+    "v_max_i32_e32 v244, %[pth" S "], " XO "\n\t"                                              \
     "s_waitcnt lgkmcnt(0)\n\t"                                                                 \
     "v_cmp_le_i32_e32 vcc, " XA ", v244\n\t"                                                   \
-    "v_cndmask_b32_e64 v244, 0, %[pua], vcc\n\t"                                               \
-    "v_cndmask_b32_e64 v245, %[puo], 0, vcc\n\t"                                               \
+    "v_cndmask_b32_e64 v244, 0, %[pua" S "], vcc\n\t"                                          \
+    "v_cndmask_b32_e64 v245, %[puo" S "], 0, vcc\n\t"                                          \
     "v_lshl_add_u64 " X ", " X ", 0, v[244:245]\n\t"                                           \
-    "v_max_i32_e32 v244, %[pth2], " XO "\n\t"                                                  \
+    "v_max_i32_e32 v244, %[pth2" S "], " XO "\n\t"                                             \
     "v_cmp_le_i32_e32 vcc, " XA ", v244\n\t"                                                   \
-    "v_cndmask_b32_e64 v244, 0, %[pua2], vcc\n\t"                                              \
-    "v_cndmask_b32_e64 v245, %[puo2], 0, vcc\n\t"                                              \
+    "v_cndmask_b32_e64 v244, 0, %[pua2" S "], vcc\n\t"                                         \
+    "v_cndmask_b32_e64 v245, %[puo2" S "], 0, vcc\n\t"                                         \
     "v_lshl_add_u64 " X ", " X ", 0, v[244:245]\n\t"                                           \
-    "v_max_i32_e32 v246, %[th], " XO "\n\t"                                                    \
+    "v_max_i32_e32 v246, %[th" S "], " XO "\n\t"                                               \
     "v_cmp_le_i32_e32 vcc, " XA ", v246\n\t"                                                   \
-    "v_cndmask_b32_e64 v244, 0, %[ua], vcc\n\t"                                                \
-    "v_cndmask_b32_e64 v245, %[uo], 0, vcc\n\t"                                                \
+    "v_cndmask_b32_e64 v244, 0, %[ua" S "], vcc\n\t"                                           \
+    "v_cndmask_b32_e64 v245, %[uo" S "], 0, vcc\n\t"                                           \
     "v_lshl_add_u64 v[246:247], " X ", 0, v[244:245]\n\t"                                      \
     "ds_write_b32 %[dz], v247\n\t"                                                             \
     "ds_write_b32 %[da], v246\n\t"
 
 #define DM_STEP_PAIR(K0, K1)                                                                   \
-    DM_STEP_TEXT(K0, "v240", "v241", "v[240:241]", "m0", "v242", "v243", "m1")                 \
-    DM_STEP_TEXT(K1, "v242", "v243", "v[242:243]", "m1", "v240", "v241", "m0")
+    DM_STEP_TEXT(K0, "v240", "v241", "v[240:241]", "m0", "v242", "v243", "m1", "A", "B")       \
+    DM_STEP_TEXT(K1, "v242", "v243", "v[242:243]", "m1", "v240", "v241", "m0", "B", "A")
 
 #define DM_SIZE_CHECK(K0, K1)                                                                  \
     ".if (.Ldmw%=_" #K1 " - .Ldmw%=_" #K0 ") != (.Ldmw%=_1 - .Ldmw%=_0)\n\t"                   \
     ".error \"walk steps differ in size\"\n\t"                                                 \
     ".endif\n\t"
 
+#define DM_SET_OPERANDS(S)                                                                     \
+    [a4##S] "v"(a4##S), [o4##S] "v"(o4##S), [wa##S] "v"(wa##S), [wo##S] "v"(wo##S),            \
+        [th##S] "v"(c##S.th), [ua##S] "v"(c##S.ua), [uo##S] "v"(c##S.uo),                      \
+        [pth##S] "v"(c##S.pth), [pua##S] "v"(c##S.pua), [puo##S] "v"(c##S.puo),                \
+        [pth2##S] "v"(c##S.pth2), [pua2##S] "v"(c##S.pua2), [puo2##S] "v"(c##S.puo2)
+
 // All depths of one window of the 32-bit walk in one block of 16 steps
 // (K = 0..15), entered at step e by a computed jump (the PC-relative
 // sequence of a long branch) and run np1 + 1 times, where the window's
-// control word (the same in every lane) is e | np1 << 4; lane l is on step K
-// of pass j when rel - 16 j = K.  The control word is read inside the block,
-// so that the compiler waits only for this window's record.  The first step
-// captures whatever its register set held, which is harmless: every lane of
-// the batch is captured again after its own depth, and inert lanes' results
-// are never read.  After the last pass the last depth's reads are captured
-// into (La, Lo).  e < 16 and np1 < 4 by the masks, and the assembler checks
+// control word (the same in every lane) is e | np1 << 4; lane l of set A
+// (B) is on even (odd) step K of pass j when its rel - 16 j = K.  The
+// control word is read inside the block, so that the compiler waits only
+// for this window's records.  The first step captures whatever its register
+// set held, which is harmless: every lane of the batch is captured again
+// after its own depth, and inert lanes' results are never read.  After the
+// last pass the last depth's reads (an odd step: set B) are captured into
+// (LaB, LoB).  e < 16 and np1 < 4 by the masks, and the assembler checks
 // that the 16 steps have one size.
 #define DM_WALK_BLOCK()                                                                        \
     asm volatile("v_readfirstlane_b32 s99, %[ctl]\n\t"                                         \
@@ -916,22 +955,21 @@ __device__ __forceinline__ uint32_t lds_addr(T* p)
                  DM_STEP_PAIR(8, 9) DM_STEP_PAIR(10, 11) DM_STEP_PAIR(12, 13)                 \
                  DM_STEP_PAIR(14, 15)                                                          \
                  ".Ldmw%=_16:\n\t"                                                             \
-                 "v_add_u32_e32 %[rel], -16, %[rel]\n\t"                                       \
+                 "v_add_u32_e32 %[relA], -16, %[relA]\n\t"                                     \
+                 "v_add_u32_e32 %[relB], -16, %[relB]\n\t"                                     \
                  "s_sub_u32 s99, s99, 1\n\t"                                                   \
                  "s_cbranch_scc0 .Ldmw%=_0\n\t"                                                \
-                 "v_cndmask_b32_e64 %[La], %[La], v242, %[m1]\n\t"                               \
-                 "v_cndmask_b32_e64 %[Lo], %[Lo], v243, %[m1]\n\t"                               \
+                 "v_cndmask_b32_e64 %[LaB], %[LaB], v242, %[m1]\n\t"                             \
+                 "v_cndmask_b32_e64 %[LoB], %[LoB], v243, %[m1]\n\t"                             \
                  DM_SIZE_CHECK(1, 2) DM_SIZE_CHECK(2, 3) DM_SIZE_CHECK(3, 4)                   \
                  DM_SIZE_CHECK(4, 5) DM_SIZE_CHECK(5, 6) DM_SIZE_CHECK(6, 7)                   \
                  DM_SIZE_CHECK(7, 8) DM_SIZE_CHECK(8, 9) DM_SIZE_CHECK(9, 10)                  \
                  DM_SIZE_CHECK(10, 11) DM_SIZE_CHECK(11, 12) DM_SIZE_CHECK(12, 13)             \
                  DM_SIZE_CHECK(13, 14) DM_SIZE_CHECK(14, 15) DM_SIZE_CHECK(15, 16)             \
-                 : [m0] "=&s"(m0), [m1] "=&s"(m1), [La] "+v"(La), [Lo] "+v"(Lo),              \
-                   [da] "=&v"(da), [dz] "=&v"(dz), [rel] "+v"(rel)                            \
-                 : [a4] "v"(a4), [o4] "v"(o4), [wa] "v"(wa), [wo] "v"(wo), [sp] "v"(sp4),     \
-                   [th] "v"(th), [ua] "v"(ua), [uo] "v"(uo), [pth] "v"(pth), [pua] "v"(pua),  \
-                   [puo] "v"(puo), [pth2] "v"(pth2), [pua2] "v"(pua2), [puo2] "v"(puo2),      \
-                   [ctl] "v"(ctl)                                                              \
+                 : [m0] "=&s"(m0), [m1] "=&s"(m1), [LaA] "+v"(LaA), [LoA] "+v"(LoA),          \
+                   [LaB] "+v"(LaB), [LoB] "+v"(LoB), [da] "=&v"(da), [dz] "=&v"(dz),          \
+                   [relA] "+v"(relA), [relB] "+v"(relB)                                        \
+                 : DM_SET_OPERANDS(A), DM_SET_OPERANDS(B), [sp] "v"(sp4), [ctl] "v"(ctl)      \
                  : "s96", "s97", "s98", "s99", "v240", "v241", "v242", "v243", "v244", "v245",  \
                    "v246", "v247", "vcc", "scc", "memory")
 
@@ -954,10 +992,9 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
     // L itself is a link-time constant (zero when it is the only array)
     const uint32_t lbase = lds_addr(reinterpret_cast<int32_t*>(L));
     const uint32_t sp4 = lbase + 4u * (kFastMaxLive + lane);
-    int32_t La32 = 0, Lo32 = 0;
-    auto window = [&](WalkRec& cur, uint64_t w) {
-        const T ua = (T)cur.ua, uo = (T)cur.uo;
-        const T pua = (T)cur.pua, puo = (T)cur.puo, pua2 = (T)cur.pua2, puo2 = (T)cur.puo2;
+    int32_t LaA32 = 0, LoA32 = 0, LaB32 = 0, LoB32 = 0;
+    // window w: set A's records cA, set B's cB (same control word)
+    auto window = [&](WalkRec& cA, WalkRec& cB, uint64_t w) {
         if constexpr (wide) {
             // the packed bounds are clamped to 32 bits: recompute them
             // exactly, relative to the base (equal matches: -inf; cache
@@ -970,18 +1007,20 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
                                                      ((int64_t)1 << qshift) -
                                                  1 - b0);
             };
-            const T th = exact(cur.th, cur.ua), pth = exact(cur.pth, cur.pua);
-            const T pth2 = exact(cur.pth2, cur.pua2);
-            // Every lane reads and writes at every depth, without branches; a
-            // lane not on the current depth, and a run member other than the
-            // last, write their own spare slot.
-            const uint32_t ctl = __builtin_amdgcn_readfirstlane(cur.ctl), e = ctl & 15u;
+            // Every lane reads and writes at every depth, without branches on
+            // lane data; a lane not on the current depth, and a run member
+            // other than the last, write their own spare slot.
+            const uint32_t ctl = __builtin_amdgcn_readfirstlane(cA.ctl), e = ctl & 15u;
             const uint32_t depth = 16u * (((ctl >> 4) & 3u) + 1u) - e;
-            const uint32_t a = cur.a4 >> 2, o = cur.o4 >> 2, wa = cur.wa >> 2, wo = cur.wo >> 2;
-            const uint32_t sp = kFastMaxLive + lane, mylv = cur.rel - e;
-            T La = 0, Lo = 0;
-            for (uint32_t l = 0; l < depth; l++) {
-                const bool act = mylv == l;
+            const uint32_t sp = kFastMaxLive + lane;
+            T La[kSets] = {0, 0}, Lo[kSets] = {0, 0};
+            auto step = [&](const WalkRec& c, uint32_t l, T& la, T& lo) {
+                const T th = exact(c.th, c.ua), pth = exact(c.pth, c.pua);
+                const T pth2 = exact(c.pth2, c.pua2);
+                const T ua = (T)c.ua, uo = (T)c.uo, pua = (T)c.pua, puo = (T)c.puo;
+                const T pua2 = (T)c.pua2, puo2 = (T)c.puo2;
+                const uint32_t a = c.a4 >> 2, o = c.o4 >> 2, wa = c.wa >> 2, wo = c.wo >> 2;
+                const bool act = c.rel - e == l;
                 const T xa = L[a], xo = L[o];
                 const bool p1 = xa <= std::max(pth, xo);
                 const T x0 = xa + (p1 ? pua : (T)0), y0 = xo + (p1 ? (T)0 : puo);
@@ -990,42 +1029,54 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
                 const bool take_a = x1 <= std::max(th, y1);
                 L[act ? wo : sp] = take_a ? y1 : y1 + uo;
                 L[act ? wa : sp] = take_a ? x1 + ua : x1;
-                La = act ? x1 : La;
-                Lo = act ? y1 : Lo;
+                la = act ? x1 : la;
+                lo = act ? y1 : lo;
+            };
+            for (uint32_t l = 0; l < depth; l++) {
+                if ((e + l) & 1u)
+                    step(cB, l, La[1], Lo[1]);
+                else
+                    step(cA, l, La[0], Lo[0]);
             }
-            lpre[w * kWave + lane] = make_longlong2(La, Lo);
+            lpre[(w * kSets) * kWave + lane] = make_longlong2(La[0], Lo[0]);
+            lpre[(w * kSets + 1) * kWave + lane] = make_longlong2(La[1], Lo[1]);
         } else {
             // The same walk in hand-scheduled depth steps (DM_WALK_BLOCK): the
             // ALU work of a step that does not wait for its reads runs in the
             // shadow of the LDS round trip, and the window's depths run as one
             // straight block entered at the step that leaves exactly its
             // depth's steps (a pass of 16 more per further 16 depths).
-            const uint32_t a4 = lbase + cur.a4, o4 = lbase + cur.o4;
-            const uint32_t wa = lbase + cur.wa, wo = lbase + cur.wo;
-            const int32_t th = cur.th, pth = cur.pth, pth2 = cur.pth2;
-            const uint32_t ctl = cur.ctl;
-            uint32_t rel = cur.rel;
+            const uint32_t a4A = lbase + cA.a4, o4A = lbase + cA.o4;
+            const uint32_t waA = lbase + cA.wa, woA = lbase + cA.wo;
+            const uint32_t a4B = lbase + cB.a4, o4B = lbase + cB.o4;
+            const uint32_t waB = lbase + cB.wa, woB = lbase + cB.wo;
+            const uint32_t ctl = cA.ctl;
+            uint32_t relA = cA.rel, relB = cB.rel;
             int32_t da, dz;
             uint64_t m0, m1;
-            int32_t La = La32, Lo = Lo32;
+            int32_t LaA = LaA32, LoA = LoA32, LaB = LaB32, LoB = LoB32;
             DM_WALK_BLOCK();
             (void)m0; (void)m1; (void)da; (void)dz;
-            La32 = La;
-            Lo32 = Lo;
-            reinterpret_cast<int2*>(lpre)[w * kWave + lane] = make_int2(La, Lo);
+            LaA32 = LaA;
+            LoA32 = LoA;
+            LaB32 = LaB;
+            LoB32 = LoB;
+            int2* lp = reinterpret_cast<int2*>(lpre);
+            lp[(w * kSets) * kWave + lane] = make_int2(LaA, LoA);
+            lp[(w * kSets + 1) * kWave + lane] = make_int2(LaB, LoB);
         }
     };
-    static_assert(kPrefetch == 12, "the walk below holds 12 record windows");
     // Records arrive kPrefetch windows ahead.  The loop is unrolled by
     // kPrefetch so that each slot is used where it was loaded (no register
     // moves, which would wait for every load in flight); windows past the
     // last (inert padded records and outputs) change nothing.
-    WalkRec q0 = rec[0 * kWave + lane], q1 = rec[1 * kWave + lane];
-    WalkRec q2 = rec[2 * kWave + lane], q3 = rec[3 * kWave + lane];
-    WalkRec q4 = rec[4 * kWave + lane], q5 = rec[5 * kWave + lane];
-    WalkRec q6 = rec[6 * kWave + lane], q7 = rec[7 * kWave + lane];
-    WalkRec q8 = rec[8 * kWave + lane], q9 = rec[9 * kWave + lane];
-    WalkRec q10 = rec[10 * kWave + lane], q11 = rec[11 * kWave + lane];
+    auto at = [&](uint64_t w, uint32_t s) { return rec[(w * kSets + s) * kWave + lane]; };
+    WalkRec qa[kPrefetch], qb[kPrefetch];
+#pragma unroll
+    for (int i = 0; i < kPrefetch; i++) {
+        qa[i] = at(i, 0);
+        qb[i] = at(i, 1);
+    }
     // Let the first records land before the loop: the wait the compiler
     // places at the loop head must hold on entry as well as on the
     // back-edge, and with these loads in flight on entry it would wait for
@@ -1033,30 +1084,12 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
     // expcnt and lgkmcnt unconstrained, in the gfx9 encoding.)
     __builtin_amdgcn_s_waitcnt(0x0F70);
     for (uint64_t w = 0; w < nw; w += kPrefetch) {
-        window(q0, w + 0);
-        q0 = rec[(w + 12) * kWave + lane];
-        window(q1, w + 1);
-        q1 = rec[(w + 13) * kWave + lane];
-        window(q2, w + 2);
-        q2 = rec[(w + 14) * kWave + lane];
-        window(q3, w + 3);
-        q3 = rec[(w + 15) * kWave + lane];
-        window(q4, w + 4);
-        q4 = rec[(w + 16) * kWave + lane];
-        window(q5, w + 5);
-        q5 = rec[(w + 17) * kWave + lane];
-        window(q6, w + 6);
-        q6 = rec[(w + 18) * kWave + lane];
-        window(q7, w + 7);
-        q7 = rec[(w + 19) * kWave + lane];
-        window(q8, w + 8);
-        q8 = rec[(w + 20) * kWave + lane];
-        window(q9, w + 9);
-        q9 = rec[(w + 21) * kWave + lane];
-        window(q10, w + 10);
-        q10 = rec[(w + 22) * kWave + lane];
-        window(q11, w + 11);
-        q11 = rec[(w + 23) * kWave + lane];
+#pragma unroll
+        for (int i = 0; i < kPrefetch; i++) {
+            window(qa[i], qb[i], w + i);
+            qa[i] = at(w + kPrefetch + i, 0);
+            qb[i] = at(w + kPrefetch + i, 1);
+        }
     }
     __syncthreads();
     for (uint32_t d = lane; d < n_live && d < kFastMaxLive; d += kWave)
@@ -1064,6 +1097,7 @@ __device__ __forceinline__ void walk_windows(const WalkRec* __restrict__ rec,
 }
 
 #undef DM_WALK_BLOCK
+#undef DM_SET_OPERANDS
 #undef DM_SIZE_CHECK
 #undef DM_STEP_PAIR
 #undef DM_STEP_TEXT
@@ -1178,11 +1212,11 @@ static void sel_sizes(uint64_t n, size_t* sizes)
     const uint64_t wcap = nblk * kWinCap;
     const size_t z[] = {
         up256(n * sizeof(SelPack)),                                  // prep
-        up256((wcap + 2 * kPrefetch) * kWave * sizeof(WalkRec)),     // rec
-        up256((wcap + kPrefetch) * kWave * sizeof(longlong2)),       // lpre
+        up256((wcap + 2 * kPrefetch) * kSets * kWave * sizeof(WalkRec)),  // rec
+        up256((wcap + kPrefetch) * kSets * kWave * sizeof(longlong2)),    // lpre
         up256(n * sizeof(uint32_t)),                                 // info
         up256(n * sizeof(uint32_t)),                                 // slot_of
-        up256(wcap * kWave * sizeof(uint16_t)),                      // slotmap
+        up256(wcap * kSets * kWave * sizeof(uint16_t)),              // slotmap
         up256(wcap),                                                 // wdepth
         up256(nblk * sizeof(uint32_t)),                              // wcount
         up256(nblk * sizeof(uint32_t)),                              // woff
@@ -1205,7 +1239,7 @@ static hipError_t sel_buffers(dm_ctx* c, uint64_t n, int par, SelBuf* b)
 {
     hipError_t e = hipSuccess;
     b->nblk = (n + kLevelBlock - 1) / kLevelBlock;
-    b->nslots = b->nblk * kWinCap * kWave;
+    b->nslots = b->nblk * kWinCap * kSets * kWave;
     size_t sizes[10];
     sel_sizes(n, sizes);
     const size_t one = select_scratch_bytes(n);
@@ -1266,7 +1300,8 @@ hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uin
     hipError_t e = sel_buffers(c, n, par, &b);
     if (e != hipSuccess)
         return e;
-    if (b.nblk > 0x7FFFFFFFull || b.nblk * kWinCap + 2 * kPrefetch > (0x7FFFFFFFull / 4))
+    const uint64_t fill_waves = (b.nblk * kWinCap + 2 * kPrefetch) * kSets;
+    if (b.nblk > 0x7FFFFFFFull || fill_waves > 0x7FFFFFFFull)
         return hipErrorInvalidValue;
     const uint32_t NL = c->n_live;
     sel_zero_kernel<<<1, 256, 0, st>>>(b.grow, NL);
@@ -1280,7 +1315,6 @@ hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uin
         sel_level_kernel<<<(uint32_t)b.nblk, kWave, 0, st>>>(b.prep, n, b.info, b.slotmap, b.wdepth,
                                                              b.wcount, c->d_status);
     sel_scan_kernel<<<1, 1024, 0, st>>>(b.wcount, b.nblk, b.woff, b.total);
-    const uint64_t fill_waves = b.nblk * kWinCap + 2 * kPrefetch;
     sel_fill_kernel<<<(uint32_t)((fill_waves + 3) / 4), 4 * kWave, 0, st>>>(
         b.prep, n, b.info, b.slotmap, b.wdepth, b.wcount, b.woff, b.total, b.nblk, b.rec,
         b.slot_of);

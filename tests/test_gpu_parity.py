@@ -666,8 +666,8 @@ def test_levels_above_64_requests_parity(wide):
     candidate pairs over 200 instances, each sent twice in a row in three
     rounds, so that consecutive same-pair requests form runs (of three, then
     of three again) and a dependency level holds far more than 64 requests.
-    The walk splits each such level between windows and must keep every run
-    whole.  Random prompts follow, across the next request block.  wide:
+    The packing cuts each such level into parts of at most 64 requests, one
+    depth each, and must keep every run whole.  Random prompts follow, across the next request block.  wide:
     loads spread beyond 2^30 (64-bit walk)."""
     gh = _h()
     wl = workloads.small_random(33, 200, 3, 16, 64, slo_us=5_000)

@@ -1,8 +1,9 @@
 """The selection walk enters its block of 16 depth steps by a computed jump
 (PC + e * step size).  These checks run on the gfx950 code object that the
 library's own flags produce, without a GPU: every entry e in 0..15 of every
-copy of the block must be the first instruction of step e, and the block's
-back-edge must return to step 0.  A wrong entry would execute from the middle
+copy of the block must be the first instruction of step e, even steps must
+test one lane set's depth register and odd steps the other's, and the
+block's back-edge must move both down by 16 and return to step 0.  A wrong entry would execute from the middle
 of an instruction, so this is checked on every build rather than on the GPU.
 """
 import os
@@ -58,18 +59,28 @@ def test_walk_entries_land_on_step_starts(tmp_path):
         assert ins[i + 7][1] == "s_setpc_b64 s[96:97]"
         step, off = int(mul.group(1), 0), int(add.group(1), 0)
         assert pc + off == ins[i + 8][0], "entry 0 is not the instruction after the jump"
+        rel = {0: set(), 1: set()}  # the rel register of each lane set
         for e in range(16):
             tgt = pc + e * step + off
             assert tgt in at, f"entry {e} lands inside an instruction"
             j = at[tgt]
             assert ins[j][1].startswith("ds_read_b32"), ins[j]
             assert ins[j + 1][1].startswith("ds_read_b32"), ins[j + 1]
-            m = re.fullmatch(r"v_cmp_eq_u32_e64 s\[\d+:\d+\], (\d+), v\d+", ins[j + 2][1])
+            m = re.fullmatch(r"v_cmp_eq_u32_e64 s\[\d+:\d+\], (\d+), (v\d+)", ins[j + 2][1])
             assert m and int(m.group(1)) == e, (e, ins[j + 2])
+            rel[e & 1].add(m.group(2))
+        # even steps test set A's rel, odd steps set B's
+        assert len(rel[0]) == 1 and len(rel[1]) == 1 and rel[0] != rel[1], rel
         j = at[pc + 16 * step + off]
-        assert re.fullmatch(r"v_add_u32_e32 (v\d+), -16, \1", ins[j][1]), ins[j]
-        assert ins[j + 1][1] == "s_sub_u32 s99, s99, 1", ins[j + 1]
-        br_addr, br = ins[j + 2]
+        # the back-edge moves both sets' rel down by 16
+        backs = set()
+        for k in (j, j + 1):
+            m = re.fullmatch(r"v_add_u32_e32 (v\d+), -16, \1", ins[k][1])
+            assert m, ins[k]
+            backs.add(m.group(1))
+        assert backs == rel[0] | rel[1], (backs, rel)
+        assert ins[j + 2][1] == "s_sub_u32 s99, s99, 1", ins[j + 2]
+        br_addr, br = ins[j + 3]
         assert br.startswith("s_cbranch_scc0"), br
         simm = int(br.split()[-1], 0)
         simm = simm - 65536 if simm >= 32768 else simm

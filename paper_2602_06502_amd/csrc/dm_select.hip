@@ -471,7 +471,8 @@ static_assert(kLevelBlock == kSelBlock && kWinCap == kSelWindowsPerBlock,
 //   - then, chunk by chunk again with the runs' sizes final, each run takes
 //     its lanes within its level after the runs that start earlier
 //     (ballots per level);
-//   - lane 0 cuts the levels into parts and places the parts into windows.
+//   - the levels are cut into parts (a lane per level), and the parts placed
+//     into windows by one uniform greedy pass over their sizes.
 // Every LDS access is by this one wave, so no barrier is needed.
 __global__ __launch_bounds__(kWave) void sel_level_kernel(
     const SelPack* __restrict__ prep, uint64_t n, uint32_t* __restrict__ info,
@@ -493,7 +494,7 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
     __shared__ uint16_t lstart[kLevelBlock + 1];
     __shared__ uint16_t sorted[kLevelBlock];   // requests by level, runs in order
     __shared__ uint16_t pl_s0[kLevelBlock];     // part: first index in sorted
-    __shared__ uint8_t pl_win[kLevelBlock], pl_lane[kLevelBlock];  // window, set << 6 | lane
+    __shared__ uint8_t pl_win[kLevelBlock], pl_base[kLevelBlock];  // window, first lane in set
     __shared__ uint16_t wfirst[kWinCap];        // first part of each window
     __shared__ uint16_t smap[kWinCap * kSets * kWave];
     __shared__ uint8_t wdep[kWinCap];
@@ -592,6 +593,7 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
     }
     for (int d = 1; d < kWave; d <<= 1)
         lmax = std::max(lmax, (uint32_t)__shfl_xor((int)lmax, d));
+    lmax = (uint32_t)__builtin_amdgcn_readfirstlane((int)lmax);  // uniform from here on
     // lanes of the runs within their levels, chunk by chunk: each run's first
     // member sums the sizes of the chunk's earlier runs of its level (every
     // lane reads the chunk's 64 keys), after the count of the earlier chunks;
@@ -633,90 +635,105 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
     }
     for (uint32_t t = lane; t < nb; t += kWave)
         sorted[lstart[lv[t]] + hrank[hd[t]] + psn[t]] = (uint16_t)t;
-    uint32_t nwin = 0, okw = 0;
-    if (lane == 0) {
-        // parts: a level of at most 64 requests is one part; a larger one is
-        // cut run by run into parts of at most 64 (its requests are
-        // independent, so its parts may take consecutive depths).  The parts
-        // cover sorted in order, so part p holds [pl_s0[p], pl_s0[p + 1]);
-        // cnt[l] becomes level l's first part once its size is read.
-        uint32_t npl = 0;
-        for (uint32_t l = 1; l <= lmax; l++) {
-            const uint32_t c = cnt[l], s0 = lstart[l];
-            cnt[l] = npl;
-            if (c <= kWave) {
-                pl_s0[npl++] = (uint16_t)s0;
-                continue;
+    // Parts, one lane per level: a level of at most 64 requests is one part;
+    // a larger one is cut run by run into parts of at most 64 (its requests
+    // are independent, so its parts may take consecutive depths).  The parts
+    // cover sorted in order, so part p holds [pl_s0[p], pl_s0[p + 1]); cnt[l]
+    // becomes level l's first part (a scan of the part counts).
+    auto cut = [&](uint32_t s0, uint32_t c, uint32_t first, bool write) -> uint32_t {
+        uint32_t np = 1, part = 0;
+        if (write)
+            pl_s0[first] = (uint16_t)s0;
+        for (uint32_t k = s0; k < s0 + c;) {
+            const uint32_t sz = key[sorted[k]] & 3u;  // k is a run's first member
+            if (part + sz > kWave) {
+                if (write)
+                    pl_s0[first + np] = (uint16_t)k;
+                np++;
+                part = 0;
             }
-            uint32_t part = 0;
-            pl_s0[npl++] = (uint16_t)s0;
-            for (uint32_t k = s0; k < s0 + c;) {
-                const uint32_t sz = key[sorted[k]] & 3u;  // k is a run's first member
-                if (part + sz > kWave) {
-                    pl_s0[npl++] = (uint16_t)k;
-                    part = 0;
-                }
-                part += sz;
-                k += sz;
-            }
+            part += sz;
+            k += sz;
         }
+        return np;
+    };
+    uint32_t npl = 0;
+    for (uint32_t l0 = 1; l0 <= lmax; l0 += kWave) {
+        const uint32_t l = l0 + lane;
+        const bool has = l <= lmax;
+        const uint32_t c = has ? cnt[l] : 0u, s0 = has ? lstart[l] : 0u;
+        const uint32_t np = !has ? 0u : c <= kWave ? 1u : cut(s0, c, 0, false);
+        uint32_t x = np;  // inclusive scan over the wave
+        for (int d = 1; d < kWave; d <<= 1) {
+            const uint32_t y = (uint32_t)__shfl_up((int)x, d);
+            if ((int)lane >= d)
+                x += y;
+        }
+        const uint32_t first = npl + x - np;
+        if (has) {
+            cnt[l] = first;
+            if (c <= kWave)
+                pl_s0[first] = (uint16_t)s0;
+            else
+                (void)cut(s0, c, first, true);
+        }
+        npl += (uint32_t)__builtin_amdgcn_readlane((int)x, kWave - 1);
+    }
+    if (lane == 0)
         cnt[lmax + 1] = npl;
-        auto psize = [&](uint32_t p) -> uint32_t {
-            return (p + 1 < npl ? (uint32_t)pl_s0[p + 1] : nb) - pl_s0[p];
-        };
-        // windows of consecutive parts, one depth each: a window of depth D
-        // is entered at step e = -D mod 16, so depth t runs on step e + t and
-        // takes the lane set of that step's parity.  S0 and S1 sum the parts
-        // at an even and an odd distance from the window's last depth (sets
-        // 1 and 0); appending a part moves every other part one further, so
-        // the window grows while c + S1 <= 64 and the depth stays below 65.
-        // A window that fits holds every window inside it, so closing at the
-        // first misfit gives the fewest windows; any window that fits one
-        // set of 64 lanes fits the two, so the bound of kWinCap holds.
-        bool ok = true;
-        uint32_t win = 0, first = 0, D = 0, S0 = 0, S1 = 0;
-        auto close = [&](uint32_t end) {
-            if (win >= kWinCap) {
-                ok = false;
-                return;
-            }
-            const uint32_t e = (0u - D) & 15u;
-            uint32_t base0 = 0, base1 = 0;
-            for (uint32_t p = first; p < end; p++) {
-                const uint32_t odd = (e + (p - first)) & 1u, c = psize(p);
-                pl_win[p] = (uint8_t)win;
-                pl_lane[p] = (uint8_t)(odd << 6 | (odd ? base1 : base0));
-                if (odd)
-                    base1 += c;
-                else
-                    base0 += c;
-            }
-            wfirst[win] = (uint16_t)first;
-            wdep[win++] = (uint8_t)D;
-        };
-        for (uint32_t p = 0; p < npl && ok; p++) {
-            const uint32_t c = psize(p);
+    // Windows of consecutive parts, one depth each: a window of depth D is
+    // entered at step e = -D mod 16, so depth t runs on step e + t and takes
+    // the lane set of that step's parity, (t + D) & 1.  S0 and S1 sum the
+    // parts at an even and an odd distance from the window's last depth;
+    // appending a part moves every other part one further, so the window
+    // grows while c + S1 <= 64 and the depth stays below 65.  A window that
+    // fits holds every window inside it, so closing at the first misfit
+    // gives the fewest windows; any window that fits one set of 64 lanes
+    // fits the two, so the bound of kWinCap holds.  Parts of one set are
+    // those of one depth parity, so a part's first lane is the sum of the
+    // earlier parts of its depth parity in the window.  The wave takes the
+    // parts 64 at a time, their sizes in lanes; the decisions are uniform.
+    uint32_t win = 0, D = 0, S0 = 0, S1 = 0, be = 0, bo = 0;
+    for (uint32_t p0 = 0; p0 < npl; p0 += kWave) {
+        const uint32_t p = p0 + lane;
+        const uint32_t cl = p < npl ? (p + 1 < npl ? (uint32_t)pl_s0[p + 1] : nb) - pl_s0[p] : 0u;
+        uint32_t wl = 0, bl = 0;
+        const uint32_t m = npl - p0 < (uint32_t)kWave ? npl - p0 : (uint32_t)kWave;
+        for (uint32_t i = 0; i < m; i++) {
+            const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)cl, (int)i);
             if (D > 0 && (D == kWave || c + S1 > kWave)) {
-                close(p);
-                first = p;
-                D = S0 = S1 = 0;
+                if (win < kWinCap) {
+                    wdep[win] = (uint8_t)D;
+                    wfirst[win] = (uint16_t)(p0 + i - D);
+                }
+                win++;
+                D = S0 = S1 = be = bo = 0;
             }
+            const uint32_t base = (D & 1u) ? bo : be;
+            if (D & 1u)
+                bo += c;
+            else
+                be += c;
+            wl = lane == i ? win : wl;
+            bl = lane == i ? base : bl;
             const uint32_t s0n = c + S1;
             S1 = S0;
             S0 = s0n;
             D++;
         }
-        if (ok && D > 0)
-            close(npl);
-        if (!ok) {  // cannot happen (see above); no window of this block is walked
-            atomicOr(status, kErrInval);
-            win = 0;
+        if (p < npl) {
+            pl_win[p] = (uint8_t)wl;
+            pl_base[p] = (uint8_t)bl;
         }
-        nwin = win;
-        okw = ok ? 1u : 0u;
     }
-    nwin = (uint32_t)__shfl((int)nwin, 0);
-    okw = (uint32_t)__shfl((int)okw, 0);
+    if (win < kWinCap) {
+        wdep[win] = (uint8_t)D;
+        wfirst[win] = (uint16_t)(npl - D);
+    }
+    const uint32_t nwin = win + 1;
+    const bool okw = nwin <= kWinCap;
+    if (!okw && lane == 0)  // cannot happen (see above); no window of this block is walked
+        atomicOr(status, kErrInval);
     if (okw) {
         for (uint32_t t = lane; t < nb; t += kWave) {
             const uint32_t L = lv[t], pos = psn[t], h = hd[t], rs = 1u + has1[h] + has2[h];
@@ -724,8 +741,8 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
             uint32_t p = cnt[L];
             while (p + 1 < cnt[L + 1] && pl_s0[p + 1] <= k)
                 p++;
-            const uint32_t w = pl_win[p], pl = pl_lane[p], set = pl >> 6;
-            const uint32_t ln = (pl & 63u) + (k - pl_s0[p]), d = p - wfirst[w];
+            const uint32_t w = pl_win[p], d = p - wfirst[w], set = (d + wdep[w]) & 1u;
+            const uint32_t ln = pl_base[p] + (k - pl_s0[p]);
             smap[(w * kSets + set) * kWave + ln] = (uint16_t)t;
             const uint32_t m1 = pos == 2 ? (uint32_t)P[t] : 0u;
             info[r0 + t] = d | pos << 6 | (pos + 1 < rs ? 1u << 8 : 0u) | h << 9 | m1 << 19;
@@ -734,9 +751,9 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
     for (uint32_t k = lane; k < kWinCap * kSets * kWave; k += kWave)
         slotmap[(uint64_t)blockIdx.x * kWinCap * kSets * kWave + k] = smap[k];
     if (lane < kWinCap)
-        wdepth[(uint64_t)blockIdx.x * kWinCap + lane] = lane < nwin ? wdep[lane] : 0;
+        wdepth[(uint64_t)blockIdx.x * kWinCap + lane] = okw && lane < nwin ? wdep[lane] : 0;
     if (lane == 0)
-        wcount[blockIdx.x] = nwin;
+        wcount[blockIdx.x] = okw ? nwin : 0;
 }
 
 // Exclusive scan of the blocks' window counts (one workgroup); total[0] =

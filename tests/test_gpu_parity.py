@@ -146,6 +146,20 @@ def test_selection_wide_loads_parity(n_inst, top):
     assert (r["flags"] & 1).sum() + (r["flags"] & 4).sum() > 0
 
 
+@pytest.mark.parametrize("n_inst,wide", [(1, False), (2, False), (2, True), (3, True)])
+def test_deep_windows_across_blocks_parity(n_inst, wide):
+    """One to three instances over several 1024-request blocks: every level
+    holds one pair (one to three requests), so windows alternate many small
+    depths between their two lane sets and reach the 64-depth cap (four
+    passes of the 16-step block); wide: loads beyond 2^30 (64-bit walk)."""
+    wl = workloads.small_random(41 + n_inst, n_inst, 3, 16, 2600, slo_us=400_000)
+    L0 = workloads.initial_loads(wl, wl.route.max_slots)
+    if wide:
+        L0[::2] += 1 << 40
+    _say("deep windows", n_inst, wide)
+    _pair_with_loads(wl, L0)
+
+
 @pytest.mark.parametrize("policy", ["cache_affinity", "least_loaded", "min_ttft"])
 @pytest.mark.parametrize("n_inst,wide", [(8, 0), (200, 0), (150, 1), (300, 0), (8, 2)])
 def test_policy_selection_parity(policy, n_inst, wide):

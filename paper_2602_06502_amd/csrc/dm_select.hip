@@ -468,9 +468,8 @@ static_assert(kLevelBlock == kSelBlock && kWinCap == kSelWindowsPerBlock,
 //     with wave-wide votes);
 //   - levels: the least fixed point of the level rule over the chunk
 //     (earlier chunks' levels are final; relaxation from 1, wave-wide votes);
-//   - then, chunk by chunk again with the runs' sizes final, each run takes
-//     its lanes within its level after the runs that start earlier
-//     (ballots per level);
+//   - then, with the runs' sizes final, each run reserves its lanes within
+//     its level (LDS atomics: any order of a level's runs is valid);
 //   - the levels are cut into parts (a lane per level), and the parts placed
 //     into windows by one uniform greedy pass over their sizes.
 // Every LDS access is by this one wave, so no barrier is needed.
@@ -594,44 +593,32 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
     for (int d = 1; d < kWave; d <<= 1)
         lmax = std::max(lmax, (uint32_t)__shfl_xor((int)lmax, d));
     lmax = (uint32_t)__builtin_amdgcn_readfirstlane((int)lmax);  // uniform from here on
-    // lanes of the runs within their levels, chunk by chunk: each run's first
-    // member sums the sizes of the chunk's earlier runs of its level (every
-    // lane reads the chunk's 64 keys), after the count of the earlier chunks;
-    // the last one of its level in the chunk advances that count
-    for (uint32_t c0 = 0; c0 < kLevelBlock; c0 += kWave) {
-        const uint32_t t = c0 + lane;
-        const uint32_t L = lv[t], rs = 1u + has1[t] + has2[t];
+    // inclusive sum over the wave
+    auto wave_incl = [&](uint32_t v) -> uint32_t {
+        for (int d = 1; d < kWave; d <<= 1) {
+            const uint32_t y = (uint32_t)__shfl_up((int)v, d);
+            if ((int)lane >= d)
+                v += y;
+        }
+        return v;
+    };
+    // the lanes of the runs within their levels, with the runs' sizes final:
+    // each run's first member reserves the run's size in its level's count.
+    // Requests of one level are independent, so any order of a level's runs
+    // is valid; a run's members stay together, in run order.
+    for (uint32_t t = lane; t < kLevelBlock; t += kWave) {
         const bool head = t < nb && psn[t] == 0;
-        const uint32_t k = head ? (L << 2 | rs) : 0u;
-        key[t] = (uint16_t)k;
-        const uint32_t base = head ? cnt[L] : 0u;
-        uint32_t acc = 0;
-        bool later = false;
-        const uint4* kq = reinterpret_cast<const uint4*>(&key[c0]);
-#pragma unroll
-        for (int q = 0; q < kWave / 8; q++) {
-            const uint4 v = kq[q];
-            const uint32_t d[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-            for (int e = 0; e < 8; e++) {
-                const uint32_t j = (uint32_t)(q * 8 + e), kj = (d[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-                const bool same = kj != 0 && (kj >> 2) == L;
-                acc += (same && j < lane) ? (kj & 3u) : 0u;
-                later = later || (same && j > lane);
-            }
-        }
-        if (head) {
-            hrank[t] = (uint16_t)(base + acc);
-            if (!later)
-                cnt[L] = base + acc + rs;
-        }
+        const uint32_t L = lv[t], rs = 1u + has1[t] + has2[t];
+        key[t] = head ? (uint16_t)(L << 2 | rs) : (uint16_t)0;
+        if (head)
+            hrank[t] = (uint16_t)atomicAdd(&cnt[L], rs);
     }
-    if (lane == 0) {
-        uint32_t start = 0;
-        for (uint32_t l = 1; l <= lmax; l++) {
-            lstart[l] = (uint16_t)start;
-            start += cnt[l];
-        }
+    // each level's first index in sorted (a scan of the counts)
+    for (uint32_t l0 = 1, start = 0; l0 <= lmax; l0 += kWave) {
+        const uint32_t l = l0 + lane, c = l <= lmax ? cnt[l] : 0u, x = wave_incl(c);
+        if (l <= lmax)
+            lstart[l] = (uint16_t)(start + x - c);
+        start += (uint32_t)__builtin_amdgcn_readlane((int)x, kWave - 1);
     }
     for (uint32_t t = lane; t < nb; t += kWave)
         sorted[lstart[lv[t]] + hrank[hd[t]] + psn[t]] = (uint16_t)t;
@@ -663,13 +650,7 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
         const bool has = l <= lmax;
         const uint32_t c = has ? cnt[l] : 0u, s0 = has ? lstart[l] : 0u;
         const uint32_t np = !has ? 0u : c <= kWave ? 1u : cut(s0, c, 0, false);
-        uint32_t x = np;  // inclusive scan over the wave
-        for (int d = 1; d < kWave; d <<= 1) {
-            const uint32_t y = (uint32_t)__shfl_up((int)x, d);
-            if ((int)lane >= d)
-                x += y;
-        }
-        const uint32_t first = npl + x - np;
+        const uint32_t x = wave_incl(np), first = npl + x - np;
         if (has) {
             cnt[l] = first;
             if (c <= kWave)

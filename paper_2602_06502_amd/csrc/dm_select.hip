@@ -25,8 +25,8 @@
 //                     packing of whole levels into windows of two sets of
 //                     64 lanes (one set for the window's even depths, one
 //                     for its odd ones);
-//   sel_scan_kernel,  the windows' places, the walk records of every
-//   sel_fill_kernel   window lane and each request's slot;
+//   sel_scan_kernel,  the windows' places, the walk records of every lane
+//   sel_fill_kernel   of both sets of every window and each request's slot;
 //   select_fast_kernel one wave walks the windows in order and, inside a
 //                     window, the levels in order: requests of one level
 //                     share no instance, so they run together on loads kept
@@ -269,12 +269,13 @@ struct SelPack {
     int32_t th;   // take a iff L_a <= max(th, L_o), relative loads
 };
 
-// Per-window-lane record of the walk, in the form its depth steps consume:
+// Per-lane record of one lane set of a window, in the form the window's
+// depth steps consume:
 // the LDS byte offsets (within the load array, 4-byte slots) of L_a and
 // L_o, where the request writes them (its spare slot unless it is the last
 // member of its run), rel = its depth in the window (0-based) + the
 // window's entry step e, and the window's control word e | (passes - 1) << 4.
-// Lanes past a window's requests and the padding windows are inert: every
+// Lanes past a set's requests and the padding windows are inert: every
 // offset is the lane's spare slot and rel matches no step.
 struct WalkRec {
     uint32_t a4, o4, wa, wo;

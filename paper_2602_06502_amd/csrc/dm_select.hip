@@ -572,23 +572,23 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
             has1[h] = 1;
         if (valid && pos == 2)
             has2[h] = 1;
-        // levels of the chunk: the least fixed point, from 1 up
+        // levels of the chunk: the least fixed point, from 1 up; levels of
+        // earlier chunks are final (read once), those of this chunk's
+        // predecessors come from their lanes
+        const bool ina = pa >= (int)c0, ino = po >= (int)c0;
+        const uint32_t la0 = !ina && pa >= 0 ? lv[pa] : 0u, lo0 = !ino && po >= 0 ? lv[po] : 0u;
+        const int sa = ina ? pa - (int)c0 : (int)lane, so = ino ? po - (int)c0 : (int)lane;
         uint32_t L = valid ? 1u : 0u;
-        lv[t] = (uint16_t)L;
         for (;;) {
-            uint32_t nl = 0;
-            if (valid)
-                nl = pos > 0 ? lv[pa]
-                             : 1u + std::max(pa >= 0 ? (uint32_t)lv[pa] : 0u,
-                                             po >= 0 ? (uint32_t)lv[po] : 0u);
+            const uint32_t xa = (uint32_t)__shfl((int)L, sa), xo = (uint32_t)__shfl((int)L, so);
+            const uint32_t va = ina ? xa : la0, vo = ino ? xo : lo0;
+            const uint32_t nl = !valid ? 0u : pos > 0 ? va : 1u + std::max(va, vo);
             const bool ch = nl != L;
-            if (ch) {
-                L = nl;
-                lv[t] = (uint16_t)L;
-            }
+            L = nl;
             if (!__any(ch))
                 break;
         }
+        lv[t] = (uint16_t)L;
         lmax = std::max(lmax, L);
     }
     for (int d = 1; d < kWave; d <<= 1)

@@ -115,7 +115,7 @@ def algorithmic_bytes(off_np, B, match, cand, n):
     return hash_bytes, stage_bytes, ntok, probes
 
 
-def walk_steps(cand, match, n, block=1024, lanes=64, run_max=3):
+def walk_steps(cand, match, n, block=None, lanes=64, run_max=3):
     """Depth steps and windows of the selection walk.  Requests are taken in
     blocks of `block` (request order); inside a block a request's level is
     1 + the larger level of the latest earlier request of the block on
@@ -128,6 +128,8 @@ def walk_steps(cand, match, n, block=1024, lanes=64, run_max=3):
     depth step.  Windows take consecutive parts and hold two sets of `lanes`
     lanes, the depths alternating between the sets: a window grows while
     both sets' parts fit and its depth stays within 64."""
+    if block is None:  # the library's blocks: 2048 requests from 512 Ki requests on
+        block = 2048 if n >= 1 << 19 else 1024
     c1, c2 = cand[:n].tolist(), cand[n:].tolist()
     m1, m2 = match[:n].tolist(), match[n:].tolist()
     steps = windows = 0
@@ -752,7 +754,7 @@ def main():
                          "ns_per_step": ref_stage[2] * 1e6 / depth_steps,
                          "note": "one wave walks windows of up to 2 x 64 requests (one lane "
                                  "set for even depths, one for odd) packed from the "
-                                 "dependency levels of 1024-request blocks, runs of up to three "
+                                 "dependency levels of 2048-request blocks, runs of up to three "
                                  "same-pair requests sharing a level; each step is an LDS "
                                  "round trip plus the run replay and the decision; time from "
                                  "the unpipelined stage (record packing and levels included)"},

@@ -173,7 +173,7 @@ typedef struct {
  * rings (DM_ESTATE otherwise).  The call does not wait for the device: its
  * work arrays are sized from n and n_tokens (they grow, synchronising once,
  * only when a batch needs more than any before it).  n = 0 is a no-op; n must be at most
- * 954,436,608 (DM_EINVAL): the selection indexes its per-request slots in
+ * 1,041,203,200 (DM_EINVAL): the selection indexes its per-request slots in
  * 32 bits.  Match lengths are 32-bit: a request with 2^32 or more full
  * blocks sets the device status word (DM_EINVAL from dm_sync). */
 dm_status dm_route_batch(dm_ctx* ctx, const int32_t* tokens, uint64_t n_tokens,

@@ -96,10 +96,10 @@ dm_status route_args_check(dm_ctx* c, const int32_t* tokens, uint64_t n_tokens,
         (out->key_len && !aligned(out->key_len)))
         return fail(c, DM_EINVAL, std::string(what) + ": misaligned pointer");
 
-    // the selection's slot indices are 32-bit: 36 windows of two sets of 64
-    // lanes per 1024 requests must stay below 2^32
+    // the selection's slot indices are 32-bit: 66 windows of two sets of 64
+    // lanes per 2048 requests must stay below 2^32
     if (n > kMaxRouteBatch)
-        return fail(c, DM_EINVAL, std::string(what) + ": batch too large (n <= 954,436,608)");
+        return fail(c, DM_EINVAL, std::string(what) + ": batch too large (n <= 1,041,203,200)");
     if (n_tokens > (1ull << 62))
         return fail(c, DM_EINVAL, std::string(what) + ": token count too large");
     return DM_OK;

@@ -28,10 +28,10 @@ constexpr uint32_t kBucket = 8;     // slots per probe bucket (one 64-byte line)
 // Device status word bits (reported by dm_sync).
 constexpr uint32_t kErrInval = 1u;
 constexpr uint32_t kErrFull = 2u;
-// Largest batch dm_route_batch takes: the selection gives each block of 1024
-// requests room for 36 windows of two sets of 64 lanes and indexes those
+// Largest batch dm_route_batch takes: the selection gives each block of 2048
+// requests room for 66 windows of two sets of 64 lanes and indexes those
 // lanes in 32 bits.
-constexpr uint64_t kSelBlock = 1024, kSelWindowsPerBlock = 36;
+constexpr uint64_t kSelBlock = 2048, kSelWindowsPerBlock = 66;
 constexpr uint64_t kMaxRouteBatch = (0xFFFFFFFFull / (kSelWindowsPerBlock * 2 * 64)) * kSelBlock;
 
 // Hash parameters of both functions, computed on the host at dm_create.

@@ -19,7 +19,8 @@
 //                     their uncached tokens, and th such that the rule reads
 //                     "take a iff L_a <= max(th, L_o)" (clamped to 32 bits;
 //                     the 64-bit walk recomputes it exactly);
-//   sel_level_kernel  one wave per block of 1024 requests: the dependency
+//   sel_level_kernel  one wave per block of requests (1024, or 2048 in
+//                     batches of at least 512 Ki requests): the dependency
 //                     level of every request inside its block (runs of up
 //                     to three same-pair requests sharing a level), and the
 //                     packing of whole levels into windows of two sets of
@@ -431,7 +432,7 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
 }
 
 // Walk windows from dependency levels.  Requests are grouped in blocks of
-// kLevelBlock (request order).  Inside a block, a request's level is 1 + the
+// LB requests (request order).  Inside a block, a request's level is 1 + the
 // larger level of the latest earlier request of the block on either
 // candidate (0 when none), except that a request that joins a run (see
 // kRunMax) takes the run's level.
@@ -446,16 +447,41 @@ __global__ __launch_bounds__(256) void sel_plan_kernel(const int64_t* __restrict
 // window holds up to 128 requests.  Packing the same parts into windows of
 // one set of 64 lanes would close a window only when the next part does not
 // fit, so any two consecutive such windows hold more than 64 requests and a
-// block needs at most 2 * ceil(kLevelBlock / 65) + 1 = 33 of them; the
-// two-set packing needs no more.
-constexpr uint32_t kLevelBlock = 1024;
-constexpr uint32_t kWinCap = 36;  // windows per block; the bound above is 35
-static_assert(kLevelBlock == kSelBlock && kWinCap == kSelWindowsPerBlock,
+// block needs at most 2 * ceil(LB / 65) + 1 of them; the two-set packing
+// needs no more.
+//
+// Larger blocks give fewer depth steps and windows (on the large batch,
+// 78,742 steps in 9,832 windows with blocks of 2048 against 79,786 in
+// 10,225 with 1024) but take the level kernel twice as long per block, which
+// only a batch long enough to hide it behind its walk repays: batches of
+// at least kLargeFrom requests use blocks of 2048, others blocks of 1024.
+template <uint32_t LB>
+struct LevelShape {
+    static constexpr uint32_t block = LB;
+    static constexpr uint32_t wincap = LB == 1024 ? 36u : 66u;  // windows per block
+    static_assert(wincap >= 2 * ((LB + 64) / 65) + 1, "room for the windows of a block");
+};
+constexpr uint64_t kLargeFrom = 1u << 19;
+// The batch limit follows the large layout; the small one only serves
+// batches whose slots stay far inside 32 bits.
+static_assert(LevelShape<2048>::block == kSelBlock &&
+                  LevelShape<2048>::wincap == kSelWindowsPerBlock &&
+                  kLargeFrom / 1024 * LevelShape<1024>::wincap * kSets * kWave < (1ull << 32),
               "dm_route_batch's batch limit assumes this layout");
+
+// Block size and window capacity of a batch of n requests.
+struct BlockShape {
+    uint32_t block, wincap;
+};
+static BlockShape block_shape(uint64_t n)
+{
+    return n >= kLargeFrom ? BlockShape{LevelShape<2048>::block, LevelShape<2048>::wincap}
+                           : BlockShape{LevelShape<1024>::block, LevelShape<1024>::wincap};
+}
 
 // One wave per block.  Writes, per request, info = depth in its window |
 // position in its run << 6 | (not the run's last) << 8 | run's first member
-// << 9 | run's second member << 19 (block-local indices); per block, its
+// << 9 | run's second member << 20 (block-local indices); per block, its
 // window count, each window's depth and the block-local request index in
 // every lane of both sets of every window (0xFFFF for none).  The result is that of taking the
 // requests one by one; the wave takes them 64 at a time, in order:
@@ -474,54 +500,56 @@ static_assert(kLevelBlock == kSelBlock && kWinCap == kSelWindowsPerBlock,
 //   - the levels are cut into parts (a lane per level), and the parts placed
 //     into windows by one uniform greedy pass over their sizes.
 // Every LDS access is by this one wave, so no barrier is needed.
+template <uint32_t LB>
 __global__ __launch_bounds__(kWave) void sel_level_kernel(
     const SelPack* __restrict__ prep, uint64_t n, uint32_t* __restrict__ info,
     uint16_t* __restrict__ slotmap, uint8_t* __restrict__ wdepth, uint32_t* __restrict__ wcount,
     uint32_t* __restrict__ status)
 {
+    constexpr uint32_t kWinCap = LevelShape<LB>::wincap;
     __shared__ unsigned long long cm[kFastMaxLive];  // lanes of the chunk on each instance
     __shared__ uint16_t last[kFastMaxLive];         // latest request of earlier chunks, + 1
-    __shared__ uint16_t W[kLevelBlock];              // a | o << 8
-    __shared__ int16_t P[kLevelBlock];               // latest earlier request on a
-    __shared__ uint8_t psn[kLevelBlock];             // position in the run
-    __shared__ uint16_t hd[kLevelBlock];             // the run's first member
-    __shared__ uint16_t lv[kLevelBlock];
-    __shared__ uint8_t has1[kLevelBlock], has2[kLevelBlock];  // a run has a 2nd / 3rd member
-    __shared__ __align__(16) uint16_t key[kLevelBlock];  // a run's first member: level << 2 | size
-    __shared__ uint16_t hrank[kLevelBlock];    // lanes of earlier runs of the same level
-    __shared__ uint32_t cnt[kLevelBlock + 2];  // requests per level (so far), then
+    __shared__ uint16_t W[LB];              // a | o << 8
+    __shared__ int16_t P[LB];               // latest earlier request on a
+    __shared__ uint8_t psn[LB];             // position in the run
+    __shared__ uint16_t hd[LB];             // the run's first member
+    __shared__ uint16_t lv[LB];
+    __shared__ uint8_t has1[LB], has2[LB];  // a run has a 2nd / 3rd member
+    __shared__ __align__(16) uint16_t key[LB];  // a run's first member: level << 2 | size
+    __shared__ uint16_t hrank[LB];    // lanes of earlier runs of the same level
+    __shared__ uint32_t cnt[LB + 2];  // requests per level (so far), then
                                                // each level's first part
-    __shared__ uint16_t lstart[kLevelBlock + 1];
-    __shared__ uint16_t sorted[kLevelBlock];   // requests by level, runs in order
-    __shared__ uint16_t pl_s0[kLevelBlock];     // part: first index in sorted
-    __shared__ uint8_t pl_win[kLevelBlock], pl_base[kLevelBlock];  // window, first lane in set
+    __shared__ uint16_t lstart[LB + 1];
+    __shared__ uint16_t sorted[LB];   // requests by level, runs in order
+    __shared__ uint16_t pl_s0[LB];     // part: first index in sorted
+    __shared__ uint8_t pl_win[LB], pl_base[LB];  // window, first lane in set
     __shared__ uint16_t wfirst[kWinCap];        // first part of each window
     __shared__ uint16_t smap[kWinCap * kSets * kWave];
     __shared__ uint8_t wdep[kWinCap];
     const uint32_t lane = (uint32_t)lane_id();
-    const uint64_t r0 = (uint64_t)blockIdx.x * kLevelBlock;
-    const uint32_t nb = (uint32_t)std::min<uint64_t>(kLevelBlock, n - r0);
+    const uint64_t r0 = (uint64_t)blockIdx.x * LB;
+    const uint32_t nb = (uint32_t)std::min<uint64_t>(LB, n - r0);
     const unsigned long long below = (1ull << lane) - 1, above = ~below << 1;
     for (uint32_t k = lane; k < kFastMaxLive; k += kWave)
         last[k] = 0;
-    for (uint32_t k = lane; k < kLevelBlock + 2; k += kWave)
+    for (uint32_t k = lane; k < LB + 2; k += kWave)
         cnt[k] = 0;
     for (uint32_t k = lane; k < kWinCap * kSets * kWave; k += kWave)
         smap[k] = 0xFFFF;
     {
-        // all pair codes first: sixteen loads in flight per lane, one wait
-        uint32_t wv[kLevelBlock / kWave];
+        // all pair codes first: 32 loads in flight per lane, one wait
+        uint32_t wv[LB / kWave];
 #pragma unroll
-        for (uint32_t k = 0; k < kLevelBlock / kWave; k++) {
+        for (uint32_t k = 0; k < LB / kWave; k++) {
             const uint32_t t = k * kWave + lane;
             wv[k] = t < nb ? prep[r0 + t].w : 0u;
         }
 #pragma unroll
-        for (uint32_t k = 0; k < kLevelBlock / kWave; k++)
+        for (uint32_t k = 0; k < LB / kWave; k++)
             W[k * kWave + lane] = (uint16_t)(wv[k] & 0xFFFFu);
     }
     uint32_t lmax = 0;
-    for (uint32_t c0 = 0; c0 < kLevelBlock; c0 += kWave) {
+    for (uint32_t c0 = 0; c0 < nb; c0 += kWave) {
         const uint32_t t = c0 + lane;
         const bool valid = t < nb;
         const uint32_t w = W[t], a = w & 0xFF, o = w >> 8;
@@ -607,8 +635,8 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
     // each run's first member reserves the run's size in its level's count.
     // Requests of one level are independent, so any order of a level's runs
     // is valid; a run's members stay together, in run order.
-    for (uint32_t t = lane; t < kLevelBlock; t += kWave) {
-        const bool head = t < nb && psn[t] == 0;
+    for (uint32_t t = lane; t < nb; t += kWave) {
+        const bool head = psn[t] == 0;
         const uint32_t L = lv[t], rs = 1u + has1[t] + has2[t];
         key[t] = head ? (uint16_t)(L << 2 | rs) : (uint16_t)0;
         if (head)
@@ -727,7 +755,7 @@ __global__ __launch_bounds__(kWave) void sel_level_kernel(
             const uint32_t ln = pl_base[p] + (k - pl_s0[p]);
             smap[(w * kSets + set) * kWave + ln] = (uint16_t)t;
             const uint32_t m1 = pos == 2 ? (uint32_t)P[t] : 0u;
-            info[r0 + t] = d | pos << 6 | (pos + 1 < rs ? 1u << 8 : 0u) | h << 9 | m1 << 19;
+            info[r0 + t] = d | pos << 6 | (pos + 1 < rs ? 1u << 8 : 0u) | h << 9 | m1 << 20;
         }
     }
     for (uint32_t k = lane; k < kWinCap * kSets * kWave; k += kWave)
@@ -784,9 +812,10 @@ __global__ __launch_bounds__(4 * kWave) void sel_fill_kernel(
     const SelPack* __restrict__ prep, uint64_t n, const uint32_t* __restrict__ info,
     const uint16_t* __restrict__ slotmap, const uint8_t* __restrict__ wdepth,
     const uint32_t* __restrict__ wcount, const uint32_t* __restrict__ woff,
-    const uint32_t* __restrict__ total, uint64_t nblk, WalkRec* __restrict__ rec,
+    const uint32_t* __restrict__ total, uint64_t nblk, BlockShape bs, WalkRec* __restrict__ rec,
     uint32_t* __restrict__ slot_of)
 {
+    const uint32_t wincap = bs.wincap, bsize = bs.block;
     const int lane = lane_id();
     const uint64_t gw = ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const uint64_t ws = gw / kSets;  // window of capacity
@@ -795,23 +824,23 @@ __global__ __launch_bounds__(4 * kWave) void sel_fill_kernel(
     uint64_t win;
     uint32_t k = 0xFFFF, depth = 1;
     uint64_t blk = 0;
-    if (ws < nblk * kWinCap) {
-        blk = ws / kWinCap;
-        const uint32_t lw = (uint32_t)(ws % kWinCap);
+    if (ws < nblk * wincap) {
+        blk = ws / wincap;
+        const uint32_t lw = (uint32_t)(ws % wincap);
         if (lw >= wcount[blk])
             return;
         win = (uint64_t)woff[blk] + lw;
         k = slotmap[gw * kWave + lane];
         depth = wdepth[ws];
-    } else if (ws < nblk * kWinCap + 2 * kPrefetch) {
-        win = (uint64_t)total[0] + (ws - nblk * kWinCap);
+    } else if (ws < nblk * wincap + 2 * kPrefetch) {
+        win = (uint64_t)total[0] + (ws - nblk * wincap);
     } else {
         return;
     }
     const uint32_t e = (0u - depth) & 15u, passes = (depth + 15u) >> 4;
     WalkRec q;
     q.ctl = e | (passes - 1) << 4;
-    const uint64_t r = blk * kLevelBlock + k;
+    const uint64_t r = blk * bsize + k;
     if (k != 0xFFFF && r < n) {
         const SelPack me = prep[r];
         const uint32_t f = info[r], pos = (f >> 6) & 3;
@@ -828,13 +857,13 @@ __global__ __launch_bounds__(4 * kWave) void sel_fill_kernel(
         q.pth = q.pth2 = 0;
         q.pad = 0;
         if (pos >= 1) {
-            const SelPack m0 = prep[blk * kLevelBlock + ((f >> 9) & 1023)];
+            const SelPack m0 = prep[blk * bsize + ((f >> 9) & (bsize - 1))];
             q.pua = m0.ua;
             q.puo = m0.uo;
             q.pth = m0.th;
         }
         if (pos >= 2) {
-            const SelPack m1 = prep[blk * kLevelBlock + ((f >> 19) & 1023)];
+            const SelPack m1 = prep[blk * bsize + ((f >> 20) & (bsize - 1))];
             q.pua2 = m1.ua;
             q.puo2 = m1.uo;
             q.pth2 = m1.th;
@@ -1201,6 +1230,7 @@ struct SelBuf {
     int64_t* base;
     uint32_t* plan;
     unsigned long long* grow;
+    BlockShape shape;  // requests per block, windows per block
     uint64_t nblk;   // request blocks
     uint64_t nslots; // walk slots that can hold a request
 };
@@ -1210,8 +1240,9 @@ static size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 // Sizes of one set's arrays for a batch of n requests, in layout order.
 static void sel_sizes(uint64_t n, size_t* sizes)
 {
-    const uint64_t nblk = (n + kLevelBlock - 1) / kLevelBlock;
-    const uint64_t wcap = nblk * kWinCap;
+    const BlockShape bs = block_shape(n);
+    const uint64_t nblk = (n + bs.block - 1) / bs.block;
+    const uint64_t wcap = nblk * bs.wincap;
     const size_t z[] = {
         up256(n * sizeof(SelPack)),                                  // prep
         up256((wcap + 2 * kPrefetch) * kSets * kWave * sizeof(WalkRec)),  // rec
@@ -1240,8 +1271,9 @@ uint64_t select_scratch_bytes(uint64_t n)
 static hipError_t sel_buffers(dm_ctx* c, uint64_t n, int par, SelBuf* b)
 {
     hipError_t e = hipSuccess;
-    b->nblk = (n + kLevelBlock - 1) / kLevelBlock;
-    b->nslots = b->nblk * kWinCap * kSets * kWave;
+    b->shape = block_shape(n);
+    b->nblk = (n + b->shape.block - 1) / b->shape.block;
+    b->nslots = b->nblk * b->shape.wincap * kSets * kWave;
     size_t sizes[10];
     sel_sizes(n, sizes);
     const size_t one = select_scratch_bytes(n);
@@ -1302,7 +1334,7 @@ hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uin
     hipError_t e = sel_buffers(c, n, par, &b);
     if (e != hipSuccess)
         return e;
-    const uint64_t fill_waves = (b.nblk * kWinCap + 2 * kPrefetch) * kSets;
+    const uint64_t fill_waves = (b.nblk * b.shape.wincap + 2 * kPrefetch) * kSets;
     if (b.nblk > 0x7FFFFFFFull || fill_waves > 0x7FFFFFFFull)
         return hipErrorInvalidValue;
     const uint32_t NL = c->n_live;
@@ -1313,13 +1345,18 @@ hipError_t select_prepare(dm_ctx* c, hipStream_t st, const int64_t* offsets, uin
     sel_prep_kernel<<<grid_for(n, 256, 512), 256, 0, st>>>(
         offsets, n, block_shift(c), out->cand, out->match, c->d_dense, NL, k.ttft_base_us,
         k.ttft_per_token_us, c->shift_div, k.slo_us, c->policy, b.prep, b.grow);
-    if (b.nblk > 0)
-        sel_level_kernel<<<(uint32_t)b.nblk, kWave, 0, st>>>(b.prep, n, b.info, b.slotmap, b.wdepth,
-                                                             b.wcount, c->d_status);
+    if (b.nblk > 0) {
+        if (b.shape.block == LevelShape<2048>::block)
+            sel_level_kernel<2048><<<(uint32_t)b.nblk, kWave, 0, st>>>(
+                b.prep, n, b.info, b.slotmap, b.wdepth, b.wcount, c->d_status);
+        else
+            sel_level_kernel<1024><<<(uint32_t)b.nblk, kWave, 0, st>>>(
+                b.prep, n, b.info, b.slotmap, b.wdepth, b.wcount, c->d_status);
+    }
     sel_scan_kernel<<<1, 1024, 0, st>>>(b.wcount, b.nblk, b.woff, b.total);
     sel_fill_kernel<<<(uint32_t)((fill_waves + 3) / 4), 4 * kWave, 0, st>>>(
-        b.prep, n, b.info, b.slotmap, b.wdepth, b.wcount, b.woff, b.total, b.nblk, b.rec,
-        b.slot_of);
+        b.prep, n, b.info, b.slotmap, b.wdepth, b.wcount, b.woff, b.total, b.nblk, b.shape,
+        b.rec, b.slot_of);
     return hipGetLastError();
 }
 

@@ -674,15 +674,17 @@ def _disjoint_pair_prompts(o, rng, n_pool):
     return out
 
 
-@pytest.mark.parametrize("wide", [False, True])
-def test_levels_above_64_requests_parity(wide):
+@pytest.mark.parametrize("wide,big", [(False, False), (True, False), (False, True)])
+def test_levels_above_64_requests_parity(wide, big):
     """Levels of more than 64 requests: prompts with pairwise disjoint
     candidate pairs over 200 instances, each sent twice in a row in three
     rounds, so that consecutive same-pair requests form runs (of three, then
     of three again) and a dependency level holds far more than 64 requests.
     The packing cuts each such level into parts of at most 64 requests, one
-    depth each, and must keep every run whole.  Random prompts follow, across the next request block.  wide:
-    loads spread beyond 2^30 (64-bit walk)."""
+    depth each, and must keep every run whole.  Random prompts follow,
+    across the next request block.  wide: loads spread beyond 2^30 (64-bit
+    walk).  big: the same 1,100 requests repeated past 512 Ki requests, so
+    that the selection takes its blocks of 2048 requests."""
     gh = _h()
     wl = workloads.small_random(33, 200, 3, 16, 64, slo_us=5_000)
     eng, o = gh.engine_for(wl), oh.oracle_for(wl)
@@ -710,6 +712,8 @@ def test_levels_above_64_requests_parity(wide):
     eng.sync()
     for _ in range(1100 - len(seq)):
         seq.append(rng.integers(0, 1 << 20, size=int(rng.integers(0, 120)), dtype=np.int32))
+    if big:
+        seq = seq * -(-600_000 // len(seq))
     off = np.zeros(len(seq) + 1, np.int64)
     off[1:] = np.cumsum([len(p) for p in seq])
     tok = np.concatenate(seq).astype(np.int32)
